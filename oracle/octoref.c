@@ -1,0 +1,833 @@
+/*
+ * octoref.c — the CPU oracle for batched pipeline-schedule simulation.
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the plain, slow, obviously-correct reference that the
+ * HIP path is checked against. Only tests, the smoke check and the benchmark's CPU-baseline leg
+ * may load it. It shares no code, header or table with the HIP library; the two read the same
+ * candidate-record byte format, each with its own decoder.
+ *
+ * What it computes (arXiv 2509.23722, "OctoPipe"):
+ *   - §5 "Simulating Pipeline Execution": a candidate pipeline schedule becomes a DAG whose nodes
+ *     are per-(stage, micro-batch) forward/backward ops and whose edges are data dependencies;
+ *     the send/recv pair of a cross-device dependency is one weighted edge here.
+ *   - §5 "Estimating Pipeline Performance": traverse the DAG recording start/end of each node;
+ *     idle time on a device is bubble.
+ *   - §6 "Optimization Objective", Eq. (1): T^pipeline = max over devices of T_d^execution.
+ *   - §3.3: the backward of a micro-batch must follow its forward; orders can deadlock.
+ *   - §6 "Scheduling Tuning": F of stage i depends on stage i-1, B of stage i on stage i+1, W only
+ *     on B of the same device.
+ * The traversal is Kahn's topological order with longest-path relaxation: the plain definition
+ * of earliest start times. A cycle (ops left unvisited) is a deadlock.
+ *
+ * Parity pins (tests/test_oracle_*.py): closed forms for AFAB/1F1B/interleaved/ZB, the §3.2
+ * Fig. 3 worked example, the §3.3 order count, the §7 comm-count table, invariants, a pure-Python
+ * tick simulator and DFS cycle check on tiny instances, and numpy's Philox.
+ */
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define REF_OK 0
+#define REF_EINVAL (-1)
+#define REF_DEADLOCK (-1) /* per-candidate sentinel */
+#define REF_INVALID (-2)  /* per-candidate sentinel */
+/* internal status of one DAG evaluation */
+#define SIM_OK 0
+#define SIM_CYCLE 1
+#define SIM_BADQ 2
+
+enum { KF = 0, KB = 1, KW = 2 };
+enum { POL_AFAB = 0, POL_1F1B = 1, POL_I1F1B = 2, POL_ZB = 3 };
+enum { GEN_AFAB = 0, GEN_INTER = 1, GEN_MERGE = 2 };
+
+/* Problem description (scalars only; mirrors the ABI's problem header, decoded independently). */
+typedef struct {
+  int32_t L, P, v_max, M, cand_stride, max_pert;
+} ref_problem;
+
+/* One op in device-local terms: kind, local chunk (index into A_d), micro-batch. */
+typedef struct {
+  int kind, chunk, m;
+} ref_op;
+
+/* A decoded candidate. */
+typedef struct {
+  int policy, v, n_pert, flags, S;
+  int b[66];   /* b[0..S] */
+  int dev[64]; /* dev[0..S-1] */
+  int pert[256][3];
+} ref_cand;
+
+static int imin(int a, int b) { return a < b ? a : b; }
+static int imax(int a, int b) { return a > b ? a : b; }
+
+/* ------------------------------------------------------------------------------------------ */
+/* Candidate record decoding (byte layout of the ABI, read independently).                    */
+/* ------------------------------------------------------------------------------------------ */
+
+static int pert_offset(int S_max) { return (3 + 2 * S_max + 1) & ~1; }
+
+static int rd16(const uint8_t* p) { return (int)p[0] | ((int)p[1] << 8); }
+
+/* Decode without judging validity beyond what decoding itself needs. */
+static void decode(const ref_problem* pr, const uint8_t* rec, ref_cand* c) {
+  int S_max = pr->P * pr->v_max;
+  c->policy = rec[0];
+  c->v = rec[1];
+  c->n_pert = rec[2];
+  c->flags = rec[3];
+  c->S = pr->P * c->v;
+  if (c->v < 1 || c->v > pr->v_max) c->S = 0;
+  c->b[0] = 0;
+  for (int s = 1; s < c->S; ++s) c->b[s] = rec[4 + s - 1];
+  if (c->S > 0) c->b[c->S] = pr->L;
+  for (int s = 0; s < c->S; ++s) c->dev[s] = rec[3 + S_max + s];
+  int po = pert_offset(S_max);
+  int np = imin(c->n_pert, pr->max_pert);
+  for (int i = 0; i < np && i < 256; ++i)
+    for (int f = 0; f < 3; ++f) c->pert[i][f] = rd16(rec + po + 6 * i + 2 * f);
+}
+
+/* A_d: the stages of device d in ascending order. Returns |A_d|. */
+static int stages_of(const ref_cand* c, int d, int* out) {
+  int n = 0;
+  for (int s = 0; s < c->S; ++s)
+    if (c->dev[s] == d) out[n++] = s;
+  return n;
+}
+
+/* Looped placement: dev[s] == dev[s mod P] for every stage. */
+static int is_looped(const ref_cand* c, int P) {
+  for (int s = 0; s < c->S; ++s)
+    if (c->dev[s] != c->dev[s % P]) return 0;
+  return 1;
+}
+
+/* Policy resolution (policy x v x placement). Returns -1 if the candidate cannot be resolved. */
+static int resolve(const ref_problem* pr, const ref_cand* c, int* split) {
+  *split = (c->policy == POL_ZB);
+  if (c->policy == POL_AFAB) return GEN_AFAB;
+  if (c->v == 1) return GEN_INTER;
+  if (c->policy == POL_1F1B) return GEN_MERGE;
+  if (!is_looped(c, pr->P)) return GEN_MERGE;
+  if (pr->M % pr->P != 0) return -1;
+  return GEN_INTER;
+}
+
+/* Structural validity, excluding perturbation ranges (checked once queues exist). */
+static int valid_structure(const ref_problem* pr, const ref_cand* c) {
+  if (c->policy > 3) return 0;
+  if (c->v < 1 || c->v > pr->v_max) return 0;
+  if (c->n_pert > pr->max_pert) return 0;
+  if (c->flags != 0) return 0;
+  for (int s = 0; s < c->S; ++s)
+    if (c->b[s + 1] <= c->b[s]) return 0; /* covers 0 < b[1] < ... < b[S-1] < L */
+  int cnt[64] = {0};
+  for (int s = 0; s < c->S; ++s) {
+    if (c->dev[s] >= pr->P) return 0;
+    cnt[c->dev[s]]++;
+  }
+  for (int d = 0; d < pr->P; ++d)
+    if (cnt[d] != c->v) return 0;
+  int split;
+  if (resolve(pr, c, &split) < 0) return 0;
+  return 1;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Queue generators.                                                                          */
+/* ------------------------------------------------------------------------------------------ */
+
+/* GPipe / all-forward-all-backward order. */
+static int gen_afab(int v, int M, ref_op* q) {
+  int n = 0;
+  for (int k = 0; k < v; ++k)
+    for (int m = 0; m < M; ++m) q[n++] = (ref_op){KF, k, m};
+  for (int k = v - 1; k >= 0; --k)
+    for (int m = 0; m < M; ++m) q[n++] = (ref_op){KB, k, m};
+  return n;
+}
+
+/* Interleaved 1F1B virtual index j -> (chunk, micro-batch) (Narayanan et al., restated). */
+static ref_op inter_fwd(int P, int v, int j) {
+  ref_op o;
+  o.kind = KF;
+  o.chunk = (j % (P * v)) / P;
+  o.m = (j / (P * v)) * P + (j % P);
+  return o;
+}
+static ref_op inter_bwd(int P, int v, int i, int kind) {
+  ref_op o = inter_fwd(P, v, i);
+  o.kind = kind;
+  o.chunk = v - 1 - o.chunk;
+  return o;
+}
+
+/* INTER(P, v, M, r, split, lag). */
+static int gen_inter(int P, int v, int M, int r, int split, int lag, ref_op* q) {
+  int N = v * M;
+  int w = (v == 1) ? imin(P - 1 - r, M) : imin(2 * (P - 1 - r) + (v - 1) * P, N);
+  int n = 0;
+  for (int j = 0; j < w; ++j) q[n++] = inter_fwd(P, v, j);
+  for (int i = 0; i < N - w; ++i) {
+    q[n++] = inter_fwd(P, v, w + i);
+    q[n++] = inter_bwd(P, v, i, KB);
+    if (split && i >= lag) q[n++] = inter_bwd(P, v, i - lag, KW);
+  }
+  for (int i = N - w; i < N; ++i) {
+    q[n++] = inter_bwd(P, v, i, KB);
+    if (split && i >= lag) q[n++] = inter_bwd(P, v, i - lag, KW);
+  }
+  if (split)
+    for (int i = imax(0, N - lag); i < N; ++i) q[n++] = inter_bwd(P, v, i, KW);
+  return n;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* The DAG and its traversal (the plain definition of the time model).                        */
+/* ------------------------------------------------------------------------------------------ */
+
+/* Ops in stage terms for the DAG: kind, stage, micro-batch. */
+typedef struct {
+  int kind, s, m;
+} ref_sop;
+
+typedef struct {
+  int S, M, split, P;
+  const int* dev;   /* [S] */
+  const int64_t* F; /* [S] stage forward */
+  const int64_t* B; /* [S] stage input-grad backward */
+  const int64_t* W; /* [S] stage weight-grad backward */
+  const int64_t* link; /* [P*P] */
+} ref_dag_in;
+
+static int node_id(int S, int M, int kind, int s, int m) { return (kind * S + s) * M + m; }
+
+static int64_t op_dur(const ref_dag_in* g, int kind, int s) {
+  if (kind == KF) return g->F[s];
+  if (kind == KB) return g->split ? g->B[s] : g->B[s] + g->W[s];
+  return g->W[s];
+}
+
+static int64_t edge_w(const ref_dag_in* g, int sp, int sc) {
+  int dp = g->dev[sp], dc = g->dev[sc];
+  return dp == dc ? 0 : g->link[dp * g->P + dc];
+}
+
+/*
+ * Evaluate explicit device queues. qlen[d] ops of device d start at queue + qoff[d].
+ * Outputs makespan, bubble[P]; start_out (optional) receives start times indexed by node id;
+ * n_cross (optional) receives the number of cross-device data edges.
+ * Returns SIM_OK, SIM_CYCLE on a cycle (deadlock), or SIM_BADQ if the queues are not exactly the
+ * op set (each op once, on the device hosting its stage).
+ */
+static int simulate(const ref_dag_in* g, const ref_sop* queue, const int* qoff, const int* qlen,
+                    int64_t* makespan, int64_t* bubble, int64_t* start_out, int64_t* n_cross) {
+  int S = g->S, M = g->M, nk = g->split ? 3 : 2;
+  int nn = nk * S * M;
+  int* owner = (int*)malloc(sizeof(int) * nn);
+  int* next = (int*)malloc(sizeof(int) * nn); /* queue successor or -1 */
+  int* indeg = (int*)calloc(nn, sizeof(int));
+  int64_t* est = (int64_t*)calloc(nn, sizeof(int64_t));
+  int64_t* fin = (int64_t*)malloc(sizeof(int64_t) * nn);
+  int* ready = (int*)malloc(sizeof(int) * nn);
+  int rc = 0;
+  for (int i = 0; i < nn; ++i) owner[i] = -1, next[i] = -1;
+  /* queue edges */
+  for (int d = 0; d < g->P; ++d) {
+    for (int i = 0; i < qlen[d]; ++i) {
+      ref_sop o = queue[qoff[d] + i];
+      if (o.kind < 0 || o.kind >= nk || o.s < 0 || o.s >= S || o.m < 0 || o.m >= M ||
+          g->dev[o.s] != d) {
+        rc = SIM_BADQ;
+        goto done;
+      }
+      int id = node_id(S, M, o.kind, o.s, o.m);
+      if (owner[id] >= 0) {
+        rc = SIM_BADQ;
+        goto done;
+      }
+      owner[id] = d;
+      if (i + 1 < qlen[d]) {
+        ref_sop n2 = queue[qoff[d] + i + 1];
+        if (n2.kind < 0 || n2.kind >= nk || n2.s < 0 || n2.s >= S || n2.m < 0 || n2.m >= M) {
+          rc = SIM_BADQ;
+          goto done;
+        }
+        next[id] = node_id(S, M, n2.kind, n2.s, n2.m);
+      }
+    }
+  }
+  for (int i = 0; i < nn; ++i)
+    if (owner[i] < 0) {
+      rc = SIM_BADQ;
+      goto done;
+    }
+  /* in-degrees: queue edges + data edges */
+  int64_t cross = 0;
+  for (int i = 0; i < nn; ++i)
+    if (next[i] >= 0) indeg[next[i]]++;
+  for (int s = 0; s < S; ++s)
+    for (int m = 0; m < M; ++m) {
+      if (s > 0) {
+        indeg[node_id(S, M, KF, s, m)]++; /* F(s-1,m) -> F(s,m) */
+        if (g->dev[s - 1] != g->dev[s]) cross++;
+      }
+      if (s < S - 1) {
+        indeg[node_id(S, M, KB, s, m)]++; /* B(s+1,m) -> B(s,m) */
+        if (g->dev[s + 1] != g->dev[s]) cross++;
+      }
+      indeg[node_id(S, M, KB, s, m)]++; /* F(s,m) -> B(s,m) */
+      if (g->split) indeg[node_id(S, M, KW, s, m)]++; /* B(s,m) -> W(s,m) */
+    }
+  if (n_cross) *n_cross = cross;
+  /* Kahn traversal with longest-path relaxation */
+  int nr = 0, head = 0, done_n = 0;
+  for (int i = 0; i < nn; ++i)
+    if (indeg[i] == 0) ready[nr++] = i;
+  while (head < nr) {
+    int u = ready[head++];
+    int kind = u / (S * M), s = (u / M) % S, m = u % M;
+    fin[u] = est[u] + op_dur(g, kind, s);
+    done_n++;
+    /* out-edges of u */
+    int outs[4];
+    int64_t ws[4];
+    int no = 0;
+    if (next[u] >= 0) outs[no] = next[u], ws[no++] = 0;
+    if (kind == KF) {
+      if (s + 1 < S) outs[no] = node_id(S, M, KF, s + 1, m), ws[no++] = edge_w(g, s, s + 1);
+      outs[no] = node_id(S, M, KB, s, m), ws[no++] = 0;
+    } else if (kind == KB) {
+      if (s > 0) outs[no] = node_id(S, M, KB, s - 1, m), ws[no++] = edge_w(g, s, s - 1);
+      if (g->split) outs[no] = node_id(S, M, KW, s, m), ws[no++] = 0;
+    }
+    for (int e = 0; e < no; ++e) {
+      int x = outs[e];
+      int64_t t = fin[u] + ws[e];
+      if (t > est[x]) est[x] = t;
+      if (--indeg[x] == 0) ready[nr++] = x;
+    }
+  }
+  if (done_n < nn) {
+    rc = SIM_CYCLE;
+    goto done;
+  }
+  int64_t ms = 0;
+  for (int i = 0; i < nn; ++i)
+    if (fin[i] > ms) ms = fin[i];
+  *makespan = ms;
+  for (int d = 0; d < g->P; ++d) {
+    int64_t busy = 0;
+    for (int i = 0; i < qlen[d]; ++i) {
+      ref_sop o = queue[qoff[d] + i];
+      busy += op_dur(g, o.kind, o.s);
+    }
+    bubble[d] = ms - busy;
+  }
+  if (start_out)
+    for (int i = 0; i < nn; ++i) start_out[i] = est[i];
+done:
+  free(owner);
+  free(next);
+  free(indeg);
+  free(est);
+  free(fin);
+  free(ready);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* MERGE: the ideal stage-level order.                                                         */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct {
+  int64_t tau;
+  int s;     /* stage (tie-break) */
+  ref_op op; /* the op in device-local terms */
+} merge_key;
+
+static int cmp_merge(const void* a, const void* b) {
+  const merge_key* x = (const merge_key*)a;
+  const merge_key* y = (const merge_key*)b;
+  if (x->tau != y->tau) return x->tau < y->tau ? -1 : 1;
+  if (x->s != y->s) return x->s < y->s ? -1 : 1;
+  return 0;
+}
+
+/* Ideal start time of every op of the stage-level pipeline (node-id indexed).
+ * Each stage s is its own virtual device running INTER(S, 1, M, s, split, s); unit costs
+ * (F = 1; fused B = 2; split B = W = 1); zero transfer cost. */
+static int merge_tau(int S, int M, int split, int64_t* tau) {
+  int per = (split ? 3 : 2) * M;
+  ref_sop* q = (ref_sop*)malloc(sizeof(ref_sop) * (size_t)per * S);
+  ref_op* tmp = (ref_op*)malloc(sizeof(ref_op) * per);
+  int* qoff = (int*)malloc(sizeof(int) * S);
+  int* qlen = (int*)malloc(sizeof(int) * S);
+  int* dev = (int*)malloc(sizeof(int) * S);
+  int64_t* F = (int64_t*)malloc(sizeof(int64_t) * S);
+  int64_t* B = (int64_t*)malloc(sizeof(int64_t) * S);
+  int64_t* W = (int64_t*)malloc(sizeof(int64_t) * S);
+  int64_t* link = (int64_t*)calloc((size_t)S * S, sizeof(int64_t));
+  int64_t* bub = (int64_t*)malloc(sizeof(int64_t) * S);
+  for (int s = 0; s < S; ++s) {
+    dev[s] = s;
+    F[s] = 1;
+    B[s] = 1; /* split: B = 1, W = 1; fused op B + W = 2 */
+    W[s] = 1;
+    int n = gen_inter(S, 1, M, s, split, s, tmp);
+    qoff[s] = s * per;
+    qlen[s] = n;
+    for (int i = 0; i < n; ++i) q[s * per + i] = (ref_sop){tmp[i].kind, s, tmp[i].m};
+  }
+  ref_dag_in g = {S, M, split, S, dev, F, B, W, link};
+  int64_t ms;
+  int rc = simulate(&g, q, qoff, qlen, &ms, bub, tau, NULL);
+  free(q);
+  free(tmp);
+  free(qoff);
+  free(qlen);
+  free(dev);
+  free(F);
+  free(B);
+  free(W);
+  free(link);
+  free(bub);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Building the queues of a candidate.                                                         */
+/* ------------------------------------------------------------------------------------------ */
+
+/* Local-op queues for every device of a structurally valid candidate, before perturbations.
+ * q holds P rows of capacity qcap. Returns 0 or an error. */
+static int build_local_queues(const ref_problem* pr, const ref_cand* c, ref_op* q, int qcap,
+                              int* qlen) {
+  int split;
+  int gen = resolve(pr, c, &split);
+  int P = pr->P, M = pr->M, v = c->v, S = c->S;
+  if (gen == GEN_AFAB) {
+    for (int d = 0; d < P; ++d) qlen[d] = gen_afab(v, M, q + (size_t)d * qcap);
+    return 0;
+  }
+  if (gen == GEN_INTER) {
+    for (int d = 0; d < P; ++d) {
+      int A[64];
+      stages_of(c, d, A);
+      int r = A[0];
+      qlen[d] = gen_inter(P, v, M, r, split, r, q + (size_t)d * qcap);
+    }
+    return 0;
+  }
+  /* MERGE */
+  int nk = split ? 3 : 2;
+  int64_t* tau = (int64_t*)malloc(sizeof(int64_t) * (size_t)nk * S * M);
+  if (merge_tau(S, M, split, tau) != SIM_OK) {
+    free(tau);
+    return REF_EINVAL;
+  }
+  merge_key* keys = (merge_key*)malloc(sizeof(merge_key) * (size_t)nk * v * M);
+  for (int d = 0; d < P; ++d) {
+    int A[64];
+    int nA = stages_of(c, d, A);
+    int n = 0;
+    for (int k = 0; k < nA; ++k)
+      for (int kind = 0; kind < nk; ++kind)
+        for (int m = 0; m < M; ++m) {
+          keys[n].tau = tau[node_id(S, M, kind, A[k], m)];
+          keys[n].s = A[k];
+          keys[n].op = (ref_op){kind, k, m};
+          n++;
+        }
+    qsort(keys, n, sizeof(merge_key), cmp_merge);
+    for (int i = 0; i < n; ++i) q[(size_t)d * qcap + i] = keys[i].op;
+    qlen[d] = n;
+  }
+  free(keys);
+  free(tau);
+  return 0;
+}
+
+/* Apply the perturbation moves in order. Returns 0, or REF_EINVAL if one is out of range. */
+static int apply_perturbations(const ref_problem* pr, const ref_cand* c, ref_op* q, int qcap,
+                               const int* qlen) {
+  for (int i = 0; i < c->n_pert; ++i) {
+    int d = c->pert[i][0], from = c->pert[i][1], to = c->pert[i][2];
+    if (d >= pr->P || from >= qlen[d] || to >= qlen[d]) return REF_EINVAL;
+    ref_op* row = q + (size_t)d * qcap;
+    ref_op moved = row[from];
+    if (from < to)
+      memmove(row + from, row + from + 1, sizeof(ref_op) * (size_t)(to - from));
+    else if (from > to)
+      memmove(row + to + 1, row + to, sizeof(ref_op) * (size_t)(from - to));
+    row[to] = moved;
+  }
+  return 0;
+}
+
+static void stage_costs(const ref_cand* c, const int64_t* costs, int64_t* F,
+                        int64_t* B, int64_t* W) {
+  for (int s = 0; s < c->S; ++s) {
+    F[s] = B[s] = W[s] = 0;
+    for (int l = c->b[s]; l < c->b[s + 1]; ++l) {
+      F[s] += costs[3 * l + 0];
+      B[s] += costs[3 * l + 1];
+      W[s] += costs[3 * l + 2];
+    }
+  }
+}
+
+/* Evaluate a candidate given its local queues (after perturbations). */
+static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
+                      const int64_t* link, const ref_op* q, int qcap, const int* qlen,
+                      int64_t* ms, int64_t* bub) {
+  int P = pr->P, S = c->S, split;
+  resolve(pr, c, &split);
+  int64_t F[64], B[64], W[64];
+  stage_costs(c, costs, F, B, W);
+  int total = 0;
+  int qoff[64];
+  for (int d = 0; d < P; ++d) qoff[d] = total, total += qlen[d];
+  ref_sop* sq = (ref_sop*)malloc(sizeof(ref_sop) * (size_t)(total > 0 ? total : 1));
+  for (int d = 0; d < P; ++d) {
+    int A[64];
+    int nA = stages_of(c, d, A);
+    for (int i = 0; i < qlen[d]; ++i) {
+      ref_op o = q[(size_t)d * qcap + i];
+      int s = (o.chunk >= 0 && o.chunk < nA) ? A[o.chunk] : -1;
+      sq[qoff[d] + i] = (ref_sop){o.kind, s, o.m};
+    }
+  }
+  ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link};
+  int rc = simulate(&g, sq, qoff, qlen, ms, bub, NULL, NULL);
+  free(sq);
+  return rc;
+}
+
+/* Full evaluation of one candidate record: makespan + bubbles, or sentinels. */
+static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                        const uint8_t* rec, int64_t* ms, int64_t* bub) {
+  ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
+  decode(pr, rec, c);
+  int P = pr->P;
+  int64_t sentinel = 0;
+  if (!valid_structure(pr, c)) {
+    sentinel = REF_INVALID;
+  } else {
+    int qcap = 3 * c->v * pr->M;
+    ref_op* q = (ref_op*)malloc(sizeof(ref_op) * (size_t)qcap * P);
+    int qlen[64];
+    if (build_local_queues(pr, c, q, qcap, qlen) != 0 ||
+        apply_perturbations(pr, c, q, qcap, qlen) != 0) {
+      sentinel = REF_INVALID;
+    } else {
+      int rc = eval_local(pr, c, costs, link, q, qcap, qlen, ms, bub);
+      if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
+      else if (rc != SIM_OK) sentinel = REF_INVALID;
+    }
+    free(q);
+  }
+  if (sentinel != 0) {
+    *ms = sentinel;
+    for (int d = 0; d < P; ++d) bub[d] = sentinel;
+  }
+  free(c);
+}
+
+static int check_problem(const ref_problem* pr) {
+  if (!pr) return 0;
+  if (pr->L < 1 || pr->L > 255 || pr->P < 1 || pr->P > 64 || pr->v_max < 1 || pr->v_max > 8 ||
+      pr->P * pr->v_max > 64 || pr->M < 1 || pr->M > 2047 || pr->max_pert < 0 ||
+      pr->max_pert > 255)
+    return 0;
+  int S_max = pr->P * pr->v_max;
+  if (pr->cand_stride < pert_offset(S_max) + 6 * pr->max_pert) return 0;
+  return 1;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Exported: batch evaluation.                                                                 */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct {
+  const ref_problem* pr;
+  const int64_t* costs;
+  const int64_t* link;
+  const uint8_t* cands;
+  int64_t lo, hi;
+  int64_t* out_ms;
+  int64_t* out_bub;
+} batch_job;
+
+static void* batch_worker(void* arg) {
+  batch_job* j = (batch_job*)arg;
+  for (int64_t i = j->lo; i < j->hi; ++i)
+    eval_record(j->pr, j->costs, j->link, j->cands + (size_t)i * j->pr->cand_stride,
+                j->out_ms + i, j->out_bub + (size_t)i * j->pr->P);
+  return NULL;
+}
+
+/* Evaluate n candidate records (host memory). nthreads >= 1 worker threads split the batch. */
+int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                     const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                     int nthreads) {
+  if (!check_problem(pr) || n < 0 || (n > 0 && (!costs || !link || !cands || !out_ms || !out_bub)))
+    return REF_EINVAL;
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 256) nthreads = 256;
+  if (n < nthreads) nthreads = n > 0 ? (int)n : 1;
+  pthread_t th[256];
+  batch_job jobs[256];
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t] = (batch_job){pr, costs, link, cands, n * t / nthreads, n * (t + 1) / nthreads,
+                          out_ms, out_bub};
+    if (nthreads == 1) batch_worker(&jobs[t]);
+    else pthread_create(&th[t], NULL, batch_worker, &jobs[t]);
+  }
+  if (nthreads > 1)
+    for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+  return REF_OK;
+}
+
+/* Dump the final (perturbed) queues of one candidate in stage terms: ops[d*qcap + i] =
+ * (kind, stage, m) packed as kind*2^24 + stage*2^16 + m. Returns the sentinel-style status:
+ * 0 ok, REF_INVALID if the candidate is invalid. */
+int oracle_dump_queues(const ref_problem* pr, const uint8_t* rec, int32_t* ops, int32_t qcap,
+                       int32_t* qlen_out) {
+  if (!check_problem(pr)) return REF_EINVAL;
+  ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
+  decode(pr, rec, c);
+  int rc = 0;
+  if (!valid_structure(pr, c)) {
+    rc = REF_INVALID;
+  } else {
+    int cap = 3 * c->v * pr->M;
+    ref_op* q = (ref_op*)malloc(sizeof(ref_op) * (size_t)cap * pr->P);
+    int qlen[64];
+    if (build_local_queues(pr, c, q, cap, qlen) != 0 || apply_perturbations(pr, c, q, cap, qlen) != 0) {
+      rc = REF_INVALID;
+    } else {
+      for (int d = 0; d < pr->P; ++d) {
+        int A[64];
+        stages_of(c, d, A);
+        qlen_out[d] = qlen[d];
+        for (int i = 0; i < qlen[d] && i < qcap; ++i) {
+          ref_op o = q[(size_t)d * cap + i];
+          ops[d * qcap + i] = (o.kind << 24) | (A[o.chunk] << 16) | o.m;
+        }
+      }
+    }
+    free(q);
+  }
+  free(c);
+  return rc;
+}
+
+/* Evaluate explicit queues given in stage terms (kind, stage, m) — for pins that build orders
+ * by hand. Stage durations are given directly. Returns 0 (ok), 1 (cycle: deadlock) or 2 (the
+ * queues are not exactly the op set), or REF_EINVAL for bad arguments. start_out (nullable) gets node-indexed start times
+ * (node = (kind*S + s)*M + m); n_cross (nullable) the cross-device data-edge count. */
+int oracle_sim_queues(int32_t P, int32_t S, int32_t M, int32_t split, const int32_t* dev,
+                      const int64_t* F, const int64_t* B, const int64_t* W, const int64_t* link,
+                      const int32_t* ops, const int32_t* qlen, int64_t* makespan, int64_t* bubble,
+                      int64_t* start_out, int64_t* n_cross) {
+  if (P < 1 || P > 64 || S < 1 || M < 1 || !dev || !F || !B || !W || !link || !ops || !qlen)
+    return REF_EINVAL;
+  int total = 0;
+  int qoff[64];
+  for (int d = 0; d < P; ++d) qoff[d] = total, total += qlen[d];
+  ref_sop* sq = (ref_sop*)malloc(sizeof(ref_sop) * (size_t)(total > 0 ? total : 1));
+  for (int i = 0; i < total; ++i)
+    sq[i] = (ref_sop){(ops[i] >> 24) & 0xff, (ops[i] >> 16) & 0xff, ops[i] & 0xffff};
+  int dv[64];
+  for (int s = 0; s < S && s < 64; ++s) dv[s] = dev[s];
+  ref_dag_in g = {S, M, split ? 1 : 0, P, dv, F, B, W, link};
+  int rc = simulate(&g, sq, qoff, qlen, makespan, bubble, start_out, n_cross);
+  free(sq);
+  return rc;
+}
+
+/* Ideal start times of the MERGE stage-level pipeline, node-indexed ((kind*S + s)*M + m). */
+int oracle_merge_tau(int32_t S, int32_t M, int32_t split, int64_t* tau) {
+  if (S < 1 || S > 64 || M < 1 || !tau) return REF_EINVAL;
+  return merge_tau(S, M, split ? 1 : 0, tau);
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3",    */
+/* SC'11): 10 rounds of the 4x64 S-box with the published multipliers and Weyl key constants.   */
+/* ------------------------------------------------------------------------------------------ */
+
+static void mulhilo64(uint64_t a, uint64_t b, uint64_t* hi, uint64_t* lo) {
+  unsigned __int128 p = (unsigned __int128)a * b;
+  *hi = (uint64_t)(p >> 64);
+  *lo = (uint64_t)p;
+}
+
+void oracle_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4]) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ULL, M1 = 0xCA5A826395121157ULL;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ULL, W1 = 0xBB67AE8584CAA73BULL;
+  uint64_t x0 = ctr_in[0], x1 = ctr_in[1], x2 = ctr_in[2], x3 = ctr_in[3];
+  uint64_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) k0 += W0, k1 += W1;
+    uint64_t hi0, lo0, hi1, lo1;
+    mulhilo64(M0, x0, &hi0, &lo0);
+    mulhilo64(M1, x2, &hi1, &lo1);
+    uint64_t n0 = hi1 ^ x1 ^ k0, n1 = lo1, n2 = hi0 ^ x3 ^ k1, n3 = lo0;
+    x0 = n0, x1 = n1, x2 = n2, x3 = n3;
+  }
+  out[0] = x0, out[1] = x1, out[2] = x2, out[3] = x3;
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Tuner: sequential local search per chain (§6, Algorithm 1's re-simulate-per-move loop, with   */
+/* the three move kinds of partitioning, placement and scheduling tuning).                      */
+/* ------------------------------------------------------------------------------------------ */
+
+static void write_record(const ref_problem* pr, const ref_cand* c, uint8_t* rec) {
+  int S_max = pr->P * pr->v_max;
+  for (int s = 1; s < c->S; ++s) rec[4 + s - 1] = (uint8_t)c->b[s];
+  for (int s = 0; s < c->S; ++s) rec[3 + S_max + s] = (uint8_t)c->dev[s];
+}
+
+typedef struct {
+  const ref_problem* pr;
+  const int64_t* costs;
+  const int64_t* link;
+  uint8_t* recs;
+  int64_t lo, hi;
+  uint64_t seed;
+  int n_steps;
+  int64_t* out_ms;
+  int64_t* out_bub;
+  int64_t* out_acc;
+  int32_t* out_queues; /* nullable: [chain][P][qcap] packed kind<<14 | chunk<<11 | m */
+} tune_job;
+
+static int64_t eff(int64_t ms) { return ms < 0 ? INT64_MAX : ms; }
+
+static void tune_chain(tune_job* j, int64_t ci) {
+  const ref_problem* pr = j->pr;
+  int P = pr->P;
+  uint8_t* rec = j->recs + (size_t)ci * pr->cand_stride;
+  int64_t* bub = j->out_bub + (size_t)ci * P;
+  ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
+  decode(pr, rec, c);
+  j->out_acc[ci] = 0;
+  if (!valid_structure(pr, c) || c->n_pert != 0) {
+    j->out_ms[ci] = REF_INVALID;
+    for (int d = 0; d < P; ++d) bub[d] = REF_INVALID;
+    free(c);
+    return;
+  }
+  int qcap = 3 * c->v * pr->M;
+  ref_op* q = (ref_op*)malloc(sizeof(ref_op) * (size_t)qcap * P);
+  int qlen[64];
+  build_local_queues(pr, c, q, qcap, qlen);
+  int64_t cur_ms, cur_bub[64], ms, tb[64];
+  int rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &cur_ms, cur_bub);
+  if (rc != SIM_OK) {
+    cur_ms = rc == SIM_CYCLE ? REF_DEADLOCK : REF_INVALID;
+    for (int d = 0; d < P; ++d) cur_bub[d] = cur_ms;
+  }
+  int S = c->S;
+  for (int t = 1; t <= j->n_steps; ++t) {
+    uint64_t ctr[4] = {(uint64_t)ci, (uint64_t)t, 0, 0}, key[2] = {j->seed, 0}, u[4];
+    oracle_philox4x64_10(ctr, key, u);
+    int kind = (int)(u[0] % 3);
+    int ok = 0;
+    if (kind == 0) {
+      if (S >= 2) {
+        int i = 1 + (int)(u[1] % (uint64_t)(S - 1));
+        int nb = c->b[i] + ((u[2] & 1) ? 1 : -1);
+        if (nb > c->b[i - 1] && nb < c->b[i + 1]) {
+          int old = c->b[i];
+          c->b[i] = nb;
+          rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &ms, tb);
+          if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
+          else c->b[i] = old;
+        }
+      }
+    } else if (kind == 1) {
+      if (P >= 2) {
+        int d1 = (int)(u[1] % (uint64_t)P);
+        int d2 = (int)((d1 + 1 + (int)(u[2] % (uint64_t)(P - 1))) % P);
+        int saved[64];
+        for (int s = 0; s < S; ++s) {
+          saved[s] = c->dev[s];
+          if (c->dev[s] == d1) c->dev[s] = d2;
+          else if (c->dev[s] == d2) c->dev[s] = d1;
+        }
+        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &ms, tb);
+        if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
+        else
+          for (int s = 0; s < S; ++s) c->dev[s] = saved[s];
+      }
+    } else {
+      int d = (int)(u[1] % (uint64_t)P);
+      if (qlen[d] >= 2) {
+        int i = (int)(u[2] % (uint64_t)(qlen[d] - 1));
+        ref_op* row = q + (size_t)d * qcap;
+        ref_op tmp = row[i];
+        row[i] = row[i + 1];
+        row[i + 1] = tmp;
+        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &ms, tb);
+        if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
+        else {
+          row[i + 1] = row[i];
+          row[i] = tmp;
+        }
+      }
+    }
+    if (ok) {
+      cur_ms = ms;
+      for (int d = 0; d < P; ++d) cur_bub[d] = tb[d];
+      j->out_acc[ci]++;
+    }
+  }
+  j->out_ms[ci] = cur_ms;
+  for (int d = 0; d < P; ++d) bub[d] = cur_bub[d];
+  write_record(pr, c, rec);
+  if (j->out_queues) {
+    int32_t* oq = j->out_queues + (size_t)ci * P * qcap;
+    for (int d = 0; d < P; ++d)
+      for (int i = 0; i < qcap; ++i) {
+        ref_op o = i < qlen[d] ? q[(size_t)d * qcap + i] : (ref_op){0, 0, 0};
+        oq[d * qcap + i] = i < qlen[d] ? ((o.kind << 14) | (o.chunk << 11) | o.m) : 0;
+      }
+  }
+  free(q);
+  free(c);
+}
+
+static void* tune_worker(void* arg) {
+  tune_job* j = (tune_job*)arg;
+  for (int64_t i = j->lo; i < j->hi; ++i) tune_chain(j, i);
+  return NULL;
+}
+
+/* Run steps 0..n_steps of the local search for chains [0, n). recs (in/out) holds the chain
+ * candidate records (updated to the final state). Outputs per chain: final makespan, bubbles,
+ * accepted-move count, and optionally the final queues (qcap = 3*v_max*M entries per device). */
+int oracle_tune(const ref_problem* pr, const int64_t* costs, const int64_t* link, uint8_t* recs,
+                int64_t n, uint64_t seed, int32_t n_steps, int64_t* out_ms, int64_t* out_bub,
+                int64_t* out_acc, int32_t* out_queues, int nthreads) {
+  if (!check_problem(pr) || n < 0 || n_steps < 0) return REF_EINVAL;
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 256) nthreads = 256;
+  if (n < nthreads) nthreads = n > 0 ? (int)n : 1;
+  pthread_t th[256];
+  tune_job jobs[256];
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t] = (tune_job){pr, costs, link, recs, n * t / nthreads, n * (t + 1) / nthreads,
+                         seed, n_steps, out_ms, out_bub, out_acc, out_queues};
+    if (nthreads == 1) tune_worker(&jobs[t]);
+    else pthread_create(&th[t], NULL, tune_worker, &jobs[t]);
+  }
+  if (nthreads > 1)
+    for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+  return REF_OK;
+}

@@ -1,0 +1,153 @@
+"""ctypes wrapper around the CPU oracle ``liboctoref.so``.
+
+Test infrastructure only: tests, the smoke check and the benchmark's CPU-baseline leg load it;
+the product path never does. Build it with ``oracle/build.py`` (``__graft_entry__.build()`` does).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboctoref.so")
+
+
+class RefProblem(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("P", ctypes.c_int32), ("v_max", ctypes.c_int32),
+                ("M", ctypes.c_int32), ("cand_stride", ctypes.c_int32),
+                ("max_pert", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            from . import build as _b  # noqa: F401  (oracle/build.py)
+            _b.build()
+        L = ctypes.CDLL(LIB_PATH)
+        p = ctypes.c_void_p
+        L.oracle_sim_batch.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64, p, p,
+                                       ctypes.c_int]
+        L.oracle_sim_batch.restype = ctypes.c_int
+        L.oracle_dump_queues.argtypes = [ctypes.POINTER(RefProblem), p, p, ctypes.c_int32, p]
+        L.oracle_dump_queues.restype = ctypes.c_int
+        L.oracle_sim_queues.argtypes = [ctypes.c_int32] * 4 + [p] * 9 + [p, p]
+        L.oracle_sim_queues.restype = ctypes.c_int
+        L.oracle_merge_tau.argtypes = [ctypes.c_int32] * 3 + [p]
+        L.oracle_merge_tau.restype = ctypes.c_int
+        L.oracle_philox4x64_10.argtypes = [p, p, p]
+        L.oracle_philox4x64_10.restype = None
+        L.oracle_tune.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64,
+                                  ctypes.c_uint64, ctypes.c_int32, p, p, p, p, ctypes.c_int]
+        L.oracle_tune.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def problem(L, P, v_max, M, cand_stride, max_pert):
+    return RefProblem(L, P, v_max, M, cand_stride, max_pert)
+
+
+def sim_batch(prob, costs, link, cands, nthreads=1):
+    """Evaluate candidate records (uint8 [n, stride]). Returns (makespan[n], bubble[n, P])."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    rc = lib().oracle_sim_batch(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(cands), n,
+                                _ptr(ms), _ptr(bub), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch rejected the arguments (rc={rc})")
+    return ms, bub
+
+
+def dump_queues(prob, rec):
+    """Final queues of one candidate as a list (per device) of (kind, stage, m) tuples,
+    or None if the candidate is invalid."""
+    qcap = 3 * prob.v_max * prob.M
+    ops = np.zeros((prob.P, qcap), dtype=np.int32)
+    qlen = np.zeros(prob.P, dtype=np.int32)
+    rec = np.ascontiguousarray(rec, dtype=np.uint8)
+    rc = lib().oracle_dump_queues(ctypes.byref(prob), _ptr(rec), _ptr(ops), qcap, _ptr(qlen))
+    if rc == -2:
+        return None
+    if rc != 0:
+        raise ValueError(f"oracle_dump_queues failed (rc={rc})")
+    out = []
+    for d in range(prob.P):
+        row = ops[d, :qlen[d]]
+        out.append([(int(x) >> 24, (int(x) >> 16) & 0xFF, int(x) & 0xFFFF) for x in row])
+    return out
+
+
+def sim_queues(P, S, M, split, dev, F, B, W, link, queues, want_start=False):
+    """Evaluate explicit queues (list per device of (kind, stage, m)).
+
+    Returns (status, makespan, bubble[P], start or None, n_cross) where status is 0 (ok),
+    1 (deadlock) or 2 (queues are not exactly the op set)."""
+    ops = np.array([(k << 24) | (s << 16) | m for q in queues for (k, s, m) in q] or [0],
+                   dtype=np.int32)
+    qlen = np.array([len(q) for q in queues], dtype=np.int32)
+    dev = np.ascontiguousarray(dev, dtype=np.int32)
+    F = np.ascontiguousarray(F, dtype=np.int64)
+    B = np.ascontiguousarray(B, dtype=np.int64)
+    W = np.ascontiguousarray(W, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    ms = np.zeros(1, dtype=np.int64)
+    bub = np.zeros(P, dtype=np.int64)
+    nk = 3 if split else 2
+    start = np.zeros(nk * S * M, dtype=np.int64) if want_start else None
+    ncross = np.zeros(1, dtype=np.int64)
+    rc = lib().oracle_sim_queues(P, S, M, int(bool(split)), _ptr(dev), _ptr(F), _ptr(B), _ptr(W),
+                                 _ptr(link), _ptr(ops), _ptr(qlen), _ptr(ms), _ptr(bub),
+                                 _ptr(start), _ptr(ncross))
+    if rc < 0:
+        raise ValueError(f"oracle_sim_queues rejected the arguments (rc={rc})")
+    return rc, int(ms[0]), bub, start, int(ncross[0])
+
+
+def merge_tau(S, M, split):
+    nk = 3 if split else 2
+    tau = np.zeros(nk * S * M, dtype=np.int64)
+    rc = lib().oracle_merge_tau(S, M, int(bool(split)), _ptr(tau))
+    if rc != 0:
+        raise ValueError(f"oracle_merge_tau failed (rc={rc})")
+    return tau.reshape(nk, S, M)
+
+
+def philox4x64_10(counter, key):
+    ctr = np.array(counter, dtype=np.uint64)
+    k = np.array(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    lib().oracle_philox4x64_10(_ptr(ctr), _ptr(k), _ptr(out))
+    return [int(x) for x in out]
+
+
+def tune(prob, costs, link, recs, seed, n_steps, nthreads=1, want_queues=False):
+    """Run the local search (steps 0..n_steps) on every chain record.
+
+    Returns (final_records, makespan[n], bubble[n, P], accepted[n], queues or None)."""
+    recs = np.array(recs, dtype=np.uint8, copy=True, order="C")
+    n = recs.shape[0]
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    acc = np.zeros(n, dtype=np.int64)
+    qcap = 3 * prob.v_max * prob.M
+    queues = np.zeros((n, prob.P, qcap), dtype=np.int32) if want_queues else None
+    rc = lib().oracle_tune(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(recs), n,
+                           ctypes.c_uint64(seed), int(n_steps), _ptr(ms), _ptr(bub), _ptr(acc),
+                           _ptr(queues), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_tune rejected the arguments (rc={rc})")
+    return recs, ms, bub, acc, queues

@@ -1,0 +1,115 @@
+"""Independent pure-Python checkers for tiny instances (test infrastructure).
+
+These recompute the time model of §5 by different means than the C oracle, so that the oracle
+is pinned to something other than itself:
+
+* ``tick_simulate`` advances an integer clock one tick at a time; at every tick each idle device
+  starts its next op if all producers have delivered (finish + transfer <= now). This is the
+  as-soon-as-possible execution the paper's traversal records (§5 "Estimating Pipeline
+  Performance"), obtained without any graph algorithm. Durations must be small integers.
+* ``has_cycle`` builds the dependency graph from its definition (§5, §6 "Scheduling Tuning") and
+  runs an iterative three-colour DFS.
+
+Queues are lists (per device) of (kind, stage, m) with kind 0 = F, 1 = B, 2 = W.
+"""
+import itertools
+
+F, B, W = 0, 1, 2
+
+
+def _dur(kind, s, split, Fs, Bs, Ws):
+    if kind == F:
+        return Fs[s]
+    if kind == B:
+        return Bs[s] if split else Bs[s] + Ws[s]
+    return Ws[s]
+
+
+def _producers(op, S, split, dev, link):
+    """(producer op, transfer cost) pairs of op, from the dependency rules."""
+    kind, s, m = op
+    out = []
+    if kind == F and s > 0:
+        out.append(((F, s - 1, m), 0 if dev[s - 1] == dev[s] else link[dev[s - 1]][dev[s]]))
+    if kind == B:
+        out.append(((F, s, m), 0))
+        if s < S - 1:
+            out.append(((B, s + 1, m), 0 if dev[s + 1] == dev[s] else link[dev[s + 1]][dev[s]]))
+    if kind == W:
+        out.append(((B, s, m), 0))
+    return out
+
+
+def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None):
+    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock."""
+    total = sum(_dur(k, s, split, Fs, Bs, Ws) for q in queues for (k, s, m) in q)
+    if max_ticks is None:
+        max_ticks = total + 2 * S * M * (max(max(r) for r in link) if P > 0 else 0) + 2
+    fin = {}
+    ptr = [0] * P
+    busy_until = [0] * P
+    running = [None] * P
+    t = 0
+    while t <= max_ticks:
+        for d in range(P):
+            if running[d] is not None and busy_until[d] <= t:
+                fin[running[d]] = busy_until[d]
+                running[d] = None
+        for d in range(P):
+            if running[d] is None and ptr[d] < len(queues[d]):
+                op = queues[d][ptr[d]]
+                ok = all(p in fin and fin[p] + w <= t
+                         for p, w in _producers(op, S, split, dev, link))
+                if ok:
+                    running[d] = op
+                    busy_until[d] = t + _dur(op[0], op[1], split, Fs, Bs, Ws)
+                    ptr[d] += 1
+                    if busy_until[d] == t:  # zero-length op finishes immediately
+                        fin[op] = t
+                        running[d] = None
+        if all(ptr[d] == len(queues[d]) and running[d] is None for d in range(P)):
+            break
+        t += 1
+    if not all(ptr[d] == len(queues[d]) and running[d] is None for d in range(P)):
+        return -1, [-1] * P
+    ms = max(fin.values()) if fin else 0
+    bub = [ms - sum(_dur(k, s, split, Fs, Bs, Ws) for (k, s, m) in queues[d]) for d in range(P)]
+    return ms, bub
+
+
+def has_cycle(P, S, M, split, dev, queues):
+    nodes = [(k, s, m) for k in range(3 if split else 2) for s in range(S) for m in range(M)]
+    succ = {n: [] for n in nodes}
+    for q in queues:
+        for a, b in zip(q, q[1:]):
+            succ[a].append(b)
+    for n in nodes:
+        for p, _ in _producers(n, S, split, dev, [[0] * P for _ in range(P)]):
+            succ[p].append(n)
+    color = {n: 0 for n in nodes}
+    for root in nodes:
+        if color[root]:
+            continue
+        stack = [(root, iter(succ[root]))]
+        color[root] = 1
+        while stack:
+            node, it = stack[-1]
+            nxt = next(it, None)
+            if nxt is None:
+                color[node] = 2
+                stack.pop()
+            elif color[nxt] == 1:
+                return True
+            elif color[nxt] == 0:
+                color[nxt] = 1
+                stack.append((nxt, iter(succ[nxt])))
+    return False
+
+
+def valid_stage_orders(s, M):
+    """All orders of one stage's F/B ops in which each B(m) follows F(m) ((2M)!/2^M of them)."""
+    ops = [(F, s, m) for m in range(M)] + [(B, s, m) for m in range(M)]
+    for perm in itertools.permutations(ops):
+        pos = {op: i for i, op in enumerate(perm)}
+        if all(pos[(F, s, m)] < pos[(B, s, m)] for m in range(M)):
+            yield list(perm)
