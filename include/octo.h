@@ -1,0 +1,146 @@
+/*
+ * octo.h — C ABI of the MI355X batched pipeline-schedule simulator (libocto.so).
+ *
+ * Computes the graph-based pipeline simulator of OctoPipe (arXiv 2509.23722, §5) for batches of
+ * candidate pipeline schedules — partitioning x placement x scheduling, the decision variables
+ * P, A, O of §6 "Optimization Objective" — and one step of a parallel local search over them
+ * (§6, Algorithm 1's re-simulate-per-move loop). All kernels run on the GPU; the host code only
+ * validates arguments, sizes workspaces and launches.
+ *
+ * Time model (§5, §6 Eq. 1). Nodes are forward F(s,m), backward B(s,m) and, for split
+ * schedules, weight-gradient W(s,m) ops of stage s and micro-batch m. Edges: each device's queue
+ * order; F(s-1,m)->F(s,m) and B(s+1,m)->B(s,m) weighted by link[dev(producer)][dev(consumer)]
+ * (0 when both stages are on one device; the send/recv pair of §5 as one edge); F(s,m)->B(s,m);
+ * B(s,m)->W(s,m). Every op starts as early as its in-edges allow. makespan = latest finish
+ * (T^pipeline of Eq. 1); bubble[d] = makespan - busy time of device d. A cycle is a deadlock.
+ *
+ * Units: all times are int64 nanoseconds; results are exact integers.
+ * Memory: every array pointer passed to octo_sim_batch / octo_tune_step is a DEVICE pointer owned
+ * by the caller; problem structs are host memory. The library keeps a private per-(device,
+ * stream) workspace that it allocates on first use and grows when needed.
+ * Streams: `stream` is a hipStream_t (NULL = the null stream). Calls are asynchronous; results
+ * are ready when the stream is synchronised. Concurrent calls on different streams are allowed.
+ * Errors: argument problems return a negative status before anything is launched; per-candidate
+ * outcomes (deadlock, invalid candidate) are data (sentinels), never errors.
+ */
+#ifndef OCTO_H
+#define OCTO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define OCTO_OK 0
+#define OCTO_EINVAL (-1)       /* bad argument (null pointer, size out of range, bad stride) */
+#define OCTO_EUNSUPPORTED (-2) /* valid problem that exceeds this GPU's limits (LDS) */
+#define OCTO_EHIP (-3)         /* a HIP runtime call or kernel launch failed */
+#define OCTO_ENOMEM (-4)       /* workspace allocation failed */
+
+/* Per-candidate sentinel values written to makespan and every bubble entry. */
+#define OCTO_MS_DEADLOCK (-1) /* the op orders and data dependencies form a cycle */
+#define OCTO_MS_INVALID (-2)  /* the candidate record breaks a validity rule (below) */
+
+/* Schedule policy byte. */
+#define OCTO_AFAB 0  /* GPipe: all forwards, then all backwards */
+#define OCTO_1F1B 1  /* one-forward-one-backward */
+#define OCTO_I1F1B 2 /* interleaved 1F1B over v chunks per device */
+#define OCTO_ZB 3    /* split backward (B input-grad, W weight-grad), W deferred by rank */
+
+/* Problem header (host memory). Limits: 1 <= L <= 255; 1 <= P <= 64; 1 <= v_max <= 8 with
+ * P*v_max <= 64; 1 <= M <= 2047; 0 <= max_pert <= 255; cand_stride a multiple of 16 and at least
+ * octo_record_stride(P, v_max, max_pert); the finish table (P*v_max + 1)*M*8 bytes must fit in
+ * one workgroup's LDS (else OCTO_EUNSUPPORTED). */
+typedef struct octo_problem {
+  int32_t L;           /* layers */
+  int32_t P;           /* pipeline devices */
+  int32_t v_max;       /* largest stages-per-device of any candidate */
+  int32_t M;           /* micro-batches */
+  int32_t cand_stride; /* bytes per candidate record */
+  int32_t max_pert;    /* perturbation slots per record */
+} octo_problem;
+
+/*
+ * Candidate record (cand_stride bytes; S = P*v, S_max = P*v_max), the decision variables of §6:
+ *   byte 0            policy (OCTO_AFAB..OCTO_ZB)
+ *   byte 1            v, stages per device (1..v_max)
+ *   byte 2            n_pert, perturbations used (0..max_pert)
+ *   byte 3            flags, must be 0
+ *   bytes 4..         b[1..S-1], uint8 stage boundaries: stage s holds layers [b[s], b[s+1]) with
+ *                     b[0] = 0, b[S] = L (partition vector P); S_max-1 bytes reserved
+ *   bytes 3+S_max..   dev[0..S-1], uint8 device of each stage (placement A); S_max bytes reserved
+ *   octo_record_pert_offset(P, v_max)..
+ *                     pert[i] = {uint16 device, uint16 from, uint16 to}, little endian: after the
+ *                     policy generates the queues, move queue entry `from` of `device` so that it
+ *                     ends at index `to` (irregular orders, §3.3), applied in list order.
+ * Unused reserved bytes are ignored.
+ *
+ * Queue generation (schedule O) from the policy, "looped" meaning dev[s] == dev[s mod P]:
+ *   AFAB  -> forwards by (stage, m) ascending, then backwards by (stage descending, m).
+ *   1F1B  -> v == 1: 1F1B with warm-up min(S-1-s, M); v >= 2: MERGE (below).
+ *   I1F1B -> v == 1: as 1F1B; v >= 2 looped: the interleaved order with warm-up
+ *            min(2(P-1-r) + (v-1)P, vM) for rank r, needs M % P == 0; otherwise MERGE.
+ *   ZB    -> as I1F1B (or MERGE) with the backward split into B and W; each W waits in a FIFO
+ *            of depth r (rank) behind its B (r = stage index inside MERGE).
+ *   MERGE -> every stage runs its own 1F1B/ZB order on an ideal pipeline (unit costs, no
+ *            transfer cost); a device executes its stages' ops sorted by ideal start time, then
+ *            stage index.
+ *
+ * Validity (else OCTO_MS_INVALID): policy <= 3; 1 <= v <= v_max; n_pert <= max_pert; flags == 0;
+ * 0 < b[1] < ... < b[S-1] < L; dev[s] < P with exactly v stages per device; M % P == 0 where the
+ * interleaved order is used; every perturbation has device < P and from, to < queue length.
+ */
+int32_t octo_record_pert_offset(int32_t P, int32_t v_max);
+/* Smallest valid cand_stride (a multiple of 16), or OCTO_EINVAL for out-of-range sizes. */
+int32_t octo_record_stride(int32_t P, int32_t v_max, int32_t max_pert);
+
+/*
+ * octo_sim_batch — evaluate n candidates (the simulator of §5 per candidate).
+ *   layer_costs  int64 [L][3], per layer {F, B (input-grad), W (weight-grad)} in ns; a fused
+ *                backward costs B + W. Stage costs are sums over the stage's layers.
+ *   link         int64 [P][P], cost of one transfer from device p to device q (diagonal unused).
+ *   candidates   n records of prob->cand_stride bytes, 16-byte aligned.
+ *   out_makespan int64 [n]; out_bubble int64 [n][P] row-major. Sentinels as above.
+ * n == 0 is allowed and launches nothing. Returns OCTO_OK or a negative status.
+ */
+int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
+                   void* stream);
+
+/*
+ * Local-search chains (§6: every tuning move re-runs the simulator; Algorithm 1's three move
+ * families). Chain state record, octo_chain_stride(prob) bytes each, 16-byte aligned:
+ *   bytes 0..cand_stride-1  the candidate record (n_pert must be 0), updated in place
+ *   +0  int64 current makespan (or sentinel)
+ *   +8  int64 accepted moves
+ *   +16 int64 current bubble[P]
+ * Queue store: uint16 [n_chains][P][octo_queue_capacity(prob)]; entry = kind << 14 | chunk << 11
+ * | m with kind 0 = F, 1 = B, 2 = W and chunk the index into the device's ascending stage list.
+ *
+ * octo_tune_step(step = 0) validates each chain, generates its queues from the policy and
+ * evaluates it. step t >= 1 draws (u0, u1, u2, u3) = Philox4x64-10(key = {seed, 0},
+ * counter = {chain, t, 0, 0}) and proposes by u0 % 3:
+ *   0: stage boundary i = 1 + u1 % (S-1) moves by (u2 & 1) ? +1 : -1 layer;
+ *   1: devices d1 = u1 % P and d2 = (d1 + 1 + u2 % (P-1)) % P swap their stage sets, each device
+ *      keeping its queue;
+ *   2: on device d = u1 % P, queue entries i = u2 % (len-1) and i+1 swap.
+ * A proposal is kept iff it is valid, does not deadlock and its makespan is <= the current one
+ * (a deadlocked current state counts as +infinity). Chains whose step-0 state is invalid stay
+ * OCTO_MS_INVALID. Deterministic in (seed, chain, step).
+ */
+int32_t octo_chain_stride(const octo_problem* prob);
+int32_t octo_queue_capacity(const octo_problem* prob);
+int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   void* chains, uint16_t* queues, int64_t n_chains, uint64_t seed, int32_t step,
+                   void* stream);
+
+/* Human-readable text for a status code (static storage). */
+const char* octo_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OCTO_H */

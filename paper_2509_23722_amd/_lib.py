@@ -1,0 +1,127 @@
+"""ctypes binding of libocto.so (argument marshalling only; every step runs in HIP kernels).
+
+Arrays are torch tensors on the GPU; the call is enqueued on torch's current stream of the
+tensors' device. Raises if the library is missing or a call returns an error status.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libocto.so")
+
+OCTO_MS_DEADLOCK = -1
+OCTO_MS_INVALID = -2
+AFAB, ONEF1B, I1F1B, ZB = 0, 1, 2, 3
+
+
+class OctoProblem(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("P", ctypes.c_int32), ("v_max", ctypes.c_int32),
+                ("M", ctypes.c_int32), ("cand_stride", ctypes.c_int32),
+                ("max_pert", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libocto.so (fails loudly when it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        pp = ctypes.POINTER(OctoProblem)
+        L.octo_record_pert_offset.argtypes = [i32, i32]
+        L.octo_record_pert_offset.restype = i32
+        L.octo_record_stride.argtypes = [i32, i32, i32]
+        L.octo_record_stride.restype = i32
+        L.octo_chain_stride.argtypes = [pp]
+        L.octo_chain_stride.restype = i32
+        L.octo_queue_capacity.argtypes = [pp]
+        L.octo_queue_capacity.restype = i32
+        L.octo_sim_batch.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
+        L.octo_sim_batch.restype = ctypes.c_int
+        L.octo_tune_step.argtypes = [pp, vp, vp, vp, vp, i64, ctypes.c_uint64, i32, vp]
+        L.octo_tune_step.restype = ctypes.c_int
+        L.octo_strerror.argtypes = [ctypes.c_int]
+        L.octo_strerror.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def problem(L, P, v_max, M, cand_stride, max_pert=0):
+    return OctoProblem(L, P, v_max, M, cand_stride, max_pert)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise RuntimeError(f"{what} failed: {lib().octo_strerror(rc).decode()} (status {rc})")
+
+
+def _dev_ptr(t, dtype, name):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous {dtype} tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t, stream):
+    s = stream if stream is not None else torch.cuda.current_stream(t.device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def record_stride(P, v_max, max_pert):
+    return lib().octo_record_stride(P, v_max, max_pert)
+
+
+def chain_stride(prob):
+    return lib().octo_chain_stride(ctypes.byref(prob))
+
+
+def queue_capacity(prob):
+    return lib().octo_queue_capacity(ctypes.byref(prob))
+
+
+def sim_batch(prob, layer_costs, link, candidates, out_makespan=None, out_bubble=None,
+              stream=None):
+    """octo_sim_batch: candidates uint8 [n, stride] -> (makespan int64 [n], bubble int64 [n, P])."""
+    n = candidates.shape[0]
+    dev = candidates.device
+    if out_makespan is None:
+        out_makespan = torch.empty(n, dtype=torch.int64, device=dev)
+    if out_bubble is None:
+        out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    rc = lib().octo_sim_batch(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+    _check(rc, "octo_sim_batch")
+    return out_makespan, out_bubble
+
+
+def tune_step(prob, layer_costs, link, chains, queues, seed, step, stream=None):
+    """octo_tune_step on chain states (uint8 [n, chain_stride]) and queues (int16/uint16)."""
+    n = chains.shape[0]
+    q = queues
+    if q.dtype not in (torch.int16, torch.uint16):
+        raise TypeError("queues must be a 16-bit tensor")
+    rc = lib().octo_tune_step(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(chains, torch.uint8, "chains"),
+        _dev_ptr(q, q.dtype, "queues"), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
+        _stream(chains, stream))
+    _check(rc, "octo_tune_step")
+
+
+def chain_state(chains, prob):
+    """Decode (makespan [n], accepted [n], bubble [n, P]) from chain-state bytes (host copy)."""
+    c = chains.cpu() if isinstance(chains, torch.Tensor) else torch.as_tensor(chains)
+    off = prob.cand_stride
+    tail = c[:, off:off + 16 + 8 * prob.P].contiguous().view(torch.int64)
+    return tail[:, 0], tail[:, 1], tail[:, 2:2 + prob.P]

@@ -1,0 +1,969 @@
+// octo.hip — kernels and host C ABI of libocto.so (declared in include/octo.h).
+//
+// One call of octo_sim_batch launches:
+//   k_prep      layer-cost prefix sums; clears the bin counters.
+//   k_merge_tab ideal stage-level start times for the MERGE order (cached per (P, v_max, M)).
+//   k_classify  one thread per candidate: validate, resolve the queue generator, write the
+//               sentinel of invalid candidates, count candidates per work bin.
+//   k_scatter   candidate indices grouped by bin (counting sort).
+//   k_sim       persistent waves; each takes a chunk of CPW candidates of one bin and simulates
+//               them together, queues generated in registers (the hot kernel).
+//   k_sim_mat   candidates with perturbations: queues materialised in global memory, moved,
+//               then simulated.
+// octo_tune_step launches k_tune (one local-search step for every chain).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "../../include/octo.h"
+#include "octo_device.hpp"
+#include "octo_sim.hpp"
+
+namespace octo {
+
+constexpr int WAVE = 64;
+
+// Workspace control block (int32 words).
+constexpr int CTL_COUNTS = 0;    // [NBINS] candidates per bin
+constexpr int CTL_CURSOR = 64;   // [NBINS] scatter cursors
+constexpr int CTL_WORK = 128;    // chunk counter of k_sim
+constexpr int CTL_WORK_MAT = 129;
+constexpr int CTL_WORDS = 256;
+
+struct SimArgs {
+  Problem pr;
+  const int64_t* pre;   // [(L+1)][3] prefix sums of layer costs
+  const int64_t* link;  // [P][P]
+  const uint8_t* cands;
+  int64_t n;
+  int64_t* out_ms;
+  int64_t* out_bub;
+  int32_t* ctl;
+  const int32_t* idx;  // candidate indices sorted by bin
+  const uint32_t* mtab;  // MERGE tables, merge_offset() entries apart
+  uint16_t* qscratch;  // materialised queues, [group slot][P][qcap]
+  int G, CPW;          // lanes per candidate, candidates per wave
+  int table_slots;     // int64 slots of one finish table ((S_cap+1)*M + 2)
+  int sink;            // slot that weight-gradient ops write ((S_cap+1)*M)
+  int group_bytes;     // LDS bytes per candidate (table + staged record)
+  int rec_bytes;       // staged record bytes (header + boundaries + placement)
+  int qcap;
+  int bin_lo, bin_hi;  // generated bins handled by this launch
+};
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
+
+__device__ __forceinline__ int bcast(int x) { return __shfl(x, 0); }
+
+// Group mask of this lane's candidate inside the wave.
+__device__ __forceinline__ uint64_t group_mask(int G) {
+  if (G >= WAVE) return ~0ull;
+  const int g = lane_id() / G;
+  return ((1ull << G) - 1) << (g * G);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Per-lane set-up of one candidate from its staged record.
+// ---------------------------------------------------------------------------------------------
+template <int VMAX>
+__device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr, const uint8_t* rec,
+                                       const int64_t* pre, const int64_t* link, int d, int v,
+                                       int split) {
+  const int S = pr.P * v;
+  const uint8_t* bnd = rec + 4;
+  const uint8_t* dev = rec + 3 + pr.s_max;
+  int cnt = 0;
+#pragma unroll
+  for (int k = 0; k < VMAX; ++k) c.st[k] = 0;
+  for (int s = 0; s < S; ++s) {
+    if (dev[s] == d) {
+#pragma unroll
+      for (int k = 0; k < VMAX; ++k)
+        if (cnt == k) c.st[k] = s;
+      ++cnt;
+    }
+  }
+  int64_t busy = 0;
+#pragma unroll
+  for (int k = 0; k < VMAX; ++k) {
+    if (k < v) {
+      const int s = c.st[k];
+      const int b0 = s > 0 ? bnd[s - 1] : 0;
+      const int b1 = s < S - 1 ? bnd[s] : pr.L;
+      const int64_t f = pre[3 * b1 + 0] - pre[3 * b0 + 0];
+      const int64_t bi = pre[3 * b1 + 1] - pre[3 * b0 + 1];
+      const int64_t wg = pre[3 * b1 + 2] - pre[3 * b0 + 2];
+      c.dF[k] = f;
+      c.dB[k] = split ? bi : bi + wg;
+      c.dW[k] = wg;
+      const int dp = s > 0 ? dev[s - 1] : d;
+      const int dn = s < S - 1 ? dev[s + 1] : d;
+      c.wF[k] = dp != d ? link[dp * pr.P + d] : 0;
+      c.wB[k] = dn != d ? link[dn * pr.P + d] : 0;
+      busy += f + bi + wg;
+    } else {
+      c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+    }
+  }
+  return busy * pr.M;
+}
+
+// Stage the first rec_bytes of a record into LDS (lanes of the candidate copy 4-byte words).
+__device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, int rec_bytes, int d, int G) {
+  const int words = (rec_bytes + 3) >> 2;
+  for (int i = d; i < words; i += G)
+    reinterpret_cast<uint32_t*>(dst)[i] = reinterpret_cast<const uint32_t*>(src)[i];
+}
+
+// Fill the finish table: row -1 = 0 (ready at time 0), rows 0..S-1 empty (-2).
+__device__ __forceinline__ void clear_table(int64_t* T, int S, int M, int d, int G) {
+  const int n = (S + 1) * M;
+  for (int i = d; i < n; i += G) T[i] = i < M ? 0 : -2;
+}
+
+// Simulate one candidate per group of the wave with generator kind GEN, write the results.
+// cand < 0: this group has no candidate. Returns nothing; results go to out_ms / out_bub.
+template <int VMAX, int GEN>
+__device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split, uint8_t* lds_group) {
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int d = lane_id() % G;
+  int64_t* T = reinterpret_cast<int64_t*>(lds_group);
+  uint8_t* rec = lds_group + (size_t)a.table_slots * 8;
+  const bool has = cand >= 0;
+  const int S = P * v;
+  const int sink = a.sink;
+  if (has) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
+  __asm__ volatile("" ::: "memory");
+
+  Chunks<VMAX> c;
+  Lane L;
+  L.clock = 0;
+  L.pos = 0;
+  L.nops = 0;
+  L.live = false;
+  int64_t busy = 0;
+  const bool mine = has && d < P;
+  if (mine) {
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+    L.nops = (split ? 3 : 2) * v * M;
+    L.live = true;
+  } else {
+#pragma unroll
+    for (int k = 0; k < VMAX; ++k) c.st[k] = 0, c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+  }
+  if (has) clear_table(T, S, M, d, G);
+  __asm__ volatile("" ::: "memory");
+
+  bool dead = false;
+  const uint64_t gm = group_mask(G);
+  if constexpr (GEN == GEN_AFAB) {
+    GenAfab g;
+    g.init(v, M);
+    if (mine) describe<VMAX>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
+    relax<VMAX>(g, c, L, T, M, S, sink, gm, dead, nullptr);
+  } else if constexpr (GEN == GEN_INTER) {
+    GenInter g;
+    const int r = c.st[0];
+    g.init(P, v, M, r, split, split ? r : 0);
+    if (mine) describe<VMAX>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
+    relax<VMAX>(g, c, L, T, M, S, sink, gm, dead, nullptr);
+  } else {
+    GenMerge<VMAX> g;
+    const int rowlen = (split ? 3 : 2) * M;
+    g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
+           [&](int k) { return pick<VMAX>(c.st, k); });
+    if (mine) describe<VMAX>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
+    relax<VMAX>(g, c, L, T, M, S, sink, gm, dead, nullptr);
+  }
+
+  const int64_t ms = group_max(L.clock, G);
+  if (mine) {
+    if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
+    a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------------------------
+
+__global__ void k_prep(const int64_t* __restrict__ costs, int L, int64_t* __restrict__ pre,
+                       int32_t* __restrict__ ctl) {
+  const int t = threadIdx.x;
+  for (int i = t; i < CTL_WORDS; i += blockDim.x) ctl[i] = 0;
+  if (t < 3) {
+    int64_t acc = 0;
+    pre[t] = 0;
+    for (int l = 0; l < L; ++l) {
+      acc += costs[3 * l + t];
+      pre[3 * (l + 1) + t] = acc;
+    }
+  }
+}
+
+// Ideal start times of the stage-level pipeline for MERGE: one block (one wave) per (v, split);
+// lane s = stage s on its own virtual device running 1F1B (warm-up min(S-1-s, M)), with the
+// split backward's W lagging s B's; unit durations, no transfer cost. Entry layout
+// rec[s][pos] = start << 16 | kind << 12 | m.
+__global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restrict__ mtab) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int v = v_lo + (int)(blockIdx.x >> 1);
+  const int split = (int)(blockIdx.x & 1);
+  if (v > v_hi) return;
+  const int S = P * v;
+  const int d = lane_id();
+  int64_t* T = reinterpret_cast<int64_t*>(smem);
+  const int rowlen = (split ? 3 : 2) * M;
+  uint32_t* tab = mtab + merge_offset(P, M, v, split);
+  clear_table(T, S, M, d, WAVE);
+  __asm__ volatile("" ::: "memory");
+  Chunks<1> c;
+  c.st[0] = d;
+  c.dF[0] = 1;
+  c.dB[0] = split ? 1 : 2;
+  c.dW[0] = 1;
+  c.wF[0] = 0;
+  c.wB[0] = 0;
+  Lane L;
+  L.clock = 0;
+  L.pos = 0;
+  L.nops = d < S ? rowlen : 0;
+  L.live = d < S;
+  const int sink = (S + 1) * M;  // the LDS table is sized for the largest v
+  GenInter g;
+  g.init(S, 1, M, d < S ? d : 0, split, split ? d : 0);
+  if (L.live) describe<1>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
+  bool dead = false;
+  relax<1>(g, c, L, T, M, S, sink, ~0ull, dead, d < S ? tab + d * rowlen : nullptr);
+}
+
+// One thread per candidate.
+__global__ void k_classify(SimArgs a, uint8_t* __restrict__ bins) {
+  __shared__ int hist[NBINS];
+  for (int i = threadIdx.x; i < NBINS; i += blockDim.x) hist[i] = 0;
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < a.n) {
+    const uint8_t* rec = a.cands + i * a.pr.stride;
+    Resolved r = resolve_record(a.pr, rec);
+    int bin = BIN_NONE;
+    if (!r.valid) {
+      a.out_ms[i] = OCTO_MS_INVALID;
+      for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
+    } else {
+      bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
+      atomicAdd(&hist[bin], 1);
+    }
+    bins[i] = (uint8_t)bin;
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
+    if (hist[b]) atomicAdd(&a.ctl[CTL_COUNTS + b], hist[b]);
+}
+
+__global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins, int32_t* __restrict__ idx) {
+  __shared__ int base[NBINS + 1];
+  __shared__ int hist[NBINS];
+  __shared__ int res[NBINS];
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int b = 0; b < NBINS; ++b) base[b] = acc, acc += a.ctl[CTL_COUNTS + b];
+    base[NBINS] = acc;
+  }
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x) hist[b] = 0;
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int bin = BIN_NONE, local = 0;
+  if (i < a.n) {
+    bin = bins[i];
+    if (bin != BIN_NONE) local = atomicAdd(&hist[bin], 1);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
+    res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_CURSOR + b], hist[b]) : 0;
+  __syncthreads();
+  if (bin != BIN_NONE) idx[base[bin] + res[bin] + local] = (int32_t)i;
+}
+
+// Locate chunk `ch` (of CPW candidates) among generated bins [lo, hi); returns the bin or -1.
+__device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, int lo, int hi, int ch,
+                                            int* entry0, int* pos0) {
+  int acc = 0, base = 0;
+  for (int b = 0; b < lo; ++b) base += ctl[CTL_COUNTS + b];
+  for (int b = lo; b < hi; ++b) {
+    const int cnt = ctl[CTL_COUNTS + b];
+    const int nch = (cnt + CPW - 1) / CPW;
+    if (ch < acc + nch) {
+      *entry0 = (ch - acc) * CPW;
+      *pos0 = base;
+      return b;
+    }
+    acc += nch;
+    base += cnt;
+  }
+  return -1;
+}
+
+template <int VMAX>
+__device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v, int split,
+                             uint8_t* lds_group) {
+  if (gen == GEN_AFAB) run_generated<VMAX, GEN_AFAB>(a, cand, v, split, lds_group);
+  else if (gen == GEN_INTER) run_generated<VMAX, GEN_INTER>(a, cand, v, split, lds_group);
+  else run_generated<VMAX, GEN_MERGE>(a, cand, v, split, lds_group);
+}
+
+// VCAP = 2 handles the bins of v = 1, 2; VCAP = 8 those of v = 3..8.
+template <int VCAP>
+__global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int g = lane_id() / a.G;
+  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
+  const int work = VCAP == 2 ? CTL_WORK : CTL_WORK + 2;
+  for (;;) {
+    int ch = 0;
+    if (lane_id() == 0) ch = atomicAdd(&a.ctl[work], 1);
+    ch = bcast(ch);
+    int entry0 = 0, pos0 = 0;
+    const int bin = locate_chunk(a.ctl, a.CPW, a.bin_lo, a.bin_hi, ch, &entry0, &pos0);
+    if (bin < 0) break;
+    int v, gen, split;
+    bin_decode(bin, &v, &gen, &split);
+    const int cnt = a.ctl[CTL_COUNTS + bin];
+    const int e = entry0 + g;
+    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
+    if constexpr (VCAP == 2) {
+      if (v == 1) dispatch_gen<1>(a, gen, cand, v, split, lds_group);
+      else dispatch_gen<2>(a, gen, cand, v, split, lds_group);
+    } else {
+      dispatch_gen<8>(a, gen, cand, v, split, lds_group);
+    }
+  }
+}
+
+// Generate one device queue into a global row (entry = kind << 14 | chunk << 11 | m).
+template <class Gen>
+__device__ __forceinline__ void emit_queue(Gen& g, uint16_t* row, int n) {
+  for (int i = 0; i < n; ++i) {
+    row[i] = qpack(g.kind(), g.chunk(), g.mb());
+    if (i + 1 < n) g.step();
+  }
+}
+
+// Materialise the queue of lane d for a staged record; returns the queue length.
+template <int VMAX>
+__device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>& c, int v, int gen,
+                                           int split, uint16_t* row) {
+  const int P = a.pr.P, M = a.pr.M;
+  const int n = (split ? 3 : 2) * v * M;
+  if (gen == GEN_AFAB) {
+    GenAfab g;
+    g.init(v, M);
+    emit_queue(g, row, n);
+  } else if (gen == GEN_INTER) {
+    GenInter g;
+    const int r = c.st[0];
+    g.init(P, v, M, r, split, split ? r : 0);
+    emit_queue(g, row, n);
+  } else {
+    GenMerge<VMAX> g;
+    g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), (split ? 3 : 2) * M, v,
+           [&](int k) { return pick<VMAX>(c.st, k); });
+    emit_queue(g, row, n);
+  }
+  return n;
+}
+
+// Move row[from] so that it ends at index to.
+__device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
+  const uint16_t x = row[from];
+  if (from < to)
+    for (int i = from; i < to; ++i) row[i] = row[i + 1];
+  else
+    for (int i = from; i > to; --i) row[i] = row[i - 1];
+  row[to] = x;
+}
+
+template <int VMAX>
+__global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
+  int64_t* T = reinterpret_cast<int64_t*>(lds_group);
+  uint8_t* rec = lds_group + (size_t)a.table_slots * 8;
+  const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
+  uint16_t* row = a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap;
+  const int sink = a.sink;
+  const uint64_t gm = group_mask(G);
+  for (;;) {
+    int ch = 0;
+    if (lane_id() == 0) ch = atomicAdd(&a.ctl[CTL_WORK_MAT], 1);
+    ch = bcast(ch);
+    int base = 0;
+    for (int b = 0; b < BIN_MAT; ++b) base += a.ctl[CTL_COUNTS + b];
+    const int cnt = a.ctl[CTL_COUNTS + BIN_MAT];
+    if (ch * a.CPW >= cnt) break;
+    const int e = ch * a.CPW + g;
+    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[base + e] : -1;
+    const bool has = cand >= 0;
+    const bool mine = has && d < P;
+    const uint8_t* grec = has ? a.cands + cand * a.pr.stride : a.cands;
+    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
+    __asm__ volatile("" ::: "memory");
+    const int policy = has ? rec[0] : 0;
+    const int v = has ? rec[1] : 1;
+    const int split = policy == POL_ZB;
+    int gen = GEN_AFAB;
+    if (has) {
+      Resolved r = resolve_record(a.pr, grec);
+      gen = r.gen;
+    }
+    Chunks<VMAX> c;
+    int64_t busy = 0;
+    Lane L;
+    L.clock = 0, L.pos = 0, L.nops = 0, L.live = false;
+    if (mine) {
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+      L.nops = materialise<VMAX>(a, c, v, gen, split, row);
+      const uint8_t* pp = grec + pert_off(a.pr.s_max);
+      const int np = grec[2];
+      for (int i = 0; i < np; ++i) {
+        const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
+        if (pd != d) continue;
+        const int from = pp[6 * i + 2] | (pp[6 * i + 3] << 8);
+        const int to = pp[6 * i + 4] | (pp[6 * i + 5] << 8);
+        move_entry(row, from, to);
+      }
+      L.live = L.nops > 0;
+    } else {
+#pragma unroll
+      for (int k = 0; k < VMAX; ++k) c.st[k] = 0, c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+    }
+    const int S = P * v;
+    if (has) clear_table(T, S, M, d, G);
+    __asm__ volatile("" ::: "memory");
+    GenMat q;
+    q.init(row, L.nops);
+    if (L.live) describe<VMAX>(L, c, q.kind(), q.chunk(), q.mb(), M, S, sink);
+    bool dead = false;
+    relax<VMAX>(q, c, L, T, M, S, sink, gm, dead, nullptr);
+    const int64_t ms = group_max(L.clock, G);
+    if (mine) {
+      if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
+      a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Local-search step (one chain per group).
+// ---------------------------------------------------------------------------------------------
+struct TuneArgs {
+  SimArgs s;
+  uint8_t* chains;
+  int chain_stride;
+  uint16_t* queues;
+  int64_t n_chains;
+  uint64_t seed;
+  int step;
+};
+
+template <int VMAX>
+__global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const SimArgs& a = t.s;
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
+  int64_t* T = reinterpret_cast<int64_t*>(lds_group);
+  uint8_t* rec = lds_group + (size_t)a.table_slots * 8;
+  const int sink = a.sink;
+  const uint64_t gm = group_mask(G);
+  const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < t.n_chains; base += n_groups) {
+    const int64_t chain = base + g;
+    const bool has = g < a.CPW && chain < t.n_chains;
+    uint8_t* crec = t.chains + (has ? chain : 0) * t.chain_stride;
+    int64_t* cstate = reinterpret_cast<int64_t*>(crec + a.pr.stride);
+    uint16_t* row = t.queues + ((size_t)(has ? chain : 0) * P + (d < P ? d : 0)) * a.qcap;
+    if (has) stage_record(rec, crec, a.rec_bytes, d, G);
+    __asm__ volatile("" ::: "memory");
+
+    // state of the chain before this step
+    bool skip = !has;
+    int v = 1, gen = GEN_AFAB, split = 0;
+    int64_t cur = 0;
+    if (has) {
+      if (t.step == 0) {
+        Resolved r = resolve_record(a.pr, crec);
+        if (!r.valid || r.n_pert != 0) {
+          if (d == 0) cstate[0] = OCTO_MS_INVALID, cstate[1] = 0;
+          if (d < P) cstate[2 + d] = OCTO_MS_INVALID;
+          skip = true;
+        }
+        v = r.v, gen = r.gen, split = r.split;
+      } else {
+        cur = cstate[0];
+        // the stored state is re-checked so that a damaged record cannot index out of range
+        Resolved r = resolve_record(a.pr, rec);
+        if (cur == OCTO_MS_INVALID || !r.valid || r.n_pert != 0) skip = true;
+        v = r.valid ? r.v : 1;
+        split = r.split;
+      }
+    }
+    const int S = P * v;
+    const int qlen = (split ? 3 : 2) * v * M;
+
+    // propose (step >= 1); the move is applied to the staged record / this chain's queue row
+    int kind = -1, mi = 0, old = 0, sd = -1;
+    bool valid = true;
+    if (!skip && t.step > 0) {
+      U4 u = philox4x64_10((uint64_t)chain, (uint64_t)t.step, 0, 0, t.seed, 0);
+      kind = (int)(u.x[0] % 3);
+      if (kind == 0) {
+        if (S < 2) {
+          valid = false;
+        } else {
+          mi = 1 + (int)(u.x[1] % (uint64_t)(S - 1));
+          const int lo = mi > 1 ? rec[4 + mi - 2] : 0;
+          const int hi = mi < S - 1 ? rec[4 + mi] : a.pr.L;
+          old = rec[4 + mi - 1];
+          const int nb = old + ((u.x[2] & 1) ? 1 : -1);
+          valid = nb > lo && nb < hi;
+          __asm__ volatile("" ::: "memory");
+          if (valid && d == 0) rec[4 + mi - 1] = (uint8_t)nb;
+        }
+      } else if (kind == 1) {
+        if (P < 2) {
+          valid = false;
+        } else {
+          const int d1 = (int)(u.x[1] % (uint64_t)P);
+          const int d2 = (int)((d1 + 1 + (int)(u.x[2] % (uint64_t)(P - 1))) % P);
+          uint8_t* dv = rec + 3 + a.pr.s_max;
+          __asm__ volatile("" ::: "memory");
+          if (d == 0)
+            for (int s = 0; s < S; ++s)
+              dv[s] = dv[s] == d1 ? (uint8_t)d2 : dv[s] == d2 ? (uint8_t)d1 : dv[s];
+        }
+      } else {
+        sd = (int)(u.x[1] % (uint64_t)P);
+        if (qlen < 2) {
+          valid = false;
+        } else {
+          mi = (int)(u.x[2] % (uint64_t)(qlen - 1));
+          if (d == sd) {
+            const uint16_t x = row[mi];
+            row[mi] = row[mi + 1];
+            row[mi + 1] = x;
+          }
+        }
+      }
+    }
+    __asm__ volatile("" ::: "memory");
+    const bool run = !skip && valid;
+
+    Chunks<VMAX> c;
+    int64_t busy = 0;
+    Lane L;
+    L.clock = 0, L.pos = 0, L.nops = 0, L.live = false;
+    if (run && d < P) {
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+      if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, row);
+      L.nops = qlen;
+      L.live = true;
+    } else {
+#pragma unroll
+      for (int k = 0; k < VMAX; ++k) c.st[k] = 0, c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+    }
+    if (run) clear_table(T, S, M, d, G);
+    __asm__ volatile("" ::: "memory");
+    GenMat q;
+    q.init(row, L.nops);
+    if (L.live) describe<VMAX>(L, c, q.kind(), q.chunk(), q.mb(), M, S, sink);
+    bool dead = false;
+    relax<VMAX>(q, c, L, T, M, S, sink, gm, dead, nullptr);
+    const int64_t ms = group_max(L.clock, G);
+
+    if (!has || skip) continue;
+    if (t.step == 0) {
+      if (d == 0) cstate[0] = dead ? OCTO_MS_DEADLOCK : ms, cstate[1] = 0;
+      if (d < P) cstate[2 + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+      continue;
+    }
+    const int64_t cur_eff = cur < 0 ? INT64_MAX : cur;
+    const bool accept = valid && !dead && ms <= cur_eff;
+    if (accept) {
+      if (d == 0) {
+        cstate[0] = ms;
+        cstate[1] += 1;
+        for (int i = 0; i < a.rec_bytes; ++i) crec[i] = rec[i];
+      }
+      if (d < P) cstate[2 + d] = ms - busy;
+    } else if (kind == 2 && valid && d == sd) {
+      const uint16_t x = row[mi];
+      row[mi] = row[mi + 1];
+      row[mi + 1] = x;
+    }
+    (void)old;
+  }
+}
+
+}  // namespace octo
+
+// =============================================================================================
+// Host side
+// =============================================================================================
+using namespace octo;
+
+namespace {
+
+struct Workspace {
+  void* base = nullptr;
+  size_t bytes = 0;
+  // cached MERGE tables
+  bool mt_valid = false;
+  int mt_P = 0, mt_vmax = 0, mt_M = 0;
+};
+
+std::mutex g_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+struct DevInfo {
+  int cus = 0;
+  int lds_max = 0;
+  bool ok = false;
+};
+std::map<int, DevInfo> g_dev;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int check_problem(const octo_problem* p) {
+  if (!p) return OCTO_EINVAL;
+  if (p->L < 1 || p->L > 255 || p->P < 1 || p->P > 64 || p->v_max < 1 || p->v_max > 8 ||
+      p->P * p->v_max > 64 || p->M < 1 || p->M > 2047 || p->max_pert < 0 || p->max_pert > 255)
+    return OCTO_EINVAL;
+  const int need = octo_record_stride(p->P, p->v_max, p->max_pert);
+  if (p->cand_stride < need || p->cand_stride % 16 != 0) return OCTO_EINVAL;
+  return OCTO_OK;
+}
+
+int dev_info(int dev, DevInfo* out) {
+  auto it = g_dev.find(dev);
+  if (it != g_dev.end()) {
+    *out = it->second;
+    return OCTO_OK;
+  }
+  DevInfo di;
+  if (hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return OCTO_EHIP;
+  if (hipDeviceGetAttribute(&di.lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+      hipSuccess)
+    return OCTO_EHIP;
+  di.ok = true;
+  g_dev[dev] = di;
+  *out = di;
+  return OCTO_OK;
+}
+
+struct Plan {
+  int G, CPW, table_slots, sink, rec_bytes, group_bytes, lds_bytes, qcap;
+};
+
+// LDS plan for tables of up to s_cap stages: G lanes per candidate (power of two >= P), as
+// many candidates per wave as lanes and LDS allow.
+Plan make_plan(const octo_problem* p, int lds_max, int s_cap) {
+  Plan pl;
+  pl.G = 1;
+  while (pl.G < p->P) pl.G <<= 1;
+  pl.table_slots = (s_cap + 1) * p->M + 2;
+  pl.sink = (s_cap + 1) * p->M;
+  pl.rec_bytes = pert_off(p->P * p->v_max);
+  pl.group_bytes = (int)(align_up((size_t)pl.table_slots * 8, 16) + align_up(pl.rec_bytes, 16));
+  pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
+  pl.lds_bytes = pl.CPW * pl.group_bytes;
+  pl.qcap = 3 * p->v_max * p->M;
+  return pl;
+}
+
+size_t mtab_entries(const octo_problem* p) {
+  return p->v_max >= 2 ? (size_t)merge_offset(p->P, p->M, p->v_max + 1, 0) : 0;
+}
+
+// Workspace layout (byte offsets).
+struct Layout {
+  size_t ctl, pre, mtab, bin_of, idx, qscr, total;
+};
+
+Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slots) {
+  Layout l;
+  size_t o = 0;
+  l.ctl = o;
+  o = align_up(o + CTL_WORDS * 4, 256);
+  l.pre = o;
+  o = align_up(o + (size_t)(p->L + 1) * 3 * 8, 256);
+  l.mtab = o;
+  o = align_up(o + mtab_entries(p) * 4, 256);
+  l.bin_of = o;
+  o = align_up(o + (size_t)n, 256);
+  l.idx = o;
+  o = align_up(o + (size_t)n * 4, 256);
+  l.qscr = o;
+  o = align_up(o + (size_t)mat_slots * p->P * big.qcap * 2, 256);
+  l.total = o;
+  return l;
+}
+
+int ensure(Workspace& ws, size_t bytes, hipStream_t stream) {
+  if (ws.bytes >= bytes) return OCTO_OK;
+  if (ws.base) {
+    if (hipStreamSynchronize(stream) != hipSuccess) return OCTO_EHIP;
+    (void)hipFree(ws.base);
+    ws.base = nullptr;
+    ws.bytes = 0;
+    ws.mt_valid = false;
+  }
+  size_t want = std::max(bytes, ws.bytes * 3 / 2);
+  if (hipMalloc(&ws.base, want) != hipSuccess) {
+    ws.base = nullptr;
+    if (hipMalloc(&ws.base, bytes) != hipSuccess) {
+      ws.base = nullptr;
+      return OCTO_ENOMEM;
+    }
+    want = bytes;
+  }
+  ws.bytes = want;
+  return OCTO_OK;
+}
+
+template <typename K>
+int occupancy_grid(K kernel, int lds, int cus, int* grid) {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, WAVE, lds) != hipSuccess)
+    return OCTO_EHIP;
+  if (per_cu < 1) return OCTO_EUNSUPPORTED;
+  *grid = per_cu * cus;
+  return OCTO_OK;
+}
+
+int launch_ok() { return hipGetLastError() == hipSuccess ? OCTO_OK : OCTO_EHIP; }
+
+struct Setup {
+  Plan small, big;  // tables for v <= 2 / for v_max
+  Layout l;
+  Workspace* ws;
+  DevInfo di;
+  int mat_grid;
+};
+
+template <int VC>
+int mat_grid_for(const Plan& big, int cus, int* g) {
+  return occupancy_grid(k_sim_mat<VC>, big.lds_bytes, cus, g);
+}
+
+// Shared front half of octo_sim_batch and octo_tune_step: device, plans, workspace, prefix
+// sums, MERGE tables.
+int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, int64_t n,
+            Setup* su) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
+  int rc = dev_info(dev, &su->di);
+  if (rc) return rc;
+  su->big = make_plan(prob, su->di.lds_max, prob->P * prob->v_max);
+  su->small = make_plan(prob, su->di.lds_max, prob->P * std::min(prob->v_max, 2));
+  if (su->big.CPW < 1) return OCTO_EUNSUPPORTED;
+  rc = prob->v_max <= 2 ? mat_grid_for<2>(su->big, su->di.cus, &su->mat_grid)
+                        : mat_grid_for<8>(su->big, su->di.cus, &su->mat_grid);
+  if (rc) return rc;
+  su->l = layout(prob, su->big, n, (int64_t)su->mat_grid * su->big.CPW);
+  Workspace& ws = g_ws[std::make_pair(dev, stream)];
+  rc = ensure(ws, su->l.total, stream);
+  if (rc) return rc;
+  su->ws = &ws;
+  char* base = static_cast<char*>(ws.base);
+  hipLaunchKernelGGL(k_prep, dim3(1), dim3(256), 0, stream, costs, prob->L,
+                     reinterpret_cast<int64_t*>(base + su->l.pre),
+                     reinterpret_cast<int32_t*>(base + su->l.ctl));
+  if ((rc = launch_ok())) return rc;
+  if (prob->v_max >= 2 && !(ws.mt_valid && ws.mt_P == prob->P && ws.mt_vmax == prob->v_max &&
+                            ws.mt_M == prob->M)) {
+    const int lds = (int)align_up((size_t)((prob->P * prob->v_max + 1) * prob->M + 2) * 8, 16);
+    if (lds > su->di.lds_max) return OCTO_EUNSUPPORTED;
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_merge_tab),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    hipLaunchKernelGGL(k_merge_tab, dim3(2 * (prob->v_max - 1)), dim3(WAVE), lds, stream, prob->P,
+                       prob->M, 2, prob->v_max, reinterpret_cast<uint32_t*>(base + su->l.mtab));
+    if ((rc = launch_ok())) return rc;
+    ws.mt_valid = true;
+    ws.mt_P = prob->P, ws.mt_vmax = prob->v_max, ws.mt_M = prob->M;
+  }
+  return OCTO_OK;
+}
+
+SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, const int64_t* link,
+                  const void* cands, int64_t n, int64_t* ms, int64_t* bub) {
+  char* base = static_cast<char*>(su.ws->base);
+  const Layout& l = su.l;
+  SimArgs a;
+  a.pr = Problem{prob->L, prob->P, prob->v_max, prob->M, prob->cand_stride, prob->max_pert,
+                 prob->P * prob->v_max};
+  a.pre = reinterpret_cast<const int64_t*>(base + l.pre);
+  a.link = link;
+  a.cands = static_cast<const uint8_t*>(cands);
+  a.n = n;
+  a.out_ms = ms;
+  a.out_bub = bub;
+  a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
+  a.idx = reinterpret_cast<const int32_t*>(base + l.idx);
+  a.mtab = reinterpret_cast<const uint32_t*>(base + l.mtab);
+  a.qscratch = reinterpret_cast<uint16_t*>(base + l.qscr);
+  a.G = pl.G;
+  a.CPW = pl.CPW;
+  a.table_slots = pl.table_slots;
+  a.sink = pl.sink;
+  a.group_bytes = pl.group_bytes;
+  a.rec_bytes = pl.rec_bytes;
+  a.qcap = pl.qcap;
+  a.bin_lo = 0;
+  a.bin_hi = NBIN_GEN;
+  return a;
+}
+
+template <int VC>
+int launch_sim(const SimArgs& a, const Plan& pl, int cus, int64_t n, hipStream_t stream) {
+  int grid = 0;
+  int rc = occupancy_grid(k_sim<VC>, pl.lds_bytes, cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (n + pl.CPW - 1) / pl.CPW;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+  hipLaunchKernelGGL(k_sim<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
+  return launch_ok();
+}
+
+template <int VC>
+int launch_tune(const TuneArgs& t, const Plan& pl, int cus, int64_t n_chains,
+                       hipStream_t stream) {
+  int grid = 0;
+  int rc = occupancy_grid(k_tune<VC>, pl.lds_bytes, cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (n_chains + pl.CPW - 1) / pl.CPW;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+  hipLaunchKernelGGL(k_tune<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, t);
+  return launch_ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t octo_record_pert_offset(int32_t P, int32_t v_max) {
+  if (P < 1 || P > 64 || v_max < 1 || v_max > 8 || P * v_max > 64) return OCTO_EINVAL;
+  return pert_off(P * v_max);
+}
+
+int32_t octo_record_stride(int32_t P, int32_t v_max, int32_t max_pert) {
+  if (P < 1 || P > 64 || v_max < 1 || v_max > 8 || P * v_max > 64 || max_pert < 0 ||
+      max_pert > 255)
+    return OCTO_EINVAL;
+  const int need = pert_off(P * v_max) + 6 * max_pert;
+  return (need + 15) / 16 * 16;
+}
+
+int32_t octo_chain_stride(const octo_problem* prob) {
+  if (check_problem(prob)) return OCTO_EINVAL;
+  return (int32_t)align_up((size_t)prob->cand_stride + 16 + 8 * prob->P, 16);
+}
+
+int32_t octo_queue_capacity(const octo_problem* prob) {
+  if (check_problem(prob)) return OCTO_EINVAL;
+  return 3 * prob->v_max * prob->M;
+}
+
+int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
+                   void* stream_) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
+  if (n == 0) return OCTO_OK;
+  if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  std::lock_guard<std::mutex> lock(g_mu);
+  Setup su;
+  rc = prepare(prob, layer_costs, stream, n, &su);
+  if (rc) return rc;
+  char* base = static_cast<char*>(su.ws->base);
+  SimArgs a = make_args(prob, su.small, su, link, candidates, n, out_makespan, out_bubble);
+  const int tb = 256;
+  const int nb = (int)((n + tb - 1) / tb);
+  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
+  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), 0, stream, a, bins);
+  if ((rc = launch_ok())) return rc;
+  hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
+                     reinterpret_cast<int32_t*>(base + su.l.idx));
+  if ((rc = launch_ok())) return rc;
+  // v <= 2 bins (the common case)
+  a.bin_lo = bin_of(2, GEN_MERGE, 1);
+  a.bin_hi = NBIN_GEN;
+  if ((rc = launch_sim<2>(a, su.small, su.di.cus, n, stream))) return rc;
+  if (prob->v_max >= 3) {
+    SimArgs b = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
+    b.bin_lo = 0;
+    b.bin_hi = bin_of(2, GEN_MERGE, 1);
+    if ((rc = launch_sim<8>(b, su.big, su.di.cus, n, stream))) return rc;
+  }
+  SimArgs m = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
+  if (prob->v_max <= 2)
+    hipLaunchKernelGGL(k_sim_mat<2>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, m);
+  else
+    hipLaunchKernelGGL(k_sim_mat<8>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, m);
+  return launch_ok();
+}
+
+int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   void* chains, uint16_t* queues, int64_t n_chains, uint64_t seed, int32_t step,
+                   void* stream_) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n_chains < 0 || step < 0) return OCTO_EINVAL;
+  if (n_chains == 0) return OCTO_OK;
+  if (!layer_costs || !link || !chains || !queues) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(chains) & 15) != 0) return OCTO_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  std::lock_guard<std::mutex> lock(g_mu);
+  Setup su;
+  rc = prepare(prob, layer_costs, stream, 0, &su);
+  if (rc) return rc;
+  TuneArgs t;
+  t.s = make_args(prob, su.big, su, link, nullptr, 0, nullptr, nullptr);
+  t.chains = static_cast<uint8_t*>(chains);
+  t.chain_stride = octo_chain_stride(prob);
+  t.queues = queues;
+  t.n_chains = n_chains;
+  t.seed = seed;
+  t.step = step;
+  return prob->v_max <= 2 ? launch_tune<2>(t, su.big, su.di.cus, n_chains, stream)
+                          : launch_tune<8>(t, su.big, su.di.cus, n_chains, stream);
+}
+
+const char* octo_strerror(int status) {
+  switch (status) {
+    case OCTO_OK: return "ok";
+    case OCTO_EINVAL: return "invalid argument";
+    case OCTO_EUNSUPPORTED: return "problem exceeds this GPU's limits (LDS per workgroup)";
+    case OCTO_EHIP: return "HIP runtime error";
+    case OCTO_ENOMEM: return "workspace allocation failed";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"
