@@ -1,0 +1,200 @@
+"""Benchmark: candidate pipeline schedules simulated per second on one MI355X.
+
+Workload: 1,048,576 synthetic candidates of a Nemotron-H-like 52-layer model on P = 8 devices
+with M = 64 micro-batches, v in {1, 2} stages per device, four placements and four schedule
+policies in equal strata (paper_2509_23722_amd/inputs.py, workload 3). One step = one
+octo_sim_batch call over the whole batch, inputs resident in GPU memory. Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--copy-calibration]
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X (gfx950): 256 CUs x 4 SIMD x 16 lanes at 2.4 GHz -> 32-bit integer VALU lane-ops/s.
+PEAK_VALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+HBM_PEAK_GBS = 8000.0
+# simulation kernels, in launch order, between the library's measurement boundaries
+SIM_KERNELS = ["k_sim<2>", "k_sim<1>", "k_sim<8>", "k_sim_mat<2>"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_k_sim_workload3.json")
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("octo.hip", "octo_sim.hpp", "octo_device.hpp"):
+        with open(os.path.join(ROOT, "paper_2509_23722_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_work(recs, P, M):
+    """Per candidate: N ops, E edges of the DAG (queue order N - P, forward and backward chains
+    2 (S-1) M, F->B S M, B->W S M when split). Relaxation = one add + one max per edge and one
+    add per op (2E + N int64 ops) = 5E + 2N 32-bit lane-ops (add = 2, max = cmp + 2 selects).
+    Returns per-candidate (int64 ops, lane-ops) arrays."""
+    v = recs[:, 1].astype(np.int64)
+    split = recs[:, 0] == 3
+    S = P * v
+    N = np.where(split, 3, 2) * S * M
+    E = (N - P) + 2 * (S - 1) * M + S * M + np.where(split, S * M, 0)
+    return 2 * E + N, 5 * E + 2 * N
+
+
+def hip_events(n):
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    evs = []
+    for _ in range(n):
+        e = ctypes.c_void_p()
+        if hip.hipEventCreate(ctypes.byref(e)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        evs.append(e.value)
+    return hip, evs
+
+
+def copy_calibration(torch):
+    """A plain device copy of known size, for scaling the HBM counters."""
+    nbytes = 1 << 30
+    x = torch.empty(nbytes // 8, dtype=torch.int64, device="cuda:0").fill_(1)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline leg")
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the batch is split across GPUs by candidate "
+              f"range with no communication in the hot loop, so --gpus {args.gpus} is not run "
+              f"here.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2509_23722_amd import _lib, inputs
+
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
+
+    dev = torch.device("cuda:0")
+    w = inputs.WORKLOADS[3]
+    costs_np, link_np = inputs.layer_costs(w), inputs.link_matrix(w.P, w.link_ns)
+    recs_np = inputs.candidates(w)
+    n = recs_np.shape[0]
+    prob = _lib.problem(w.L, w.P, w.v_max, w.M, recs_np.shape[1], w.max_pert)
+    costs = torch.from_numpy(costs_np).to(dev)
+    link = torch.from_numpy(link_np).to(dev)
+    recs = torch.from_numpy(recs_np).to(dev)
+    ms = torch.empty(n, dtype=torch.int64, device=dev)
+    bub = torch.empty((n, w.P), dtype=torch.int64, device=dev)
+
+    for _ in range(args.warmup):
+        _lib.sim_batch(prob, costs, link, recs, ms, bub)
+    torch.cuda.synchronize()
+
+    nb = len(SIM_KERNELS) + 1
+    hip, evs = hip_events(nb * args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        _lib.profile_events(evs[nb * k:nb * (k + 1)])
+        _lib.sim_batch(prob, costs, link, recs, ms, bub)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    _lib.profile_events([])
+    kern_ms = np.zeros((args.steps, len(SIM_KERNELS)))
+    for k in range(args.steps):
+        for j in range(len(SIM_KERNELS)):
+            f = ctypes.c_float()
+            hip.hipEventElapsedTime(ctypes.byref(f), evs[nb * k + j], evs[nb * k + j + 1])
+            kern_ms[k, j] = f.value
+    for e in evs:
+        hip.hipEventDestroy(e)
+
+    secs = t1 - t0
+    value = n * args.steps / secs
+    ms_per_step = secs / args.steps * 1e3
+    per_kernel_ms = kern_ms.mean(axis=0)
+    int64_c, lane_c = algorithmic_work(recs_np, w.P, w.M)
+    v = recs_np[:, 1]
+    # the dominant kernel: k_sim<2>, which simulates the v = 2 candidates
+    dom = 0
+    dom_ms = float(per_kernel_ms[dom])
+    dom_lane_ops = int(lane_c[v == 2].sum())
+    achieved = dom_lane_ops / (dom_ms * 1e-3) / 1e12
+    n_dom = int((v == 2).sum())
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        t = json.load(open(TRAFFIC_FILE))
+        if t.get("kernel_source_sha") == kernel_source_hash():
+            traffic = t.get("hbm_bytes_per_launch")
+    all_ms = float(per_kernel_ms.sum())
+    roofline = {
+        "bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU_TOPS, 2),
+        "unit": "Tops/s (32-bit VALU lane-ops)", "frac": round(achieved / PEAK_VALU_TOPS, 5),
+        "traffic": traffic, "kernel": SIM_KERNELS[dom], "kernel_ms": round(dom_ms, 4),
+        "kernel_candidates": n_dom, "alg_lane_ops_per_launch": dom_lane_ops,
+        "alg_int64_ops_per_launch": int(int64_c[v == 2].sum()),
+        "hbm_alg_gbs": round(n_dom * (recs_np.shape[1] + 8 + 8 * w.P) / (dom_ms * 1e-3) / 1e9, 2),
+        "hbm_peak_gbs": HBM_PEAK_GBS,
+        "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, per_kernel_ms)},
+        "all_sim_kernels_frac": round(int(lane_c.sum()) / (all_ms * 1e-3) / 1e12 / PEAK_VALU_TOPS,
+                                      5),
+    }
+
+    gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
+    cpu = None
+    if not args.no_cpu:
+        from oracle import octoref
+        sample = np.arange(0, n, 16)
+        threads = min(16, os.cpu_count() or 1)
+        rprob = octoref.problem(w.L, w.P, w.v_max, w.M, recs_np.shape[1], w.max_pert)
+        c0 = time.perf_counter()
+        rms, rbub = octoref.sim_batch(rprob, costs_np, link_np, recs_np[sample], nthreads=threads)
+        c1 = time.perf_counter()
+        same = bool((rms == gms[sample]).all() and (rbub == gbub[sample]).all())
+        cpu = {"value": round(len(sample) / (c1 - c0), 1), "unit": "candidates/s",
+               "cores": threads, "kind": "oracle",
+               "sample": f"every 16th candidate of the same batch ({len(sample)} candidates, "
+                         f"{c1 - c0:.2f} s wall on {threads} threads)",
+               "parity_on_sample": same}
+        if not same:
+            print("bench: GPU results differ from the oracle on the sample", file=sys.stderr)
+
+    out = {
+        "metric": "candidate schedules simulated/sec at P=8,M=64",
+        "value": round(value, 1), "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": w.name, "candidates": n, "P": w.P, "M": w.M, "L": w.L,
+                   "v": [1, 2], "policies": ["AFAB", "1F1B", "I1F1B", "ZB"],
+                   "placements": list(inputs.PLACEMENTS), "seed": w.seed},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

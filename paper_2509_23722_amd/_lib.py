@@ -47,6 +47,8 @@ def lib():
         L.octo_sim_batch.restype = ctypes.c_int
         L.octo_tune_step.argtypes = [pp, vp, vp, vp, vp, i64, ctypes.c_uint64, i32, vp]
         L.octo_tune_step.restype = ctypes.c_int
+        L.octo_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), i32]
+        L.octo_profile_events.restype = ctypes.c_int
         L.octo_strerror.argtypes = [ctypes.c_int]
         L.octo_strerror.restype = ctypes.c_char_p
         _lib = L
@@ -117,6 +119,13 @@ def tune_step(prob, layer_costs, link, chains, queues, seed, step, stream=None):
         _dev_ptr(q, q.dtype, "queues"), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
         _stream(chains, stream))
     _check(rc, "octo_tune_step")
+
+
+def profile_events(events):
+    """Record hipEvent_t handles (ints) at the simulation-kernel boundaries of later calls
+    (see include/octo.h); an empty list turns it off."""
+    arr = (ctypes.c_void_p * max(len(events), 1))(*events)
+    _check(lib().octo_profile_events(arr, len(events)), "octo_profile_events")
 
 
 def chain_state(chains, prob):

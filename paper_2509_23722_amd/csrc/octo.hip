@@ -29,62 +29,68 @@ namespace octo {
 constexpr int WAVE = 64;
 
 // Workspace control block (int32 words).
-constexpr int CTL_COUNTS = 0;    // [NBINS] candidates per bin
-constexpr int CTL_CURSOR = 64;   // [NBINS] scatter cursors
-constexpr int CTL_WORK = 128;    // chunk counter of k_sim
-constexpr int CTL_WORK_MAT = 129;
+constexpr int CTL_COUNTS = 0;     // [NBINS] candidates per bin
+constexpr int CTL_CURSOR = 64;    // [NBINS] scatter cursors
+constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (3)
+constexpr int CTL_WORK_MAT = 131; // chunk counter of k_sim_mat, perturbed list
+constexpr int CTL_WORK_REDO = 132;// chunk counter of k_sim_mat, redo list
+constexpr int CTL_REDO = 133;     // candidates whose times overflowed the 40-bit slots
 constexpr int CTL_WORDS = 256;
 
 struct SimArgs {
   Problem pr;
-  const int64_t* pre;   // [(L+1)][3] prefix sums of layer costs
-  const int64_t* link;  // [P][P]
+  const int64_t* pre;    // [(L+1)][3] prefix sums of layer costs
+  const int64_t* link;   // [P][P]
   const uint8_t* cands;
   int64_t n;
   int64_t* out_ms;
   int64_t* out_bub;
   int32_t* ctl;
-  const int32_t* idx;  // candidate indices sorted by bin
+  const int32_t* idx;    // candidate indices sorted by bin
+  int32_t* redo;         // candidates to recompute with 64-bit slots
   const uint32_t* mtab;  // MERGE tables, merge_offset() entries apart
-  uint16_t* qscratch;  // materialised queues, [group slot][P][qcap]
-  int G, CPW;          // lanes per candidate, candidates per wave
-  int table_slots;     // int64 slots of one finish table ((S_cap+1)*M + 2)
-  int sink;            // slot that weight-gradient ops write ((S_cap+1)*M)
-  int group_bytes;     // LDS bytes per candidate (table + staged record)
-  int rec_bytes;       // staged record bytes (header + boundaries + placement)
+  uint16_t* qscratch;    // materialised queues, [group slot][P][qcap]
+  int G, CPW;            // lanes per candidate, candidates per wave
+  int slots;             // slots of one finish table (S_cap * M)
+  int table_bytes;       // LDS bytes of one finish table
+  int group_bytes;       // LDS bytes per candidate
+  int rec_bytes;         // staged record bytes (header + boundaries + placement)
   int qcap;
-  int bin_lo, bin_hi;  // generated bins handled by this launch
+  int bin_lo, bin_hi;    // generated bins handled by this launch
+  int work;              // chunk counter index of this launch
 };
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
 
 __device__ __forceinline__ int bcast(int x) { return __shfl(x, 0); }
 
-// Group mask of this lane's candidate inside the wave.
-__device__ __forceinline__ uint64_t group_mask(int G) {
-  if (G >= WAVE) return ~0ull;
-  const int g = lane_id() / G;
-  return ((1ull << G) - 1) << (g * G);
-}
-
 // ---------------------------------------------------------------------------------------------
 // Per-lane set-up of one candidate from its staged record.
 // ---------------------------------------------------------------------------------------------
 template <int VMAX>
-__device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr, const uint8_t* rec,
-                                       const int64_t* pre, const int64_t* link, int d, int v,
-                                       int split) {
-  const int S = pr.P * v;
+__device__ __forceinline__ void zero_chunks(Chunks<VMAX>& c) {
+#pragma unroll
+  for (int k = 0; k < VMAX; ++k) {
+    c.st[k] = 0, c.base[k] = 0, c.foff[k] = 0, c.fneed[k] = 0, c.boff[k] = 0, c.bneed[k] = 0;
+    c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+  }
+}
+
+// Stages of device d (ascending), their durations, incoming link weights and slot offsets;
+// returns busy(d).
+template <int VMAX>
+__device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr,
+                                                const uint8_t* rec, const int64_t* pre,
+                                                const int64_t* link, int d, int v, int split) {
+  const int S = pr.P * v, M = pr.M;
   const uint8_t* bnd = rec + 4;
   const uint8_t* dev = rec + 3 + pr.s_max;
+  zero_chunks<VMAX>(c);
   int cnt = 0;
-#pragma unroll
-  for (int k = 0; k < VMAX; ++k) c.st[k] = 0;
   for (int s = 0; s < S; ++s) {
     if (dev[s] == d) {
 #pragma unroll
-      for (int k = 0; k < VMAX; ++k)
-        if (cnt == k) c.st[k] = s;
+      for (int k = 0; k < VMAX; ++k) c.st[k] = cnt == k ? s : c.st[k];
       ++cnt;
     }
   }
@@ -98,6 +104,11 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       const int64_t f = pre[3 * b1 + 0] - pre[3 * b0 + 0];
       const int64_t bi = pre[3 * b1 + 1] - pre[3 * b0 + 1];
       const int64_t wg = pre[3 * b1 + 2] - pre[3 * b0 + 2];
+      c.base[k] = s * M;
+      c.foff[k] = s > 0 ? -M : 0;     // stage 0 reads its own start token
+      c.fneed[k] = s > 0 ? 1 : 2;     // bit of ST_F / ST_TOKEN
+      c.boff[k] = s < S - 1 ? M : 0;  // the last stage reads its own F
+      c.bneed[k] = s < S - 1 ? 0 : 1; // bit of ST_B / ST_F
       c.dF[k] = f;
       c.dB[k] = split ? bi : bi + wg;
       c.dW[k] = wg;
@@ -106,37 +117,43 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       c.wF[k] = dp != d ? link[dp * pr.P + d] : 0;
       c.wB[k] = dn != d ? link[dn * pr.P + d] : 0;
       busy += f + bi + wg;
-    } else {
-      c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
     }
   }
-  return busy * pr.M;
+  return busy * M;
+}
+
+// Group bits for deadlock folding: this lane's group bit and the set of all group bits.
+__device__ __forceinline__ void group_bits(int G, uint64_t* gbit, uint64_t* lsb) {
+  uint64_t x = 0;
+  for (int i = 0; i < WAVE; i += G) x |= 1ull << i;
+  *lsb = x;
+  *gbit = 1ull << ((lane_id() / G) * G);
 }
 
 // Stage the first rec_bytes of a record into LDS (lanes of the candidate copy 4-byte words).
-__device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, int rec_bytes, int d, int G) {
+__device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, int rec_bytes,
+                                             int d, int G) {
   const int words = (rec_bytes + 3) >> 2;
   for (int i = d; i < words; i += G)
     reinterpret_cast<uint32_t*>(dst)[i] = reinterpret_cast<const uint32_t*>(src)[i];
 }
 
-// Fill the finish table: row -1 = 0 (ready at time 0), rows 0..S-1 empty (-2).
-__device__ __forceinline__ void clear_table(int64_t* T, int S, int M, int d, int G) {
-  const int n = (S + 1) * M;
-  for (int i = d; i < n; i += G) T[i] = i < M ? 0 : -2;
+__device__ __forceinline__ Table40 table40(uint8_t* g, int slots) {
+  return Table40{reinterpret_cast<uint32_t*>(g), g + (size_t)slots * 4};
 }
 
-// Simulate one candidate per group of the wave with generator kind GEN, write the results.
-// cand < 0: this group has no candidate. Returns nothing; results go to out_ms / out_bub.
-template <int VMAX, int GEN>
-__device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split, uint8_t* lds_group) {
+// Simulate one candidate per group of the wave with generator kind GEN (40-bit slots; the
+// staged record shares the table's memory until the table is cleared), write the results.
+// cand < 0: this group has no candidate. P2: P and v are powers of two.
+template <int VMAX, int GEN, bool P2>
+__device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split,
+                                              uint8_t* lds_group) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
   const int d = lane_id() % G;
-  int64_t* T = reinterpret_cast<int64_t*>(lds_group);
-  uint8_t* rec = lds_group + (size_t)a.table_slots * 8;
+  const Table40 T = table40(lds_group, a.slots);
+  uint8_t* rec = lds_group;
   const bool has = cand >= 0;
   const int S = P * v;
-  const int sink = a.sink;
   if (has) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
   __asm__ volatile("" ::: "memory");
 
@@ -145,46 +162,57 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   L.clock = 0;
   L.pos = 0;
   L.nops = 0;
-  L.live = false;
   int64_t busy = 0;
   const bool mine = has && d < P;
   if (mine) {
     busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
     L.nops = (split ? 3 : 2) * v * M;
-    L.live = true;
   } else {
-#pragma unroll
-    for (int k = 0; k < VMAX; ++k) c.st[k] = 0, c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+    zero_chunks<VMAX>(c);
   }
-  if (has) clear_table(T, S, M, d, G);
+  __asm__ volatile("" ::: "memory");
+  if (has) T.clear(S * M, M, d, G);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
-  const uint64_t gm = group_mask(G);
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
   if constexpr (GEN == GEN_AFAB) {
     GenAfab g;
     g.init(v, M);
-    if (mine) describe<VMAX>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
-    relax<VMAX>(g, c, L, T, M, S, sink, gm, dead, nullptr);
+    describe<VMAX>(L, c, g.kind, g.k, g.m);
+    relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
   } else if constexpr (GEN == GEN_INTER) {
-    GenInter g;
     const int r = c.st[0];
-    g.init(P, v, M, r, split, split ? r : 0);
-    if (mine) describe<VMAX>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
-    relax<VMAX>(g, c, L, T, M, S, sink, gm, dead, nullptr);
+    if constexpr (P2) {
+      GenInterP2 g;
+      g.init(P, v, M, r, split, split ? r : 0);
+      describe<VMAX>(L, c, g.kind, g.k, g.m);
+      relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
+    } else {
+      GenInter g;
+      g.init(P, v, M, r, split, split ? r : 0);
+      describe<VMAX>(L, c, g.kind, g.k, g.m);
+      relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
+    }
   } else {
     GenMerge<VMAX> g;
     const int rowlen = (split ? 3 : 2) * M;
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
            [&](int k) { return pick<VMAX>(c.st, k); });
-    if (mine) describe<VMAX>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
-    relax<VMAX>(g, c, L, T, M, S, sink, gm, dead, nullptr);
+    describe<VMAX>(L, c, g.kind, g.k, g.m);
+    relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
   }
 
   const int64_t ms = group_max(L.clock, G);
   if (mine) {
-    if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
-    a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+    if (ms >= Table40::LIMIT) {
+      // times beyond the 40-bit slots: recompute this candidate with 64-bit slots
+      if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+    } else {
+      if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
+      a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+    }
   }
 }
 
@@ -217,29 +245,31 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   if (v > v_hi) return;
   const int S = P * v;
   const int d = lane_id();
-  int64_t* T = reinterpret_cast<int64_t*>(smem);
+  const Table64 T{reinterpret_cast<int64_t*>(smem)};
   const int rowlen = (split ? 3 : 2) * M;
   uint32_t* tab = mtab + merge_offset(P, M, v, split);
-  clear_table(T, S, M, d, WAVE);
+  T.clear(S * M, M, d, WAVE);
   __asm__ volatile("" ::: "memory");
   Chunks<1> c;
+  zero_chunks<1>(c);
   c.st[0] = d;
+  c.base[0] = d * M;
+  c.foff[0] = d > 0 ? -M : 0;
+  c.fneed[0] = d > 0 ? 1 : 2;
+  c.boff[0] = d < S - 1 ? M : 0;
+  c.bneed[0] = d < S - 1 ? 0 : 1;
   c.dF[0] = 1;
   c.dB[0] = split ? 1 : 2;
   c.dW[0] = 1;
-  c.wF[0] = 0;
-  c.wB[0] = 0;
   Lane L;
   L.clock = 0;
   L.pos = 0;
   L.nops = d < S ? rowlen : 0;
-  L.live = d < S;
-  const int sink = (S + 1) * M;  // the LDS table is sized for the largest v
   GenInter g;
   g.init(S, 1, M, d < S ? d : 0, split, split ? d : 0);
-  if (L.live) describe<1>(L, c, g.kind(), g.chunk(), g.mb(), M, S, sink);
+  describe<1>(L, c, g.kind, g.k, g.m);
   bool dead = false;
-  relax<1>(g, c, L, T, M, S, sink, ~0ull, dead, d < S ? tab + d * rowlen : nullptr);
+  relax<1>(g, c, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
 }
 
 // One thread per candidate.
@@ -266,7 +296,8 @@ __global__ void k_classify(SimArgs a, uint8_t* __restrict__ bins) {
     if (hist[b]) atomicAdd(&a.ctl[CTL_COUNTS + b], hist[b]);
 }
 
-__global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins, int32_t* __restrict__ idx) {
+__global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
+                          int32_t* __restrict__ idx) {
   __shared__ int base[NBINS + 1];
   __shared__ int hist[NBINS];
   __shared__ int res[NBINS];
@@ -310,23 +341,25 @@ __device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, int lo,
 }
 
 template <int VMAX>
-__device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v, int split,
-                             uint8_t* lds_group) {
-  if (gen == GEN_AFAB) run_generated<VMAX, GEN_AFAB>(a, cand, v, split, lds_group);
-  else if (gen == GEN_INTER) run_generated<VMAX, GEN_INTER>(a, cand, v, split, lds_group);
-  else run_generated<VMAX, GEN_MERGE>(a, cand, v, split, lds_group);
+__device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
+                                             int split, uint8_t* lds_group) {
+  const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
+  if (gen == GEN_AFAB) run_generated<VMAX, GEN_AFAB, false>(a, cand, v, split, lds_group);
+  else if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_group);
+  else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_group);
+  else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_group);
 }
 
-// VCAP = 2 handles the bins of v = 1, 2; VCAP = 8 those of v = 3..8.
-template <int VCAP>
+// Generated-queue simulation for the bins of one v class: VC = 1 (v = 1), 2 (v = 2) or 8
+// (v = 3..8); finish tables sized for that class.
+template <int VC>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int g = lane_id() / a.G;
   uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
-  const int work = VCAP == 2 ? CTL_WORK : CTL_WORK + 2;
   for (;;) {
     int ch = 0;
-    if (lane_id() == 0) ch = atomicAdd(&a.ctl[work], 1);
+    if (lane_id() == 0) ch = atomicAdd(&a.ctl[a.work], 1);
     ch = bcast(ch);
     int entry0 = 0, pos0 = 0;
     const int bin = locate_chunk(a.ctl, a.CPW, a.bin_lo, a.bin_hi, ch, &entry0, &pos0);
@@ -336,12 +369,7 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     const int cnt = a.ctl[CTL_COUNTS + bin];
     const int e = entry0 + g;
     const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
-    if constexpr (VCAP == 2) {
-      if (v == 1) dispatch_gen<1>(a, gen, cand, v, split, lds_group);
-      else dispatch_gen<2>(a, gen, cand, v, split, lds_group);
-    } else {
-      dispatch_gen<8>(a, gen, cand, v, split, lds_group);
-    }
+    dispatch_gen<VC>(a, gen, cand, v, split, lds_group);
   }
 }
 
@@ -349,15 +377,15 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
 template <class Gen>
 __device__ __forceinline__ void emit_queue(Gen& g, uint16_t* row, int n) {
   for (int i = 0; i < n; ++i) {
-    row[i] = qpack(g.kind(), g.chunk(), g.mb());
-    if (i + 1 < n) g.step();
+    row[i] = qpack(g.kind, g.k, g.m);
+    g.advance(true);
   }
 }
 
 // Materialise the queue of lane d for a staged record; returns the queue length.
 template <int VMAX>
-__device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>& c, int v, int gen,
-                                           int split, uint16_t* row) {
+__device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>& c, int v,
+                                           int gen, int split, uint16_t* row) {
   const int P = a.pr.P, M = a.pr.M;
   const int n = (split ? 3 : 2) * v * M;
   if (gen == GEN_AFAB) {
@@ -388,6 +416,8 @@ __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
   row[to] = x;
 }
 
+// Candidates with perturbations, then candidates whose times overflowed the 40-bit slots:
+// queues materialised in global memory, moves applied, 64-bit finish tables.
 template <int VMAX>
 __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
@@ -395,74 +425,76 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   const int g = lane_id() / G;
   const int d = lane_id() % G;
   uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
-  int64_t* T = reinterpret_cast<int64_t*>(lds_group);
-  uint8_t* rec = lds_group + (size_t)a.table_slots * 8;
+  const Table64 T{reinterpret_cast<int64_t*>(lds_group)};
+  uint8_t* rec = lds_group + a.table_bytes;
   const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
   uint16_t* row = a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap;
-  const int sink = a.sink;
-  const uint64_t gm = group_mask(G);
-  for (;;) {
-    int ch = 0;
-    if (lane_id() == 0) ch = atomicAdd(&a.ctl[CTL_WORK_MAT], 1);
-    ch = bcast(ch);
-    int base = 0;
-    for (int b = 0; b < BIN_MAT; ++b) base += a.ctl[CTL_COUNTS + b];
-    const int cnt = a.ctl[CTL_COUNTS + BIN_MAT];
-    if (ch * a.CPW >= cnt) break;
-    const int e = ch * a.CPW + g;
-    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[base + e] : -1;
-    const bool has = cand >= 0;
-    const bool mine = has && d < P;
-    const uint8_t* grec = has ? a.cands + cand * a.pr.stride : a.cands;
-    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
-    __asm__ volatile("" ::: "memory");
-    const int policy = has ? rec[0] : 0;
-    const int v = has ? rec[1] : 1;
-    const int split = policy == POL_ZB;
-    int gen = GEN_AFAB;
-    if (has) {
-      Resolved r = resolve_record(a.pr, grec);
-      gen = r.gen;
-    }
-    Chunks<VMAX> c;
-    int64_t busy = 0;
-    Lane L;
-    L.clock = 0, L.pos = 0, L.nops = 0, L.live = false;
-    if (mine) {
-      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
-      L.nops = materialise<VMAX>(a, c, v, gen, split, row);
-      const uint8_t* pp = grec + pert_off(a.pr.s_max);
-      const int np = grec[2];
-      for (int i = 0; i < np; ++i) {
-        const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
-        if (pd != d) continue;
-        const int from = pp[6 * i + 2] | (pp[6 * i + 3] << 8);
-        const int to = pp[6 * i + 4] | (pp[6 * i + 5] << 8);
-        move_entry(row, from, to);
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  int base = 0;
+  for (int b = 0; b < BIN_MAT; ++b) base += a.ctl[CTL_COUNTS + b];
+  for (int phase = 0; phase < 2; ++phase) {
+    const int32_t* list = phase == 0 ? a.idx + base : a.redo;
+    const int cnt = phase == 0 ? a.ctl[CTL_COUNTS + BIN_MAT] : a.ctl[CTL_REDO];
+    const int counter = phase == 0 ? CTL_WORK_MAT : CTL_WORK_REDO;
+    for (;;) {
+      int ch = 0;
+      if (lane_id() == 0) ch = atomicAdd(&a.ctl[counter], 1);
+      ch = bcast(ch);
+      if (ch * a.CPW >= cnt) break;
+      const int e = ch * a.CPW + g;
+      const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)list[e] : -1;
+      const bool has = cand >= 0;
+      const bool mine = has && d < P;
+      const uint8_t* grec = has ? a.cands + cand * a.pr.stride : a.cands;
+      if (has) stage_record(rec, grec, a.rec_bytes, d, G);
+      __asm__ volatile("" ::: "memory");
+      const int policy = has ? rec[0] : 0;
+      const int v = has ? rec[1] : 1;
+      const int split = policy == POL_ZB;
+      int gen = GEN_AFAB;
+      if (has) {
+        Resolved r = resolve_record(a.pr, grec);
+        gen = r.gen;
       }
-      L.live = L.nops > 0;
-    } else {
-#pragma unroll
-      for (int k = 0; k < VMAX; ++k) c.st[k] = 0, c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
-    }
-    const int S = P * v;
-    if (has) clear_table(T, S, M, d, G);
-    __asm__ volatile("" ::: "memory");
-    GenMat q;
-    q.init(row, L.nops);
-    if (L.live) describe<VMAX>(L, c, q.kind(), q.chunk(), q.mb(), M, S, sink);
-    bool dead = false;
-    relax<VMAX>(q, c, L, T, M, S, sink, gm, dead, nullptr);
-    const int64_t ms = group_max(L.clock, G);
-    if (mine) {
-      if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
-      a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+      Chunks<VMAX> c;
+      int64_t busy = 0;
+      Lane L;
+      L.clock = 0, L.pos = 0, L.nops = 0;
+      if (mine) {
+        busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+        L.nops = materialise<VMAX>(a, c, v, gen, split, row);
+        const uint8_t* pp = grec + pert_off(a.pr.s_max);
+        const int np = grec[2];
+        for (int i = 0; i < np; ++i) {
+          const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
+          if (pd != d) continue;
+          const int from = pp[6 * i + 2] | (pp[6 * i + 3] << 8);
+          const int to = pp[6 * i + 4] | (pp[6 * i + 5] << 8);
+          move_entry(row, from, to);
+        }
+      } else {
+        zero_chunks<VMAX>(c);
+      }
+      const int S = P * v;
+      if (has) T.clear(S * M, M, d, G);
+      __asm__ volatile("" ::: "memory");
+      GenMat q;
+      q.init(row, L.nops);
+      describe<VMAX>(L, c, q.kind, q.k, q.m);
+      bool dead = false;
+      relax<VMAX>(q, c, L, T, G, gbit, lsb, dead, nullptr);
+      const int64_t ms = group_max(L.clock, G);
+      if (mine) {
+        if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
+        a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// Local-search step (one chain per group).
+// Local-search step (one chain per group, 64-bit finish tables).
 // ---------------------------------------------------------------------------------------------
 struct TuneArgs {
   SimArgs s;
@@ -482,10 +514,10 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   const int g = lane_id() / G;
   const int d = lane_id() % G;
   uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
-  int64_t* T = reinterpret_cast<int64_t*>(lds_group);
-  uint8_t* rec = lds_group + (size_t)a.table_slots * 8;
-  const int sink = a.sink;
-  const uint64_t gm = group_mask(G);
+  const Table64 T{reinterpret_cast<int64_t*>(lds_group)};
+  uint8_t* rec = lds_group + a.table_bytes;
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
   for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < t.n_chains; base += n_groups) {
     const int64_t chain = base + g;
@@ -522,7 +554,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     const int qlen = (split ? 3 : 2) * v * M;
 
     // propose (step >= 1); the move is applied to the staged record / this chain's queue row
-    int kind = -1, mi = 0, old = 0, sd = -1;
+    int kind = -1, mi = 0, sd = -1;
     bool valid = true;
     if (!skip && t.step > 0) {
       U4 u = philox4x64_10((uint64_t)chain, (uint64_t)t.step, 0, 0, t.seed, 0);
@@ -534,8 +566,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
           mi = 1 + (int)(u.x[1] % (uint64_t)(S - 1));
           const int lo = mi > 1 ? rec[4 + mi - 2] : 0;
           const int hi = mi < S - 1 ? rec[4 + mi] : a.pr.L;
-          old = rec[4 + mi - 1];
-          const int nb = old + ((u.x[2] & 1) ? 1 : -1);
+          const int nb = rec[4 + mi - 1] + ((u.x[2] & 1) ? 1 : -1);
           valid = nb > lo && nb < hi;
           __asm__ volatile("" ::: "memory");
           if (valid && d == 0) rec[4 + mi - 1] = (uint8_t)nb;
@@ -572,23 +603,21 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     Chunks<VMAX> c;
     int64_t busy = 0;
     Lane L;
-    L.clock = 0, L.pos = 0, L.nops = 0, L.live = false;
+    L.clock = 0, L.pos = 0, L.nops = 0;
     if (run && d < P) {
       busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
       if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, row);
       L.nops = qlen;
-      L.live = true;
     } else {
-#pragma unroll
-      for (int k = 0; k < VMAX; ++k) c.st[k] = 0, c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+      zero_chunks<VMAX>(c);
     }
-    if (run) clear_table(T, S, M, d, G);
+    if (run) T.clear(S * M, M, d, G);
     __asm__ volatile("" ::: "memory");
     GenMat q;
     q.init(row, L.nops);
-    if (L.live) describe<VMAX>(L, c, q.kind(), q.chunk(), q.mb(), M, S, sink);
+    describe<VMAX>(L, c, q.kind, q.k, q.m);
     bool dead = false;
-    relax<VMAX>(q, c, L, T, M, S, sink, gm, dead, nullptr);
+    relax<VMAX>(q, c, L, T, G, gbit, lsb, dead, nullptr);
     const int64_t ms = group_max(L.clock, G);
 
     if (!has || skip) continue;
@@ -611,7 +640,6 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
       row[mi] = row[mi + 1];
       row[mi + 1] = x;
     }
-    (void)old;
   }
 }
 
@@ -634,6 +662,8 @@ struct Workspace {
 
 std::mutex g_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+hipEvent_t g_prof[8] = {};  // measurement hook: events at the simulation-kernel boundaries
+int g_prof_n = 0;
 
 struct DevInfo {
   int cus = 0;
@@ -673,19 +703,38 @@ int dev_info(int dev, DevInfo* out) {
 }
 
 struct Plan {
-  int G, CPW, table_slots, sink, rec_bytes, group_bytes, lds_bytes, qcap;
+  int G, CPW, slots, table_bytes, rec_bytes, group_bytes, lds_bytes, qcap;
 };
 
-// LDS plan for tables of up to s_cap stages: G lanes per candidate (power of two >= P), as
-// many candidates per wave as lanes and LDS allow.
-Plan make_plan(const octo_problem* p, int lds_max, int s_cap) {
+int lanes_per_candidate(int P) {
+  int G = 1;
+  while (G < P) G <<= 1;
+  return G;
+}
+
+// 40-bit-slot plan for generated queues with up to s_cap stages; the staged record shares the
+// table's memory.
+Plan fast_plan(const octo_problem* p, int lds_max, int s_cap) {
   Plan pl;
-  pl.G = 1;
-  while (pl.G < p->P) pl.G <<= 1;
-  pl.table_slots = (s_cap + 1) * p->M + 2;
-  pl.sink = (s_cap + 1) * p->M;
+  pl.G = lanes_per_candidate(p->P);
+  pl.slots = s_cap * p->M;
   pl.rec_bytes = pert_off(p->P * p->v_max);
-  pl.group_bytes = (int)(align_up((size_t)pl.table_slots * 8, 16) + align_up(pl.rec_bytes, 16));
+  pl.table_bytes = (int)(pl.slots * 4 + align_up(pl.slots, 4));
+  pl.group_bytes = (int)align_up(std::max<size_t>(pl.table_bytes, align_up(pl.rec_bytes, 4)), 16);
+  pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
+  pl.lds_bytes = pl.CPW * pl.group_bytes;
+  pl.qcap = 3 * p->v_max * p->M;
+  return pl;
+}
+
+// 64-bit-slot plan for materialised queues and tuner chains (record staged separately).
+Plan big_plan(const octo_problem* p, int lds_max) {
+  Plan pl;
+  pl.G = lanes_per_candidate(p->P);
+  pl.slots = p->P * p->v_max * p->M;
+  pl.rec_bytes = pert_off(p->P * p->v_max);
+  pl.table_bytes = (int)align_up((size_t)pl.slots * 8, 16);
+  pl.group_bytes = pl.table_bytes + (int)align_up(pl.rec_bytes, 16);
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
   pl.lds_bytes = pl.CPW * pl.group_bytes;
   pl.qcap = 3 * p->v_max * p->M;
@@ -698,7 +747,7 @@ size_t mtab_entries(const octo_problem* p) {
 
 // Workspace layout (byte offsets).
 struct Layout {
-  size_t ctl, pre, mtab, bin_of, idx, qscr, total;
+  size_t ctl, pre, mtab, bin_of, idx, redo, qscr, total;
 };
 
 Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slots) {
@@ -713,6 +762,8 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   l.bin_of = o;
   o = align_up(o + (size_t)n, 256);
   l.idx = o;
+  o = align_up(o + (size_t)n * 4, 256);
+  l.redo = o;
   o = align_up(o + (size_t)n * 4, 256);
   l.qscr = o;
   o = align_up(o + (size_t)mat_slots * p->P * big.qcap * 2, 256);
@@ -757,7 +808,7 @@ int occupancy_grid(K kernel, int lds, int cus, int* grid) {
 int launch_ok() { return hipGetLastError() == hipSuccess ? OCTO_OK : OCTO_EHIP; }
 
 struct Setup {
-  Plan small, big;  // tables for v <= 2 / for v_max
+  Plan big;
   Layout l;
   Workspace* ws;
   DevInfo di;
@@ -777,8 +828,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
   if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
   int rc = dev_info(dev, &su->di);
   if (rc) return rc;
-  su->big = make_plan(prob, su->di.lds_max, prob->P * prob->v_max);
-  su->small = make_plan(prob, su->di.lds_max, prob->P * std::min(prob->v_max, 2));
+  su->big = big_plan(prob, su->di.lds_max);
   if (su->big.CPW < 1) return OCTO_EUNSUPPORTED;
   rc = prob->v_max <= 2 ? mat_grid_for<2>(su->big, su->di.cus, &su->mat_grid)
                         : mat_grid_for<8>(su->big, su->di.cus, &su->mat_grid);
@@ -795,7 +845,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
   if ((rc = launch_ok())) return rc;
   if (prob->v_max >= 2 && !(ws.mt_valid && ws.mt_P == prob->P && ws.mt_vmax == prob->v_max &&
                             ws.mt_M == prob->M)) {
-    const int lds = (int)align_up((size_t)((prob->P * prob->v_max + 1) * prob->M + 2) * 8, 16);
+    const int lds = (int)align_up((size_t)prob->P * prob->v_max * prob->M * 8, 16);
     if (lds > su->di.lds_max) return OCTO_EUNSUPPORTED;
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_merge_tab),
                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -823,24 +873,33 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.out_bub = bub;
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
   a.idx = reinterpret_cast<const int32_t*>(base + l.idx);
+  a.redo = reinterpret_cast<int32_t*>(base + l.redo);
   a.mtab = reinterpret_cast<const uint32_t*>(base + l.mtab);
   a.qscratch = reinterpret_cast<uint16_t*>(base + l.qscr);
   a.G = pl.G;
   a.CPW = pl.CPW;
-  a.table_slots = pl.table_slots;
-  a.sink = pl.sink;
+  a.slots = pl.slots;
+  a.table_bytes = pl.table_bytes;
   a.group_bytes = pl.group_bytes;
   a.rec_bytes = pl.rec_bytes;
   a.qcap = pl.qcap;
   a.bin_lo = 0;
   a.bin_hi = NBIN_GEN;
+  a.work = CTL_WORK;
   return a;
 }
 
+// Launch k_sim<VC> over generated bins [lo, hi) with its own 40-bit plan.
 template <int VC>
-int launch_sim(const SimArgs& a, const Plan& pl, int cus, int64_t n, hipStream_t stream) {
+int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
+               int64_t n, int64_t* ms, int64_t* bub, int s_cap, int lo, int hi, int work,
+               hipStream_t stream) {
+  const Plan pl = fast_plan(prob, su.di.lds_max, s_cap);
+  if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
+  SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub);
+  a.bin_lo = lo, a.bin_hi = hi, a.work = work;
   int grid = 0;
-  int rc = occupancy_grid(k_sim<VC>, pl.lds_bytes, cus, &grid);
+  int rc = occupancy_grid(k_sim<VC>, pl.lds_bytes, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
@@ -850,7 +909,7 @@ int launch_sim(const SimArgs& a, const Plan& pl, int cus, int64_t n, hipStream_t
 
 template <int VC>
 int launch_tune(const TuneArgs& t, const Plan& pl, int cus, int64_t n_chains,
-                       hipStream_t stream) {
+                hipStream_t stream) {
   int grid = 0;
   int rc = occupancy_grid(k_tune<VC>, pl.lds_bytes, cus, &grid);
   if (rc) return rc;
@@ -858,6 +917,12 @@ int launch_tune(const TuneArgs& t, const Plan& pl, int cus, int64_t n_chains,
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
   hipLaunchKernelGGL(k_tune<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, t);
   return launch_ok();
+}
+
+int record_mark(int i, hipStream_t stream) {
+  if (i < g_prof_n && g_prof[i] && hipEventRecord(g_prof[i], stream) != hipSuccess)
+    return OCTO_EHIP;
+  return OCTO_OK;
 }
 
 }  // namespace
@@ -902,7 +967,7 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   rc = prepare(prob, layer_costs, stream, n, &su);
   if (rc) return rc;
   char* base = static_cast<char*>(su.ws->base);
-  SimArgs a = make_args(prob, su.small, su, link, candidates, n, out_makespan, out_bubble);
+  SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
   const int tb = 256;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
@@ -911,22 +976,31 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
                      reinterpret_cast<int32_t*>(base + su.l.idx));
   if ((rc = launch_ok())) return rc;
-  // v <= 2 bins (the common case)
-  a.bin_lo = bin_of(2, GEN_MERGE, 1);
-  a.bin_hi = NBIN_GEN;
-  if ((rc = launch_sim<2>(a, su.small, su.di.cus, n, stream))) return rc;
-  if (prob->v_max >= 3) {
-    SimArgs b = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
-    b.bin_lo = 0;
-    b.bin_hi = bin_of(2, GEN_MERGE, 1);
-    if ((rc = launch_sim<8>(b, su.big, su.di.cus, n, stream))) return rc;
-  }
-  SimArgs m = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
+  // generated queues, one launch per v class with finish tables sized for it:
+  // v = 2, then v = 1, then v = 3..8; then materialised queues (perturbations, 64-bit redo).
+  const int P = prob->P;
+  const int b2 = bin_of(2, GEN_MERGE, 1), b1 = bin_of(1, GEN_MERGE, 1);
+  if ((rc = record_mark(0, stream))) return rc;
+  if (prob->v_max >= 2 &&
+      (rc = launch_sim<2>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P, b2, b1,
+                          CTL_WORK + 1, stream)))
+    return rc;
+  if ((rc = record_mark(1, stream))) return rc;
+  if ((rc = launch_sim<1>(prob, su, link, candidates, n, out_makespan, out_bubble, P, b1,
+                          NBIN_GEN, CTL_WORK + 0, stream)))
+    return rc;
+  if ((rc = record_mark(2, stream))) return rc;
+  if (prob->v_max >= 3 &&
+      (rc = launch_sim<8>(prob, su, link, candidates, n, out_makespan, out_bubble,
+                          P * prob->v_max, 0, b2, CTL_WORK + 2, stream)))
+    return rc;
+  if ((rc = record_mark(3, stream))) return rc;
   if (prob->v_max <= 2)
-    hipLaunchKernelGGL(k_sim_mat<2>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, m);
+    hipLaunchKernelGGL(k_sim_mat<2>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
   else
-    hipLaunchKernelGGL(k_sim_mat<8>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, m);
-  return launch_ok();
+    hipLaunchKernelGGL(k_sim_mat<8>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
+  if ((rc = launch_ok())) return rc;
+  return record_mark(4, stream);
 }
 
 int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
@@ -953,6 +1027,14 @@ int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const i
   t.step = step;
   return prob->v_max <= 2 ? launch_tune<2>(t, su.big, su.di.cus, n_chains, stream)
                           : launch_tune<8>(t, su.big, su.di.cus, n_chains, stream);
+}
+
+int octo_profile_events(void* const* events, int32_t n_events) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (n_events < 0 || n_events > 8 || (n_events > 0 && !events)) return OCTO_EINVAL;
+  for (int i = 0; i < 8; ++i) g_prof[i] = i < n_events ? static_cast<hipEvent_t>(events[i]) : nullptr;
+  g_prof_n = n_events;
+  return OCTO_OK;
 }
 
 const char* octo_strerror(int status) {

@@ -127,26 +127,27 @@ __device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint
 }
 
 // ------------------------------------------------------------------------------------------
-// Queue generators. Each lane owns one device queue and walks it front to back; a generator
-// exposes the current op (kind, chunk, m) and steps to the next one.
+// Queue generators. Each lane owns one device queue and walks it front to back. A generator
+// holds the current op in (kind, k, m) — kind, local chunk, micro-batch — and advance(ok) steps
+// to the next op when ok is true. The step is straight-line code (selects), so lanes that do
+// not advance cost no divergent branches.
 // ------------------------------------------------------------------------------------------
 
 // GPipe order: forwards by (chunk asc, m), then backwards by (chunk desc, m).
 struct GenAfab {
-  int v, M, ph, k, m;
-  __device__ __forceinline__ void init(int v_, int M_) { v = v_, M = M_, ph = 0, k = 0, m = 0; }
-  __device__ __forceinline__ int kind() const { return ph; }
-  __device__ __forceinline__ int chunk() const { return k; }
-  __device__ __forceinline__ int mb() const { return m; }
-  __device__ __forceinline__ void step() {
-    if (++m == M) {
-      m = 0;
-      if (ph == 0) {
-        if (++k == v) ph = 1, k = v - 1;
-      } else {
-        --k;
-      }
-    }
+  int v, M;
+  int kind, k, m;
+  __device__ __forceinline__ void init(int v_, int M_) { v = v_, M = M_, kind = KF, k = 0, m = 0; }
+  __device__ __forceinline__ void advance(bool ok) {
+    const int m1 = m + 1;
+    const bool wrap = m1 == M;
+    const bool isF = kind == KF;
+    const int kf = k + (wrap ? 1 : 0);
+    const bool flip = isF && kf == v;
+    const int kn = isF ? (flip ? v - 1 : kf) : k - (wrap ? 1 : 0);
+    m = ok ? (wrap ? 0 : m1) : m;
+    k = ok ? kn : k;
+    kind = ok ? ((isF && !flip) ? KF : KB) : kind;
   }
 };
 
@@ -154,31 +155,63 @@ struct GenAfab {
 // micro-batch c*P + a for forwards; backwards take chunk v-1-b. Warm-up w forwards, then
 // (F, B) pairs, then the remaining B; with a split backward each B's W follows `lag` B's later
 // (a FIFO of depth lag), flushed at the end. At v = 1 this is 1F1B.
+__device__ __forceinline__ int inter_warmup(int P, int v, int M, int r) {
+  return v == 1 ? min(P - 1 - r, M) : min(2 * (P - 1 - r) + (v - 1) * P, v * M);
+}
+__device__ __forceinline__ int inter_kind(int nF, int nB, int nW, int w, int N, int split,
+                                          int lag) {
+  const int fcap = min(N, w + nB + 1);
+  const int body = nF < fcap ? KF : KB;
+  const int k1 = nB < N ? body : KW;
+  const int k2 = (split && nW < nB - lag) ? KW : k1;
+  return nF < w ? KF : k2;
+}
+
+// Power-of-two P and v: the virtual index decomposes with shifts and masks.
+struct GenInterP2 {
+  int lgP, lgPv, Pm1, vm1, N, w, lag, split;
+  int nF, nB, nW;
+  int kind, k, m;
+  __device__ __forceinline__ void init(int P, int v, int M, int r, int split_, int lag_) {
+    lgP = __ffs(P) - 1;
+    lgPv = lgP + __ffs(v) - 1;
+    Pm1 = P - 1, vm1 = v - 1, N = v * M, split = split_, lag = lag_;
+    w = inter_warmup(P, v, M, r);
+    nF = nB = nW = 0;
+    update();
+  }
+  __device__ __forceinline__ void update() {
+    kind = inter_kind(nF, nB, nW, w, N, split, lag);
+    const int j = kind == KF ? nF : kind == KB ? nB : nW;
+    const int kx = (j >> lgP) & vm1;
+    m = ((j >> lgPv) << lgP) | (j & Pm1);
+    k = kind == KF ? kx : vm1 - kx;
+  }
+  __device__ __forceinline__ void advance(bool ok) {
+    nF += (ok && kind == KF) ? 1 : 0;
+    nB += (ok && kind == KB) ? 1 : 0;
+    nW += (ok && kind == KW) ? 1 : 0;
+    update();
+  }
+};
+
+// Any P and v: each stream keeps its virtual index decomposed as (a, b, c).
 struct GenInter {
   int P, v, N, w, lag, split;
   int nF, nB, nW;
   int fa, fb, fc, ba, bb, bc, wa, wb, wc;
-  int cur;  // kind of the current op
-
+  int kind, k, m;
   __device__ __forceinline__ void init(int P_, int v_, int M, int r, int split_, int lag_) {
     P = P_, v = v_, N = v_ * M, split = split_, lag = lag_;
-    w = v == 1 ? min(P - 1 - r, M) : min(2 * (P - 1 - r) + (v - 1) * P, N);
+    w = inter_warmup(P, v, M, r);
     nF = nB = nW = 0;
     fa = fb = fc = ba = bb = bc = wa = wb = wc = 0;
-    cur = next_kind();
+    update();
   }
-  __device__ __forceinline__ int next_kind() const {
-    if (nF < w) return KF;
-    if (split && nW < nB - lag) return KW;
-    if (nB < N) return nF < min(N, w + nB + 1) ? KF : KB;
-    return KW;
-  }
-  __device__ __forceinline__ int kind() const { return cur; }
-  __device__ __forceinline__ int chunk() const {
-    return cur == KF ? fb : cur == KB ? v - 1 - bb : v - 1 - wb;
-  }
-  __device__ __forceinline__ int mb() const {
-    return cur == KF ? fc * P + fa : cur == KB ? bc * P + ba : wc * P + wa;
+  __device__ __forceinline__ void update() {
+    kind = inter_kind(nF, nB, nW, w, N, split, lag);
+    k = kind == KF ? fb : kind == KB ? v - 1 - bb : v - 1 - wb;
+    m = kind == KF ? fc * P + fa : kind == KB ? bc * P + ba : wc * P + wa;
   }
   __device__ __forceinline__ static void inc(int& a, int& b, int& c, int P, int v) {
     if (++a == P) {
@@ -186,89 +219,106 @@ struct GenInter {
       if (++b == v) b = 0, ++c;
     }
   }
-  __device__ __forceinline__ void step() {
-    if (cur == KF) ++nF, inc(fa, fb, fc, P, v);
-    else if (cur == KB) ++nB, inc(ba, bb, bc, P, v);
-    else ++nW, inc(wa, wb, wc, P, v);
-    cur = next_kind();
+  __device__ __forceinline__ void advance(bool ok) {
+    if (ok) {
+      if (kind == KF) ++nF, inc(fa, fb, fc, P, v);
+      else if (kind == KB) ++nB, inc(ba, bb, bc, P, v);
+      else ++nW, inc(wa, wb, wc, P, v);
+    }
+    update();
   }
 };
 
 // MERGE: a device's stages each follow the ideal stage-level order of a shared table (rows of
 // `rowlen` entries, one row per stage); the device takes the entry with the smallest ideal
-// start, the lower stage on ties. Two entries per chunk are kept in registers so the table
-// load for a chunk is issued one step before it is needed.
+// start, the lower stage on ties. Each chunk keeps its head entry and the next one in
+// registers. The load for a chunk's following entry is issued when the chunk advances and
+// committed at the next advance, so its latency overlaps a whole round.
 template <int VMAX>
 struct GenMerge {
   const uint32_t* tab;
-  int rowlen, v;
+  int rowlen;
   int row[VMAX], pos[VMAX];
   uint32_t ent[VMAX], nxt[VMAX];
-  int sel;
-
-  __device__ __forceinline__ uint32_t fetch(int k, int p) const {
-    return p < rowlen ? tab[row[k] + p] : MERGE_END;
+  uint32_t px;  // load in flight for chunk pk (pk < 0: none)
+  int pk;
+  int kind, k, m;
+  __device__ __forceinline__ uint32_t fetch(int r, int p) const {
+    const uint32_t x = tab[r + min(p, rowlen - 1)];
+    return p < rowlen ? x : MERGE_END;
   }
   template <class StageOf>
-  __device__ __forceinline__ void init(const uint32_t* tab_, int rowlen_, int v_, StageOf stage_of) {
-    tab = tab_, rowlen = rowlen_, v = v_;
+  __device__ __forceinline__ void init(const uint32_t* tab_, int rowlen_, int v, StageOf stage_of) {
+    tab = tab_, rowlen = rowlen_;
 #pragma unroll
-    for (int k = 0; k < VMAX; ++k) {
-      row[k] = k < v ? stage_of(k) * rowlen : 0;
-      pos[k] = 0;
-      ent[k] = k < v ? fetch(k, 0) : MERGE_END;
-      nxt[k] = k < v ? fetch(k, 1) : MERGE_END;
+    for (int c = 0; c < VMAX; ++c) {
+      row[c] = c < v ? stage_of(c) * rowlen : 0;
+      pos[c] = 0;
+      ent[c] = c < v ? fetch(row[c], 0) : MERGE_END;
+      nxt[c] = c < v ? fetch(row[c], 1) : MERGE_END;
     }
-    pick();
+    px = MERGE_END, pk = -1;
+    update();
   }
-  __device__ __forceinline__ void pick() {
+  __device__ __forceinline__ void update() {
     uint32_t best = ent[0];
     int b = 0;
 #pragma unroll
-    for (int k = 1; k < VMAX; ++k)
-      if ((ent[k] >> 16) < (best >> 16)) best = ent[k], b = k;
-    sel = b;
+    for (int c = 1; c < VMAX; ++c) {
+      const bool lt = (ent[c] >> 16) < (best >> 16);
+      best = lt ? ent[c] : best;
+      b = lt ? c : b;
+    }
+    k = b;
+    kind = (best >> 12) & 3;
+    m = best == MERGE_END ? 0 : best & 0x7FF;
   }
-  __device__ __forceinline__ uint32_t cur_entry() const {
-    uint32_t e = ent[0];
+  __device__ __forceinline__ void advance(bool ok) {
 #pragma unroll
-    for (int k = 1; k < VMAX; ++k)
-      if (sel == k) e = ent[k];
-    return e;
-  }
-  __device__ __forceinline__ int kind() const { return (cur_entry() >> 12) & 3; }
-  __device__ __forceinline__ int chunk() const { return sel; }
-  __device__ __forceinline__ int mb() const { return cur_entry() & 0x7FF; }
-  __device__ __forceinline__ void step() {
+    for (int c = 0; c < VMAX; ++c) nxt[c] = pk == c ? px : nxt[c];
+    int r = row[0], p = pos[0];
 #pragma unroll
-    for (int k = 0; k < VMAX; ++k)
-      if (sel == k) {
-        pos[k] += 1;
-        ent[k] = nxt[k];
-        nxt[k] = fetch(k, pos[k] + 1);
-      }
-    pick();
+    for (int c = 1; c < VMAX; ++c) r = k == c ? row[c] : r, p = k == c ? pos[c] : p;
+    px = fetch(r, p + 2);
+    pk = ok ? k : -1;
+#pragma unroll
+    for (int c = 0; c < VMAX; ++c) {
+      const bool t = ok && k == c;
+      pos[c] += t ? 1 : 0;
+      ent[c] = t ? nxt[c] : ent[c];
+    }
+    update();
   }
 };
 
-// Materialised queue row in global memory (perturbed candidates, tuner chains). The next entry
-// is loaded one step ahead.
+// Materialised queue row in global memory (perturbed candidates, tuner chains). The entry after
+// next is loaded at each step and committed at the following step.
 struct GenMat {
   const uint16_t* rowp;
   int len, pos;
-  uint32_t cur, nxt;
+  uint32_t cur, nxt, px;
+  bool pv;
+  int kind, k, m;
+  __device__ __forceinline__ uint32_t fetch(int p) const { return rowp[min(p, max(len - 1, 0))]; }
   __device__ __forceinline__ void init(const uint16_t* r, int len_) {
     rowp = r, len = len_, pos = 0;
-    cur = len > 0 ? rowp[0] : 0;
-    nxt = len > 1 ? rowp[1] : 0;
+    cur = fetch(0);
+    nxt = fetch(1);
+    px = 0, pv = false;
+    update();
   }
-  __device__ __forceinline__ int kind() const { return (cur >> 14) & 3; }
-  __device__ __forceinline__ int chunk() const { return (cur >> 11) & 7; }
-  __device__ __forceinline__ int mb() const { return cur & 0x7FF; }
-  __device__ __forceinline__ void step() {
-    ++pos;
-    cur = nxt;
-    nxt = pos + 1 < len ? rowp[pos + 1] : 0;
+  __device__ __forceinline__ void update() {
+    kind = (cur >> 14) & 3;
+    k = (cur >> 11) & 7;
+    m = cur & 0x7FF;
+  }
+  __device__ __forceinline__ void advance(bool ok) {
+    nxt = pv ? px : nxt;
+    px = fetch(pos + 2);
+    pv = ok;
+    pos += ok ? 1 : 0;
+    cur = ok ? nxt : cur;
+    update();
   }
 };
 

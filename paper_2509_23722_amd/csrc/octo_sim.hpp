@@ -2,119 +2,140 @@
 // lanes per candidate, lane d = pipeline device d. Each candidate owns a finish table in LDS
 // with one slot per (stage, micro-batch).
 //
-// Slot encoding: empty = -2; after F(s,m) finishes the slot holds fin << 1; after B(s,m) it
-// holds fin << 1 | 1. A single slot suffices because B(s,m) can only finish after F(s+1,m)
-// (which consumed F(s,m)) has finished: B(s,m) needs B(s+1,m), which needs F(s+1,m). Row -1 is
-// all zeros (F of stage 0 is always ready at time 0).
+// Slot value = fin << 3 | state, state bits: 1 = B(s,m) finished, 2 = F(s,m) finished (kept
+// after B), 4 = stage-0 start token (row 0 starts as 4: "ready at time 0"); empty = 0. One slot
+// per (s,m) suffices because B(s,m) can only finish after F(s+1,m) (which consumed F(s,m)) has
+// finished: B(s,m) needs B(s+1,m), which needs F(s+1,m).
 //
-// Every op reads exactly one slot:
-//   F(s,m): row s-1, ready when finished (>= 0); in = fin + link weight of the stage boundary.
-//   B(s,m), s < S-1: row s+1, ready when it holds a B finish; in = fin + link weight.
-//   B(S-1,m): its own row, ready when F(S-1,m) finished (the loss turns the forward around).
-//   W(s,m): its own row, ready when B(s,m) finished.
+// Every op reads exactly one slot and needs one state bit there:
+//   F(0,m): its own slot, token;   F(s,m), s > 0: row s-1, bit 2; in = fin + link weight.
+//   B(s,m), s < S-1: row s+1, bit 1; in = fin + link weight.
+//   B(S-1,m): its own slot, bit 2 (the loss turns the forward around).
+//   W(s,m): its own slot, bit 1; W writes nothing.
 // Other dependencies are implied: F(s,m) -> B(s,m) for s < S-1 follows from F(s,m) ->
 // F(s+1,m) -> B(s+1,m) -> B(s,m). start = max(device clock, in); fin = start + duration
 // (§5: record start/end per node; §6 Eq. 1: makespan = latest finish).
 //
-// Rounds: every live lane tries its head op once per round; a round in which no lane of a
-// candidate advances while some still have ops is a deadlock (nothing can ever change again).
+// Rounds: every live lane tries its head op once per round; readiness is structural, so when
+// no lane of the wave advances in a round, every candidate that still has work is deadlocked.
+// The round body is straight-line code: generators and descriptors advance under a predicate.
 #pragma once
 
 #include "octo_device.hpp"
 
 namespace octo {
 
+constexpr uint32_t ST_B = 1, ST_F = 2, ST_TOKEN = 4;
+
+// 64-bit slots: one int64 per (stage, micro-batch).
+struct Table64 {
+  int64_t* T;
+  __device__ __forceinline__ uint64_t load(int i) const { return (uint64_t)T[i]; }
+  __device__ __forceinline__ void store(int i, uint64_t v) const { T[i] = (int64_t)v; }
+  __device__ __forceinline__ void clear(int n, int M, int d, int G) const {
+    for (int i = d; i < n; i += G) T[i] = i < M ? ST_TOKEN : 0;
+  }
+  __host__ __device__ static size_t bytes(int slots) { return (size_t)slots * 8; }
+};
+
+// 40-bit slots: a 32-bit low array and an 8-bit high array (fin < 2^37 ns; larger times are
+// detected and the candidate is recomputed with 64-bit slots).
+struct Table40 {
+  uint32_t* lo;
+  uint8_t* hi;
+  __device__ __forceinline__ uint64_t load(int i) const {
+    return (uint64_t)lo[i] | ((uint64_t)hi[i] << 32);
+  }
+  __device__ __forceinline__ void store(int i, uint64_t v) const {
+    lo[i] = (uint32_t)v;
+    hi[i] = (uint8_t)(v >> 32);
+  }
+  __device__ __forceinline__ void clear(int n, int M, int d, int G) const {
+    for (int i = d; i < n; i += G) lo[i] = i < M ? ST_TOKEN : 0;
+    uint32_t* h = reinterpret_cast<uint32_t*>(hi);
+    for (int i = d; i < (n + 3) / 4; i += G) h[i] = 0;
+  }
+  __host__ __device__ static size_t bytes(int slots) { return (size_t)slots * 5; }
+  static constexpr int64_t LIMIT = (int64_t)1 << 37;
+};
+
 template <int VMAX>
 struct Chunks {
-  int st[VMAX];                                        // stage of chunk k
+  int st[VMAX];                      // stage of chunk k
+  int base[VMAX];                    // slot index of the stage's own row: s M
+  int foff[VMAX], fneed[VMAX];       // F read offset / needed state bit index
+  int boff[VMAX], bneed[VMAX];       // B read offset / needed state bit index
   int64_t dF[VMAX], dB[VMAX], dW[VMAX], wF[VMAX], wB[VMAX];
 };
 
 struct Lane {
   int64_t clock;
   int pos, nops;
-  bool live;
-  // current op
-  int rd, wr, tag, needB;
+  int rd, wr, need, store;
+  uint32_t state;  // state bits written on finish
   int64_t w, dur;
-  int s, kind, m;  // for recording ideal starts
 };
 
 template <int VMAX, typename T>
 __device__ __forceinline__ T pick(const T (&a)[VMAX], int k) {
   T x = a[0];
 #pragma unroll
-  for (int i = 1; i < VMAX; ++i)
-    if (k == i) x = a[i];
+  for (int i = 1; i < VMAX; ++i) x = k == i ? a[i] : x;
   return x;
 }
 
-// Describe op (kind, chunk k, micro-batch m) for the slot layout index(row r, m) = (r+1)*M + m.
+// Describe op (kind, chunk k, micro-batch m); slot index of (row r, m) = r M + m.
 template <int VMAX>
-__device__ __forceinline__ void describe(Lane& L, const Chunks<VMAX>& c, int kind, int k, int m, int M,
-                                int S, int sink) {
-  const int s = pick<VMAX>(c.st, k);
-  const int own = (s + 1) * M + m;
-  L.s = s, L.kind = kind, L.m = m;
-  if (kind == KF) {
-    L.rd = own - M;
-    L.wr = own;
-    L.needB = 0;
-    L.tag = 0;
-    L.w = pick<VMAX>(c.wF, k);
-    L.dur = pick<VMAX>(c.dF, k);
-  } else if (kind == KB) {
-    const bool last = s == S - 1;
-    L.rd = last ? own : own + M;
-    L.wr = own;
-    L.needB = last ? 0 : 1;
-    L.tag = 1;
-    L.w = last ? 0 : pick<VMAX>(c.wB, k);
-    L.dur = pick<VMAX>(c.dB, k);
-  } else {
-    L.rd = own;
-    L.wr = sink;
-    L.needB = 1;
-    L.tag = 0;
-    L.w = 0;
-    L.dur = pick<VMAX>(c.dW, k);
-  }
+__device__ __forceinline__ void describe(Lane& L, const Chunks<VMAX>& c, int kind, int k, int m) {
+  const bool isF = kind == KF, isB = kind == KB;
+  const int own = pick<VMAX>(c.base, k) + m;
+  const int fo = pick<VMAX>(c.foff, k), bo = pick<VMAX>(c.boff, k);
+  const int fn = pick<VMAX>(c.fneed, k), bn = pick<VMAX>(c.bneed, k);
+  L.rd = own + (isF ? fo : isB ? bo : 0);
+  L.wr = own;
+  L.store = isF || isB;
+  L.need = isF ? fn : isB ? bn : 0;
+  L.state = isF ? ST_F : (ST_F | ST_B);
+  const int64_t wf = pick<VMAX>(c.wF, k), wb = pick<VMAX>(c.wB, k);
+  const int64_t df = pick<VMAX>(c.dF, k), db = pick<VMAX>(c.dB, k), dw = pick<VMAX>(c.dW, k);
+  L.w = isF ? wf : isB ? wb : 0;
+  L.dur = isF ? df : isB ? db : dw;
+}
+
+// Fold every G-lane group of a 64-bit lane mask into the group's lowest bit.
+__device__ __forceinline__ uint64_t fold_groups(uint64_t x, int G, uint64_t lsb) {
+  for (int sh = 1; sh < G; sh <<= 1) x |= x >> sh;
+  return x & lsb;
 }
 
 // Run the rounds until every candidate of the wave is done or deadlocked.
-// gmask: the lanes of this lane's candidate. rec (nullable): ideal-start recording for the
-// MERGE table, rec[pos] = start << 16 | kind << 12 | m.
-template <int VMAX, class Gen>
-__device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, Lane& L, int64_t* T, int M, int S,
-                             int sink, uint64_t gmask, bool& dead, uint32_t* rec) {
+// gbit: this lane's group bit in folded masks; lsb: all group bits. rec (nullable): ideal-start
+// recording for the MERGE table, rec[pos] = start << 16 | kind << 12 | m.
+template <int VMAX, class Tab, class Gen>
+__device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, Lane& L, const Tab& T,
+                                      int G, uint64_t gbit, uint64_t lsb, bool& dead,
+                                      uint32_t* rec) {
+  bool live = L.pos < L.nops;
   for (;;) {
-    int adv = 0;
-    if (L.live) {
-      const int64_t p = T[L.rd];
-      const bool ok = L.needB ? ((p & 1) != 0) : (p >= 0);
-      if (ok) {
-        const int64_t tin = (p >> 1) + L.w;
-        const int64_t st = tin > L.clock ? tin : L.clock;
-        L.clock = st + L.dur;
-        T[L.wr] = (L.clock << 1) | L.tag;
-        if (rec) rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)L.kind << 12) | (uint32_t)L.m;
-        adv = 1;
-        if (++L.pos < L.nops) {
-          gen.step();
-          describe<VMAX>(L, c, gen.kind(), gen.chunk(), gen.mb(), M, S, sink);
-        } else {
-          L.live = false;
-        }
-      }
-    }
+    const uint64_t p = T.load(live ? L.rd : 0);
+    const bool ok = live && (((uint32_t)p >> L.need) & 1u) != 0;
+    const int64_t tin = (int64_t)(p >> 3) + L.w;
+    const int64_t st = tin > L.clock ? tin : L.clock;
+    const int64_t fin = st + L.dur;
+    if (ok && L.store) T.store(L.wr, ((uint64_t)fin << 3) | L.state);
+    if (rec && ok)
+      rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)gen.kind << 12) | (uint32_t)gen.m;
+    L.clock = ok ? fin : L.clock;
+    L.pos += ok ? 1 : 0;
+    live = L.pos < L.nops;
+    gen.advance(ok);
+    describe<VMAX>(L, c, gen.kind, gen.k, gen.m);
     __asm__ volatile("" ::: "memory");
-    const uint64_t advm = __ballot(adv);
-    const uint64_t actm = __ballot(L.live);
-    if ((actm & gmask) != 0 && (advm & gmask) == 0) {
-      dead = true;
-      L.live = false;
+    if (__ballot(ok) == 0) {
+      const uint64_t actm = __ballot(live);
+      if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
+      break;
     }
-    if (__ballot(L.live) == 0) break;
   }
 }
 

@@ -164,6 +164,22 @@ def test_edge_cases(gpu):
         assert_same(*g, *r, f"edge {c}")
 
 
+def test_times_beyond_40bit_slots(gpu):
+    """Layer costs so large that finish times pass 2^37 ns: those candidates are recomputed with
+    64-bit finish tables and must still match the oracle exactly; small ones stay fast."""
+    rng = np.random.default_rng(21)
+    P, v_max, M, L = 4, 2, 8, 12
+    log("huge costs P=4 v_max=2 M=8")
+    costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+    costs[5] = [40_000_000_000, 30_000_000_000, 20_000_000_000]  # ~ 2^35 per op of that layer
+    link = I.link_matrix(P, 1000)
+    recs = I.random_candidates(rng, L, P, v_max, M, 400, max_pert=1, pert_rate=0.1)
+    g = run_gpu(gpu, L, P, v_max, M, 1, costs, link, recs)
+    r = run_oracle(L, P, v_max, M, 1, costs, link, recs)
+    assert_same(*g, *r, "huge costs")
+    assert (r[0] >= 2 ** 37).sum() > 50
+
+
 def test_repeatable_and_stream_independent(gpu):
     import torch
     w = I.WORKLOADS[2]
