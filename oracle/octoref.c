@@ -705,6 +705,7 @@ typedef struct {
   int64_t* out_bub;
   int64_t* out_acc;
   int32_t* out_queues; /* nullable: [chain][P][qcap] packed kind<<14 | chunk<<11 | m */
+  const int64_t* ids;  /* nullable: chain index of each record (Philox counter); default i */
 } tune_job;
 
 static int64_t eff(int64_t ms) { return ms < 0 ? INT64_MAX : ms; }
@@ -735,7 +736,8 @@ static void tune_chain(tune_job* j, int64_t ci) {
   }
   int S = c->S;
   for (int t = 1; t <= j->n_steps; ++t) {
-    uint64_t ctr[4] = {(uint64_t)ci, (uint64_t)t, 0, 0}, key[2] = {j->seed, 0}, u[4];
+    const uint64_t chain_id = j->ids ? (uint64_t)j->ids[ci] : (uint64_t)ci;
+    uint64_t ctr[4] = {chain_id, (uint64_t)t, 0, 0}, key[2] = {j->seed, 0}, u[4];
     oracle_philox4x64_10(ctr, key, u);
     int kind = (int)(u[0] % 3);
     int ok = 0;
@@ -792,11 +794,13 @@ static void tune_chain(tune_job* j, int64_t ci) {
   for (int d = 0; d < P; ++d) bub[d] = cur_bub[d];
   write_record(pr, c, rec);
   if (j->out_queues) {
-    int32_t* oq = j->out_queues + (size_t)ci * P * qcap;
+    /* output rows have the queue store's capacity 3 * v_max * M, whatever this chain's v */
+    const int ocap = 3 * pr->v_max * pr->M;
+    int32_t* oq = j->out_queues + (size_t)ci * P * ocap;
     for (int d = 0; d < P; ++d)
-      for (int i = 0; i < qcap; ++i) {
+      for (int i = 0; i < ocap; ++i) {
         ref_op o = i < qlen[d] ? q[(size_t)d * qcap + i] : (ref_op){0, 0, 0};
-        oq[d * qcap + i] = i < qlen[d] ? ((o.kind << 14) | (o.chunk << 11) | o.m) : 0;
+        oq[d * ocap + i] = i < qlen[d] ? ((o.kind << 14) | (o.chunk << 11) | o.m) : 0;
       }
   }
   free(q);
@@ -809,12 +813,14 @@ static void* tune_worker(void* arg) {
   return NULL;
 }
 
-/* Run steps 0..n_steps of the local search for chains [0, n). recs (in/out) holds the chain
- * candidate records (updated to the final state). Outputs per chain: final makespan, bubbles,
- * accepted-move count, and optionally the final queues (qcap = 3*v_max*M entries per device). */
+/* Run steps 0..n_steps of the local search for n chains. recs (in/out) holds the chain
+ * candidate records (updated to the final state); chain_ids (nullable) gives each record's chain
+ * index for the Philox counter (default: its position). Outputs per chain: final makespan,
+ * bubbles, accepted-move count, and optionally the final queues (qcap = 3*v_max*M entries per
+ * device). */
 int oracle_tune(const ref_problem* pr, const int64_t* costs, const int64_t* link, uint8_t* recs,
                 int64_t n, uint64_t seed, int32_t n_steps, int64_t* out_ms, int64_t* out_bub,
-                int64_t* out_acc, int32_t* out_queues, int nthreads) {
+                int64_t* out_acc, int32_t* out_queues, const int64_t* chain_ids, int nthreads) {
   if (!check_problem(pr) || n < 0 || n_steps < 0) return REF_EINVAL;
   if (nthreads < 1) nthreads = 1;
   if (nthreads > 256) nthreads = 256;
@@ -823,7 +829,7 @@ int oracle_tune(const ref_problem* pr, const int64_t* costs, const int64_t* link
   tune_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
     jobs[t] = (tune_job){pr, costs, link, recs, n * t / nthreads, n * (t + 1) / nthreads,
-                         seed, n_steps, out_ms, out_bub, out_acc, out_queues};
+                         seed, n_steps, out_ms, out_bub, out_acc, out_queues, chain_ids};
     if (nthreads == 1) tune_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, tune_worker, &jobs[t]);
   }

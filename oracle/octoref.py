@@ -41,7 +41,7 @@ def lib():
         L.oracle_philox4x64_10.argtypes = [p, p, p]
         L.oracle_philox4x64_10.restype = None
         L.oracle_tune.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64,
-                                  ctypes.c_uint64, ctypes.c_int32, p, p, p, p, ctypes.c_int]
+                                  ctypes.c_uint64, ctypes.c_int32, p, p, p, p, p, ctypes.c_int]
         L.oracle_tune.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -132,11 +132,13 @@ def philox4x64_10(counter, key):
     return [int(x) for x in out]
 
 
-def tune(prob, costs, link, recs, seed, n_steps, nthreads=1, want_queues=False):
-    """Run the local search (steps 0..n_steps) on every chain record.
+def tune(prob, costs, link, recs, seed, n_steps, nthreads=1, want_queues=False, chain_ids=None):
+    """Run the local search (steps 0..n_steps) on every chain record (chain index = position,
+    or chain_ids[i]).
 
     Returns (final_records, makespan[n], bubble[n, P], accepted[n], queues or None)."""
     recs = np.array(recs, dtype=np.uint8, copy=True, order="C")
+    ids = None if chain_ids is None else np.ascontiguousarray(chain_ids, dtype=np.int64)
     n = recs.shape[0]
     costs = np.ascontiguousarray(costs, dtype=np.int64)
     link = np.ascontiguousarray(link, dtype=np.int64)
@@ -147,7 +149,14 @@ def tune(prob, costs, link, recs, seed, n_steps, nthreads=1, want_queues=False):
     queues = np.zeros((n, prob.P, qcap), dtype=np.int32) if want_queues else None
     rc = lib().oracle_tune(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(recs), n,
                            ctypes.c_uint64(seed), int(n_steps), _ptr(ms), _ptr(bub), _ptr(acc),
-                           _ptr(queues), int(nthreads))
+                           _ptr(queues), _ptr(ids), int(nthreads))
     if rc != 0:
         raise ValueError(f"oracle_tune rejected the arguments (rc={rc})")
     return recs, ms, bub, acc, queues
+
+
+def tune_chains(prob, costs, link, all_recs, chain_ids, seed, n_steps, nthreads=1):
+    """Replay only the chains chain_ids of a larger set; returns (records, ms, bub, acc)."""
+    recs, ms, bub, acc, _ = tune(prob, costs, link, np.asarray(all_recs)[chain_ids], seed,
+                                 n_steps, nthreads=nthreads, chain_ids=chain_ids)
+    return recs, ms, bub, acc

@@ -55,6 +55,7 @@ struct SimArgs {
   int table_bytes;       // LDS bytes of one finish table
   int group_bytes;       // LDS bytes per candidate
   int rec_bytes;         // staged record bytes (header + boundaries + placement)
+  int rec_stride;        // bytes between staged records of a wave
   int qcap;
   int bin_lo, bin_hi;    // generated bins handled by this launch
   int work;              // chunk counter index of this launch
@@ -138,20 +139,18 @@ __device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, i
     reinterpret_cast<uint32_t*>(dst)[i] = reinterpret_cast<const uint32_t*>(src)[i];
 }
 
-__device__ __forceinline__ Table40 table40(uint8_t* g, int slots) {
-  return Table40{reinterpret_cast<uint32_t*>(g), g + (size_t)slots * 4};
-}
-
-// Simulate one candidate per group of the wave with generator kind GEN (40-bit slots; the
-// staged record shares the table's memory until the table is cleared), write the results.
-// cand < 0: this group has no candidate. P2: P and v are powers of two.
+// Simulate one candidate per group of the wave with generator kind GEN (40-bit slots shared by
+// the wave's groups; each group's staged record sits in that memory until it is cleared), write
+// the results. cand < 0: this group has no candidate. P2: P and v are powers of two.
 template <int VMAX, int GEN, bool P2>
 __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split,
-                                              uint8_t* lds_group) {
+                                              uint8_t* lds_wave) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
   const int d = lane_id() % G;
-  const Table40 T = table40(lds_group, a.slots);
-  uint8_t* rec = lds_group;
+  const Table40 T{reinterpret_cast<uint32_t*>(lds_wave),
+                  lds_wave + (size_t)a.slots * a.CPW * 4, a.CPW, g < a.CPW ? g : 0};
+  uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
   const bool has = cand >= 0;
   const int S = P * v;
   if (has) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
@@ -171,7 +170,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     zero_chunks<VMAX>(c);
   }
   __asm__ volatile("" ::: "memory");
-  if (has) T.clear(S * M, M, d, G);
+  T.clear_all(S * M, M, lane_id(), WAVE);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
@@ -342,12 +341,12 @@ __device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, int lo,
 
 template <int VMAX>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
-                                             int split, uint8_t* lds_group) {
+                                             int split, uint8_t* lds_wave) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
-  if (gen == GEN_AFAB) run_generated<VMAX, GEN_AFAB, false>(a, cand, v, split, lds_group);
-  else if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_group);
-  else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_group);
-  else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_group);
+  if (gen == GEN_AFAB) run_generated<VMAX, GEN_AFAB, false>(a, cand, v, split, lds_wave);
+  else if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_wave);
+  else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_wave);
+  else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_wave);
 }
 
 // Generated-queue simulation for the bins of one v class: VC = 1 (v = 1), 2 (v = 2) or 8
@@ -356,7 +355,6 @@ template <int VC>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int g = lane_id() / a.G;
-  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
   for (;;) {
     int ch = 0;
     if (lane_id() == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -369,7 +367,7 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     const int cnt = a.ctl[CTL_COUNTS + bin];
     const int e = entry0 + g;
     const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
-    dispatch_gen<VC>(a, gen, cand, v, split, lds_group);
+    dispatch_gen<VC>(a, gen, cand, v, split, smem);
   }
 }
 
@@ -653,9 +651,11 @@ using namespace octo;
 namespace {
 
 struct Workspace {
-  void* base = nullptr;
+  void* base = nullptr;  // per-call scratch (control words, prefix sums, bins, queues)
   size_t bytes = 0;
-  // cached MERGE tables
+  // MERGE tables: their own allocation, kept between calls for the same (P, v_max, M)
+  void* mt = nullptr;
+  size_t mt_bytes = 0;
   bool mt_valid = false;
   int mt_P = 0, mt_vmax = 0, mt_M = 0;
 };
@@ -703,7 +703,7 @@ int dev_info(int dev, DevInfo* out) {
 }
 
 struct Plan {
-  int G, CPW, slots, table_bytes, rec_bytes, group_bytes, lds_bytes, qcap;
+  int G, CPW, slots, table_bytes, rec_bytes, rec_stride, group_bytes, lds_bytes, qcap;
 };
 
 int lanes_per_candidate(int P) {
@@ -719,8 +719,9 @@ Plan fast_plan(const octo_problem* p, int lds_max, int s_cap) {
   pl.G = lanes_per_candidate(p->P);
   pl.slots = s_cap * p->M;
   pl.rec_bytes = pert_off(p->P * p->v_max);
-  pl.table_bytes = (int)(pl.slots * 4 + align_up(pl.slots, 4));
-  pl.group_bytes = (int)align_up(std::max<size_t>(pl.table_bytes, align_up(pl.rec_bytes, 4)), 16);
+  pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
+  pl.table_bytes = (int)(pl.slots * 4 + pl.slots);
+  pl.group_bytes = (int)align_up(std::max<size_t>(pl.table_bytes, pl.rec_stride), 16);
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
   pl.lds_bytes = pl.CPW * pl.group_bytes;
   pl.qcap = 3 * p->v_max * p->M;
@@ -733,6 +734,7 @@ Plan big_plan(const octo_problem* p, int lds_max) {
   pl.G = lanes_per_candidate(p->P);
   pl.slots = p->P * p->v_max * p->M;
   pl.rec_bytes = pert_off(p->P * p->v_max);
+  pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
   pl.table_bytes = (int)align_up((size_t)pl.slots * 8, 16);
   pl.group_bytes = pl.table_bytes + (int)align_up(pl.rec_bytes, 16);
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
@@ -747,7 +749,7 @@ size_t mtab_entries(const octo_problem* p) {
 
 // Workspace layout (byte offsets).
 struct Layout {
-  size_t ctl, pre, mtab, bin_of, idx, redo, qscr, total;
+  size_t ctl, pre, bin_of, idx, redo, qscr, total;
 };
 
 Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slots) {
@@ -757,8 +759,6 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   o = align_up(o + CTL_WORDS * 4, 256);
   l.pre = o;
   o = align_up(o + (size_t)(p->L + 1) * 3 * 8, 256);
-  l.mtab = o;
-  o = align_up(o + mtab_entries(p) * 4, 256);
   l.bin_of = o;
   o = align_up(o + (size_t)n, 256);
   l.idx = o;
@@ -771,25 +771,25 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   return l;
 }
 
-int ensure(Workspace& ws, size_t bytes, hipStream_t stream) {
-  if (ws.bytes >= bytes) return OCTO_OK;
-  if (ws.base) {
+// Grow-only device buffer; the old one is freed after the stream's pending work.
+int ensure_buf(void*& ptr, size_t& have, size_t bytes, hipStream_t stream) {
+  if (have >= bytes) return OCTO_OK;
+  if (ptr) {
     if (hipStreamSynchronize(stream) != hipSuccess) return OCTO_EHIP;
-    (void)hipFree(ws.base);
-    ws.base = nullptr;
-    ws.bytes = 0;
-    ws.mt_valid = false;
+    (void)hipFree(ptr);
+    ptr = nullptr;
+    have = 0;
   }
-  size_t want = std::max(bytes, ws.bytes * 3 / 2);
-  if (hipMalloc(&ws.base, want) != hipSuccess) {
-    ws.base = nullptr;
-    if (hipMalloc(&ws.base, bytes) != hipSuccess) {
-      ws.base = nullptr;
+  size_t want = std::max(bytes, have * 3 / 2);
+  if (hipMalloc(&ptr, want) != hipSuccess) {
+    ptr = nullptr;
+    if (hipMalloc(&ptr, bytes) != hipSuccess) {
+      ptr = nullptr;
       return OCTO_ENOMEM;
     }
     want = bytes;
   }
-  ws.bytes = want;
+  have = want;
   return OCTO_OK;
 }
 
@@ -835,7 +835,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
   if (rc) return rc;
   su->l = layout(prob, su->big, n, (int64_t)su->mat_grid * su->big.CPW);
   Workspace& ws = g_ws[std::make_pair(dev, stream)];
-  rc = ensure(ws, su->l.total, stream);
+  rc = ensure_buf(ws.base, ws.bytes, su->l.total, stream);
   if (rc) return rc;
   su->ws = &ws;
   char* base = static_cast<char*>(ws.base);
@@ -843,6 +843,12 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
                      reinterpret_cast<int64_t*>(base + su->l.pre),
                      reinterpret_cast<int32_t*>(base + su->l.ctl));
   if ((rc = launch_ok())) return rc;
+  if (prob->v_max >= 2) {
+    void* old = ws.mt;
+    rc = ensure_buf(ws.mt, ws.mt_bytes, std::max<size_t>(mtab_entries(prob) * 4, 256), stream);
+    if (rc) return rc;
+    if (ws.mt != old) ws.mt_valid = false;
+  }
   if (prob->v_max >= 2 && !(ws.mt_valid && ws.mt_P == prob->P && ws.mt_vmax == prob->v_max &&
                             ws.mt_M == prob->M)) {
     const int lds = (int)align_up((size_t)prob->P * prob->v_max * prob->M * 8, 16);
@@ -850,7 +856,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_merge_tab),
                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     hipLaunchKernelGGL(k_merge_tab, dim3(2 * (prob->v_max - 1)), dim3(WAVE), lds, stream, prob->P,
-                       prob->M, 2, prob->v_max, reinterpret_cast<uint32_t*>(base + su->l.mtab));
+                       prob->M, 2, prob->v_max, static_cast<uint32_t*>(ws.mt));
     if ((rc = launch_ok())) return rc;
     ws.mt_valid = true;
     ws.mt_P = prob->P, ws.mt_vmax = prob->v_max, ws.mt_M = prob->M;
@@ -874,7 +880,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
   a.idx = reinterpret_cast<const int32_t*>(base + l.idx);
   a.redo = reinterpret_cast<int32_t*>(base + l.redo);
-  a.mtab = reinterpret_cast<const uint32_t*>(base + l.mtab);
+  a.mtab = static_cast<const uint32_t*>(su.ws->mt);
   a.qscratch = reinterpret_cast<uint16_t*>(base + l.qscr);
   a.G = pl.G;
   a.CPW = pl.CPW;
@@ -882,6 +888,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.table_bytes = pl.table_bytes;
   a.group_bytes = pl.group_bytes;
   a.rec_bytes = pl.rec_bytes;
+  a.rec_stride = pl.rec_stride;
   a.qcap = pl.qcap;
   a.bin_lo = 0;
   a.bin_hi = NBIN_GEN;

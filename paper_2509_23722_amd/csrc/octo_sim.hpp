@@ -39,23 +39,29 @@ struct Table64 {
 };
 
 // 40-bit slots: a 32-bit low array and an 8-bit high array (fin < 2^37 ns; larger times are
-// detected and the candidate is recomputed with 64-bit slots).
+// detected and the candidate is recomputed with 64-bit slots). The CPW candidates of a wave
+// share the arrays interleaved — slot i of group g lives at i * cpw + g — so that groups
+// running the same op pattern in lockstep touch consecutive LDS banks.
 struct Table40 {
   uint32_t* lo;
   uint8_t* hi;
+  int cpw, g;
   __device__ __forceinline__ uint64_t load(int i) const {
-    return (uint64_t)lo[i] | ((uint64_t)hi[i] << 32);
+    const int j = i * cpw + g;
+    return (uint64_t)lo[j] | ((uint64_t)hi[j] << 32);
   }
   __device__ __forceinline__ void store(int i, uint64_t v) const {
-    lo[i] = (uint32_t)v;
-    hi[i] = (uint8_t)(v >> 32);
+    const int j = i * cpw + g;
+    lo[j] = (uint32_t)v;
+    hi[j] = (uint8_t)(v >> 32);
   }
-  __device__ __forceinline__ void clear(int n, int M, int d, int G) const {
-    for (int i = d; i < n; i += G) lo[i] = i < M ? ST_TOKEN : 0;
+  // Clear n slots of every group (all lanes of the wave together): row 0 holds the start token.
+  __device__ __forceinline__ void clear_all(int n, int M, int lane, int nlanes) const {
+    const int tot = n * cpw, tok = M * cpw;
+    for (int j = lane; j < tot; j += nlanes) lo[j] = j < tok ? ST_TOKEN : 0;
     uint32_t* h = reinterpret_cast<uint32_t*>(hi);
-    for (int i = d; i < (n + 3) / 4; i += G) h[i] = 0;
+    for (int j = lane; j < (tot + 3) / 4; j += nlanes) h[j] = 0;
   }
-  __host__ __device__ static size_t bytes(int slots) { return (size_t)slots * 5; }
   static constexpr int64_t LIMIT = (int64_t)1 << 37;
 };
 

@@ -180,6 +180,21 @@ def test_times_beyond_40bit_slots(gpu):
     assert (r[0] >= 2 ** 37).sum() > 50
 
 
+def test_interleaved_problems_keep_results(gpu):
+    """Calls on one stream alternate between problems of different sizes (and v_max, so the
+    library's cached MERGE tables must survive calls that do not use them)."""
+    rng = np.random.default_rng(31)
+    cases = [(4, 2, 8, 12), (8, 1, 32, 40), (4, 2, 8, 30), (6, 2, 6, 20), (4, 2, 8, 16)]
+    for P, v_max, M, L in cases * 2:
+        log(f"interleaved P={P} v_max={v_max} M={M} L={L}")
+        costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+        link = I.link_matrix(P, 300_000)
+        recs = I.random_candidates(rng, L, P, v_max, M, 2000 if v_max == 1 else 300)
+        g = run_gpu(gpu, L, P, v_max, M, 0, costs, link, recs)
+        r = run_oracle(L, P, v_max, M, 0, costs, link, recs)
+        assert_same(*g, *r, f"interleaved P={P} v_max={v_max} M={M} L={L}")
+
+
 def test_repeatable_and_stream_independent(gpu):
     import torch
     w = I.WORKLOADS[2]
