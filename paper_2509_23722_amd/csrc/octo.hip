@@ -149,7 +149,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   const int g = lane_id() / G;
   const int d = lane_id() % G;
   const Table40 T{reinterpret_cast<uint32_t*>(lds_wave),
-                  lds_wave + (size_t)a.slots * a.CPW * 4, a.CPW, g < a.CPW ? g : 0};
+                  lds_wave + (size_t)a.slots * a.CPW * 4, __ffs(a.CPW) - 1, g < a.CPW ? g : 0};
   uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
   const bool has = cand >= 0;
   const int S = P * v;
@@ -723,6 +723,7 @@ Plan fast_plan(const octo_problem* p, int lds_max, int s_cap) {
   pl.table_bytes = (int)(pl.slots * 4 + pl.slots);
   pl.group_bytes = (int)align_up(std::max<size_t>(pl.table_bytes, pl.rec_stride), 16);
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
+  while (pl.CPW & (pl.CPW - 1)) pl.CPW &= pl.CPW - 1;  // interleaving uses shifts
   pl.lds_bytes = pl.CPW * pl.group_bytes;
   pl.qcap = 3 * p->v_max * p->M;
   return pl;

@@ -149,6 +149,9 @@ struct GenAfab {
     k = ok ? kn : k;
     kind = ok ? ((isF && !flip) ? KF : KB) : kind;
   }
+  __device__ __forceinline__ void take_if(bool t, const GenAfab& o) {
+    kind = t ? o.kind : kind, k = t ? o.k : k, m = t ? o.m : m;
+  }
 };
 
 // Interleaved 1F1B (Narayanan et al.): virtual index j = c*P*v + b*P + a maps to chunk b and
@@ -193,6 +196,10 @@ struct GenInterP2 {
     nW += (ok && kind == KW) ? 1 : 0;
     update();
   }
+  __device__ __forceinline__ void take_if(bool t, const GenInterP2& o) {
+    nF = t ? o.nF : nF, nB = t ? o.nB : nB, nW = t ? o.nW : nW;
+    kind = t ? o.kind : kind, k = t ? o.k : k, m = t ? o.m : m;
+  }
 };
 
 // Any P and v: each stream keeps its virtual index decomposed as (a, b, c).
@@ -226,6 +233,9 @@ struct GenInter {
       else ++nW, inc(wa, wb, wc, P, v);
     }
     update();
+  }
+  __device__ __forceinline__ void take_if(bool t, const GenInter& o) {
+    if (t) *this = o;
   }
 };
 
@@ -289,6 +299,16 @@ struct GenMerge {
     }
     update();
   }
+  __device__ __forceinline__ void take_if(bool t, const GenMerge& o) {
+#pragma unroll
+    for (int c = 0; c < VMAX; ++c) {
+      pos[c] = t ? o.pos[c] : pos[c];
+      ent[c] = t ? o.ent[c] : ent[c];
+      nxt[c] = t ? o.nxt[c] : nxt[c];
+    }
+    px = t ? o.px : px, pk = t ? o.pk : pk;
+    kind = t ? o.kind : kind, k = t ? o.k : k, m = t ? o.m : m;
+  }
 };
 
 // Materialised queue row in global memory (perturbed candidates, tuner chains). The entry after
@@ -319,6 +339,11 @@ struct GenMat {
     pos += ok ? 1 : 0;
     cur = ok ? nxt : cur;
     update();
+  }
+  __device__ __forceinline__ void take_if(bool t, const GenMat& o) {
+    pos = t ? o.pos : pos, cur = t ? o.cur : cur, nxt = t ? o.nxt : nxt;
+    px = t ? o.px : px, pv = t ? o.pv : pv;
+    kind = t ? o.kind : kind, k = t ? o.k : k, m = t ? o.m : m;
   }
 };
 

@@ -30,6 +30,11 @@ constexpr uint32_t ST_B = 1, ST_F = 2, ST_TOKEN = 4;
 // 64-bit slots: one int64 per (stage, micro-batch).
 struct Table64 {
   int64_t* T;
+  __device__ __forceinline__ void issue(int i, uint32_t& l, uint32_t& h) const {
+    const uint64_t x = (uint64_t)T[i];
+    l = (uint32_t)x;
+    h = (uint32_t)(x >> 32);
+  }
   __device__ __forceinline__ uint64_t load(int i) const { return (uint64_t)T[i]; }
   __device__ __forceinline__ void store(int i, uint64_t v) const { T[i] = (int64_t)v; }
   __device__ __forceinline__ void clear(int n, int M, int d, int G) const {
@@ -40,24 +45,30 @@ struct Table64 {
 
 // 40-bit slots: a 32-bit low array and an 8-bit high array (fin < 2^37 ns; larger times are
 // detected and the candidate is recomputed with 64-bit slots). The CPW candidates of a wave
-// share the arrays interleaved — slot i of group g lives at i * cpw + g — so that groups
-// running the same op pattern in lockstep touch consecutive LDS banks.
+// (a power of two, 2^lg) share the arrays interleaved — slot i of group g lives at
+// i * CPW + g — so that groups running the same op pattern in lockstep touch consecutive banks.
 struct Table40 {
   uint32_t* lo;
   uint8_t* hi;
-  int cpw, g;
+  int lg, g;
+  __device__ __forceinline__ void issue(int i, uint32_t& l, uint32_t& h) const {
+    const int j = (i << lg) | g;
+    l = lo[j];
+    h = hi[j];
+  }
   __device__ __forceinline__ uint64_t load(int i) const {
-    const int j = i * cpw + g;
-    return (uint64_t)lo[j] | ((uint64_t)hi[j] << 32);
+    uint32_t l, h;
+    issue(i, l, h);
+    return (uint64_t)l | ((uint64_t)h << 32);
   }
   __device__ __forceinline__ void store(int i, uint64_t v) const {
-    const int j = i * cpw + g;
+    const int j = (i << lg) | g;
     lo[j] = (uint32_t)v;
     hi[j] = (uint8_t)(v >> 32);
   }
   // Clear n slots of every group (all lanes of the wave together): row 0 holds the start token.
   __device__ __forceinline__ void clear_all(int n, int M, int lane, int nlanes) const {
-    const int tot = n * cpw, tok = M * cpw;
+    const int tot = n << lg, tok = M << lg;
     for (int j = lane; j < tot; j += nlanes) lo[j] = j < tok ? ST_TOKEN : 0;
     uint32_t* h = reinterpret_cast<uint32_t*>(hi);
     for (int j = lane; j < (tot + 3) / 4; j += nlanes) h[j] = 0;
@@ -74,12 +85,25 @@ struct Chunks {
   int64_t dF[VMAX], dB[VMAX], dW[VMAX], wF[VMAX], wB[VMAX];
 };
 
-struct Lane {
-  int64_t clock;
-  int pos, nops;
+// Descriptor of one op: slot read, slot written, needed state bit, edge weight, duration.
+struct Desc {
   int rd, wr, need, store;
   uint32_t state;  // state bits written on finish
   int64_t w, dur;
+  __device__ __forceinline__ void take_if(bool t, const Desc& o) {
+    rd = t ? o.rd : rd;
+    wr = t ? o.wr : wr;
+    need = t ? o.need : need;
+    store = t ? o.store : store;
+    state = t ? o.state : state;
+    w = t ? o.w : w;
+    dur = t ? o.dur : dur;
+  }
+};
+
+struct Lane : Desc {
+  int64_t clock;
+  int pos, nops;
 };
 
 template <int VMAX, typename T>
@@ -92,7 +116,7 @@ __device__ __forceinline__ T pick(const T (&a)[VMAX], int k) {
 
 // Describe op (kind, chunk k, micro-batch m); slot index of (row r, m) = r M + m.
 template <int VMAX>
-__device__ __forceinline__ void describe(Lane& L, const Chunks<VMAX>& c, int kind, int k, int m) {
+__device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, int kind, int k, int m) {
   const bool isF = kind == KF, isB = kind == KB;
   const int own = pick<VMAX>(c.base, k) + m;
   const int fo = pick<VMAX>(c.foff, k), bo = pick<VMAX>(c.boff, k);
@@ -123,8 +147,17 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, Lane& L, 
                                       uint32_t* rec) {
   bool live = L.pos < L.nops;
   for (;;) {
-    const uint64_t p = T.load(live ? L.rd : 0);
-    const bool ok = live && (((uint32_t)p >> L.need) & 1u) != 0;
+    uint32_t plo, phi;
+    T.issue(live ? L.rd : 0, plo, phi);
+    // the next op, computed while the read is in flight; kept only if this op completes
+    Gen g2 = gen;
+    g2.advance(true);
+    Desc d2;
+    describe<VMAX>(d2, c, g2.kind, g2.k, g2.m);
+    // the slot is consumed only after the next op's descriptor exists
+    __asm__ volatile("" : "+v"(plo), "+v"(phi), "+v"(d2.rd), "+v"(d2.need), "+v"(d2.dur));
+    const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
+    const bool ok = live && ((plo >> L.need) & 1u) != 0;
     const int64_t tin = (int64_t)(p >> 3) + L.w;
     const int64_t st = tin > L.clock ? tin : L.clock;
     const int64_t fin = st + L.dur;
@@ -134,8 +167,8 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, Lane& L, 
     L.clock = ok ? fin : L.clock;
     L.pos += ok ? 1 : 0;
     live = L.pos < L.nops;
-    gen.advance(ok);
-    describe<VMAX>(L, c, gen.kind, gen.k, gen.m);
+    gen.take_if(ok, g2);
+    L.take_if(ok, d2);
     __asm__ volatile("" ::: "memory");
     if (__ballot(ok) == 0) {
       const uint64_t actm = __ballot(live);
