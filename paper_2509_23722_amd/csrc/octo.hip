@@ -4,8 +4,10 @@
 //   k_prep      layer-cost prefix sums; clears the bin counters.
 //   k_merge_tab ideal stage-level start times for the MERGE order (cached per (P, v_max, M)).
 //   k_classify  one thread per candidate: validate, resolve the queue generator, write the
-//               sentinel of invalid candidates, count candidates per work bin.
-//   k_scatter   candidate indices grouped by bin (counting sort).
+//               sentinel of invalid candidates, count candidates per fine bin (work bin and
+//               sort key).
+//   k_plan      fine-bin start positions and per-bin counts.
+//   k_scatter   candidate indices grouped by fine bin (counting sort).
 //   k_sim       persistent waves; each takes a chunk of CPW candidates of one bin and simulates
 //               them together, queues generated in registers (the hot kernel).
 //   k_sim_mat   candidates with perturbations: queues materialised in global memory, moved,
@@ -30,12 +32,14 @@ constexpr int WAVE = 64;
 
 // Workspace control block (int32 words).
 constexpr int CTL_COUNTS = 0;     // [NBINS] candidates per bin
-constexpr int CTL_CURSOR = 64;    // [NBINS] scatter cursors
 constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (3)
 constexpr int CTL_WORK_MAT = 131; // chunk counter of k_sim_mat, perturbed list
 constexpr int CTL_WORK_REDO = 132;// chunk counter of k_sim_mat, redo list
 constexpr int CTL_REDO = 133;     // candidates whose times overflowed the 40-bit slots
-constexpr int CTL_WORDS = 256;
+constexpr int CTL_FINE = 256;     // [NFINE] candidates per fine bin
+constexpr int CTL_FPOS = 256 + 672; // [NFINE] next index position of each fine bin
+constexpr int CTL_WORDS = CTL_FPOS + 672;
+static_assert(NFINE <= 672, "fine-bin counters overlap");
 
 struct SimArgs {
   Problem pr;
@@ -272,52 +276,79 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
 }
 
 // One thread per candidate.
-__global__ void k_classify(SimArgs a, uint8_t* __restrict__ bins) {
-  __shared__ int hist[NBINS];
-  for (int i = threadIdx.x; i < NBINS; i += blockDim.x) hist[i] = 0;
+// One thread per candidate; dynamic LDS: P ints per thread for the AFAB round count.
+__global__ void k_classify(SimArgs a, uint16_t* __restrict__ bins) {
+  extern __shared__ int fr[];
+  __shared__ int hist[NFINE];
+  for (int i = threadIdx.x; i < NFINE; i += blockDim.x) hist[i] = 0;
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < a.n) {
     const uint8_t* rec = a.cands + i * a.pr.stride;
     Resolved r = resolve_record(a.pr, rec);
-    int bin = BIN_NONE;
+    int fine = BIN_NONE;
     if (!r.valid) {
       a.out_ms[i] = OCTO_MS_INVALID;
       for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
+    } else if (r.n_pert > 0) {
+      fine = BIN_MAT * NSUB;
     } else {
-      bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
-      atomicAdd(&hist[bin], 1);
+      int key = 0;
+      if (r.gen == GEN_AFAB && r.v >= 2)
+        key = round_key(afab_rounds(rec + 3 + a.pr.s_max, a.pr.P, r.S, a.pr.M, fr + threadIdx.x,
+                                    blockDim.x),
+                        r.v, a.pr.M);
+      fine = bin_of(r.v, r.gen, r.split) * NSUB + key;
     }
-    bins[i] = (uint8_t)bin;
+    if (fine != BIN_NONE) atomicAdd(&hist[fine], 1);
+    bins[i] = (uint16_t)fine;
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
-    if (hist[b]) atomicAdd(&a.ctl[CTL_COUNTS + b], hist[b]);
+  for (int b = threadIdx.x; b < NFINE; b += blockDim.x)
+    if (hist[b]) atomicAdd(&a.ctl[CTL_FINE + b], hist[b]);
 }
 
-__global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
-                          int32_t* __restrict__ idx) {
-  __shared__ int base[NBINS + 1];
-  __shared__ int hist[NBINS];
-  __shared__ int res[NBINS];
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int b = 0; b < NBINS; ++b) base[b] = acc, acc += a.ctl[CTL_COUNTS + b];
-    base[NBINS] = acc;
+// One block of PLAN_THREADS: fine-bin start positions (exclusive prefix sum) and bin counts.
+constexpr int PLAN_THREADS = 1024;
+static_assert(NFINE <= PLAN_THREADS, "one fine bin per thread");
+__global__ void __launch_bounds__(PLAN_THREADS) k_plan(int32_t* __restrict__ ctl) {
+  __shared__ int buf[2][PLAN_THREADS];
+  const int t = threadIdx.x;
+  const int c = t < NFINE ? ctl[CTL_FINE + t] : 0;
+  buf[0][t] = c;
+  __syncthreads();
+  int src = 0;
+  for (int off = 1; off < PLAN_THREADS; off <<= 1) {
+    const int x = buf[src][t] + (t >= off ? buf[src][t - off] : 0);
+    buf[src ^ 1][t] = x;
+    src ^= 1;
+    __syncthreads();
   }
-  for (int b = threadIdx.x; b < NBINS; b += blockDim.x) hist[b] = 0;
+  if (t < NFINE) ctl[CTL_FPOS + t] = buf[src][t] - c;
+  if (t < NBINS) {
+    int sum = 0;
+    for (int k = 0; k < NSUB; ++k) sum += ctl[CTL_FINE + t * NSUB + k];
+    ctl[CTL_COUNTS + t] = sum;
+  }
+}
+
+__global__ void k_scatter(SimArgs a, const uint16_t* __restrict__ bins,
+                          int32_t* __restrict__ idx) {
+  __shared__ int hist[NFINE];
+  __shared__ int res[NFINE];
+  for (int b = threadIdx.x; b < NFINE; b += blockDim.x) hist[b] = 0;
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int bin = BIN_NONE, local = 0;
+  int fine = BIN_NONE, local = 0;
   if (i < a.n) {
-    bin = bins[i];
-    if (bin != BIN_NONE) local = atomicAdd(&hist[bin], 1);
+    fine = bins[i];
+    if (fine != BIN_NONE) local = atomicAdd(&hist[fine], 1);
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
-    res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_CURSOR + b], hist[b]) : 0;
+  for (int b = threadIdx.x; b < NFINE; b += blockDim.x)
+    res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_FPOS + b], hist[b]) : 0;
   __syncthreads();
-  if (bin != BIN_NONE) idx[base[bin] + res[bin] + local] = (int32_t)i;
+  if (fine != BIN_NONE) idx[res[fine] + local] = (int32_t)i;
 }
 
 // Locate chunk `ch` (of CPW candidates) among generated bins [lo, hi); returns the bin or -1.
@@ -761,7 +792,7 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   l.pre = o;
   o = align_up(o + (size_t)(p->L + 1) * 3 * 8, 256);
   l.bin_of = o;
-  o = align_up(o + (size_t)n, 256);
+  o = align_up(o + (size_t)n * 2, 256);
   l.idx = o;
   o = align_up(o + (size_t)n * 4, 256);
   l.redo = o;
@@ -976,10 +1007,15 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   if (rc) return rc;
   char* base = static_cast<char*>(su.ws->base);
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
-  const int tb = 256;
+  const int tb = 128;
   const int nb = (int)((n + tb - 1) / tb);
-  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
-  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), 0, stream, a, bins);
+  uint16_t* bins = reinterpret_cast<uint16_t*>(base + su.l.bin_of);
+  const int cls_lds = tb * prob->P * (int)sizeof(int);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, cls_lds);
+  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), cls_lds, stream, a, bins);
+  if ((rc = launch_ok())) return rc;
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(PLAN_THREADS), 0, stream, a.ctl);
   if ((rc = launch_ok())) return rc;
   hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
                      reinterpret_cast<int32_t*>(base + su.l.idx));
@@ -987,7 +1023,7 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   // generated queues, one launch per v class with finish tables sized for it:
   // v = 2, then v = 1, then v = 3..8; then materialised queues (perturbations, 64-bit redo).
   const int P = prob->P;
-  const int b2 = bin_of(2, GEN_MERGE, 1), b1 = bin_of(1, GEN_MERGE, 1);
+  const int b2 = first_bin(2), b1 = first_bin(1);
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&
       (rc = launch_sim<2>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P, b2, b1,
