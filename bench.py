@@ -24,7 +24,8 @@ sys.path.insert(0, ROOT)
 PEAK_VALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 HBM_PEAK_GBS = 8000.0
 # simulation kernels, in launch order, between the library's measurement boundaries
-SIM_KERNELS = ["k_sim<2>", "k_sim<1>", "k_sim<8>", "k_sim_mat<2>"]
+SIM_KERNELS = ["k_sim<2, true>", "k_sim<2, false>", "k_sim<1, true>", "k_sim<1, false>",
+               "k_sim<8, false>", "k_sim_mat<2>"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_k_sim_workload3.json")
 
 
@@ -137,17 +138,21 @@ def main():
     ms_per_step = secs / args.steps * 1e3
     per_kernel_ms = kern_ms.mean(axis=0)
     int64_c, lane_c = algorithmic_work(recs_np, w.P, w.M)
-    v = recs_np[:, 1]
-    # the dominant kernel: k_sim<2>, which simulates the v = 2 candidates
-    dom = 0
+    v, pol = recs_np[:, 1], recs_np[:, 0]
+    # candidates each simulation kernel handles (no moves in this workload)
+    sets = [(v == 2) & (pol == 0), (v == 2) & (pol != 0), (v == 1) & (pol == 0),
+            (v == 1) & (pol != 0), v >= 3, np.zeros(n, dtype=bool)]
+    # the dominant kernel: the one that takes longest
+    dom = int(np.argmax(per_kernel_ms))
     dom_ms = float(per_kernel_ms[dom])
-    dom_lane_ops = int(lane_c[v == 2].sum())
+    dom_set = sets[dom]
+    dom_lane_ops = int(lane_c[dom_set].sum())
     achieved = dom_lane_ops / (dom_ms * 1e-3) / 1e12
-    n_dom = int((v == 2).sum())
+    n_dom = int(dom_set.sum())
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         t = json.load(open(TRAFFIC_FILE))
-        if t.get("kernel_source_sha") == kernel_source_hash():
+        if t.get("kernel_source_sha") == kernel_source_hash() and t.get("kernel") == SIM_KERNELS[dom]:
             traffic = t.get("hbm_bytes_per_launch")
     all_ms = float(per_kernel_ms.sum())
     roofline = {
@@ -155,7 +160,7 @@ def main():
         "unit": "Tops/s (32-bit VALU lane-ops)", "frac": round(achieved / PEAK_VALU_TOPS, 5),
         "traffic": traffic, "kernel": SIM_KERNELS[dom], "kernel_ms": round(dom_ms, 4),
         "kernel_candidates": n_dom, "alg_lane_ops_per_launch": dom_lane_ops,
-        "alg_int64_ops_per_launch": int(int64_c[v == 2].sum()),
+        "alg_int64_ops_per_launch": int(int64_c[dom_set].sum()),
         "hbm_alg_gbs": round(n_dom * (recs_np.shape[1] + 8 + 8 * w.P) / (dom_ms * 1e-3) / 1e9, 2),
         "hbm_peak_gbs": HBM_PEAK_GBS,
         "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, per_kernel_ms)},

@@ -32,10 +32,10 @@ constexpr int WAVE = 64;
 
 // Workspace control block (int32 words).
 constexpr int CTL_COUNTS = 0;     // [NBINS] candidates per bin
-constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (3)
-constexpr int CTL_WORK_MAT = 131; // chunk counter of k_sim_mat, perturbed list
-constexpr int CTL_WORK_REDO = 132;// chunk counter of k_sim_mat, redo list
-constexpr int CTL_REDO = 133;     // candidates whose times overflowed the 40-bit slots
+constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (5)
+constexpr int CTL_WORK_MAT = 136; // chunk counter of k_sim_mat, perturbed list
+constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
+constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
 constexpr int CTL_FINE = 256;     // [NFINE] candidates per fine bin
 constexpr int CTL_FPOS = 256 + 672; // [NFINE] next index position of each fine bin
 constexpr int CTL_WORDS = CTL_FPOS + 672;
@@ -63,6 +63,8 @@ struct SimArgs {
   int qcap;
   int bin_lo, bin_hi;    // generated bins handled by this launch
   int work;              // chunk counter index of this launch
+  int ring;              // slots per stage row of this launch's finish tables (R)
+  uint64_t redo_bins;    // bins whose queues may exceed R in flight: sent to the 64-bit path
 };
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
@@ -76,17 +78,18 @@ template <int VMAX>
 __device__ __forceinline__ void zero_chunks(Chunks<VMAX>& c) {
 #pragma unroll
   for (int k = 0; k < VMAX; ++k) {
-    c.st[k] = 0, c.base[k] = 0, c.foff[k] = 0, c.fneed[k] = 0, c.boff[k] = 0, c.bneed[k] = 0;
+    c.st[k] = 0, c.base[k] = 0, c.first[k] = 0, c.fmask[k] = 0, c.brow[k] = 0, c.bmask[k] = 0;
     c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
   }
 }
 
-// Stages of device d (ascending), their durations, incoming link weights and slot offsets;
-// returns busy(d).
+// Stages of device d (ascending), their durations, incoming link weights and finish-table
+// rows; returns busy(d).
 template <int VMAX>
 __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr,
                                                 const uint8_t* rec, const int64_t* pre,
-                                                const int64_t* link, int d, int v, int split) {
+                                                const int64_t* link, int d, int v, int split,
+                                                const Ring& ring) {
   const int S = pr.P * v, M = pr.M;
   const uint8_t* bnd = rec + 4;
   const uint8_t* dev = rec + 3 + pr.s_max;
@@ -109,11 +112,11 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       const int64_t f = pre[3 * b1 + 0] - pre[3 * b0 + 0];
       const int64_t bi = pre[3 * b1 + 1] - pre[3 * b0 + 1];
       const int64_t wg = pre[3 * b1 + 2] - pre[3 * b0 + 2];
-      c.base[k] = s * M;
-      c.foff[k] = s > 0 ? -M : 0;     // stage 0 reads its own start token
-      c.fneed[k] = s > 0 ? 1 : 2;     // bit of ST_F / ST_TOKEN
-      c.boff[k] = s < S - 1 ? M : 0;  // the last stage reads its own F
-      c.bneed[k] = s < S - 1 ? 0 : 1; // bit of ST_B / ST_F
+      c.base[k] = s * ring.R;
+      c.first[k] = s == 0;
+      c.fmask[k] = s > 0 ? (int)(ST_F | ST_PAR) : 0;
+      c.brow[k] = s < S - 1 ? ring.R : 0;  // the last stage reads its own F
+      c.bmask[k] = (int)((s < S - 1 ? ST_B : ST_F) | ST_PAR);
       c.dF[k] = f;
       c.dB[k] = split ? bi : bi + wg;
       c.dW[k] = wg;
@@ -157,6 +160,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
   const bool has = cand >= 0;
   const int S = P * v;
+  const Ring ring = make_ring(S, M, a.ring);
   if (has) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
   __asm__ volatile("" ::: "memory");
 
@@ -168,13 +172,13 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   int64_t busy = 0;
   const bool mine = has && d < P;
   if (mine) {
-    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
     L.nops = (split ? 3 : 2) * v * M;
   } else {
     zero_chunks<VMAX>(c);
   }
   __asm__ volatile("" ::: "memory");
-  T.clear_all(S * M, M, lane_id(), WAVE);
+  T.clear_all(ring.zero + 1, lane_id(), WAVE);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
@@ -183,28 +187,28 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   if constexpr (GEN == GEN_AFAB) {
     GenAfab g;
     g.init(v, M);
-    describe<VMAX>(L, c, g.kind, g.k, g.m);
-    relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
+    describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
+    relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   } else if constexpr (GEN == GEN_INTER) {
     const int r = c.st[0];
     if constexpr (P2) {
       GenInterP2 g;
       g.init(P, v, M, r, split, split ? r : 0);
-      describe<VMAX>(L, c, g.kind, g.k, g.m);
-      relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
+      describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
+      relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     } else {
       GenInter g;
       g.init(P, v, M, r, split, split ? r : 0);
-      describe<VMAX>(L, c, g.kind, g.k, g.m);
-      relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
+      describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
+      relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     }
   } else {
     GenMerge<VMAX> g;
     const int rowlen = (split ? 3 : 2) * M;
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
            [&](int k) { return pick<VMAX>(c.st, k); });
-    describe<VMAX>(L, c, g.kind, g.k, g.m);
-    relax<VMAX>(g, c, L, T, G, gbit, lsb, dead, nullptr);
+    describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
+    relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   }
 
   const int64_t ms = group_max(L.clock, G);
@@ -251,16 +255,17 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   const Table64 T{reinterpret_cast<int64_t*>(smem)};
   const int rowlen = (split ? 3 : 2) * M;
   uint32_t* tab = mtab + merge_offset(P, M, v, split);
-  T.clear(S * M, M, d, WAVE);
+  const Ring ring = make_ring(S, M, M);
+  T.clear(ring.zero + 1, d, WAVE);
   __asm__ volatile("" ::: "memory");
   Chunks<1> c;
   zero_chunks<1>(c);
   c.st[0] = d;
   c.base[0] = d * M;
-  c.foff[0] = d > 0 ? -M : 0;
-  c.fneed[0] = d > 0 ? 1 : 2;
-  c.boff[0] = d < S - 1 ? M : 0;
-  c.bneed[0] = d < S - 1 ? 0 : 1;
+  c.first[0] = d == 0;
+  c.fmask[0] = d > 0 ? (int)(ST_F | ST_PAR) : 0;
+  c.brow[0] = d < S - 1 ? M : 0;
+  c.bmask[0] = (int)((d < S - 1 ? ST_B : ST_F) | ST_PAR);
   c.dF[0] = 1;
   c.dB[0] = split ? 1 : 2;
   c.dW[0] = 1;
@@ -270,12 +275,11 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   L.nops = d < S ? rowlen : 0;
   GenInter g;
   g.init(S, 1, M, d < S ? d : 0, split, split ? d : 0);
-  describe<1>(L, c, g.kind, g.k, g.m);
+  describe<1>(L, c, ring, g.kind, g.k, g.m);
   bool dead = false;
-  relax<1>(g, c, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
+  relax<1>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
 }
 
-// One thread per candidate.
 // One thread per candidate; dynamic LDS: P ints per thread for the AFAB round count.
 __global__ void k_classify(SimArgs a, uint16_t* __restrict__ bins) {
   extern __shared__ int fr[];
@@ -370,22 +374,27 @@ __device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, int lo,
   return -1;
 }
 
-template <int VMAX>
+// ONLY_AFAB: the launch holds only AFAB bins (a smaller kernel).
+template <int VMAX, bool ONLY_AFAB>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
                                              int split, uint8_t* lds_wave) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
-  if (gen == GEN_AFAB) run_generated<VMAX, GEN_AFAB, false>(a, cand, v, split, lds_wave);
-  else if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_wave);
-  else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_wave);
-  else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_wave);
+  if (ONLY_AFAB || gen == GEN_AFAB) {
+    run_generated<VMAX, GEN_AFAB, false>(a, cand, v, split, lds_wave);
+  } else if constexpr (!ONLY_AFAB) {
+    if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_wave);
+    else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_wave);
+    else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_wave);
+  }
 }
 
-// Generated-queue simulation for the bins of one v class: VC = 1 (v = 1), 2 (v = 2) or 8
-// (v = 3..8); finish tables sized for that class.
-template <int VC>
+// Generated-queue simulation for the bins [bin_lo, bin_hi) of one v class: VC = 1 (v = 1),
+// 2 (v = 2) or 8 (v = 3..8); finish tables sized for that class with a.ring slots per row.
+template <int VC, bool ONLY_AFAB>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int g = lane_id() / a.G;
+  const int d = lane_id() % a.G;
   for (;;) {
     int ch = 0;
     if (lane_id() == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -398,7 +407,12 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     const int cnt = a.ctl[CTL_COUNTS + bin];
     const int e = entry0 + g;
     const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
-    dispatch_gen<VC>(a, gen, cand, v, split, smem);
+    if ((a.redo_bins >> bin) & 1) {
+      // this bin's queues may hold more than a.ring micro-batches in flight
+      if (cand >= 0 && d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      continue;
+    }
+    dispatch_gen<VC, ONLY_AFAB>(a, gen, cand, v, split, smem);
   }
 }
 
@@ -486,12 +500,14 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
         Resolved r = resolve_record(a.pr, grec);
         gen = r.gen;
       }
+      const int S = P * v;
+      const Ring ring = make_ring(S, M, M);
       Chunks<VMAX> c;
       int64_t busy = 0;
       Lane L;
       L.clock = 0, L.pos = 0, L.nops = 0;
       if (mine) {
-        busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+        busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
         L.nops = materialise<VMAX>(a, c, v, gen, split, row);
         const uint8_t* pp = grec + pert_off(a.pr.s_max);
         const int np = grec[2];
@@ -505,14 +521,13 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       } else {
         zero_chunks<VMAX>(c);
       }
-      const int S = P * v;
-      if (has) T.clear(S * M, M, d, G);
+      if (has) T.clear(ring.zero + 1, d, G);
       __asm__ volatile("" ::: "memory");
       GenMat q;
       q.init(row, L.nops);
-      describe<VMAX>(L, c, q.kind, q.k, q.m);
+      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
       bool dead = false;
-      relax<VMAX>(q, c, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       const int64_t ms = group_max(L.clock, G);
       if (mine) {
         if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
@@ -581,6 +596,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     }
     const int S = P * v;
     const int qlen = (split ? 3 : 2) * v * M;
+    const Ring ring = make_ring(S, M, M);
 
     // propose (step >= 1); the move is applied to the staged record / this chain's queue row
     int kind = -1, mi = 0, sd = -1;
@@ -634,19 +650,19 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     Lane L;
     L.clock = 0, L.pos = 0, L.nops = 0;
     if (run && d < P) {
-      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split);
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
       if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, row);
       L.nops = qlen;
     } else {
       zero_chunks<VMAX>(c);
     }
-    if (run) T.clear(S * M, M, d, G);
+    if (run) T.clear(ring.zero + 1, d, G);
     __asm__ volatile("" ::: "memory");
     GenMat q;
     q.init(row, L.nops);
-    describe<VMAX>(L, c, q.kind, q.k, q.m);
+    describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
     bool dead = false;
-    relax<VMAX>(q, c, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     const int64_t ms = group_max(L.clock, G);
 
     if (!has || skip) continue;
@@ -689,6 +705,9 @@ struct Workspace {
   size_t mt_bytes = 0;
   bool mt_valid = false;
   int mt_P = 0, mt_vmax = 0, mt_M = 0;
+  // largest number of micro-batches in flight per stage, per generated bin of v = 1, 2
+  int inflight[NBIN_GEN] = {};
+  int if_P = 0, if_M = 0;
 };
 
 std::mutex g_mu;
@@ -745,10 +764,11 @@ int lanes_per_candidate(int P) {
 
 // 40-bit-slot plan for generated queues with up to s_cap stages; the staged record shares the
 // table's memory.
-Plan fast_plan(const octo_problem* p, int lds_max, int s_cap) {
+// s_cap stages of R slots plus the zero slot.
+Plan fast_plan(const octo_problem* p, int lds_max, int s_cap, int R) {
   Plan pl;
   pl.G = lanes_per_candidate(p->P);
-  pl.slots = s_cap * p->M;
+  pl.slots = s_cap * R + 1;
   pl.rec_bytes = pert_off(p->P * p->v_max);
   pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
   pl.table_bytes = (int)(pl.slots * 4 + pl.slots);
@@ -767,7 +787,7 @@ Plan big_plan(const octo_problem* p, int lds_max) {
   pl.slots = p->P * p->v_max * p->M;
   pl.rec_bytes = pert_off(p->P * p->v_max);
   pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
-  pl.table_bytes = (int)align_up((size_t)pl.slots * 8, 16);
+  pl.table_bytes = (int)align_up((size_t)(pl.slots + 1) * 8, 16);  // + the zero slot
   pl.group_bytes = pl.table_bytes + (int)align_up(pl.rec_bytes, 16);
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
   pl.lds_bytes = pl.CPW * pl.group_bytes;
@@ -852,6 +872,52 @@ int mat_grid_for(const Plan& big, int cus, int* g) {
   return occupancy_grid(k_sim_mat<VC>, big.lds_bytes, cus, g);
 }
 
+// Largest number of micro-batches of one stage in flight over one device queue of the
+// interleaved order: forwards issued minus backwards, and minus weight-gradient ops when split.
+int inflight_inter(int P, int v, int M, int r, int split, int lag) {
+  GenInter g;
+  g.init(P, v, M, r, split, lag);
+  int nF[8] = {}, nB[8] = {}, nW[8] = {};
+  int worst = 0;
+  const int n = (split ? 3 : 2) * v * M;
+  for (int i = 0; i < n; ++i) {
+    const int k = g.k;
+    if (g.kind == KF) {
+      ++nF[k];
+      worst = std::max(worst, nF[k] - nB[k]);
+      if (split) worst = std::max(worst, nF[k] - nW[k]);
+    } else if (g.kind == KB) {
+      ++nB[k];
+    } else {
+      ++nW[k];
+    }
+    g.advance(true);
+  }
+  return worst;
+}
+
+// Per generated bin of v = 1, 2: the in-flight bound of its queues. INTER queues depend on the
+// device's first stage r; a MERGE queue keeps, for each of its stages s, the order of stage s in
+// the ideal stage-level schedule (interleaved order on S devices, v = 1, device s), so its bound
+// is the largest over those orders. AFAB keeps all M micro-batches in flight.
+void compute_inflight(const octo_problem* p, Workspace& ws) {
+  if (ws.if_P == p->P && ws.if_M == p->M) return;
+  const int P = p->P, M = p->M;
+  for (int b = 0; b < NBIN_GEN; ++b) ws.inflight[b] = M;
+  for (int v = 1; v <= 2; ++v) {
+    for (int split = 0; split <= 1; ++split) {
+      int wi = 0, wm = 0;
+      for (int r = 0; r < P; ++r) wi = std::max(wi, inflight_inter(P, v, M, r, split, split ? r : 0));
+      const int S = P * v;
+      for (int st = 0; st < S; ++st)
+        wm = std::max(wm, inflight_inter(S, 1, M, st, split, split ? st : 0));
+      ws.inflight[bin_of(v, GEN_INTER, split)] = wi;
+      ws.inflight[bin_of(v, GEN_MERGE, split)] = wm;
+    }
+  }
+  ws.if_P = P, ws.if_M = M;
+}
+
 // Shared front half of octo_sim_batch and octo_tune_step: device, plans, workspace, prefix
 // sums, MERGE tables.
 int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, int64_t n,
@@ -883,7 +949,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
   }
   if (prob->v_max >= 2 && !(ws.mt_valid && ws.mt_P == prob->P && ws.mt_vmax == prob->v_max &&
                             ws.mt_M == prob->M)) {
-    const int lds = (int)align_up((size_t)prob->P * prob->v_max * prob->M * 8, 16);
+    const int lds = (int)align_up(((size_t)prob->P * prob->v_max * prob->M + 1) * 8, 16);
     if (lds > su->di.lds_max) return OCTO_EUNSUPPORTED;
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_merge_tab),
                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -925,24 +991,33 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.bin_lo = 0;
   a.bin_hi = NBIN_GEN;
   a.work = CTL_WORK;
+  a.ring = prob->M;
+  a.redo_bins = 0;
   return a;
 }
 
-// Launch k_sim<VC> over generated bins [lo, hi) with its own 40-bit plan.
-template <int VC>
+// Launch k_sim<VC, ONLY_AFAB> over generated bins [lo, hi) with its own 40-bit plan: s_cap
+// stages of ring_want (rounded up to a power of two, or M) slots; bins whose in-flight bound
+// exceeds the ring go to the 64-bit path. Nothing is launched for bins without candidates.
+template <int VC, bool ONLY_AFAB>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-               int64_t n, int64_t* ms, int64_t* bub, int s_cap, int lo, int hi, int work,
-               hipStream_t stream) {
-  const Plan pl = fast_plan(prob, su.di.lds_max, s_cap);
+               int64_t n, int64_t* ms, int64_t* bub, int s_cap, int ring_want, int lo, int hi,
+               int work, hipStream_t stream) {
+  const Ring ring = make_ring(s_cap, prob->M, ring_want);
+  const Plan pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R);
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub);
   a.bin_lo = lo, a.bin_hi = hi, a.work = work;
+  a.ring = ring.R;
+  a.redo_bins = 0;
+  for (int b = lo; b < hi; ++b)
+    if (ring.R < prob->M && su.ws->inflight[b] > ring.R) a.redo_bins |= 1ull << b;
   int grid = 0;
-  int rc = occupancy_grid(k_sim<VC>, pl.lds_bytes, su.di.cus, &grid);
+  int rc = occupancy_grid(k_sim<VC, ONLY_AFAB>, pl.lds_bytes, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  hipLaunchKernelGGL(k_sim<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
+  hipLaunchKernelGGL((k_sim<VC, ONLY_AFAB>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
   return launch_ok();
 }
 
@@ -1020,31 +1095,44 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
                      reinterpret_cast<int32_t*>(base + su.l.idx));
   if ((rc = launch_ok())) return rc;
-  // generated queues, one launch per v class with finish tables sized for it:
-  // v = 2, then v = 1, then v = 3..8; then materialised queues (perturbations, 64-bit redo).
-  const int P = prob->P;
+  // generated queues, launches per v class with finish tables sized for it: v = 2 AFAB, then
+  // v = 2 other generators (ring rows), v = 1 likewise, then v = 3..8; then materialised queues
+  // (perturbations, 64-bit redo).
+  compute_inflight(prob, *su.ws);
+  const int P = prob->P, M = prob->M;
   const int b2 = first_bin(2), b1 = first_bin(1);
   if ((rc = record_mark(0, stream))) return rc;
-  if (prob->v_max >= 2 &&
-      (rc = launch_sim<2>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P, b2, b1,
-                          CTL_WORK + 1, stream)))
+  if (prob->v_max >= 2) {
+    if ((rc = launch_sim<2, true>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P,
+                                  M, b2, b2 + 1, CTL_WORK + 3, stream)))
+      return rc;
+    if ((rc = record_mark(1, stream))) return rc;
+    if ((rc = launch_sim<2, false>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P,
+                                   2 * P, b2 + 1, b1, CTL_WORK + 1, stream)))
+      return rc;
+  } else if ((rc = record_mark(1, stream))) {
     return rc;
-  if ((rc = record_mark(1, stream))) return rc;
-  if ((rc = launch_sim<1>(prob, su, link, candidates, n, out_makespan, out_bubble, P, b1,
-                          NBIN_GEN, CTL_WORK + 0, stream)))
-    return rc;
+  }
   if ((rc = record_mark(2, stream))) return rc;
-  if (prob->v_max >= 3 &&
-      (rc = launch_sim<8>(prob, su, link, candidates, n, out_makespan, out_bubble,
-                          P * prob->v_max, 0, b2, CTL_WORK + 2, stream)))
+  if ((rc = launch_sim<1, true>(prob, su, link, candidates, n, out_makespan, out_bubble, P, M, b1,
+                                b1 + 1, CTL_WORK + 4, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
+  if ((rc = launch_sim<1, false>(prob, su, link, candidates, n, out_makespan, out_bubble, P, P,
+                                 b1 + 1, NBIN_GEN, CTL_WORK + 0, stream)))
+    return rc;
+  if ((rc = record_mark(4, stream))) return rc;
+  if (prob->v_max >= 3 &&
+      (rc = launch_sim<8, false>(prob, su, link, candidates, n, out_makespan, out_bubble,
+                                 P * prob->v_max, M, 0, b2, CTL_WORK + 2, stream)))
+    return rc;
+  if ((rc = record_mark(5, stream))) return rc;
   if (prob->v_max <= 2)
     hipLaunchKernelGGL(k_sim_mat<2>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
   else
     hipLaunchKernelGGL(k_sim_mat<8>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
   if ((rc = launch_ok())) return rc;
-  return record_mark(4, stream);
+  return record_mark(6, stream);
 }
 
 int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,

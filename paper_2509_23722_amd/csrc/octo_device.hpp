@@ -199,12 +199,13 @@ struct GenAfab {
 // micro-batch c*P + a for forwards; backwards take chunk v-1-b. Warm-up w forwards, then
 // (F, B) pairs, then the remaining B; with a split backward each B's W follows `lag` B's later
 // (a FIFO of depth lag), flushed at the end. At v = 1 this is 1F1B.
-__device__ __forceinline__ int inter_warmup(int P, int v, int M, int r) {
-  return v == 1 ? min(P - 1 - r, M) : min(2 * (P - 1 - r) + (v - 1) * P, v * M);
+__host__ __device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
+__host__ __device__ __forceinline__ int inter_warmup(int P, int v, int M, int r) {
+  return v == 1 ? imin(P - 1 - r, M) : imin(2 * (P - 1 - r) + (v - 1) * P, v * M);
 }
-__device__ __forceinline__ int inter_kind(int nF, int nB, int nW, int w, int N, int split,
-                                          int lag) {
-  const int fcap = min(N, w + nB + 1);
+__host__ __device__ __forceinline__ int inter_kind(int nF, int nB, int nW, int w, int N,
+                                                   int split, int lag) {
+  const int fcap = imin(N, w + nB + 1);
   const int body = nF < fcap ? KF : KB;
   const int k1 = nB < N ? body : KW;
   const int k2 = (split && nW < nB - lag) ? KW : k1;
@@ -249,25 +250,26 @@ struct GenInter {
   int nF, nB, nW;
   int fa, fb, fc, ba, bb, bc, wa, wb, wc;
   int kind, k, m;
-  __device__ __forceinline__ void init(int P_, int v_, int M, int r, int split_, int lag_) {
+  __host__ __device__ __forceinline__ void init(int P_, int v_, int M, int r, int split_,
+                                                int lag_) {
     P = P_, v = v_, N = v_ * M, split = split_, lag = lag_;
     w = inter_warmup(P, v, M, r);
     nF = nB = nW = 0;
     fa = fb = fc = ba = bb = bc = wa = wb = wc = 0;
     update();
   }
-  __device__ __forceinline__ void update() {
+  __host__ __device__ __forceinline__ void update() {
     kind = inter_kind(nF, nB, nW, w, N, split, lag);
     k = kind == KF ? fb : kind == KB ? v - 1 - bb : v - 1 - wb;
     m = kind == KF ? fc * P + fa : kind == KB ? bc * P + ba : wc * P + wa;
   }
-  __device__ __forceinline__ static void inc(int& a, int& b, int& c, int P, int v) {
+  __host__ __device__ __forceinline__ static void inc(int& a, int& b, int& c, int P, int v) {
     if (++a == P) {
       a = 0;
       if (++b == v) b = 0, ++c;
     }
   }
-  __device__ __forceinline__ void advance(bool ok) {
+  __host__ __device__ __forceinline__ void advance(bool ok) {
     if (ok) {
       if (kind == KF) ++nF, inc(fa, fb, fc, P, v);
       else if (kind == KB) ++nB, inc(ba, bb, bc, P, v);
@@ -275,7 +277,7 @@ struct GenInter {
     }
     update();
   }
-  __device__ __forceinline__ void take_if(bool t, const GenInter& o) {
+  __host__ __device__ __forceinline__ void take_if(bool t, const GenInter& o) {
     if (t) *this = o;
   }
 };

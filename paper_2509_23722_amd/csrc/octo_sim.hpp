@@ -1,20 +1,29 @@
 // octo_sim.hpp — the max-plus relaxation core: one wave simulates CPW candidates at once, G
 // lanes per candidate, lane d = pipeline device d. Each candidate owns a finish table in LDS
-// with one slot per (stage, micro-batch).
+// with one slot per (stage, micro-batch ring position).
 //
 // Slot value = fin << 3 | state, state bits: 1 = B(s,m) finished, 2 = F(s,m) finished (kept
-// after B), 4 = stage-0 start token (row 0 starts as 4: "ready at time 0"); empty = 0. One slot
-// per (s,m) suffices because B(s,m) can only finish after F(s+1,m) (which consumed F(s,m)) has
-// finished: B(s,m) needs B(s+1,m), which needs F(s+1,m).
+// after B), 4 = parity of the occupant's micro-batch round m / R; empty = 0. One slot per (s,m)
+// suffices because B(s,m) can only finish after F(s+1,m) (which consumed F(s,m)) has finished:
+// B(s,m) needs B(s+1,m), which needs F(s+1,m).
 //
-// Every op reads exactly one slot and needs one state bit there:
-//   F(0,m): its own slot, token;   F(s,m), s > 0: row s-1, bit 2; in = fin + link weight.
+// Every op reads exactly one slot and needs one state bit there (and the parity of its own m):
+//   F(0,m): the zero slot (always ready, time 0);   F(s,m), s > 0: row s-1, bit 2;
+//   in = fin + link weight.
 //   B(s,m), s < S-1: row s+1, bit 1; in = fin + link weight.
 //   B(S-1,m): its own slot, bit 2 (the loss turns the forward around).
 //   W(s,m): its own slot, bit 1; W writes nothing.
 // Other dependencies are implied: F(s,m) -> B(s,m) for s < S-1 follows from F(s,m) ->
 // F(s+1,m) -> B(s+1,m) -> B(s,m). start = max(device clock, in); fin = start + duration
 // (§5: record start/end per node; §6 Eq. 1: makespan = latest finish).
+//
+// Ring rows: micro-batch m of stage s lives in slot s R + (m mod R). This is exact whenever no
+// stage ever has more than R micro-batches in flight on its device (forwards issued minus
+// backwards, and minus weight-gradient ops when split): then B(s,m) and W(s,m) precede
+// F(s,m+R) in the device's queue, every reader of (s,m) — F(s+1,m), B(s-1,m), B(S-1,m) and
+// W(s,m) — precedes F(s,m+R) in the graph, so it has read the slot in an earlier round than the
+// overwrite; and a reader that finds the previous occupant m-R (never an older one) tells it
+// apart by the parity bit. R = M (no wrap) is the plain table.
 //
 // Rounds: every live lane tries its head op once per round; readiness is structural, so when
 // no lane of the wave advances in a round, every candidate that still has work is deadlocked.
@@ -25,7 +34,26 @@
 
 namespace octo {
 
-constexpr uint32_t ST_B = 1, ST_F = 2, ST_TOKEN = 4;
+constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
+
+// Ring geometry of one finish table: R slots per stage row, slot of m = m & mask, parity
+// (m >> lg) & 1; `zero` = index of the always-ready slot (holds 0). Without wrap (R = M):
+// mask = all ones, lg = 30.
+struct Ring {
+  int R, mask, lg, zero;
+};
+__host__ __device__ __forceinline__ Ring make_ring(int S, int M, int R) {
+  Ring r;
+  if (R >= M) {
+    r.R = M, r.mask = 0x7FFFFFFF, r.lg = 30;
+  } else {
+    int lg = 0;
+    while ((1 << lg) < R) ++lg;
+    r.R = 1 << lg, r.mask = r.R - 1, r.lg = lg;
+  }
+  r.zero = S * r.R;
+  return r;
+}
 
 // 64-bit slots: one int64 per (stage, micro-batch).
 struct Table64 {
@@ -37,8 +65,8 @@ struct Table64 {
   }
   __device__ __forceinline__ uint64_t load(int i) const { return (uint64_t)T[i]; }
   __device__ __forceinline__ void store(int i, uint64_t v) const { T[i] = (int64_t)v; }
-  __device__ __forceinline__ void clear(int n, int M, int d, int G) const {
-    for (int i = d; i < n; i += G) T[i] = i < M ? ST_TOKEN : 0;
+  __device__ __forceinline__ void clear(int n, int d, int G) const {
+    for (int i = d; i < n; i += G) T[i] = 0;
   }
   __host__ __device__ static size_t bytes(int slots) { return (size_t)slots * 8; }
 };
@@ -66,10 +94,10 @@ struct Table40 {
     lo[j] = (uint32_t)v;
     hi[j] = (uint8_t)(v >> 32);
   }
-  // Clear n slots of every group (all lanes of the wave together): row 0 holds the start token.
-  __device__ __forceinline__ void clear_all(int n, int M, int lane, int nlanes) const {
-    const int tot = n << lg, tok = M << lg;
-    for (int j = lane; j < tot; j += nlanes) lo[j] = j < tok ? ST_TOKEN : 0;
+  // Clear n slots of every group (all lanes of the wave together).
+  __device__ __forceinline__ void clear_all(int n, int lane, int nlanes) const {
+    const int tot = n << lg;
+    for (int j = lane; j < tot; j += nlanes) lo[j] = 0;
     uint32_t* h = reinterpret_cast<uint32_t*>(hi);
     for (int j = lane; j < (tot + 3) / 4; j += nlanes) h[j] = 0;
   }
@@ -79,21 +107,24 @@ struct Table40 {
 template <int VMAX>
 struct Chunks {
   int st[VMAX];                      // stage of chunk k
-  int base[VMAX];                    // slot index of the stage's own row: s M
-  int foff[VMAX], fneed[VMAX];       // F read offset / needed state bit index
-  int boff[VMAX], bneed[VMAX];       // B read offset / needed state bit index
+  int base[VMAX];                    // first slot of the stage's own row: s R
+  int first[VMAX];                   // stage 0: forwards read the zero slot
+  int fmask[VMAX];                   // state bits a forward needs (0: always ready)
+  int brow[VMAX], bmask[VMAX];       // backward read row offset / needed state bits
   int64_t dF[VMAX], dB[VMAX], dW[VMAX], wF[VMAX], wB[VMAX];
 };
 
-// Descriptor of one op: slot read, slot written, needed state bit, edge weight, duration.
+// Descriptor of one op: slot read, slot written, readiness test (slot & mask) == want, edge
+// weight, duration.
 struct Desc {
-  int rd, wr, need, store;
+  int rd, wr, mask, want, store;
   uint32_t state;  // state bits written on finish
   int64_t w, dur;
   __device__ __forceinline__ void take_if(bool t, const Desc& o) {
     rd = t ? o.rd : rd;
     wr = t ? o.wr : wr;
-    need = t ? o.need : need;
+    mask = t ? o.mask : mask;
+    want = t ? o.want : want;
     store = t ? o.store : store;
     state = t ? o.state : state;
     w = t ? o.w : w;
@@ -114,18 +145,22 @@ __device__ __forceinline__ T pick(const T (&a)[VMAX], int k) {
   return x;
 }
 
-// Describe op (kind, chunk k, micro-batch m); slot index of (row r, m) = r M + m.
+// Describe op (kind, chunk k, micro-batch m).
 template <int VMAX>
-__device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, int kind, int k, int m) {
+__device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, const Ring& ring,
+                                         int kind, int k, int m) {
   const bool isF = kind == KF, isB = kind == KB;
-  const int own = pick<VMAX>(c.base, k) + m;
-  const int fo = pick<VMAX>(c.foff, k), bo = pick<VMAX>(c.boff, k);
-  const int fn = pick<VMAX>(c.fneed, k), bn = pick<VMAX>(c.bneed, k);
-  L.rd = own + (isF ? fo : isB ? bo : 0);
+  const int own = pick<VMAX>(c.base, k) + (m & ring.mask);
+  const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
+  const int fm = pick<VMAX>(c.fmask, k), bm = pick<VMAX>(c.bmask, k);
+  const int br = pick<VMAX>(c.brow, k);
+  const bool zf = isF && pick<VMAX>(c.first, k) != 0;
+  L.rd = zf ? ring.zero : own + (isF ? -ring.R : isB ? br : 0);
   L.wr = own;
   L.store = isF || isB;
-  L.need = isF ? fn : isB ? bn : 0;
-  L.state = isF ? ST_F : (ST_F | ST_B);
+  L.mask = isF ? fm : isB ? bm : (int)(ST_B | ST_PAR);
+  L.want = L.mask & (int)(par ? (ST_B | ST_F | ST_PAR) : (ST_B | ST_F));
+  L.state = (isF ? ST_F : (ST_F | ST_B)) | (par << 2);
   const int64_t wf = pick<VMAX>(c.wF, k), wb = pick<VMAX>(c.wB, k);
   const int64_t df = pick<VMAX>(c.dF, k), db = pick<VMAX>(c.dB, k), dw = pick<VMAX>(c.dW, k);
   L.w = isF ? wf : isB ? wb : 0;
@@ -142,9 +177,9 @@ __device__ __forceinline__ uint64_t fold_groups(uint64_t x, int G, uint64_t lsb)
 // gbit: this lane's group bit in folded masks; lsb: all group bits. rec (nullable): ideal-start
 // recording for the MERGE table, rec[pos] = start << 16 | kind << 12 | m.
 template <int VMAX, class Tab, class Gen>
-__device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, Lane& L, const Tab& T,
-                                      int G, uint64_t gbit, uint64_t lsb, bool& dead,
-                                      uint32_t* rec) {
+__device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
+                                      const Tab& T, int G, uint64_t gbit, uint64_t lsb,
+                                      bool& dead, uint32_t* rec) {
   bool live = L.pos < L.nops;
   for (;;) {
     uint32_t plo, phi;
@@ -153,11 +188,11 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, Lane& L, 
     Gen g2 = gen;
     g2.advance(true);
     Desc d2;
-    describe<VMAX>(d2, c, g2.kind, g2.k, g2.m);
+    describe<VMAX>(d2, c, ring, g2.kind, g2.k, g2.m);
     // the slot is consumed only after the next op's descriptor exists
-    __asm__ volatile("" : "+v"(plo), "+v"(phi), "+v"(d2.rd), "+v"(d2.need), "+v"(d2.dur));
+    __asm__ volatile("" : "+v"(plo), "+v"(phi), "+v"(d2.rd), "+v"(d2.want), "+v"(d2.dur));
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
-    const bool ok = live && ((plo >> L.need) & 1u) != 0;
+    const bool ok = live && (plo & (uint32_t)L.mask) == (uint32_t)L.want;
     const int64_t tin = (int64_t)(p >> 3) + L.w;
     const int64_t st = tin > L.clock ? tin : L.clock;
     const int64_t fin = st + L.dur;

@@ -64,6 +64,10 @@ def test_workload1_all_candidates(gpu):
     (4, 3, 4, 14, 2), (5, 1, 7, 9, 2), (6, 2, 12, 15, 2), (8, 2, 16, 20, 2), (8, 4, 8, 40, 2),
     (7, 3, 14, 30, 1), (16, 2, 16, 40, 2), (16, 4, 4, 64, 1), (32, 2, 8, 70, 1),
     (12, 1, 24, 20, 2), (33, 1, 3, 40, 1), (64, 1, 2, 64, 1), (8, 8, 3, 64, 1),
+    # finish-table rows as rings of R = next power of two >= P v slots: M = R + 1, M not a
+    # multiple of R, non-power-of-two P, long wraps
+    (4, 1, 5, 8, 1), (4, 2, 9, 12, 1), (2, 2, 33, 8, 1), (3, 1, 40, 9, 2), (8, 2, 17, 20, 1),
+    (5, 2, 23, 14, 1), (2, 1, 64, 3, 1),
 ])
 def test_random_structures(gpu, P, v_max, M, L, pert):
     """Every policy, placement kind, v, ragged P / M, random moves (some cyclic) and invalid
