@@ -24,8 +24,7 @@ sys.path.insert(0, ROOT)
 PEAK_VALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 HBM_PEAK_GBS = 8000.0
 # simulation kernels, in launch order, between the library's measurement boundaries
-SIM_KERNELS = ["k_sim<2, true>", "k_sim<2, false>", "k_sim<1, true>", "k_sim<1, false>",
-               "k_sim<8, false>", "k_sim_mat<2>"]
+SIM_KERNELS = ["k_sim<2>", "k_sim<1>", "k_sim<8>", "k_afab", "k_sim_mat<2>"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_k_sim_workload3.json")
 
 
@@ -140,8 +139,8 @@ def main():
     int64_c, lane_c = algorithmic_work(recs_np, w.P, w.M)
     v, pol = recs_np[:, 1], recs_np[:, 0]
     # candidates each simulation kernel handles (no moves in this workload)
-    sets = [(v == 2) & (pol == 0), (v == 2) & (pol != 0), (v == 1) & (pol == 0),
-            (v == 1) & (pol != 0), v >= 3, np.zeros(n, dtype=bool)]
+    sets = [(v == 2) & (pol != 0), (v == 1) & (pol != 0), (v >= 3) & (pol != 0), pol == 0,
+            np.zeros(n, dtype=bool)]
     # the dominant kernel: the one that takes longest
     dom = int(np.argmax(per_kernel_ms))
     dom_ms = float(per_kernel_ms[dom])

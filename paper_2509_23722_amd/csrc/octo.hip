@@ -8,8 +8,10 @@
 //               sort key).
 //   k_plan      fine-bin start positions and per-bin counts.
 //   k_scatter   candidate indices grouped by fine bin (counting sort).
-//   k_sim       persistent waves; each takes a chunk of CPW candidates of one bin and simulates
-//               them together, queues generated in registers (the hot kernel).
+//   k_sim       persistent waves; each takes a chunk of CPW candidates of one INTER or MERGE
+//               bin and simulates them together, queues generated in registers (the hot
+//               kernel); finish tables with ring rows.
+//   k_afab      AFAB candidates, one lane each: a pass over the stage rows in chain order.
 //   k_sim_mat   candidates with perturbations: queues materialised in global memory, moved,
 //               then simulated.
 // octo_tune_step launches k_tune (one local-search step for every chain).
@@ -61,7 +63,7 @@ struct SimArgs {
   int rec_bytes;         // staged record bytes (header + boundaries + placement)
   int rec_stride;        // bytes between staged records of a wave
   int qcap;
-  int bin_lo, bin_hi;    // generated bins handled by this launch
+  uint64_t bin_mask;     // generated bins handled by this launch
   int work;              // chunk counter index of this launch
   int ring;              // slots per stage row of this launch's finish tables (R)
   uint64_t redo_bins;    // bins whose queues may exceed R in flight: sent to the 64-bit path
@@ -355,42 +357,41 @@ __global__ void k_scatter(SimArgs a, const uint16_t* __restrict__ bins,
   if (fine != BIN_NONE) idx[res[fine] + local] = (int32_t)i;
 }
 
-// Locate chunk `ch` (of CPW candidates) among generated bins [lo, hi); returns the bin or -1.
-__device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, int lo, int hi, int ch,
+// Locate chunk `ch` (of CPW candidates) among the generated bins in `mask`, in bin order;
+// returns the bin or -1. entry0: first entry of the chunk in its bin; pos0: the bin's first
+// position in the index array.
+__device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, uint64_t mask, int ch,
                                             int* entry0, int* pos0) {
   int acc = 0, base = 0;
-  for (int b = 0; b < lo; ++b) base += ctl[CTL_COUNTS + b];
-  for (int b = lo; b < hi; ++b) {
+  for (int b = 0; b < NBIN_GEN; ++b) {
     const int cnt = ctl[CTL_COUNTS + b];
-    const int nch = (cnt + CPW - 1) / CPW;
-    if (ch < acc + nch) {
-      *entry0 = (ch - acc) * CPW;
-      *pos0 = base;
-      return b;
+    if ((mask >> b) & 1) {
+      const int nch = (cnt + CPW - 1) / CPW;
+      if (ch < acc + nch) {
+        *entry0 = (ch - acc) * CPW;
+        *pos0 = base;
+        return b;
+      }
+      acc += nch;
     }
-    acc += nch;
     base += cnt;
   }
   return -1;
 }
 
-// ONLY_AFAB: the launch holds only AFAB bins (a smaller kernel).
-template <int VMAX, bool ONLY_AFAB>
+template <int VMAX>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
                                              int split, uint8_t* lds_wave) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
-  if (ONLY_AFAB || gen == GEN_AFAB) {
-    run_generated<VMAX, GEN_AFAB, false>(a, cand, v, split, lds_wave);
-  } else if constexpr (!ONLY_AFAB) {
-    if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_wave);
-    else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_wave);
-    else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_wave);
-  }
+  if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_wave);
+  else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_wave);
+  else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_wave);
 }
 
-// Generated-queue simulation for the bins [bin_lo, bin_hi) of one v class: VC = 1 (v = 1),
-// 2 (v = 2) or 8 (v = 3..8); finish tables sized for that class with a.ring slots per row.
-template <int VC, bool ONLY_AFAB>
+// Generated-queue simulation (INTER and MERGE) for the bins in a.bin_mask of one v class:
+// VC = 1 (v = 1), 2 (v = 2) or 8 (v = 3..8); finish tables sized for that class with a.ring
+// slots per row.
+template <int VC>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int g = lane_id() / a.G;
@@ -400,19 +401,121 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     if (lane_id() == 0) ch = atomicAdd(&a.ctl[a.work], 1);
     ch = bcast(ch);
     int entry0 = 0, pos0 = 0;
-    const int bin = locate_chunk(a.ctl, a.CPW, a.bin_lo, a.bin_hi, ch, &entry0, &pos0);
+    const int bin = locate_chunk(a.ctl, a.CPW, a.bin_mask, ch, &entry0, &pos0);
     if (bin < 0) break;
     int v, gen, split;
     bin_decode(bin, &v, &gen, &split);
     const int cnt = a.ctl[CTL_COUNTS + bin];
     const int e = entry0 + g;
     const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
-    if ((a.redo_bins >> bin) & 1) {
-      // this bin's queues may hold more than a.ring micro-batches in flight
+    if (gen == GEN_AFAB || ((a.redo_bins >> bin) & 1)) {
+      // queues that may hold more than a.ring micro-batches of a stage in flight
       if (cand >= 0 && d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
       continue;
     }
-    dispatch_gen<VC, ONLY_AFAB>(a, gen, cand, v, split, smem);
+    dispatch_gen<VC>(a, gen, cand, v, split, smem);
+  }
+}
+
+// GPipe (AFAB) queues without moves. Every device runs the forwards of its stages in ascending
+// stage order, each over m = 0..M-1, then the backwards in descending stage order. Visiting the
+// stage rows in chain order — forwards s = 0..S-1, then backwards s = S-1..0 — therefore meets
+// every device's ops in its queue order, and one row is one pass over m:
+//   fin(s, m) = dur(s) + max(fin(s, m-1), in(s, m)),  fin(s, -1) = the device's clock;
+//   in(s, m) = fin of micro-batch m in the row visited before (+ the link weight between the
+// two stages' devices); F(0, m) has no input, B(S-1, m) takes F(S-1, m) from its own device.
+// This is the earliest-start relaxation of the time model over the AFAB graph, in an order that
+// reaches every op after all its predecessors. One lane per candidate; the previous row lives in
+// LDS as M int64 per lane (lanes interleaved), device clocks and busy times after it.
+
+// One row: row[m] <- f = dur + max(f, row[m] + w) for m = 0..M-1 (stride = lanes); returns f.
+// Reads are issued eight at a time ahead of the dependent updates.
+__device__ __forceinline__ int64_t sweep_row(int64_t* row, int stride, int M, int64_t f,
+                                             int64_t w, int64_t dur) {
+  int m = 0;
+  for (; m + 8 <= M; m += 8) {
+    int64_t x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = row[(m + i) * stride];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t y = x[i] + w;
+      f = (y > f ? y : f) + dur;
+      x[i] = f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) row[(m + i) * stride] = x[i];
+  }
+  for (; m < M; ++m) {
+    const int64_t y = row[m * stride] + w;
+    f = (y > f ? y : f) + dur;
+    row[m * stride] = f;
+  }
+  return f;
+}
+
+__global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int lane = lane_id();
+  const int P = a.pr.P, M = a.pr.M, L = a.pr.L;
+  const int li = lane < lanes ? lane : 0;
+  int64_t* row = reinterpret_cast<int64_t*>(smem) + li;  // row[m * lanes]
+  int64_t* clk = row + (size_t)M * lanes;                // clk[d * lanes]
+  int64_t* bsy = clk + (size_t)P * lanes;                // bsy[d * lanes]
+  for (;;) {
+    int ch = 0;
+    if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
+    ch = bcast(ch);
+    int entry0 = 0, pos0 = 0;
+    const int bin = locate_chunk(a.ctl, lanes, a.bin_mask, ch, &entry0, &pos0);
+    if (bin < 0) break;
+    int v, gen, split;
+    bin_decode(bin, &v, &gen, &split);
+    const int e = entry0 + lane;
+    if (lane >= lanes || e >= a.ctl[CTL_COUNTS + bin]) continue;
+    const int64_t cand = a.idx[pos0 + e];
+    const uint8_t* rec = a.cands + cand * a.pr.stride;
+    const uint8_t* bnd = rec + 4;
+    const uint8_t* dev = rec + 3 + a.pr.s_max;
+    const int S = P * v;
+    for (int d = 0; d < P; ++d) clk[d * lanes] = 0, bsy[d * lanes] = 0;
+    // forwards
+    int dp = 0;
+    for (int s = 0; s < S; ++s) {
+      const int d = dev[s];
+      const int b0 = s > 0 ? bnd[s - 1] : 0, b1 = s < S - 1 ? bnd[s] : L;
+      const int64_t df = a.pre[3 * b1] - a.pre[3 * b0];
+      const int64_t db = a.pre[3 * b1 + 1] - a.pre[3 * b0 + 1] + a.pre[3 * b1 + 2] -
+                         a.pre[3 * b0 + 2];
+      bsy[d * lanes] += (df + db) * M;
+      int64_t f = clk[d * lanes];
+      if (s == 0) {
+        for (int m = 0; m < M; ++m) {
+          f += df;
+          row[m * lanes] = f;
+        }
+      } else {
+        f = sweep_row(row, lanes, M, f, dp != d ? a.link[dp * P + d] : 0, df);
+      }
+      clk[d * lanes] = f;
+      dp = d;
+    }
+    // backwards
+    int dn = dp;
+    for (int s = S - 1; s >= 0; --s) {
+      const int d = dev[s];
+      const int b0 = s > 0 ? bnd[s - 1] : 0, b1 = s < S - 1 ? bnd[s] : L;
+      const int64_t db = a.pre[3 * b1 + 1] - a.pre[3 * b0 + 1] + a.pre[3 * b1 + 2] -
+                         a.pre[3 * b0 + 2];
+      const int64_t f = sweep_row(row, lanes, M, clk[d * lanes], dn != d ? a.link[dn * P + d] : 0,
+                                  db);
+      clk[d * lanes] = f;
+      dn = d;
+    }
+    int64_t ms = 0;
+    for (int d = 0; d < P; ++d) ms = clk[d * lanes] > ms ? clk[d * lanes] : ms;
+    a.out_ms[cand] = ms;
+    for (int d = 0; d < P; ++d) a.out_bub[cand * P + d] = ms - bsy[d * lanes];
   }
 }
 
@@ -907,7 +1010,8 @@ void compute_inflight(const octo_problem* p, Workspace& ws) {
   for (int v = 1; v <= 2; ++v) {
     for (int split = 0; split <= 1; ++split) {
       int wi = 0, wm = 0;
-      for (int r = 0; r < P; ++r) wi = std::max(wi, inflight_inter(P, v, M, r, split, split ? r : 0));
+      for (int r = 0; r < P; ++r)
+        wi = std::max(wi, inflight_inter(P, v, M, r, split, split ? r : 0));
       const int S = P * v;
       for (int st = 0; st < S; ++st)
         wm = std::max(wm, inflight_inter(S, 1, M, st, split, split ? st : 0));
@@ -988,36 +1092,65 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.rec_bytes = pl.rec_bytes;
   a.rec_stride = pl.rec_stride;
   a.qcap = pl.qcap;
-  a.bin_lo = 0;
-  a.bin_hi = NBIN_GEN;
+  a.bin_mask = 0;
   a.work = CTL_WORK;
   a.ring = prob->M;
   a.redo_bins = 0;
   return a;
 }
 
-// Launch k_sim<VC, ONLY_AFAB> over generated bins [lo, hi) with its own 40-bit plan: s_cap
-// stages of ring_want (rounded up to a power of two, or M) slots; bins whose in-flight bound
-// exceeds the ring go to the 64-bit path. Nothing is launched for bins without candidates.
-template <int VC, bool ONLY_AFAB>
+// Bits of the generated bins of v in [v_lo, v_hi], without AFAB (AFAB: only AFAB).
+uint64_t bins_of(int v_lo, int v_hi, bool afab) {
+  uint64_t m = 0;
+  for (int v = v_lo; v <= v_hi; ++v)
+    for (int b = first_bin(v); b < first_bin(v) + 5; ++b)
+      if ((b == bin_of(v, GEN_AFAB, 0)) == afab) m |= 1ull << b;
+  return m;
+}
+
+// Launch k_sim<VC> over the generated bins in `mask` with its own 40-bit plan: s_cap stages of
+// ring_want (rounded up to a power of two, or M) slots; bins whose in-flight bound exceeds the
+// ring go to the 64-bit path.
+template <int VC>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-               int64_t n, int64_t* ms, int64_t* bub, int s_cap, int ring_want, int lo, int hi,
+               int64_t n, int64_t* ms, int64_t* bub, int s_cap, int ring_want, uint64_t mask,
                int work, hipStream_t stream) {
   const Ring ring = make_ring(s_cap, prob->M, ring_want);
   const Plan pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R);
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub);
-  a.bin_lo = lo, a.bin_hi = hi, a.work = work;
+  a.bin_mask = mask, a.work = work;
   a.ring = ring.R;
   a.redo_bins = 0;
-  for (int b = lo; b < hi; ++b)
-    if (ring.R < prob->M && su.ws->inflight[b] > ring.R) a.redo_bins |= 1ull << b;
+  for (int b = 0; b < NBIN_GEN; ++b)
+    if (((mask >> b) & 1) && ring.R < prob->M && su.ws->inflight[b] > ring.R)
+      a.redo_bins |= 1ull << b;
   int grid = 0;
-  int rc = occupancy_grid(k_sim<VC, ONLY_AFAB>, pl.lds_bytes, su.di.cus, &grid);
+  int rc = occupancy_grid(k_sim<VC>, pl.lds_bytes, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  hipLaunchKernelGGL((k_sim<VC, ONLY_AFAB>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
+  hipLaunchKernelGGL(k_sim<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
+  return launch_ok();
+}
+
+// Launch k_afab over the AFAB bins of every v: one lane per candidate, each lane's row of M
+// int64 plus 2 P device words in LDS (at most 64 KiB per wave).
+int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
+                int64_t n, int64_t* ms, int64_t* bub, hipStream_t stream) {
+  const size_t per_lane = (size_t)(prob->M + 2 * prob->P) * 8;
+  const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
+  const int lds = (int)(lanes * per_lane);
+  if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
+  SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
+  a.bin_mask = bins_of(1, prob->v_max, true);
+  a.work = CTL_WORK + 3;
+  int grid = 0;
+  int rc = occupancy_grid(k_afab, lds, su.di.cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (n + lanes - 1) / lanes;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+  hipLaunchKernelGGL(k_afab, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   return launch_ok();
 }
 
@@ -1095,44 +1228,35 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
                      reinterpret_cast<int32_t*>(base + su.l.idx));
   if ((rc = launch_ok())) return rc;
-  // generated queues, launches per v class with finish tables sized for it: v = 2 AFAB, then
-  // v = 2 other generators (ring rows), v = 1 likewise, then v = 3..8; then materialised queues
-  // (perturbations, 64-bit redo).
+  // generated INTER / MERGE queues, one launch per v class with finish tables sized for it:
+  // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
+  // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
   const int P = prob->P, M = prob->M;
-  const int b2 = first_bin(2), b1 = first_bin(1);
   if ((rc = record_mark(0, stream))) return rc;
-  if (prob->v_max >= 2) {
-    if ((rc = launch_sim<2, true>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P,
-                                  M, b2, b2 + 1, CTL_WORK + 3, stream)))
-      return rc;
-    if ((rc = record_mark(1, stream))) return rc;
-    if ((rc = launch_sim<2, false>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P,
-                                   2 * P, b2 + 1, b1, CTL_WORK + 1, stream)))
-      return rc;
-  } else if ((rc = record_mark(1, stream))) {
+  if (prob->v_max >= 2 &&
+      (rc = launch_sim<2>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P, 2 * P,
+                          bins_of(2, 2, false), CTL_WORK + 1, stream)))
     return rc;
-  }
+  if ((rc = record_mark(1, stream))) return rc;
+  if ((rc = launch_sim<1>(prob, su, link, candidates, n, out_makespan, out_bubble, P, P,
+                          bins_of(1, 1, false), CTL_WORK + 0, stream)))
+    return rc;
   if ((rc = record_mark(2, stream))) return rc;
-  if ((rc = launch_sim<1, true>(prob, su, link, candidates, n, out_makespan, out_bubble, P, M, b1,
-                                b1 + 1, CTL_WORK + 4, stream)))
+  if (prob->v_max >= 3 &&
+      (rc = launch_sim<8>(prob, su, link, candidates, n, out_makespan, out_bubble,
+                          P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if ((rc = launch_sim<1, false>(prob, su, link, candidates, n, out_makespan, out_bubble, P, P,
-                                 b1 + 1, NBIN_GEN, CTL_WORK + 0, stream)))
+  if ((rc = launch_afab(prob, su, link, candidates, n, out_makespan, out_bubble, stream)))
     return rc;
   if ((rc = record_mark(4, stream))) return rc;
-  if (prob->v_max >= 3 &&
-      (rc = launch_sim<8, false>(prob, su, link, candidates, n, out_makespan, out_bubble,
-                                 P * prob->v_max, M, 0, b2, CTL_WORK + 2, stream)))
-    return rc;
-  if ((rc = record_mark(5, stream))) return rc;
   if (prob->v_max <= 2)
     hipLaunchKernelGGL(k_sim_mat<2>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
   else
     hipLaunchKernelGGL(k_sim_mat<8>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
   if ((rc = launch_ok())) return rc;
-  return record_mark(6, stream);
+  return record_mark(5, stream);
 }
 
 int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
