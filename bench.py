@@ -25,7 +25,7 @@ PEAK_VALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 HBM_PEAK_GBS = 8000.0
 # simulation kernels, in launch order, between the library's measurement boundaries
 SIM_KERNELS = ["k_sim<2>", "k_sim<1>", "k_sim<8>", "k_afab", "k_sim_mat<2>"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_k_sim_workload3.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_nemotron-h-like-52L-P8-M64.json")
 
 
 def kernel_source_hash():

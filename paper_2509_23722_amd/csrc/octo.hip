@@ -4,10 +4,9 @@
 //   k_prep      layer-cost prefix sums; clears the bin counters.
 //   k_merge_tab ideal stage-level start times for the MERGE order (cached per (P, v_max, M)).
 //   k_classify  one thread per candidate: validate, resolve the queue generator, write the
-//               sentinel of invalid candidates, count candidates per fine bin (work bin and
-//               sort key).
-//   k_plan      fine-bin start positions and per-bin counts.
-//   k_scatter   candidate indices grouped by fine bin (counting sort).
+//               sentinel of invalid candidates, count candidates per work bin.
+//   k_plan      start position of each bin.
+//   k_scatter   candidate indices grouped by bin (counting sort).
 //   k_sim       persistent waves; each takes a chunk of CPW candidates of one INTER or MERGE
 //               bin and simulates them together, queues generated in registers (the hot
 //               kernel); finish tables with ring rows.
@@ -38,10 +37,8 @@ constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (5)
 constexpr int CTL_WORK_MAT = 136; // chunk counter of k_sim_mat, perturbed list
 constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
 constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
-constexpr int CTL_FINE = 256;     // [NFINE] candidates per fine bin
-constexpr int CTL_FPOS = 256 + 672; // [NFINE] next index position of each fine bin
-constexpr int CTL_WORDS = CTL_FPOS + 672;
-static_assert(NFINE <= 672, "fine-bin counters overlap");
+constexpr int CTL_POS = 64;       // [NBINS] next index position of each bin (scatter cursor)
+constexpr int CTL_WORDS = 256;
 
 struct SimArgs {
   Problem pr;
@@ -282,79 +279,55 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   relax<1>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
 }
 
-// One thread per candidate; dynamic LDS: P ints per thread for the AFAB round count.
-__global__ void k_classify(SimArgs a, uint16_t* __restrict__ bins) {
-  extern __shared__ int fr[];
-  __shared__ int hist[NFINE];
-  for (int i = threadIdx.x; i < NFINE; i += blockDim.x) hist[i] = 0;
+// One thread per candidate.
+__global__ void k_classify(SimArgs a, uint8_t* __restrict__ bins) {
+  __shared__ int hist[NBINS];
+  for (int i = threadIdx.x; i < NBINS; i += blockDim.x) hist[i] = 0;
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < a.n) {
     const uint8_t* rec = a.cands + i * a.pr.stride;
     Resolved r = resolve_record(a.pr, rec);
-    int fine = BIN_NONE;
+    int bin = BIN_NONE;
     if (!r.valid) {
       a.out_ms[i] = OCTO_MS_INVALID;
       for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
-    } else if (r.n_pert > 0) {
-      fine = BIN_MAT * NSUB;
     } else {
-      int key = 0;
-      if (r.gen == GEN_AFAB && r.v >= 2)
-        key = round_key(afab_rounds(rec + 3 + a.pr.s_max, a.pr.P, r.S, a.pr.M, fr + threadIdx.x,
-                                    blockDim.x),
-                        r.v, a.pr.M);
-      fine = bin_of(r.v, r.gen, r.split) * NSUB + key;
+      bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
+      atomicAdd(&hist[bin], 1);
     }
-    if (fine != BIN_NONE) atomicAdd(&hist[fine], 1);
-    bins[i] = (uint16_t)fine;
+    bins[i] = (uint8_t)bin;
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < NFINE; b += blockDim.x)
-    if (hist[b]) atomicAdd(&a.ctl[CTL_FINE + b], hist[b]);
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
+    if (hist[b]) atomicAdd(&a.ctl[CTL_COUNTS + b], hist[b]);
 }
 
-// One block of PLAN_THREADS: fine-bin start positions (exclusive prefix sum) and bin counts.
-constexpr int PLAN_THREADS = 1024;
-static_assert(NFINE <= PLAN_THREADS, "one fine bin per thread");
-__global__ void __launch_bounds__(PLAN_THREADS) k_plan(int32_t* __restrict__ ctl) {
-  __shared__ int buf[2][PLAN_THREADS];
-  const int t = threadIdx.x;
-  const int c = t < NFINE ? ctl[CTL_FINE + t] : 0;
-  buf[0][t] = c;
-  __syncthreads();
-  int src = 0;
-  for (int off = 1; off < PLAN_THREADS; off <<= 1) {
-    const int x = buf[src][t] + (t >= off ? buf[src][t - off] : 0);
-    buf[src ^ 1][t] = x;
-    src ^= 1;
-    __syncthreads();
-  }
-  if (t < NFINE) ctl[CTL_FPOS + t] = buf[src][t] - c;
-  if (t < NBINS) {
-    int sum = 0;
-    for (int k = 0; k < NSUB; ++k) sum += ctl[CTL_FINE + t * NSUB + k];
-    ctl[CTL_COUNTS + t] = sum;
+// One wave: start position of every bin in the index array (exclusive prefix sum).
+__global__ void k_plan(int32_t* __restrict__ ctl) {
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int b = 0; b < NBINS; ++b) ctl[CTL_POS + b] = acc, acc += ctl[CTL_COUNTS + b];
   }
 }
 
-__global__ void k_scatter(SimArgs a, const uint16_t* __restrict__ bins,
+__global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
                           int32_t* __restrict__ idx) {
-  __shared__ int hist[NFINE];
-  __shared__ int res[NFINE];
-  for (int b = threadIdx.x; b < NFINE; b += blockDim.x) hist[b] = 0;
+  __shared__ int hist[NBINS];
+  __shared__ int res[NBINS];
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x) hist[b] = 0;
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int fine = BIN_NONE, local = 0;
+  int bin = BIN_NONE, local = 0;
   if (i < a.n) {
-    fine = bins[i];
-    if (fine != BIN_NONE) local = atomicAdd(&hist[fine], 1);
+    bin = bins[i];
+    if (bin != BIN_NONE) local = atomicAdd(&hist[bin], 1);
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < NFINE; b += blockDim.x)
-    res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_FPOS + b], hist[b]) : 0;
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
+    res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_POS + b], hist[b]) : 0;
   __syncthreads();
-  if (fine != BIN_NONE) idx[res[fine] + local] = (int32_t)i;
+  if (bin != BIN_NONE) idx[res[bin] + local] = (int32_t)i;
 }
 
 // Locate chunk `ch` (of CPW candidates) among the generated bins in `mask`, in bin order;
@@ -915,7 +888,7 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   l.pre = o;
   o = align_up(o + (size_t)(p->L + 1) * 3 * 8, 256);
   l.bin_of = o;
-  o = align_up(o + (size_t)n * 2, 256);
+  o = align_up(o + (size_t)n, 256);
   l.idx = o;
   o = align_up(o + (size_t)n * 4, 256);
   l.redo = o;
@@ -1215,15 +1188,12 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   if (rc) return rc;
   char* base = static_cast<char*>(su.ws->base);
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
-  const int tb = 128;
+  const int tb = 256;
   const int nb = (int)((n + tb - 1) / tb);
-  uint16_t* bins = reinterpret_cast<uint16_t*>(base + su.l.bin_of);
-  const int cls_lds = tb * prob->P * (int)sizeof(int);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, cls_lds);
-  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), cls_lds, stream, a, bins);
+  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
+  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), 0, stream, a, bins);
   if ((rc = launch_ok())) return rc;
-  hipLaunchKernelGGL(k_plan, dim3(1), dim3(PLAN_THREADS), 0, stream, a.ctl);
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, a.ctl);
   if ((rc = launch_ok())) return rc;
   hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
                      reinterpret_cast<int32_t*>(base + su.l.idx));

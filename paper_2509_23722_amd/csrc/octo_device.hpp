@@ -19,18 +19,12 @@ constexpr int POL_AFAB = 0, POL_1F1B = 1, POL_I1F1B = 2, POL_ZB = 3;
 constexpr int GEN_AFAB = 0, GEN_INTER = 1, GEN_MERGE = 2, GEN_MAT = 3;
 
 // Work bins. Generated queues are binned by (v, generator) so that the lanes of a wave run one
-// code path; bins are numbered heaviest first (large v first; within one v: AFAB, whose round
-// counts spread widest, then split backward, then fused).
+// code path; bins are numbered heaviest first (large v first; within one v: AFAB, then split
+// backward, then fused).
 constexpr int NBIN_GEN = 40;          // (8 - v) * 5 + rank, v = 1..8
 constexpr int BIN_MAT = 40;           // candidates with perturbations: queues materialised
 constexpr int NBINS = 41;
-constexpr int BIN_NONE = 0xFFFF;      // invalid: sentinel already written
-// Within a bin, candidates are ordered by a sort key (NSUB levels, heaviest first) so that the
-// candidates sharing a wave need similar numbers of rounds. The counting sort runs over fine
-// bins bin * NSUB + key.
-constexpr int NSUB = 16;
-constexpr int NFINE = NBINS * NSUB;
-
+constexpr int BIN_NONE = 0xFF;        // invalid: sentinel already written
 // rank of a generator within one v: 0 AFAB, 1 MERGE split, 2 INTER split, 3 MERGE fused,
 // 4 INTER fused
 __host__ __device__ __forceinline__ int bin_of(int v, int gen, int split) {
@@ -43,40 +37,6 @@ __host__ __device__ __forceinline__ void bin_decode(int bin, int* v, int* gen, i
   int r = bin % 5;
   *gen = r == 0 ? GEN_AFAB : (r == 2 || r == 4) ? GEN_INTER : GEN_MERGE;
   *split = (r == 1 || r == 2);
-}
-
-// Number of lockstep rounds an AFAB candidate without moves needs (one op per device per round;
-// an op runs in the round after its last predecessor finished). Each stage's M forwards (and
-// later its M backwards) then run in consecutive rounds, so one pass over the stages in chain
-// order — forwards ascending, backwards descending — with the round at which every device
-// becomes free gives the exact count. fr: per-device scratch, P entries `stride` apart.
-__device__ __forceinline__ int afab_rounds(const uint8_t* dev, int P, int S, int M, int* fr,
-                                           int stride) {
-  for (int d = 0; d < P; ++d) fr[d * stride] = 0;
-  int prev = 0, last = 0;
-  for (int s = 0; s < S; ++s) {
-    int* f = fr + dev[s] * stride;
-    const int b = (*f > prev ? *f : prev) + 1;
-    *f = b + M - 1;
-    prev = b;
-  }
-  for (int s = S - 1; s >= 0; --s) {
-    int* f = fr + dev[s] * stride;
-    const int b = (*f > prev ? *f : prev) + 1;
-    *f = b + M - 1;
-    prev = b;
-    last = *f > last ? *f : last;
-  }
-  return last;
-}
-
-// Sort key of a round count relative to the 2 v M rounds every device needs at least:
-// eight levels per doubling, largest first.
-__device__ __forceinline__ int round_key(int rounds, int v, int M) {
-  const float x = (float)rounds / (float)(2 * v * M);
-  int k = x > 1.0f ? (int)(8.0f * __log2f(x)) : 0;
-  k = k < 0 ? 0 : k > NSUB - 1 ? NSUB - 1 : k;
-  return NSUB - 1 - k;
 }
 
 __host__ __device__ __forceinline__ int pert_off(int s_max) { return (3 + 2 * s_max + 1) & ~1; }
