@@ -187,19 +187,19 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     GenAfab g;
     g.init(v, M);
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   } else if constexpr (GEN == GEN_INTER) {
     const int r = c.st[0];
     if constexpr (P2) {
       GenInterP2 g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     } else {
       GenInter g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     }
   } else {
     GenMerge<VMAX> g;
@@ -207,7 +207,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
            [&](int k) { return pick<VMAX>(c.st, k); });
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   }
 
   const int64_t ms = group_max(L.clock, G);
@@ -276,7 +276,7 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   g.init(S, 1, M, d < S ? d : 0, split, split ? d : 0);
   describe<1>(L, c, ring, g.kind, g.k, g.m);
   bool dead = false;
-  relax<1>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
+  relax<1, true>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
 }
 
 // One thread per candidate.
@@ -603,7 +603,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       q.init(row, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
       bool dead = false;
-      relax<VMAX>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, true>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       const int64_t ms = group_max(L.clock, G);
       if (mine) {
         if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
@@ -738,7 +738,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     q.init(row, L.nops);
     describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
     bool dead = false;
-    relax<VMAX>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, true>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     const int64_t ms = group_max(L.clock, G);
 
     if (!has || skip) continue;

@@ -176,7 +176,11 @@ __device__ __forceinline__ uint64_t fold_groups(uint64_t x, int G, uint64_t lsb)
 // Run the rounds until every candidate of the wave is done or deadlocked.
 // gbit: this lane's group bit in folded masks; lsb: all group bits. rec (nullable): ideal-start
 // recording for the MERGE table, rec[pos] = start << 16 | kind << 12 | m.
-template <int VMAX, class Tab, class Gen>
+// SPEC: compute the next op and its descriptor while the slot read is in flight and keep them
+// only if this op completes (pays when one wave per SIMD must hide the LDS latency itself);
+// otherwise advance and describe after the readiness test (fewer instructions per round, the
+// latency hidden by other waves).
+template <int VMAX, bool SPEC, class Tab, class Gen>
 __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
                                       const Tab& T, int G, uint64_t gbit, uint64_t lsb,
                                       bool& dead, uint32_t* rec) {
@@ -184,13 +188,15 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
   for (;;) {
     uint32_t plo, phi;
     T.issue(live ? L.rd : 0, plo, phi);
-    // the next op, computed while the read is in flight; kept only if this op completes
     Gen g2 = gen;
-    g2.advance(true);
     Desc d2;
-    describe<VMAX>(d2, c, ring, g2.kind, g2.k, g2.m);
-    // the slot is consumed only after the next op's descriptor exists
-    __asm__ volatile("" : "+v"(plo), "+v"(phi), "+v"(d2.rd), "+v"(d2.want), "+v"(d2.dur));
+    if constexpr (SPEC) {
+      // the next op, computed while the read is in flight; kept only if this op completes
+      g2.advance(true);
+      describe<VMAX>(d2, c, ring, g2.kind, g2.k, g2.m);
+      // the slot is consumed only after the next op's descriptor exists
+      __asm__ volatile("" : "+v"(plo), "+v"(phi), "+v"(d2.rd), "+v"(d2.want), "+v"(d2.dur));
+    }
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
     const bool ok = live && (plo & (uint32_t)L.mask) == (uint32_t)L.want;
     const int64_t tin = (int64_t)(p >> 3) + L.w;
@@ -202,8 +208,13 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
     L.clock = ok ? fin : L.clock;
     L.pos += ok ? 1 : 0;
     live = L.pos < L.nops;
-    gen.take_if(ok, g2);
-    L.take_if(ok, d2);
+    if constexpr (SPEC) {
+      gen.take_if(ok, g2);
+      L.take_if(ok, d2);
+    } else {
+      gen.advance(ok);
+      describe<VMAX>(L, c, ring, gen.kind, gen.k, gen.m);
+    }
     __asm__ volatile("" ::: "memory");
     if (__ballot(ok) == 0) {
       const uint64_t actm = __ballot(live);
