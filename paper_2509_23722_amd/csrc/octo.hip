@@ -64,6 +64,11 @@ struct SimArgs {
   int work;              // chunk counter index of this launch
   int ring;              // slots per stage row of this launch's finish tables (R)
   uint64_t redo_bins;    // bins whose queues may exceed R in flight: sent to the 64-bit path
+  // queue tables (v <= 2), entry offsets of each block's first row; null: generate in-kernel
+  const uint32_t* qtab;
+  int64_t qt_inter[2][2];  // [v - 1][split], one row per rank
+  int64_t qt_merge[2];     // [split], v = 2, one row per stage pair s0 < s1
+  int strm_off;            // LDS byte offset of the per-lane stream table
 };
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
@@ -77,7 +82,7 @@ template <int VMAX>
 __device__ __forceinline__ void zero_chunks(Chunks<VMAX>& c) {
 #pragma unroll
   for (int k = 0; k < VMAX; ++k) {
-    c.st[k] = 0, c.base[k] = 0, c.first[k] = 0, c.fmask[k] = 0, c.brow[k] = 0, c.bmask[k] = 0;
+    c.st[k] = 0, c.base[k] = 0, c.frow[k] = 0, c.fmask[k] = 0, c.brow[k] = 0, c.bmask[k] = 0;
     c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
   }
 }
@@ -112,7 +117,7 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       const int64_t bi = pre[3 * b1 + 1] - pre[3 * b0 + 1];
       const int64_t wg = pre[3 * b1 + 2] - pre[3 * b0 + 2];
       c.base[k] = s * ring.R;
-      c.first[k] = s == 0;
+      c.frow[k] = s > 0 ? -ring.R : 0;
       c.fmask[k] = s > 0 ? (int)(ST_F | ST_PAR) : 0;
       c.brow[k] = s < S - 1 ? ring.R : 0;  // the last stage reads its own F
       c.bmask[k] = (int)((s < S - 1 ? ST_B : ST_F) | ST_PAR);
@@ -159,7 +164,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
   const bool has = cand >= 0;
   const int S = P * v;
-  const Ring ring = make_ring(S, M, a.ring);
+  const Ring ring = make_ring(M, a.ring);
   if (has) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
   __asm__ volatile("" ::: "memory");
 
@@ -177,7 +182,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     zero_chunks<VMAX>(c);
   }
   __asm__ volatile("" ::: "memory");
-  T.clear_all(ring.zero + 1, lane_id(), WAVE);
+  T.clear_all(S * ring.R, lane_id(), WAVE);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
@@ -222,6 +227,82 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   }
 }
 
+// Row of the queue table that holds device d's queue (v <= 2): INTER by the device's first
+// stage (its rank), MERGE by its stage pair.
+template <int VMAX>
+__device__ __forceinline__ const uint32_t* qt_row(const SimArgs& a, int gen, int v, int split,
+                                                  const Chunks<VMAX>& c) {
+  const int M = a.pr.M, S = a.pr.P * v;
+  const int64_t n = (int64_t)(split ? 3 : 2) * v * M;
+  if (gen == GEN_INTER) return a.qtab + a.qt_inter[v - 1][split] + c.st[0] * n;
+  const int s0 = c.st[0], s1 = pick<VMAX>(c.st, 1);
+  const int64_t pair = (int64_t)s0 * (2 * S - s0 - 1) / 2 + (s1 - s0 - 1);
+  return a.qtab + a.qt_merge[split] + pair * n;
+}
+
+// Table-driven simulation of one candidate per group (INTER or MERGE at v <= 2). Durations and
+// weights must fit 32 bits; a candidate with a larger one, or whose times pass the 40-bit
+// slots, is recomputed on the 64-bit path.
+template <int VMAX>
+__device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, int gen,
+                                        int split, uint8_t* lds_wave) {
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  const Table40 T{reinterpret_cast<uint32_t*>(lds_wave),
+                  lds_wave + (size_t)a.slots * a.CPW * 4, __ffs(a.CPW) - 1, g < a.CPW ? g : 0};
+  uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
+  uint2* strm = reinterpret_cast<uint2*>(lds_wave + a.strm_off) + lane_id();
+  const bool has = cand >= 0;
+  const int S = P * v;
+  const Ring ring = make_ring(M, a.ring);
+  if (has) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
+  __asm__ volatile("" ::: "memory");
+
+  Chunks<VMAX> c;
+  int64_t busy = 0;
+  int nops = 0;
+  bool fits = true;
+  const bool mine = has && d < P;
+  if (mine) {
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
+    nops = (split ? 3 : 2) * v * M;
+    for (int e = 0; e < 3 * v; ++e) {
+      const int kind = e / v, k = e - kind * v;
+      const int64_t w = kind == KF ? pick<VMAX>(c.wF, k) : kind == KB ? pick<VMAX>(c.wB, k) : 0;
+      const int64_t du = kind == KF   ? pick<VMAX>(c.dF, k)
+                         : kind == KB ? pick<VMAX>(c.dB, k)
+                                      : pick<VMAX>(c.dW, k);
+      fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
+      strm[e * 64] = make_uint2((uint32_t)w, (uint32_t)du);
+    }
+  } else {
+    zero_chunks<VMAX>(c);
+  }
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  const bool wide = (fold_groups(__ballot(!fits), G, lsb) & gbit) != 0;
+  if (wide) nops = 0;
+  const uint32_t* qrow = mine ? qt_row<VMAX>(a, gen, v, split, c) : a.qtab;
+  __asm__ volatile("" ::: "memory");
+  T.clear_all(S * ring.R, lane_id(), WAVE);
+  __asm__ volatile("" ::: "memory");
+
+  bool dead = false;
+  int64_t clock = 0;
+  relax_tab(qrow, nops, ring, strm, clock, T, G, gbit, lsb, dead);
+
+  const int64_t ms = group_max(clock, G);
+  if (mine) {
+    if (wide || ms >= Table40::LIMIT) {
+      if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+    } else {
+      if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
+      a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------------------------
@@ -254,14 +335,14 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   const Table64 T{reinterpret_cast<int64_t*>(smem)};
   const int rowlen = (split ? 3 : 2) * M;
   uint32_t* tab = mtab + merge_offset(P, M, v, split);
-  const Ring ring = make_ring(S, M, M);
-  T.clear(ring.zero + 1, d, WAVE);
+  const Ring ring = make_ring(M, M);
+  T.clear(S * M, d, WAVE);
   __asm__ volatile("" ::: "memory");
   Chunks<1> c;
   zero_chunks<1>(c);
   c.st[0] = d;
   c.base[0] = d * M;
-  c.first[0] = d == 0;
+  c.frow[0] = d > 0 ? -M : 0;
   c.fmask[0] = d > 0 ? (int)(ST_F | ST_PAR) : 0;
   c.brow[0] = d < S - 1 ? M : 0;
   c.bmask[0] = (int)((d < S - 1 ? ST_B : ST_F) | ST_PAR);
@@ -277,6 +358,41 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   describe<1>(L, c, ring, g.kind, g.k, g.m);
   bool dead = false;
   relax<1, true>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
+}
+
+// Queue-table rows of the interleaved order (v <= 2): thread r writes rank r's queue; chunk k
+// of rank r is stage r + k P.
+__global__ void k_qtab_inter(uint32_t* __restrict__ out, int P, int v, int M, int split) {
+  const int r = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (r >= P) return;
+  const int n = (split ? 3 : 2) * v * M, S = P * v;
+  uint32_t* row = out + (int64_t)r * n;
+  GenInter g;
+  g.init(P, v, M, r, split, split ? r : 0);
+  for (int i = 0; i < n; ++i) {
+    row[i] = qt_entry(g.kind, g.k, g.m, v, r + g.k * P, S);
+    g.advance(true);
+  }
+}
+
+// Queue-table rows of the MERGE order at v = 2: thread i writes the queue of stage pair i
+// (pairs s0 < s1 in lexicographic order).
+__global__ void k_qtab_merge(uint32_t* __restrict__ out, const uint32_t* __restrict__ mtab, int P,
+                             int M, int split) {
+  const int S = 2 * P;
+  const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (i >= S * (S - 1) / 2) return;
+  int s0 = 0, rem = i;
+  while (rem >= S - 1 - s0) rem -= S - 1 - s0, ++s0;
+  const int s1 = s0 + 1 + rem;
+  const int rowlen = (split ? 3 : 2) * M, n = 2 * rowlen;
+  uint32_t* row = out + (int64_t)i * n;
+  GenMerge<2> g;
+  g.init(mtab + merge_offset(P, M, 2, split), rowlen, 2, [&](int k) { return k == 0 ? s0 : s1; });
+  for (int j = 0; j < n; ++j) {
+    row[j] = qt_entry(g.kind, g.k, g.m, 2, g.k == 0 ? s0 : s1, S);
+    g.advance(true);
+  }
 }
 
 // One thread per candidate.
@@ -385,6 +501,12 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
       // queues that may hold more than a.ring micro-batches of a stage in flight
       if (cand >= 0 && d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
       continue;
+    }
+    if constexpr (VC <= 2) {
+      if (a.qtab) {
+        run_tab<VC>(a, cand, v, gen, split, smem);
+        continue;
+      }
     }
     dispatch_gen<VC>(a, gen, cand, v, split, smem);
   }
@@ -577,7 +699,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
         gen = r.gen;
       }
       const int S = P * v;
-      const Ring ring = make_ring(S, M, M);
+      const Ring ring = make_ring(M, M);
       Chunks<VMAX> c;
       int64_t busy = 0;
       Lane L;
@@ -597,7 +719,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       } else {
         zero_chunks<VMAX>(c);
       }
-      if (has) T.clear(ring.zero + 1, d, G);
+      if (has) T.clear(S * M, d, G);
       __asm__ volatile("" ::: "memory");
       GenMat q;
       q.init(row, L.nops);
@@ -672,7 +794,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     }
     const int S = P * v;
     const int qlen = (split ? 3 : 2) * v * M;
-    const Ring ring = make_ring(S, M, M);
+    const Ring ring = make_ring(M, M);
 
     // propose (step >= 1); the move is applied to the staged record / this chain's queue row
     int kind = -1, mi = 0, sd = -1;
@@ -732,7 +854,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     } else {
       zero_chunks<VMAX>(c);
     }
-    if (run) T.clear(ring.zero + 1, d, G);
+    if (run) T.clear(S * M, d, G);
     __asm__ volatile("" ::: "memory");
     GenMat q;
     q.init(row, L.nops);
@@ -784,6 +906,12 @@ struct Workspace {
   // largest number of micro-batches in flight per stage, per generated bin of v = 1, 2
   int inflight[NBIN_GEN] = {};
   int if_P = 0, if_M = 0;
+  // queue tables for v <= 2 (INTER by rank, MERGE by stage pair), same cache key as mt
+  void* qt = nullptr;
+  size_t qt_bytes = 0;
+  bool qt_valid = false;
+  int qt_P = 0, qt_vmax = 0, qt_M = 0;
+  int64_t qt_inter[2][2] = {}, qt_merge[2] = {};
 };
 
 std::mutex g_mu;
@@ -830,6 +958,7 @@ int dev_info(int dev, DevInfo* out) {
 
 struct Plan {
   int G, CPW, slots, table_bytes, rec_bytes, rec_stride, group_bytes, lds_bytes, qcap;
+  int strm_off;  // table-driven plans: per-lane stream table after the finish tables
 };
 
 int lanes_per_candidate(int P) {
@@ -840,18 +969,20 @@ int lanes_per_candidate(int P) {
 
 // 40-bit-slot plan for generated queues with up to s_cap stages; the staged record shares the
 // table's memory.
-// s_cap stages of R slots plus the zero slot.
-Plan fast_plan(const octo_problem* p, int lds_max, int s_cap, int R) {
+// s_cap stages of R slots; streams > 0: a per-lane table of that many {w, dur} pairs.
+Plan fast_plan(const octo_problem* p, int lds_max, int s_cap, int R, int streams) {
   Plan pl;
   pl.G = lanes_per_candidate(p->P);
-  pl.slots = s_cap * R + 1;
+  pl.slots = s_cap * R;
   pl.rec_bytes = pert_off(p->P * p->v_max);
   pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
   pl.table_bytes = (int)(pl.slots * 4 + pl.slots);
   pl.group_bytes = (int)align_up(std::max<size_t>(pl.table_bytes, pl.rec_stride), 16);
-  pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
+  const int strm = streams * WAVE * 8;
+  pl.CPW = std::min(WAVE / pl.G, (lds_max - strm) / pl.group_bytes);
   while (pl.CPW & (pl.CPW - 1)) pl.CPW &= pl.CPW - 1;  // interleaving uses shifts
-  pl.lds_bytes = pl.CPW * pl.group_bytes;
+  pl.strm_off = (int)align_up((size_t)pl.CPW * pl.group_bytes, 16);
+  pl.lds_bytes = streams > 0 ? pl.strm_off + strm : pl.CPW * pl.group_bytes;
   pl.qcap = 3 * p->v_max * p->M;
   return pl;
 }
@@ -863,10 +994,11 @@ Plan big_plan(const octo_problem* p, int lds_max) {
   pl.slots = p->P * p->v_max * p->M;
   pl.rec_bytes = pert_off(p->P * p->v_max);
   pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
-  pl.table_bytes = (int)align_up((size_t)(pl.slots + 1) * 8, 16);  // + the zero slot
+  pl.table_bytes = (int)align_up((size_t)pl.slots * 8, 16);
   pl.group_bytes = pl.table_bytes + (int)align_up(pl.rec_bytes, 16);
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
   pl.lds_bytes = pl.CPW * pl.group_bytes;
+  pl.strm_off = 0;
   pl.qcap = 3 * p->v_max * p->M;
   return pl;
 }
@@ -995,6 +1127,44 @@ void compute_inflight(const octo_problem* p, Workspace& ws) {
   ws.if_P = P, ws.if_M = M;
 }
 
+// Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), rebuilt when
+// (P, v_max, M) changes or the MERGE tables were rebuilt. Entry offsets are kept in the
+// workspace.
+int build_qtab(const octo_problem* p, Workspace& ws, hipStream_t stream) {
+  if (ws.qt_valid && ws.qt_P == p->P && ws.qt_vmax == p->v_max && ws.qt_M == p->M)
+    return OCTO_OK;
+  const int P = p->P, M = p->M, vmax2 = std::min(p->v_max, 2);
+  int64_t off = 0;
+  for (int v = 1; v <= vmax2; ++v)
+    for (int split = 0; split <= 1; ++split) {
+      ws.qt_inter[v - 1][split] = off;
+      off += (int64_t)P * (split ? 3 : 2) * v * M;
+    }
+  const int S2 = 2 * P;
+  const int64_t pairs = (int64_t)S2 * (S2 - 1) / 2;
+  for (int split = 0; split <= 1; ++split) {
+    ws.qt_merge[split] = off;
+    if (vmax2 >= 2) off += pairs * (split ? 3 : 2) * 2 * M;
+  }
+  ws.qt_valid = false;
+  const int rc = ensure_buf(ws.qt, ws.qt_bytes, std::max<size_t>((size_t)off * 4, 256), stream);
+  if (rc) return rc;
+  uint32_t* q = static_cast<uint32_t*>(ws.qt);
+  for (int v = 1; v <= vmax2; ++v)
+    for (int split = 0; split <= 1; ++split)
+      hipLaunchKernelGGL(k_qtab_inter, dim3((P + 63) / 64), dim3(64), 0, stream,
+                         q + ws.qt_inter[v - 1][split], P, v, M, split);
+  if (vmax2 >= 2)
+    for (int split = 0; split <= 1; ++split)
+      hipLaunchKernelGGL(k_qtab_merge, dim3((int)((pairs + 63) / 64)), dim3(64), 0, stream,
+                         q + ws.qt_merge[split], static_cast<const uint32_t*>(ws.mt), P, M,
+                         split);
+  if (hipGetLastError() != hipSuccess) return OCTO_EHIP;
+  ws.qt_valid = true;
+  ws.qt_P = p->P, ws.qt_vmax = p->v_max, ws.qt_M = p->M;
+  return OCTO_OK;
+}
+
 // Shared front half of octo_sim_batch and octo_tune_step: device, plans, workspace, prefix
 // sums, MERGE tables.
 int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, int64_t n,
@@ -1026,7 +1196,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
   }
   if (prob->v_max >= 2 && !(ws.mt_valid && ws.mt_P == prob->P && ws.mt_vmax == prob->v_max &&
                             ws.mt_M == prob->M)) {
-    const int lds = (int)align_up(((size_t)prob->P * prob->v_max * prob->M + 1) * 8, 16);
+    const int lds = (int)align_up((size_t)prob->P * prob->v_max * prob->M * 8, 16);
     if (lds > su->di.lds_max) return OCTO_EUNSUPPORTED;
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_merge_tab),
                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -1035,8 +1205,9 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
     if ((rc = launch_ok())) return rc;
     ws.mt_valid = true;
     ws.mt_P = prob->P, ws.mt_vmax = prob->v_max, ws.mt_M = prob->M;
+    ws.qt_valid = false;
   }
-  return OCTO_OK;
+  return build_qtab(prob, ws, stream);
 }
 
 SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, const int64_t* link,
@@ -1069,6 +1240,12 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.work = CTL_WORK;
   a.ring = prob->M;
   a.redo_bins = 0;
+  a.qtab = su.ws->qt_valid ? static_cast<const uint32_t*>(su.ws->qt) : nullptr;
+  for (int i = 0; i < 2; ++i) {
+    a.qt_merge[i] = su.ws->qt_merge[i];
+    for (int j = 0; j < 2; ++j) a.qt_inter[i][j] = su.ws->qt_inter[i][j];
+  }
+  a.strm_off = pl.strm_off;
   return a;
 }
 
@@ -1088,8 +1265,10 @@ template <int VC>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
                int64_t n, int64_t* ms, int64_t* bub, int s_cap, int ring_want, uint64_t mask,
                int work, hipStream_t stream) {
-  const Ring ring = make_ring(s_cap, prob->M, ring_want);
-  const Plan pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R);
+  const Ring ring = make_ring(prob->M, ring_want);
+  // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS
+  const int streams = (VC <= 2 && su.ws->qt_valid) ? 3 * VC : 0;
+  const Plan pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R, streams);
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub);
   a.bin_mask = mask, a.work = work;

@@ -253,7 +253,8 @@ struct GenMerge {
   int rowlen;
   int row[VMAX], pos[VMAX];
   uint32_t ent[VMAX], nxt[VMAX];
-  uint32_t px;  // load in flight for chunk pk (pk < 0: none)
+  uint32_t px;  // raw word of the load in flight for chunk pk (pk < 0: none)
+  bool pv;      // that load is inside the row (else the row has ended)
   int pk;
   int kind, k, m;
   __device__ __forceinline__ uint32_t fetch(int r, int p) const {
@@ -270,7 +271,7 @@ struct GenMerge {
       ent[c] = c < v ? fetch(row[c], 0) : MERGE_END;
       nxt[c] = c < v ? fetch(row[c], 1) : MERGE_END;
     }
-    px = MERGE_END, pk = -1;
+    px = MERGE_END, pv = false, pk = -1;
     update();
   }
   __device__ __forceinline__ void update() {
@@ -287,12 +288,15 @@ struct GenMerge {
     m = best == MERGE_END ? 0 : best & 0x7FF;
   }
   __device__ __forceinline__ void advance(bool ok) {
+    // commit the load issued at the previous advance (its latency covered a whole round)
+    const uint32_t got = pv ? px : MERGE_END;
 #pragma unroll
-    for (int c = 0; c < VMAX; ++c) nxt[c] = pk == c ? px : nxt[c];
+    for (int c = 0; c < VMAX; ++c) nxt[c] = pk == c ? got : nxt[c];
     int r = row[0], p = pos[0];
 #pragma unroll
     for (int c = 1; c < VMAX; ++c) r = k == c ? row[c] : r, p = k == c ? pos[c] : p;
-    px = fetch(r, p + 2);
+    px = tab[r + min(p + 2, rowlen - 1)];
+    pv = p + 2 < rowlen;
     pk = ok ? k : -1;
 #pragma unroll
     for (int c = 0; c < VMAX; ++c) {
@@ -309,7 +313,7 @@ struct GenMerge {
       ent[c] = t ? o.ent[c] : ent[c];
       nxt[c] = t ? o.nxt[c] : nxt[c];
     }
-    px = t ? o.px : px, pk = t ? o.pk : pk;
+    px = t ? o.px : px, pv = t ? o.pv : pv, pk = t ? o.pk : pk;
     kind = t ? o.kind : kind, k = t ? o.k : k, m = t ? o.m : m;
   }
 };

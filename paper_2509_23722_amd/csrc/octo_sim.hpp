@@ -8,8 +8,9 @@
 // B(s,m) needs B(s+1,m), which needs F(s+1,m).
 //
 // Every op reads exactly one slot and needs one state bit there (and the parity of its own m):
-//   F(0,m): the zero slot (always ready, time 0);   F(s,m), s > 0: row s-1, bit 2;
-//   in = fin + link weight.
+//   F(0,m): its own slot, always ready, weight 0: the slot is empty, or (ring rows) holds the
+//   backward of m - R, which the same device ran earlier, so in <= the device clock;
+//   F(s,m), s > 0: row s-1, bit 2; in = fin + link weight.
 //   B(s,m), s < S-1: row s+1, bit 1; in = fin + link weight.
 //   B(S-1,m): its own slot, bit 2 (the loss turns the forward around).
 //   W(s,m): its own slot, bit 1; W writes nothing.
@@ -37,12 +38,11 @@ namespace octo {
 constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
 
 // Ring geometry of one finish table: R slots per stage row, slot of m = m & mask, parity
-// (m >> lg) & 1; `zero` = index of the always-ready slot (holds 0). Without wrap (R = M):
-// mask = all ones, lg = 30.
+// (m >> lg) & 1. Without wrap (R = M): mask = all ones, lg = 30.
 struct Ring {
-  int R, mask, lg, zero;
+  int R, mask, lg;
 };
-__host__ __device__ __forceinline__ Ring make_ring(int S, int M, int R) {
+__host__ __device__ __forceinline__ Ring make_ring(int M, int R) {
   Ring r;
   if (R >= M) {
     r.R = M, r.mask = 0x7FFFFFFF, r.lg = 30;
@@ -51,7 +51,6 @@ __host__ __device__ __forceinline__ Ring make_ring(int S, int M, int R) {
     while ((1 << lg) < R) ++lg;
     r.R = 1 << lg, r.mask = r.R - 1, r.lg = lg;
   }
-  r.zero = S * r.R;
   return r;
 }
 
@@ -108,7 +107,7 @@ template <int VMAX>
 struct Chunks {
   int st[VMAX];                      // stage of chunk k
   int base[VMAX];                    // first slot of the stage's own row: s R
-  int first[VMAX];                   // stage 0: forwards read the zero slot
+  int frow[VMAX];                    // forward read row offset (-R; stage 0: its own row)
   int fmask[VMAX];                   // state bits a forward needs (0: always ready)
   int brow[VMAX], bmask[VMAX];       // backward read row offset / needed state bits
   int64_t dF[VMAX], dB[VMAX], dW[VMAX], wF[VMAX], wB[VMAX];
@@ -153,9 +152,8 @@ __device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, const R
   const int own = pick<VMAX>(c.base, k) + (m & ring.mask);
   const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
   const int fm = pick<VMAX>(c.fmask, k), bm = pick<VMAX>(c.bmask, k);
-  const int br = pick<VMAX>(c.brow, k);
-  const bool zf = isF && pick<VMAX>(c.first, k) != 0;
-  L.rd = zf ? ring.zero : own + (isF ? -ring.R : isB ? br : 0);
+  const int fr = pick<VMAX>(c.frow, k), br = pick<VMAX>(c.brow, k);
+  L.rd = own + (isF ? fr : isB ? br : 0);
   L.wr = own;
   L.store = isF || isB;
   L.mask = isF ? fm : isB ? bm : (int)(ST_B | ST_PAR);
@@ -215,6 +213,101 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
       gen.advance(ok);
       describe<VMAX>(L, c, ring, gen.kind, gen.k, gen.m);
     }
+    __asm__ volatile("" ::: "memory");
+    if (__ballot(ok) == 0) {
+      const uint64_t actm = __ballot(live);
+      if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
+      break;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Table-driven rounds. A queue-table row is a device queue for one stage set (its stages in
+// ascending order), each op pre-encoded with everything that does not depend on the candidate:
+//   bits 0-10 m | 11-13 stream e = kind * v + chunk | 14-19 read row | 20-25 write row |
+//   26-28 state bits the op needs (B, F, parity) | 29-30 state bits it writes (B, F; 0 = none).
+// The candidate's per-stream input weight and duration (32-bit) sit in LDS, 64 lanes
+// interleaved: strm[e * 64 + lane] = {w, dur}.
+// ------------------------------------------------------------------------------------------
+__host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, int v, int s,
+                                                      int S) {
+  int rdrow, need, wst;
+  if (kind == KF) {
+    rdrow = s > 0 ? s - 1 : s;  // stage 0 reads its own row, always ready (see relax_tab)
+    need = s > 0 ? (int)(ST_F | ST_PAR) : 0;
+    wst = ST_F;
+  } else if (kind == KB) {
+    rdrow = s < S - 1 ? s + 1 : s;
+    need = (int)((s < S - 1 ? ST_B : ST_F) | ST_PAR);
+    wst = ST_F | ST_B;
+  } else {
+    rdrow = s;
+    need = (int)(ST_B | ST_PAR);
+    wst = 0;
+  }
+  return (uint32_t)m | (uint32_t)(kind * v + k) << 11 | (uint32_t)rdrow << 14 |
+         (uint32_t)s << 20 | (uint32_t)need << 26 | (uint32_t)wst << 29;
+}
+
+struct TabOp {
+  int rd, wr, mask, want, store;
+  uint32_t state;
+  uint32_t w, dur;
+};
+
+// Decode entry x for this lane: slots from the ring, parity from m, {w, dur} from its stream.
+__device__ __forceinline__ void qt_decode(TabOp& o, uint32_t x, const Ring& ring,
+                                          const uint2* strm) {
+  const int m = (int)(x & 0x7FF);
+  const int e = (int)((x >> 11) & 7);
+  const int mr = m & ring.mask;
+  const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
+  o.rd = (int)((x >> 14) & 63) * ring.R + mr;
+  o.wr = (int)((x >> 20) & 63) * ring.R + mr;
+  o.mask = (int)((x >> 26) & 7);
+  o.want = o.mask & (int)(par ? (ST_B | ST_F | ST_PAR) : (ST_B | ST_F));
+  const uint32_t wst = (x >> 29) & 3u;
+  o.store = wst != 0;
+  o.state = wst | (par << 2);
+  const uint2 wd = strm[e * 64];
+  o.w = wd.x;
+  o.dur = wd.y;
+}
+
+// Rounds over a queue-table row (nops entries; nops = 0: idle lane). A stage-0 forward reads
+// its own slot and needs nothing: the slot is empty or holds the backward of micro-batch m - R,
+// which this device has already run, so its time never exceeds the device clock.
+template <class Tab>
+__device__ __forceinline__ void relax_tab(const uint32_t* qrow, int nops, const Ring& ring,
+                                          const uint2* strm, int64_t& clock, const Tab& T,
+                                          int G, uint64_t gbit, uint64_t lsb, bool& dead) {
+  const int last = nops > 0 ? nops - 1 : 0;
+  uint32_t cur = qrow[0], nxt = qrow[1 < last ? 1 : last], px = 0;
+  bool pv = false;
+  int pos = 0;
+  bool live = nops > 0;
+  TabOp o;
+  qt_decode(o, cur, ring, strm);
+  for (;;) {
+    uint32_t plo, phi;
+    T.issue(live ? o.rd : 0, plo, phi);
+    const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
+    const bool ok = live && (plo & (uint32_t)o.mask) == (uint32_t)o.want;
+    const int64_t tin = (int64_t)(p >> 3) + (int64_t)o.w;
+    const int64_t st = tin > clock ? tin : clock;
+    const int64_t fin = st + (int64_t)o.dur;
+    if (ok && o.store) T.store(o.wr, ((uint64_t)fin << 3) | o.state);
+    clock = ok ? fin : clock;
+    // next entry: the load issued last round is committed now, one round after it was issued
+    nxt = pv ? px : nxt;
+    const int ahead = pos + 2;
+    px = qrow[ahead < last ? ahead : last];
+    pv = ok;
+    pos += ok ? 1 : 0;
+    live = pos < nops;
+    cur = ok ? nxt : cur;
+    qt_decode(o, cur, ring, strm);
     __asm__ volatile("" ::: "memory");
     if (__ballot(ok) == 0) {
       const uint64_t actm = __ballot(live);
