@@ -263,8 +263,8 @@ __device__ __forceinline__ void qt_decode(TabOp& o, uint32_t x, const Ring& ring
   const int e = (int)((x >> 11) & 7);
   const int mr = m & ring.mask;
   const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
-  o.rd = (int)((x >> 14) & 63) * ring.R + mr;
-  o.wr = (int)((x >> 20) & 63) * ring.R + mr;
+  o.rd = __mul24((int)((x >> 14) & 63), ring.R) + mr;
+  o.wr = __mul24((int)((x >> 20) & 63), ring.R) + mr;
   o.mask = (int)((x >> 26) & 7);
   o.want = o.mask & (int)(par ? (ST_B | ST_F | ST_PAR) : (ST_B | ST_F));
   const uint32_t wst = (x >> 29) & 3u;
@@ -277,7 +277,8 @@ __device__ __forceinline__ void qt_decode(TabOp& o, uint32_t x, const Ring& ring
 
 // Rounds over a queue-table row (nops entries; nops = 0: idle lane). A stage-0 forward reads
 // its own slot and needs nothing: the slot is empty or holds the backward of micro-batch m - R,
-// which this device has already run, so its time never exceeds the device clock.
+// which this device has already run, so its time never exceeds the device clock. Each round
+// decodes its op first, so the stream read and the slot read are in flight together.
 template <class Tab>
 __device__ __forceinline__ void relax_tab(const uint32_t* qrow, int nops, const Ring& ring,
                                           const uint2* strm, int64_t& clock, const Tab& T,
@@ -287,11 +288,11 @@ __device__ __forceinline__ void relax_tab(const uint32_t* qrow, int nops, const 
   bool pv = false;
   int pos = 0;
   bool live = nops > 0;
-  TabOp o;
-  qt_decode(o, cur, ring, strm);
   for (;;) {
+    TabOp o;
+    qt_decode(o, cur, ring, strm);
     uint32_t plo, phi;
-    T.issue(live ? o.rd : 0, plo, phi);
+    T.issue(o.rd, plo, phi);
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
     const bool ok = live && (plo & (uint32_t)o.mask) == (uint32_t)o.want;
     const int64_t tin = (int64_t)(p >> 3) + (int64_t)o.w;
@@ -307,7 +308,6 @@ __device__ __forceinline__ void relax_tab(const uint32_t* qrow, int nops, const 
     pos += ok ? 1 : 0;
     live = pos < nops;
     cur = ok ? nxt : cur;
-    qt_decode(o, cur, ring, strm);
     __asm__ volatile("" ::: "memory");
     if (__ballot(ok) == 0) {
       const uint64_t actm = __ballot(live);
