@@ -64,7 +64,8 @@ struct SimArgs {
   int work;              // chunk counter index of this launch
   int ring;              // slots per stage row of this launch's finish tables (R)
   uint64_t redo_bins;    // bins whose queues may exceed R in flight: sent to the 64-bit path
-  // queue tables (v <= 2), entry offsets of each block's first row; null: generate in-kernel
+  // queue tables (v <= 2) for this launch's geometry, entry index of each block's first row;
+  // null: generate queues in-kernel
   const uint32_t* qtab;
   int64_t qt_inter[2][2];  // [v - 1][split], one row per rank
   int64_t qt_merge[2];     // [split], v = 2, one row per stage pair s0 < s1
@@ -228,16 +229,16 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
 }
 
 // Row of the queue table that holds device d's queue (v <= 2): INTER by the device's first
-// stage (its rank), MERGE by its stage pair.
+// stage (its rank), MERGE by its stage pair. Returns the row's first entry index.
 template <int VMAX>
-__device__ __forceinline__ const uint32_t* qt_row(const SimArgs& a, int gen, int v, int split,
-                                                  const Chunks<VMAX>& c) {
+__device__ __forceinline__ int qt_row(const SimArgs& a, int gen, int v, int split,
+                                      const Chunks<VMAX>& c) {
   const int M = a.pr.M, S = a.pr.P * v;
   const int64_t n = (int64_t)(split ? 3 : 2) * v * M;
-  if (gen == GEN_INTER) return a.qtab + a.qt_inter[v - 1][split] + c.st[0] * n;
+  if (gen == GEN_INTER) return (int)(a.qt_inter[v - 1][split] + c.st[0] * n);
   const int s0 = c.st[0], s1 = pick<VMAX>(c.st, 1);
   const int64_t pair = (int64_t)s0 * (2 * S - s0 - 1) / 2 + (s1 - s0 - 1);
-  return a.qtab + a.qt_merge[split] + pair * n;
+  return (int)(a.qt_merge[split] + pair * n);
 }
 
 // Table-driven simulation of one candidate per group (INTER or MERGE at v <= 2). Durations and
@@ -252,7 +253,7 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   const Table40 T{reinterpret_cast<uint32_t*>(lds_wave),
                   lds_wave + (size_t)a.slots * a.CPW * 4, __ffs(a.CPW) - 1, g < a.CPW ? g : 0};
   uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
-  uint2* strm = reinterpret_cast<uint2*>(lds_wave + a.strm_off) + lane_id();
+  uint8_t* strm = lds_wave + a.strm_off + lane_id() * 8;
   const bool has = cand >= 0;
   const int S = P * v;
   const Ring ring = make_ring(M, a.ring);
@@ -274,7 +275,7 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
                          : kind == KB ? pick<VMAX>(c.dB, k)
                                       : pick<VMAX>(c.dW, k);
       fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
-      strm[e * 64] = make_uint2((uint32_t)w, (uint32_t)du);
+      *reinterpret_cast<uint2*>(strm + e * 512) = make_uint2((uint32_t)w, (uint32_t)du);
     }
   } else {
     zero_chunks<VMAX>(c);
@@ -283,14 +284,14 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   group_bits(G, &gbit, &lsb);
   const bool wide = (fold_groups(__ballot(!fits), G, lsb) & gbit) != 0;
   if (wide) nops = 0;
-  const uint32_t* qrow = mine ? qt_row<VMAX>(a, gen, v, split, c) : a.qtab;
+  const int row = mine ? qt_row<VMAX>(a, gen, v, split, c) : 0;
   __asm__ volatile("" ::: "memory");
   T.clear_all(S * ring.R, lane_id(), WAVE);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
   int64_t clock = 0;
-  relax_tab(qrow, nops, ring, strm, clock, T, G, gbit, lsb, dead);
+  relax_tab(a.qtab, row, nops, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead);
 
   const int64_t ms = group_max(clock, G);
   if (mine) {
@@ -360,25 +361,31 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   relax<1, true>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
 }
 
-// Queue-table rows of the interleaved order (v <= 2): thread r writes rank r's queue; chunk k
-// of rank r is stage r + k P.
-__global__ void k_qtab_inter(uint32_t* __restrict__ out, int P, int v, int M, int split) {
+__global__ void k_zero_u32(uint32_t* __restrict__ p, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
+}
+
+// Queue-table rows of the interleaved order (v <= 2) for one launch geometry: thread r writes
+// rank r's queue; chunk k of rank r is stage r + k P.
+__global__ void k_qtab_inter(uint32_t* __restrict__ out, int P, int v, int M, int split, int R,
+                             int lg) {
   const int r = (int)(blockIdx.x * blockDim.x + threadIdx.x);
   if (r >= P) return;
   const int n = (split ? 3 : 2) * v * M, S = P * v;
+  const Ring ring = make_ring(M, R);
   uint32_t* row = out + (int64_t)r * n;
   GenInter g;
   g.init(P, v, M, r, split, split ? r : 0);
   for (int i = 0; i < n; ++i) {
-    row[i] = qt_entry(g.kind, g.k, g.m, v, r + g.k * P, S);
+    row[i] = qt_entry(g.kind, g.k, g.m, v, r + g.k * P, S, ring, lg);
     g.advance(true);
   }
 }
 
 // Queue-table rows of the MERGE order at v = 2: thread i writes the queue of stage pair i
 // (pairs s0 < s1 in lexicographic order).
-__global__ void k_qtab_merge(uint32_t* __restrict__ out, const uint32_t* __restrict__ mtab, int P,
-                             int M, int split) {
+__global__ void k_qtab_merge(uint32_t* __restrict__ out, const uint32_t* __restrict__ mtab,
+                             int P, int M, int split, int R, int lg) {
   const int S = 2 * P;
   const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
   if (i >= S * (S - 1) / 2) return;
@@ -386,11 +393,12 @@ __global__ void k_qtab_merge(uint32_t* __restrict__ out, const uint32_t* __restr
   while (rem >= S - 1 - s0) rem -= S - 1 - s0, ++s0;
   const int s1 = s0 + 1 + rem;
   const int rowlen = (split ? 3 : 2) * M, n = 2 * rowlen;
+  const Ring ring = make_ring(M, R);
   uint32_t* row = out + (int64_t)i * n;
   GenMerge<2> g;
   g.init(mtab + merge_offset(P, M, 2, split), rowlen, 2, [&](int k) { return k == 0 ? s0 : s1; });
   for (int j = 0; j < n; ++j) {
-    row[j] = qt_entry(g.kind, g.k, g.m, 2, g.k == 0 ? s0 : s1, S);
+    row[j] = qt_entry(g.kind, g.k, g.m, 2, g.k == 0 ? s0 : s1, S, ring, lg);
     g.advance(true);
   }
 }
@@ -911,6 +919,7 @@ struct Workspace {
   size_t qt_bytes = 0;
   bool qt_valid = false;
   int qt_P = 0, qt_vmax = 0, qt_M = 0;
+  int qt_R[2] = {}, qt_lg[2] = {};  // launch geometry the entries were encoded for, per v
   int64_t qt_inter[2][2] = {}, qt_merge[2] = {};
 };
 
@@ -1127,13 +1136,32 @@ void compute_inflight(const octo_problem* p, Workspace& ws) {
   ws.if_P = P, ws.if_M = M;
 }
 
-// Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), rebuilt when
-// (P, v_max, M) changes or the MERGE tables were rebuilt. Entry offsets are kept in the
-// workspace.
-int build_qtab(const octo_problem* p, Workspace& ws, hipStream_t stream) {
-  if (ws.qt_valid && ws.qt_P == p->P && ws.qt_vmax == p->v_max && ws.qt_M == p->M)
-    return OCTO_OK;
+// Launch geometry of the table-driven k_sim launch for v (1 or 2): ring rows and plan.
+struct TabGeom {
+  Ring ring;
+  Plan plan;
+  int lg;
+};
+TabGeom tab_geom(const octo_problem* p, int lds_max, int v) {
+  TabGeom t;
+  t.ring = make_ring(p->M, v * p->P);
+  t.plan = fast_plan(p, lds_max, v * p->P, t.ring.R, 3 * v);
+  t.lg = t.plan.CPW > 0 ? __builtin_ctz(t.plan.CPW) : 0;
+  return t;
+}
+
+// Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), encoded for
+// each v's launch geometry; rebuilt when (P, v_max, M), the geometry or the MERGE tables
+// change. Entry offsets are kept in the workspace.
+int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, hipStream_t stream) {
   const int P = p->P, M = p->M, vmax2 = std::min(p->v_max, 2);
+  TabGeom geo[2] = {tab_geom(p, lds_max, 1), tab_geom(p, lds_max, 2)};
+  bool same = ws.qt_valid && ws.qt_P == P && ws.qt_vmax == p->v_max && ws.qt_M == M;
+  for (int v = 1; v <= vmax2; ++v)
+    same = same && ws.qt_R[v - 1] == geo[v - 1].ring.R && ws.qt_lg[v - 1] == geo[v - 1].lg;
+  if (same) return OCTO_OK;
+  for (int v = 1; v <= vmax2; ++v)
+    if (geo[v - 1].plan.CPW < 1) return OCTO_OK;  // no table-driven launch fits: generate
   int64_t off = 0;
   for (int v = 1; v <= vmax2; ++v)
     for (int split = 0; split <= 1; ++split) {
@@ -1146,22 +1174,28 @@ int build_qtab(const octo_problem* p, Workspace& ws, hipStream_t stream) {
     ws.qt_merge[split] = off;
     if (vmax2 >= 2) off += pairs * (split ? 3 : 2) * 2 * M;
   }
+  if (off + 2 > INT32_MAX) return OCTO_OK;  // entry indices are int: generate instead
   ws.qt_valid = false;
-  const int rc = ensure_buf(ws.qt, ws.qt_bytes, std::max<size_t>((size_t)off * 4, 256), stream);
+  // two padding entries after the last row: the kernel's look-ahead reads up to row + nops + 1
+  const size_t bytes = (size_t)(off + 2) * 4;
+  const int rc = ensure_buf(ws.qt, ws.qt_bytes, bytes, stream);
   if (rc) return rc;
   uint32_t* q = static_cast<uint32_t*>(ws.qt);
   for (int v = 1; v <= vmax2; ++v)
     for (int split = 0; split <= 1; ++split)
       hipLaunchKernelGGL(k_qtab_inter, dim3((P + 63) / 64), dim3(64), 0, stream,
-                         q + ws.qt_inter[v - 1][split], P, v, M, split);
+                         q + ws.qt_inter[v - 1][split], P, v, M, split, geo[v - 1].ring.R,
+                         geo[v - 1].lg);
   if (vmax2 >= 2)
     for (int split = 0; split <= 1; ++split)
       hipLaunchKernelGGL(k_qtab_merge, dim3((int)((pairs + 63) / 64)), dim3(64), 0, stream,
                          q + ws.qt_merge[split], static_cast<const uint32_t*>(ws.mt), P, M,
-                         split);
+                         split, geo[1].ring.R, geo[1].lg);
   if (hipGetLastError() != hipSuccess) return OCTO_EHIP;
   ws.qt_valid = true;
-  ws.qt_P = p->P, ws.qt_vmax = p->v_max, ws.qt_M = p->M;
+  ws.qt_P = P, ws.qt_vmax = p->v_max, ws.qt_M = M;
+  for (int v = 1; v <= 2; ++v) ws.qt_R[v - 1] = geo[v - 1].ring.R, ws.qt_lg[v - 1] = geo[v - 1].lg;
+  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(64), 0, stream, q + off, 2);
   return OCTO_OK;
 }
 
@@ -1207,7 +1241,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
     ws.mt_P = prob->P, ws.mt_vmax = prob->v_max, ws.mt_M = prob->M;
     ws.qt_valid = false;
   }
-  return build_qtab(prob, ws, stream);
+  return OCTO_OK;
 }
 
 SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, const int64_t* link,
@@ -1240,7 +1274,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.work = CTL_WORK;
   a.ring = prob->M;
   a.redo_bins = 0;
-  a.qtab = su.ws->qt_valid ? static_cast<const uint32_t*>(su.ws->qt) : nullptr;
+  a.qtab = nullptr;
   for (int i = 0; i < 2; ++i) {
     a.qt_merge[i] = su.ws->qt_merge[i];
     for (int j = 0; j < 2; ++j) a.qt_inter[i][j] = su.ws->qt_inter[i][j];
@@ -1266,11 +1300,20 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
                int64_t n, int64_t* ms, int64_t* bub, int s_cap, int ring_want, uint64_t mask,
                int work, hipStream_t stream) {
   const Ring ring = make_ring(prob->M, ring_want);
-  // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS
-  const int streams = (VC <= 2 && su.ws->qt_valid) ? 3 * VC : 0;
-  const Plan pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R, streams);
+  // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS and need tables
+  // encoded for exactly this geometry
+  bool tab = false;
+  Plan pl{};
+  if (VC <= 2 && su.ws->qt_valid) {
+    const TabGeom geo = tab_geom(prob, su.di.lds_max, VC);
+    tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[VC - 1] == geo.ring.R &&
+          su.ws->qt_lg[VC - 1] == geo.lg && geo.plan.G * geo.plan.CPW <= WAVE;
+    pl = geo.plan;
+  }
+  if (!tab) pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R, 0);
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub);
+  if (tab) a.qtab = static_cast<const uint32_t*>(su.ws->qt);
   a.bin_mask = mask, a.work = work;
   a.ring = ring.R;
   a.redo_bins = 0;
@@ -1381,6 +1424,7 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
   // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
+  if ((rc = build_qtab(prob, *su.ws, su.di.lds_max, stream))) return rc;
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&

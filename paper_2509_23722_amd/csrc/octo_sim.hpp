@@ -224,17 +224,20 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
 
 // ------------------------------------------------------------------------------------------
 // Table-driven rounds. A queue-table row is a device queue for one stage set (its stages in
-// ascending order), each op pre-encoded with everything that does not depend on the candidate:
-//   bits 0-10 m | 11-13 stream e = kind * v + chunk | 14-19 read row | 20-25 write row |
-//   26-28 state bits the op needs (B, F, parity) | 29-30 state bits it writes (B, F; 0 = none).
+// ascending order), each op pre-encoded in 32 bits, for one launch geometry (ring R,
+// CPW = 2^lg candidates per wave), with everything that does not depend on the candidate:
+//   bits 0-14 read slot << lg | 15-16 write row relative to the read row, + 1 (the write slot
+//   is read slot + (code - 1) R << lg) | 17-19 state bits needed (B, F, parity) | 20-22 their
+//   wanted values | 23-25 state bits written, parity included (0 = writes nothing) |
+//   26-28 stream e = kind * v + chunk.
 // The candidate's per-stream input weight and duration (32-bit) sit in LDS, 64 lanes
-// interleaved: strm[e * 64 + lane] = {w, dur}.
+// interleaved: the pair of lane l for stream e at byte e * 512 + l * 8.
 // ------------------------------------------------------------------------------------------
 __host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, int v, int s,
-                                                      int S) {
+                                                      int S, const Ring& ring, int lg) {
   int rdrow, need, wst;
   if (kind == KF) {
-    rdrow = s > 0 ? s - 1 : s;  // stage 0 reads its own row, always ready (see relax_tab)
+    rdrow = s > 0 ? s - 1 : s;  // stage 0 reads its own slot, always ready (see relax_tab)
     need = s > 0 ? (int)(ST_F | ST_PAR) : 0;
     wst = ST_F;
   } else if (kind == KB) {
@@ -246,69 +249,51 @@ __host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, in
     need = (int)(ST_B | ST_PAR);
     wst = 0;
   }
-  return (uint32_t)m | (uint32_t)(kind * v + k) << 11 | (uint32_t)rdrow << 14 |
-         (uint32_t)s << 20 | (uint32_t)need << 26 | (uint32_t)wst << 29;
-}
-
-struct TabOp {
-  int rd, wr, mask, want, store;
-  uint32_t state;
-  uint32_t w, dur;
-};
-
-// Decode entry x for this lane: slots from the ring, parity from m, {w, dur} from its stream.
-__device__ __forceinline__ void qt_decode(TabOp& o, uint32_t x, const Ring& ring,
-                                          const uint2* strm) {
-  const int m = (int)(x & 0x7FF);
-  const int e = (int)((x >> 11) & 7);
   const int mr = m & ring.mask;
-  const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
-  o.rd = __mul24((int)((x >> 14) & 63), ring.R) + mr;
-  o.wr = __mul24((int)((x >> 20) & 63), ring.R) + mr;
-  o.mask = (int)((x >> 26) & 7);
-  o.want = o.mask & (int)(par ? (ST_B | ST_F | ST_PAR) : (ST_B | ST_F));
-  const uint32_t wst = (x >> 29) & 3u;
-  o.store = wst != 0;
-  o.state = wst | (par << 2);
-  const uint2 wd = strm[e * 64];
-  o.w = wd.x;
-  o.dur = wd.y;
+  const int par = (m >> ring.lg) & 1;
+  const uint32_t rd = (uint32_t)(rdrow * ring.R + mr) << lg;
+  const uint32_t code = (uint32_t)(s - rdrow + 1);
+  const int want = need & (par ? (int)(ST_B | ST_F | ST_PAR) : (int)(ST_B | ST_F));
+  const int state = wst ? (wst | (par << 2)) : 0;
+  return rd | code << 15 | (uint32_t)need << 17 | (uint32_t)want << 20 | (uint32_t)state << 23 |
+         (uint32_t)(kind * v + k) << 26;
 }
 
-// Rounds over a queue-table row (nops entries; nops = 0: idle lane). A stage-0 forward reads
-// its own slot and needs nothing: the slot is empty or holds the backward of micro-batch m - R,
+// Rounds over one queue-table row: entries [row, row + nops) (nops = 0: idle lane); the table
+// ends with two padding entries, so the look-ahead never leaves it. A stage-0 forward reads its
+// own slot and needs nothing: the slot is empty or holds the backward of micro-batch m - R,
 // which this device has already run, so its time never exceeds the device clock. Each round
-// decodes its op first, so the stream read and the slot read are in flight together.
-template <class Tab>
-__device__ __forceinline__ void relax_tab(const uint32_t* qrow, int nops, const Ring& ring,
-                                          const uint2* strm, int64_t& clock, const Tab& T,
-                                          int G, uint64_t gbit, uint64_t lsb, bool& dead) {
-  const int last = nops > 0 ? nops - 1 : 0;
-  uint32_t cur = qrow[0], nxt = qrow[1 < last ? 1 : last], px = 0;
-  bool pv = false;
+// decodes its op first, so the stream read and the slot read are in flight together, and loads
+// the entry after next at its start, to be committed at its end. Rl = R << lg.
+__device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, int row, int nops,
+                                          int Rl, const uint8_t* strm, int64_t& clock,
+                                          const Table40& T, int G, uint64_t gbit, uint64_t lsb,
+                                          bool& dead) {
+  uint32_t cur = qt[row], nxt = qt[row + 1];
   int pos = 0;
   bool live = nops > 0;
   for (;;) {
-    TabOp o;
-    qt_decode(o, cur, ring, strm);
-    uint32_t plo, phi;
-    T.issue(o.rd, plo, phi);
+    // the entry after next, needed only if this op completes; its load overlaps the round
+    const uint32_t ahead = qt[row + pos + 2];
+    const int rdj = (int)(cur & 0x7FFFu) | T.g;
+    const int wrj = rdj + ((int)((cur >> 15) & 3u) - 1) * Rl;
+    const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
+    const uint2 wd = *reinterpret_cast<const uint2*>(strm + ((cur >> 17) & 0xE00u));
+    const uint32_t plo = T.lo[rdj], phi = T.hi[rdj];
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
-    const bool ok = live && (plo & (uint32_t)o.mask) == (uint32_t)o.want;
-    const int64_t tin = (int64_t)(p >> 3) + (int64_t)o.w;
+    const bool ok = live && (plo & mask) == want;
+    const int64_t tin = (int64_t)(p >> 3) + (int64_t)wd.x;
     const int64_t st = tin > clock ? tin : clock;
-    const int64_t fin = st + (int64_t)o.dur;
-    if (ok && o.store) T.store(o.wr, ((uint64_t)fin << 3) | o.state);
+    const int64_t fin = st + (int64_t)wd.y;
+    if (ok && state != 0) {
+      T.lo[wrj] = (uint32_t)(((uint64_t)fin << 3) | state);
+      T.hi[wrj] = (uint8_t)((uint64_t)fin >> 29);
+    }
     clock = ok ? fin : clock;
-    // next entry: the load issued last round is committed now, one round after it was issued
-    nxt = pv ? px : nxt;
-    const int ahead = pos + 2;
-    px = qrow[ahead < last ? ahead : last];
-    pv = ok;
     pos += ok ? 1 : 0;
     live = pos < nops;
     cur = ok ? nxt : cur;
-    __asm__ volatile("" ::: "memory");
+    nxt = ok ? ahead : nxt;
     if (__ballot(ok) == 0) {
       const uint64_t actm = __ballot(live);
       if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
