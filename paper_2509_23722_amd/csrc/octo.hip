@@ -268,14 +268,18 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   if (mine) {
     busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
     nops = (split ? 3 : 2) * v * M;
-    for (int e = 0; e < 3 * v; ++e) {
-      const int kind = e / v, k = e - kind * v;
-      const int64_t w = kind == KF ? pick<VMAX>(c.wF, k) : kind == KB ? pick<VMAX>(c.wB, k) : 0;
-      const int64_t du = kind == KF   ? pick<VMAX>(c.dF, k)
-                         : kind == KB ? pick<VMAX>(c.dB, k)
-                                      : pick<VMAX>(c.dW, k);
-      fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
-      *reinterpret_cast<uint2*>(strm + e * 512) = make_uint2((uint32_t)w, (uint32_t)du);
+#pragma unroll
+    for (int kind = 0; kind < 3; ++kind) {
+#pragma unroll
+      for (int k = 0; k < VMAX; ++k) {
+        if (k < v) {
+          const int64_t w = kind == KF ? c.wF[k] : kind == KB ? c.wB[k] : 0;
+          const int64_t du = kind == KF ? c.dF[k] : kind == KB ? c.dB[k] : c.dW[k];
+          fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
+          *reinterpret_cast<uint2*>(strm + (kind * v + k) * 512) =
+              make_uint2((uint32_t)w, (uint32_t)du);
+        }
+      }
     }
   } else {
     zero_chunks<VMAX>(c);
@@ -978,11 +982,12 @@ int lanes_per_candidate(int P) {
 
 // 40-bit-slot plan for generated queues with up to s_cap stages; the staged record shares the
 // table's memory.
-// s_cap stages of R slots; streams > 0: a per-lane table of that many {w, dur} pairs.
+// s_cap stages of R slots (rounded up to 16, so that both slot arrays are 16-byte aligned and
+// sized); streams > 0: a per-lane table of that many {w, dur} pairs.
 Plan fast_plan(const octo_problem* p, int lds_max, int s_cap, int R, int streams) {
   Plan pl;
   pl.G = lanes_per_candidate(p->P);
-  pl.slots = s_cap * R;
+  pl.slots = (int)align_up((size_t)s_cap * R, 16);
   pl.rec_bytes = pert_off(p->P * p->v_max);
   pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
   pl.table_bytes = (int)(pl.slots * 4 + pl.slots);

@@ -93,12 +93,14 @@ struct Table40 {
     lo[j] = (uint32_t)v;
     hi[j] = (uint8_t)(v >> 32);
   }
-  // Clear n slots of every group (all lanes of the wave together).
+  // Clear n slots of every group (all lanes of the wave together), 16 bytes per store; the
+  // arrays start 16-byte aligned and a plan rounds both up to 16 bytes.
   __device__ __forceinline__ void clear_all(int n, int lane, int nlanes) const {
     const int tot = n << lg;
-    for (int j = lane; j < tot; j += nlanes) lo[j] = 0;
-    uint32_t* h = reinterpret_cast<uint32_t*>(hi);
-    for (int j = lane; j < (tot + 3) / 4; j += nlanes) h[j] = 0;
+    uint4* l4 = reinterpret_cast<uint4*>(lo);
+    for (int j = lane; j < (tot + 3) / 4; j += nlanes) l4[j] = make_uint4(0, 0, 0, 0);
+    uint4* h4 = reinterpret_cast<uint4*>(hi);
+    for (int j = lane; j < (tot + 15) / 16; j += nlanes) h4[j] = make_uint4(0, 0, 0, 0);
   }
   static constexpr int64_t LIMIT = (int64_t)1 << 37;
 };
@@ -269,14 +271,14 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, int r
                                           int Rl, const uint8_t* strm, int64_t& clock,
                                           const Table40& T, int G, uint64_t gbit, uint64_t lsb,
                                           bool& dead) {
-  uint32_t cur = qt[row], nxt = qt[row + 1];
+  uint32_t cur = qt[(uint32_t)row], nxt = qt[(uint32_t)row + 1u];
   int pos = 0;
   bool live = nops > 0;
   for (;;) {
     // the entry after next, needed only if this op completes; its load overlaps the round
-    const uint32_t ahead = qt[row + pos + 2];
+    const uint32_t ahead = qt[(uint32_t)(row + pos + 2)];
     const int rdj = (int)(cur & 0x7FFFu) | T.g;
-    const int wrj = rdj + ((int)((cur >> 15) & 3u) - 1) * Rl;
+    const int wrj = rdj + __mul24((int)((cur >> 15) & 3u), Rl) - Rl;
     const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
     const uint2 wd = *reinterpret_cast<const uint2*>(strm + ((cur >> 17) & 0xE00u));
     const uint32_t plo = T.lo[rdj], phi = T.hi[rdj];
