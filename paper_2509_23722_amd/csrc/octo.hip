@@ -69,6 +69,7 @@ struct SimArgs {
   const uint32_t* qtab;
   int64_t qt_inter[2][2];  // [v - 1][split], one row per rank
   int64_t qt_merge[2];     // [split], v = 2, one row per stage pair s0 < s1
+  int64_t qt_end;          // the table's final terminators
   int strm_off;            // LDS byte offset of the per-lane stream table
 };
 
@@ -234,7 +235,7 @@ template <int VMAX>
 __device__ __forceinline__ int qt_row(const SimArgs& a, int gen, int v, int split,
                                       const Chunks<VMAX>& c) {
   const int M = a.pr.M, S = a.pr.P * v;
-  const int64_t n = (int64_t)(split ? 3 : 2) * v * M;
+  const int64_t n = (int64_t)(split ? 3 : 2) * v * M + 2;  // row + two terminators
   if (gen == GEN_INTER) return (int)(a.qt_inter[v - 1][split] + c.st[0] * n);
   const int s0 = c.st[0], s1 = pick<VMAX>(c.st, 1);
   const int64_t pair = (int64_t)s0 * (2 * S - s0 - 1) / 2 + (s1 - s0 - 1);
@@ -262,12 +263,10 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
 
   Chunks<VMAX> c;
   int64_t busy = 0;
-  int nops = 0;
   bool fits = true;
   const bool mine = has && d < P;
   if (mine) {
     busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
-    nops = (split ? 3 : 2) * v * M;
 #pragma unroll
     for (int kind = 0; kind < 3; ++kind) {
 #pragma unroll
@@ -287,15 +286,16 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
   const bool wide = (fold_groups(__ballot(!fits), G, lsb) & gbit) != 0;
-  if (wide) nops = 0;
-  const int row = mine ? qt_row<VMAX>(a, gen, v, split, c) : 0;
+  // idle lanes and candidates for the 64-bit path start on the table's final terminators
+  const uint32_t row = (mine && !wide) ? (uint32_t)qt_row<VMAX>(a, gen, v, split, c)
+                                       : (uint32_t)a.qt_end;
   __asm__ volatile("" ::: "memory");
   T.clear_all(S * ring.R, lane_id(), WAVE);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
   int64_t clock = 0;
-  relax_tab(a.qtab, row, nops, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead);
+  relax_tab(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead);
 
   const int64_t ms = group_max(clock, G);
   if (mine) {
@@ -365,8 +365,8 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   relax<1, true>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
 }
 
-__global__ void k_zero_u32(uint32_t* __restrict__ p, int n) {
-  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
+__global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t x) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = x;
 }
 
 // Queue-table rows of the interleaved order (v <= 2) for one launch geometry: thread r writes
@@ -377,13 +377,14 @@ __global__ void k_qtab_inter(uint32_t* __restrict__ out, int P, int v, int M, in
   if (r >= P) return;
   const int n = (split ? 3 : 2) * v * M, S = P * v;
   const Ring ring = make_ring(M, R);
-  uint32_t* row = out + (int64_t)r * n;
+  uint32_t* row = out + (int64_t)r * (n + 2);
   GenInter g;
   g.init(P, v, M, r, split, split ? r : 0);
   for (int i = 0; i < n; ++i) {
     row[i] = qt_entry(g.kind, g.k, g.m, v, r + g.k * P, S, ring, lg);
     g.advance(true);
   }
+  row[n] = row[n + 1] = QT_END;
 }
 
 // Queue-table rows of the MERGE order at v = 2: thread i writes the queue of stage pair i
@@ -398,13 +399,14 @@ __global__ void k_qtab_merge(uint32_t* __restrict__ out, const uint32_t* __restr
   const int s1 = s0 + 1 + rem;
   const int rowlen = (split ? 3 : 2) * M, n = 2 * rowlen;
   const Ring ring = make_ring(M, R);
-  uint32_t* row = out + (int64_t)i * n;
+  uint32_t* row = out + (int64_t)i * (n + 2);
   GenMerge<2> g;
   g.init(mtab + merge_offset(P, M, 2, split), rowlen, 2, [&](int k) { return k == 0 ? s0 : s1; });
   for (int j = 0; j < n; ++j) {
     row[j] = qt_entry(g.kind, g.k, g.m, 2, g.k == 0 ? s0 : s1, S, ring, lg);
     g.advance(true);
   }
+  row[n] = row[n + 1] = QT_END;
 }
 
 // One thread per candidate.
@@ -924,7 +926,7 @@ struct Workspace {
   bool qt_valid = false;
   int qt_P = 0, qt_vmax = 0, qt_M = 0;
   int qt_R[2] = {}, qt_lg[2] = {};  // launch geometry the entries were encoded for, per v
-  int64_t qt_inter[2][2] = {}, qt_merge[2] = {};
+  int64_t qt_inter[2][2] = {}, qt_merge[2] = {}, qt_end = 0;
 };
 
 std::mutex g_mu;
@@ -1168,21 +1170,24 @@ int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, hipStream_t st
   for (int v = 1; v <= vmax2; ++v)
     if (geo[v - 1].plan.CPW < 1) return OCTO_OK;  // no table-driven launch fits: generate
   int64_t off = 0;
+  // rows of n entries + 2 terminators
   for (int v = 1; v <= vmax2; ++v)
     for (int split = 0; split <= 1; ++split) {
       ws.qt_inter[v - 1][split] = off;
-      off += (int64_t)P * (split ? 3 : 2) * v * M;
+      off += (int64_t)P * ((split ? 3 : 2) * v * M + 2);
     }
   const int S2 = 2 * P;
   const int64_t pairs = (int64_t)S2 * (S2 - 1) / 2;
   for (int split = 0; split <= 1; ++split) {
     ws.qt_merge[split] = off;
-    if (vmax2 >= 2) off += pairs * (split ? 3 : 2) * 2 * M;
+    if (vmax2 >= 2) off += pairs * ((split ? 3 : 2) * 2 * M + 2);
   }
-  if (off + 2 > INT32_MAX) return OCTO_OK;  // entry indices are int: generate instead
+  ws.qt_end = off;
+  if (off + 3 > INT32_MAX) return OCTO_OK;  // entry indices are 32-bit: generate instead
   ws.qt_valid = false;
-  // two padding entries after the last row: the kernel's look-ahead reads up to row + nops + 1
-  const size_t bytes = (size_t)(off + 2) * 4;
+  // the final terminators: idle lanes start there, and a lane past its last op reads up to
+  // two entries beyond its row
+  const size_t bytes = (size_t)(off + 3) * 4;
   const int rc = ensure_buf(ws.qt, ws.qt_bytes, bytes, stream);
   if (rc) return rc;
   uint32_t* q = static_cast<uint32_t*>(ws.qt);
@@ -1200,7 +1205,7 @@ int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, hipStream_t st
   ws.qt_valid = true;
   ws.qt_P = P, ws.qt_vmax = p->v_max, ws.qt_M = M;
   for (int v = 1; v <= 2; ++v) ws.qt_R[v - 1] = geo[v - 1].ring.R, ws.qt_lg[v - 1] = geo[v - 1].lg;
-  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(64), 0, stream, q + off, 2);
+  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, q + off, 3, QT_END);
   return OCTO_OK;
 }
 
@@ -1282,6 +1287,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.qtab = nullptr;
   for (int i = 0; i < 2; ++i) {
     a.qt_merge[i] = su.ws->qt_merge[i];
+    a.qt_end = su.ws->qt_end;
     for (int j = 0; j < 2; ++j) a.qt_inter[i][j] = su.ws->qt_inter[i][j];
   }
   a.strm_off = pl.strm_off;

@@ -261,29 +261,31 @@ __host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, in
          (uint32_t)(kind * v + k) << 26;
 }
 
-// Rounds over one queue-table row: entries [row, row + nops) (nops = 0: idle lane); the table
-// ends with two padding entries, so the look-ahead never leaves it. A stage-0 forward reads its
-// own slot and needs nothing: the slot is empty or holds the backward of micro-batch m - R,
-// which this device has already run, so its time never exceeds the device clock. Each round
-// decodes its op first, so the stream read and the slot read are in flight together, and loads
-// the entry after next at its start, to be committed at its end. Rl = R << lg.
-__device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, int row, int nops,
-                                          int Rl, const uint8_t* strm, int64_t& clock,
-                                          const Table40& T, int G, uint64_t gbit, uint64_t lsb,
-                                          bool& dead) {
-  uint32_t cur = qt[(uint32_t)row], nxt = qt[(uint32_t)row + 1u];
-  int pos = 0;
-  bool live = nops > 0;
+// Row terminator: needs nothing but wants a bit that is never there, so it is never ready.
+constexpr uint32_t QT_END = 1u << 20;
+
+// Rounds over one queue-table row starting at entry `row`; every row is followed by two
+// QT_END entries (and the table by two more), so a lane that has run its last op stays on a
+// terminator, and an idle lane starts on one. A stage-0 forward reads its own slot and needs
+// nothing: the slot is empty or holds the backward of micro-batch m - R, which this device has
+// already run, so its time never exceeds the device clock. Each round decodes its op first, so
+// the stream read and the slot read are in flight together, and loads the entry after next at
+// its start, to be committed at its end. Rl = R << lg.
+__device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint32_t row, int Rl,
+                                          const uint8_t* strm, int64_t& clock, const Table40& T,
+                                          int G, uint64_t gbit, uint64_t lsb, bool& dead) {
+  uint32_t cur = qt[row], nxt = qt[row + 1u];
+  uint32_t qa = row + 2u;  // entry after next
   for (;;) {
     // the entry after next, needed only if this op completes; its load overlaps the round
-    const uint32_t ahead = qt[(uint32_t)(row + pos + 2)];
+    const uint32_t ahead = qt[qa];
     const int rdj = (int)(cur & 0x7FFFu) | T.g;
     const int wrj = rdj + __mul24((int)((cur >> 15) & 3u), Rl) - Rl;
     const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
     const uint2 wd = *reinterpret_cast<const uint2*>(strm + ((cur >> 17) & 0xE00u));
     const uint32_t plo = T.lo[rdj], phi = T.hi[rdj];
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
-    const bool ok = live && (plo & mask) == want;
+    const bool ok = (plo & mask) == want;
     const int64_t tin = (int64_t)(p >> 3) + (int64_t)wd.x;
     const int64_t st = tin > clock ? tin : clock;
     const int64_t fin = st + (int64_t)wd.y;
@@ -292,12 +294,11 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, int r
       T.hi[wrj] = (uint8_t)((uint64_t)fin >> 29);
     }
     clock = ok ? fin : clock;
-    pos += ok ? 1 : 0;
-    live = pos < nops;
+    qa += ok ? 1u : 0u;
     cur = ok ? nxt : cur;
     nxt = ok ? ahead : nxt;
     if (__ballot(ok) == 0) {
-      const uint64_t actm = __ballot(live);
+      const uint64_t actm = __ballot(cur != QT_END);
       if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
       break;
     }
