@@ -563,14 +563,56 @@ __device__ __forceinline__ int64_t sweep_row(int64_t* row, int stride, int M, in
   return f;
 }
 
+// The previous row of a k_afab lane: MMAX > 0 keeps it in registers (M == MMAX, the loop fully
+// unrolled), MMAX = 0 in LDS (M int64 per lane, lanes interleaved).
+template <int MMAX>
+struct AfabRow {
+  int64_t r[MMAX];
+  __device__ __forceinline__ void init(uint8_t*, int, int) {}
+  __device__ __forceinline__ void clear(int) {
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) r[m] = 0;
+  }
+  __device__ __forceinline__ int64_t sweep(int, int64_t f, int64_t w, int64_t dur) {
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+      const int64_t y = r[m] + w;
+      f = (y > f ? y : f) + dur;
+      r[m] = f;
+    }
+    return f;
+  }
+};
+template <>
+struct AfabRow<0> {
+  int64_t* row;
+  int stride;
+  __device__ __forceinline__ void init(uint8_t* base, int li, int lanes) {
+    row = reinterpret_cast<int64_t*>(base) + li;
+    stride = lanes;
+  }
+  __device__ __forceinline__ void clear(int M) {
+    for (int m = 0; m < M; ++m) row[m * stride] = 0;
+  }
+  __device__ __forceinline__ int64_t sweep(int M, int64_t f, int64_t w, int64_t dur) {
+    return sweep_row(row, stride, M, f, w, dur);
+  }
+};
+
+// Input weight of the first stage's forwards: their row holds zeros, so any value this far below
+// zero leaves fin(0, m) = dur + fin(0, m - 1).
+constexpr int64_t AFAB_NO_INPUT = -((int64_t)1 << 62);
+
+template <int MMAX>
 __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int lane = lane_id();
   const int P = a.pr.P, M = a.pr.M, L = a.pr.L;
   const int li = lane < lanes ? lane : 0;
-  int64_t* row = reinterpret_cast<int64_t*>(smem) + li;  // row[m * lanes]
-  int64_t* clk = row + (size_t)M * lanes;                // clk[d * lanes]
-  int64_t* bsy = clk + (size_t)P * lanes;                // bsy[d * lanes]
+  AfabRow<MMAX> row;
+  row.init(smem, li, lanes);
+  int64_t* clk = reinterpret_cast<int64_t*>(smem) + (MMAX == 0 ? (size_t)M * lanes : 0) + li;
+  int64_t* bsy = clk + (size_t)P * lanes;  // clk[d * lanes], bsy[d * lanes]
   for (;;) {
     int ch = 0;
     if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -588,38 +630,22 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
     const uint8_t* dev = rec + 3 + a.pr.s_max;
     const int S = P * v;
     for (int d = 0; d < P; ++d) clk[d * lanes] = 0, bsy[d * lanes] = 0;
-    // forwards
-    int dp = 0;
-    for (int s = 0; s < S; ++s) {
-      const int d = dev[s];
-      const int b0 = s > 0 ? bnd[s - 1] : 0, b1 = s < S - 1 ? bnd[s] : L;
+    row.clear(M);
+    // rows t = 0..S-1: forwards of stage t; t = S..2S-1: backwards of stage 2S-1-t
+    for (int t = 0; t < 2 * S; ++t) {
+      const bool fwd = t < S;
+      const int st = fwd ? t : 2 * S - 1 - t;
+      const int d = dev[st];
+      const int b0 = st > 0 ? bnd[st - 1] : 0, b1 = st < S - 1 ? bnd[st] : L;
       const int64_t df = a.pre[3 * b1] - a.pre[3 * b0];
       const int64_t db = a.pre[3 * b1 + 1] - a.pre[3 * b0 + 1] + a.pre[3 * b1 + 2] -
                          a.pre[3 * b0 + 2];
-      bsy[d * lanes] += (df + db) * M;
-      int64_t f = clk[d * lanes];
-      if (s == 0) {
-        for (int m = 0; m < M; ++m) {
-          f += df;
-          row[m * lanes] = f;
-        }
-      } else {
-        f = sweep_row(row, lanes, M, f, dp != d ? a.link[dp * P + d] : 0, df);
-      }
-      clk[d * lanes] = f;
-      dp = d;
-    }
-    // backwards
-    int dn = dp;
-    for (int s = S - 1; s >= 0; --s) {
-      const int d = dev[s];
-      const int b0 = s > 0 ? bnd[s - 1] : 0, b1 = s < S - 1 ? bnd[s] : L;
-      const int64_t db = a.pre[3 * b1 + 1] - a.pre[3 * b0 + 1] + a.pre[3 * b1 + 2] -
-                         a.pre[3 * b0 + 2];
-      const int64_t f = sweep_row(row, lanes, M, clk[d * lanes], dn != d ? a.link[dn * P + d] : 0,
-                                  db);
-      clk[d * lanes] = f;
-      dn = d;
+      if (fwd) bsy[d * lanes] += (df + db) * M;
+      // the stage whose finish times this row consumes: st - 1 (forward), st + 1 (backward)
+      const int q = fwd ? st - 1 : st + 1;
+      const int dq = q >= 0 && q < S && t != S ? dev[q] : d;
+      const int64_t w = (fwd && st == 0) ? AFAB_NO_INPUT : dq != d ? a.link[dq * P + d] : 0;
+      clk[d * lanes] = row.sweep(M, clk[d * lanes], w, fwd ? df : db);
     }
     int64_t ms = 0;
     for (int d = 0; d < P; ++d) ms = clk[d * lanes] > ms ? clk[d * lanes] : ms;
@@ -1344,7 +1370,9 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
 // int64 plus 2 P device words in LDS (at most 64 KiB per wave).
 int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
                 int64_t n, int64_t* ms, int64_t* bub, hipStream_t stream) {
-  const size_t per_lane = (size_t)(prob->M + 2 * prob->P) * 8;
+  // rows of exactly 32 or 64 micro-batches live in registers; other lengths in LDS
+  const int mmax = prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
+  const size_t per_lane = (size_t)((mmax ? 0 : prob->M) + 2 * prob->P) * 8;
   const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
   const int lds = (int)(lanes * per_lane);
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
@@ -1352,11 +1380,18 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
   a.bin_mask = bins_of(1, prob->v_max, true);
   a.work = CTL_WORK + 3;
   int grid = 0;
-  int rc = occupancy_grid(k_afab, lds, su.di.cus, &grid);
+  int rc = mmax == 32   ? occupancy_grid(k_afab<32>, lds, su.di.cus, &grid)
+           : mmax == 64 ? occupancy_grid(k_afab<64>, lds, su.di.cus, &grid)
+                        : occupancy_grid(k_afab<0>, lds, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + lanes - 1) / lanes;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  hipLaunchKernelGGL(k_afab, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+  if (mmax == 32)
+    hipLaunchKernelGGL(k_afab<32>, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+  else if (mmax == 64)
+    hipLaunchKernelGGL(k_afab<64>, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+  else
+    hipLaunchKernelGGL(k_afab<0>, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   return launch_ok();
 }
 
