@@ -75,7 +75,8 @@ struct SimArgs {
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
 
-__device__ __forceinline__ int bcast(int x) { return __shfl(x, 0); }
+// Lane 0's value, as a wave-uniform (scalar) value: all lanes are active where it is used.
+__device__ __forceinline__ int bcast(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // ---------------------------------------------------------------------------------------------
 // Per-lane set-up of one candidate from its staged record.
