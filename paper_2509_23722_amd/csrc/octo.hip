@@ -33,6 +33,7 @@ constexpr int WAVE = 64;
 
 // Workspace control block (int32 words).
 constexpr int CTL_COUNTS = 0;     // [NBINS] candidates per bin
+constexpr int CTL_START = 192;    // [NBINS] first index position of each bin
 constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (5)
 constexpr int CTL_WORK_MAT = 136; // chunk counter of k_sim_mat, perturbed list
 constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
@@ -410,35 +411,72 @@ __global__ void k_qtab_merge(uint32_t* __restrict__ out, const uint32_t* __restr
   row[n] = row[n + 1] = QT_END;
 }
 
-// One thread per candidate.
-__global__ void k_classify(SimArgs a, uint8_t* __restrict__ bins) {
+// Add one to hist[key] for every lane with `active`, one LDS atomic per distinct key of the
+// wave; returns the lane's index among the wave's additions to its key (valid when active).
+__device__ __forceinline__ int wave_hist_add(int* hist, int key, bool active) {
+  const int lane = lane_id();
+  const uint64_t below = (1ull << lane) - 1;
+  uint64_t rem = __ballot(active);
+  int mine = 0;
+  while (rem) {
+    const int leader = __ffsll((unsigned long long)rem) - 1;
+    const int k = __shfl(key, leader);
+    const uint64_t grp = __ballot(active && key == k);
+    int base = 0;
+    if (lane == leader) base = atomicAdd(&hist[k], __popcll(grp));
+    base = __shfl(base, leader);
+    if (active && key == k) mine = base + __popcll(grp & below);
+    rem &= ~grp;
+  }
+  return mine;
+}
+
+// One thread per candidate, blocks of CLS_THREADS. The records' heads (first hb bytes: header,
+// boundaries, placement) are staged through LDS with 16-byte coalesced loads.
+constexpr int CLS_THREADS = 256;
+__global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __restrict__ bins,
+                                                          int hb) {
+  extern __shared__ __align__(16) uint8_t heads[];
   __shared__ int hist[NBINS];
   for (int i = threadIdx.x; i < NBINS; i += blockDim.x) hist[i] = 0;
+  const int64_t first = (int64_t)blockIdx.x * CLS_THREADS;
+  const int cnt = (int)(a.n - first < CLS_THREADS ? a.n - first : CLS_THREADS);
+  const int q = hb / 16, stride16 = a.pr.stride / 16;
+  const uint4* src = reinterpret_cast<const uint4*>(a.cands + first * a.pr.stride);
+  uint4* dst = reinterpret_cast<uint4*>(heads);
+  for (int j = threadIdx.x; j < cnt * q; j += CLS_THREADS) {
+    const int r = j / q, c = j - r * q;
+    dst[j] = src[(int64_t)r * stride16 + c];
+  }
   __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < a.n) {
-    const uint8_t* rec = a.cands + i * a.pr.stride;
-    Resolved r = resolve_record(a.pr, rec);
-    int bin = BIN_NONE;
+  const int64_t i = first + threadIdx.x;
+  int bin = BIN_NONE;
+  if (threadIdx.x < cnt) {
+    const Resolved r = resolve_record(a.pr, heads + threadIdx.x * hb,
+                                      a.cands + i * a.pr.stride + pert_off(a.pr.s_max));
     if (!r.valid) {
       a.out_ms[i] = OCTO_MS_INVALID;
       for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
     } else {
       bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
-      atomicAdd(&hist[bin], 1);
     }
     bins[i] = (uint8_t)bin;
   }
+  wave_hist_add(hist, bin, bin != BIN_NONE);
   __syncthreads();
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
     if (hist[b]) atomicAdd(&a.ctl[CTL_COUNTS + b], hist[b]);
 }
 
-// One wave: start position of every bin in the index array (exclusive prefix sum).
+// One wave: first position of every bin in the index array (exclusive prefix sum), kept in
+// CTL_START and copied to the scatter cursors.
 __global__ void k_plan(int32_t* __restrict__ ctl) {
   if (threadIdx.x == 0) {
     int acc = 0;
-    for (int b = 0; b < NBINS; ++b) ctl[CTL_POS + b] = acc, acc += ctl[CTL_COUNTS + b];
+    for (int b = 0; b < NBINS; ++b) {
+      ctl[CTL_START + b] = ctl[CTL_POS + b] = acc;
+      acc += ctl[CTL_COUNTS + b];
+    }
   }
 }
 
@@ -449,11 +487,8 @@ __global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x) hist[b] = 0;
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int bin = BIN_NONE, local = 0;
-  if (i < a.n) {
-    bin = bins[i];
-    if (bin != BIN_NONE) local = atomicAdd(&hist[bin], 1);
-  }
+  const int bin = i < a.n ? bins[i] : BIN_NONE;
+  const int local = wave_hist_add(hist, bin, bin != BIN_NONE);
   __syncthreads();
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
     res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_POS + b], hist[b]) : 0;
@@ -714,11 +749,12 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
   int base = 0;
-  for (int b = 0; b < BIN_MAT; ++b) base += a.ctl[CTL_COUNTS + b];
+  base = a.ctl[CTL_START + BIN_MAT];
   for (int phase = 0; phase < 2; ++phase) {
     const int32_t* list = phase == 0 ? a.idx + base : a.redo;
     const int cnt = phase == 0 ? a.ctl[CTL_COUNTS + BIN_MAT] : a.ctl[CTL_REDO];
     const int counter = phase == 0 ? CTL_WORK_MAT : CTL_WORK_REDO;
+    if (cnt == 0) continue;  // no work: leave the shared counter alone
     for (;;) {
       int ch = 0;
       if (lane_id() == 0) ch = atomicAdd(&a.ctl[counter], 1);
@@ -1457,10 +1493,13 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
   if (rc) return rc;
   char* base = static_cast<char*>(su.ws->base);
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
-  const int tb = 256;
+  const int tb = CLS_THREADS;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
-  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), 0, stream, a, bins);
+  const int hb = (int)align_up((size_t)pert_off(prob->P * prob->v_max), 16);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, tb * hb);
+  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), tb * hb, stream, a, bins, hb);
   if ((rc = launch_ok())) return rc;
   hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, a.ctl);
   if ((rc = launch_ok())) return rc;

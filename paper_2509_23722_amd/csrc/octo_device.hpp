@@ -70,8 +70,12 @@ struct Resolved {
   int v, S, gen, split, n_pert;
 };
 
-// Looped placement test and balanced-placement test for a record in memory `rec`.
-__device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint8_t* rec) {
+// Validity, looped-placement and balanced-placement tests of one record.
+// head: the record's first pert_off(s_max) bytes (may be a staged copy); pert: its perturbation
+// list (in the record itself).
+__device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint8_t* head,
+                                                  const uint8_t* pert) {
+  const uint8_t* rec = head;
   Resolved r;
   int policy = rec[0], v = rec[1], n_pert = rec[2], flags = rec[3];
   r.v = v;
@@ -116,7 +120,7 @@ __device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint
   }
   // perturbations in range (queue length = (split ? 3 : 2) v M)
   const int qlen = (r.split ? 3 : 2) * v * pr.M;
-  const uint8_t* pp = rec + pert_off(pr.s_max);
+  const uint8_t* pp = pert;
   for (int i = 0; i < n_pert; ++i) {
     int d = pp[6 * i] | (pp[6 * i + 1] << 8);
     int from = pp[6 * i + 2] | (pp[6 * i + 3] << 8);
@@ -377,4 +381,10 @@ __device__ __forceinline__ U4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c
   return r;
 }
 
+}  // namespace octo
+
+namespace octo {
+__device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint8_t* rec) {
+  return resolve_record(pr, rec, rec + pert_off(pr.s_max));
+}
 }  // namespace octo
