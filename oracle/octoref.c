@@ -479,10 +479,59 @@ static void stage_costs(const ref_cand* c, const int64_t* costs, int64_t* F,
   }
 }
 
-/* Evaluate a candidate given its local queues (after perturbations). */
+/* Memory model (§5 memory nodes; §6 Eq. 2's peak per device). Every op of a device holds its
+ * memory node's tensors: a forward F(s,m) allocates the activations of stage s for micro-batch m
+ * when it starts; the last backward op of (s,m) — B when fused, W when split — releases them
+ * when it ends. Static bytes (weights, gradients, optimizer state) of the device's stages are
+ * held throughout. Events are replayed in time order (an op's release before a later op's
+ * allocation at the same instant; ties between ops of one device in their queue order), and
+ * peak_d = static_d + the largest running activation total. act[s], stat[s]: per-stage bytes. */
+typedef struct {
+  int64_t t;
+  int key; /* 2 * queue position, + 1 for a release */
+  int64_t delta;
+} mem_event;
+
+static int cmp_event(const void* a, const void* b) {
+  const mem_event* x = (const mem_event*)a;
+  const mem_event* y = (const mem_event*)b;
+  if (x->t != y->t) return x->t < y->t ? -1 : 1;
+  return x->key < y->key ? -1 : x->key > y->key ? 1 : 0;
+}
+
+static void peak_memory(const ref_dag_in* g, const ref_sop* sq, const int* qoff, const int* qlen,
+                        const int64_t* start, const int64_t* act, const int64_t* stat,
+                        int64_t* peak) {
+  for (int d = 0; d < g->P; ++d) {
+    int64_t base = 0;
+    for (int s = 0; s < g->S; ++s)
+      if (g->dev[s] == d) base += stat[s];
+    mem_event* ev = (mem_event*)malloc(sizeof(mem_event) * (size_t)(qlen[d] > 0 ? qlen[d] : 1));
+    int ne = 0;
+    for (int i = 0; i < qlen[d]; ++i) {
+      ref_sop o = sq[qoff[d] + i];
+      int64_t st = start[node_id(g->S, g->M, o.kind, o.s, o.m)];
+      if (o.kind == KF)
+        ev[ne++] = (mem_event){st, 2 * i, act[o.s]};
+      else if ((o.kind == KB && !g->split) || o.kind == KW)
+        ev[ne++] = (mem_event){st + op_dur(g, o.kind, o.s), 2 * i + 1, -act[o.s]};
+    }
+    qsort(ev, ne, sizeof(mem_event), cmp_event);
+    int64_t cur = 0, hi = 0;
+    for (int i = 0; i < ne; ++i) {
+      cur += ev[i].delta;
+      if (cur > hi) hi = cur;
+    }
+    peak[d] = base + hi;
+    free(ev);
+  }
+}
+
+/* Evaluate a candidate given its local queues (after perturbations). mem (nullable): layer
+ * memory [L][2] = {activation bytes per micro-batch, static bytes}; then peak[P] is filled. */
 static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                       const int64_t* link, const ref_op* q, int qcap, const int* qlen,
-                      int64_t* ms, int64_t* bub) {
+                      const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak) {
   int P = pr->P, S = c->S, split;
   resolve(pr, c, &split);
   int64_t F[64], B[64], W[64];
@@ -501,14 +550,25 @@ static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* c
     }
   }
   ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link};
-  int rc = simulate(&g, sq, qoff, qlen, ms, bub, NULL, NULL);
+  int64_t* start = mem ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M) : NULL;
+  int rc = simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
+  if (mem && rc == SIM_OK) {
+    int64_t act[64], stat[64];
+    for (int s = 0; s < S; ++s) {
+      act[s] = stat[s] = 0;
+      for (int l = c->b[s]; l < c->b[s + 1]; ++l) act[s] += mem[2 * l], stat[s] += mem[2 * l + 1];
+    }
+    peak_memory(&g, sq, qoff, qlen, start, act, stat, peak);
+  }
+  free(start);
   free(sq);
   return rc;
 }
 
 /* Full evaluation of one candidate record: makespan + bubbles, or sentinels. */
-static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* link,
-                        const uint8_t* rec, int64_t* ms, int64_t* bub) {
+static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
+                        const int64_t* link, const uint8_t* rec, int64_t* ms, int64_t* bub,
+                        int64_t* peak) {
   ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
   decode(pr, rec, c);
   int P = pr->P;
@@ -523,7 +583,7 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
         apply_perturbations(pr, c, q, qcap, qlen) != 0) {
       sentinel = REF_INVALID;
     } else {
-      int rc = eval_local(pr, c, costs, link, q, qcap, qlen, ms, bub);
+      int rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak);
       if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
       else if (rc != SIM_OK) sentinel = REF_INVALID;
     }
@@ -532,6 +592,8 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
   if (sentinel != 0) {
     *ms = sentinel;
     for (int d = 0; d < P; ++d) bub[d] = sentinel;
+    if (peak)
+      for (int d = 0; d < P; ++d) peak[d] = sentinel;
   }
   free(c);
 }
@@ -554,41 +616,52 @@ static int check_problem(const ref_problem* pr) {
 typedef struct {
   const ref_problem* pr;
   const int64_t* costs;
+  const int64_t* mem;
   const int64_t* link;
   const uint8_t* cands;
   int64_t lo, hi;
   int64_t* out_ms;
   int64_t* out_bub;
+  int64_t* out_peak;
 } batch_job;
 
 static void* batch_worker(void* arg) {
   batch_job* j = (batch_job*)arg;
   for (int64_t i = j->lo; i < j->hi; ++i)
-    eval_record(j->pr, j->costs, j->link, j->cands + (size_t)i * j->pr->cand_stride,
-                j->out_ms + i, j->out_bub + (size_t)i * j->pr->P);
+    eval_record(j->pr, j->costs, j->mem, j->link, j->cands + (size_t)i * j->pr->cand_stride,
+                j->out_ms + i, j->out_bub + (size_t)i * j->pr->P,
+                j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL);
   return NULL;
 }
 
-/* Evaluate n candidate records (host memory). nthreads >= 1 worker threads split the batch. */
-int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t* link,
-                     const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
-                     int nthreads) {
+/* Evaluate n candidate records (host memory). nthreads >= 1 worker threads split the batch.
+ * mem (nullable, with out_peak): layer memory [L][2]; out_peak[n][P] = peak bytes per device. */
+int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
+                         const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
+                         int64_t* out_bub, int64_t* out_peak, int nthreads) {
   if (!check_problem(pr) || n < 0 || (n > 0 && (!costs || !link || !cands || !out_ms || !out_bub)))
     return REF_EINVAL;
+  if ((mem == NULL) != (out_peak == NULL)) return REF_EINVAL;
   if (nthreads < 1) nthreads = 1;
   if (nthreads > 256) nthreads = 256;
   if (n < nthreads) nthreads = n > 0 ? (int)n : 1;
   pthread_t th[256];
   batch_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
-    jobs[t] = (batch_job){pr, costs, link, cands, n * t / nthreads, n * (t + 1) / nthreads,
-                          out_ms, out_bub};
+    jobs[t] = (batch_job){pr,     costs,  mem,     link,    cands, n * t / nthreads,
+                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak};
     if (nthreads == 1) batch_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, batch_worker, &jobs[t]);
   }
   if (nthreads > 1)
     for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
   return REF_OK;
+}
+
+int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                     const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                     int nthreads) {
+  return oracle_sim_batch_mem(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, nthreads);
 }
 
 /* Dump the final (perturbed) queues of one candidate in stage terms: ops[d*qcap + i] =
@@ -729,7 +802,7 @@ static void tune_chain(tune_job* j, int64_t ci) {
   int qlen[64];
   build_local_queues(pr, c, q, qcap, qlen);
   int64_t cur_ms, cur_bub[64], ms, tb[64];
-  int rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &cur_ms, cur_bub);
+  int rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &cur_ms, cur_bub, NULL);
   if (rc != SIM_OK) {
     cur_ms = rc == SIM_CYCLE ? REF_DEADLOCK : REF_INVALID;
     for (int d = 0; d < P; ++d) cur_bub[d] = cur_ms;
@@ -748,7 +821,7 @@ static void tune_chain(tune_job* j, int64_t ci) {
         if (nb > c->b[i - 1] && nb < c->b[i + 1]) {
           int old = c->b[i];
           c->b[i] = nb;
-          rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &ms, tb);
+          rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &ms, tb, NULL);
           if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
           else c->b[i] = old;
         }
@@ -763,7 +836,7 @@ static void tune_chain(tune_job* j, int64_t ci) {
           if (c->dev[s] == d1) c->dev[s] = d2;
           else if (c->dev[s] == d2) c->dev[s] = d1;
         }
-        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &ms, tb);
+        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &ms, tb, NULL);
         if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
         else
           for (int s = 0; s < S; ++s) c->dev[s] = saved[s];
@@ -776,7 +849,7 @@ static void tune_chain(tune_job* j, int64_t ci) {
         ref_op tmp = row[i];
         row[i] = row[i + 1];
         row[i + 1] = tmp;
-        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, &ms, tb);
+        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &ms, tb, NULL);
         if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
         else {
           row[i + 1] = row[i];

@@ -32,6 +32,9 @@ def lib():
         L.oracle_sim_batch.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64, p, p,
                                        ctypes.c_int]
         L.oracle_sim_batch.restype = ctypes.c_int
+        L.oracle_sim_batch_mem.argtypes = [ctypes.POINTER(RefProblem), p, p, p, p,
+                                           ctypes.c_int64, p, p, p, ctypes.c_int]
+        L.oracle_sim_batch_mem.restype = ctypes.c_int
         L.oracle_dump_queues.argtypes = [ctypes.POINTER(RefProblem), p, p, ctypes.c_int32, p]
         L.oracle_dump_queues.restype = ctypes.c_int
         L.oracle_sim_queues.argtypes = [ctypes.c_int32] * 4 + [p] * 9 + [p, p]
@@ -68,6 +71,24 @@ def sim_batch(prob, costs, link, cands, nthreads=1):
     if rc != 0:
         raise ValueError(f"oracle_sim_batch rejected the arguments (rc={rc})")
     return ms, bub
+
+
+def sim_batch_mem(prob, costs, mem, link, cands, nthreads=1):
+    """Evaluate candidate records with the memory model: mem int64 [L, 2] = {activation bytes
+    per micro-batch, static bytes} per layer. Returns (makespan[n], bubble[n, P], peak[n, P])."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    mem = np.ascontiguousarray(mem, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    peak = np.zeros((n, prob.P), dtype=np.int64)
+    rc = lib().oracle_sim_batch_mem(ctypes.byref(prob), _ptr(costs), _ptr(mem), _ptr(link),
+                                    _ptr(cands), n, _ptr(ms), _ptr(bub), _ptr(peak), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch_mem rejected the arguments (rc={rc})")
+    return ms, bub, peak
 
 
 def dump_queues(prob, rec):
