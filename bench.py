@@ -167,6 +167,36 @@ def main():
                                       5),
     }
 
+    # the same batch with the memory model (peak bytes per device), timed the same way
+    mem = torch.from_numpy(inputs.layer_mem(w)).to(dev)
+    peak = torch.empty((n, w.P), dtype=torch.int64, device=dev)
+    for _ in range(args.warmup):
+        _lib.sim_batch_mem(prob, costs, mem, link, recs, ms, bub, peak)
+    torch.cuda.synchronize()
+    hip2, evs2 = hip_events(nb * args.steps)
+    torch.cuda.synchronize()
+    m0 = time.perf_counter()
+    for k in range(args.steps):
+        _lib.profile_events(evs2[nb * k:nb * (k + 1)])
+        _lib.sim_batch_mem(prob, costs, mem, link, recs, ms, bub, peak)
+    torch.cuda.synchronize()
+    m1 = time.perf_counter()
+    _lib.profile_events([])
+    mk = np.zeros((args.steps, len(SIM_KERNELS)))
+    for k in range(args.steps):
+        for j in range(len(SIM_KERNELS)):
+            f = ctypes.c_float()
+            hip2.hipEventElapsedTime(ctypes.byref(f), evs2[nb * k + j], evs2[nb * k + j + 1])
+            mk[k, j] = f.value
+    for e in evs2:
+        hip2.hipEventDestroy(e)
+    memory_model = {
+        "value": round(n * args.steps / (m1 - m0), 1), "unit": "candidates/s",
+        "ms_per_step": round((m1 - m0) / args.steps * 1e3, 4),
+        "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, mk.mean(axis=0))},
+        "layer_mem": "inputs.layer_mem (per-type activation and static bytes)",
+    }
+
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     cpu = None
     if not args.no_cpu:
@@ -196,6 +226,7 @@ def main():
                    "placements": list(inputs.PLACEMENTS), "seed": w.seed},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "memory_model": memory_model,
     }
     print(json.dumps(out), flush=True)
 

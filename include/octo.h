@@ -110,6 +110,24 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
                    void* stream);
 
 /*
+ * octo_sim_batch_mem — octo_sim_batch plus the memory model (§5: every compute node has a memory
+ * node allocating or releasing intermediate tensors; §6 Eq. 2: peak memory per device against
+ * its capacity). A forward F(s,m) allocates stage s's activation bytes for micro-batch m when it
+ * starts; the last backward op of (s,m) — B when fused, W when split — releases them when it
+ * ends; a device's static bytes (its stages' weights, gradients, optimizer state) are held
+ * throughout. One device's ops never overlap, so its peak follows from its queue order.
+ *   layer_mem  int64 [L][2], per layer {activation bytes per micro-batch, static bytes}; stage
+ *              figures are sums over the stage's layers.
+ *   out_peak   int64 [n][P]: static bytes + the largest activation total held, per device;
+ *              OCTO_MS_DEADLOCK / OCTO_MS_INVALID like the makespan.
+ * Other arguments, results and status as octo_sim_batch (layer_mem and out_peak non-NULL).
+ */
+int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
+                       const int64_t* layer_mem, const int64_t* link, const void* candidates,
+                       int64_t n, int64_t* out_makespan, int64_t* out_bubble, int64_t* out_peak,
+                       void* stream);
+
+/*
  * Local-search chains (§6: every tuning move re-runs the simulator; Algorithm 1's three move
  * families). Chain state record, octo_chain_stride(prob) bytes each, 16-byte aligned:
  *   bytes 0..cand_stride-1  the candidate record (n_pert must be 0), updated in place

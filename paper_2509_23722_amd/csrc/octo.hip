@@ -44,6 +44,8 @@ constexpr int CTL_WORDS = 256;
 struct SimArgs {
   Problem pr;
   const int64_t* pre;    // [(L+1)][3] prefix sums of layer costs
+  const int64_t* pre_mem;  // [(L+1)][2] prefix sums of layer memory (memory-model calls)
+  int64_t* out_peak;       // [n][P] peak bytes per device (memory-model calls)
   const int64_t* link;   // [P][P]
   const uint8_t* cands;
   int64_t n;
@@ -87,17 +89,20 @@ __device__ __forceinline__ void zero_chunks(Chunks<VMAX>& c) {
 #pragma unroll
   for (int k = 0; k < VMAX; ++k) {
     c.st[k] = 0, c.base[k] = 0, c.frow[k] = 0, c.fmask[k] = 0, c.brow[k] = 0, c.bmask[k] = 0;
-    c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = 0;
+    c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = c.mA[k] = 0;
   }
+  c.split = 0;
 }
 
 // Stages of device d (ascending), their durations, incoming link weights and finish-table
-// rows; returns busy(d).
+// rows; returns busy(d). pre_mem (nullable): memory prefix sums; then each chunk's activation
+// bytes go to c.mA and the device's static bytes to *stat.
 template <int VMAX>
 __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr,
                                                 const uint8_t* rec, const int64_t* pre,
                                                 const int64_t* link, int d, int v, int split,
-                                                const Ring& ring) {
+                                                const Ring& ring, const int64_t* pre_mem = nullptr,
+                                                int64_t* stat = nullptr) {
   const int S = pr.P * v, M = pr.M;
   const uint8_t* bnd = rec + 4;
   const uint8_t* dev = rec + 3 + pr.s_max;
@@ -110,7 +115,8 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       ++cnt;
     }
   }
-  int64_t busy = 0;
+  int64_t busy = 0, st_bytes = 0;
+  c.split = split;
 #pragma unroll
   for (int k = 0; k < VMAX; ++k) {
     if (k < v) {
@@ -133,9 +139,25 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       c.wF[k] = dp != d ? link[dp * pr.P + d] : 0;
       c.wB[k] = dn != d ? link[dn * pr.P + d] : 0;
       busy += f + bi + wg;
+      if (pre_mem) {
+        c.mA[k] = pre_mem[2 * b1] - pre_mem[2 * b0];
+        st_bytes += pre_mem[2 * b1 + 1] - pre_mem[2 * b0 + 1];
+      }
     }
   }
+  if (stat) *stat = st_bytes;
   return busy * M;
+}
+
+// One device's results for candidate cand (deadlock: sentinels); MEM adds its peak bytes.
+template <bool MEM>
+__device__ __forceinline__ void put_results(const SimArgs& a, int64_t cand, int d, bool dead,
+                                            int64_t ms, int64_t busy, int64_t stat,
+                                            int64_t peak) {
+  const int P = a.pr.P;
+  if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
+  a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+  if constexpr (MEM) a.out_peak[cand * P + d] = dead ? OCTO_MS_DEADLOCK : stat + peak;
 }
 
 // Group bits for deadlock folding: this lane's group bit and the set of all group bits.
@@ -157,7 +179,7 @@ __device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, i
 // Simulate one candidate per group of the wave with generator kind GEN (40-bit slots shared by
 // the wave's groups; each group's staged record sits in that memory until it is cleared), write
 // the results. cand < 0: this group has no candidate. P2: P and v are powers of two.
-template <int VMAX, int GEN, bool P2>
+template <int VMAX, int GEN, bool P2, bool MEM>
 __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split,
                                               uint8_t* lds_wave) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -177,10 +199,11 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   L.clock = 0;
   L.pos = 0;
   L.nops = 0;
-  int64_t busy = 0;
+  L.mem = L.peak = 0;
+  int64_t busy = 0, stat = 0;
   const bool mine = has && d < P;
   if (mine) {
-    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat);
     L.nops = (split ? 3 : 2) * v * M;
   } else {
     zero_chunks<VMAX>(c);
@@ -196,19 +219,19 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     GenAfab g;
     g.init(v, M);
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   } else if constexpr (GEN == GEN_INTER) {
     const int r = c.st[0];
     if constexpr (P2) {
       GenInterP2 g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     } else {
       GenInter g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     }
   } else {
     GenMerge<VMAX> g;
@@ -216,7 +239,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
            [&](int k) { return pick<VMAX>(c.st, k); });
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX, false>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   }
 
   const int64_t ms = group_max(L.clock, G);
@@ -225,8 +248,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
       // times beyond the 40-bit slots: recompute this candidate with 64-bit slots
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
     } else {
-      if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
-      a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+      put_results<MEM>(a, cand, d, dead, ms, busy, stat, L.peak);
     }
   }
 }
@@ -247,7 +269,7 @@ __device__ __forceinline__ int qt_row(const SimArgs& a, int gen, int v, int spli
 // Table-driven simulation of one candidate per group (INTER or MERGE at v <= 2). Durations and
 // weights must fit 32 bits; a candidate with a larger one, or whose times pass the 40-bit
 // slots, is recomputed on the 64-bit path.
-template <int VMAX>
+template <int VMAX, bool MEM>
 __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, int gen,
                                         int split, uint8_t* lds_wave) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -256,7 +278,8 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   const Table40 T{reinterpret_cast<uint32_t*>(lds_wave),
                   lds_wave + (size_t)a.slots * a.CPW * 4, __ffs(a.CPW) - 1, g < a.CPW ? g : 0};
   uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
-  uint8_t* strm = lds_wave + a.strm_off + lane_id() * 8;
+  constexpr int SREC = MEM ? 16 : 8;  // bytes per stream record
+  uint8_t* strm = lds_wave + a.strm_off + lane_id() * SREC;
   const bool has = cand >= 0;
   const int S = P * v;
   const Ring ring = make_ring(M, a.ring);
@@ -264,11 +287,11 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   __asm__ volatile("" ::: "memory");
 
   Chunks<VMAX> c;
-  int64_t busy = 0;
+  int64_t busy = 0, stat = 0;
   bool fits = true;
   const bool mine = has && d < P;
   if (mine) {
-    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat);
 #pragma unroll
     for (int kind = 0; kind < 3; ++kind) {
 #pragma unroll
@@ -277,8 +300,12 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
           const int64_t w = kind == KF ? c.wF[k] : kind == KB ? c.wB[k] : 0;
           const int64_t du = kind == KF ? c.dF[k] : kind == KB ? c.dB[k] : c.dW[k];
           fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
-          *reinterpret_cast<uint2*>(strm + (kind * v + k) * 512) =
-              make_uint2((uint32_t)w, (uint32_t)du);
+          uint8_t* rec_e = strm + (kind * v + k) * 64 * SREC;
+          *reinterpret_cast<uint2*>(rec_e) = make_uint2((uint32_t)w, (uint32_t)du);
+          if constexpr (MEM) {
+            const int64_t dm = kind == KF ? c.mA[k] : (kind == KB && split) ? 0 : -c.mA[k];
+            *reinterpret_cast<int64_t*>(rec_e + 8) = dm;
+          }
         }
       }
     }
@@ -296,16 +323,15 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
-  int64_t clock = 0;
-  relax_tab(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead);
+  int64_t clock = 0, mem = 0, peak = 0;
+  relax_tab<MEM>(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead, mem, peak);
 
   const int64_t ms = group_max(clock, G);
   if (mine) {
     if (wide || ms >= Table40::LIMIT) {
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
     } else {
-      if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
-      a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+      put_results<MEM>(a, cand, d, dead, ms, busy, stat, peak);
     }
   }
 }
@@ -314,7 +340,9 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
 // Kernels
 // ---------------------------------------------------------------------------------------------
 
-__global__ void k_prep(const int64_t* __restrict__ costs, int L, int64_t* __restrict__ pre,
+// mem (nullable): layer memory [L][2], its prefix sums go to pre_mem.
+__global__ void k_prep(const int64_t* __restrict__ costs, const int64_t* __restrict__ mem, int L,
+                       int64_t* __restrict__ pre, int64_t* __restrict__ pre_mem,
                        int32_t* __restrict__ ctl) {
   const int t = threadIdx.x;
   for (int i = t; i < CTL_WORDS; i += blockDim.x) ctl[i] = 0;
@@ -324,6 +352,14 @@ __global__ void k_prep(const int64_t* __restrict__ costs, int L, int64_t* __rest
     for (int l = 0; l < L; ++l) {
       acc += costs[3 * l + t];
       pre[3 * (l + 1) + t] = acc;
+    }
+  } else if (t < 5 && mem) {
+    const int c = t - 3;
+    int64_t acc = 0;
+    pre_mem[c] = 0;
+    for (int l = 0; l < L; ++l) {
+      acc += mem[2 * l + c];
+      pre_mem[2 * (l + 1) + c] = acc;
     }
   }
 }
@@ -364,7 +400,8 @@ __global__ void k_merge_tab(int P, int M, int v_lo, int v_hi, uint32_t* __restri
   g.init(S, 1, M, d < S ? d : 0, split, split ? d : 0);
   describe<1>(L, c, ring, g.kind, g.k, g.m);
   bool dead = false;
-  relax<1, true>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead, d < S ? tab + d * rowlen : nullptr);
+  relax<1, true, false>(g, c, ring, L, T, WAVE, 1ull, 1ull, dead,
+                        d < S ? tab + d * rowlen : nullptr);
 }
 
 __global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t x) {
@@ -457,6 +494,8 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
     if (!r.valid) {
       a.out_ms[i] = OCTO_MS_INVALID;
       for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
+      if (a.out_peak)
+        for (int d = 0; d < a.pr.P; ++d) a.out_peak[i * a.pr.P + d] = OCTO_MS_INVALID;
     } else {
       bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
     }
@@ -518,19 +557,19 @@ __device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, uint64_
   return -1;
 }
 
-template <int VMAX>
+template <int VMAX, bool MEM>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
                                              int split, uint8_t* lds_wave) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
-  if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false>(a, cand, v, split, lds_wave);
-  else if (p2) run_generated<VMAX, GEN_INTER, true>(a, cand, v, split, lds_wave);
-  else run_generated<VMAX, GEN_INTER, false>(a, cand, v, split, lds_wave);
+  if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false, MEM>(a, cand, v, split, lds_wave);
+  else if (p2) run_generated<VMAX, GEN_INTER, true, MEM>(a, cand, v, split, lds_wave);
+  else run_generated<VMAX, GEN_INTER, false, MEM>(a, cand, v, split, lds_wave);
 }
 
 // Generated-queue simulation (INTER and MERGE) for the bins in a.bin_mask of one v class:
 // VC = 1 (v = 1), 2 (v = 2) or 8 (v = 3..8); finish tables sized for that class with a.ring
-// slots per row.
-template <int VC>
+// slots per row. MEM: also the peak activation memory per device.
+template <int VC, bool MEM>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int g = lane_id() / a.G;
@@ -554,11 +593,11 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     }
     if constexpr (VC <= 2) {
       if (a.qtab) {
-        run_tab<VC>(a, cand, v, gen, split, smem);
+        run_tab<VC, MEM>(a, cand, v, gen, split, smem);
         continue;
       }
     }
-    dispatch_gen<VC>(a, gen, cand, v, split, smem);
+    dispatch_gen<VC, MEM>(a, gen, cand, v, split, smem);
   }
 }
 
@@ -639,7 +678,9 @@ struct AfabRow<0> {
 // zero leaves fin(0, m) = dur + fin(0, m - 1).
 constexpr int64_t AFAB_NO_INPUT = -((int64_t)1 << 62);
 
-template <int MMAX>
+// MEM: a GPipe device holds every micro-batch of all its stages after its forwards, so its peak
+// is its static bytes + M x its stages' activation bytes.
+template <int MMAX, bool MEM>
 __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int lane = lane_id();
@@ -649,6 +690,7 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   row.init(smem, li, lanes);
   int64_t* clk = reinterpret_cast<int64_t*>(smem) + (MMAX == 0 ? (size_t)M * lanes : 0) + li;
   int64_t* bsy = clk + (size_t)P * lanes;  // clk[d * lanes], bsy[d * lanes]
+  int64_t* pk = bsy + (size_t)P * lanes;   // MEM: peak bytes pk[d * lanes]
   for (;;) {
     int ch = 0;
     if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -665,7 +707,10 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
     const uint8_t* bnd = rec + 4;
     const uint8_t* dev = rec + 3 + a.pr.s_max;
     const int S = P * v;
-    for (int d = 0; d < P; ++d) clk[d * lanes] = 0, bsy[d * lanes] = 0;
+    for (int d = 0; d < P; ++d) {
+      clk[d * lanes] = 0, bsy[d * lanes] = 0;
+      if constexpr (MEM) pk[d * lanes] = 0;
+    }
     row.clear(M);
     // rows t = 0..S-1: forwards of stage t; t = S..2S-1: backwards of stage 2S-1-t
     for (int t = 0; t < 2 * S; ++t) {
@@ -677,6 +722,11 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       const int64_t db = a.pre[3 * b1 + 1] - a.pre[3 * b0 + 1] + a.pre[3 * b1 + 2] -
                          a.pre[3 * b0 + 2];
       if (fwd) bsy[d * lanes] += (df + db) * M;
+      if constexpr (MEM) {
+        if (fwd)
+          pk[d * lanes] += (a.pre_mem[2 * b1] - a.pre_mem[2 * b0]) * M +
+                           a.pre_mem[2 * b1 + 1] - a.pre_mem[2 * b0 + 1];
+      }
       // the stage whose finish times this row consumes: st - 1 (forward), st + 1 (backward)
       const int q = fwd ? st - 1 : st + 1;
       const int dq = q >= 0 && q < S && t != S ? dev[q] : d;
@@ -687,6 +737,8 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
     for (int d = 0; d < P; ++d) ms = clk[d * lanes] > ms ? clk[d * lanes] : ms;
     a.out_ms[cand] = ms;
     for (int d = 0; d < P; ++d) a.out_bub[cand * P + d] = ms - bsy[d * lanes];
+    if constexpr (MEM)
+      for (int d = 0; d < P; ++d) a.out_peak[cand * P + d] = pk[d * lanes];
   }
 }
 
@@ -735,7 +787,7 @@ __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
 
 // Candidates with perturbations, then candidates whose times overflowed the 40-bit slots:
 // queues materialised in global memory, moves applied, 64-bit finish tables.
-template <int VMAX>
+template <int VMAX, bool MEM>
 __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -778,11 +830,12 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       const int S = P * v;
       const Ring ring = make_ring(M, M);
       Chunks<VMAX> c;
-      int64_t busy = 0;
+      int64_t busy = 0, stat = 0;
       Lane L;
-      L.clock = 0, L.pos = 0, L.nops = 0;
+      L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
       if (mine) {
-        busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
+        busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem,
+                                  &stat);
         L.nops = materialise<VMAX>(a, c, v, gen, split, row);
         const uint8_t* pp = grec + pert_off(a.pr.s_max);
         const int np = grec[2];
@@ -802,12 +855,9 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       q.init(row, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
       bool dead = false;
-      relax<VMAX, true>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, true, MEM>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       const int64_t ms = group_max(L.clock, G);
-      if (mine) {
-        if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
-        a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
-      }
+      if (mine) put_results<MEM>(a, cand, d, dead, ms, busy, stat, L.peak);
     }
   }
 }
@@ -923,7 +973,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     Chunks<VMAX> c;
     int64_t busy = 0;
     Lane L;
-    L.clock = 0, L.pos = 0, L.nops = 0;
+    L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
     if (run && d < P) {
       busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
       if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, row);
@@ -937,7 +987,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     q.init(row, L.nops);
     describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
     bool dead = false;
-    relax<VMAX, true>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, true, false>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     const int64_t ms = group_max(L.clock, G);
 
     if (!has || skip) continue;
@@ -1088,7 +1138,7 @@ size_t mtab_entries(const octo_problem* p) {
 
 // Workspace layout (byte offsets).
 struct Layout {
-  size_t ctl, pre, bin_of, idx, redo, qscr, total;
+  size_t ctl, pre, pre_mem, bin_of, idx, redo, qscr, total;
 };
 
 Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slots) {
@@ -1098,6 +1148,8 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   o = align_up(o + CTL_WORDS * 4, 256);
   l.pre = o;
   o = align_up(o + (size_t)(p->L + 1) * 3 * 8, 256);
+  l.pre_mem = o;
+  o = align_up(o + (size_t)(p->L + 1) * 2 * 8, 256);
   l.bin_of = o;
   o = align_up(o + (size_t)n, 256);
   l.idx = o;
@@ -1156,7 +1208,8 @@ struct Setup {
 
 template <int VC>
 int mat_grid_for(const Plan& big, int cus, int* g) {
-  return occupancy_grid(k_sim_mat<VC>, big.lds_bytes, cus, g);
+  // the memory-model variant is sized the same way; its grid is taken for both
+  return occupancy_grid(k_sim_mat<VC, true>, big.lds_bytes, cus, g);
 }
 
 // Largest number of micro-batches of one stage in flight over one device queue of the
@@ -1212,10 +1265,11 @@ struct TabGeom {
   Plan plan;
   int lg;
 };
-TabGeom tab_geom(const octo_problem* p, int lds_max, int v) {
+// mem: 16-byte stream records (two 8-byte units) with the activation delta.
+TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool mem) {
   TabGeom t;
   t.ring = make_ring(p->M, v * p->P);
-  t.plan = fast_plan(p, lds_max, v * p->P, t.ring.R, 3 * v);
+  t.plan = fast_plan(p, lds_max, v * p->P, t.ring.R, 3 * v * (mem ? 2 : 1));
   t.lg = t.plan.CPW > 0 ? __builtin_ctz(t.plan.CPW) : 0;
   return t;
 }
@@ -1223,9 +1277,9 @@ TabGeom tab_geom(const octo_problem* p, int lds_max, int v) {
 // Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), encoded for
 // each v's launch geometry; rebuilt when (P, v_max, M), the geometry or the MERGE tables
 // change. Entry offsets are kept in the workspace.
-int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, hipStream_t stream) {
+int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool mem, hipStream_t stream) {
   const int P = p->P, M = p->M, vmax2 = std::min(p->v_max, 2);
-  TabGeom geo[2] = {tab_geom(p, lds_max, 1), tab_geom(p, lds_max, 2)};
+  TabGeom geo[2] = {tab_geom(p, lds_max, 1, mem), tab_geom(p, lds_max, 2, mem)};
   bool same = ws.qt_valid && ws.qt_P == P && ws.qt_vmax == p->v_max && ws.qt_M == M;
   for (int v = 1; v <= vmax2; ++v)
     same = same && ws.qt_R[v - 1] == geo[v - 1].ring.R && ws.qt_lg[v - 1] == geo[v - 1].lg;
@@ -1274,8 +1328,9 @@ int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, hipStream_t st
 
 // Shared front half of octo_sim_batch and octo_tune_step: device, plans, workspace, prefix
 // sums, MERGE tables.
-int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, int64_t n,
-            Setup* su) {
+// mem (nullable): layer memory [L][2], prefix-summed next to the costs.
+int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
+            hipStream_t stream, int64_t n, Setup* su) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
   int rc = dev_info(dev, &su->di);
@@ -1291,8 +1346,9 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
   if (rc) return rc;
   su->ws = &ws;
   char* base = static_cast<char*>(ws.base);
-  hipLaunchKernelGGL(k_prep, dim3(1), dim3(256), 0, stream, costs, prob->L,
+  hipLaunchKernelGGL(k_prep, dim3(1), dim3(256), 0, stream, costs, mem, prob->L,
                      reinterpret_cast<int64_t*>(base + su->l.pre),
+                     reinterpret_cast<int64_t*>(base + su->l.pre_mem),
                      reinterpret_cast<int32_t*>(base + su->l.ctl));
   if ((rc = launch_ok())) return rc;
   if (prob->v_max >= 2) {
@@ -1318,13 +1374,16 @@ int prepare(const octo_problem* prob, const int64_t* costs, hipStream_t stream, 
 }
 
 SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, const int64_t* link,
-                  const void* cands, int64_t n, int64_t* ms, int64_t* bub) {
+                  const void* cands, int64_t n, int64_t* ms, int64_t* bub,
+                  int64_t* peak = nullptr) {
   char* base = static_cast<char*>(su.ws->base);
   const Layout& l = su.l;
   SimArgs a;
   a.pr = Problem{prob->L, prob->P, prob->v_max, prob->M, prob->cand_stride, prob->max_pert,
                  prob->P * prob->v_max};
   a.pre = reinterpret_cast<const int64_t*>(base + l.pre);
+  a.pre_mem = peak ? reinterpret_cast<const int64_t*>(base + l.pre_mem) : nullptr;
+  a.out_peak = peak;
   a.link = link;
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
@@ -1369,24 +1428,24 @@ uint64_t bins_of(int v_lo, int v_hi, bool afab) {
 // Launch k_sim<VC> over the generated bins in `mask` with its own 40-bit plan: s_cap stages of
 // ring_want (rounded up to a power of two, or M) slots; bins whose in-flight bound exceeds the
 // ring go to the 64-bit path.
-template <int VC>
+template <int VC, bool MEM>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-               int64_t n, int64_t* ms, int64_t* bub, int s_cap, int ring_want, uint64_t mask,
-               int work, hipStream_t stream) {
+               int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int s_cap, int ring_want,
+               uint64_t mask, int work, hipStream_t stream) {
   const Ring ring = make_ring(prob->M, ring_want);
   // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS and need tables
   // encoded for exactly this geometry
   bool tab = false;
   Plan pl{};
   if (VC <= 2 && su.ws->qt_valid) {
-    const TabGeom geo = tab_geom(prob, su.di.lds_max, VC);
+    const TabGeom geo = tab_geom(prob, su.di.lds_max, VC, MEM);
     tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[VC - 1] == geo.ring.R &&
           su.ws->qt_lg[VC - 1] == geo.lg && geo.plan.G * geo.plan.CPW <= WAVE;
     pl = geo.plan;
   }
   if (!tab) pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R, 0);
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
-  SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub);
+  SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub, peak);
   if (tab) a.qtab = static_cast<const uint32_t*>(su.ws->qt);
   a.bin_mask = mask, a.work = work;
   a.ring = ring.R;
@@ -1395,40 +1454,41 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
     if (((mask >> b) & 1) && ring.R < prob->M && su.ws->inflight[b] > ring.R)
       a.redo_bins |= 1ull << b;
   int grid = 0;
-  int rc = occupancy_grid(k_sim<VC>, pl.lds_bytes, su.di.cus, &grid);
+  int rc = occupancy_grid(k_sim<VC, MEM>, pl.lds_bytes, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  hipLaunchKernelGGL(k_sim<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
+  hipLaunchKernelGGL((k_sim<VC, MEM>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
   return launch_ok();
 }
 
 // Launch k_afab over the AFAB bins of every v: one lane per candidate, each lane's row of M
 // int64 plus 2 P device words in LDS (at most 64 KiB per wave).
+template <bool MEM>
 int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-                int64_t n, int64_t* ms, int64_t* bub, hipStream_t stream) {
+                int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, hipStream_t stream) {
   // rows of exactly 32 or 64 micro-batches live in registers; other lengths in LDS
   const int mmax = prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
-  const size_t per_lane = (size_t)((mmax ? 0 : prob->M) + 2 * prob->P) * 8;
+  const size_t per_lane = (size_t)((mmax ? 0 : prob->M) + (MEM ? 3 : 2) * prob->P) * 8;
   const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
   const int lds = (int)(lanes * per_lane);
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
-  SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
+  SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub, peak);
   a.bin_mask = bins_of(1, prob->v_max, true);
   a.work = CTL_WORK + 3;
   int grid = 0;
-  int rc = mmax == 32   ? occupancy_grid(k_afab<32>, lds, su.di.cus, &grid)
-           : mmax == 64 ? occupancy_grid(k_afab<64>, lds, su.di.cus, &grid)
-                        : occupancy_grid(k_afab<0>, lds, su.di.cus, &grid);
+  int rc = mmax == 32   ? occupancy_grid(k_afab<32, MEM>, lds, su.di.cus, &grid)
+           : mmax == 64 ? occupancy_grid(k_afab<64, MEM>, lds, su.di.cus, &grid)
+                        : occupancy_grid(k_afab<0, MEM>, lds, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + lanes - 1) / lanes;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
   if (mmax == 32)
-    hipLaunchKernelGGL(k_afab<32>, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+    hipLaunchKernelGGL((k_afab<32, MEM>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   else if (mmax == 64)
-    hipLaunchKernelGGL(k_afab<64>, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+    hipLaunchKernelGGL((k_afab<64, MEM>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   else
-    hipLaunchKernelGGL(k_afab<0>, dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+    hipLaunchKernelGGL((k_afab<0, MEM>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   return launch_ok();
 }
 
@@ -1448,6 +1508,73 @@ int record_mark(int i, hipStream_t stream) {
   if (i < g_prof_n && g_prof[i] && hipEventRecord(g_prof[i], stream) != hipSuccess)
     return OCTO_EHIP;
   return OCTO_OK;
+}
+
+// The batch evaluation behind octo_sim_batch (MEM = false) and octo_sim_batch_mem.
+template <bool MEM>
+int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
+                   const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
+                   int64_t* out_bubble, int64_t* out_peak, hipStream_t stream) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
+  if (n == 0) return OCTO_OK;
+  if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
+  if (MEM && (!layer_mem || !out_peak)) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
+  std::lock_guard<std::mutex> lock(g_mu);
+  Setup su;
+  rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, n, &su);
+  if (rc) return rc;
+  char* base = static_cast<char*>(su.ws->base);
+  int64_t* pk = MEM ? out_peak : nullptr;
+  SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble, pk);
+  const int tb = CLS_THREADS;
+  const int nb = (int)((n + tb - 1) / tb);
+  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
+  const int hb = (int)align_up((size_t)pert_off(prob->P * prob->v_max), 16);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, tb * hb);
+  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), tb * hb, stream, a, bins, hb);
+  if ((rc = launch_ok())) return rc;
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, a.ctl);
+  if ((rc = launch_ok())) return rc;
+  hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
+                     reinterpret_cast<int32_t*>(base + su.l.idx));
+  if ((rc = launch_ok())) return rc;
+  // generated INTER / MERGE queues, one launch per v class with finish tables sized for it:
+  // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
+  // materialised queues (perturbations, 64-bit redo).
+  compute_inflight(prob, *su.ws);
+  if ((rc = build_qtab(prob, *su.ws, su.di.lds_max, MEM, stream))) return rc;
+  const int P = prob->P, M = prob->M;
+  if ((rc = record_mark(0, stream))) return rc;
+  if (prob->v_max >= 2 &&
+      (rc = launch_sim<2, MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk,
+                               2 * P, 2 * P, bins_of(2, 2, false), CTL_WORK + 1, stream)))
+    return rc;
+  if ((rc = record_mark(1, stream))) return rc;
+  if ((rc = launch_sim<1, MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, P, P,
+                               bins_of(1, 1, false), CTL_WORK + 0, stream)))
+    return rc;
+  if ((rc = record_mark(2, stream))) return rc;
+  if (prob->v_max >= 3 &&
+      (rc = launch_sim<8, MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk,
+                               P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
+    return rc;
+  if ((rc = record_mark(3, stream))) return rc;
+  if ((rc = launch_afab<MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk,
+                             stream)))
+    return rc;
+  if ((rc = record_mark(4, stream))) return rc;
+  if (prob->v_max <= 2)
+    hipLaunchKernelGGL((k_sim_mat<2, MEM>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((k_sim_mat<8, MEM>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
+                       stream, a);
+  if ((rc = launch_ok())) return rc;
+  return record_mark(5, stream);
 }
 
 }  // namespace
@@ -1479,63 +1606,17 @@ int32_t octo_queue_capacity(const octo_problem* prob) {
 
 int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
-                   void* stream_) {
-  int rc = check_problem(prob);
-  if (rc) return rc;
-  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
-  if (n == 0) return OCTO_OK;
-  if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
-  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
-  hipStream_t stream = static_cast<hipStream_t>(stream_);
-  std::lock_guard<std::mutex> lock(g_mu);
-  Setup su;
-  rc = prepare(prob, layer_costs, stream, n, &su);
-  if (rc) return rc;
-  char* base = static_cast<char*>(su.ws->base);
-  SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble);
-  const int tb = CLS_THREADS;
-  const int nb = (int)((n + tb - 1) / tb);
-  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
-  const int hb = (int)align_up((size_t)pert_off(prob->P * prob->v_max), 16);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, tb * hb);
-  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), tb * hb, stream, a, bins, hb);
-  if ((rc = launch_ok())) return rc;
-  hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, a.ctl);
-  if ((rc = launch_ok())) return rc;
-  hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
-                     reinterpret_cast<int32_t*>(base + su.l.idx));
-  if ((rc = launch_ok())) return rc;
-  // generated INTER / MERGE queues, one launch per v class with finish tables sized for it:
-  // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
-  // materialised queues (perturbations, 64-bit redo).
-  compute_inflight(prob, *su.ws);
-  if ((rc = build_qtab(prob, *su.ws, su.di.lds_max, stream))) return rc;
-  const int P = prob->P, M = prob->M;
-  if ((rc = record_mark(0, stream))) return rc;
-  if (prob->v_max >= 2 &&
-      (rc = launch_sim<2>(prob, su, link, candidates, n, out_makespan, out_bubble, 2 * P, 2 * P,
-                          bins_of(2, 2, false), CTL_WORK + 1, stream)))
-    return rc;
-  if ((rc = record_mark(1, stream))) return rc;
-  if ((rc = launch_sim<1>(prob, su, link, candidates, n, out_makespan, out_bubble, P, P,
-                          bins_of(1, 1, false), CTL_WORK + 0, stream)))
-    return rc;
-  if ((rc = record_mark(2, stream))) return rc;
-  if (prob->v_max >= 3 &&
-      (rc = launch_sim<8>(prob, su, link, candidates, n, out_makespan, out_bubble,
-                          P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
-    return rc;
-  if ((rc = record_mark(3, stream))) return rc;
-  if ((rc = launch_afab(prob, su, link, candidates, n, out_makespan, out_bubble, stream)))
-    return rc;
-  if ((rc = record_mark(4, stream))) return rc;
-  if (prob->v_max <= 2)
-    hipLaunchKernelGGL(k_sim_mat<2>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
-  else
-    hipLaunchKernelGGL(k_sim_mat<8>, dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes, stream, a);
-  if ((rc = launch_ok())) return rc;
-  return record_mark(5, stream);
+                   void* stream) {
+  return sim_batch_impl<false>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                               out_bubble, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
+                       const int64_t* layer_mem, const int64_t* link, const void* candidates,
+                       int64_t n, int64_t* out_makespan, int64_t* out_bubble, int64_t* out_peak,
+                       void* stream) {
+  return sim_batch_impl<true>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
+                              out_bubble, out_peak, static_cast<hipStream_t>(stream));
 }
 
 int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
@@ -1550,7 +1631,7 @@ int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const i
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   std::lock_guard<std::mutex> lock(g_mu);
   Setup su;
-  rc = prepare(prob, layer_costs, stream, 0, &su);
+  rc = prepare(prob, layer_costs, nullptr, stream, 0, &su);
   if (rc) return rc;
   TuneArgs t;
   t.s = make_args(prob, su.big, su, link, nullptr, 0, nullptr, nullptr);

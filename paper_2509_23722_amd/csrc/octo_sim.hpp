@@ -113,6 +113,8 @@ struct Chunks {
   int fmask[VMAX];                   // state bits a forward needs (0: always ready)
   int brow[VMAX], bmask[VMAX];       // backward read row offset / needed state bits
   int64_t dF[VMAX], dB[VMAX], dW[VMAX], wF[VMAX], wB[VMAX];
+  int64_t mA[VMAX];                  // activation bytes of the stage per micro-batch
+  int split;                         // backward split into B and W
 };
 
 // Descriptor of one op: slot read, slot written, readiness test (slot & mask) == want, edge
@@ -121,7 +123,9 @@ struct Desc {
   int rd, wr, mask, want, store;
   uint32_t state;  // state bits written on finish
   int64_t w, dur;
+  int64_t dm;      // activation bytes the op allocates (> 0) or releases (< 0)
   __device__ __forceinline__ void take_if(bool t, const Desc& o) {
+    dm = t ? o.dm : dm;
     rd = t ? o.rd : rd;
     wr = t ? o.wr : wr;
     mask = t ? o.mask : mask;
@@ -136,6 +140,7 @@ struct Desc {
 struct Lane : Desc {
   int64_t clock;
   int pos, nops;
+  int64_t mem, peak;  // activation bytes held now / at most (memory-model variants)
 };
 
 template <int VMAX, typename T>
@@ -165,6 +170,10 @@ __device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, const R
   const int64_t df = pick<VMAX>(c.dF, k), db = pick<VMAX>(c.dB, k), dw = pick<VMAX>(c.dW, k);
   L.w = isF ? wf : isB ? wb : 0;
   L.dur = isF ? df : isB ? db : dw;
+  // memory nodes: a forward allocates its stage's activations, the last backward op of the
+  // micro-batch (B fused, W split) releases them
+  const int64_t a = pick<VMAX>(c.mA, k);
+  L.dm = isF ? a : (isB && c.split) ? 0 : -a;
 }
 
 // Fold every G-lane group of a 64-bit lane mask into the group's lowest bit.
@@ -180,7 +189,8 @@ __device__ __forceinline__ uint64_t fold_groups(uint64_t x, int G, uint64_t lsb)
 // only if this op completes (pays when one wave per SIMD must hide the LDS latency itself);
 // otherwise advance and describe after the readiness test (fewer instructions per round, the
 // latency hidden by other waves).
-template <int VMAX, bool SPEC, class Tab, class Gen>
+// MEM: also track the activation bytes each device holds (L.mem) and their maximum (L.peak).
+template <int VMAX, bool SPEC, bool MEM, class Tab, class Gen>
 __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
                                       const Tab& T, int G, uint64_t gbit, uint64_t lsb,
                                       bool& dead, uint32_t* rec) {
@@ -206,6 +216,10 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
     if (rec && ok)
       rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)gen.kind << 12) | (uint32_t)gen.m;
     L.clock = ok ? fin : L.clock;
+    if constexpr (MEM) {
+      L.mem = ok ? L.mem + L.dm : L.mem;
+      L.peak = L.mem > L.peak ? L.mem : L.peak;
+    }
     L.pos += ok ? 1 : 0;
     live = L.pos < L.nops;
     if constexpr (SPEC) {
@@ -233,7 +247,8 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
 //   wanted values | 23-25 state bits written, parity included (0 = writes nothing) |
 //   26-28 stream e = kind * v + chunk.
 // The candidate's per-stream input weight and duration (32-bit) sit in LDS, 64 lanes
-// interleaved: the pair of lane l for stream e at byte e * 512 + l * 8.
+// interleaved: the pair of lane l for stream e at byte e * 512 + l * 8 (memory-model variants:
+// 16-byte records {w, dur, activation delta} at e * 1024 + l * 16).
 // ------------------------------------------------------------------------------------------
 __host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, int v, int s,
                                                       int S, const Ring& ring, int lg) {
@@ -270,10 +285,13 @@ constexpr uint32_t QT_END = 1u << 20;
 // nothing: the slot is empty or holds the backward of micro-batch m - R, which this device has
 // already run, so its time never exceeds the device clock. Each round decodes its op first, so
 // the stream read and the slot read are in flight together, and loads the entry after next at
-// its start, to be committed at its end. Rl = R << lg.
+// its start, to be committed at its end. Rl = R << lg. MEM: streams are 16-byte records
+// {w, dur, activation delta}; mem / peak track the activation bytes held.
+template <bool MEM>
 __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint32_t row, int Rl,
                                           const uint8_t* strm, int64_t& clock, const Table40& T,
-                                          int G, uint64_t gbit, uint64_t lsb, bool& dead) {
+                                          int G, uint64_t gbit, uint64_t lsb, bool& dead,
+                                          int64_t& mem, int64_t& peak) {
   uint32_t cur = qt[row], nxt = qt[row + 1u];
   uint32_t qa = row + 2u;  // entry after next
   for (;;) {
@@ -282,7 +300,8 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
     const int rdj = (int)(cur & 0x7FFFu) | T.g;
     const int wrj = rdj + __mul24((int)((cur >> 15) & 3u), Rl) - Rl;
     const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
-    const uint2 wd = *reinterpret_cast<const uint2*>(strm + ((cur >> 17) & 0xE00u));
+    const uint32_t soff = MEM ? ((cur >> 16) & 0x1C00u) : ((cur >> 17) & 0xE00u);
+    const uint2 wd = *reinterpret_cast<const uint2*>(strm + soff);
     const uint32_t plo = T.lo[rdj], phi = T.hi[rdj];
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
     const bool ok = (plo & mask) == want;
@@ -294,6 +313,11 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
       T.hi[wrj] = (uint8_t)((uint64_t)fin >> 29);
     }
     clock = ok ? fin : clock;
+    if constexpr (MEM) {
+      const int64_t dm = *reinterpret_cast<const int64_t*>(strm + soff + 8);
+      mem = ok ? mem + dm : mem;
+      peak = mem > peak ? mem : peak;
+    }
     qa += ok ? 1u : 0u;
     cur = ok ? nxt : cur;
     nxt = ok ? ahead : nxt;

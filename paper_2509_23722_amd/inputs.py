@@ -150,8 +150,13 @@ WORKLOADS = {
 }
 
 
-def layer_costs(w: Workload):
-    """int64 [L, 3] = {F, B, W} per layer for workload w."""
+def layer_costs(w: Workload, with_types=False):
+    """int64 [L, 3] = {F, B, W} per layer for workload w (and the layer types, if asked)."""
+    f, types = _layer_draws(w)
+    return (_fbw(f), types) if with_types else _fbw(f)
+
+
+def _layer_draws(w: Workload):
     rng = np.random.default_rng(w.seed)
     L = w.L
     if w.key == 1:
@@ -159,15 +164,17 @@ def layer_costs(w: Workload):
         for i in range(L):
             lo, hi = (800, 1200) if i % 2 == 0 else (1500, 2500)
             f[i] = int(rng.integers(lo, hi, endpoint=True)) * 1000
-        return _fbw(f)
+        return f, ["dense" if i % 2 == 0 else "moe" for i in range(L)]
     if w.key == 2:
         sig = 0.15
         f = np.empty(L, dtype=np.int64)
+        types = []
         for i in range(L):
             mixer = "attention" if i % 8 == 0 else "mamba"
             ffn = "moe" if i % 2 == 1 else "dense"
             f[i] = _lognormal_ns(rng, MEAN_NS[mixer], sig) + _lognormal_ns(rng, MEAN_NS[ffn], sig)
-        return _fbw(f)
+            types.append(mixer + "+" + ffn)
+        return f, types
     if w.key == 3:
         sig = 0.15
         n_attn = int(round(0.08 * L))
@@ -180,21 +187,48 @@ def layer_costs(w: Workload):
                 types.append("mamba" if alt % 2 == 0 else "dense")
                 alt += 1
         f = np.array([_lognormal_ns(rng, MEAN_NS[t], sig) for t in types], dtype=np.int64)
-        return _fbw(f)
+        return f, types
     if w.key == 4:
         sig = 0.2
         types = ["dense"] * 3 + ["moe"] * (L - 3)
         f = np.array([_lognormal_ns(rng, MEAN_NS[t], sig) for t in types], dtype=np.int64)
         f[0] += 3 * _lognormal_ns(rng, MEAN_NS["dense"], sig)      # embedding
         f[L - 1] += 3 * _lognormal_ns(rng, MEAN_NS["dense"], sig)  # LM head
-        return _fbw(f)
+        return f, types
     if w.key == 5:
         sig = 0.15
         names = ["attention", "mamba", "moe", "dense"]
         idx = rng.choice(4, size=L, p=[0.2, 0.3, 0.3, 0.2])
         f = np.array([_lognormal_ns(rng, MEAN_NS[names[k]], sig) for k in idx], dtype=np.int64)
-        return _fbw(f)
+        return f, [names[k] for k in idx]
     raise KeyError(w.key)
+
+
+# Memory per layer type, as multiples of one micro-batch's inter-stage activation (activation
+# bytes a layer keeps for its backward) and static GiB (weights, gradients and optimizer state).
+MEM_ACT = {"attention": 3.0, "mamba": 2.0, "moe": 2.5, "dense": 2.0}
+MEM_STATIC_GIB = {"attention": 1.0, "mamba": 0.8, "moe": 6.0, "dense": 1.5}
+
+
+def layer_mem(w: Workload):
+    """int64 [L, 2] = {activation bytes per micro-batch, static bytes} per layer for workload w:
+    per-type means (a combined "mixer+ffn" layer sums both parts), lognormal sigma 0.1, drawn
+    from their own seed so that the cost tables stay as they are."""
+    _, types = layer_costs(w, with_types=True)
+    rng = np.random.default_rng(w.seed + 3000)
+    act = np.empty(w.L, dtype=np.int64)
+    st = np.empty(w.L, dtype=np.int64)
+    for i, t in enumerate(types):
+        parts = t.split("+")
+        a = sum(MEM_ACT[p] for p in parts) * w.act_bytes
+        g = sum(MEM_STATIC_GIB[p] for p in parts) * (1 << 30)
+        act[i] = int(np.rint(a * np.exp(0.1 * rng.standard_normal())))
+        st[i] = int(np.rint(g * np.exp(0.1 * rng.standard_normal())))
+    # embedding and LM head of the DeepSeek-V3-like model carry large tables
+    if w.key == 4:
+        st[0] += 2 << 30
+        st[w.L - 1] += 2 << 30
+    return np.stack([act, st], axis=1)
 
 
 # ---------------------------------------------------------------------------------------------
