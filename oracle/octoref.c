@@ -451,18 +451,23 @@ static int build_local_queues(const ref_problem* pr, const ref_cand* c, ref_op* 
 }
 
 /* Apply the perturbation moves in order. Returns 0, or REF_EINVAL if one is out of range. */
+/* Move entry `from` of a queue row so that it ends at index `to`; the entries between shift by
+ * one place. */
+static void move_op(ref_op* row, int from, int to) {
+  ref_op moved = row[from];
+  if (from < to)
+    memmove(row + from, row + from + 1, sizeof(ref_op) * (size_t)(to - from));
+  else if (from > to)
+    memmove(row + to + 1, row + to, sizeof(ref_op) * (size_t)(from - to));
+  row[to] = moved;
+}
+
 static int apply_perturbations(const ref_problem* pr, const ref_cand* c, ref_op* q, int qcap,
                                const int* qlen) {
   for (int i = 0; i < c->n_pert; ++i) {
     int d = c->pert[i][0], from = c->pert[i][1], to = c->pert[i][2];
     if (d >= pr->P || from >= qlen[d] || to >= qlen[d]) return REF_EINVAL;
-    ref_op* row = q + (size_t)d * qcap;
-    ref_op moved = row[from];
-    if (from < to)
-      memmove(row + from, row + from + 1, sizeof(ref_op) * (size_t)(to - from));
-    else if (from > to)
-      memmove(row + to + 1, row + to, sizeof(ref_op) * (size_t)(from - to));
-    row[to] = moved;
+    move_op(q + (size_t)d * qcap, from, to);
   }
   return 0;
 }
@@ -501,7 +506,7 @@ static int cmp_event(const void* a, const void* b) {
 
 static void peak_memory(const ref_dag_in* g, const ref_sop* sq, const int* qoff, const int* qlen,
                         const int64_t* start, const int64_t* act, const int64_t* stat,
-                        int64_t* peak) {
+                        int64_t* peak, int* ppos) {
   for (int d = 0; d < g->P; ++d) {
     int64_t base = 0;
     for (int s = 0; s < g->S; ++s)
@@ -518,20 +523,24 @@ static void peak_memory(const ref_dag_in* g, const ref_sop* sq, const int* qoff,
     }
     qsort(ev, ne, sizeof(mem_event), cmp_event);
     int64_t cur = 0, hi = 0;
+    int at = -1;
     for (int i = 0; i < ne; ++i) {
       cur += ev[i].delta;
-      if (cur > hi) hi = cur;
+      if (cur > hi) hi = cur, at = ev[i].key / 2;
     }
     peak[d] = base + hi;
+    if (ppos) ppos[d] = at; /* queue position of the allocation that first reaches the peak */
     free(ev);
   }
 }
 
 /* Evaluate a candidate given its local queues (after perturbations). mem (nullable): layer
- * memory [L][2] = {activation bytes per micro-batch, static bytes}; then peak[P] is filled. */
+ * memory [L][2] = {activation bytes per micro-batch, static bytes}; then peak[P] is filled, and
+ * ppos[P] (nullable) with the queue position at which each device first reaches its peak (-1
+ * when it holds no activations). */
 static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                       const int64_t* link, const ref_op* q, int qcap, const int* qlen,
-                      const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak) {
+                      const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos) {
   int P = pr->P, S = c->S, split;
   resolve(pr, c, &split);
   int64_t F[64], B[64], W[64];
@@ -558,7 +567,7 @@ static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* c
       act[s] = stat[s] = 0;
       for (int l = c->b[s]; l < c->b[s + 1]; ++l) act[s] += mem[2 * l], stat[s] += mem[2 * l + 1];
     }
-    peak_memory(&g, sq, qoff, qlen, start, act, stat, peak);
+    peak_memory(&g, sq, qoff, qlen, start, act, stat, peak, ppos);
   }
   free(start);
   free(sq);
@@ -583,7 +592,7 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
         apply_perturbations(pr, c, q, qcap, qlen) != 0) {
       sentinel = REF_INVALID;
     } else {
-      int rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak);
+      int rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL);
       if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
       else if (rc != SIM_OK) sentinel = REF_INVALID;
     }
@@ -596,6 +605,93 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
       for (int d = 0; d < P; ++d) peak[d] = sentinel;
   }
   free(c);
+}
+
+/* ------------------------------------------------------------------------------------------ */
+/* Selective W advancing (§6 "Scheduling Tuning", the third policy; §6 Eq. 2's capacity bound). */
+/* While some device's peak exceeds its capacity, take the lowest-numbered such device and the */
+/* queue position p at which its running activation total first reaches the peak (an F). A W   */
+/* of that device is eligible when it sits after p, its B sits before p (so its stage's         */
+/* activations are held at p) and the stage holds activations; advancing it moves it to index  */
+/* p, so its release comes before that allocation. Eligible W are tried in queue order: the     */
+/* first whose advance does not lengthen the makespan is taken (a device's busy time is fixed,  */
+/* so then no bubble grows); if every one lengthens it, the first (earliest) is taken. Repeat   */
+/* until all devices fit, nothing is eligible, or max_adv advances have been made.              */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct {
+  int d, from, to;
+} ref_move;
+
+/* Runs the policy on queues q (changed in place). Returns the evaluation status (SIM_OK,
+ * SIM_CYCLE, SIM_BADQ) of the given queues; on SIM_OK, ms/bub/peak describe the final queues,
+ * *fits tells whether every device is within cap, and moves (nullable) receives the advances,
+ * *n_moves of them, as perturbation triples (device, from, to). */
+static int advance_w(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
+                     const int64_t* mem, const int64_t* cap, const int64_t* link, ref_op* q,
+                     int qcap, const int* qlen, int max_adv, int64_t* ms, int64_t* bub,
+                     int64_t* peak, int* fits, ref_move* moves, int* n_moves) {
+  const int P = pr->P, M = pr->M;
+  int ppos[64];
+  *n_moves = 0;
+  *fits = 0;
+  int rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, ppos);
+  if (rc != SIM_OK) return rc;
+  int64_t act[64];
+  for (int s = 0; s < c->S; ++s) {
+    act[s] = 0;
+    for (int l = c->b[s]; l < c->b[s + 1]; ++l) act[s] += mem[2 * l];
+  }
+  int* posB = (int*)malloc(sizeof(int) * (size_t)c->v * M);
+  int64_t tms, tbub[64], tpeak[64];
+  int tpos[64];
+  for (;;) {
+    int d = -1;
+    for (int e = 0; e < P; ++e)
+      if (peak[e] > cap[e]) {
+        d = e;
+        break;
+      }
+    if (d < 0) {
+      *fits = 1;
+      break;
+    }
+    if (*n_moves >= max_adv || ppos[d] < 0) break;
+    const int p = ppos[d];
+    ref_op* row = q + (size_t)d * qcap;
+    int A[64];
+    stages_of(c, d, A);
+    for (int i = 0; i < c->v * M; ++i) posB[i] = qlen[d];
+    for (int i = 0; i < qlen[d]; ++i)
+      if (row[i].kind == KB) posB[row[i].chunk * M + row[i].m] = i;
+    int first = -1, chosen = -1;
+    for (int j = p + 1; j < qlen[d]; ++j) {
+      const ref_op o = row[j];
+      if (o.kind != KW || act[A[o.chunk]] <= 0 || posB[o.chunk * M + o.m] > p) continue;
+      if (first < 0) first = j;
+      move_op(row, j, p);
+      rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, &tms, tbub, tpeak, tpos);
+      if (rc == SIM_OK && tms <= *ms) {
+        chosen = j;
+        break;
+      }
+      move_op(row, p, j);
+    }
+    if (first < 0) break;
+    if (chosen < 0) {
+      chosen = first;
+      move_op(row, first, p);
+      rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, &tms, tbub, tpeak, tpos);
+    }
+    /* a W has no consumers, so advancing it past other ops of its device creates no cycle */
+    if (rc != SIM_OK) break;
+    *ms = tms;
+    for (int e = 0; e < P; ++e) bub[e] = tbub[e], peak[e] = tpeak[e], ppos[e] = tpos[e];
+    if (moves) moves[*n_moves] = (ref_move){d, chosen, p};
+    ++*n_moves;
+  }
+  free(posB);
+  return rc;
 }
 
 static int check_problem(const ref_problem* pr) {
@@ -662,6 +758,99 @@ int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t*
                      const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                      int nthreads) {
   return oracle_sim_batch_mem(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, nthreads);
+}
+
+/* Selective W advancing on a batch of candidate records. Each record's queues (policy, then its
+ * perturbations) are repaired with at most max_pert - n_pert advances, which are appended to the
+ * record as perturbations (out_cands, same stride; the bytes after the last used perturbation
+ * are copied unchanged). out_ms/out_bub/out_peak describe the output record; deadlocked or
+ * invalid records are copied unchanged with the sentinels. cap: int64 [P] bytes per device. */
+typedef struct {
+  const ref_problem* pr;
+  const int64_t *costs, *mem, *cap, *link;
+  const uint8_t* cands;
+  uint8_t* out_cands;
+  int64_t lo, hi;
+  int64_t *out_ms, *out_bub, *out_peak;
+} advance_job;
+
+static void advance_record(const advance_job* j, int64_t i) {
+  const ref_problem* pr = j->pr;
+  const int P = pr->P;
+  const uint8_t* rec = j->cands + (size_t)i * pr->cand_stride;
+  uint8_t* out = j->out_cands + (size_t)i * pr->cand_stride;
+  int64_t* ms = j->out_ms + i;
+  int64_t* bub = j->out_bub + (size_t)i * P;
+  int64_t* peak = j->out_peak + (size_t)i * P;
+  memmove(out, rec, (size_t)pr->cand_stride);
+  ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
+  decode(pr, out, c);
+  int64_t sentinel = 0;
+  if (!valid_structure(pr, c)) {
+    sentinel = REF_INVALID;
+  } else {
+    int qcap = 3 * c->v * pr->M;
+    ref_op* q = (ref_op*)malloc(sizeof(ref_op) * (size_t)qcap * P);
+    int qlen[64];
+    if (build_local_queues(pr, c, q, qcap, qlen) != 0 ||
+        apply_perturbations(pr, c, q, qcap, qlen) != 0) {
+      sentinel = REF_INVALID;
+    } else {
+      const int room = pr->max_pert - c->n_pert;
+      ref_move* mv = (ref_move*)malloc(sizeof(ref_move) * (size_t)(room > 0 ? room : 1));
+      int fits, nm;
+      int rc = advance_w(pr, c, j->costs, j->mem, j->cap, j->link, q, qcap, qlen, room, ms, bub,
+                         peak, &fits, mv, &nm);
+      if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
+      else if (rc != SIM_OK) sentinel = REF_INVALID;
+      else {
+        uint8_t* pp = out + pert_offset(P * pr->v_max) + 6 * c->n_pert;
+        for (int k = 0; k < nm; ++k) {
+          const int f[3] = {mv[k].d, mv[k].from, mv[k].to};
+          for (int t = 0; t < 3; ++t) pp[6 * k + 2 * t] = (uint8_t)f[t],
+                                      pp[6 * k + 2 * t + 1] = (uint8_t)(f[t] >> 8);
+        }
+        out[2] = (uint8_t)(c->n_pert + nm);
+      }
+      free(mv);
+    }
+    free(q);
+  }
+  if (sentinel != 0) {
+    *ms = sentinel;
+    for (int d = 0; d < P; ++d) bub[d] = peak[d] = sentinel;
+  }
+  free(c);
+}
+
+static void* advance_worker(void* arg) {
+  advance_job* j = (advance_job*)arg;
+  for (int64_t i = j->lo; i < j->hi; ++i) advance_record(j, i);
+  return NULL;
+}
+
+int oracle_advance_w(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
+                     const int64_t* cap, const int64_t* link, const uint8_t* cands, int64_t n,
+                     uint8_t* out_cands, int64_t* out_ms, int64_t* out_bub, int64_t* out_peak,
+                     int nthreads) {
+  if (!check_problem(pr) || n < 0 ||
+      (n > 0 && (!costs || !mem || !cap || !link || !cands || !out_cands || !out_ms ||
+                 !out_bub || !out_peak)))
+    return REF_EINVAL;
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > 256) nthreads = 256;
+  if (n < nthreads) nthreads = n > 0 ? (int)n : 1;
+  pthread_t th[256];
+  advance_job jobs[256];
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t] = (advance_job){pr, costs, mem, cap, link, cands, out_cands,
+                            n * t / nthreads, n * (t + 1) / nthreads, out_ms, out_bub, out_peak};
+    if (nthreads == 1) advance_worker(&jobs[t]);
+    else pthread_create(&th[t], NULL, advance_worker, &jobs[t]);
+  }
+  if (nthreads > 1)
+    for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+  return REF_OK;
 }
 
 /* Dump the final (perturbed) queues of one candidate in stage terms: ops[d*qcap + i] =
@@ -779,33 +968,59 @@ typedef struct {
   int64_t* out_acc;
   int32_t* out_queues; /* nullable: [chain][P][qcap] packed kind<<14 | chunk<<11 | m */
   const int64_t* ids;  /* nullable: chain index of each record (Philox counter); default i */
+  /* memory constraint (all NULL for the plain search) */
+  const int64_t* mem; /* layer memory [L][2] */
+  const int64_t* cap; /* capacity per device [P] */
+  int max_adv;        /* W advances per evaluation */
+  int64_t* out_peak;  /* [chain][P] */
 } tune_job;
 
-static int64_t eff(int64_t ms) { return ms < 0 ? INT64_MAX : ms; }
+/* Evaluate a chain state. Plain: the simulator. With memory: selective W advancing on the
+ * queues (changed in place); *fits tells whether every device ends within its capacity. */
+static int tune_eval(const tune_job* j, const ref_cand* c, ref_op* q, int qcap, const int* qlen,
+                     int64_t* ms, int64_t* bub, int64_t* peak, int* fits) {
+  if (!j->mem) {
+    *fits = 1;
+    return eval_local(j->pr, c, j->costs, j->link, q, qcap, qlen, NULL, ms, bub, NULL, NULL);
+  }
+  int nm;
+  return advance_w(j->pr, c, j->costs, j->mem, j->cap, j->link, q, qcap, qlen, j->max_adv, ms,
+                   bub, peak, fits, NULL, &nm);
+}
 
 static void tune_chain(tune_job* j, int64_t ci) {
   const ref_problem* pr = j->pr;
   int P = pr->P;
   uint8_t* rec = j->recs + (size_t)ci * pr->cand_stride;
   int64_t* bub = j->out_bub + (size_t)ci * P;
+  int64_t* opk = j->out_peak ? j->out_peak + (size_t)ci * P : NULL;
   ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
   decode(pr, rec, c);
   j->out_acc[ci] = 0;
   if (!valid_structure(pr, c) || c->n_pert != 0) {
     j->out_ms[ci] = REF_INVALID;
-    for (int d = 0; d < P; ++d) bub[d] = REF_INVALID;
+    for (int d = 0; d < P; ++d) {
+      bub[d] = REF_INVALID;
+      if (opk) opk[d] = REF_INVALID;
+    }
     free(c);
     return;
   }
   int qcap = 3 * c->v * pr->M;
-  ref_op* q = (ref_op*)malloc(sizeof(ref_op) * (size_t)qcap * P);
+  size_t qbytes = sizeof(ref_op) * (size_t)qcap * P;
+  ref_op* q = (ref_op*)malloc(qbytes);
+  ref_op* q2 = (ref_op*)malloc(qbytes); /* the proposal's queues */
   int qlen[64];
   build_local_queues(pr, c, q, qcap, qlen);
-  int64_t cur_ms, cur_bub[64], ms, tb[64];
-  int rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &cur_ms, cur_bub, NULL);
+  /* the current state: its makespan, bubbles, peaks and whether it fits (a deadlocked state
+   * counts as +infinity, an over-capacity one as infeasible) */
+  int64_t cur_ms, cur_bub[64], cur_peak[64], ms, tb[64], tp[64];
+  int cur_fits, fits;
+  int rc = tune_eval(j, c, q, qcap, qlen, &cur_ms, cur_bub, cur_peak, &cur_fits);
   if (rc != SIM_OK) {
     cur_ms = rc == SIM_CYCLE ? REF_DEADLOCK : REF_INVALID;
-    for (int d = 0; d < P; ++d) cur_bub[d] = cur_ms;
+    for (int d = 0; d < P; ++d) cur_bub[d] = cur_peak[d] = cur_ms;
+    cur_fits = 0;
   }
   int S = c->S;
   for (int t = 1; t <= j->n_steps; ++t) {
@@ -813,58 +1028,61 @@ static void tune_chain(tune_job* j, int64_t ci) {
     uint64_t ctr[4] = {chain_id, (uint64_t)t, 0, 0}, key[2] = {j->seed, 0}, u[4];
     oracle_philox4x64_10(ctr, key, u);
     int kind = (int)(u[0] % 3);
-    int ok = 0;
+    memcpy(q2, q, qbytes);
+    /* apply the proposal to the record c (kinds 0, 1) or the queue copy q2 (kind 2) */
+    int proposed = 0, saved_b = 0, saved_i = 0, saved_dev[64];
     if (kind == 0) {
       if (S >= 2) {
         int i = 1 + (int)(u[1] % (uint64_t)(S - 1));
         int nb = c->b[i] + ((u[2] & 1) ? 1 : -1);
         if (nb > c->b[i - 1] && nb < c->b[i + 1]) {
-          int old = c->b[i];
+          saved_i = i, saved_b = c->b[i];
           c->b[i] = nb;
-          rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &ms, tb, NULL);
-          if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
-          else c->b[i] = old;
+          proposed = 1;
         }
       }
     } else if (kind == 1) {
       if (P >= 2) {
         int d1 = (int)(u[1] % (uint64_t)P);
         int d2 = (int)((d1 + 1 + (int)(u[2] % (uint64_t)(P - 1))) % P);
-        int saved[64];
         for (int s = 0; s < S; ++s) {
-          saved[s] = c->dev[s];
+          saved_dev[s] = c->dev[s];
           if (c->dev[s] == d1) c->dev[s] = d2;
           else if (c->dev[s] == d2) c->dev[s] = d1;
         }
-        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &ms, tb, NULL);
-        if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
-        else
-          for (int s = 0; s < S; ++s) c->dev[s] = saved[s];
+        proposed = 1;
       }
     } else {
       int d = (int)(u[1] % (uint64_t)P);
       if (qlen[d] >= 2) {
         int i = (int)(u[2] % (uint64_t)(qlen[d] - 1));
-        ref_op* row = q + (size_t)d * qcap;
+        ref_op* row = q2 + (size_t)d * qcap;
         ref_op tmp = row[i];
         row[i] = row[i + 1];
         row[i + 1] = tmp;
-        rc = eval_local(pr, c, j->costs, j->link, q, qcap, qlen, NULL, &ms, tb, NULL);
-        if (rc == SIM_OK && ms <= eff(cur_ms)) ok = 1;
-        else {
-          row[i + 1] = row[i];
-          row[i] = tmp;
-        }
+        proposed = 1;
       }
     }
-    if (ok) {
+    if (!proposed) continue;
+    rc = tune_eval(j, c, q2, qcap, qlen, &ms, tb, tp, &fits);
+    const int cur_ok = cur_ms >= 0 && cur_fits;
+    if (rc == SIM_OK && fits && (!cur_ok || ms <= cur_ms)) {
+      memcpy(q, q2, qbytes);
       cur_ms = ms;
-      for (int d = 0; d < P; ++d) cur_bub[d] = tb[d];
+      cur_fits = 1;
+      for (int d = 0; d < P; ++d) cur_bub[d] = tb[d], cur_peak[d] = tp[d];
       j->out_acc[ci]++;
+    } else if (kind == 0) {
+      c->b[saved_i] = saved_b;
+    } else if (kind == 1) {
+      for (int s = 0; s < S; ++s) c->dev[s] = saved_dev[s];
     }
   }
   j->out_ms[ci] = cur_ms;
-  for (int d = 0; d < P; ++d) bub[d] = cur_bub[d];
+  for (int d = 0; d < P; ++d) {
+    bub[d] = cur_bub[d];
+    if (opk) opk[d] = cur_peak[d];
+  }
   write_record(pr, c, rec);
   if (j->out_queues) {
     /* output rows have the queue store's capacity 3 * v_max * M, whatever this chain's v */
@@ -876,6 +1094,7 @@ static void tune_chain(tune_job* j, int64_t ci) {
         oq[d * ocap + i] = i < qlen[d] ? ((o.kind << 14) | (o.chunk << 11) | o.m) : 0;
       }
   }
+  free(q2);
   free(q);
   free(c);
 }
@@ -890,23 +1109,38 @@ static void* tune_worker(void* arg) {
  * candidate records (updated to the final state); chain_ids (nullable) gives each record's chain
  * index for the Philox counter (default: its position). Outputs per chain: final makespan,
  * bubbles, accepted-move count, and optionally the final queues (qcap = 3*v_max*M entries per
- * device). */
-int oracle_tune(const ref_problem* pr, const int64_t* costs, const int64_t* link, uint8_t* recs,
-                int64_t n, uint64_t seed, int32_t n_steps, int64_t* out_ms, int64_t* out_bub,
-                int64_t* out_acc, int32_t* out_queues, const int64_t* chain_ids, int nthreads) {
+ * device). With mem (layer memory [L][2]) and cap (bytes per device [P]), every evaluation
+ * runs selective W advancing (at most max_adv advances) and a state counts as feasible only if
+ * every device's peak fits; a proposal is kept iff feasible and (the current state is not, or
+ * its makespan is not larger); out_peak[n][P] receives the final peaks. */
+int oracle_tune_mem(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
+                    const int64_t* cap, int32_t max_adv, const int64_t* link, uint8_t* recs,
+                    int64_t n, uint64_t seed, int32_t n_steps, int64_t* out_ms, int64_t* out_bub,
+                    int64_t* out_peak, int64_t* out_acc, int32_t* out_queues,
+                    const int64_t* chain_ids, int nthreads) {
   if (!check_problem(pr) || n < 0 || n_steps < 0) return REF_EINVAL;
+  if (mem && (!cap || !out_peak || max_adv < 0)) return REF_EINVAL;
   if (nthreads < 1) nthreads = 1;
   if (nthreads > 256) nthreads = 256;
   if (n < nthreads) nthreads = n > 0 ? (int)n : 1;
   pthread_t th[256];
   tune_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
-    jobs[t] = (tune_job){pr, costs, link, recs, n * t / nthreads, n * (t + 1) / nthreads,
-                         seed, n_steps, out_ms, out_bub, out_acc, out_queues, chain_ids};
+    jobs[t] = (tune_job){pr,       costs,      link,      recs,     n * t / nthreads,
+                         n * (t + 1) / nthreads, seed, n_steps,   out_ms,   out_bub,
+                         out_acc,  out_queues, chain_ids, mem,      mem ? cap : NULL,
+                         max_adv,  mem ? out_peak : NULL};
     if (nthreads == 1) tune_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, tune_worker, &jobs[t]);
   }
   if (nthreads > 1)
     for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
   return REF_OK;
+}
+
+int oracle_tune(const ref_problem* pr, const int64_t* costs, const int64_t* link, uint8_t* recs,
+                int64_t n, uint64_t seed, int32_t n_steps, int64_t* out_ms, int64_t* out_bub,
+                int64_t* out_acc, int32_t* out_queues, const int64_t* chain_ids, int nthreads) {
+  return oracle_tune_mem(pr, costs, NULL, NULL, 0, link, recs, n, seed, n_steps, out_ms, out_bub,
+                         NULL, out_acc, out_queues, chain_ids, nthreads);
 }

@@ -46,6 +46,13 @@ def lib():
         L.oracle_tune.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64,
                                   ctypes.c_uint64, ctypes.c_int32, p, p, p, p, p, ctypes.c_int]
         L.oracle_tune.restype = ctypes.c_int
+        L.oracle_tune_mem.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int32, p, p,
+                                      ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32, p, p, p,
+                                      p, p, p, ctypes.c_int]
+        L.oracle_tune_mem.restype = ctypes.c_int
+        L.oracle_advance_w.argtypes = [ctypes.POINTER(RefProblem), p, p, p, p, p,
+                                       ctypes.c_int64, p, p, p, p, ctypes.c_int]
+        L.oracle_advance_w.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -89,6 +96,29 @@ def sim_batch_mem(prob, costs, mem, link, cands, nthreads=1):
     if rc != 0:
         raise ValueError(f"oracle_sim_batch_mem rejected the arguments (rc={rc})")
     return ms, bub, peak
+
+
+def advance_w(prob, costs, mem, cap, link, cands, nthreads=1):
+    """Selective W advancing on candidate records: each record gains at most max_pert - n_pert
+    perturbations that advance W ops until every device's peak is within cap (int64 [P]).
+
+    Returns (records, makespan[n], bubble[n, P], peak[n, P]) of the output records."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    mem = np.ascontiguousarray(mem, dtype=np.int64)
+    cap = np.ascontiguousarray(cap, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    out = np.zeros_like(cands)
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    peak = np.zeros((n, prob.P), dtype=np.int64)
+    rc = lib().oracle_advance_w(ctypes.byref(prob), _ptr(costs), _ptr(mem), _ptr(cap),
+                                _ptr(link), _ptr(cands), n, _ptr(out), _ptr(ms), _ptr(bub),
+                                _ptr(peak), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_advance_w rejected the arguments (rc={rc})")
+    return out, ms, bub, peak
 
 
 def dump_queues(prob, rec):
@@ -174,6 +204,35 @@ def tune(prob, costs, link, recs, seed, n_steps, nthreads=1, want_queues=False, 
     if rc != 0:
         raise ValueError(f"oracle_tune rejected the arguments (rc={rc})")
     return recs, ms, bub, acc, queues
+
+
+def tune_mem(prob, costs, mem, cap, max_adv, link, recs, seed, n_steps, nthreads=1,
+             want_queues=False, chain_ids=None):
+    """The local search under the memory constraint (cap int64 [P]) with selective W advancing
+    (at most max_adv advances per evaluation).
+
+    Returns (final_records, makespan[n], bubble[n, P], peak[n, P], accepted[n], queues or
+    None)."""
+    recs = np.array(recs, dtype=np.uint8, copy=True, order="C")
+    ids = None if chain_ids is None else np.ascontiguousarray(chain_ids, dtype=np.int64)
+    n = recs.shape[0]
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    mem = np.ascontiguousarray(mem, dtype=np.int64)
+    cap = np.ascontiguousarray(cap, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    peak = np.zeros((n, prob.P), dtype=np.int64)
+    acc = np.zeros(n, dtype=np.int64)
+    qcap = 3 * prob.v_max * prob.M
+    queues = np.zeros((n, prob.P, qcap), dtype=np.int32) if want_queues else None
+    rc = lib().oracle_tune_mem(ctypes.byref(prob), _ptr(costs), _ptr(mem), _ptr(cap),
+                               int(max_adv), _ptr(link), _ptr(recs), n, ctypes.c_uint64(seed),
+                               int(n_steps), _ptr(ms), _ptr(bub), _ptr(peak), _ptr(acc),
+                               _ptr(queues), _ptr(ids), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_tune_mem rejected the arguments (rc={rc})")
+    return recs, ms, bub, peak, acc, queues
 
 
 def tune_chains(prob, costs, link, all_recs, chain_ids, seed, n_steps, nthreads=1):
