@@ -128,12 +128,39 @@ int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        void* stream);
 
 /*
+ * octo_advance_w — selective W advancing (§6 "Scheduling Tuning", third policy) under the
+ * per-device capacity of §6 Eq. 2, on a batch of candidate records. For each record, after its
+ * queues are generated and its moves applied: while some device's peak (as octo_sim_batch_mem)
+ * exceeds capacity[d], take the lowest such device d and the queue position p where its
+ * activation total first reaches the peak (a forward). A weight-gradient op W of d is eligible
+ * if it sits after p, its B sits before p and its stage has activation bytes; advancing it moves
+ * it to index p (its release then precedes that allocation). Eligible W are tried in queue
+ * order; the first whose advance does not lengthen the makespan is kept (busy time is fixed, so
+ * no device's bubble grows), else the first eligible one. The search stops when every device
+ * fits, nothing is eligible, or the record's free move slots (max_pert - n_pert) are used up.
+ *   capacity        int64 [P] bytes per device.
+ *   out_candidates  n records (same stride, 16-byte aligned; may be `candidates` itself): the
+ *                   input record with each advance appended as a move {device, from, to} and
+ *                   n_pert raised; bytes past the last move are copied. Invalid or deadlocked
+ *                   records are copied unchanged.
+ *   out_makespan, out_bubble, out_peak  as octo_sim_batch_mem for the output record (so a
+ *                   record still over capacity shows it in out_peak).
+ * Fused schedules have no W: their records come back unchanged. Returns OCTO_OK or a negative
+ * status.
+ */
+int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
+                   const int64_t* capacity, const int64_t* link, const void* candidates,
+                   int64_t n, void* out_candidates, int64_t* out_makespan, int64_t* out_bubble,
+                   int64_t* out_peak, void* stream);
+
+/*
  * Local-search chains (§6: every tuning move re-runs the simulator; Algorithm 1's three move
  * families). Chain state record, octo_chain_stride(prob) bytes each, 16-byte aligned:
  *   bytes 0..cand_stride-1  the candidate record (n_pert must be 0), updated in place
  *   +0  int64 current makespan (or sentinel)
  *   +8  int64 accepted moves
  *   +16 int64 current bubble[P]
+ *   +16+8P int64 current peak bytes[P] (written by octo_tune_step_mem only)
  * Queue store: uint16 [n_chains][P][octo_queue_capacity(prob)]; entry = kind << 14 | chunk << 11
  * | m with kind 0 = F, 1 = B, 2 = W and chunk the index into the device's ascending stage list.
  *
@@ -153,6 +180,22 @@ int32_t octo_queue_capacity(const octo_problem* prob);
 int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    void* chains, uint16_t* queues, int64_t n_chains, uint64_t seed, int32_t step,
                    void* stream);
+
+/*
+ * octo_tune_step_mem — octo_tune_step under the memory constraint of §6 Eq. 2. Every
+ * evaluation (the step-0 state and each proposal) runs selective W advancing as octo_advance_w
+ * does, on the chain's queues, with at most max_advance advances (0..OCTO_MAX_ADVANCE); a state
+ * is feasible if it does not deadlock and every device's peak fits capacity[d]. A proposal is
+ * kept iff it is feasible and the current state is not, or its makespan is <= the current one;
+ * kept advances stay in the chain's queues. Step 0 stores the (advanced) initial state whether
+ * or not it fits; the peak area of the chain record holds each state's peaks. layer_mem as
+ * octo_sim_batch_mem. Use it for every step of a chain set (it reads the peaks it stored).
+ */
+#define OCTO_MAX_ADVANCE 4096
+int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
+                       const int64_t* layer_mem, const int64_t* capacity, int32_t max_advance,
+                       const int64_t* link, void* chains, uint16_t* queues, int64_t n_chains,
+                       uint64_t seed, int32_t step, void* stream);
 
 /*
  * Measurement hook. events[0..n_events-1] are hipEvent_t handles (n_events <= 8; entries may be

@@ -48,6 +48,9 @@ def lib():
         L.octo_sim_batch_mem.argtypes = [pp, vp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_mem.restype = ctypes.c_int
         L.octo_tune_step.argtypes = [pp, vp, vp, vp, vp, i64, ctypes.c_uint64, i32, vp]
+        L.octo_tune_step_mem.argtypes = [pp, vp, vp, vp, i32, vp, vp, vp, i64, ctypes.c_uint64,
+                                         i32, vp]
+        L.octo_advance_w.argtypes = [pp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
         L.octo_tune_step.restype = ctypes.c_int
         L.octo_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), i32]
         L.octo_profile_events.restype = ctypes.c_int
@@ -146,6 +149,51 @@ def tune_step(prob, layer_costs, link, chains, queues, seed, step, stream=None):
     _check(rc, "octo_tune_step")
 
 
+def tune_step_mem(prob, layer_costs, layer_mem, capacity, max_advance, link, chains, queues,
+                  seed, step, stream=None):
+    """octo_tune_step_mem: the local-search step under per-device capacities (int64 [P]) with
+    selective W advancing (at most max_advance advances per evaluation)."""
+    n = chains.shape[0]
+    q = queues
+    if q.dtype not in (torch.int16, torch.uint16):
+        raise TypeError("queues must be a 16-bit tensor")
+    rc = lib().octo_tune_step_mem(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(layer_mem, torch.int64, "layer_mem"),
+        _dev_ptr(capacity, torch.int64, "capacity"), int(max_advance),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(chains, torch.uint8, "chains"),
+        _dev_ptr(q, q.dtype, "queues"), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
+        _stream(chains, stream))
+    _check(rc, "octo_tune_step_mem")
+
+
+def advance_w(prob, layer_costs, layer_mem, capacity, link, candidates, out_candidates=None,
+              out_makespan=None, out_bubble=None, out_peak=None, stream=None):
+    """octo_advance_w: selective W advancing on candidate records under capacity (int64 [P]).
+    Returns (records, makespan, bubble, peak) of the output records."""
+    n = candidates.shape[0]
+    dev = candidates.device
+    if out_candidates is None:
+        out_candidates = torch.empty_like(candidates)
+    if out_makespan is None:
+        out_makespan = torch.empty(n, dtype=torch.int64, device=dev)
+    if out_bubble is None:
+        out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    if out_peak is None:
+        out_peak = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    rc = lib().octo_advance_w(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(layer_mem, torch.int64, "layer_mem"),
+        _dev_ptr(capacity, torch.int64, "capacity"), _dev_ptr(link, torch.int64, "link"),
+        _dev_ptr(candidates, torch.uint8, "candidates"), n,
+        _dev_ptr(out_candidates, torch.uint8, "out_candidates"),
+        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
+        _dev_ptr(out_peak, torch.int64, "out_peak"), _stream(candidates, stream))
+    _check(rc, "octo_advance_w")
+    return out_candidates, out_makespan, out_bubble, out_peak
+
+
 def profile_events(events):
     """Record hipEvent_t handles (ints) at the simulation-kernel boundaries of later calls
     (see include/octo.h); an empty list turns it off."""
@@ -153,9 +201,11 @@ def profile_events(events):
     _check(lib().octo_profile_events(arr, len(events)), "octo_profile_events")
 
 
-def chain_state(chains, prob):
-    """Decode (makespan [n], accepted [n], bubble [n, P]) from chain-state bytes (host copy)."""
+def chain_state(chains, prob, with_peak=False):
+    """Decode (makespan [n], accepted [n], bubble [n, P]) from chain-state bytes (host copy);
+    with_peak: also the peak bytes [n, P] stored by tune_step_mem."""
     c = chains.cpu() if isinstance(chains, torch.Tensor) else torch.as_tensor(chains)
     off = prob.cand_stride
-    tail = c[:, off:off + 16 + 8 * prob.P].contiguous().view(torch.int64)
-    return tail[:, 0], tail[:, 1], tail[:, 2:2 + prob.P]
+    tail = c[:, off:off + 16 + 16 * prob.P].contiguous().view(torch.int64)
+    out = (tail[:, 0], tail[:, 1], tail[:, 2:2 + prob.P])
+    return out + (tail[:, 2 + prob.P:2 + 2 * prob.P],) if with_peak else out

@@ -863,6 +863,234 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// Selective W advancing (§6 "Scheduling Tuning", third policy) under per-device capacities
+// (§6 Eq. 2). While a device's peak exceeds its capacity, take the lowest such device d and
+// the queue position p at which its running activation total first reaches the peak (an F).
+// Eligible: a W of d after p whose B precedes p and whose stage holds activations; advancing it
+// moves it to index p, so its release comes before that allocation. Eligible W are tried in
+// queue order: the first whose advance does not lengthen the makespan is kept (busy time is
+// fixed, so no bubble grows), else the first one is. Repeat until every device fits, nothing is
+// eligible, or max_adv advances were made. A W has no consumers, so no advance can deadlock.
+// ---------------------------------------------------------------------------------------------
+constexpr int AW_SIM = 0, AW_TRIAL = 1, AW_WALK = 2, AW_NEXT = 3, AW_DONE = 4;
+
+// Lane-local result of one group's advancing.
+struct AdvOut {
+  bool dead;    // the queues deadlock (nothing advanced)
+  bool fits;    // every device of the group is within capacity
+  int adv;      // advances made
+  int64_t ms;   // makespan of the final queues
+  int64_t hi;   // largest activation total this lane's device holds
+};
+
+// Running activation total along one device queue: its maximum and the first position that
+// reaches it (-1 when nothing is allocated).
+template <int VMAX>
+__device__ __forceinline__ void act_walk(const uint16_t* row, int n, const Chunks<VMAX>& c,
+                                         int64_t& hi, int& at) {
+  int64_t cur = 0;
+  hi = 0, at = -1;
+  for (int i = 0; i < n; ++i) {
+    const uint32_t e = row[i];
+    const int kind = (int)(e >> 14) & 3;
+    const int64_t a = pick<VMAX>(c.mA, (int)(e >> 11) & 7);
+    if (kind == KF) {
+      cur += a;
+      if (cur > hi) hi = cur, at = i;
+    } else if (kind == KW || !c.split) {
+      cur -= a;
+    }
+  }
+}
+
+// First eligible W after position `from` (>= p): its B is not between p and it (a live queue
+// has B before W, so B precedes p), and its stage holds activations. -1 if none.
+template <int VMAX>
+__device__ __forceinline__ int next_eligible(const uint16_t* row, int n, int p, int from,
+                                             const Chunks<VMAX>& c) {
+  for (int j = from + 1; j < n; ++j) {
+    const uint32_t e = row[j];
+    if (((e >> 14) & 3) != (uint32_t)KW || pick<VMAX>(c.mA, (int)(e >> 11) & 7) <= 0) continue;
+    const uint16_t b = (uint16_t)((KB << 14) | (e & 0x3FFF));
+    bool later = false;
+    for (int i = p + 1; i < j && !later; ++i) later = row[i] == b;
+    if (!later) return j;
+  }
+  return -1;
+}
+
+// Runs the policy for every group of the wave (all lanes call it; groups with run == false
+// take no part). row: this lane's queue (n entries, changed in place); cap: this device's
+// capacity; stat: its static bytes. pert (nullable): where advance k of the group is written as
+// (device, from, to), uint16 each, by the lane of that device.
+template <int VMAX>
+__device__ AdvOut advance_w(const Table64& T, uint16_t* row, int n, const Chunks<VMAX>& c,
+                            const Ring& ring, int S, int M, int P, bool run, int64_t cap,
+                            int64_t stat, int max_adv, int G, uint64_t gbit, uint64_t lsb,
+                            uint16_t* pert) {
+  const int d = lane_id() % G;
+  const int gl = lane_id() - d;
+  const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
+  AdvOut o;
+  o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0;
+  int phase = run ? AW_SIM : AW_DONE;
+  int dstar = 0, p = -1, cursor = -1, first = -1, j = -1, at = -1;
+  int64_t ms_first = 0;
+  for (;;) {
+    const bool need = phase == AW_SIM || phase == AW_TRIAL;
+    int64_t ms = 0;
+    bool dead = false;
+    if (__ballot(need) != 0) {
+      Lane L;
+      L.clock = 0, L.pos = 0, L.nops = need && d < P ? n : 0, L.mem = L.peak = 0;
+      if (need) T.clear(S * M, d, G);
+      __asm__ volatile("" ::: "memory");
+      GenMat q;
+      q.init(row, L.nops);
+      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+      relax<VMAX, true, false>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      ms = group_max(L.clock, G);
+    }
+    if (phase == AW_SIM) {
+      o.dead = dead;
+      o.ms = ms;
+      phase = dead ? AW_DONE : AW_WALK;
+    } else if (phase == AW_TRIAL) {
+      if (j == first) ms_first = ms;
+      if (ms <= o.ms) {
+        o.ms = ms;
+        if (pert && d == dstar) {
+          pert[3 * o.adv] = (uint16_t)dstar, pert[3 * o.adv + 1] = (uint16_t)j;
+          pert[3 * o.adv + 2] = (uint16_t)p;
+        }
+        ++o.adv;
+        phase = AW_WALK;
+      } else {
+        if (d == dstar) move_entry(row, p, j);
+        cursor = j;
+        phase = AW_NEXT;
+      }
+    }
+    // walks and searches need no simulation: settle them before the next round
+    while (phase == AW_WALK || phase == AW_NEXT) {
+      if (phase == AW_WALK) {
+        if (d < P) act_walk<VMAX>(row, n, c, o.hi, at);
+        const bool over = d < P && stat + o.hi > cap;
+        const uint64_t om = (__ballot(over) >> gl) & gmask;
+        if (om == 0) {
+          o.fits = true;
+          phase = AW_DONE;
+        } else if (o.adv >= max_adv) {
+          phase = AW_DONE;
+        } else {
+          dstar = __ffsll((unsigned long long)om) - 1;
+          p = __shfl(at, gl + dstar);
+          cursor = p, first = -1;
+          phase = p < 0 ? AW_DONE : AW_NEXT;
+        }
+      } else {
+        int jj = d == dstar ? next_eligible<VMAX>(row, n, p, cursor, c) : -1;
+        jj = __shfl(jj, gl + dstar);
+        if (jj >= 0) {
+          first = first < 0 ? jj : first;
+          j = jj;
+          if (d == dstar) move_entry(row, jj, p);
+          phase = AW_TRIAL;
+        } else if (first >= 0) {
+          // every eligible W lengthens the makespan: take the earliest
+          j = first;
+          if (d == dstar) {
+            move_entry(row, first, p);
+            if (pert) {
+              pert[3 * o.adv] = (uint16_t)dstar, pert[3 * o.adv + 1] = (uint16_t)first;
+              pert[3 * o.adv + 2] = (uint16_t)p;
+            }
+          }
+          o.ms = ms_first;
+          ++o.adv;
+          phase = AW_WALK;
+        } else {
+          phase = AW_DONE;
+        }
+      }
+    }
+    if (__ballot(phase != AW_DONE) == 0) break;
+  }
+  return o;
+}
+
+// Selective W advancing on candidate records: queues materialised (policy, then the record's
+// moves), at most max_pert - n_pert advances appended to the output record as moves.
+template <int VMAX>
+__global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __restrict__ cap,
+                                                  uint8_t* __restrict__ out_cands) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
+  const Table64 T{reinterpret_cast<int64_t*>(lds_group)};
+  uint8_t* rec = lds_group + a.table_bytes;
+  const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
+  uint16_t* row = a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap;
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  const int po = pert_off(a.pr.s_max);
+  const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < a.n; base += n_groups) {
+    const int64_t cand = base + g;
+    const bool has = g < a.CPW && cand < a.n;
+    const uint8_t* grec = a.cands + (has ? cand : 0) * a.pr.stride;
+    uint8_t* orec = out_cands + (has ? cand : 0) * a.pr.stride;
+    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
+    __asm__ volatile("" ::: "memory");
+    Resolved r;
+    r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
+    if (has) r = resolve_record(a.pr, grec);
+    const bool run = has && r.valid;
+    const int v = run ? r.v : 1;
+    const int S = P * v;
+    const Ring ring = make_ring(M, M);
+    Chunks<VMAX> c;
+    int64_t busy = 0, stat = 0;
+    int n = 0;
+    if (run && d < P) {
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, a.pre_mem,
+                                &stat);
+      n = materialise<VMAX>(a, c, v, r.gen, r.split, row);
+      const uint8_t* pp = grec + po;
+      for (int i = 0; i < r.n_pert; ++i) {
+        const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
+        if (pd != d) continue;
+        move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
+      }
+    } else {
+      zero_chunks<VMAX>(c);
+    }
+    __asm__ volatile("" ::: "memory");
+    const int n0 = run ? r.n_pert : 0;
+    uint16_t* pert = reinterpret_cast<uint16_t*>(orec + po) + 3 * n0;
+    const AdvOut o = advance_w<VMAX>(T, row, n, c, ring, S, M, P, run, d < P ? cap[d] : 0, stat,
+                                     a.pr.max_pert - n0, G, gbit, lsb, has ? pert : nullptr);
+    if (!has) continue;
+    // the output record: the input's bytes (the new moves aside), then the move count
+    const int halves = a.pr.stride >> 1;
+    const int a0 = (po >> 1) + 3 * n0, a1 = a0 + 3 * o.adv;
+    const uint16_t* in16 = reinterpret_cast<const uint16_t*>(grec);
+    uint16_t* out16 = reinterpret_cast<uint16_t*>(orec);
+    for (int h = d; h < halves; h += G)
+      if (h != 1 && (h < a0 || h >= a1)) out16[h] = in16[h];
+    if (d == 0) out16[1] = (uint16_t)((rec[2] + o.adv) | (rec[3] << 8));
+    if (d < P) {
+      const int64_t sv = run ? (o.dead ? (int64_t)OCTO_MS_DEADLOCK : 0) : (int64_t)OCTO_MS_INVALID;
+      if (d == 0) a.out_ms[cand] = sv ? sv : o.ms;
+      a.out_bub[cand * P + d] = sv ? sv : o.ms - busy;
+      a.out_peak[cand * P + d] = sv ? sv : stat + o.hi;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Local-search step (one chain per group, 64-bit finish tables).
 // ---------------------------------------------------------------------------------------------
 struct TuneArgs {
@@ -873,9 +1101,15 @@ struct TuneArgs {
   int64_t n_chains;
   uint64_t seed;
   int step;
+  const int64_t* cap;  // memory-constrained search: capacity per device [P]
+  int max_adv;         // W advances per evaluation
 };
 
-template <int VMAX>
+// One step of every chain. MEM: the memory-constrained search — proposals are built in a
+// working copy of the chain's queues (group slot rows of qscratch), selective W advancing runs
+// on it, and a state is feasible only if every device fits; the copy replaces the chain's
+// queues when the proposal is kept.
+template <int VMAX, bool MEM>
 __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   extern __shared__ __align__(16) uint8_t smem[];
   const SimArgs& a = t.s;
@@ -887,6 +1121,10 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   uint8_t* rec = lds_group + a.table_bytes;
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
+  const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
+  uint16_t* wrow = MEM ? a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap : nullptr;
+  const int gl = lane_id() - d;
+  const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
   for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < t.n_chains; base += n_groups) {
     const int64_t chain = base + g;
@@ -894,6 +1132,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     uint8_t* crec = t.chains + (has ? chain : 0) * t.chain_stride;
     int64_t* cstate = reinterpret_cast<int64_t*>(crec + a.pr.stride);
     uint16_t* row = t.queues + ((size_t)(has ? chain : 0) * P + (d < P ? d : 0)) * a.qcap;
+    uint16_t* qrow = MEM ? wrow : row;  // the queues the proposal is evaluated on
     if (has) stage_record(rec, crec, a.rec_bytes, d, G);
     __asm__ volatile("" ::: "memory");
 
@@ -907,6 +1146,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
         if (!r.valid || r.n_pert != 0) {
           if (d == 0) cstate[0] = OCTO_MS_INVALID, cstate[1] = 0;
           if (d < P) cstate[2 + d] = OCTO_MS_INVALID;
+          if (MEM && d < P) cstate[2 + P + d] = OCTO_MS_INVALID;
           skip = true;
         }
         v = r.v, gen = r.gen, split = r.split;
@@ -922,8 +1162,10 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     const int S = P * v;
     const int qlen = (split ? 3 : 2) * v * M;
     const Ring ring = make_ring(M, M);
+    if (MEM && !skip && t.step > 0 && d < P)
+      for (int i = 0; i < qlen; ++i) wrow[i] = row[i];
 
-    // propose (step >= 1); the move is applied to the staged record / this chain's queue row
+    // propose (step >= 1); the move is applied to the staged record / the queue row qrow
     int kind = -1, mi = 0, sd = -1;
     bool valid = true;
     if (!skip && t.step > 0) {
@@ -960,9 +1202,9 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
         } else {
           mi = (int)(u.x[2] % (uint64_t)(qlen - 1));
           if (d == sd) {
-            const uint16_t x = row[mi];
-            row[mi] = row[mi + 1];
-            row[mi + 1] = x;
+            const uint16_t x = qrow[mi];
+            qrow[mi] = qrow[mi + 1];
+            qrow[mi + 1] = x;
           }
         }
       }
@@ -971,41 +1213,60 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     const bool run = !skip && valid;
 
     Chunks<VMAX> c;
-    int64_t busy = 0;
-    Lane L;
-    L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
+    int64_t busy = 0, stat = 0;
     if (run && d < P) {
-      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring);
-      if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, row);
-      L.nops = qlen;
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring,
+                                MEM ? a.pre_mem : nullptr, &stat);
+      if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, qrow);
     } else {
       zero_chunks<VMAX>(c);
     }
-    if (run) T.clear(S * M, d, G);
     __asm__ volatile("" ::: "memory");
-    GenMat q;
-    q.init(row, L.nops);
-    describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
-    bool dead = false;
-    relax<VMAX, true, false>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
-    const int64_t ms = group_max(L.clock, G);
+    bool dead = false, fits = true;
+    int64_t ms = 0, held = 0;
+    if constexpr (MEM) {
+      const AdvOut o = advance_w<VMAX>(T, qrow, run && d < P ? qlen : 0, c, ring, S, M, P, run,
+                                       d < P ? t.cap[d] : 0, stat, t.max_adv, G, gbit, lsb,
+                                       nullptr);
+      dead = o.dead, fits = o.fits, ms = o.ms, held = o.hi;
+    } else {
+      Lane L;
+      L.clock = 0, L.pos = 0, L.nops = run && d < P ? qlen : 0, L.mem = L.peak = 0;
+      if (run) T.clear(S * M, d, G);
+      __asm__ volatile("" ::: "memory");
+      GenMat q;
+      q.init(qrow, L.nops);
+      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+      relax<VMAX, true, false>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      ms = group_max(L.clock, G);
+    }
 
     if (!has || skip) continue;
-    if (t.step == 0) {
-      if (d == 0) cstate[0] = dead ? OCTO_MS_DEADLOCK : ms, cstate[1] = 0;
-      if (d < P) cstate[2 + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
-      continue;
-    }
-    const int64_t cur_eff = cur < 0 ? INT64_MAX : cur;
-    const bool accept = valid && !dead && ms <= cur_eff;
-    if (accept) {
-      if (d == 0) {
-        cstate[0] = ms;
-        cstate[1] += 1;
-        for (int i = 0; i < a.rec_bytes; ++i) crec[i] = rec[i];
+    bool keep = t.step == 0;
+    if (t.step > 0) {
+      // the current state counts as +infinity when deadlocked or (MEM) over capacity
+      bool cur_ok = cur >= 0;
+      if constexpr (MEM) {
+        const bool over = d < P && cstate[2 + P + d] > t.cap[d];
+        cur_ok = cur_ok && ((__ballot(over) >> gl) & gmask) == 0;
       }
-      if (d < P) cstate[2 + d] = ms - busy;
-    } else if (kind == 2 && valid && d == sd) {
+      keep = valid && !dead && fits && (!cur_ok || ms <= cur);
+    }
+    if (keep) {
+      if (d == 0) {
+        cstate[0] = dead ? OCTO_MS_DEADLOCK : ms;
+        cstate[1] = t.step == 0 ? 0 : cstate[1] + 1;
+        if (t.step > 0)
+          for (int i = 0; i < a.rec_bytes; ++i) crec[i] = rec[i];
+      }
+      if (d < P) cstate[2 + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+      if constexpr (MEM) {
+        if (d < P) {
+          cstate[2 + P + d] = dead ? OCTO_MS_DEADLOCK : stat + held;
+          for (int i = 0; i < qlen; ++i) row[i] = wrow[i];
+        }
+      }
+    } else if (!MEM && kind == 2 && valid && d == sd) {
       const uint16_t x = row[mi];
       row[mi] = row[mi + 1];
       row[mi + 1] = x;
@@ -1439,8 +1700,9 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
   Plan pl{};
   if (VC <= 2 && su.ws->qt_valid) {
     const TabGeom geo = tab_geom(prob, su.di.lds_max, VC, MEM);
-    tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[VC - 1] == geo.ring.R &&
-          su.ws->qt_lg[VC - 1] == geo.lg && geo.plan.G * geo.plan.CPW <= WAVE;
+    constexpr int vi = VC <= 2 ? VC - 1 : 0;
+    tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[vi] == geo.ring.R &&
+          su.ws->qt_lg[vi] == geo.lg && geo.plan.G * geo.plan.CPW <= WAVE;
     pl = geo.plan;
   }
   if (!tab) pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R, 0);
@@ -1492,15 +1754,30 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
   return launch_ok();
 }
 
-template <int VC>
-int launch_tune(const TuneArgs& t, const Plan& pl, int cus, int64_t n_chains,
+// MEM: the working queue rows are group slots of the workspace, sized for mat_grid blocks.
+template <int VC, bool MEM>
+int launch_tune(const TuneArgs& t, const Plan& pl, int cus, int mat_grid, int64_t n_chains,
                 hipStream_t stream) {
   int grid = 0;
-  int rc = occupancy_grid(k_tune<VC>, pl.lds_bytes, cus, &grid);
+  int rc = occupancy_grid(k_tune<VC, MEM>, pl.lds_bytes, cus, &grid);
   if (rc) return rc;
   const int64_t need = (n_chains + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  hipLaunchKernelGGL(k_tune<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, t);
+  if (MEM) grid = std::min(grid, mat_grid);
+  hipLaunchKernelGGL((k_tune<VC, MEM>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, t);
+  return launch_ok();
+}
+
+// k_advance over n records; its queue rows are group slots of the workspace (mat_grid blocks).
+template <int VC>
+int launch_advance(const SimArgs& a, const Plan& pl, int cus, int mat_grid, const int64_t* cap,
+                   uint8_t* out, hipStream_t stream) {
+  int grid = 0;
+  int rc = occupancy_grid(k_advance<VC>, pl.lds_bytes, cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (a.n + pl.CPW - 1) / pl.CPW;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min(grid, mat_grid), need));
+  hipLaunchKernelGGL(k_advance<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a, cap, out);
   return launch_ok();
 }
 
@@ -1577,6 +1854,41 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   return record_mark(5, stream);
 }
 
+// The local-search step behind octo_tune_step (MEM = false) and octo_tune_step_mem.
+template <bool MEM>
+int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
+                   const int64_t* capacity, int32_t max_advance, const int64_t* link,
+                   void* chains, uint16_t* queues, int64_t n_chains, uint64_t seed, int32_t step,
+                   hipStream_t stream) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n_chains < 0 || step < 0) return OCTO_EINVAL;
+  if (MEM && (max_advance < 0 || max_advance > OCTO_MAX_ADVANCE)) return OCTO_EINVAL;
+  if (n_chains == 0) return OCTO_OK;
+  if (!layer_costs || !link || !chains || !queues) return OCTO_EINVAL;
+  if (MEM && (!layer_mem || !capacity)) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(chains) & 15) != 0) return OCTO_EINVAL;
+  std::lock_guard<std::mutex> lock(g_mu);
+  Setup su;
+  rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, 0, &su);
+  if (rc) return rc;
+  TuneArgs t;
+  t.s = make_args(prob, su.big, su, link, nullptr, 0, nullptr, nullptr);
+  if (MEM)
+    t.s.pre_mem = reinterpret_cast<const int64_t*>(static_cast<char*>(su.ws->base) + su.l.pre_mem);
+  t.chains = static_cast<uint8_t*>(chains);
+  t.chain_stride = octo_chain_stride(prob);
+  t.queues = queues;
+  t.n_chains = n_chains;
+  t.seed = seed;
+  t.step = step;
+  t.cap = capacity;
+  t.max_adv = max_advance;
+  return prob->v_max <= 2
+             ? launch_tune<2, MEM>(t, su.big, su.di.cus, su.mat_grid, n_chains, stream)
+             : launch_tune<8, MEM>(t, su.big, su.di.cus, su.mat_grid, n_chains, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1596,7 +1908,7 @@ int32_t octo_record_stride(int32_t P, int32_t v_max, int32_t max_pert) {
 
 int32_t octo_chain_stride(const octo_problem* prob) {
   if (check_problem(prob)) return OCTO_EINVAL;
-  return (int32_t)align_up((size_t)prob->cand_stride + 16 + 8 * prob->P, 16);
+  return (int32_t)align_up((size_t)prob->cand_stride + 16 + 16 * prob->P, 16);
 }
 
 int32_t octo_queue_capacity(const octo_problem* prob) {
@@ -1619,30 +1931,45 @@ int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                               out_bubble, out_peak, static_cast<hipStream_t>(stream));
 }
 
-int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
-                   void* chains, uint16_t* queues, int64_t n_chains, uint64_t seed, int32_t step,
-                   void* stream_) {
+int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
+                   const int64_t* capacity, const int64_t* link, const void* candidates,
+                   int64_t n, void* out_candidates, int64_t* out_makespan, int64_t* out_bubble,
+                   int64_t* out_peak, void* stream_) {
   int rc = check_problem(prob);
   if (rc) return rc;
-  if (n_chains < 0 || step < 0) return OCTO_EINVAL;
-  if (n_chains == 0) return OCTO_OK;
-  if (!layer_costs || !link || !chains || !queues) return OCTO_EINVAL;
-  if ((reinterpret_cast<uintptr_t>(chains) & 15) != 0) return OCTO_EINVAL;
+  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
+  if (n == 0) return OCTO_OK;
+  if (!layer_costs || !layer_mem || !capacity || !link || !candidates || !out_candidates ||
+      !out_makespan || !out_bubble || !out_peak)
+    return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0 ||
+      (reinterpret_cast<uintptr_t>(out_candidates) & 15) != 0)
+    return OCTO_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   std::lock_guard<std::mutex> lock(g_mu);
   Setup su;
-  rc = prepare(prob, layer_costs, nullptr, stream, 0, &su);
+  rc = prepare(prob, layer_costs, layer_mem, stream, 0, &su);
   if (rc) return rc;
-  TuneArgs t;
-  t.s = make_args(prob, su.big, su, link, nullptr, 0, nullptr, nullptr);
-  t.chains = static_cast<uint8_t*>(chains);
-  t.chain_stride = octo_chain_stride(prob);
-  t.queues = queues;
-  t.n_chains = n_chains;
-  t.seed = seed;
-  t.step = step;
-  return prob->v_max <= 2 ? launch_tune<2>(t, su.big, su.di.cus, n_chains, stream)
-                          : launch_tune<8>(t, su.big, su.di.cus, n_chains, stream);
+  SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble, out_peak);
+  uint8_t* out = static_cast<uint8_t*>(out_candidates);
+  return prob->v_max <= 2
+             ? launch_advance<2>(a, su.big, su.di.cus, su.mat_grid, capacity, out, stream)
+             : launch_advance<8>(a, su.big, su.di.cus, su.mat_grid, capacity, out, stream);
+}
+
+int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   void* chains, uint16_t* queues, int64_t n_chains, uint64_t seed, int32_t step,
+                   void* stream) {
+  return tune_step_impl<false>(prob, layer_costs, nullptr, nullptr, 0, link, chains, queues,
+                               n_chains, seed, step, static_cast<hipStream_t>(stream));
+}
+
+int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
+                       const int64_t* layer_mem, const int64_t* capacity, int32_t max_advance,
+                       const int64_t* link, void* chains, uint16_t* queues, int64_t n_chains,
+                       uint64_t seed, int32_t step, void* stream) {
+  return tune_step_impl<true>(prob, layer_costs, layer_mem, capacity, max_advance, link, chains,
+                              queues, n_chains, seed, step, static_cast<hipStream_t>(stream));
 }
 
 int octo_profile_events(void* const* events, int32_t n_events) {

@@ -36,7 +36,7 @@ def test_record_layout_matches_inputs():
 def test_argument_checks_without_gpu():
     L = _lib.lib()
     good = _lib.problem(16, 4, 1, 8, inputs.record_stride(4, 1, 0), 0)
-    assert _lib.chain_stride(good) == (good.cand_stride + 16 + 8 * 4 + 15) // 16 * 16
+    assert _lib.chain_stride(good) == (good.cand_stride + 16 + 16 * 4 + 15) // 16 * 16
     assert _lib.queue_capacity(good) == 3 * 1 * 8
     bad = [
         _lib.problem(16, 65, 1, 8, 256, 0),       # P > 64
@@ -51,10 +51,22 @@ def test_argument_checks_without_gpu():
     for p in bad:
         assert L.octo_sim_batch(ctypes.byref(p), None, None, None, 1, None, None, None) == -1
         assert L.octo_tune_step(ctypes.byref(p), None, None, None, None, 1, 0, 0, None) == -1
+        assert L.octo_tune_step_mem(ctypes.byref(p), None, None, None, 0, None, None, None, 1, 0,
+                                    0, None) == -1
+        assert L.octo_advance_w(ctypes.byref(p), None, None, None, None, None, 1, None, None,
+                                None, None, None) == -1
     # valid problem but null arrays / negative sizes are rejected before any launch
     assert L.octo_sim_batch(ctypes.byref(good), None, None, None, 4, None, None, None) == -1
     assert L.octo_sim_batch(ctypes.byref(good), None, None, None, -1, None, None, None) == -1
     assert L.octo_tune_step(ctypes.byref(good), None, None, None, None, 2, 0, -1, None) == -1
+    assert L.octo_tune_step_mem(ctypes.byref(good), None, None, None, 8, None, None, None, 2, 0,
+                                0, None) == -1
+    assert L.octo_tune_step_mem(ctypes.byref(good), None, None, None, 5000, None, None, None, 2,
+                                0, 0, None) == -1  # max_advance above OCTO_MAX_ADVANCE
+    assert L.octo_advance_w(ctypes.byref(good), None, None, None, None, None, 3, None, None, None,
+                            None, None) == -1
+    assert L.octo_advance_w(ctypes.byref(good), None, None, None, None, None, 0, None, None, None,
+                            None, None) == 0
     # an empty batch is a no-op
     assert L.octo_sim_batch(ctypes.byref(good), None, None, None, 0, None, None, None) == 0
     assert L.octo_strerror(-1) == b"invalid argument"
