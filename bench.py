@@ -76,6 +76,58 @@ def copy_calibration(torch):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}), flush=True)
 
 
+def time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev, warmup, steps,
+                   with_cpu):
+    """Selective W advancing (octo_advance_w) on the batch's first 65,536 split-backward (ZB)
+    candidates, each given 255 move slots, under one capacity for all devices: the 40th
+    percentile of the candidates' largest peaks."""
+    zb = recs_np[recs_np[:, 0] == inputs.POLICY["ZB"]][:65536]
+    mp = 255
+    stride = inputs.record_stride(w.P, w.v_max, mp)
+    r_np = np.zeros((len(zb), stride), np.uint8)
+    r_np[:, :zb.shape[1]] = zb
+    n = len(r_np)
+    prob = _lib.problem(w.L, w.P, w.v_max, w.M, stride, mp)
+    r = torch.from_numpy(r_np).to(dev)
+    _, _, pk0 = _lib.sim_batch_mem(prob, costs, mem, link, r)
+    cap_np = np.full(w.P, int(np.percentile(pk0.max(dim=1).values.cpu().numpy(), 40)), np.int64)
+    cap = torch.from_numpy(cap_np).to(dev)
+    out = torch.empty_like(r)
+    for _ in range(max(warmup, 1)):
+        res = _lib.advance_w(prob, costs, mem, cap, link, r, out_candidates=out)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        res = _lib.advance_w(prob, costs, mem, cap, link, r, out_candidates=out)
+    torch.cuda.synchronize()
+    secs = (time.perf_counter() - t0) / steps
+    o_rec, o_ms, o_bub, o_pk = (x.cpu().numpy() for x in res)
+    fit0 = int(((pk0.cpu().numpy() <= cap_np).all(axis=1)).sum())
+    fit1 = int(((o_pk <= cap_np).all(axis=1) & (o_ms > 0)).sum())
+    adv = o_rec[:, 2].astype(np.int64) - r_np[:, 2]
+    res = {"value": round(n / secs, 1), "unit": "candidates/s", "ms_per_call": round(secs * 1e3, 3),
+           "candidates": n, "move_slots": mp, "capacity_bytes": int(cap_np[0]),
+           "fit_before": fit0, "fit_after": fit1, "mean_advances": round(float(adv.mean()), 2),
+           "cpu_baseline": None}
+    if with_cpu:
+        from oracle import octoref
+        sample = np.arange(0, n, 32)
+        threads = min(16, os.cpu_count() or 1)
+        rprob = octoref.problem(w.L, w.P, w.v_max, w.M, stride, mp)
+        c0 = time.perf_counter()
+        rr = octoref.advance_w(rprob, inputs.layer_costs(w), inputs.layer_mem(w),
+                               cap_np, inputs.link_matrix(w.P, w.link_ns), r_np[sample],
+                               nthreads=threads)
+        c1 = time.perf_counter()
+        same = bool((rr[0] == o_rec[sample]).all() and (rr[1] == o_ms[sample]).all() and
+                    (rr[3] == o_pk[sample]).all())
+        res["cpu_baseline"] = {"value": round(len(sample) / (c1 - c0), 1), "unit": "candidates/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"every 32nd of the same candidates ({len(sample)})",
+                               "parity_on_sample": same}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -198,6 +250,8 @@ def main():
     }
 
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
+    w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
+                               args.warmup, min(args.steps, 3), not args.no_cpu)
     cpu = None
     if not args.no_cpu:
         from oracle import octoref
@@ -227,6 +281,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "memory_model": memory_model,
+        "w_advance": w_advance,
     }
     print(json.dumps(out), flush=True)
 
