@@ -203,7 +203,8 @@ def main():
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         t = json.load(open(TRAFFIC_FILE))
-        if t.get("kernel_source_sha") == kernel_source_hash() and t.get("kernel") == SIM_KERNELS[dom]:
+        tk = str(t.get("kernel", "")).replace(", false>", ">")
+        if t.get("kernel_source_sha") == kernel_source_hash() and tk == SIM_KERNELS[dom]:
             traffic = t.get("hbm_bytes_per_launch")
     all_ms = float(per_kernel_ms.sum())
     roofline = {
