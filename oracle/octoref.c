@@ -534,13 +534,65 @@ static void peak_memory(const ref_dag_in* g, const ref_sop* sq, const int* qoff,
   }
 }
 
+/* Communication nodes and their overlap (§5 "Estimating Pipeline Performance"; the comm counts
+ * of §7's communication table). Every cross-device data edge X -> Y is a send node on X's device
+ * and a receive node on Y's, each lasting c = link[dev X][dev Y]; the transfer runs from X's
+ * end for c. A node overlaps with the computation adjacent to it in its device's order — a send
+ * with the op that follows X, a receive with the op that precedes Y — by the time both run:
+ * overlap = |[start, end] of that op ∩ [end of X, end of X + c]|; overlappable iff > 0.
+ * comm[4] += {nodes, overlappable nodes, node time (2c per edge), overlap time}. */
+static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff, const int* qlen,
+                         const int64_t* start, int64_t* comm) {
+  const int S = g->S, M = g->M;
+  for (int d = 0; d < g->P; ++d) {
+    for (int i = 0; i < qlen[d]; ++i) {
+      const ref_sop o = sq[qoff[d] + i];
+      const int64_t st = start[node_id(S, M, o.kind, o.s, o.m)];
+      const int64_t fin = st + op_dur(g, o.kind, o.s);
+      /* the op's input from another device, and the op it is received during */
+      int sp = -1;
+      if (o.kind == KF && o.s > 0) sp = o.s - 1;
+      if (o.kind == KB && o.s < S - 1) sp = o.s + 1;
+      if (sp >= 0 && g->dev[sp] != d) {
+        const int64_t c = g->link[g->dev[sp] * g->P + d];
+        const int64_t xs = start[node_id(S, M, o.kind, sp, o.m)];
+        const int64_t xf = xs + op_dur(g, o.kind, sp);
+        comm[0] += 1, comm[2] += c;
+        if (i > 0) {
+          const ref_sop z = sq[qoff[d] + i - 1];
+          const int64_t zs = start[node_id(S, M, z.kind, z.s, z.m)];
+          const int64_t zf = zs + op_dur(g, z.kind, z.s);
+          const int64_t lo = zs > xf ? zs : xf, hi = zf < xf + c ? zf : xf + c;
+          if (hi > lo) comm[1] += 1, comm[3] += hi - lo;
+        }
+      }
+      /* the op's output to another device, and the op it is sent during */
+      int sc = -1;
+      if (o.kind == KF && o.s < S - 1) sc = o.s + 1;
+      if (o.kind == KB && o.s > 0) sc = o.s - 1;
+      if (sc >= 0 && g->dev[sc] != d) {
+        const int64_t c = g->link[d * g->P + g->dev[sc]];
+        comm[0] += 1, comm[2] += c;
+        if (i + 1 < qlen[d]) {
+          const ref_sop nx = sq[qoff[d] + i + 1];
+          const int64_t ns = start[node_id(S, M, nx.kind, nx.s, nx.m)];
+          const int64_t nf = ns + op_dur(g, nx.kind, nx.s);
+          const int64_t lo = ns > fin ? ns : fin, hi = nf < fin + c ? nf : fin + c;
+          if (hi > lo) comm[1] += 1, comm[3] += hi - lo;
+        }
+      }
+    }
+  }
+}
+
 /* Evaluate a candidate given its local queues (after perturbations). mem (nullable): layer
  * memory [L][2] = {activation bytes per micro-batch, static bytes}; then peak[P] is filled, and
  * ppos[P] (nullable) with the queue position at which each device first reaches its peak (-1
  * when it holds no activations). */
-static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
-                      const int64_t* link, const ref_op* q, int qcap, const int* qlen,
-                      const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos) {
+static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
+                        const int64_t* link, const ref_op* q, int qcap, const int* qlen,
+                        const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos,
+                        int64_t* comm) {
   int P = pr->P, S = c->S, split;
   resolve(pr, c, &split);
   int64_t F[64], B[64], W[64];
@@ -559,8 +611,13 @@ static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* c
     }
   }
   ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link};
-  int64_t* start = mem ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M) : NULL;
+  int64_t* start =
+      (mem || comm) ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M) : NULL;
   int rc = simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
+  if (comm && rc == SIM_OK) {
+    for (int k = 0; k < 4; ++k) comm[k] = 0;
+    comm_overlap(&g, sq, qoff, qlen, start, comm);
+  }
   if (mem && rc == SIM_OK) {
     int64_t act[64], stat[64];
     for (int s = 0; s < S; ++s) {
@@ -574,10 +631,16 @@ static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* c
   return rc;
 }
 
+static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
+                      const int64_t* link, const ref_op* q, int qcap, const int* qlen,
+                      const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos) {
+  return eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, ppos, NULL);
+}
+
 /* Full evaluation of one candidate record: makespan + bubbles, or sentinels. */
 static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                         const int64_t* link, const uint8_t* rec, int64_t* ms, int64_t* bub,
-                        int64_t* peak) {
+                        int64_t* peak, int64_t* comm) {
   ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
   decode(pr, rec, c);
   int P = pr->P;
@@ -592,7 +655,7 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
         apply_perturbations(pr, c, q, qcap, qlen) != 0) {
       sentinel = REF_INVALID;
     } else {
-      int rc = eval_local(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL);
+      int rc = eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm);
       if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
       else if (rc != SIM_OK) sentinel = REF_INVALID;
     }
@@ -603,6 +666,8 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
     for (int d = 0; d < P; ++d) bub[d] = sentinel;
     if (peak)
       for (int d = 0; d < P; ++d) peak[d] = sentinel;
+    if (comm)
+      for (int k = 0; k < 4; ++k) comm[k] = sentinel;
   }
   free(c);
 }
@@ -719,6 +784,7 @@ typedef struct {
   int64_t* out_ms;
   int64_t* out_bub;
   int64_t* out_peak;
+  int64_t* out_comm;
 } batch_job;
 
 static void* batch_worker(void* arg) {
@@ -726,15 +792,16 @@ static void* batch_worker(void* arg) {
   for (int64_t i = j->lo; i < j->hi; ++i)
     eval_record(j->pr, j->costs, j->mem, j->link, j->cands + (size_t)i * j->pr->cand_stride,
                 j->out_ms + i, j->out_bub + (size_t)i * j->pr->P,
-                j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL);
+                j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL,
+                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL);
   return NULL;
 }
 
 /* Evaluate n candidate records (host memory). nthreads >= 1 worker threads split the batch.
  * mem (nullable, with out_peak): layer memory [L][2]; out_peak[n][P] = peak bytes per device. */
-int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
-                         const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
-                         int64_t* out_bub, int64_t* out_peak, int nthreads) {
+static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
+                     const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
+                     int64_t* out_bub, int64_t* out_peak, int64_t* out_comm, int nthreads) {
   if (!check_problem(pr) || n < 0 || (n > 0 && (!costs || !link || !cands || !out_ms || !out_bub)))
     return REF_EINVAL;
   if ((mem == NULL) != (out_peak == NULL)) return REF_EINVAL;
@@ -745,7 +812,7 @@ int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int6
   batch_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
     jobs[t] = (batch_job){pr,     costs,  mem,     link,    cands, n * t / nthreads,
-                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak};
+                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm};
     if (nthreads == 1) batch_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, batch_worker, &jobs[t]);
   }
@@ -754,10 +821,25 @@ int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int6
   return REF_OK;
 }
 
+int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
+                         const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
+                         int64_t* out_bub, int64_t* out_peak, int nthreads) {
+  return run_batch(pr, costs, mem, link, cands, n, out_ms, out_bub, out_peak, NULL, nthreads);
+}
+
 int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t* link,
                      const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                      int nthreads) {
-  return oracle_sim_batch_mem(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, nthreads);
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, nthreads);
+}
+
+/* Evaluation plus communication accounting: out_comm[n][4] = {comm nodes, overlappable nodes,
+ * comm node time, overlap time} (sentinels for deadlocked / invalid candidates). */
+int oracle_sim_batch_comm(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                          const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                          int64_t* out_comm, int nthreads) {
+  if (n > 0 && !out_comm) return REF_EINVAL;
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, out_comm, nthreads);
 }
 
 /* Selective W advancing on a batch of candidate records. Each record's queues (policy, then its

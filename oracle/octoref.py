@@ -35,6 +35,9 @@ def lib():
         L.oracle_sim_batch_mem.argtypes = [ctypes.POINTER(RefProblem), p, p, p, p,
                                            ctypes.c_int64, p, p, p, ctypes.c_int]
         L.oracle_sim_batch_mem.restype = ctypes.c_int
+        L.oracle_sim_batch_comm.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64,
+                                            p, p, p, ctypes.c_int]
+        L.oracle_sim_batch_comm.restype = ctypes.c_int
         L.oracle_dump_queues.argtypes = [ctypes.POINTER(RefProblem), p, p, ctypes.c_int32, p]
         L.oracle_dump_queues.restype = ctypes.c_int
         L.oracle_sim_queues.argtypes = [ctypes.c_int32] * 4 + [p] * 9 + [p, p]
@@ -96,6 +99,24 @@ def sim_batch_mem(prob, costs, mem, link, cands, nthreads=1):
     if rc != 0:
         raise ValueError(f"oracle_sim_batch_mem rejected the arguments (rc={rc})")
     return ms, bub, peak
+
+
+def sim_batch_comm(prob, costs, link, cands, nthreads=1):
+    """Evaluate candidate records with communication accounting. Returns (makespan[n],
+    bubble[n, P], comm[n, 4]) with comm = {comm nodes, overlappable nodes, comm node time,
+    overlap time}."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    comm = np.zeros((n, 4), dtype=np.int64)
+    rc = lib().oracle_sim_batch_comm(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(cands), n,
+                                     _ptr(ms), _ptr(bub), _ptr(comm), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch_comm rejected the arguments (rc={rc})")
+    return ms, bub, comm
 
 
 def advance_w(prob, costs, mem, cap, link, cands, nthreads=1):
