@@ -128,6 +128,25 @@ int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        void* stream);
 
 /*
+ * octo_sim_batch_comm — octo_sim_batch plus communication accounting (§5: send and receive
+ * nodes of the cross-device dependencies; the simulator marks a node overlappable when it can
+ * run beside a computation and records the overlap time; §7's communication statistics). Every
+ * data edge between stages on different devices, F(s,m) -> F(s+1,m) or B(s+1,m) -> B(s,m), is
+ * one send node on the producer's device and one receive node on the consumer's, each lasting
+ * c = link[producer device][consumer device], the transfer running from the producer's end for
+ * c (as in the time model). A send overlaps with the op that follows the producer on its device,
+ * a receive with the op that precedes the consumer on its device, by the length of time that op
+ * and the transfer both run; a node is overlappable iff that length is > 0.
+ *   out_comm  int64 [n][4]: {comm nodes, overlappable nodes, total node time (each edge counted
+ *             twice, once per node), total overlap time}; OCTO_MS_DEADLOCK / OCTO_MS_INVALID in
+ *             all four like the makespan.
+ * Other arguments, results and status as octo_sim_batch (out_comm non-NULL).
+ */
+int octo_sim_batch_comm(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                        const void* candidates, int64_t n, int64_t* out_makespan,
+                        int64_t* out_bubble, int64_t* out_comm, void* stream);
+
+/*
  * octo_advance_w — selective W advancing (§6 "Scheduling Tuning", third policy) under the
  * per-device capacity of §6 Eq. 2, on a batch of candidate records. For each record, after its
  * queues are generated and its moves applied: while some device's peak (as octo_sim_batch_mem)

@@ -46,6 +46,7 @@ struct SimArgs {
   const int64_t* pre;    // [(L+1)][3] prefix sums of layer costs
   const int64_t* pre_mem;  // [(L+1)][2] prefix sums of layer memory (memory-model calls)
   int64_t* out_peak;       // [n][P] peak bytes per device (memory-model calls)
+  int64_t* out_comm;       // [n][4] communication tally (communication-accounting calls)
   const int64_t* link;   // [P][P]
   const uint8_t* cands;
   int64_t n;
@@ -90,19 +91,21 @@ __device__ __forceinline__ void zero_chunks(Chunks<VMAX>& c) {
   for (int k = 0; k < VMAX; ++k) {
     c.st[k] = 0, c.base[k] = 0, c.frow[k] = 0, c.fmask[k] = 0, c.brow[k] = 0, c.bmask[k] = 0;
     c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = c.mA[k] = 0;
+    c.cF[k] = c.cB[k] = 0, c.xF[k] = c.xB[k] = 0;
   }
   c.split = 0;
 }
 
 // Stages of device d (ascending), their durations, incoming link weights and finish-table
 // rows; returns busy(d). pre_mem (nullable): memory prefix sums; then each chunk's activation
-// bytes go to c.mA and the device's static bytes to *stat.
+// bytes go to c.mA and the device's static bytes to *stat. comm: also the transfer time of each
+// op's output and the CX flags of its input and output.
 template <int VMAX>
 __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr,
                                                 const uint8_t* rec, const int64_t* pre,
                                                 const int64_t* link, int d, int v, int split,
                                                 const Ring& ring, const int64_t* pre_mem = nullptr,
-                                                int64_t* stat = nullptr) {
+                                                int64_t* stat = nullptr, bool comm = false) {
   const int S = pr.P * v, M = pr.M;
   const uint8_t* bnd = rec + 4;
   const uint8_t* dev = rec + 3 + pr.s_max;
@@ -138,6 +141,13 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       const int dn = s < S - 1 ? dev[s + 1] : d;
       c.wF[k] = dp != d ? link[dp * pr.P + d] : 0;
       c.wB[k] = dn != d ? link[dn * pr.P + d] : 0;
+      if (comm) {
+        // a forward's output goes to stage s + 1, a backward's to stage s - 1
+        c.cF[k] = dn != d ? link[d * pr.P + dn] : 0;
+        c.cB[k] = dp != d ? link[d * pr.P + dp] : 0;
+        c.xF[k] = (dp != d ? CX_IN : 0) | (dn != d ? CX_OUT : 0);
+        c.xB[k] = (dn != d ? CX_IN : 0) | (dp != d ? CX_OUT : 0);
+      }
       busy += f + bi + wg;
       if (pre_mem) {
         c.mA[k] = pre_mem[2 * b1] - pre_mem[2 * b0];
@@ -149,15 +159,36 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
   return busy * M;
 }
 
-// One device's results for candidate cand (deadlock: sentinels); MEM adds its peak bytes.
-template <bool MEM>
+// Sum of the communication tallies of a group's lanes (all lanes of the group take part).
+__device__ __forceinline__ CommTally group_tally(CommTally x, int G) {
+  for (int off = G >> 1; off > 0; off >>= 1) {
+    x.n += __shfl_xor(x.n, off, G);
+    x.nov += __shfl_xor(x.nov, off, G);
+    x.t += __shfl_xor(x.t, off, G);
+    x.tov += __shfl_xor(x.tov, off, G);
+  }
+  return x;
+}
+
+// One device's results for candidate cand (deadlock: sentinels); XM adds its peak bytes, XC the
+// candidate's communication tally (tot: the group's sum).
+template <int X>
 __device__ __forceinline__ void put_results(const SimArgs& a, int64_t cand, int d, bool dead,
-                                            int64_t ms, int64_t busy, int64_t stat,
-                                            int64_t peak) {
+                                            int64_t ms, int64_t busy, int64_t stat, int64_t peak,
+                                            const CommTally& tot) {
   const int P = a.pr.P;
   if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
   a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
-  if constexpr (MEM) a.out_peak[cand * P + d] = dead ? OCTO_MS_DEADLOCK : stat + peak;
+  if constexpr (X == XM) a.out_peak[cand * P + d] = dead ? OCTO_MS_DEADLOCK : stat + peak;
+  if constexpr (X == XC) {
+    if (d == 0) {
+      int64_t* o = a.out_comm + cand * 4;
+      o[0] = dead ? OCTO_MS_DEADLOCK : tot.n;
+      o[1] = dead ? OCTO_MS_DEADLOCK : tot.nov;
+      o[2] = dead ? OCTO_MS_DEADLOCK : tot.t;
+      o[3] = dead ? OCTO_MS_DEADLOCK : tot.tov;
+    }
+  }
 }
 
 // Group bits for deadlock folding: this lane's group bit and the set of all group bits.
@@ -179,7 +210,7 @@ __device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, i
 // Simulate one candidate per group of the wave with generator kind GEN (40-bit slots shared by
 // the wave's groups; each group's staged record sits in that memory until it is cleared), write
 // the results. cand < 0: this group has no candidate. P2: P and v are powers of two.
-template <int VMAX, int GEN, bool P2, bool MEM>
+template <int VMAX, int GEN, bool P2, int X>
 __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split,
                                               uint8_t* lds_wave) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -200,10 +231,12 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   L.pos = 0;
   L.nops = 0;
   L.mem = L.peak = 0;
+  L.cm.reset();
   int64_t busy = 0, stat = 0;
   const bool mine = has && d < P;
   if (mine) {
-    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat);
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat,
+                              X == XC);
     L.nops = (split ? 3 : 2) * v * M;
   } else {
     zero_chunks<VMAX>(c);
@@ -219,19 +252,19 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     GenAfab g;
     g.init(v, M);
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   } else if constexpr (GEN == GEN_INTER) {
     const int r = c.st[0];
     if constexpr (P2) {
       GenInterP2 g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     } else {
       GenInter g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     }
   } else {
     GenMerge<VMAX> g;
@@ -239,16 +272,18 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
            [&](int k) { return pick<VMAX>(c.st, k); });
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX, false, MEM>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
   }
 
   const int64_t ms = group_max(L.clock, G);
+  CommTally tot = L.cm;
+  if constexpr (X == XC) tot = group_tally(L.cm, G);
   if (mine) {
     if (ms >= Table40::LIMIT) {
       // times beyond the 40-bit slots: recompute this candidate with 64-bit slots
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
     } else {
-      put_results<MEM>(a, cand, d, dead, ms, busy, stat, L.peak);
+      put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot);
     }
   }
 }
@@ -269,7 +304,7 @@ __device__ __forceinline__ int qt_row(const SimArgs& a, int gen, int v, int spli
 // Table-driven simulation of one candidate per group (INTER or MERGE at v <= 2). Durations and
 // weights must fit 32 bits; a candidate with a larger one, or whose times pass the 40-bit
 // slots, is recomputed on the 64-bit path.
-template <int VMAX, bool MEM>
+template <int VMAX, int X>
 __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, int gen,
                                         int split, uint8_t* lds_wave) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -278,7 +313,7 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   const Table40 T{reinterpret_cast<uint32_t*>(lds_wave),
                   lds_wave + (size_t)a.slots * a.CPW * 4, __ffs(a.CPW) - 1, g < a.CPW ? g : 0};
   uint8_t* rec = lds_wave + (size_t)(g < a.CPW ? g : 0) * a.rec_stride;
-  constexpr int SREC = MEM ? 16 : 8;  // bytes per stream record
+  constexpr int SREC = X != XP ? 16 : 8;  // bytes per stream record
   uint8_t* strm = lds_wave + a.strm_off + lane_id() * SREC;
   const bool has = cand >= 0;
   const int S = P * v;
@@ -291,7 +326,8 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   bool fits = true;
   const bool mine = has && d < P;
   if (mine) {
-    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat);
+    busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat,
+                              X == XC);
 #pragma unroll
     for (int kind = 0; kind < 3; ++kind) {
 #pragma unroll
@@ -302,9 +338,15 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
           fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
           uint8_t* rec_e = strm + (kind * v + k) * 64 * SREC;
           *reinterpret_cast<uint2*>(rec_e) = make_uint2((uint32_t)w, (uint32_t)du);
-          if constexpr (MEM) {
+          if constexpr (X == XM) {
             const int64_t dm = kind == KF ? c.mA[k] : (kind == KB && split) ? 0 : -c.mA[k];
             *reinterpret_cast<int64_t*>(rec_e + 8) = dm;
+          }
+          if constexpr (X == XC) {
+            const int64_t co = kind == KF ? c.cF[k] : kind == KB ? c.cB[k] : 0;
+            const int cx = kind == KF ? c.xF[k] : kind == KB ? c.xB[k] : 0;
+            fits = fits && (uint64_t)co <= 0xFFFFFFFFull;
+            *reinterpret_cast<uint2*>(rec_e + 8) = make_uint2((uint32_t)co, (uint32_t)cx);
           }
         }
       }
@@ -324,14 +366,18 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
 
   bool dead = false;
   int64_t clock = 0, mem = 0, peak = 0;
-  relax_tab<MEM>(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead, mem, peak);
+  CommTally cm;
+  cm.reset();
+  relax_tab<X>(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead, mem, peak, cm);
 
   const int64_t ms = group_max(clock, G);
+  CommTally tot = cm;
+  if constexpr (X == XC) tot = group_tally(cm, G);
   if (mine) {
     if (wide || ms >= Table40::LIMIT) {
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
     } else {
-      put_results<MEM>(a, cand, d, dead, ms, busy, stat, peak);
+      put_results<X>(a, cand, d, dead, ms, busy, stat, peak, tot);
     }
   }
 }
@@ -496,6 +542,8 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
       for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
       if (a.out_peak)
         for (int d = 0; d < a.pr.P; ++d) a.out_peak[i * a.pr.P + d] = OCTO_MS_INVALID;
+      if (a.out_comm)
+        for (int k = 0; k < 4; ++k) a.out_comm[i * 4 + k] = OCTO_MS_INVALID;
     } else {
       bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
     }
@@ -557,19 +605,19 @@ __device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, uint64_
   return -1;
 }
 
-template <int VMAX, bool MEM>
+template <int VMAX, int X>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
                                              int split, uint8_t* lds_wave) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
-  if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false, MEM>(a, cand, v, split, lds_wave);
-  else if (p2) run_generated<VMAX, GEN_INTER, true, MEM>(a, cand, v, split, lds_wave);
-  else run_generated<VMAX, GEN_INTER, false, MEM>(a, cand, v, split, lds_wave);
+  if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false, X>(a, cand, v, split, lds_wave);
+  else if (p2) run_generated<VMAX, GEN_INTER, true, X>(a, cand, v, split, lds_wave);
+  else run_generated<VMAX, GEN_INTER, false, X>(a, cand, v, split, lds_wave);
 }
 
 // Generated-queue simulation (INTER and MERGE) for the bins in a.bin_mask of one v class:
 // VC = 1 (v = 1), 2 (v = 2) or 8 (v = 3..8); finish tables sized for that class with a.ring
-// slots per row. MEM: also the peak activation memory per device.
-template <int VC, bool MEM>
+// slots per row. X: XM also the peak activation memory per device, XC the communication tally.
+template <int VC, int X>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int g = lane_id() / a.G;
@@ -593,11 +641,11 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     }
     if constexpr (VC <= 2) {
       if (a.qtab) {
-        run_tab<VC, MEM>(a, cand, v, gen, split, smem);
+        run_tab<VC, X>(a, cand, v, gen, split, smem);
         continue;
       }
     }
-    dispatch_gen<VC, MEM>(a, gen, cand, v, split, smem);
+    dispatch_gen<VC, X>(a, gen, cand, v, split, smem);
   }
 }
 
@@ -657,6 +705,19 @@ struct AfabRow {
     }
     return f;
   }
+  // the same row, tallying each op's communication nodes (flags cx, output transfer cout)
+  __device__ __forceinline__ int64_t sweep_c(int, int64_t f, int64_t w, int64_t dur, int cx,
+                                             int64_t cout, CommTally& ct) {
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+      const int64_t y = r[m] + w;
+      const int64_t st = y > f ? y : f;
+      ct.op(true, cx, y, w, f, st, st + dur, cout);
+      f = st + dur;
+      r[m] = f;
+    }
+    return f;
+  }
 };
 template <>
 struct AfabRow<0> {
@@ -672,16 +733,29 @@ struct AfabRow<0> {
   __device__ __forceinline__ int64_t sweep(int M, int64_t f, int64_t w, int64_t dur) {
     return sweep_row(row, stride, M, f, w, dur);
   }
+  __device__ __forceinline__ int64_t sweep_c(int M, int64_t f, int64_t w, int64_t dur, int cx,
+                                             int64_t cout, CommTally& ct) {
+    for (int m = 0; m < M; ++m) {
+      const int64_t y = row[m * stride] + w;
+      const int64_t st = y > f ? y : f;
+      ct.op(true, cx, y, w, f, st, st + dur, cout);
+      f = st + dur;
+      row[m * stride] = f;
+    }
+    return f;
+  }
 };
 
 // Input weight of the first stage's forwards: their row holds zeros, so any value this far below
 // zero leaves fin(0, m) = dur + fin(0, m - 1).
 constexpr int64_t AFAB_NO_INPUT = -((int64_t)1 << 62);
 
-// MEM: a GPipe device holds every micro-batch of all its stages after its forwards, so its peak
-// is its static bytes + M x its stages' activation bytes.
-template <int MMAX, bool MEM>
+// XM: a GPipe device holds every micro-batch of all its stages after its forwards, so its peak
+// is its static bytes + M x its stages' activation bytes. XC: rows tally communication nodes,
+// each device's last op start and pending transfer end kept after its clock and busy time.
+template <int MMAX, int X>
 __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
+  constexpr bool MEM = X == XM;
   extern __shared__ __align__(16) uint8_t smem[];
   const int lane = lane_id();
   const int P = a.pr.P, M = a.pr.M, L = a.pr.L;
@@ -691,6 +765,8 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   int64_t* clk = reinterpret_cast<int64_t*>(smem) + (MMAX == 0 ? (size_t)M * lanes : 0) + li;
   int64_t* bsy = clk + (size_t)P * lanes;  // clk[d * lanes], bsy[d * lanes]
   int64_t* pk = bsy + (size_t)P * lanes;   // MEM: peak bytes pk[d * lanes]
+  int64_t* cps = bsy + (size_t)P * lanes;  // XC: last op start cps[d * lanes], then
+  int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
   for (;;) {
     int ch = 0;
     if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -710,7 +786,10 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
     for (int d = 0; d < P; ++d) {
       clk[d * lanes] = 0, bsy[d * lanes] = 0;
       if constexpr (MEM) pk[d * lanes] = 0;
+      if constexpr (X == XC) cps[d * lanes] = 0, cpe[d * lanes] = -1;
     }
+    CommTally acc;
+    acc.reset();
     row.clear(M);
     // rows t = 0..S-1: forwards of stage t; t = S..2S-1: backwards of stage 2S-1-t
     for (int t = 0; t < 2 * S; ++t) {
@@ -731,7 +810,18 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       const int q = fwd ? st - 1 : st + 1;
       const int dq = q >= 0 && q < S && t != S ? dev[q] : d;
       const int64_t w = (fwd && st == 0) ? AFAB_NO_INPUT : dq != d ? a.link[dq * P + d] : 0;
-      clk[d * lanes] = row.sweep(M, clk[d * lanes], w, fwd ? df : db);
+      if constexpr (X == XC) {
+        // the stage this row's outputs go to: st + 1 (forward), st - 1 (backward)
+        const int o = fwd ? st + 1 : st - 1;
+        const int dout = o >= 0 && o < S ? dev[o] : d;
+        const int cx = (dq != d ? CX_IN : 0) | (dout != d ? CX_OUT : 0);
+        acc.pst = cps[d * lanes], acc.pend = cpe[d * lanes];
+        clk[d * lanes] = row.sweep_c(M, clk[d * lanes], w, fwd ? df : db, cx,
+                                     dout != d ? a.link[d * P + dout] : 0, acc);
+        cps[d * lanes] = acc.pst, cpe[d * lanes] = acc.pend;
+      } else {
+        clk[d * lanes] = row.sweep(M, clk[d * lanes], w, fwd ? df : db);
+      }
     }
     int64_t ms = 0;
     for (int d = 0; d < P; ++d) ms = clk[d * lanes] > ms ? clk[d * lanes] : ms;
@@ -739,6 +829,10 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
     for (int d = 0; d < P; ++d) a.out_bub[cand * P + d] = ms - bsy[d * lanes];
     if constexpr (MEM)
       for (int d = 0; d < P; ++d) a.out_peak[cand * P + d] = pk[d * lanes];
+    if constexpr (X == XC) {
+      int64_t* oc = a.out_comm + cand * 4;
+      oc[0] = acc.n, oc[1] = acc.nov, oc[2] = acc.t, oc[3] = acc.tov;
+    }
   }
 }
 
@@ -787,7 +881,7 @@ __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
 
 // Candidates with perturbations, then candidates whose times overflowed the 40-bit slots:
 // queues materialised in global memory, moves applied, 64-bit finish tables.
-template <int VMAX, bool MEM>
+template <int VMAX, int X>
 __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -833,9 +927,10 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       int64_t busy = 0, stat = 0;
       Lane L;
       L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
+      L.cm.reset();
       if (mine) {
         busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem,
-                                  &stat);
+                                  &stat, X == XC);
         L.nops = materialise<VMAX>(a, c, v, gen, split, row);
         const uint8_t* pp = grec + pert_off(a.pr.s_max);
         const int np = grec[2];
@@ -855,9 +950,11 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       q.init(row, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
       bool dead = false;
-      relax<VMAX, true, MEM>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       const int64_t ms = group_max(L.clock, G);
-      if (mine) put_results<MEM>(a, cand, d, dead, ms, busy, stat, L.peak);
+      CommTally tot = L.cm;
+      if constexpr (X == XC) tot = group_tally(L.cm, G);
+      if (mine) put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot);
     }
   }
 }
@@ -948,7 +1045,7 @@ __device__ AdvOut advance_w(const Table64& T, uint16_t* row, int n, const Chunks
       GenMat q;
       q.init(row, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
-      relax<VMAX, true, false>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       ms = group_max(L.clock, G);
     }
     if (phase == AW_SIM) {
@@ -1237,7 +1334,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
       GenMat q;
       q.init(qrow, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
-      relax<VMAX, true, false>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       ms = group_max(L.clock, G);
     }
 
@@ -1469,8 +1566,8 @@ struct Setup {
 
 template <int VC>
 int mat_grid_for(const Plan& big, int cus, int* g) {
-  // the memory-model variant is sized the same way; its grid is taken for both
-  return occupancy_grid(k_sim_mat<VC, true>, big.lds_bytes, cus, g);
+  // the accounting variants are sized the same way; the memory variant's grid is taken for all
+  return occupancy_grid(k_sim_mat<VC, XM>, big.lds_bytes, cus, g);
 }
 
 // Largest number of micro-batches of one stage in flight over one device queue of the
@@ -1526,11 +1623,12 @@ struct TabGeom {
   Plan plan;
   int lg;
 };
-// mem: 16-byte stream records (two 8-byte units) with the activation delta.
-TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool mem) {
+// wide: 16-byte stream records (two 8-byte units) with the activation delta or the output
+// transfer.
+TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool wide) {
   TabGeom t;
   t.ring = make_ring(p->M, v * p->P);
-  t.plan = fast_plan(p, lds_max, v * p->P, t.ring.R, 3 * v * (mem ? 2 : 1));
+  t.plan = fast_plan(p, lds_max, v * p->P, t.ring.R, 3 * v * (wide ? 2 : 1));
   t.lg = t.plan.CPW > 0 ? __builtin_ctz(t.plan.CPW) : 0;
   return t;
 }
@@ -1538,9 +1636,9 @@ TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool mem) {
 // Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), encoded for
 // each v's launch geometry; rebuilt when (P, v_max, M), the geometry or the MERGE tables
 // change. Entry offsets are kept in the workspace.
-int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool mem, hipStream_t stream) {
+int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool wide, hipStream_t stream) {
   const int P = p->P, M = p->M, vmax2 = std::min(p->v_max, 2);
-  TabGeom geo[2] = {tab_geom(p, lds_max, 1, mem), tab_geom(p, lds_max, 2, mem)};
+  TabGeom geo[2] = {tab_geom(p, lds_max, 1, wide), tab_geom(p, lds_max, 2, wide)};
   bool same = ws.qt_valid && ws.qt_P == P && ws.qt_vmax == p->v_max && ws.qt_M == M;
   for (int v = 1; v <= vmax2; ++v)
     same = same && ws.qt_R[v - 1] == geo[v - 1].ring.R && ws.qt_lg[v - 1] == geo[v - 1].lg;
@@ -1645,6 +1743,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.pre = reinterpret_cast<const int64_t*>(base + l.pre);
   a.pre_mem = peak ? reinterpret_cast<const int64_t*>(base + l.pre_mem) : nullptr;
   a.out_peak = peak;
+  a.out_comm = nullptr;
   a.link = link;
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
@@ -1689,17 +1788,17 @@ uint64_t bins_of(int v_lo, int v_hi, bool afab) {
 // Launch k_sim<VC> over the generated bins in `mask` with its own 40-bit plan: s_cap stages of
 // ring_want (rounded up to a power of two, or M) slots; bins whose in-flight bound exceeds the
 // ring go to the 64-bit path.
-template <int VC, bool MEM>
+template <int VC, int X>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-               int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int s_cap, int ring_want,
-               uint64_t mask, int work, hipStream_t stream) {
+               int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm, int s_cap,
+               int ring_want, uint64_t mask, int work, hipStream_t stream) {
   const Ring ring = make_ring(prob->M, ring_want);
   // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS and need tables
   // encoded for exactly this geometry
   bool tab = false;
   Plan pl{};
   if (VC <= 2 && su.ws->qt_valid) {
-    const TabGeom geo = tab_geom(prob, su.di.lds_max, VC, MEM);
+    const TabGeom geo = tab_geom(prob, su.di.lds_max, VC, X != XP);
     constexpr int vi = VC <= 2 ? VC - 1 : 0;
     tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[vi] == geo.ring.R &&
           su.ws->qt_lg[vi] == geo.lg && geo.plan.G * geo.plan.CPW <= WAVE;
@@ -1708,6 +1807,7 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
   if (!tab) pl = fast_plan(prob, su.di.lds_max, s_cap, ring.R, 0);
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub, peak);
+  a.out_comm = comm;
   if (tab) a.qtab = static_cast<const uint32_t*>(su.ws->qt);
   a.bin_mask = mask, a.work = work;
   a.ring = ring.R;
@@ -1716,41 +1816,45 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
     if (((mask >> b) & 1) && ring.R < prob->M && su.ws->inflight[b] > ring.R)
       a.redo_bins |= 1ull << b;
   int grid = 0;
-  int rc = occupancy_grid(k_sim<VC, MEM>, pl.lds_bytes, su.di.cus, &grid);
+  int rc = occupancy_grid(k_sim<VC, X>, pl.lds_bytes, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  hipLaunchKernelGGL((k_sim<VC, MEM>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
+  hipLaunchKernelGGL((k_sim<VC, X>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a);
   return launch_ok();
 }
 
 // Launch k_afab over the AFAB bins of every v: one lane per candidate, each lane's row of M
 // int64 plus 2 P device words in LDS (at most 64 KiB per wave).
-template <bool MEM>
+template <int X>
 int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-                int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, hipStream_t stream) {
-  // rows of exactly 32 or 64 micro-batches live in registers; other lengths in LDS
-  const int mmax = prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
-  const size_t per_lane = (size_t)((mmax ? 0 : prob->M) + (MEM ? 3 : 2) * prob->P) * 8;
+                int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm,
+                hipStream_t stream) {
+  // rows of exactly 32 or 64 micro-batches live in registers; other lengths, and the rows of
+  // the communication variant (whose unrolled sweep would not fit the register file), in LDS
+  const int mmax = X == XC ? 0 : prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
+  const int words = X == XM ? 3 : X == XC ? 4 : 2;  // per device
+  const size_t per_lane = (size_t)((mmax ? 0 : prob->M) + words * prob->P) * 8;
   const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
   const int lds = (int)(lanes * per_lane);
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub, peak);
+  a.out_comm = comm;
   a.bin_mask = bins_of(1, prob->v_max, true);
   a.work = CTL_WORK + 3;
   int grid = 0;
-  int rc = mmax == 32   ? occupancy_grid(k_afab<32, MEM>, lds, su.di.cus, &grid)
-           : mmax == 64 ? occupancy_grid(k_afab<64, MEM>, lds, su.di.cus, &grid)
-                        : occupancy_grid(k_afab<0, MEM>, lds, su.di.cus, &grid);
+  int rc = mmax == 32   ? occupancy_grid(k_afab<32, X>, lds, su.di.cus, &grid)
+           : mmax == 64 ? occupancy_grid(k_afab<64, X>, lds, su.di.cus, &grid)
+                        : occupancy_grid(k_afab<0, X>, lds, su.di.cus, &grid);
   if (rc) return rc;
   const int64_t need = (n + lanes - 1) / lanes;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
   if (mmax == 32)
-    hipLaunchKernelGGL((k_afab<32, MEM>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+    hipLaunchKernelGGL((k_afab<32, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   else if (mmax == 64)
-    hipLaunchKernelGGL((k_afab<64, MEM>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+    hipLaunchKernelGGL((k_afab<64, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   else
-    hipLaunchKernelGGL((k_afab<0, MEM>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+    hipLaunchKernelGGL((k_afab<0, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
   return launch_ok();
 }
 
@@ -1787,17 +1891,20 @@ int record_mark(int i, hipStream_t stream) {
   return OCTO_OK;
 }
 
-// The batch evaluation behind octo_sim_batch (MEM = false) and octo_sim_batch_mem.
-template <bool MEM>
+// The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM) and
+// octo_sim_batch_comm (XC).
+template <int X>
 int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
                    const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
-                   int64_t* out_bubble, int64_t* out_peak, hipStream_t stream) {
+                   int64_t* out_bubble, int64_t* out_peak, int64_t* out_comm, hipStream_t stream) {
+  constexpr bool MEM = X == XM;
   int rc = check_problem(prob);
   if (rc) return rc;
   if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
   if (n == 0) return OCTO_OK;
   if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
   if (MEM && (!layer_mem || !out_peak)) return OCTO_EINVAL;
+  if (X == XC && !out_comm) return OCTO_EINVAL;
   if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
   std::lock_guard<std::mutex> lock(g_mu);
   Setup su;
@@ -1805,7 +1912,9 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   if (rc) return rc;
   char* base = static_cast<char*>(su.ws->base);
   int64_t* pk = MEM ? out_peak : nullptr;
+  int64_t* cm = X == XC ? out_comm : nullptr;
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble, pk);
+  a.out_comm = cm;
   const int tb = CLS_THREADS;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
@@ -1823,32 +1932,32 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
   // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
-  if ((rc = build_qtab(prob, *su.ws, su.di.lds_max, MEM, stream))) return rc;
+  if ((rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream))) return rc;
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&
-      (rc = launch_sim<2, MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk,
-                               2 * P, 2 * P, bins_of(2, 2, false), CTL_WORK + 1, stream)))
+      (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                             2 * P, 2 * P, bins_of(2, 2, false), CTL_WORK + 1, stream)))
     return rc;
   if ((rc = record_mark(1, stream))) return rc;
-  if ((rc = launch_sim<1, MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, P, P,
+  if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, P, P,
                                bins_of(1, 1, false), CTL_WORK + 0, stream)))
     return rc;
   if ((rc = record_mark(2, stream))) return rc;
   if (prob->v_max >= 3 &&
-      (rc = launch_sim<8, MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk,
-                               P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
+      (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                             P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if ((rc = launch_afab<MEM>(prob, su, link, candidates, n, out_makespan, out_bubble, pk,
-                             stream)))
+  if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                           stream)))
     return rc;
   if ((rc = record_mark(4, stream))) return rc;
   if (prob->v_max <= 2)
-    hipLaunchKernelGGL((k_sim_mat<2, MEM>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
+    hipLaunchKernelGGL((k_sim_mat<2, X>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
                        stream, a);
   else
-    hipLaunchKernelGGL((k_sim_mat<8, MEM>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
+    hipLaunchKernelGGL((k_sim_mat<8, X>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
                        stream, a);
   if ((rc = launch_ok())) return rc;
   return record_mark(5, stream);
@@ -1919,16 +2028,24 @@ int32_t octo_queue_capacity(const octo_problem* prob) {
 int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
                    void* stream) {
-  return sim_batch_impl<false>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
-                               out_bubble, nullptr, static_cast<hipStream_t>(stream));
+  return sim_batch_impl<XP>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                            out_bubble, nullptr, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        const int64_t* layer_mem, const int64_t* link, const void* candidates,
                        int64_t n, int64_t* out_makespan, int64_t* out_bubble, int64_t* out_peak,
                        void* stream) {
-  return sim_batch_impl<true>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
-                              out_bubble, out_peak, static_cast<hipStream_t>(stream));
+  return sim_batch_impl<XM>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
+                            out_bubble, out_peak, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_comm(const octo_problem* prob, const int64_t* layer_costs,
+                        const int64_t* link, const void* candidates, int64_t n,
+                        int64_t* out_makespan, int64_t* out_bubble, int64_t* out_comm,
+                        void* stream) {
+  return sim_batch_impl<XC>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                            out_bubble, nullptr, out_comm, static_cast<hipStream_t>(stream));
 }
 
 int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,

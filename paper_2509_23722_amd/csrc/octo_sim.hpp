@@ -37,6 +37,12 @@ namespace octo {
 
 constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
 
+// What an evaluation accounts for besides times: nothing, the memory model (activation bytes
+// held per device, §5 memory nodes), or communication nodes and their overlap (§5).
+constexpr int XP = 0, XM = 1, XC = 2;
+// Communication flags of an op: its input comes from another device / its output goes to one.
+constexpr int CX_IN = 1, CX_OUT = 2;
+
 // Ring geometry of one finish table: R slots per stage row, slot of m = m & mask, parity
 // (m >> lg) & 1. Without wrap (R = M): mask = all ones, lg = 30.
 struct Ring {
@@ -114,6 +120,8 @@ struct Chunks {
   int brow[VMAX], bmask[VMAX];       // backward read row offset / needed state bits
   int64_t dF[VMAX], dB[VMAX], dW[VMAX], wF[VMAX], wB[VMAX];
   int64_t mA[VMAX];                  // activation bytes of the stage per micro-batch
+  int64_t cF[VMAX], cB[VMAX];        // transfer time of the forward's / backward's output
+  int xF[VMAX], xB[VMAX];            // CX_IN | CX_OUT of the forward / backward
   int split;                         // backward split into B and W
 };
 
@@ -124,8 +132,12 @@ struct Desc {
   uint32_t state;  // state bits written on finish
   int64_t w, dur;
   int64_t dm;      // activation bytes the op allocates (> 0) or releases (< 0)
+  int64_t cout;    // transfer time of the op's output to another device
+  int cx;          // CX_IN | CX_OUT
   __device__ __forceinline__ void take_if(bool t, const Desc& o) {
     dm = t ? o.dm : dm;
+    cout = t ? o.cout : cout;
+    cx = t ? o.cx : cx;
     rd = t ? o.rd : rd;
     wr = t ? o.wr : wr;
     mask = t ? o.mask : mask;
@@ -137,10 +149,37 @@ struct Desc {
   }
 };
 
+// Communication tally of one device (XC): nodes and overlappable nodes, their time and the
+// overlap time; the last op's start and the end of its outgoing transfer (-1: none).
+struct CommTally {
+  int n, nov;
+  int64_t t, tov, pst, pend;
+  __device__ __forceinline__ void reset() { n = nov = 0, t = tov = 0, pst = 0, pend = -1; }
+  // An op ran over [st, fin] after a device clock `clock` (the previous op's end); its input
+  // arrived at tin after a transfer of w (cx & CX_IN); its output leaves for cout
+  // (cx & CX_OUT). A receive overlaps the previous op, a send the next one (§5).
+  __device__ __forceinline__ void op(bool ok, int cx, int64_t tin, int64_t w, int64_t clock,
+                                     int64_t st, int64_t fin, int64_t cout) {
+    const bool rin = ok && (cx & CX_IN);
+    const int64_t rlo = pst > tin - w ? pst : tin - w, rhi = clock < tin ? clock : tin;
+    const bool rov = rin && rhi > rlo;
+    const int64_t shi = fin < pend ? fin : pend;
+    const bool sov = ok && shi > st;
+    const bool sout = ok && (cx & CX_OUT);
+    n += (rin ? 1 : 0) + (sout ? 1 : 0);
+    t += (rin ? w : 0) + (sout ? cout : 0);
+    nov += (rov ? 1 : 0) + (sov ? 1 : 0);
+    tov += (rov ? rhi - rlo : 0) + (sov ? shi - st : 0);
+    pend = ok ? (sout ? fin + cout : -1) : pend;
+    pst = ok ? st : pst;
+  }
+};
+
 struct Lane : Desc {
   int64_t clock;
   int pos, nops;
   int64_t mem, peak;  // activation bytes held now / at most (memory-model variants)
+  CommTally cm;       // communication variants
 };
 
 template <int VMAX, typename T>
@@ -174,6 +213,8 @@ __device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, const R
   // micro-batch (B fused, W split) releases them
   const int64_t a = pick<VMAX>(c.mA, k);
   L.dm = isF ? a : (isB && c.split) ? 0 : -a;
+  L.cout = isF ? pick<VMAX>(c.cF, k) : isB ? pick<VMAX>(c.cB, k) : 0;
+  L.cx = isF ? pick<VMAX>(c.xF, k) : isB ? pick<VMAX>(c.xB, k) : 0;
 }
 
 // Fold every G-lane group of a 64-bit lane mask into the group's lowest bit.
@@ -189,8 +230,9 @@ __device__ __forceinline__ uint64_t fold_groups(uint64_t x, int G, uint64_t lsb)
 // only if this op completes (pays when one wave per SIMD must hide the LDS latency itself);
 // otherwise advance and describe after the readiness test (fewer instructions per round, the
 // latency hidden by other waves).
-// MEM: also track the activation bytes each device holds (L.mem) and their maximum (L.peak).
-template <int VMAX, bool SPEC, bool MEM, class Tab, class Gen>
+// X: XM also tracks the activation bytes each device holds (L.mem) and their maximum
+// (L.peak); XC tallies communication nodes and their overlap (L.cm).
+template <int VMAX, bool SPEC, int X, class Tab, class Gen>
 __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
                                       const Tab& T, int G, uint64_t gbit, uint64_t lsb,
                                       bool& dead, uint32_t* rec) {
@@ -215,8 +257,9 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
     if (ok && L.store) T.store(L.wr, ((uint64_t)fin << 3) | L.state);
     if (rec && ok)
       rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)gen.kind << 12) | (uint32_t)gen.m;
+    if constexpr (X == XC) L.cm.op(ok, L.cx, tin, L.w, L.clock, st, fin, L.cout);
     L.clock = ok ? fin : L.clock;
-    if constexpr (MEM) {
+    if constexpr (X == XM) {
       L.mem = ok ? L.mem + L.dm : L.mem;
       L.peak = L.mem > L.peak ? L.mem : L.peak;
     }
@@ -285,13 +328,14 @@ constexpr uint32_t QT_END = 1u << 20;
 // nothing: the slot is empty or holds the backward of micro-batch m - R, which this device has
 // already run, so its time never exceeds the device clock. Each round decodes its op first, so
 // the stream read and the slot read are in flight together, and loads the entry after next at
-// its start, to be committed at its end. Rl = R << lg. MEM: streams are 16-byte records
-// {w, dur, activation delta}; mem / peak track the activation bytes held.
-template <bool MEM>
+// its start, to be committed at its end. Rl = R << lg. XM: streams are 16-byte records
+// {w, dur, activation delta}; mem / peak track the activation bytes held. XC: 16-byte records
+// {w, dur, output transfer time, CX flags}; cm tallies the communication nodes.
+template <int X>
 __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint32_t row, int Rl,
                                           const uint8_t* strm, int64_t& clock, const Table40& T,
                                           int G, uint64_t gbit, uint64_t lsb, bool& dead,
-                                          int64_t& mem, int64_t& peak) {
+                                          int64_t& mem, int64_t& peak, CommTally& cm) {
   uint32_t cur = qt[row], nxt = qt[row + 1u];
   uint32_t qa = row + 2u;  // entry after next
   for (;;) {
@@ -300,7 +344,7 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
     const int rdj = (int)(cur & 0x7FFFu) | T.g;
     const int wrj = rdj + __mul24((int)((cur >> 15) & 3u), Rl) - Rl;
     const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
-    const uint32_t soff = MEM ? ((cur >> 16) & 0x1C00u) : ((cur >> 17) & 0xE00u);
+    const uint32_t soff = X != XP ? ((cur >> 16) & 0x1C00u) : ((cur >> 17) & 0xE00u);
     const uint2 wd = *reinterpret_cast<const uint2*>(strm + soff);
     const uint32_t plo = T.lo[rdj], phi = T.hi[rdj];
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
@@ -312,8 +356,12 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
       T.lo[wrj] = (uint32_t)(((uint64_t)fin << 3) | state);
       T.hi[wrj] = (uint8_t)((uint64_t)fin >> 29);
     }
+    if constexpr (X == XC) {
+      const uint2 cc = *reinterpret_cast<const uint2*>(strm + soff + 8);
+      cm.op(ok, (int)cc.y, tin, (int64_t)wd.x, clock, st, fin, (int64_t)cc.x);
+    }
     clock = ok ? fin : clock;
-    if constexpr (MEM) {
+    if constexpr (X == XM) {
       const int64_t dm = *reinterpret_cast<const int64_t*>(strm + soff + 8);
       mem = ok ? mem + dm : mem;
       peak = mem > peak ? mem : peak;
