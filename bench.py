@@ -250,6 +250,37 @@ def main():
         "layer_mem": "inputs.layer_mem (per-type activation and static bytes)",
     }
 
+    # the same batch with communication accounting (nodes, overlap), timed the same way
+    comm = torch.empty((n, 4), dtype=torch.int64, device=dev)
+    for _ in range(args.warmup):
+        _lib.sim_batch_comm(prob, costs, link, recs, ms, bub, comm)
+    torch.cuda.synchronize()
+    hip3, evs3 = hip_events(nb * args.steps)
+    torch.cuda.synchronize()
+    q0 = time.perf_counter()
+    for k in range(args.steps):
+        _lib.profile_events(evs3[nb * k:nb * (k + 1)])
+        _lib.sim_batch_comm(prob, costs, link, recs, ms, bub, comm)
+    torch.cuda.synchronize()
+    q1 = time.perf_counter()
+    _lib.profile_events([])
+    qk = np.zeros((args.steps, len(SIM_KERNELS)))
+    for k in range(args.steps):
+        for j in range(len(SIM_KERNELS)):
+            f = ctypes.c_float()
+            hip3.hipEventElapsedTime(ctypes.byref(f), evs3[nb * k + j], evs3[nb * k + j + 1])
+            qk[k, j] = f.value
+    for e in evs3:
+        hip3.hipEventDestroy(e)
+    cm_np = comm.cpu().numpy()
+    comm_model = {
+        "value": round(n * args.steps / (q1 - q0), 1), "unit": "candidates/s",
+        "ms_per_step": round((q1 - q0) / args.steps * 1e3, 4),
+        "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, qk.mean(axis=0))},
+        "overlap_rate_nodes": round(float(cm_np[:, 1].sum() / max(cm_np[:, 0].sum(), 1)), 4),
+        "overlap_rate_time": round(float(cm_np[:, 3].sum() / max(cm_np[:, 2].sum(), 1)), 4),
+    }
+
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
                                args.warmup, min(args.steps, 3), not args.no_cpu)
@@ -282,6 +313,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "memory_model": memory_model,
+        "comm_model": comm_model,
         "w_advance": w_advance,
     }
     print(json.dumps(out), flush=True)
