@@ -200,6 +200,7 @@ typedef struct {
   const int64_t* B; /* [S] stage input-grad backward */
   const int64_t* W; /* [S] stage weight-grad backward */
   const int64_t* link; /* [P*P] */
+  int serial;          /* transfers on one directed link run one at a time, in issue order */
 } ref_dag_in;
 
 static int node_id(int S, int M, int kind, int s, int m) { return (kind * S + s) * M + m; }
@@ -216,6 +217,13 @@ static int64_t edge_w(const ref_dag_in* g, int sp, int sc) {
 }
 
 /*
+ * Link serialisation (a variant of the §5 communication nodes): a directed link p -> q carries
+ * one transfer at a time, first come first served. A device issues its sends as its ops end, so
+ * its transfers on a link queue in its op order: the transfer of X starts at max(end of X, end of
+ * the link's previous transfer) and arrives c = link[p][q] later; its consumer may start then.
+ * Kahn's order below finishes a device's ops in queue order, so the link's FIFO is kept by
+ * updating its free time as each producer is finished.
+ *
  * Evaluate explicit device queues. qlen[d] ops of device d start at queue + qoff[d].
  * Outputs makespan, bubble[P]; start_out (optional) receives start times indexed by node id;
  * n_cross (optional) receives the number of cross-device data edges.
@@ -232,6 +240,7 @@ static int simulate(const ref_dag_in* g, const ref_sop* queue, const int* qoff, 
   int64_t* est = (int64_t*)calloc(nn, sizeof(int64_t));
   int64_t* fin = (int64_t*)malloc(sizeof(int64_t) * nn);
   int* ready = (int*)malloc(sizeof(int) * nn);
+  int64_t* lfree = g->serial ? (int64_t*)calloc((size_t)g->P * g->P, sizeof(int64_t)) : NULL;
   int rc = 0;
   for (int i = 0; i < nn; ++i) owner[i] = -1, next[i] = -1;
   /* queue edges */
@@ -306,6 +315,14 @@ static int simulate(const ref_dag_in* g, const ref_sop* queue, const int* qoff, 
     for (int e = 0; e < no; ++e) {
       int x = outs[e];
       int64_t t = fin[u] + ws[e];
+      const int sx = (x / M) % S;
+      if (lfree && sx != s && g->dev[sx] != g->dev[s]) {
+        /* the transfer waits for the link to be free */
+        int64_t* lf = &lfree[g->dev[s] * g->P + g->dev[sx]];
+        const int64_t go = fin[u] > *lf ? fin[u] : *lf;
+        t = go + ws[e];
+        *lf = t;
+      }
       if (t > est[x]) est[x] = t;
       if (--indeg[x] == 0) ready[nr++] = x;
     }
@@ -335,6 +352,7 @@ done:
   free(est);
   free(fin);
   free(ready);
+  free(lfree);
   return rc;
 }
 
@@ -381,7 +399,7 @@ static int merge_tau(int S, int M, int split, int64_t* tau) {
     qlen[s] = n;
     for (int i = 0; i < n; ++i) q[s * per + i] = (ref_sop){tmp[i].kind, s, tmp[i].m};
   }
-  ref_dag_in g = {S, M, split, S, dev, F, B, W, link};
+  ref_dag_in g = {S, M, split, S, dev, F, B, W, link, 0};
   int64_t ms;
   int rc = simulate(&g, q, qoff, qlen, &ms, bub, tau, NULL);
   free(q);
@@ -592,7 +610,7 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
 static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                         const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                         const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos,
-                        int64_t* comm) {
+                        int64_t* comm, int serial) {
   int P = pr->P, S = c->S, split;
   resolve(pr, c, &split);
   int64_t F[64], B[64], W[64];
@@ -610,7 +628,7 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
       sq[qoff[d] + i] = (ref_sop){o.kind, s, o.m};
     }
   }
-  ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link};
+  ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link, serial};
   int64_t* start =
       (mem || comm) ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M) : NULL;
   int rc = simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
@@ -634,13 +652,13 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
 static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                       const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                       const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos) {
-  return eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, ppos, NULL);
+  return eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, ppos, NULL, 0);
 }
 
 /* Full evaluation of one candidate record: makespan + bubbles, or sentinels. */
 static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                         const int64_t* link, const uint8_t* rec, int64_t* ms, int64_t* bub,
-                        int64_t* peak, int64_t* comm) {
+                        int64_t* peak, int64_t* comm, int serial) {
   ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
   decode(pr, rec, c);
   int P = pr->P;
@@ -655,7 +673,8 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
         apply_perturbations(pr, c, q, qcap, qlen) != 0) {
       sentinel = REF_INVALID;
     } else {
-      int rc = eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm);
+      int rc =
+          eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm, serial);
       if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
       else if (rc != SIM_OK) sentinel = REF_INVALID;
     }
@@ -785,6 +804,7 @@ typedef struct {
   int64_t* out_bub;
   int64_t* out_peak;
   int64_t* out_comm;
+  int serial;
 } batch_job;
 
 static void* batch_worker(void* arg) {
@@ -793,7 +813,7 @@ static void* batch_worker(void* arg) {
     eval_record(j->pr, j->costs, j->mem, j->link, j->cands + (size_t)i * j->pr->cand_stride,
                 j->out_ms + i, j->out_bub + (size_t)i * j->pr->P,
                 j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL,
-                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL);
+                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL, j->serial);
   return NULL;
 }
 
@@ -801,7 +821,8 @@ static void* batch_worker(void* arg) {
  * mem (nullable, with out_peak): layer memory [L][2]; out_peak[n][P] = peak bytes per device. */
 static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                      const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
-                     int64_t* out_bub, int64_t* out_peak, int64_t* out_comm, int nthreads) {
+                     int64_t* out_bub, int64_t* out_peak, int64_t* out_comm, int serial,
+                     int nthreads) {
   if (!check_problem(pr) || n < 0 || (n > 0 && (!costs || !link || !cands || !out_ms || !out_bub)))
     return REF_EINVAL;
   if ((mem == NULL) != (out_peak == NULL)) return REF_EINVAL;
@@ -812,7 +833,7 @@ static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t*
   batch_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
     jobs[t] = (batch_job){pr,     costs,  mem,     link,    cands, n * t / nthreads,
-                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm};
+                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm, serial};
     if (nthreads == 1) batch_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, batch_worker, &jobs[t]);
   }
@@ -824,13 +845,20 @@ static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t*
 int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                          const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
                          int64_t* out_bub, int64_t* out_peak, int nthreads) {
-  return run_batch(pr, costs, mem, link, cands, n, out_ms, out_bub, out_peak, NULL, nthreads);
+  return run_batch(pr, costs, mem, link, cands, n, out_ms, out_bub, out_peak, NULL, 0, nthreads);
 }
 
 int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t* link,
                      const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                      int nthreads) {
-  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, nthreads);
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 0, nthreads);
+}
+
+/* Evaluation with serialised links (see simulate). */
+int oracle_sim_batch_serial(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                            const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                            int nthreads) {
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 1, nthreads);
 }
 
 /* Evaluation plus communication accounting: out_comm[n][4] = {comm nodes, overlappable nodes,
@@ -839,7 +867,8 @@ int oracle_sim_batch_comm(const ref_problem* pr, const int64_t* costs, const int
                           const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                           int64_t* out_comm, int nthreads) {
   if (n > 0 && !out_comm) return REF_EINVAL;
-  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, out_comm, nthreads);
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, out_comm, 0,
+                   nthreads);
 }
 
 /* Selective W advancing on a batch of candidate records. Each record's queues (policy, then its
@@ -987,7 +1016,7 @@ int oracle_sim_queues(int32_t P, int32_t S, int32_t M, int32_t split, const int3
     sq[i] = (ref_sop){(ops[i] >> 24) & 0xff, (ops[i] >> 16) & 0xff, ops[i] & 0xffff};
   int dv[64];
   for (int s = 0; s < S && s < 64; ++s) dv[s] = dev[s];
-  ref_dag_in g = {S, M, split ? 1 : 0, P, dv, F, B, W, link};
+  ref_dag_in g = {S, M, split ? 1 : 0, P, dv, F, B, W, link, 0};
   int rc = simulate(&g, sq, qoff, qlen, makespan, bubble, start_out, n_cross);
   free(sq);
   return rc;

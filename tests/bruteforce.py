@@ -7,6 +7,8 @@ is pinned to something other than itself:
   starts its next op if all producers have delivered (finish + transfer <= now). This is the
   as-soon-as-possible execution the paper's traversal records (§5 "Estimating Pipeline
   Performance"), obtained without any graph algorithm. Durations must be small integers.
+  With ``serial``, a directed link carries one transfer at a time: when an op ends, each of its
+  transfers joins its link's queue and starts once the link is free.
 * ``has_cycle`` builds the dependency graph from its definition (§5, §6 "Scheduling Tuning") and
   runs an iterative three-colour DFS.
 
@@ -40,11 +42,36 @@ def _producers(op, S, split, dev, link):
     return out
 
 
-def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None):
+def _consumers(op, S, dev):
+    """Ops on other devices that take op's output."""
+    kind, s, m = op
+    if kind == F and s < S - 1 and dev[s + 1] != dev[s]:
+        return [(F, s + 1, m)]
+    if kind == B and s > 0 and dev[s - 1] != dev[s]:
+        return [(B, s - 1, m)]
+    return []
+
+
+def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None, serial=False):
     """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock."""
     total = sum(_dur(k, s, split, Fs, Bs, Ws) for q in queues for (k, s, m) in q)
     if max_ticks is None:
         max_ticks = total + 2 * S * M * (max(max(r) for r in link) if P > 0 else 0) + 2
+    arrive = {}                        # (producer, consumer) -> arrival tick (serial links)
+    link_free = {}                     # (p, q) -> tick the link is free again
+
+    def sent(op, t):
+        for c in _consumers(op, S, dev):
+            key = (dev[op[1]], dev[c[1]])
+            go = max(t, link_free.get(key, 0))
+            arrive[(op, c)] = go + link[key[0]][key[1]]
+            link_free[key] = arrive[(op, c)]
+
+    def delivered(p, w, op, t):
+        if serial and (p, op) in arrive:
+            return arrive[(p, op)] <= t
+        return p in fin and fin[p] + w <= t
+
     fin = {}
     ptr = [0] * P
     busy_until = [0] * P
@@ -54,18 +81,19 @@ def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None)
         for d in range(P):
             if running[d] is not None and busy_until[d] <= t:
                 fin[running[d]] = busy_until[d]
+                sent(running[d], busy_until[d])
                 running[d] = None
         for d in range(P):
             if running[d] is None and ptr[d] < len(queues[d]):
                 op = queues[d][ptr[d]]
-                ok = all(p in fin and fin[p] + w <= t
-                         for p, w in _producers(op, S, split, dev, link))
+                ok = all(delivered(p, w, op, t) for p, w in _producers(op, S, split, dev, link))
                 if ok:
                     running[d] = op
                     busy_until[d] = t + _dur(op[0], op[1], split, Fs, Bs, Ws)
                     ptr[d] += 1
                     if busy_until[d] == t:  # zero-length op finishes immediately
                         fin[op] = t
+                        sent(op, t)
                         running[d] = None
         if all(ptr[d] == len(queues[d]) and running[d] is None for d in range(P)):
             break
