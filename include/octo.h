@@ -147,6 +147,19 @@ int octo_sim_batch_comm(const octo_problem* prob, const int64_t* layer_costs, co
                         int64_t* out_bubble, int64_t* out_comm, void* stream);
 
 /*
+ * octo_sim_batch_serial — octo_sim_batch with serialised links (a variant of the §5 send /
+ * receive nodes): a directed link p -> q carries one transfer at a time, first come first
+ * served. A device issues each op's output transfer when the op ends, so the transfers on one
+ * of its links queue in its op order: the transfer of X starts at max(end of X, end of the
+ * link's previous transfer) and ends c = link[p][q] later, when its consumer may start. Deadlock
+ * and validity are as in octo_sim_batch (a link queue adds no cycle). Arguments, results and
+ * status as octo_sim_batch.
+ */
+int octo_sim_batch_serial(const octo_problem* prob, const int64_t* layer_costs,
+                          const int64_t* link, const void* candidates, int64_t n,
+                          int64_t* out_makespan, int64_t* out_bubble, void* stream);
+
+/*
  * octo_advance_w — selective W advancing (§6 "Scheduling Tuning", third policy) under the
  * per-device capacity of §6 Eq. 2, on a batch of candidate records. For each record, after its
  * queues are generated and its moves applied: while some device's peak (as octo_sim_batch_mem)

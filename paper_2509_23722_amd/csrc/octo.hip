@@ -91,21 +91,23 @@ __device__ __forceinline__ void zero_chunks(Chunks<VMAX>& c) {
   for (int k = 0; k < VMAX; ++k) {
     c.st[k] = 0, c.base[k] = 0, c.frow[k] = 0, c.fmask[k] = 0, c.brow[k] = 0, c.bmask[k] = 0;
     c.dF[k] = c.dB[k] = c.dW[k] = c.wF[k] = c.wB[k] = c.mA[k] = 0;
-    c.cF[k] = c.cB[k] = 0, c.xF[k] = c.xB[k] = 0;
+    c.cF[k] = c.cB[k] = 0, c.xF[k] = c.xB[k] = 0, c.dnF[k] = c.dnB[k] = -1;
   }
+  c.wW = 0;
   c.split = 0;
 }
 
 // Stages of device d (ascending), their durations, incoming link weights and finish-table
 // rows; returns busy(d). pre_mem (nullable): memory prefix sums; then each chunk's activation
-// bytes go to c.mA and the device's static bytes to *stat. comm: also the transfer time of each
-// op's output and the CX flags of its input and output.
+// bytes go to c.mA and the device's static bytes to *stat. mode XC: also the transfer time of
+// each op's output and the CX flags of its input and output; XS: those and the device each
+// output goes to, with the transfer moved from the reader's weight into the writer's slot time.
 template <int VMAX>
 __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& pr,
                                                 const uint8_t* rec, const int64_t* pre,
                                                 const int64_t* link, int d, int v, int split,
                                                 const Ring& ring, const int64_t* pre_mem = nullptr,
-                                                int64_t* stat = nullptr, bool comm = false) {
+                                                int64_t* stat = nullptr, int mode = XP) {
   const int S = pr.P * v, M = pr.M;
   const uint8_t* bnd = rec + 4;
   const uint8_t* dev = rec + 3 + pr.s_max;
@@ -141,12 +143,17 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       const int dn = s < S - 1 ? dev[s + 1] : d;
       c.wF[k] = dp != d ? link[dp * pr.P + d] : 0;
       c.wB[k] = dn != d ? link[dn * pr.P + d] : 0;
-      if (comm) {
+      if (mode == XC || mode == XS) {
         // a forward's output goes to stage s + 1, a backward's to stage s - 1
         c.cF[k] = dn != d ? link[d * pr.P + dn] : 0;
         c.cB[k] = dp != d ? link[d * pr.P + dp] : 0;
         c.xF[k] = (dp != d ? CX_IN : 0) | (dn != d ? CX_OUT : 0);
         c.xB[k] = (dn != d ? CX_IN : 0) | (dp != d ? CX_OUT : 0);
+      }
+      if (mode == XS) {
+        c.dnF[k] = dn != d ? dn : -1;
+        c.dnB[k] = dp != d ? dp : -1;
+        c.wF[k] = 0, c.wB[k] = 0;  // the writer's slot holds the arrival time
       }
       busy += f + bi + wg;
       if (pre_mem) {
@@ -155,6 +162,7 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       }
     }
   }
+  if (mode == XS) c.wW = W_NO_TIME;
   if (stat) *stat = st_bytes;
   return busy * M;
 }
@@ -232,11 +240,13 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   L.nops = 0;
   L.mem = L.peak = 0;
   L.cm.reset();
+  if constexpr (X == XS)
+    for (int i = 0; i < 16; ++i) L.lf[i] = 0;
   int64_t busy = 0, stat = 0;
   const bool mine = has && d < P;
   if (mine) {
     busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat,
-                              X == XC);
+                              X);
     L.nops = (split ? 3 : 2) * v * M;
   } else {
     zero_chunks<VMAX>(c);
@@ -327,7 +337,7 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   const bool mine = has && d < P;
   if (mine) {
     busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem, &stat,
-                              X == XC);
+                              X);
 #pragma unroll
     for (int kind = 0; kind < 3; ++kind) {
 #pragma unroll
@@ -928,9 +938,11 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       Lane L;
       L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
       L.cm.reset();
+      if constexpr (X == XS)
+        for (int i = 0; i < 16; ++i) L.lf[i] = 0;
       if (mine) {
         busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem,
-                                  &stat, X == XC);
+                                  &stat, X);
         L.nops = materialise<VMAX>(a, c, v, gen, split, row);
         const uint8_t* pp = grec + pert_off(a.pr.s_max);
         const int np = grec[2];
@@ -1797,7 +1809,7 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
   // encoded for exactly this geometry
   bool tab = false;
   Plan pl{};
-  if (VC <= 2 && su.ws->qt_valid) {
+  if (VC <= 2 && X != XS && su.ws->qt_valid) {
     const TabGeom geo = tab_geom(prob, su.di.lds_max, VC, X != XP);
     constexpr int vi = VC <= 2 ? VC - 1 : 0;
     tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[vi] == geo.ring.R &&
@@ -1891,8 +1903,9 @@ int record_mark(int i, hipStream_t stream) {
   return OCTO_OK;
 }
 
-// The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM) and
-// octo_sim_batch_comm (XC).
+// The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM),
+// octo_sim_batch_comm (XC) and octo_sim_batch_serial (XS: generated queues only; GPipe
+// candidates take the materialised path with the full table).
 template <int X>
 int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
                    const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
@@ -1932,25 +1945,29 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
   // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
-  if ((rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream))) return rc;
+  if (X != XS && (rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream))) return rc;
+  // XS: the GPipe bins join the generated launches, which hand them to the materialised path
+  auto launch_bins = [&](int lo, int hi) {
+    return bins_of(lo, hi, false) | (X == XS ? bins_of(lo, hi, true) : 0ull);
+  };
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&
       (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                             2 * P, 2 * P, bins_of(2, 2, false), CTL_WORK + 1, stream)))
+                             2 * P, 2 * P, launch_bins(2, 2), CTL_WORK + 1, stream)))
     return rc;
   if ((rc = record_mark(1, stream))) return rc;
   if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, P, P,
-                               bins_of(1, 1, false), CTL_WORK + 0, stream)))
+                               launch_bins(1, 1), CTL_WORK + 0, stream)))
     return rc;
   if ((rc = record_mark(2, stream))) return rc;
   if (prob->v_max >= 3 &&
       (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                             P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
+                             P * prob->v_max, M, launch_bins(3, 8), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                           stream)))
+  if (X != XS && (rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble,
+                                      pk, cm, stream)))
     return rc;
   if ((rc = record_mark(4, stream))) return rc;
   if (prob->v_max <= 2)
@@ -2038,6 +2055,13 @@ int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        void* stream) {
   return sim_batch_impl<XM>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
                             out_bubble, out_peak, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_serial(const octo_problem* prob, const int64_t* layer_costs,
+                          const int64_t* link, const void* candidates, int64_t n,
+                          int64_t* out_makespan, int64_t* out_bubble, void* stream) {
+  return sim_batch_impl<XS>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                            out_bubble, nullptr, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_comm(const octo_problem* prob, const int64_t* layer_costs,

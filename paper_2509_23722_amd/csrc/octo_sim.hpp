@@ -37,9 +37,13 @@ namespace octo {
 
 constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
 
-// What an evaluation accounts for besides times: nothing, the memory model (activation bytes
-// held per device, §5 memory nodes), or communication nodes and their overlap (§5).
-constexpr int XP = 0, XM = 1, XC = 2;
+// What an evaluation computes besides the plain times: the memory model (activation bytes held
+// per device, §5 memory nodes), communication nodes and their overlap (§5), or times with
+// serialised links (a directed link carries one transfer at a time, in issue order).
+constexpr int XP = 0, XM = 1, XC = 2, XS = 3;
+// Weight of a weight-gradient op's read under serialised links: its B is on its own device and
+// earlier in its queue, so only the readiness bit matters, not the (possibly delayed) slot time.
+constexpr int64_t W_NO_TIME = -((int64_t)1 << 50);
 // Communication flags of an op: its input comes from another device / its output goes to one.
 constexpr int CX_IN = 1, CX_OUT = 2;
 
@@ -122,6 +126,8 @@ struct Chunks {
   int64_t mA[VMAX];                  // activation bytes of the stage per micro-batch
   int64_t cF[VMAX], cB[VMAX];        // transfer time of the forward's / backward's output
   int xF[VMAX], xB[VMAX];            // CX_IN | CX_OUT of the forward / backward
+  int dnF[VMAX], dnB[VMAX];          // device the forward's / backward's output goes to
+  int64_t wW;                        // weight of a weight-gradient op's read
   int split;                         // backward split into B and W
 };
 
@@ -134,10 +140,12 @@ struct Desc {
   int64_t dm;      // activation bytes the op allocates (> 0) or releases (< 0)
   int64_t cout;    // transfer time of the op's output to another device
   int cx;          // CX_IN | CX_OUT
+  int dst;         // device the op's output goes to
   __device__ __forceinline__ void take_if(bool t, const Desc& o) {
     dm = t ? o.dm : dm;
     cout = t ? o.cout : cout;
     cx = t ? o.cx : cx;
+    dst = t ? o.dst : dst;
     rd = t ? o.rd : rd;
     wr = t ? o.wr : wr;
     mask = t ? o.mask : mask;
@@ -180,6 +188,8 @@ struct Lane : Desc {
   int pos, nops;
   int64_t mem, peak;  // activation bytes held now / at most (memory-model variants)
   CommTally cm;       // communication variants
+  int64_t lf[16];     // serialised links: when the link to device dst is free, per stream
+                      // (forward outputs of chunk k at k, backward outputs at VMAX + k)
 };
 
 template <int VMAX, typename T>
@@ -207,7 +217,7 @@ __device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, const R
   L.state = (isF ? ST_F : (ST_F | ST_B)) | (par << 2);
   const int64_t wf = pick<VMAX>(c.wF, k), wb = pick<VMAX>(c.wB, k);
   const int64_t df = pick<VMAX>(c.dF, k), db = pick<VMAX>(c.dB, k), dw = pick<VMAX>(c.dW, k);
-  L.w = isF ? wf : isB ? wb : 0;
+  L.w = isF ? wf : isB ? wb : c.wW;
   L.dur = isF ? df : isB ? db : dw;
   // memory nodes: a forward allocates its stage's activations, the last backward op of the
   // micro-batch (B fused, W split) releases them
@@ -215,6 +225,7 @@ __device__ __forceinline__ void describe(Desc& L, const Chunks<VMAX>& c, const R
   L.dm = isF ? a : (isB && c.split) ? 0 : -a;
   L.cout = isF ? pick<VMAX>(c.cF, k) : isB ? pick<VMAX>(c.cB, k) : 0;
   L.cx = isF ? pick<VMAX>(c.xF, k) : isB ? pick<VMAX>(c.xB, k) : 0;
+  L.dst = isF ? pick<VMAX>(c.dnF, k) : isB ? pick<VMAX>(c.dnB, k) : -1;
 }
 
 // Fold every G-lane group of a 64-bit lane mask into the group's lowest bit.
@@ -254,7 +265,25 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
     const int64_t tin = (int64_t)(p >> 3) + L.w;
     const int64_t st = tin > L.clock ? tin : L.clock;
     const int64_t fin = st + L.dur;
-    if (ok && L.store) T.store(L.wr, ((uint64_t)fin << 3) | L.state);
+    int64_t put = fin;  // the time its readers see
+    if constexpr (X == XS) {
+      // the output's transfer queues on the link to its consumer's device: it leaves when both
+      // the op and the link's previous transfer are done; the slot holds its arrival. Every
+      // stream to the same device shares the link's free time.
+      const bool out = ok && (L.cx & CX_OUT);
+      const bool isF = gen.kind == KF;
+      int64_t fr = 0;
+#pragma unroll
+      for (int k = 0; k < VMAX; ++k) fr = gen.k == k ? (isF ? L.lf[k] : L.lf[VMAX + k]) : fr;
+      const int64_t arr = (fin > fr ? fin : fr) + L.cout;
+#pragma unroll
+      for (int k = 0; k < VMAX; ++k) {
+        L.lf[k] = (out && c.dnF[k] == L.dst) ? arr : L.lf[k];
+        L.lf[VMAX + k] = (out && c.dnB[k] == L.dst) ? arr : L.lf[VMAX + k];
+      }
+      put = (L.cx & CX_OUT) ? arr : fin;
+    }
+    if (ok && L.store) T.store(L.wr, ((uint64_t)put << 3) | L.state);
     if (rec && ok)
       rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)gen.kind << 12) | (uint32_t)gen.m;
     if constexpr (X == XC) L.cm.op(ok, L.cx, tin, L.w, L.clock, st, fin, L.cout);
