@@ -76,6 +76,35 @@ def copy_calibration(torch):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}), flush=True)
 
 
+def time_variant(torch, _lib, call, n, steps, warmup):
+    """Time `call` (one batch evaluation) like the headline: wall clock over `steps` calls after
+    `warmup`, and each simulation kernel by the library's HIP events. Returns (candidates/s,
+    ms per call, {kernel: ms})."""
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    nb = len(SIM_KERNELS) + 1
+    hip, evs = hip_events(nb * steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        _lib.profile_events(evs[nb * k:nb * (k + 1)])
+        call()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    _lib.profile_events([])
+    km = np.zeros((steps, len(SIM_KERNELS)))
+    for k in range(steps):
+        for j in range(len(SIM_KERNELS)):
+            f = ctypes.c_float()
+            hip.hipEventElapsedTime(ctypes.byref(f), evs[nb * k + j], evs[nb * k + j + 1])
+            km[k, j] = f.value
+    for e in evs:
+        hip.hipEventDestroy(e)
+    return (round(n * steps / (t1 - t0), 1), round((t1 - t0) / steps * 1e3, 4),
+            {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, km.mean(axis=0))})
+
+
 def time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev, warmup, steps,
                    with_cpu):
     """Selective W advancing (octo_advance_w) on the batch's first 65,536 split-backward (ZB)
@@ -223,63 +252,33 @@ def main():
     # the same batch with the memory model (peak bytes per device), timed the same way
     mem = torch.from_numpy(inputs.layer_mem(w)).to(dev)
     peak = torch.empty((n, w.P), dtype=torch.int64, device=dev)
-    for _ in range(args.warmup):
-        _lib.sim_batch_mem(prob, costs, mem, link, recs, ms, bub, peak)
-    torch.cuda.synchronize()
-    hip2, evs2 = hip_events(nb * args.steps)
-    torch.cuda.synchronize()
-    m0 = time.perf_counter()
-    for k in range(args.steps):
-        _lib.profile_events(evs2[nb * k:nb * (k + 1)])
-        _lib.sim_batch_mem(prob, costs, mem, link, recs, ms, bub, peak)
-    torch.cuda.synchronize()
-    m1 = time.perf_counter()
-    _lib.profile_events([])
-    mk = np.zeros((args.steps, len(SIM_KERNELS)))
-    for k in range(args.steps):
-        for j in range(len(SIM_KERNELS)):
-            f = ctypes.c_float()
-            hip2.hipEventElapsedTime(ctypes.byref(f), evs2[nb * k + j], evs2[nb * k + j + 1])
-            mk[k, j] = f.value
-    for e in evs2:
-        hip2.hipEventDestroy(e)
-    memory_model = {
-        "value": round(n * args.steps / (m1 - m0), 1), "unit": "candidates/s",
-        "ms_per_step": round((m1 - m0) / args.steps * 1e3, 4),
-        "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, mk.mean(axis=0))},
-        "layer_mem": "inputs.layer_mem (per-type activation and static bytes)",
-    }
+    v_, t_, k_ = time_variant(
+        torch, _lib, lambda: _lib.sim_batch_mem(prob, costs, mem, link, recs, ms, bub, peak), n,
+        args.steps, args.warmup)
+    memory_model = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "sim_kernels_ms": k_,
+                    "layer_mem": "inputs.layer_mem (per-type activation and static bytes)"}
 
-    # the same batch with communication accounting (nodes, overlap), timed the same way
+    # with communication accounting (nodes, overlap)
     comm = torch.empty((n, 4), dtype=torch.int64, device=dev)
-    for _ in range(args.warmup):
-        _lib.sim_batch_comm(prob, costs, link, recs, ms, bub, comm)
-    torch.cuda.synchronize()
-    hip3, evs3 = hip_events(nb * args.steps)
-    torch.cuda.synchronize()
-    q0 = time.perf_counter()
-    for k in range(args.steps):
-        _lib.profile_events(evs3[nb * k:nb * (k + 1)])
-        _lib.sim_batch_comm(prob, costs, link, recs, ms, bub, comm)
-    torch.cuda.synchronize()
-    q1 = time.perf_counter()
-    _lib.profile_events([])
-    qk = np.zeros((args.steps, len(SIM_KERNELS)))
-    for k in range(args.steps):
-        for j in range(len(SIM_KERNELS)):
-            f = ctypes.c_float()
-            hip3.hipEventElapsedTime(ctypes.byref(f), evs3[nb * k + j], evs3[nb * k + j + 1])
-            qk[k, j] = f.value
-    for e in evs3:
-        hip3.hipEventDestroy(e)
+    v_, t_, k_ = time_variant(
+        torch, _lib, lambda: _lib.sim_batch_comm(prob, costs, link, recs, ms, bub, comm), n,
+        args.steps, args.warmup)
     cm_np = comm.cpu().numpy()
     comm_model = {
-        "value": round(n * args.steps / (q1 - q0), 1), "unit": "candidates/s",
-        "ms_per_step": round((q1 - q0) / args.steps * 1e3, 4),
-        "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, qk.mean(axis=0))},
+        "value": v_, "unit": "candidates/s", "ms_per_step": t_, "sim_kernels_ms": k_,
         "overlap_rate_nodes": round(float(cm_np[:, 1].sum() / max(cm_np[:, 0].sum(), 1)), 4),
         "overlap_rate_time": round(float(cm_np[:, 3].sum() / max(cm_np[:, 2].sum(), 1)), 4),
     }
+
+    # with serialised links (one transfer at a time per directed link)
+    sms = torch.empty_like(ms)
+    sbub = torch.empty_like(bub)
+    v_, t_, k_ = time_variant(
+        torch, _lib, lambda: _lib.sim_batch_serial(prob, costs, link, recs, sms, sbub), n,
+        args.steps, args.warmup)
+    s_np = sms.cpu().numpy()
+    serial_links = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "sim_kernels_ms": k_,
+                    "makespan_changed": int((s_np != ms.cpu().numpy()).sum())}
 
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
@@ -314,6 +313,7 @@ def main():
         "cpu_baseline": cpu,
         "memory_model": memory_model,
         "comm_model": comm_model,
+        "serial_links": serial_links,
         "w_advance": w_advance,
     }
     print(json.dumps(out), flush=True)

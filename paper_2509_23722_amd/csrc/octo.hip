@@ -715,6 +715,19 @@ struct AfabRow {
     }
     return f;
   }
+  // the same row with each output queued on a link (XS): lf = the link's free time; the row
+  // then holds the arrival times
+  __device__ __forceinline__ int64_t sweep_s(int, int64_t f, int64_t w, int64_t dur,
+                                             int64_t cout, int64_t& lf) {
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+      const int64_t y = r[m] + w;
+      f = (y > f ? y : f) + dur;
+      lf = (f > lf ? f : lf) + cout;
+      r[m] = lf;
+    }
+    return f;
+  }
   // the same row, tallying each op's communication nodes (flags cx, output transfer cout)
   __device__ __forceinline__ int64_t sweep_c(int, int64_t f, int64_t w, int64_t dur, int cx,
                                              int64_t cout, CommTally& ct) {
@@ -743,6 +756,16 @@ struct AfabRow<0> {
   __device__ __forceinline__ int64_t sweep(int M, int64_t f, int64_t w, int64_t dur) {
     return sweep_row(row, stride, M, f, w, dur);
   }
+  __device__ __forceinline__ int64_t sweep_s(int M, int64_t f, int64_t w, int64_t dur,
+                                             int64_t cout, int64_t& lf) {
+    for (int m = 0; m < M; ++m) {
+      const int64_t y = row[m * stride] + w;
+      f = (y > f ? y : f) + dur;
+      lf = (f > lf ? f : lf) + cout;
+      row[m * stride] = lf;
+    }
+    return f;
+  }
   __device__ __forceinline__ int64_t sweep_c(int M, int64_t f, int64_t w, int64_t dur, int cx,
                                              int64_t cout, CommTally& ct) {
     for (int m = 0; m < M; ++m) {
@@ -762,7 +785,10 @@ constexpr int64_t AFAB_NO_INPUT = -((int64_t)1 << 62);
 
 // XM: a GPipe device holds every micro-batch of all its stages after its forwards, so its peak
 // is its static bytes + M x its stages' activation bytes. XC: rows tally communication nodes,
-// each device's last op start and pending transfer end kept after its clock and busy time.
+// each device's last op start and pending transfer end kept after its clock and busy time. XS:
+// a row whose outputs cross devices queues them on its link, whose free time it takes from the
+// latest earlier row on the same directed link (rows are visited in every device's op order,
+// so that is the link's issue order); the row then holds arrival times, read with weight 0.
 template <int MMAX, int X>
 __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   constexpr bool MEM = X == XM;
@@ -777,6 +803,7 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   int64_t* pk = bsy + (size_t)P * lanes;   // MEM: peak bytes pk[d * lanes]
   int64_t* cps = bsy + (size_t)P * lanes;  // XC: last op start cps[d * lanes], then
   int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
+  int64_t* lfr = bsy + (size_t)P * lanes;  // XS: link free time after row t, lfr[t * lanes]
   for (;;) {
     int ch = 0;
     if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -820,7 +847,26 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       const int q = fwd ? st - 1 : st + 1;
       const int dq = q >= 0 && q < S && t != S ? dev[q] : d;
       const int64_t w = (fwd && st == 0) ? AFAB_NO_INPUT : dq != d ? a.link[dq * P + d] : 0;
-      if constexpr (X == XC) {
+      if constexpr (X == XS) {
+        const int o = fwd ? st + 1 : st - 1;
+        const int dout = o >= 0 && o < S ? dev[o] : d;
+        const int64_t wr = (fwd && st == 0) ? AFAB_NO_INPUT : 0;  // arrivals are in the row
+        if (dout != d) {
+          int64_t lf = 0;
+          for (int u = 0; u < t; ++u) {
+            const bool fu = u < S;
+            const int su = fu ? u : 2 * S - 1 - u, ou = fu ? su + 1 : su - 1;
+            if (dev[su] == d && ou >= 0 && ou < S && dev[ou] == dout)
+              lf = lfr[u * lanes] > lf ? lfr[u * lanes] : lf;
+          }
+          clk[d * lanes] = row.sweep_s(M, clk[d * lanes], wr, fwd ? df : db,
+                                       a.link[d * P + dout], lf);
+          lfr[t * lanes] = lf;
+        } else {
+          clk[d * lanes] = row.sweep(M, clk[d * lanes], wr, fwd ? df : db);
+          lfr[t * lanes] = 0;
+        }
+      } else if constexpr (X == XC) {
         // the stage this row's outputs go to: st + 1 (forward), st - 1 (backward)
         const int o = fwd ? st + 1 : st - 1;
         const int dout = o >= 0 && o < S ? dev[o] : d;
@@ -1846,7 +1892,9 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
   // the communication variant (whose unrolled sweep would not fit the register file), in LDS
   const int mmax = X == XC ? 0 : prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
   const int words = X == XM ? 3 : X == XC ? 4 : 2;  // per device
-  const size_t per_lane = (size_t)((mmax ? 0 : prob->M) + words * prob->P) * 8;
+  const size_t per_lane =
+      (size_t)((mmax ? 0 : prob->M) + words * prob->P + (X == XS ? 2 * prob->P * prob->v_max : 0)) *
+      8;
   const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
   const int lds = (int)(lanes * per_lane);
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
@@ -1904,8 +1952,7 @@ int record_mark(int i, hipStream_t stream) {
 }
 
 // The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM),
-// octo_sim_batch_comm (XC) and octo_sim_batch_serial (XS: generated queues only; GPipe
-// candidates take the materialised path with the full table).
+// octo_sim_batch_comm (XC) and octo_sim_batch_serial (XS: generated queues, not tables).
 template <int X>
 int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
                    const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
@@ -1946,10 +1993,7 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
   if (X != XS && (rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream))) return rc;
-  // XS: the GPipe bins join the generated launches, which hand them to the materialised path
-  auto launch_bins = [&](int lo, int hi) {
-    return bins_of(lo, hi, false) | (X == XS ? bins_of(lo, hi, true) : 0ull);
-  };
+  auto launch_bins = [&](int lo, int hi) { return bins_of(lo, hi, false); };
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&
@@ -1966,8 +2010,8 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
                              P * prob->v_max, M, launch_bins(3, 8), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if (X != XS && (rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble,
-                                      pk, cm, stream)))
+  if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                           stream)))
     return rc;
   if ((rc = record_mark(4, stream))) return rc;
   if (prob->v_max <= 2)
