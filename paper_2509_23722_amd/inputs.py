@@ -96,6 +96,26 @@ def link_matrix(P, cost):
     return m
 
 
+# MI355X platform links: eight GPUs per node, each pair joined by one xGMI link (seven per GPU)
+# of about 153 GB/s per direction; nodes joined by one 400 Gb/s NIC per GPU (50 GB/s). The
+# latencies are assumptions of this recipe: 5 us on xGMI, 20 us across nodes (as the paper's
+# own link model).
+XGMI_GPUS_PER_NODE = 8
+XGMI_GB_PER_S, XGMI_LATENCY_NS = 153, 5_000
+NIC_GB_PER_S, NIC_LATENCY_NS = 50, 20_000
+
+
+def xgmi_link_matrix(P, nbytes):
+    """Transfer cost (ns) of nbytes between pipeline devices 0..P-1 placed on consecutive GPUs
+    of MI355X nodes: xGMI within a node, the NIC between nodes; diagonal 0."""
+    intra = link_cost_ns(nbytes, XGMI_LATENCY_NS, XGMI_GB_PER_S)
+    inter = link_cost_ns(nbytes, NIC_LATENCY_NS, NIC_GB_PER_S)
+    node = np.arange(P) // XGMI_GPUS_PER_NODE
+    m = np.where(node[:, None] == node[None, :], intra, inter).astype(np.int64)
+    np.fill_diagonal(m, 0)
+    return m
+
+
 def _lognormal_ns(rng, mean_ns, sigma, size=None):
     z = rng.standard_normal(size)
     return np.rint(mean_ns * np.exp(sigma * z)).astype(np.int64)

@@ -118,3 +118,19 @@ def test_workload4_cyclic_and_huge(gpu):
     recs = I.random_candidates(rng, L, P, v_max, M, 300, max_pert=1, pert_rate=0.1)
     args = (L, P, v_max, M, 1, costs, link, recs)
     assert_same(run_gpu(gpu, *args), run_oracle(*args), "huge")
+
+
+def test_two_mi355x_nodes(gpu):
+    """P = 16 over two nodes with the xGMI / NIC link recipe and 1 GiB activations, so that the
+    node-crossing link queues: every policy and placement, against the oracle."""
+    rng = np.random.default_rng(616)
+    P, v_max, M, L = 16, 2, 16, 40
+    log("serial: two MI355X nodes")
+    costs = rng.integers(500_000, 3_000_000, size=(L, 3)).astype(np.int64)
+    link = I.xgmi_link_matrix(P, 1 << 30)
+    recs = I.random_candidates(rng, L, P, v_max, M, 400)
+    args = (L, P, v_max, M, 0, costs, link, recs)
+    g = run_gpu(gpu, *args)
+    assert_same(g, run_oracle(*args), "two nodes")
+    prob = R.problem(L, P, v_max, M, recs.shape[1], 0)
+    assert (g[0] > R.sim_batch(prob, costs, link, recs, NTHREADS)[0]).sum() > 50

@@ -93,3 +93,21 @@ def test_invariants():
     z = np.zeros((P, P), np.int64)
     assert (R.sim_batch(prob, costs, z, recs, NTHREADS)[0] ==
             R.sim_batch_serial(prob, costs, z, recs, NTHREADS)[0]).all()
+
+
+def test_xgmi_link_matrix_and_queues_across_nodes():
+    """The MI355X link recipe: xGMI inside a node of eight GPUs, the NIC between nodes. With
+    large activations on a two-node pipeline the slower node-crossing link queues transfers."""
+    m = I.xgmi_link_matrix(16, 32 << 20)
+    assert (np.diag(m) == 0).all() and (m == m.T).all()
+    assert m[0, 1] == I.link_cost_ns(32 << 20, 5_000, 153) and m[0, 8] == I.link_cost_ns(
+        32 << 20, 20_000, 50)
+    assert m[3, 7] < m[7, 8]
+    P, M = 16, 16
+    recs = I.pack_records(P, 1, 0, [I.POLICY["1F1B"]], [1], [np.arange(1, P)], [np.arange(P)])
+    prob = R.problem(P, P, 1, M, recs.shape[1], 0)
+    costs = np.full((P, 3), 1_000_000, np.int64)
+    link = I.xgmi_link_matrix(P, 1 << 30)
+    plain, serial = R.sim_batch(prob, costs, link, recs)[0][0], \
+        R.sim_batch_serial(prob, costs, link, recs)[0][0]
+    assert serial > plain
