@@ -610,7 +610,7 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
 static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                         const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                         const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos,
-                        int64_t* comm, int serial) {
+                        int64_t* comm, int serial, int64_t* bounds) {
   int P = pr->P, S = c->S, split;
   resolve(pr, c, &split);
   int64_t F[64], B[64], W[64];
@@ -629,9 +629,21 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
     }
   }
   ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link, serial};
-  int64_t* start =
-      (mem || comm) ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M) : NULL;
+  int64_t* start = (mem || comm || bounds)
+                       ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M)
+                       : NULL;
   int rc = simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
+  if (bounds && rc == SIM_OK) {
+    /* per device: start of its first op, end of its last op (0, 0 for an empty queue) */
+    for (int d = 0; d < P; ++d) {
+      bounds[2 * d] = bounds[2 * d + 1] = 0;
+      if (qlen[d] > 0) {
+        const ref_sop a = sq[qoff[d]], z = sq[qoff[d] + qlen[d] - 1];
+        bounds[2 * d] = start[node_id(S, pr->M, a.kind, a.s, a.m)];
+        bounds[2 * d + 1] = start[node_id(S, pr->M, z.kind, z.s, z.m)] + op_dur(&g, z.kind, z.s);
+      }
+    }
+  }
   if (comm && rc == SIM_OK) {
     for (int k = 0; k < 4; ++k) comm[k] = 0;
     comm_overlap(&g, sq, qoff, qlen, start, comm);
@@ -652,13 +664,13 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
 static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                       const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                       const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos) {
-  return eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, ppos, NULL, 0);
+  return eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, ppos, NULL, 0, NULL);
 }
 
 /* Full evaluation of one candidate record: makespan + bubbles, or sentinels. */
 static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                         const int64_t* link, const uint8_t* rec, int64_t* ms, int64_t* bub,
-                        int64_t* peak, int64_t* comm, int serial) {
+                        int64_t* peak, int64_t* comm, int serial, int64_t* bounds) {
   ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
   decode(pr, rec, c);
   int P = pr->P;
@@ -674,7 +686,8 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
       sentinel = REF_INVALID;
     } else {
       int rc =
-          eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm, serial);
+          eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm, serial,
+                       bounds);
       if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
       else if (rc != SIM_OK) sentinel = REF_INVALID;
     }
@@ -687,6 +700,8 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
       for (int d = 0; d < P; ++d) peak[d] = sentinel;
     if (comm)
       for (int k = 0; k < 4; ++k) comm[k] = sentinel;
+    if (bounds)
+      for (int k = 0; k < 2 * P; ++k) bounds[k] = sentinel;
   }
   free(c);
 }
@@ -805,6 +820,7 @@ typedef struct {
   int64_t* out_peak;
   int64_t* out_comm;
   int serial;
+  int64_t* out_bounds;
 } batch_job;
 
 static void* batch_worker(void* arg) {
@@ -813,7 +829,8 @@ static void* batch_worker(void* arg) {
     eval_record(j->pr, j->costs, j->mem, j->link, j->cands + (size_t)i * j->pr->cand_stride,
                 j->out_ms + i, j->out_bub + (size_t)i * j->pr->P,
                 j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL,
-                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL, j->serial);
+                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL, j->serial,
+                j->out_bounds ? j->out_bounds + (size_t)i * 2 * j->pr->P : NULL);
   return NULL;
 }
 
@@ -822,7 +839,7 @@ static void* batch_worker(void* arg) {
 static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                      const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
                      int64_t* out_bub, int64_t* out_peak, int64_t* out_comm, int serial,
-                     int nthreads) {
+                     int64_t* out_bounds, int nthreads) {
   if (!check_problem(pr) || n < 0 || (n > 0 && (!costs || !link || !cands || !out_ms || !out_bub)))
     return REF_EINVAL;
   if ((mem == NULL) != (out_peak == NULL)) return REF_EINVAL;
@@ -833,7 +850,8 @@ static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t*
   batch_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
     jobs[t] = (batch_job){pr,     costs,  mem,     link,    cands, n * t / nthreads,
-                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm, serial};
+                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm, serial,
+                          out_bounds};
     if (nthreads == 1) batch_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, batch_worker, &jobs[t]);
   }
@@ -845,20 +863,23 @@ static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t*
 int oracle_sim_batch_mem(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                          const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
                          int64_t* out_bub, int64_t* out_peak, int nthreads) {
-  return run_batch(pr, costs, mem, link, cands, n, out_ms, out_bub, out_peak, NULL, 0, nthreads);
+  return run_batch(pr, costs, mem, link, cands, n, out_ms, out_bub, out_peak, NULL, 0, NULL,
+                   nthreads);
 }
 
 int oracle_sim_batch(const ref_problem* pr, const int64_t* costs, const int64_t* link,
                      const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                      int nthreads) {
-  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 0, nthreads);
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 0, NULL,
+                   nthreads);
 }
 
 /* Evaluation with serialised links (see simulate). */
 int oracle_sim_batch_serial(const ref_problem* pr, const int64_t* costs, const int64_t* link,
                             const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                             int nthreads) {
-  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 1, nthreads);
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 1, NULL,
+                   nthreads);
 }
 
 /* Evaluation plus communication accounting: out_comm[n][4] = {comm nodes, overlappable nodes,
@@ -867,7 +888,18 @@ int oracle_sim_batch_comm(const ref_problem* pr, const int64_t* costs, const int
                           const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                           int64_t* out_comm, int nthreads) {
   if (n > 0 && !out_comm) return REF_EINVAL;
-  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, out_comm, 0,
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, out_comm, 0, NULL,
+                   nthreads);
+}
+
+/* Evaluation plus each device's first start and last finish: out_bounds[n][P][2] (sentinels for
+ * deadlocked / invalid candidates). Leading idle fs_d and trailing idle makespan - lf_d are the
+ * device's boundary bubble; the rest of its bubble lies between its ops. */
+int oracle_sim_batch_bounds(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                            const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                            int64_t* out_bounds, int nthreads) {
+  if (n > 0 && !out_bounds) return REF_EINVAL;
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 0, out_bounds,
                    nthreads);
 }
 

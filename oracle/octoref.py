@@ -38,6 +38,9 @@ def lib():
         L.oracle_sim_batch_serial.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                               ctypes.c_int64, p, p, ctypes.c_int]
         L.oracle_sim_batch_serial.restype = ctypes.c_int
+        L.oracle_sim_batch_bounds.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
+                                              ctypes.c_int64, p, p, p, ctypes.c_int]
+        L.oracle_sim_batch_bounds.restype = ctypes.c_int
         L.oracle_sim_batch_comm.argtypes = [ctypes.POINTER(RefProblem), p, p, p, ctypes.c_int64,
                                             p, p, p, ctypes.c_int]
         L.oracle_sim_batch_comm.restype = ctypes.c_int
@@ -118,6 +121,23 @@ def sim_batch_serial(prob, costs, link, cands, nthreads=1):
     if rc != 0:
         raise ValueError(f"oracle_sim_batch_serial rejected the arguments (rc={rc})")
     return ms, bub
+
+
+def sim_batch_bounds(prob, costs, link, cands, nthreads=1):
+    """Evaluate candidate records plus each device's first start and last finish. Returns
+    (makespan[n], bubble[n, P], bounds[n, P, 2])."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    bounds = np.zeros((n, prob.P, 2), dtype=np.int64)
+    rc = lib().oracle_sim_batch_bounds(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(cands),
+                                       n, _ptr(ms), _ptr(bub), _ptr(bounds), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch_bounds rejected the arguments (rc={rc})")
+    return ms, bub, bounds
 
 
 def sim_batch_comm(prob, costs, link, cands, nthreads=1):
