@@ -128,6 +128,20 @@ int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        void* stream);
 
 /*
+ * octo_sim_batch_bounds — octo_sim_batch plus, per device, the start of its first op and the
+ * end of its last op: its leading idle (first start) and trailing idle (makespan - last finish)
+ * are the boundary bubble that §6's Algorithm 1 tells apart from the residual bubble between
+ * its ops.
+ *   out_bounds  int64 [n][P][2] {first start, last finish}; OCTO_MS_DEADLOCK / OCTO_MS_INVALID
+ *               in every entry like the makespan.
+ * Other arguments, results and status as octo_sim_batch (out_bounds non-NULL).
+ */
+int octo_sim_batch_bounds(const octo_problem* prob, const int64_t* layer_costs,
+                          const int64_t* link, const void* candidates, int64_t n,
+                          int64_t* out_makespan, int64_t* out_bubble, int64_t* out_bounds,
+                          void* stream);
+
+/*
  * octo_sim_batch_comm — octo_sim_batch plus communication accounting (§5: send and receive
  * nodes of the cross-device dependencies; the simulator marks a node overlappable when it can
  * run beside a computation and records the overlap time; §7's communication statistics). Every

@@ -47,6 +47,7 @@ struct SimArgs {
   const int64_t* pre_mem;  // [(L+1)][2] prefix sums of layer memory (memory-model calls)
   int64_t* out_peak;       // [n][P] peak bytes per device (memory-model calls)
   int64_t* out_comm;       // [n][4] communication tally (communication-accounting calls)
+  int64_t* out_bound;      // [n][P][2] first start, last finish per device (bounds calls)
   const int64_t* link;   // [P][P]
   const uint8_t* cands;
   int64_t n;
@@ -183,11 +184,17 @@ __device__ __forceinline__ CommTally group_tally(CommTally x, int G) {
 template <int X>
 __device__ __forceinline__ void put_results(const SimArgs& a, int64_t cand, int d, bool dead,
                                             int64_t ms, int64_t busy, int64_t stat, int64_t peak,
-                                            const CommTally& tot) {
+                                            const CommTally& tot, int64_t fs = 0,
+                                            int64_t lf = 0) {
   const int P = a.pr.P;
   if (d == 0) a.out_ms[cand] = dead ? OCTO_MS_DEADLOCK : ms;
   a.out_bub[cand * P + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
   if constexpr (X == XM) a.out_peak[cand * P + d] = dead ? OCTO_MS_DEADLOCK : stat + peak;
+  if constexpr (X == XB) {
+    // an empty queue (no op ran) has neither: 0, 0
+    a.out_bound[(cand * P + d) * 2] = dead ? OCTO_MS_DEADLOCK : fs < 0 ? 0 : fs;
+    a.out_bound[(cand * P + d) * 2 + 1] = dead ? OCTO_MS_DEADLOCK : lf;
+  }
   if constexpr (X == XC) {
     if (d == 0) {
       int64_t* o = a.out_comm + cand * 4;
@@ -240,6 +247,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   L.nops = 0;
   L.mem = L.peak = 0;
   L.cm.reset();
+  L.fs = -1;
   if constexpr (X == XS)
     for (int i = 0; i < 16; ++i) L.lf[i] = 0;
   int64_t busy = 0, stat = 0;
@@ -293,7 +301,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
       // times beyond the 40-bit slots: recompute this candidate with 64-bit slots
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
     } else {
-      put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot);
+      put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot, L.fs, L.clock);
     }
   }
 }
@@ -378,7 +386,9 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   int64_t clock = 0, mem = 0, peak = 0;
   CommTally cm;
   cm.reset();
-  relax_tab<X>(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead, mem, peak, cm);
+  int64_t fs = -1;
+  relax_tab<X>(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead, mem, peak, cm,
+               fs);
 
   const int64_t ms = group_max(clock, G);
   CommTally tot = cm;
@@ -387,7 +397,7 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
     if (wide || ms >= Table40::LIMIT) {
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
     } else {
-      put_results<X>(a, cand, d, dead, ms, busy, stat, peak, tot);
+      put_results<X>(a, cand, d, dead, ms, busy, stat, peak, tot, fs, clock);
     }
   }
 }
@@ -554,6 +564,8 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
         for (int d = 0; d < a.pr.P; ++d) a.out_peak[i * a.pr.P + d] = OCTO_MS_INVALID;
       if (a.out_comm)
         for (int k = 0; k < 4; ++k) a.out_comm[i * 4 + k] = OCTO_MS_INVALID;
+      if (a.out_bound)
+        for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
     } else {
       bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
     }
@@ -706,6 +718,7 @@ struct AfabRow {
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) r[m] = 0;
   }
+  __device__ __forceinline__ int64_t first() const { return r[0]; }
   __device__ __forceinline__ int64_t sweep(int, int64_t f, int64_t w, int64_t dur) {
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
@@ -753,6 +766,7 @@ struct AfabRow<0> {
   __device__ __forceinline__ void clear(int M) {
     for (int m = 0; m < M; ++m) row[m * stride] = 0;
   }
+  __device__ __forceinline__ int64_t first() const { return row[0]; }
   __device__ __forceinline__ int64_t sweep(int M, int64_t f, int64_t w, int64_t dur) {
     return sweep_row(row, stride, M, f, w, dur);
   }
@@ -804,6 +818,7 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   int64_t* cps = bsy + (size_t)P * lanes;  // XC: last op start cps[d * lanes], then
   int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
   int64_t* lfr = bsy + (size_t)P * lanes;  // XS: link free time after row t, lfr[t * lanes]
+  int64_t* bfs = bsy + (size_t)P * lanes;  // XB: first start bfs[d * lanes] (-1 before)
   for (;;) {
     int ch = 0;
     if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
@@ -824,6 +839,7 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       clk[d * lanes] = 0, bsy[d * lanes] = 0;
       if constexpr (MEM) pk[d * lanes] = 0;
       if constexpr (X == XC) cps[d * lanes] = 0, cpe[d * lanes] = -1;
+      if constexpr (X == XB) bfs[d * lanes] = -1;
     }
     CommTally acc;
     acc.reset();
@@ -847,6 +863,13 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       const int q = fwd ? st - 1 : st + 1;
       const int dq = q >= 0 && q < S && t != S ? dev[q] : d;
       const int64_t w = (fwd && st == 0) ? AFAB_NO_INPUT : dq != d ? a.link[dq * P + d] : 0;
+      if constexpr (X == XB) {
+        // the device's first op is micro-batch 0 of its first row
+        if (bfs[d * lanes] < 0) {
+          const int64_t y = row.first() + w;
+          bfs[d * lanes] = y > clk[d * lanes] ? y : clk[d * lanes];
+        }
+      }
       if constexpr (X == XS) {
         const int o = fwd ? st + 1 : st - 1;
         const int dout = o >= 0 && o < S ? dev[o] : d;
@@ -889,6 +912,11 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       int64_t* oc = a.out_comm + cand * 4;
       oc[0] = acc.n, oc[1] = acc.nov, oc[2] = acc.t, oc[3] = acc.tov;
     }
+    if constexpr (X == XB)
+      for (int d = 0; d < P; ++d) {
+        a.out_bound[(cand * P + d) * 2] = bfs[d * lanes] < 0 ? 0 : bfs[d * lanes];
+        a.out_bound[(cand * P + d) * 2 + 1] = clk[d * lanes];
+      }
   }
 }
 
@@ -984,6 +1012,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       Lane L;
       L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
       L.cm.reset();
+      L.fs = -1;
       if constexpr (X == XS)
         for (int i = 0; i < 16; ++i) L.lf[i] = 0;
       if (mine) {
@@ -1012,7 +1041,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       const int64_t ms = group_max(L.clock, G);
       CommTally tot = L.cm;
       if constexpr (X == XC) tot = group_tally(L.cm, G);
-      if (mine) put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot);
+      if (mine) put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot, L.fs, L.clock);
     }
   }
 }
@@ -1802,6 +1831,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.pre_mem = peak ? reinterpret_cast<const int64_t*>(base + l.pre_mem) : nullptr;
   a.out_peak = peak;
   a.out_comm = nullptr;
+  a.out_bound = nullptr;
   a.link = link;
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
@@ -1848,8 +1878,9 @@ uint64_t bins_of(int v_lo, int v_hi, bool afab) {
 // ring go to the 64-bit path.
 template <int VC, int X>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
-               int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm, int s_cap,
-               int ring_want, uint64_t mask, int work, hipStream_t stream) {
+               int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm,
+               int64_t* bound, int s_cap, int ring_want, uint64_t mask, int work,
+               hipStream_t stream) {
   const Ring ring = make_ring(prob->M, ring_want);
   // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS and need tables
   // encoded for exactly this geometry
@@ -1866,6 +1897,7 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
   if (pl.CPW < 1) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, pl, su, link, cands, n, ms, bub, peak);
   a.out_comm = comm;
+  a.out_bound = bound;
   if (tab) a.qtab = static_cast<const uint32_t*>(su.ws->qt);
   a.bin_mask = mask, a.work = work;
   a.ring = ring.R;
@@ -1887,11 +1919,11 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
 template <int X>
 int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
                 int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm,
-                hipStream_t stream) {
+                int64_t* bound, hipStream_t stream) {
   // rows of exactly 32 or 64 micro-batches live in registers; other lengths, and the rows of
   // the communication variant (whose unrolled sweep would not fit the register file), in LDS
   const int mmax = X == XC ? 0 : prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
-  const int words = X == XM ? 3 : X == XC ? 4 : 2;  // per device
+  const int words = (X == XM || X == XB) ? 3 : X == XC ? 4 : 2;  // per device
   const size_t per_lane =
       (size_t)((mmax ? 0 : prob->M) + words * prob->P + (X == XS ? 2 * prob->P * prob->v_max : 0)) *
       8;
@@ -1900,6 +1932,7 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub, peak);
   a.out_comm = comm;
+  a.out_bound = bound;
   a.bin_mask = bins_of(1, prob->v_max, true);
   a.work = CTL_WORK + 3;
   int grid = 0;
@@ -1951,30 +1984,32 @@ int record_mark(int i, hipStream_t stream) {
   return OCTO_OK;
 }
 
+// Evaluation outputs besides makespan and bubbles (null where the kind has none).
+struct Extra {
+  int64_t* peak = nullptr;   // XM [n][P]
+  int64_t* comm = nullptr;   // XC [n][4]
+  int64_t* bound = nullptr;  // XB [n][P][2]
+};
+
 // The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM),
-// octo_sim_batch_comm (XC) and octo_sim_batch_serial (XS: generated queues, not tables).
+// octo_sim_batch_comm (XC), octo_sim_batch_serial (XS: generated queues, not tables) and
+// octo_sim_batch_bounds (XB). The caller has checked the arguments and holds g_mu.
 template <int X>
-int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
-                   const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
-                   int64_t* out_bubble, int64_t* out_peak, int64_t* out_comm, hipStream_t stream) {
+int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
+                  const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
+                  int64_t* out_bubble, const Extra& ex, hipStream_t stream) {
   constexpr bool MEM = X == XM;
-  int rc = check_problem(prob);
-  if (rc) return rc;
-  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
   if (n == 0) return OCTO_OK;
-  if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
-  if (MEM && (!layer_mem || !out_peak)) return OCTO_EINVAL;
-  if (X == XC && !out_comm) return OCTO_EINVAL;
-  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
-  std::lock_guard<std::mutex> lock(g_mu);
   Setup su;
-  rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, n, &su);
+  int rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, n, &su);
   if (rc) return rc;
   char* base = static_cast<char*>(su.ws->base);
-  int64_t* pk = MEM ? out_peak : nullptr;
-  int64_t* cm = X == XC ? out_comm : nullptr;
+  int64_t* pk = MEM ? ex.peak : nullptr;
+  int64_t* cm = X == XC ? ex.comm : nullptr;
+  int64_t* bd = X == XB ? ex.bound : nullptr;
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble, pk);
   a.out_comm = cm;
+  a.out_bound = bd;
   const int tb = CLS_THREADS;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
@@ -1993,24 +2028,23 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
   if (X != XS && (rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream))) return rc;
-  auto launch_bins = [&](int lo, int hi) { return bins_of(lo, hi, false); };
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&
-      (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                             2 * P, 2 * P, launch_bins(2, 2), CTL_WORK + 1, stream)))
+      (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
+                             2 * P, 2 * P, bins_of(2, 2, false), CTL_WORK + 1, stream)))
     return rc;
   if ((rc = record_mark(1, stream))) return rc;
-  if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, P, P,
-                               launch_bins(1, 1), CTL_WORK + 0, stream)))
+  if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
+                             P, P, bins_of(1, 1, false), CTL_WORK + 0, stream)))
     return rc;
   if ((rc = record_mark(2, stream))) return rc;
   if (prob->v_max >= 3 &&
-      (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                             P * prob->v_max, M, launch_bins(3, 8), CTL_WORK + 2, stream)))
+      (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
+                             P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+  if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
                            stream)))
     return rc;
   if ((rc = record_mark(4, stream))) return rc;
@@ -2022,6 +2056,25 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
                        stream, a);
   if ((rc = launch_ok())) return rc;
   return record_mark(5, stream);
+}
+
+// Argument checks and locking around sim_batch_run.
+template <int X>
+int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
+                   const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
+                   int64_t* out_bubble, const Extra& ex, hipStream_t stream) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
+  if (n == 0) return OCTO_OK;
+  if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
+  if (X == XM && (!layer_mem || !ex.peak)) return OCTO_EINVAL;
+  if (X == XC && !ex.comm) return OCTO_EINVAL;
+  if (X == XB && !ex.bound) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
+  std::lock_guard<std::mutex> lock(g_mu);
+  return sim_batch_run<X>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
+                          out_bubble, ex, stream);
 }
 
 // The local-search step behind octo_tune_step (MEM = false) and octo_tune_step_mem.
@@ -2090,30 +2143,44 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
                    const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
                    void* stream) {
   return sim_batch_impl<XP>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
-                            out_bubble, nullptr, nullptr, static_cast<hipStream_t>(stream));
+                            out_bubble, Extra{}, static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        const int64_t* layer_mem, const int64_t* link, const void* candidates,
                        int64_t n, int64_t* out_makespan, int64_t* out_bubble, int64_t* out_peak,
                        void* stream) {
+  Extra ex;
+  ex.peak = out_peak;
   return sim_batch_impl<XM>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
-                            out_bubble, out_peak, nullptr, static_cast<hipStream_t>(stream));
+                            out_bubble, ex, static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_serial(const octo_problem* prob, const int64_t* layer_costs,
                           const int64_t* link, const void* candidates, int64_t n,
                           int64_t* out_makespan, int64_t* out_bubble, void* stream) {
   return sim_batch_impl<XS>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
-                            out_bubble, nullptr, nullptr, static_cast<hipStream_t>(stream));
+                            out_bubble, Extra{}, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_bounds(const octo_problem* prob, const int64_t* layer_costs,
+                          const int64_t* link, const void* candidates, int64_t n,
+                          int64_t* out_makespan, int64_t* out_bubble, int64_t* out_bounds,
+                          void* stream) {
+  Extra ex;
+  ex.bound = out_bounds;
+  return sim_batch_impl<XB>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                            out_bubble, ex, static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_comm(const octo_problem* prob, const int64_t* layer_costs,
                         const int64_t* link, const void* candidates, int64_t n,
                         int64_t* out_makespan, int64_t* out_bubble, int64_t* out_comm,
                         void* stream) {
+  Extra ex;
+  ex.comm = out_comm;
   return sim_batch_impl<XC>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
-                            out_bubble, nullptr, out_comm, static_cast<hipStream_t>(stream));
+                            out_bubble, ex, static_cast<hipStream_t>(stream));
 }
 
 int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,

@@ -39,8 +39,9 @@ constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
 
 // What an evaluation computes besides the plain times: the memory model (activation bytes held
 // per device, §5 memory nodes), communication nodes and their overlap (§5), or times with
-// serialised links (a directed link carries one transfer at a time, in issue order).
-constexpr int XP = 0, XM = 1, XC = 2, XS = 3;
+// serialised links (a directed link carries one transfer at a time, in issue order), or each
+// device's first start and last finish (its leading and trailing idle).
+constexpr int XP = 0, XM = 1, XC = 2, XS = 3, XB = 4;
 // Weight of a weight-gradient op's read under serialised links: its B is on its own device and
 // earlier in its queue, so only the readiness bit matters, not the (possibly delayed) slot time.
 constexpr int64_t W_NO_TIME = -((int64_t)1 << 50);
@@ -190,6 +191,7 @@ struct Lane : Desc {
   CommTally cm;       // communication variants
   int64_t lf[16];     // serialised links: when the link to device dst is free, per stream
                       // (forward outputs of chunk k at k, backward outputs at VMAX + k)
+  int64_t fs;         // start of the device's first op (-1 before it), bounds variants
 };
 
 template <int VMAX, typename T>
@@ -287,6 +289,7 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
     if (rec && ok)
       rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)gen.kind << 12) | (uint32_t)gen.m;
     if constexpr (X == XC) L.cm.op(ok, L.cx, tin, L.w, L.clock, st, fin, L.cout);
+    if constexpr (X == XB) L.fs = (ok && L.fs < 0) ? st : L.fs;
     L.clock = ok ? fin : L.clock;
     if constexpr (X == XM) {
       L.mem = ok ? L.mem + L.dm : L.mem;
@@ -364,7 +367,8 @@ template <int X>
 __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint32_t row, int Rl,
                                           const uint8_t* strm, int64_t& clock, const Table40& T,
                                           int G, uint64_t gbit, uint64_t lsb, bool& dead,
-                                          int64_t& mem, int64_t& peak, CommTally& cm) {
+                                          int64_t& mem, int64_t& peak, CommTally& cm,
+                                          int64_t& fs) {
   uint32_t cur = qt[row], nxt = qt[row + 1u];
   uint32_t qa = row + 2u;  // entry after next
   for (;;) {
@@ -389,6 +393,7 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
       const uint2 cc = *reinterpret_cast<const uint2*>(strm + soff + 8);
       cm.op(ok, (int)cc.y, tin, (int64_t)wd.x, clock, st, fin, (int64_t)cc.x);
     }
+    if constexpr (X == XB) fs = (ok && fs < 0) ? st : fs;
     clock = ok ? fin : clock;
     if constexpr (X == XM) {
       const int64_t dm = *reinterpret_cast<const int64_t*>(strm + soff + 8);
