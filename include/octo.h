@@ -244,6 +244,47 @@ int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
                        uint64_t seed, int32_t step, void* stream);
 
 /*
+ * octo_alg1_tune — Algorithm 1 of §6 ("Iterative and Bubble-Aware Tuning"): one independent
+ * search per record, all records advanced together for `iters` iterations (the paper's time
+ * budget, counted in iterations). An iteration of a record's search:
+ *   1. From its current evaluation (as octo_sim_batch_bounds): bubble gap
+ *      Δb = max_d bubble[d] - min_d bubble[d]; boundary bubble b_bd = Σ_d (first start[d] +
+ *      makespan - last finish[d]); residual bubble b_res = Σ_d bubble[d] - b_bd; and
+ *      t_layer = M * min over layers of (F + B + W).
+ *   2. Phase: partitioning if Δb > t_layer, else placement if b_bd > b_res, else scheduling. A
+ *      phase whose last search found nothing better stays exhausted until a move is kept; an
+ *      exhausted pick falls to the first open phase in that order; with none open (or when the
+ *      record is invalid or deadlocks) the search has ended and later iterations skip it.
+ *   3. The phase's neighbourhood, in this order (the order breaks ties):
+ *      partitioning — one layer migrates from a stage a of the most loaded device (largest
+ *        busy time; lowest index on ties) to a stage b of the least loaded one, the stages in
+ *        between passing one layer along: for a, then b, ascending, a having >= 2 layers;
+ *      placement — the device with the largest bubble exchanges one of its stages with one of
+ *        another device's (other device, its stage, the other's stage, ascending); then, if
+ *        2v <= v_max and every stage has >= 2 layers, stage dispersion: every stage splits at
+ *        its middle layer (first half floor(size/2) layers), new stage k going to the device
+ *        of old stage k mod S, v doubled, moves cleared;
+ *      scheduling — each other policy, moves cleared; then, if n_pert < max_pert, every
+ *        adjacent swap {d, i, i+1} of the device d with the largest residual bubble (bubble
+ *        minus leading and trailing idle), appended as a move.
+ *      Reserved boundary and placement bytes read as 0 in every neighbour; other bytes copy.
+ *   4. The neighbour with the smallest makespan among those that neither deadlock nor are
+ *      invalid (the first on ties) replaces the record iff its makespan is strictly smaller;
+ *      every phase is open again. Otherwise the phase is exhausted.
+ *   records       n records (prob->cand_stride <= 1664, 16-byte aligned) updated in place to
+ *                 each search's final record.
+ *   out_makespan  int64 [n], out_bubble int64 [n][P]: the final records' evaluation.
+ *   out_stats     int64 [n][4]: moves kept in the partitioning, placement and scheduling
+ *                 phases, and the iterations in which a phase was searched.
+ * The library evaluates each iteration's neighbours as one batch in its workspace, at most
+ * n * max(v_max^2, (P-1) v_max^2 + 1, 3 v_max M + 2) records (OCTO_EINVAL above 2^31 - 1;
+ * OCTO_ENOMEM if it cannot be allocated). Returns OCTO_OK or a negative status.
+ */
+int octo_alg1_tune(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   void* records, int64_t n, int32_t iters, int64_t* out_makespan,
+                   int64_t* out_bubble, int64_t* out_stats, void* stream);
+
+/*
  * Measurement hook. events[0..n_events-1] are hipEvent_t handles (n_events <= 8; entries may be
  * NULL). Each later octo_sim_batch call records them on its stream at fixed boundaries around
  * its simulation kernels: events[0] before the v = 2 kernel (1F1B, I1F1B, ZB queues), [1]

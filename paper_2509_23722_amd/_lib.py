@@ -55,6 +55,8 @@ def lib():
                                          i32, vp]
         L.octo_advance_w.argtypes = [pp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
         L.octo_tune_step.restype = ctypes.c_int
+        L.octo_alg1_tune.argtypes = [pp, vp, vp, vp, i64, i32, vp, vp, vp, vp]
+        L.octo_alg1_tune.restype = ctypes.c_int
         L.octo_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), i32]
         L.octo_profile_events.restype = ctypes.c_int
         L.octo_strerror.argtypes = [ctypes.c_int]
@@ -258,6 +260,29 @@ def advance_w(prob, layer_costs, layer_mem, capacity, link, candidates, out_cand
         _dev_ptr(out_peak, torch.int64, "out_peak"), _stream(candidates, stream))
     _check(rc, "octo_advance_w")
     return out_candidates, out_makespan, out_bubble, out_peak
+
+
+def alg1_tune(prob, layer_costs, link, records, iters, out_makespan=None, out_bubble=None,
+              out_stats=None, stream=None):
+    """octo_alg1_tune: Algorithm 1 on every record (uint8 [n, stride], updated in place) for
+    `iters` iterations. Returns (makespan [n], bubble [n, P], stats [n, 4] = kept moves per
+    phase (partitioning, placement, scheduling) and iterations that searched)."""
+    n = records.shape[0]
+    dev = records.device
+    if out_makespan is None:
+        out_makespan = torch.empty(n, dtype=torch.int64, device=dev)
+    if out_bubble is None:
+        out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    if out_stats is None:
+        out_stats = torch.empty((n, 4), dtype=torch.int64, device=dev)
+    rc = lib().octo_alg1_tune(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(records, torch.uint8, "records"), n,
+        int(iters), _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
+        _dev_ptr(out_stats, torch.int64, "out_stats"), _stream(records, stream))
+    _check(rc, "octo_alg1_tune")
+    return out_makespan, out_bubble, out_stats
 
 
 def profile_events(events):

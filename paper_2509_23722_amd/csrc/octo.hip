@@ -51,6 +51,7 @@ struct SimArgs {
   const int64_t* link;   // [P][P]
   const uint8_t* cands;
   int64_t n;
+  const int32_t* n_live;  // nullable: only the first *n_live of the n records are evaluated
   int64_t* out_ms;
   int64_t* out_bub;
   int32_t* ctl;
@@ -534,6 +535,13 @@ __device__ __forceinline__ int wave_hist_add(int* hist, int key, bool active) {
   return mine;
 }
 
+// Records to evaluate: a.n, or fewer when a count on the device says so.
+__device__ __forceinline__ int64_t live_count(const SimArgs& a) {
+  if (!a.n_live) return a.n;
+  const int64_t l = *a.n_live;
+  return l < a.n ? l : a.n;
+}
+
 // One thread per candidate, blocks of CLS_THREADS. The records' heads (first hb bytes: header,
 // boundaries, placement) are staged through LDS with 16-byte coalesced loads.
 constexpr int CLS_THREADS = 256;
@@ -543,7 +551,8 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
   __shared__ int hist[NBINS];
   for (int i = threadIdx.x; i < NBINS; i += blockDim.x) hist[i] = 0;
   const int64_t first = (int64_t)blockIdx.x * CLS_THREADS;
-  const int cnt = (int)(a.n - first < CLS_THREADS ? a.n - first : CLS_THREADS);
+  const int64_t n = live_count(a);
+  const int cnt = first >= n ? 0 : (int)(n - first < CLS_THREADS ? n - first : CLS_THREADS);
   const int q = hb / 16, stride16 = a.pr.stride / 16;
   const uint4* src = reinterpret_cast<const uint4*>(a.cands + first * a.pr.stride);
   uint4* dst = reinterpret_cast<uint4*>(heads);
@@ -596,7 +605,7 @@ __global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x) hist[b] = 0;
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int bin = i < a.n ? bins[i] : BIN_NONE;
+  const int bin = i < live_count(a) ? bins[i] : BIN_NONE;
   const int local = wave_hist_add(hist, bin, bin != BIN_NONE);
   __syncthreads();
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
@@ -1458,6 +1467,314 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   }
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// Algorithm 1 of §6 (iterative bubble-aware tuning), one search per record, all records in
+// lockstep iterations. Per iteration: k_alg1_expand picks each record's phase from its bubble
+// breakdown and writes that phase's neighbourhood into one compacted batch; the batch is
+// evaluated like any other (bounds variant); k_alg1_select keeps each record's best neighbour
+// when it shortens the makespan. One wave per record in both kernels.
+// ---------------------------------------------------------------------------------------------
+
+// Search state per record (int32 words): the phase searched this iteration, flags (bits 0..2:
+// phases whose last search found nothing better; A1_OVER: the search has ended), the first
+// neighbour's position in the batch and the neighbour count.
+constexpr int A1_PHASE = 0, A1_FLAGS = 1, A1_BASE = 2, A1_CNT = 3, A1_WORDS = 4;
+constexpr int A1_OVER = 8;
+constexpr int A1_REC_MAX = 1664;  // largest record stride (S_max = 64, 255 moves)
+
+struct A1Args {
+  Problem pr;
+  const int64_t* costs;    // [L][3]
+  uint8_t* recs;           // [n] current records, updated in place
+  int64_t n;
+  int64_t* ms;             // [n] current makespan
+  int64_t* bub;            // [n][P] current bubbles
+  int64_t* bnd;            // [n][P][2] current first start, last finish
+  int32_t* st;             // [n][A1_WORDS]
+  int64_t* stats;          // [n][4] kept moves per phase, iterations that searched
+  uint8_t* nb_rec;         // neighbour records of this iteration, compacted
+  const int64_t* nb_ms;    // [batch] their makespan
+  const int64_t* nb_bub;   // [batch][P]
+  const int64_t* nb_bnd;   // [batch][P][2]
+  int32_t* total;          // neighbours written this iteration (atomic cursor)
+};
+
+__device__ __forceinline__ int64_t wave_sum64(int64_t x) {
+  for (int o = WAVE >> 1; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+__device__ __forceinline__ int64_t wave_max64(int64_t x) {
+  for (int o = WAVE >> 1; o > 0; o >>= 1) {
+    const int64_t y = __shfl_xor(x, o);
+    x = y > x ? y : x;
+  }
+  return x;
+}
+__device__ __forceinline__ int64_t wave_min64(int64_t x) {
+  for (int o = WAVE >> 1; o > 0; o >>= 1) {
+    const int64_t y = __shfl_xor(x, o);
+    x = y < x ? y : x;
+  }
+  return x;
+}
+// Lane of the largest x, the lowest such lane on ties.
+__device__ __forceinline__ int wave_argmax64(int64_t x) {
+  int i = lane_id();
+  for (int o = WAVE >> 1; o > 0; o >>= 1) {
+    const int64_t y = __shfl_xor(x, o);
+    const int j = __shfl_xor(i, o);
+    if (y > x || (y == x && j < i)) x = y, i = j;
+  }
+  return i;
+}
+
+__global__ void k_alg1_init(int32_t* __restrict__ st, int64_t* __restrict__ stats, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    for (int k = 0; k < A1_WORDS; ++k) st[i * A1_WORDS + k] = 0;
+    for (int k = 0; k < 4; ++k) stats[i * 4 + k] = 0;
+  }
+}
+
+// One neighbour as byte edits of the current record: edited spans [lo, hi) and what goes there.
+struct A1Edit {
+  int kind;  // 0 layer migration, 1 stage exchange, 2 stage dispersion, 3 policy, 4 op swap
+  int x, y;  // 0: boundaries x+1..y shift by -1 (x < y) or x+1..y by +1 (swapped: y < x holds
+             //    the lower stage); 1: stages x, y; 3: new policy; 4: device x, position y
+  int lo1, hi1, lo2, hi2;
+};
+
+// Byte p of the neighbour (p inside one of its spans). rec: the current record, reserved bytes
+// cleared; S, v: its stage count and stages per device.
+__device__ __forceinline__ uint32_t a1_byte(const A1Edit& e, const uint8_t* rec, int p, int L,
+                                            int s_max, int S, int v, int po) {
+  auto bnd = [&](int s) -> int { return s == 0 ? 0 : s == S ? L : rec[3 + s]; };
+  switch (e.kind) {
+    case 0:  // boundary b[k] at byte 3 + k
+      return (uint32_t)(rec[p] + e.x);
+    case 1: {
+      const int s = p - 3 - s_max;
+      return rec[3 + s_max + (s == e.x ? e.y : e.x)];
+    }
+    case 2: {
+      if (p == 1) return (uint32_t)(2 * v);
+      if (p == 2) return 0;
+      if (p < 4) return rec[p];
+      if (p < 3 + s_max) {  // new boundary k: stage k/2 split at its middle layer
+        const int k = p - 3;
+        if (k >= 2 * S) return 0;
+        const int s = k >> 1;
+        return (uint32_t)((k & 1) ? bnd(s) + (bnd(s + 1) - bnd(s)) / 2 : bnd(s));
+      }
+      const int s = p - 3 - s_max;  // new stage s on the device of old stage s mod S
+      return s < 2 * S ? rec[3 + s_max + s % S] : 0;
+    }
+    case 3:
+      return p == 0 ? (uint32_t)e.x : p == 2 ? 0u : rec[p];
+    default: {
+      if (p == 2) return (uint32_t)(rec[2] + 1);
+      const int q = p - (po + 6 * rec[2]);  // the appended move {device, from, to}, u16 LE
+      const int val = q < 2 ? e.x : q < 4 ? e.y : e.y + 1;
+      return (uint32_t)((q & 1) ? (val >> 8) & 0xFF : val & 0xFF);
+    }
+  }
+}
+
+// Algorithm 1's branch and the chosen phase's neighbourhood, written to the batch.
+// Neighbourhoods, in order (their order settles ties between equal makespans):
+//  0 partitioning: one layer migrates from a stage a of the most loaded device (largest busy
+//    time) to a stage b of the least loaded one, the stages between passing it on; pairs (a, b)
+//    ascending, a with at least two layers;
+//  1 placement: the device with the largest bubble exchanges one of its stages with one of each
+//    other device's (devices, then its stages, then theirs, ascending); then, when v can double
+//    and every stage has two layers, every stage splits at its middle layer and the 2S stages
+//    go round the old devices (new stage k on the device of old stage k mod S), moves cleared;
+//  2 scheduling: each other policy (moves cleared); then, with a move slot free, each adjacent
+//    swap of the device with the largest bubble between its first and last op, as a move.
+__global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
+  __shared__ __align__(16) uint8_t rec[A1_REC_MAX];
+  __shared__ uint8_t sd[64];     // stages of device d at sd[d v ..], ascending
+  __shared__ uint8_t alist[8];   // partitioning: the loaded device's stages that can give a layer
+  const int lane = lane_id();
+  const int P = a.pr.P, M = a.pr.M, L = a.pr.L, s_max = a.pr.s_max, stride = a.pr.stride;
+  const int po = pert_off(s_max);
+  int64_t tl = INT64_MAX;  // t_layer = M * the smallest layer's F + B + W
+  for (int l = lane; l < L; l += WAVE) {
+    const int64_t c = a.costs[3 * l] + a.costs[3 * l + 1] + a.costs[3 * l + 2];
+    tl = c < tl ? c : tl;
+  }
+  tl = wave_min64(tl) * M;
+  for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
+    int32_t* st = a.st + i * A1_WORDS;
+    const int flags = st[A1_FLAGS];
+    const int64_t ms = a.ms[i];
+    if ((flags & A1_OVER) || ms < 0) {  // ended, or deadlocked / invalid: nothing to search
+      if (lane == 0) st[A1_FLAGS] = flags | A1_OVER, st[A1_CNT] = 0;
+      continue;
+    }
+    const bool dv = lane < P;
+    const int64_t bub = dv ? a.bub[i * P + lane] : 0;
+    const int64_t fs = dv ? a.bnd[(i * P + lane) * 2] : 0;
+    const int64_t lf = dv ? a.bnd[(i * P + lane) * 2 + 1] : 0;
+    const int64_t busy = ms - bub;
+    const int64_t edge = fs + ms - lf;  // leading plus trailing idle: the boundary bubble
+    const int64_t resid = bub - edge;
+    const int64_t delta = wave_max64(dv ? bub : INT64_MIN) - wave_min64(dv ? bub : INT64_MAX);
+    const int64_t b_bd = wave_sum64(dv ? edge : 0);
+    const int64_t b_res = wave_sum64(dv ? bub : 0) - b_bd;
+    const int pref = delta > tl ? 0 : b_bd > b_res ? 1 : 2;
+    const int ex = flags & 7;
+    const int phase = !((ex >> pref) & 1) ? pref : !(ex & 1) ? 0 : !(ex & 2) ? 1 : !(ex & 4) ? 2 : -1;
+    if (phase < 0) {  // every phase exhausted: converged
+      if (lane == 0) st[A1_FLAGS] = flags | A1_OVER, st[A1_CNT] = 0;
+      continue;
+    }
+    const int dmax = wave_argmax64(dv ? busy : INT64_MIN);
+    const int dmin = wave_argmax64(dv ? -busy : INT64_MIN);
+    const int d1 = wave_argmax64(dv ? bub : INT64_MIN);
+    const int dr = wave_argmax64(dv ? resid : INT64_MIN);
+    // the record, reserved boundary and placement bytes cleared (as every neighbour has them)
+    const uint4* src = reinterpret_cast<const uint4*>(a.recs + i * stride);
+    for (int q = lane; q < stride / 16; q += WAVE) reinterpret_cast<uint4*>(rec)[q] = src[q];
+    __syncthreads();
+    const int policy = rec[0], v = rec[1], np = rec[2];
+    const int S = P * v;
+    for (int p = 3 + S + lane; p < 3 + s_max; p += WAVE) rec[p] = 0;
+    for (int p = 3 + s_max + S + lane; p < 3 + 2 * s_max; p += WAVE) rec[p] = 0;
+    if (dv) {
+      int k = 0;
+      for (int s = 0; s < S; ++s)
+        if (rec[3 + s_max + s] == lane) sd[lane * v + k++] = (uint8_t)s;
+    }
+    __syncthreads();
+    auto bnd = [&](int s) -> int { return s == 0 ? 0 : s == S ? L : rec[3 + s]; };
+    int cnt = 0, na = 0;
+    if (phase == 0) {
+      if (dmax != dmin) {
+        for (int k = 0; k < v; ++k) {
+          const int s = sd[dmax * v + k];
+          if (bnd(s + 1) - bnd(s) >= 2) {
+            if (lane == 0) alist[na] = (uint8_t)s;
+            ++na;
+          }
+        }
+        cnt = na * v;
+      }
+    } else if (phase == 1) {
+      const bool thin = lane < S && bnd(lane + 1) - bnd(lane) < 2;
+      const bool disp = 2 * v <= a.pr.v_max && __ballot(thin) == 0;
+      cnt = (P - 1) * v * v + (disp ? 1 : 0);
+    } else {
+      const int qlen = (policy == POL_ZB ? 3 : 2) * v * M;
+      cnt = 3 + (np < a.pr.max_pert ? qlen - 1 : 0);
+    }
+    int base = 0;
+    if (lane == 0) {
+      base = atomicAdd(a.total, cnt);
+      st[A1_PHASE] = phase, st[A1_BASE] = base, st[A1_CNT] = cnt;
+      a.stats[i * 4 + 3] += 1;
+    }
+    base = __shfl(base, 0);
+    __syncthreads();
+    for (int j = lane; j < cnt; j += WAVE) {
+      A1Edit e;
+      e.lo2 = e.hi2 = 0;
+      if (phase == 0) {
+        const int sa = alist[j / v], sb = sd[dmin * v + j % v];
+        e.kind = 0;
+        e.x = sa < sb ? -1 : 1;
+        const int lo = sa < sb ? sa : sb, hi = sa < sb ? sb : sa;
+        e.lo1 = 4 + lo, e.hi1 = 4 + hi;  // boundaries lo+1..hi
+      } else if (phase == 1) {
+        const int vv = v * v;
+        if (j < (P - 1) * vv) {
+          const int k2 = j / vv, r = j - k2 * vv;
+          const int d2 = k2 < d1 ? k2 : k2 + 1;
+          e.kind = 1;
+          e.x = sd[d1 * v + r / v], e.y = sd[d2 * v + r % v];
+          e.lo1 = 3 + s_max + e.x, e.hi1 = e.lo1 + 1;
+          e.lo2 = 3 + s_max + e.y, e.hi2 = e.lo2 + 1;
+        } else {
+          e.kind = 2;
+          e.lo1 = 1, e.hi1 = 3 + 2 * s_max;
+        }
+      } else if (j < 3) {
+        e.kind = 3;
+        e.x = j < policy ? j : j + 1;
+        e.lo1 = 0, e.hi1 = 3;
+      } else {
+        e.kind = 4;
+        e.x = dr, e.y = j - 3;
+        e.lo1 = 2, e.hi1 = 3;
+        e.lo2 = po + 6 * np, e.hi2 = e.lo2 + 6;
+      }
+      uint4* dst = reinterpret_cast<uint4*>(a.nb_rec + (int64_t)(base + j) * stride);
+      for (int q = 0; q < stride / 16; ++q) {
+        uint4 x = reinterpret_cast<const uint4*>(rec)[q];
+        const int p0 = 16 * q;
+        if ((e.lo1 < p0 + 16 && e.hi1 > p0) || (e.lo2 < p0 + 16 && e.hi2 > p0)) {
+          uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+          for (int b = 0; b < 16; ++b) {
+            const int p = p0 + b;
+            if ((p >= e.lo1 && p < e.hi1) || (p >= e.lo2 && p < e.hi2)) {
+              const uint32_t nv = a1_byte(e, rec, p, L, s_max, S, v, po) & 0xFF;
+              w[b >> 2] = (w[b >> 2] & ~(0xFFu << (8 * (b & 3)))) | (nv << (8 * (b & 3)));
+            }
+          }
+          x = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+        dst[q] = x;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Each record's best neighbour — the smallest makespan among those that neither deadlock nor
+// are invalid, the first in neighbourhood order on ties — replaces it iff strictly shorter; the
+// phase is then fresh again for all three phases, else this phase is exhausted.
+__global__ void __launch_bounds__(WAVE) k_alg1_select(A1Args a) {
+  const int lane = lane_id();
+  const int P = a.pr.P, stride = a.pr.stride;
+  for (int64_t i = blockIdx.x; i < a.n; i += gridDim.x) {
+    int32_t* st = a.st + i * A1_WORDS;
+    const int flags = st[A1_FLAGS];
+    if (flags & A1_OVER) continue;
+    const int phase = st[A1_PHASE], base = st[A1_BASE], cnt = st[A1_CNT];
+    int64_t best = INT64_MAX;
+    int bj = INT32_MAX;
+    for (int j = lane; j < cnt; j += WAVE) {
+      const int64_t x = a.nb_ms[base + j];
+      if (x >= 0 && x < best) best = x, bj = j;
+    }
+    for (int o = WAVE >> 1; o > 0; o >>= 1) {
+      const int64_t y = __shfl_xor(best, o);
+      const int k = __shfl_xor(bj, o);
+      if (y < best || (y == best && k < bj)) best = y, bj = k;
+    }
+    if (bj != INT32_MAX && best < a.ms[i]) {
+      const int64_t nb = base + bj;
+      const uint4* src = reinterpret_cast<const uint4*>(a.nb_rec + nb * stride);
+      uint4* dst = reinterpret_cast<uint4*>(a.recs + i * stride);
+      for (int q = lane; q < stride / 16; q += WAVE) dst[q] = src[q];
+      if (lane < P) {
+        a.bub[i * P + lane] = a.nb_bub[nb * P + lane];
+        a.bnd[(i * P + lane) * 2] = a.nb_bnd[(nb * P + lane) * 2];
+        a.bnd[(i * P + lane) * 2 + 1] = a.nb_bnd[(nb * P + lane) * 2 + 1];
+      }
+      if (lane == 0) {
+        a.ms[i] = best;
+        a.stats[i * 4 + phase] += 1;
+        st[A1_FLAGS] = 0;
+      }
+    } else if (lane == 0) {
+      st[A1_FLAGS] = flags | (1 << phase);
+    }
+  }
+}
+
 }  // namespace octo
 
 // =============================================================================================
@@ -1485,6 +1802,9 @@ struct Workspace {
   int qt_P = 0, qt_vmax = 0, qt_M = 0;
   int qt_R[2] = {}, qt_lg[2] = {};  // launch geometry the entries were encoded for, per v
   int64_t qt_inter[2][2] = {}, qt_merge[2] = {}, qt_end = 0;
+  // Algorithm 1: search state and each iteration's neighbour batch
+  void* a1 = nullptr;
+  size_t a1_bytes = 0;
 };
 
 std::mutex g_mu;
@@ -1835,6 +2155,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.link = link;
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
+  a.n_live = nullptr;
   a.out_ms = ms;
   a.out_bub = bub;
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
@@ -1989,6 +2310,7 @@ struct Extra {
   int64_t* peak = nullptr;   // XM [n][P]
   int64_t* comm = nullptr;   // XC [n][4]
   int64_t* bound = nullptr;  // XB [n][P][2]
+  const int32_t* n_live = nullptr;  // device count of the records to evaluate (<= n)
 };
 
 // The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM),
@@ -2010,6 +2332,7 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble, pk);
   a.out_comm = cm;
   a.out_bound = bd;
+  a.n_live = ex.n_live;
   const int tb = CLS_THREADS;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
@@ -2110,6 +2433,95 @@ int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   return prob->v_max <= 2
              ? launch_tune<2, MEM>(t, su.big, su.di.cus, su.mat_grid, n_chains, stream)
              : launch_tune<8, MEM>(t, su.big, su.di.cus, su.mat_grid, n_chains, stream);
+}
+
+
+// Neighbour slots one record can need in one iteration of Algorithm 1 (the largest of the three
+// neighbourhoods over v <= v_max).
+int64_t alg1_slots(const octo_problem* p) {
+  const int64_t v = p->v_max;
+  return std::max({v * v, (int64_t)(p->P - 1) * v * v + 1, 3 * v * p->M + 2});
+}
+
+// Algorithm 1 behind octo_alg1_tune: state and batch in the workspace's a1 buffer, iterations
+// enqueued back to back on the stream (no host synchronisation).
+int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+              void* records, int64_t n, int32_t iters, int64_t* out_makespan, int64_t* out_bubble,
+              int64_t* out_stats, hipStream_t stream) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n < 0 || iters < 0) return OCTO_EINVAL;
+  if (n == 0) return OCTO_OK;
+  const int64_t slots = alg1_slots(prob);
+  if (n > (int64_t)INT32_MAX / slots || prob->cand_stride > A1_REC_MAX) return OCTO_EINVAL;
+  if (!layer_costs || !link || !records || !out_makespan || !out_bubble || !out_stats)
+    return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(records) & 15) != 0) return OCTO_EINVAL;
+  const int64_t nb = n * slots;
+  std::lock_guard<std::mutex> lock(g_mu);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
+  Workspace& ws = g_ws[std::make_pair(dev, stream)];
+  const int P = prob->P;
+  size_t o = 0;
+  const size_t o_total = o;
+  o = align_up(o + 256, 256);
+  const size_t o_bnd = o;
+  o = align_up(o + (size_t)n * P * 16, 256);
+  const size_t o_st = o;
+  o = align_up(o + (size_t)n * A1_WORDS * 4, 256);
+  const size_t o_rec = o;
+  o = align_up(o + (size_t)nb * prob->cand_stride, 256);
+  const size_t o_ms = o;
+  o = align_up(o + (size_t)nb * 8, 256);
+  const size_t o_bub = o;
+  o = align_up(o + (size_t)nb * P * 8, 256);
+  const size_t o_nbnd = o;
+  o = align_up(o + (size_t)nb * P * 16, 256);
+  if ((rc = ensure_buf(ws.a1, ws.a1_bytes, o, stream))) return rc;
+  char* base = static_cast<char*>(ws.a1);
+  A1Args a;
+  a.pr = Problem{prob->L, prob->P, prob->v_max, prob->M, prob->cand_stride, prob->max_pert,
+                 prob->P * prob->v_max};
+  a.costs = layer_costs;
+  a.recs = static_cast<uint8_t*>(records);
+  a.n = n;
+  a.ms = out_makespan;
+  a.bub = out_bubble;
+  a.bnd = reinterpret_cast<int64_t*>(base + o_bnd);
+  a.st = reinterpret_cast<int32_t*>(base + o_st);
+  a.stats = out_stats;
+  a.nb_rec = reinterpret_cast<uint8_t*>(base + o_rec);
+  a.nb_ms = reinterpret_cast<int64_t*>(base + o_ms);
+  a.nb_bub = reinterpret_cast<int64_t*>(base + o_bub);
+  a.nb_bnd = reinterpret_cast<int64_t*>(base + o_nbnd);
+  a.total = reinterpret_cast<int32_t*>(base + o_total);
+  const int grid = (int)std::min<int64_t>(n, 1 << 16);
+  hipLaunchKernelGGL(k_alg1_init, dim3((int)std::min<int64_t>((n + 255) / 256, 1024)), dim3(256),
+                     0, stream, a.st, a.stats, n);
+  if ((rc = launch_ok())) return rc;
+  Extra cur;
+  cur.bound = a.bnd;
+  if ((rc = sim_batch_run<XB>(prob, layer_costs, nullptr, link, records, n, out_makespan,
+                              out_bubble, cur, stream)))
+    return rc;
+  Extra nbx;
+  nbx.bound = reinterpret_cast<int64_t*>(base + o_nbnd);
+  nbx.n_live = a.total;
+  for (int it = 0; it < iters; ++it) {
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, stream,
+                       reinterpret_cast<uint32_t*>(a.total), 1, 0u);
+    if ((rc = launch_ok())) return rc;
+    hipLaunchKernelGGL(k_alg1_expand, dim3(grid), dim3(WAVE), 0, stream, a);
+    if ((rc = launch_ok())) return rc;
+    if ((rc = sim_batch_run<XB>(prob, layer_costs, nullptr, link, a.nb_rec, nb,
+                                reinterpret_cast<int64_t*>(base + o_ms),
+                                reinterpret_cast<int64_t*>(base + o_bub), nbx, stream)))
+      return rc;
+    hipLaunchKernelGGL(k_alg1_select, dim3(grid), dim3(WAVE), 0, stream, a);
+    if ((rc = launch_ok())) return rc;
+  }
+  return OCTO_OK;
 }
 
 }  // namespace
@@ -2222,6 +2634,13 @@ int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
                        uint64_t seed, int32_t step, void* stream) {
   return tune_step_impl<true>(prob, layer_costs, layer_mem, capacity, max_advance, link, chains,
                               queues, n_chains, seed, step, static_cast<hipStream_t>(stream));
+}
+
+int octo_alg1_tune(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                   void* records, int64_t n, int32_t iters, int64_t* out_makespan,
+                   int64_t* out_bubble, int64_t* out_stats, void* stream) {
+  return alg1_impl(prob, layer_costs, link, records, n, iters, out_makespan, out_bubble,
+                   out_stats, static_cast<hipStream_t>(stream));
 }
 
 int octo_profile_events(void* const* events, int32_t n_events) {

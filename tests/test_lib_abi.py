@@ -55,9 +55,19 @@ def test_argument_checks_without_gpu():
                                     0, None) == -1
         assert L.octo_advance_w(ctypes.byref(p), None, None, None, None, None, 1, None, None,
                                 None, None, None) == -1
+        assert L.octo_alg1_tune(ctypes.byref(p), None, None, None, 1, 1, None, None, None,
+                                None) == -1
     # valid problem but null arrays / negative sizes are rejected before any launch
     assert L.octo_sim_batch(ctypes.byref(good), None, None, None, 4, None, None, None) == -1
     assert L.octo_sim_batch(ctypes.byref(good), None, None, None, -1, None, None, None) == -1
+    assert L.octo_alg1_tune(ctypes.byref(good), None, None, None, 4, 1, None, None, None,
+                            None) == -1
+    assert L.octo_alg1_tune(ctypes.byref(good), None, None, None, 4, -1, None, None, None,
+                            None) == -1
+    # the neighbour batch of one iteration (n x the largest neighbourhood) must fit int32
+    nbig = (2**31 - 1) // (3 * 1 * 8 + 2) + 1
+    assert L.octo_alg1_tune(ctypes.byref(good), None, None, None, nbig, 1, None, None, None,
+                            None) == -1
     assert L.octo_tune_step(ctypes.byref(good), None, None, None, None, 2, 0, -1, None) == -1
     assert L.octo_tune_step_mem(ctypes.byref(good), None, None, None, 8, None, None, None, 2, 0,
                                 0, None) == -1
