@@ -157,6 +157,58 @@ def time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev, warmu
     return res
 
 
+def time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, warmup, steps, with_cpu):
+    """Algorithm 1 (octo_alg1_tune) on 4,096 records of the batch (every 256th), widened to four
+    move slots, 32 iterations per call; the unit of work is one iteration of one record's search
+    (phase choice, its whole neighbourhood evaluated, best kept)."""
+    from oracle import alg1 as A
+    n, iters, mp = 4096, 32, 4
+    base = recs_np[::len(recs_np) // n][:n]
+    stride = inputs.record_stride(w.P, w.v_max, mp)
+    r_np = np.zeros((n, stride), np.uint8)
+    r_np[:, :base.shape[1]] = base
+    prob = _lib.problem(w.L, w.P, w.v_max, w.M, stride, mp)
+    r0 = torch.from_numpy(r_np).to(dev)
+    r = torch.empty_like(r0)
+    for _ in range(max(warmup, 1)):
+        r.copy_(r0)
+        res = _lib.alg1_tune(prob, costs, link, r, iters)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r.copy_(r0)
+        res = _lib.alg1_tune(prob, costs, link, r, iters)
+    torch.cuda.synchronize()
+    secs = (time.perf_counter() - t0) / steps
+    o_rec, o_ms = r.cpu().numpy(), res[0].cpu().numpy()
+    stats = res[2].cpu().numpy()
+    ms0 = _lib.sim_batch(prob, costs, link, r0)[0].cpu().numpy()
+    ok = ms0 > 0
+    out = {"value": round(n * iters / secs, 1), "unit": "record-iterations/s",
+           "ms_per_call": round(secs * 1e3, 3), "records": n, "iterations": iters,
+           "move_slots": mp, "searched_iterations": int(stats[:, 3].sum()),
+           "kept_moves": {"partition": int(stats[:, 0].sum()), "placement": int(stats[:, 1].sum()),
+                          "schedule": int(stats[:, 2].sum())},
+           "mean_makespan_gain": round(float(1 - (o_ms[ok] / ms0[ok]).mean()), 4),
+           "cpu_baseline": None}
+    if with_cpu:
+        from oracle import octoref
+        sample = np.arange(0, n, 256)
+        threads = min(16, os.cpu_count() or 1)
+        rprob = octoref.problem(w.L, w.P, w.v_max, w.M, stride, mp)
+        c0 = time.perf_counter()
+        rr = A.tune(rprob, inputs.layer_costs(w), inputs.link_matrix(w.P, w.link_ns),
+                    r_np[sample], iters, nthreads=threads)
+        c1 = time.perf_counter()
+        same = bool((rr[0] == o_rec[sample]).all() and (rr[1] == o_ms[sample]).all() and
+                    (rr[3] == stats[sample, :3]).all() and (rr[4] == stats[sample, 3]).all())
+        out["cpu_baseline"] = {"value": round(len(sample) * iters / (c1 - c0), 1),
+                               "unit": "record-iterations/s", "cores": threads, "kind": "oracle",
+                               "sample": f"every 256th of the same records ({len(sample)})",
+                               "parity_on_sample": same}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,6 +335,8 @@ def main():
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
                                args.warmup, min(args.steps, 3), not args.no_cpu)
+    alg1 = time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, args.warmup,
+                     min(args.steps, 3), not args.no_cpu)
     cpu = None
     if not args.no_cpu:
         from oracle import octoref
@@ -315,6 +369,7 @@ def main():
         "comm_model": comm_model,
         "serial_links": serial_links,
         "w_advance": w_advance,
+        "alg1": alg1,
     }
     print(json.dumps(out), flush=True)
 
