@@ -356,6 +356,124 @@ done:
   return rc;
 }
 
+/*
+ * Blocking rendezvous transfers (the naive coordination of §3.3, "Irregular Execution Orders"):
+ * a device receives an op's input from another device right before the op and sends the op's
+ * output to another device right after it, and a transfer holds both devices from the moment
+ * both have reached it until it ends c = link[p][q] later (blocking point-to-point send and
+ * receive). Each device's program is its queue with these transfer nodes inserted:
+ *   [receive of Y's cross-device input]  Y  [send of Y's cross-device output]
+ * and a transfer is ONE node of duration c in both its producer's and its consumer's program.
+ * Edges: program order on every device; data edges between stages on one device (weight 0);
+ * F(s,m) -> B(s,m); B(s,m) -> W(s,m). A cross-device data edge X -> Y is implied (X precedes
+ * the transfer in one program, the transfer precedes Y in the other). Longest path by Kahn's
+ * algorithm; a cycle is a deadlock (devices waiting on each other's transfers). Outputs as
+ * simulate; busy time counts computation only, so time spent in transfers is bubble.
+ */
+static int simulate_rdv(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                        const int* qlen, int64_t* makespan, int64_t* bubble) {
+  int S = g->S, M = g->M, nk = g->split ? 3 : 2;
+  int nc = nk * S * M;         /* compute nodes: node_id */
+  int nn = nc + 2 * S * M;     /* transfer nodes: nc + (dir * S + producer stage) * M + m */
+  /* successors: at most two program successors (a transfer sits in two programs) + 3 data */
+  int* succ = (int*)malloc(sizeof(int) * (size_t)nn * 5);
+  int* nsucc = (int*)calloc(nn, sizeof(int));
+  int* indeg = (int*)calloc(nn, sizeof(int));
+  int64_t* dur = (int64_t*)calloc(nn, sizeof(int64_t));
+  int64_t* est = (int64_t*)calloc(nn, sizeof(int64_t));
+  int64_t* fin = (int64_t*)malloc(sizeof(int64_t) * nn);
+  int* ready = (int*)malloc(sizeof(int) * nn);
+  int* seen = (int*)calloc(nc, sizeof(int));
+  int rc = SIM_OK;
+#define RDV_EDGE(a, b) (succ[(size_t)(a) * 5 + nsucc[a]++] = (b), indeg[b]++)
+  for (int s = 0; s < S; ++s)
+    for (int m = 0; m < M; ++m) {
+      for (int k = 0; k < nk; ++k) dur[node_id(S, M, k, s, m)] = op_dur(g, k, s);
+      if (s + 1 < S && g->dev[s] != g->dev[s + 1])
+        dur[nc + (0 * S + s) * M + m] = g->link[g->dev[s] * g->P + g->dev[s + 1]];
+      if (s > 0 && g->dev[s] != g->dev[s - 1])
+        dur[nc + (1 * S + s) * M + m] = g->link[g->dev[s] * g->P + g->dev[s - 1]];
+    }
+  /* programs */
+  for (int d = 0; d < g->P && rc == SIM_OK; ++d) {
+    int prev = -1;
+    for (int i = 0; i < qlen[d]; ++i) {
+      ref_sop o = queue[qoff[d] + i];
+      if (o.kind < 0 || o.kind >= nk || o.s < 0 || o.s >= S || o.m < 0 || o.m >= M ||
+          g->dev[o.s] != d || seen[node_id(S, M, o.kind, o.s, o.m)]) {
+        rc = SIM_BADQ;
+        break;
+      }
+      const int y = node_id(S, M, o.kind, o.s, o.m);
+      seen[y] = 1;
+      int tin = -1, tout = -1;
+      if (o.kind == KF) {
+        if (o.s > 0 && g->dev[o.s - 1] != d) tin = nc + (0 * S + o.s - 1) * M + o.m;
+        if (o.s + 1 < S && g->dev[o.s + 1] != d) tout = nc + (0 * S + o.s) * M + o.m;
+      } else if (o.kind == KB) {
+        if (o.s + 1 < S && g->dev[o.s + 1] != d) tin = nc + (1 * S + o.s + 1) * M + o.m;
+        if (o.s > 0 && g->dev[o.s - 1] != d) tout = nc + (1 * S + o.s) * M + o.m;
+      }
+      const int items[3] = {tin, y, tout};
+      for (int k = 0; k < 3; ++k) {
+        if (items[k] < 0) continue;
+        if (prev >= 0) RDV_EDGE(prev, items[k]);
+        prev = items[k];
+      }
+    }
+  }
+  if (rc == SIM_OK)
+    for (int i = 0; i < nc; ++i)
+      if (!seen[i]) rc = SIM_BADQ;
+  if (rc != SIM_OK) goto done;
+  /* data edges within one device, and F -> B, B -> W */
+  for (int s = 0; s < S; ++s)
+    for (int m = 0; m < M; ++m) {
+      if (s + 1 < S && g->dev[s] == g->dev[s + 1])
+        RDV_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KF, s + 1, m));
+      if (s > 0 && g->dev[s] == g->dev[s - 1])
+        RDV_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KB, s - 1, m));
+      RDV_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KB, s, m));
+      if (g->split) RDV_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KW, s, m));
+    }
+#undef RDV_EDGE
+  int nr = 0, head = 0;
+  for (int i = 0; i < nn; ++i)
+    if (indeg[i] == 0) ready[nr++] = i;
+  while (head < nr) {
+    const int u = ready[head++];
+    fin[u] = est[u] + dur[u];
+    for (int e = 0; e < nsucc[u]; ++e) {
+      const int x = succ[(size_t)u * 5 + e];
+      if (fin[u] > est[x]) est[x] = fin[u];
+      if (--indeg[x] == 0) ready[nr++] = x;
+    }
+  }
+  if (nr < nn) { /* some node never became ready: a cycle (unused transfer slots have no edges) */
+    rc = SIM_CYCLE;
+    goto done;
+  }
+  int64_t ms = 0;
+  for (int i = 0; i < nn; ++i)
+    if (fin[i] > ms) ms = fin[i];
+  *makespan = ms;
+  for (int d = 0; d < g->P; ++d) {
+    int64_t busy = 0;
+    for (int i = 0; i < qlen[d]; ++i) busy += op_dur(g, queue[qoff[d] + i].kind, queue[qoff[d] + i].s);
+    bubble[d] = ms - busy;
+  }
+done:
+  free(succ);
+  free(nsucc);
+  free(indeg);
+  free(dur);
+  free(est);
+  free(fin);
+  free(ready);
+  free(seen);
+  return rc;
+}
+
 /* ------------------------------------------------------------------------------------------ */
 /* MERGE: the ideal stage-level order.                                                         */
 /* ------------------------------------------------------------------------------------------ */
@@ -607,10 +725,11 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
  * memory [L][2] = {activation bytes per micro-batch, static bytes}; then peak[P] is filled, and
  * ppos[P] (nullable) with the queue position at which each device first reaches its peak (-1
  * when it holds no activations). */
+/* xfer: 0 asynchronous transfers (the plain model), 1 serialised links, 2 blocking rendezvous. */
 static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                         const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                         const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos,
-                        int64_t* comm, int serial, int64_t* bounds) {
+                        int64_t* comm, int xfer, int64_t* bounds) {
   int P = pr->P, S = c->S, split;
   resolve(pr, c, &split);
   int64_t F[64], B[64], W[64];
@@ -628,11 +747,12 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
       sq[qoff[d] + i] = (ref_sop){o.kind, s, o.m};
     }
   }
-  ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link, serial};
+  ref_dag_in g = {S, pr->M, split, P, c->dev, F, B, W, link, xfer == 1};
   int64_t* start = (mem || comm || bounds)
                        ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M)
                        : NULL;
-  int rc = simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
+  int rc = xfer == 2 ? simulate_rdv(&g, sq, qoff, qlen, ms, bub)
+                       : simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
   if (bounds && rc == SIM_OK) {
     /* per device: start of its first op, end of its last op (0, 0 for an empty queue) */
     for (int d = 0; d < P; ++d) {
@@ -670,7 +790,7 @@ static int eval_local(const ref_problem* pr, const ref_cand* c, const int64_t* c
 /* Full evaluation of one candidate record: makespan + bubbles, or sentinels. */
 static void eval_record(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                         const int64_t* link, const uint8_t* rec, int64_t* ms, int64_t* bub,
-                        int64_t* peak, int64_t* comm, int serial, int64_t* bounds) {
+                        int64_t* peak, int64_t* comm, int xfer, int64_t* bounds) {
   ref_cand* c = (ref_cand*)malloc(sizeof(ref_cand));
   decode(pr, rec, c);
   int P = pr->P;
@@ -686,7 +806,7 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
       sentinel = REF_INVALID;
     } else {
       int rc =
-          eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm, serial,
+          eval_local_c(pr, c, costs, link, q, qcap, qlen, mem, ms, bub, peak, NULL, comm, xfer,
                        bounds);
       if (rc == SIM_CYCLE) sentinel = REF_DEADLOCK;
       else if (rc != SIM_OK) sentinel = REF_INVALID;
@@ -819,7 +939,7 @@ typedef struct {
   int64_t* out_bub;
   int64_t* out_peak;
   int64_t* out_comm;
-  int serial;
+  int xfer;
   int64_t* out_bounds;
 } batch_job;
 
@@ -829,7 +949,7 @@ static void* batch_worker(void* arg) {
     eval_record(j->pr, j->costs, j->mem, j->link, j->cands + (size_t)i * j->pr->cand_stride,
                 j->out_ms + i, j->out_bub + (size_t)i * j->pr->P,
                 j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL,
-                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL, j->serial,
+                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL, j->xfer,
                 j->out_bounds ? j->out_bounds + (size_t)i * 2 * j->pr->P : NULL);
   return NULL;
 }
@@ -838,7 +958,7 @@ static void* batch_worker(void* arg) {
  * mem (nullable, with out_peak): layer memory [L][2]; out_peak[n][P] = peak bytes per device. */
 static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t* mem,
                      const int64_t* link, const uint8_t* cands, int64_t n, int64_t* out_ms,
-                     int64_t* out_bub, int64_t* out_peak, int64_t* out_comm, int serial,
+                     int64_t* out_bub, int64_t* out_peak, int64_t* out_comm, int xfer,
                      int64_t* out_bounds, int nthreads) {
   if (!check_problem(pr) || n < 0 || (n > 0 && (!costs || !link || !cands || !out_ms || !out_bub)))
     return REF_EINVAL;
@@ -850,7 +970,7 @@ static int run_batch(const ref_problem* pr, const int64_t* costs, const int64_t*
   batch_job jobs[256];
   for (int t = 0; t < nthreads; ++t) {
     jobs[t] = (batch_job){pr,     costs,  mem,     link,    cands, n * t / nthreads,
-                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm, serial,
+                          n * (t + 1) / nthreads, out_ms, out_bub, out_peak, out_comm, xfer,
                           out_bounds};
     if (nthreads == 1) batch_worker(&jobs[t]);
     else pthread_create(&th[t], NULL, batch_worker, &jobs[t]);
@@ -879,6 +999,14 @@ int oracle_sim_batch_serial(const ref_problem* pr, const int64_t* costs, const i
                             const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                             int nthreads) {
   return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 1, NULL,
+                   nthreads);
+}
+
+/* Evaluation with blocking rendezvous transfers (see simulate_rdv). */
+int oracle_sim_batch_rdv(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                         const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                         int nthreads) {
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 2, NULL,
                    nthreads);
 }
 

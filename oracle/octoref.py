@@ -38,6 +38,9 @@ def lib():
         L.oracle_sim_batch_serial.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                               ctypes.c_int64, p, p, ctypes.c_int]
         L.oracle_sim_batch_serial.restype = ctypes.c_int
+        L.oracle_sim_batch_rdv.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
+                                           ctypes.c_int64, p, p, ctypes.c_int]
+        L.oracle_sim_batch_rdv.restype = ctypes.c_int
         L.oracle_sim_batch_bounds.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                               ctypes.c_int64, p, p, p, ctypes.c_int]
         L.oracle_sim_batch_bounds.restype = ctypes.c_int
@@ -105,6 +108,23 @@ def sim_batch_mem(prob, costs, mem, link, cands, nthreads=1):
     if rc != 0:
         raise ValueError(f"oracle_sim_batch_mem rejected the arguments (rc={rc})")
     return ms, bub, peak
+
+
+def sim_batch_rdv(prob, costs, link, cands, nthreads=1):
+    """Evaluate candidate records with blocking rendezvous transfers (receive right before the
+    consumer, send right after the producer; a transfer holds both devices until it ends).
+    Returns (makespan[n], bubble[n, P])."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    rc = lib().oracle_sim_batch_rdv(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(cands), n,
+                                    _ptr(ms), _ptr(bub), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch_rdv rejected the arguments (rc={rc})")
+    return ms, bub
 
 
 def sim_batch_serial(prob, costs, link, cands, nthreads=1):

@@ -9,6 +9,11 @@ is pinned to something other than itself:
   Performance"), obtained without any graph algorithm. Durations must be small integers.
   With ``serial``, a directed link carries one transfer at a time: when an op ends, each of its
   transfers joins its link's queue and starts once the link is free.
+* ``rdv_tick_simulate`` executes device programs with blocking rendezvous transfers (the naive
+  coordination of §3.3): each device receives an op's cross-device input right before the op and
+  sends its cross-device output right after it; a device that reaches a send or receive waits
+  there, and once both ends have arrived the transfer runs for the link time, holding both.
+  Tick by tick, with no graph: a program that can never move again is a deadlock.
 * ``has_cycle`` builds the dependency graph from its definition (§5, §6 "Scheduling Tuning") and
   runs an iterative three-colour DFS.
 
@@ -101,6 +106,76 @@ def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None,
     if not all(ptr[d] == len(queues[d]) and running[d] is None for d in range(P)):
         return -1, [-1] * P
     ms = max(fin.values()) if fin else 0
+    bub = [ms - sum(_dur(k, s, split, Fs, Bs, Ws) for (k, s, m) in queues[d]) for d in range(P)]
+    return ms, bub
+
+
+def rdv_programs(S, dev, queues):
+    """Per device: ("r", producer op) before an op with a cross-device input, ("c", op), and
+    ("s", op) after an op with a cross-device output. A transfer is named by its producer."""
+    progs = []
+    for d, q in enumerate(queues):
+        prog = []
+        for op in q:
+            kind, s, m = op
+            if kind == F and s > 0 and dev[s - 1] != d:
+                prog.append(("r", (F, s - 1, m)))
+            if kind == B and s < S - 1 and dev[s + 1] != d:
+                prog.append(("r", (B, s + 1, m)))
+            prog.append(("c", op))
+            if _consumers(op, S, dev):
+                prog.append(("s", op))
+        progs.append(prog)
+    return progs
+
+
+def rdv_tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues):
+    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock."""
+    progs = rdv_programs(S, dev, queues)
+    total = sum(_dur(k, s, split, Fs, Bs, Ws) for q in queues for (k, s, m) in q)
+    max_ticks = total + sum(max(r) for r in link) * 2 * S * M + 2
+    ptr = [0] * P
+    running = [None] * P               # ("c", op) or ("x", transfer) until busy_until
+    busy_until = [0] * P
+    arrived = {}                       # transfer -> the ends ("s", "r") waiting at it
+    fin = {}
+    t = 0
+    while t <= max_ticks:
+        changed = True
+        while changed:
+            changed = False
+            for d in range(P):
+                if running[d] is not None and busy_until[d] <= t:
+                    if running[d][0] == "c":
+                        fin[running[d][1]] = busy_until[d]
+                    running[d] = None
+                    ptr[d] += 1
+                    changed = True
+            for d in range(P):
+                if running[d] is not None or ptr[d] >= len(progs[d]):
+                    continue
+                what, x = progs[d][ptr[d]]
+                if what == "c":
+                    local = [p for p, _ in _producers(x, S, split, dev, link) if dev[p[1]] == d]
+                    if all(p in fin and fin[p] <= t for p in local):
+                        running[d] = ("c", x)
+                        busy_until[d] = t + _dur(x[0], x[1], split, Fs, Bs, Ws)
+                        changed = True
+                elif what not in arrived.setdefault(x, set()):
+                    arrived[x].add(what)
+                    if arrived[x] == {"s", "r"}:
+                        p = dev[x[1]]
+                        q = dev[_consumers(x, S, dev)[0][1]]
+                        for e in (p, q):
+                            running[e] = ("x", x)
+                            busy_until[e] = t + link[p][q]
+                    changed = True
+        if all(ptr[d] == len(progs[d]) for d in range(P)):
+            break
+        t += 1
+    if not all(ptr[d] == len(progs[d]) for d in range(P)):
+        return -1, [-1] * P
+    ms = max(max(fin.values(), default=0), max(busy_until, default=0))
     bub = [ms - sum(_dur(k, s, split, Fs, Bs, Ws) for (k, s, m) in queues[d]) for d in range(P)]
     return ms, bub
 
