@@ -174,6 +174,22 @@ int octo_sim_batch_serial(const octo_problem* prob, const int64_t* layer_costs,
                           int64_t* out_makespan, int64_t* out_bubble, void* stream);
 
 /*
+ * octo_sim_batch_rdv — octo_sim_batch with blocking rendezvous transfers, the naive
+ * coordination of computation and point-to-point communication that §3.3 ("Irregular Execution
+ * Orders", Fig. 3(a)-(b)) shows deadlocking: a device receives an op's input from another device
+ * right before the op and sends the op's output to another device right after it, and a
+ * transfer starts once both devices have reached it and holds both until it ends
+ * c = link[p][q] later (blocking send and receive). Each device's program is thus its queue with
+ * [receive] op [send] around every op that has a cross-device input / output. A cycle of waits
+ * (e.g. two devices sending to each other at once, as in 1F1B's steady state) is a deadlock:
+ * OCTO_MS_DEADLOCK. Busy time counts computation only, so transfer time is bubble. Validity,
+ * arguments, results and status as octo_sim_batch.
+ */
+int octo_sim_batch_rdv(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                       const void* candidates, int64_t n, int64_t* out_makespan,
+                       int64_t* out_bubble, void* stream);
+
+/*
  * octo_advance_w — selective W advancing (§6 "Scheduling Tuning", third policy) under the
  * per-device capacity of §6 Eq. 2, on a batch of candidate records. For each record, after its
  * queues are generated and its moves applied: while some device's peak (as octo_sim_batch_mem)

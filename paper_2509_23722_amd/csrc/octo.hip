@@ -52,6 +52,7 @@ struct SimArgs {
   const uint8_t* cands;
   int64_t n;
   const int32_t* n_live;  // nullable: only the first *n_live of the n records are evaluated
+  int afab_mat;           // GPipe queues take the materialised path (rendezvous calls)
   int64_t* out_ms;
   int64_t* out_bub;
   int32_t* ctl;
@@ -145,12 +146,16 @@ __device__ __forceinline__ int64_t setup_chunks(Chunks<VMAX>& c, const Problem& 
       const int dn = s < S - 1 ? dev[s + 1] : d;
       c.wF[k] = dp != d ? link[dp * pr.P + d] : 0;
       c.wB[k] = dn != d ? link[dn * pr.P + d] : 0;
-      if (mode == XC || mode == XS) {
+      if (mode == XC || mode == XS || mode == XR) {
         // a forward's output goes to stage s + 1, a backward's to stage s - 1
         c.cF[k] = dn != d ? link[d * pr.P + dn] : 0;
         c.cB[k] = dp != d ? link[d * pr.P + dp] : 0;
         c.xF[k] = (dp != d ? CX_IN : 0) | (dn != d ? CX_OUT : 0);
         c.xB[k] = (dn != d ? CX_IN : 0) | (dp != d ? CX_OUT : 0);
+      }
+      if (mode == XR) {  // where each op's input comes from (its producer's mailbox)
+        c.dnF[k] = dp != d ? dp : -1;
+        c.dnB[k] = dn != d ? dn : -1;
       }
       if (mode == XS) {
         c.dnF[k] = dn != d ? dn : -1;
@@ -228,7 +233,7 @@ __device__ __forceinline__ void stage_record(uint8_t* dst, const uint8_t* src, i
 // the results. cand < 0: this group has no candidate. P2: P and v are powers of two.
 template <int VMAX, int GEN, bool P2, int X>
 __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, int v, int split,
-                                              uint8_t* lds_wave) {
+                                              uint8_t* lds_wave, int64_t* mbox) {
   const int G = a.G, P = a.pr.P, M = a.pr.M;
   const int g = lane_id() / G;
   const int d = lane_id() % G;
@@ -267,23 +272,24 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
   bool dead = false;
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
+  if constexpr (X == XR) mbox[lane_id()] = RDV_EMPTY;
   if constexpr (GEN == GEN_AFAB) {
     GenAfab g;
     g.init(v, M);
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    rounds<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, mbox);
   } else if constexpr (GEN == GEN_INTER) {
     const int r = c.st[0];
     if constexpr (P2) {
       GenInterP2 g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      rounds<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, mbox);
     } else {
       GenInter g;
       g.init(P, v, M, r, split, split ? r : 0);
       describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-      relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      rounds<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, mbox);
     }
   } else {
     GenMerge<VMAX> g;
@@ -291,7 +297,7 @@ __device__ __forceinline__ void run_generated(const SimArgs& a, int64_t cand, in
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), rowlen, mine ? v : 0,
            [&](int k) { return pick<VMAX>(c.st, k); });
     describe<VMAX>(L, c, ring, g.kind, g.k, g.m);
-    relax<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    rounds<VMAX, false, X>(g, c, ring, L, T, G, gbit, lsb, dead, mbox);
   }
 
   const int64_t ms = group_max(L.clock, G);
@@ -576,7 +582,8 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
       if (a.out_bound)
         for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
     } else {
-      bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
+      bin = (r.n_pert > 0 || (a.afab_mat && r.gen == GEN_AFAB)) ? BIN_MAT
+                                                                 : bin_of(r.v, r.gen, r.split);
     }
     bins[i] = (uint8_t)bin;
   }
@@ -638,11 +645,14 @@ __device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, uint64_
 
 template <int VMAX, int X>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
-                                             int split, uint8_t* lds_wave) {
+                                             int split, uint8_t* lds_wave, int64_t* mbox) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
-  if (gen == GEN_MERGE) run_generated<VMAX, GEN_MERGE, false, X>(a, cand, v, split, lds_wave);
-  else if (p2) run_generated<VMAX, GEN_INTER, true, X>(a, cand, v, split, lds_wave);
-  else run_generated<VMAX, GEN_INTER, false, X>(a, cand, v, split, lds_wave);
+  if (gen == GEN_MERGE)
+    run_generated<VMAX, GEN_MERGE, false, X>(a, cand, v, split, lds_wave, mbox);
+  else if (p2)
+    run_generated<VMAX, GEN_INTER, true, X>(a, cand, v, split, lds_wave, mbox);
+  else
+    run_generated<VMAX, GEN_INTER, false, X>(a, cand, v, split, lds_wave, mbox);
 }
 
 // Generated-queue simulation (INTER and MERGE) for the bins in a.bin_mask of one v class:
@@ -651,6 +661,7 @@ __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t 
 template <int VC, int X>
 __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int64_t mbox[X == XR ? WAVE : 1];  // rendezvous mailboxes
   const int g = lane_id() / a.G;
   const int d = lane_id() % a.G;
   for (;;) {
@@ -676,7 +687,7 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
         continue;
       }
     }
-    dispatch_gen<VC, X>(a, gen, cand, v, split, smem);
+    dispatch_gen<VC, X>(a, gen, cand, v, split, smem, mbox);
   }
 }
 
@@ -977,6 +988,7 @@ __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
 template <int VMAX, int X>
 __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int64_t mbox[X == XR ? WAVE : 1];  // rendezvous mailboxes
   const int G = a.G, P = a.pr.P, M = a.pr.M;
   const int g = lane_id() / G;
   const int d = lane_id() % G;
@@ -1045,8 +1057,9 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       GenMat q;
       q.init(row, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+      if constexpr (X == XR) mbox[lane_id()] = RDV_EMPTY;
       bool dead = false;
-      relax<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      rounds<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, mbox);
       const int64_t ms = group_max(L.clock, G);
       CommTally tot = L.cm;
       if constexpr (X == XC) tot = group_tally(L.cm, G);
@@ -2156,6 +2169,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
   a.n_live = nullptr;
+  a.afab_mat = 0;
   a.out_ms = ms;
   a.out_bub = bub;
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
@@ -2207,7 +2221,7 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
   // encoded for exactly this geometry
   bool tab = false;
   Plan pl{};
-  if (VC <= 2 && X != XS && su.ws->qt_valid) {
+  if (VC <= 2 && X != XS && X != XR && su.ws->qt_valid) {
     const TabGeom geo = tab_geom(prob, su.di.lds_max, VC, X != XP);
     constexpr int vi = VC <= 2 ? VC - 1 : 0;
     tab = geo.plan.CPW >= 1 && geo.ring.R == ring.R && su.ws->qt_R[vi] == geo.ring.R &&
@@ -2333,6 +2347,7 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   a.out_comm = cm;
   a.out_bound = bd;
   a.n_live = ex.n_live;
+  a.afab_mat = X == XR;
   const int tb = CLS_THREADS;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
@@ -2350,7 +2365,8 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
   // materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
-  if (X != XS && (rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream))) return rc;
+  if (X != XS && X != XR && (rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream)))
+    return rc;
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
   if (prob->v_max >= 2 &&
@@ -2367,9 +2383,11 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
                              P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
-                           stream)))
-    return rc;
+  if constexpr (X != XR) {  // rendezvous: GPipe queues were sent to the materialised path
+    if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
+                             stream)))
+      return rc;
+  }
   if ((rc = record_mark(4, stream))) return rc;
   if (prob->v_max <= 2)
     hipLaunchKernelGGL((k_sim_mat<2, X>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
@@ -2572,6 +2590,13 @@ int octo_sim_batch_serial(const octo_problem* prob, const int64_t* layer_costs,
                           const int64_t* link, const void* candidates, int64_t n,
                           int64_t* out_makespan, int64_t* out_bubble, void* stream) {
   return sim_batch_impl<XS>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                            out_bubble, Extra{}, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_rdv(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                       const void* candidates, int64_t n, int64_t* out_makespan,
+                       int64_t* out_bubble, void* stream) {
+  return sim_batch_impl<XR>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
                             out_bubble, Extra{}, static_cast<hipStream_t>(stream));
 }
 

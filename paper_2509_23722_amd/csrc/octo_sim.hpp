@@ -41,7 +41,9 @@ constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
 // per device, §5 memory nodes), communication nodes and their overlap (§5), or times with
 // serialised links (a directed link carries one transfer at a time, in issue order), or each
 // device's first start and last finish (its leading and trailing idle).
-constexpr int XP = 0, XM = 1, XC = 2, XS = 3, XB = 4;
+// XR: blocking rendezvous transfers (a device receives an op's cross-device input right before
+// the op and sends its cross-device output right after it; a transfer holds both devices).
+constexpr int XP = 0, XM = 1, XC = 2, XS = 3, XB = 4, XR = 5;
 // Weight of a weight-gradient op's read under serialised links: its B is on its own device and
 // earlier in its queue, so only the readiness bit matters, not the (possibly delayed) slot time.
 constexpr int64_t W_NO_TIME = -((int64_t)1 << 50);
@@ -141,7 +143,7 @@ struct Desc {
   int64_t dm;      // activation bytes the op allocates (> 0) or releases (< 0)
   int64_t cout;    // transfer time of the op's output to another device
   int cx;          // CX_IN | CX_OUT
-  int dst;         // device the op's output goes to
+  int dst;         // device the op's output goes to (XR: the device its input comes from)
   __device__ __forceinline__ void take_if(bool t, const Desc& o) {
     dm = t ? o.dm : dm;
     cout = t ? o.cout : cout;
@@ -311,6 +313,73 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
       break;
     }
   }
+}
+
+// Blocking rendezvous transfers (XR). Per op a lane takes up to three steps: receive, when the
+// op's input comes from another device — ready once the producer's slot shows it finished; the
+// transfer runs from max(producer's finish, this device's clock) for the link time, this
+// device's clock moves to its end, and the end goes to the producer's mailbox; compute, as in
+// relax; send, when the op's output goes to another device — the lane waits until its mailbox
+// holds the transfer's end (posted by the receiver), takes it as its clock and clears the box.
+// A producer reaches its send in the round it finishes the op, so the receiver (which reads the
+// slot in a later round) always posts to a waiting sender, and each box has one writer at a
+// time. mbox: one int64 per lane of the wave (RDV_EMPTY = nothing posted), set to RDV_EMPTY by
+// the caller. A round in which no lane of the wave takes a step changes nothing, so every group
+// with work left is deadlocked.
+constexpr int64_t RDV_EMPTY = -1;
+template <int VMAX, class Tab, class Gen>
+__device__ __forceinline__ void relax_rdv(Gen& gen, const Chunks<VMAX>& c, const Ring& ring,
+                                          Lane& L, const Tab& T, int G, uint64_t gbit,
+                                          uint64_t lsb, bool& dead, int64_t* mbox) {
+  const int me = (int)(threadIdx.x & 63);
+  const int g0 = me - me % G;  // the group's first lane
+  bool live = L.pos < L.nops;
+  int step = (live && (L.cx & CX_IN)) ? 0 : 1;  // 0 receive, 1 compute, 2 send
+  for (;;) {
+    uint32_t plo, phi;
+    T.issue(live ? L.rd : 0, plo, phi);
+    const int64_t box = mbox[me];
+    const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
+    const bool rdy = live && (plo & (uint32_t)L.mask) == (uint32_t)L.want;
+    const int64_t tx = (int64_t)(p >> 3);
+    const bool okR = step == 0 && rdy;
+    const int64_t xend = (tx > L.clock ? tx : L.clock) + L.w;
+    const bool okC = step == 1 && rdy;
+    const int64_t tin = tx + L.w;
+    const int64_t st = tin > L.clock ? tin : L.clock;
+    const int64_t fin = st + L.dur;
+    const bool okS = step == 2 && box != RDV_EMPTY;
+    if (okR) mbox[g0 + L.dst] = xend;
+    if (okC && L.store) T.store(L.wr, ((uint64_t)fin << 3) | L.state);
+    if (okS) mbox[me] = RDV_EMPTY;
+    L.clock = okR ? xend : okC ? fin : okS ? box : L.clock;
+    const bool sends = (L.cx & CX_OUT) != 0;
+    const bool done = (okC && !sends) || okS;
+    step = okR ? 1 : (okC && sends) ? 2 : step;
+    L.pos += done ? 1 : 0;
+    live = L.pos < L.nops;
+    gen.advance(done);
+    describe<VMAX>(L, c, ring, gen.kind, gen.k, gen.m);
+    step = done ? ((live && (L.cx & CX_IN)) ? 0 : 1) : step;
+    __asm__ volatile("" ::: "memory");
+    if (__ballot(okR || okC || okS) == 0) {
+      const uint64_t actm = __ballot(live);
+      if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
+      break;
+    }
+  }
+}
+
+// The rounds of one evaluation: relax, or relax_rdv for rendezvous transfers (mbox: its
+// mailboxes, unused otherwise).
+template <int VMAX, bool SPEC, int X, class Tab, class Gen>
+__device__ __forceinline__ void rounds(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
+                                       const Tab& T, int G, uint64_t gbit, uint64_t lsb,
+                                       bool& dead, int64_t* mbox) {
+  if constexpr (X == XR)
+    relax_rdv<VMAX>(gen, c, ring, L, T, G, gbit, lsb, dead, mbox);
+  else
+    relax<VMAX, SPEC, X>(gen, c, ring, L, T, G, gbit, lsb, dead, nullptr);
 }
 
 // ------------------------------------------------------------------------------------------
