@@ -12,6 +12,7 @@ import ctypes
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -284,7 +285,7 @@ def main():
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         t = json.load(open(TRAFFIC_FILE))
-        tk = str(t.get("kernel", "")).replace(", false>", ">")
+        tk = re.sub(r", (false|0)>$", ">", str(t.get("kernel", "")))
         if t.get("kernel_source_sha") == kernel_source_hash() and tk == SIM_KERNELS[dom]:
             traffic = t.get("hbm_bytes_per_launch")
     all_ms = float(per_kernel_ms.sum())
@@ -332,6 +333,16 @@ def main():
     serial_links = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "sim_kernels_ms": k_,
                     "makespan_changed": int((s_np != ms.cpu().numpy()).sum())}
 
+    # with blocking rendezvous transfers (receive before the consumer, send after the producer)
+    rms_ = torch.empty_like(ms)
+    rbub_ = torch.empty_like(bub)
+    v_, t_, k_ = time_variant(
+        torch, _lib, lambda: _lib.sim_batch_rdv(prob, costs, link, recs, rms_, rbub_), n,
+        args.steps, args.warmup)
+    r_np = rms_.cpu().numpy()
+    rendezvous = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "sim_kernels_ms": k_,
+                  "deadlocked": int((r_np == -1).sum()), "completed": int((r_np > 0).sum())}
+
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
                                args.warmup, min(args.steps, 3), not args.no_cpu)
@@ -368,6 +379,7 @@ def main():
         "memory_model": memory_model,
         "comm_model": comm_model,
         "serial_links": serial_links,
+        "rendezvous": rendezvous,
         "w_advance": w_advance,
         "alg1": alg1,
     }
