@@ -357,35 +357,125 @@ done:
 }
 
 /*
- * Blocking rendezvous transfers (the naive coordination of §3.3, "Irregular Execution Orders"):
- * a device receives an op's input from another device right before the op and sends the op's
- * output to another device right after it, and a transfer holds both devices from the moment
- * both have reached it until it ends c = link[p][q] later (blocking point-to-point send and
- * receive). Each device's program is its queue with these transfer nodes inserted:
- *   [receive of Y's cross-device input]  Y  [send of Y's cross-device output]
- * and a transfer is ONE node of duration c in both its producer's and its consumer's program.
- * Edges: program order on every device; data edges between stages on one device (weight 0);
- * F(s,m) -> B(s,m); B(s,m) -> W(s,m). A cross-device data edge X -> Y is implied (X precedes
- * the transfer in one program, the transfer precedes Y in the other). Longest path by Kahn's
- * algorithm; a cycle is a deadlock (devices waiting on each other's transfers). Outputs as
- * simulate; busy time counts computation only, so time spent in transfers is bubble.
+ * Device programs with blocking rendezvous transfers. A program is a device's sequence of
+ * items: computing an op, sending an op's output to another device, or receiving an op's input
+ * from another device. A transfer (producer X on device p -> consumer Y on device q) is ONE node
+ * of duration c = link[p][q] that sits in both p's program (as the send) and q's (as the
+ * receive): it starts once both devices have reached it and holds both until it ends (blocking
+ * point-to-point send and receive). Item codes: (kind << 28) | node, kind 0 compute (node = the
+ * op's node id), 1 send, 2 receive (node = the PRODUCER's node id).
  */
-static int simulate_rdv(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
-                        const int* qlen, int64_t* makespan, int64_t* bubble) {
+#define PI_COMP 0
+#define PI_SEND 1
+#define PI_RECV 2
+
+/* The consumer of X's output on another device, or -1. */
+static int cross_consumer(const ref_dag_in* g, int kind, int s, int m) {
+  const int S = g->S, M = g->M;
+  if (kind == KF && s + 1 < S && g->dev[s + 1] != g->dev[s]) return node_id(S, M, KF, s + 1, m);
+  if (kind == KB && s > 0 && g->dev[s - 1] != g->dev[s]) return node_id(S, M, KB, s - 1, m);
+  return -1;
+}
+
+/* The producer of Y's input on another device, or -1. */
+static int cross_producer(const ref_dag_in* g, int kind, int s, int m) {
+  const int S = g->S, M = g->M;
+  if (kind == KF && s > 0 && g->dev[s - 1] != g->dev[s]) return node_id(S, M, KF, s - 1, m);
+  if (kind == KB && s + 1 < S && g->dev[s + 1] != g->dev[s]) return node_id(S, M, KB, s + 1, m);
+  return -1;
+}
+
+/* The naive coordination of §3.3 ("Irregular Execution Orders"): receive an op's cross-device
+ * input right before it, send its cross-device output right after it. prog gets at most 3 qlen[d]
+ * items per device at poff[d] = 3 qoff[d]; plen[d] their number. */
+static void naive_programs(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                           const int* qlen, int* prog, int* plen) {
+  for (int d = 0; d < g->P; ++d) {
+    int n = 0, *out = prog + 3 * qoff[d];
+    for (int i = 0; i < qlen[d]; ++i) {
+      const ref_sop o = queue[qoff[d] + i];
+      const int x = cross_producer(g, o.kind, o.s, o.m);
+      if (x >= 0) out[n++] = (PI_RECV << 28) | x;
+      const int y = node_id(g->S, g->M, o.kind, o.s, o.m);
+      out[n++] = (PI_COMP << 28) | y;
+      if (cross_consumer(g, o.kind, o.s, o.m) >= 0) out[n++] = (PI_SEND << 28) | y;
+    }
+    plen[d] = n;
+  }
+}
+
+/*
+ * Deadlock-free, overlap-aware reordering of the communication (§8, "Unified Pipeline Executor"):
+ * each device keeps its compute order, and every transfer is placed at its ideal start — the end
+ * of its producer in the asynchronous schedule (start[] of the plain model), the moment its data
+ * is ready. A device's items are sorted by one global key: (time, communication before
+ * computation, node id), the time of a compute item being its start and of a transfer its
+ * producer's end. The two ends of a transfer get the same key on both devices, so they are
+ * posted together (the smallest communication span the schedule allows) and every program
+ * follows one global order: with positive durations every dependency strictly increases the
+ * key, so no cycle of waits can form.
+ */
+typedef struct {
+  int64_t t;
+  int cls, node, code;
+} prog_key;
+
+static int cmp_prog_key(const void* a, const void* b) {
+  const prog_key *x = (const prog_key*)a, *y = (const prog_key*)b;
+  if (x->t != y->t) return x->t < y->t ? -1 : 1;
+  if (x->cls != y->cls) return x->cls < y->cls ? -1 : 1;
+  return x->node < y->node ? -1 : x->node > y->node;
+}
+
+static void ordered_programs(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                             const int* qlen, const int64_t* start, int* prog, int* plen) {
+  const int S = g->S, M = g->M;
+  int total = 0;
+  for (int d = 0; d < g->P; ++d) total += qlen[d];
+  prog_key* keys = (prog_key*)malloc(sizeof(prog_key) * (size_t)(3 * total + 1));
+  for (int d = 0; d < g->P; ++d) {
+    int n = 0;
+    for (int i = 0; i < qlen[d]; ++i) {
+      const ref_sop o = queue[qoff[d] + i];
+      const int y = node_id(S, M, o.kind, o.s, o.m);
+      keys[n++] = (prog_key){start[y], 1, y, (PI_COMP << 28) | y};
+      const int x = cross_producer(g, o.kind, o.s, o.m);
+      if (x >= 0) {
+        const int xk = x / (S * M), xs = (x / M) % S;
+        keys[n++] = (prog_key){start[x] + op_dur(g, xk, xs), 0, x, (PI_RECV << 28) | x};
+      }
+      if (cross_consumer(g, o.kind, o.s, o.m) >= 0)
+        keys[n++] = (prog_key){start[y] + op_dur(g, o.kind, o.s), 0, y, (PI_SEND << 28) | y};
+    }
+    qsort(keys, (size_t)n, sizeof(prog_key), cmp_prog_key);
+    for (int i = 0; i < n; ++i) prog[3 * qoff[d] + i] = keys[i].code;
+    plen[d] = n;
+  }
+  free(keys);
+}
+
+/*
+ * Evaluate device programs (3 qoff[d] + i, i < plen[d]). Edges: program order on every device;
+ * data edges between stages on one device (weight 0); F(s,m) -> B(s,m); B(s,m) -> W(s,m); a
+ * producer before its transfer and a transfer before its consumer (both also implied by any
+ * program a builder above makes). Longest path by Kahn's algorithm; a cycle is a deadlock.
+ * Busy time counts computation only, so time spent in transfers is bubble.
+ */
+static int simulate_programs(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                             const int* qlen, const int* prog, const int* plen,
+                             int64_t* makespan, int64_t* bubble) {
   int S = g->S, M = g->M, nk = g->split ? 3 : 2;
   int nc = nk * S * M;         /* compute nodes: node_id */
   int nn = nc + 2 * S * M;     /* transfer nodes: nc + (dir * S + producer stage) * M + m */
-  /* successors: at most two program successors (a transfer sits in two programs) + 3 data */
-  int* succ = (int*)malloc(sizeof(int) * (size_t)nn * 5);
+  /* successors: at most two program successors (a transfer sits in two programs) + 4 data */
+  int* succ = (int*)malloc(sizeof(int) * (size_t)nn * 6);
   int* nsucc = (int*)calloc(nn, sizeof(int));
   int* indeg = (int*)calloc(nn, sizeof(int));
   int64_t* dur = (int64_t*)calloc(nn, sizeof(int64_t));
   int64_t* est = (int64_t*)calloc(nn, sizeof(int64_t));
   int64_t* fin = (int64_t*)malloc(sizeof(int64_t) * nn);
   int* ready = (int*)malloc(sizeof(int) * nn);
-  int* seen = (int*)calloc(nc, sizeof(int));
-  int rc = SIM_OK;
-#define RDV_EDGE(a, b) (succ[(size_t)(a) * 5 + nsucc[a]++] = (b), indeg[b]++)
+#define PG_EDGE(a, b) (succ[(size_t)(a) * 6 + nsucc[a]++] = (b), indeg[b]++)
   for (int s = 0; s < S; ++s)
     for (int m = 0; m < M; ++m) {
       for (int k = 0; k < nk; ++k) dur[node_id(S, M, k, s, m)] = op_dur(g, k, s);
@@ -394,75 +484,67 @@ static int simulate_rdv(const ref_dag_in* g, const ref_sop* queue, const int* qo
       if (s > 0 && g->dev[s] != g->dev[s - 1])
         dur[nc + (1 * S + s) * M + m] = g->link[g->dev[s] * g->P + g->dev[s - 1]];
     }
-  /* programs */
-  for (int d = 0; d < g->P && rc == SIM_OK; ++d) {
+  for (int d = 0; d < g->P; ++d) {
     int prev = -1;
-    for (int i = 0; i < qlen[d]; ++i) {
-      ref_sop o = queue[qoff[d] + i];
-      if (o.kind < 0 || o.kind >= nk || o.s < 0 || o.s >= S || o.m < 0 || o.m >= M ||
-          g->dev[o.s] != d || seen[node_id(S, M, o.kind, o.s, o.m)]) {
-        rc = SIM_BADQ;
-        break;
+    for (int i = 0; i < plen[d]; ++i) {
+      const int code = prog[3 * qoff[d] + i], node = code & 0x0FFFFFFF;
+      int item = node;
+      if ((code >> 28) != PI_COMP) {
+        const int xk = node / (S * M), xs = (node / M) % S, xm = node % M;
+        item = nc + ((xk == KF ? 0 : 1) * S + xs) * M + xm;
       }
-      const int y = node_id(S, M, o.kind, o.s, o.m);
-      seen[y] = 1;
-      int tin = -1, tout = -1;
-      if (o.kind == KF) {
-        if (o.s > 0 && g->dev[o.s - 1] != d) tin = nc + (0 * S + o.s - 1) * M + o.m;
-        if (o.s + 1 < S && g->dev[o.s + 1] != d) tout = nc + (0 * S + o.s) * M + o.m;
-      } else if (o.kind == KB) {
-        if (o.s + 1 < S && g->dev[o.s + 1] != d) tin = nc + (1 * S + o.s + 1) * M + o.m;
-        if (o.s > 0 && g->dev[o.s - 1] != d) tout = nc + (1 * S + o.s) * M + o.m;
-      }
-      const int items[3] = {tin, y, tout};
-      for (int k = 0; k < 3; ++k) {
-        if (items[k] < 0) continue;
-        if (prev >= 0) RDV_EDGE(prev, items[k]);
-        prev = items[k];
-      }
+      if (prev >= 0) PG_EDGE(prev, item);
+      prev = item;
     }
   }
-  if (rc == SIM_OK)
-    for (int i = 0; i < nc; ++i)
-      if (!seen[i]) rc = SIM_BADQ;
-  if (rc != SIM_OK) goto done;
-  /* data edges within one device, and F -> B, B -> W */
   for (int s = 0; s < S; ++s)
     for (int m = 0; m < M; ++m) {
-      if (s + 1 < S && g->dev[s] == g->dev[s + 1])
-        RDV_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KF, s + 1, m));
-      if (s > 0 && g->dev[s] == g->dev[s - 1])
-        RDV_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KB, s - 1, m));
-      RDV_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KB, s, m));
-      if (g->split) RDV_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KW, s, m));
+      if (s + 1 < S) {
+        if (g->dev[s] == g->dev[s + 1]) {
+          PG_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KF, s + 1, m));
+        } else {
+          PG_EDGE(node_id(S, M, KF, s, m), nc + (0 * S + s) * M + m);
+          PG_EDGE(nc + (0 * S + s) * M + m, node_id(S, M, KF, s + 1, m));
+        }
+      }
+      if (s > 0) {
+        if (g->dev[s] == g->dev[s - 1]) {
+          PG_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KB, s - 1, m));
+        } else {
+          PG_EDGE(node_id(S, M, KB, s, m), nc + (1 * S + s) * M + m);
+          PG_EDGE(nc + (1 * S + s) * M + m, node_id(S, M, KB, s - 1, m));
+        }
+      }
+      PG_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KB, s, m));
+      if (g->split) PG_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KW, s, m));
     }
-#undef RDV_EDGE
-  int nr = 0, head = 0;
+#undef PG_EDGE
+  int nr = 0, head = 0, rc = SIM_OK;
   for (int i = 0; i < nn; ++i)
     if (indeg[i] == 0) ready[nr++] = i;
   while (head < nr) {
     const int u = ready[head++];
     fin[u] = est[u] + dur[u];
     for (int e = 0; e < nsucc[u]; ++e) {
-      const int x = succ[(size_t)u * 5 + e];
+      const int x = succ[(size_t)u * 6 + e];
       if (fin[u] > est[x]) est[x] = fin[u];
       if (--indeg[x] == 0) ready[nr++] = x;
     }
   }
   if (nr < nn) { /* some node never became ready: a cycle (unused transfer slots have no edges) */
     rc = SIM_CYCLE;
-    goto done;
+  } else {
+    int64_t ms = 0;
+    for (int i = 0; i < nn; ++i)
+      if (fin[i] > ms) ms = fin[i];
+    *makespan = ms;
+    for (int d = 0; d < g->P; ++d) {
+      int64_t busy = 0;
+      for (int i = 0; i < qlen[d]; ++i)
+        busy += op_dur(g, queue[qoff[d] + i].kind, queue[qoff[d] + i].s);
+      bubble[d] = ms - busy;
+    }
   }
-  int64_t ms = 0;
-  for (int i = 0; i < nn; ++i)
-    if (fin[i] > ms) ms = fin[i];
-  *makespan = ms;
-  for (int d = 0; d < g->P; ++d) {
-    int64_t busy = 0;
-    for (int i = 0; i < qlen[d]; ++i) busy += op_dur(g, queue[qoff[d] + i].kind, queue[qoff[d] + i].s);
-    bubble[d] = ms - busy;
-  }
-done:
   free(succ);
   free(nsucc);
   free(indeg);
@@ -470,7 +552,32 @@ done:
   free(est);
   free(fin);
   free(ready);
-  free(seen);
+  return rc;
+}
+
+/* xfer 2: the naive coordination; xfer 3: the reordered one (needs the asynchronous schedule). */
+static int simulate_coordinated(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                                const int* qlen, int ordered, int64_t* makespan,
+                                int64_t* bubble) {
+  int total = 0;
+  for (int d = 0; d < g->P; ++d) total += qlen[d];
+  int* prog = (int*)malloc(sizeof(int) * (size_t)(3 * total + 1));
+  int plen[64];
+  int rc = SIM_OK;
+  if (ordered) {
+    const int nk = g->split ? 3 : 2;
+    int64_t* start = (int64_t*)malloc(sizeof(int64_t) * (size_t)nk * g->S * g->M);
+    int64_t ms0, bub0[64];
+    ref_dag_in plain = *g;
+    plain.serial = 0;
+    rc = simulate(&plain, queue, qoff, qlen, &ms0, bub0, start, NULL);
+    if (rc == SIM_OK) ordered_programs(g, queue, qoff, qlen, start, prog, plen);
+    free(start);
+  } else {
+    naive_programs(g, queue, qoff, qlen, prog, plen);
+  }
+  if (rc == SIM_OK) rc = simulate_programs(g, queue, qoff, qlen, prog, plen, makespan, bubble);
+  free(prog);
   return rc;
 }
 
@@ -725,7 +832,8 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
  * memory [L][2] = {activation bytes per micro-batch, static bytes}; then peak[P] is filled, and
  * ppos[P] (nullable) with the queue position at which each device first reaches its peak (-1
  * when it holds no activations). */
-/* xfer: 0 asynchronous transfers (the plain model), 1 serialised links, 2 blocking rendezvous. */
+/* xfer: 0 asynchronous transfers (the plain model), 1 serialised links, 2 blocking rendezvous in
+ * the naive coordination, 3 blocking rendezvous in the reordered coordination. */
 static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                         const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                         const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos,
@@ -751,8 +859,8 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
   int64_t* start = (mem || comm || bounds)
                        ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M)
                        : NULL;
-  int rc = xfer == 2 ? simulate_rdv(&g, sq, qoff, qlen, ms, bub)
-                       : simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
+  int rc = xfer >= 2 ? simulate_coordinated(&g, sq, qoff, qlen, xfer == 3, ms, bub)
+                     : simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
   if (bounds && rc == SIM_OK) {
     /* per device: start of its first op, end of its last op (0, 0 for an empty queue) */
     for (int d = 0; d < P; ++d) {
@@ -1002,11 +1110,21 @@ int oracle_sim_batch_serial(const ref_problem* pr, const int64_t* costs, const i
                    nthreads);
 }
 
-/* Evaluation with blocking rendezvous transfers (see simulate_rdv). */
+/* Evaluation with blocking rendezvous transfers in the naive coordination (naive_programs). */
 int oracle_sim_batch_rdv(const ref_problem* pr, const int64_t* costs, const int64_t* link,
                          const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                          int nthreads) {
   return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 2, NULL,
+                   nthreads);
+}
+
+/* Evaluation with blocking rendezvous transfers in the reordered coordination (ordered_programs):
+ * deadlocks only where the asynchronous schedule itself deadlocks (-1), or with zero-length
+ * ops that tie the order. */
+int oracle_sim_batch_ordered(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                             const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                             int nthreads) {
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 3, NULL,
                    nthreads);
 }
 

@@ -41,6 +41,9 @@ def lib():
         L.oracle_sim_batch_rdv.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                            ctypes.c_int64, p, p, ctypes.c_int]
         L.oracle_sim_batch_rdv.restype = ctypes.c_int
+        L.oracle_sim_batch_ordered.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
+                                               ctypes.c_int64, p, p, ctypes.c_int]
+        L.oracle_sim_batch_ordered.restype = ctypes.c_int
         L.oracle_sim_batch_bounds.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                               ctypes.c_int64, p, p, p, ctypes.c_int]
         L.oracle_sim_batch_bounds.restype = ctypes.c_int
@@ -124,6 +127,23 @@ def sim_batch_rdv(prob, costs, link, cands, nthreads=1):
                                     _ptr(ms), _ptr(bub), int(nthreads))
     if rc != 0:
         raise ValueError(f"oracle_sim_batch_rdv rejected the arguments (rc={rc})")
+    return ms, bub
+
+
+def sim_batch_ordered(prob, costs, link, cands, nthreads=1):
+    """Evaluate candidate records with blocking rendezvous transfers in the reordered
+    coordination (every transfer at its ideal start in the asynchronous schedule, one global
+    order per device). Returns (makespan[n], bubble[n, P])."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    rc = lib().oracle_sim_batch_ordered(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(cands),
+                                        n, _ptr(ms), _ptr(bub), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch_ordered rejected the arguments (rc={rc})")
     return ms, bub
 
 

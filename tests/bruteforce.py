@@ -57,8 +57,10 @@ def _consumers(op, S, dev):
     return []
 
 
-def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None, serial=False):
-    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock."""
+def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None, serial=False,
+                  starts=None):
+    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock. starts (a dict, optional)
+    receives each op's start tick."""
     total = sum(_dur(k, s, split, Fs, Bs, Ws) for q in queues for (k, s, m) in q)
     if max_ticks is None:
         max_ticks = total + 2 * S * M * (max(max(r) for r in link) if P > 0 else 0) + 2
@@ -94,6 +96,8 @@ def tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, max_ticks=None,
                 ok = all(delivered(p, w, op, t) for p, w in _producers(op, S, split, dev, link))
                 if ok:
                     running[d] = op
+                    if starts is not None:
+                        starts[op] = t
                     busy_until[d] = t + _dur(op[0], op[1], split, Fs, Bs, Ws)
                     ptr[d] += 1
                     if busy_until[d] == t:  # zero-length op finishes immediately
@@ -129,9 +133,37 @@ def rdv_programs(S, dev, queues):
     return progs
 
 
-def rdv_tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues):
-    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock."""
-    progs = rdv_programs(S, dev, queues)
+def ordered_programs(S, M, split, dev, Fs, Bs, Ws, queues, starts):
+    """The reordered coordination: a device keeps its compute order and places each transfer at
+    the end of its producer in the asynchronous schedule (starts: op -> start); its items are
+    sorted by (time, communication first, node id), node id = (kind S + stage) M + m, a
+    transfer named by its producer."""
+    node = lambda op: (op[0] * S + op[1]) * M + op[2]
+    end = lambda op: starts[op] + _dur(op[0], op[1], split, Fs, Bs, Ws)
+    progs = []
+    for d, q in enumerate(queues):
+        items = []
+        for op in q:
+            kind, s, m = op
+            items.append(((starts[op], 1, node(op)), ("c", op)))
+            src = None
+            if kind == F and s > 0 and dev[s - 1] != d:
+                src = (F, s - 1, m)
+            if kind == B and s < S - 1 and dev[s + 1] != d:
+                src = (B, s + 1, m)
+            if src is not None:
+                items.append(((end(src), 0, node(src)), ("r", src)))
+            if _consumers(op, S, dev):
+                items.append(((end(op), 0, node(op)), ("s", op)))
+        progs.append([it for _, it in sorted(items)])
+    return progs
+
+
+def rdv_tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, progs=None):
+    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock. progs: the device programs
+    (default: the naive coordination)."""
+    if progs is None:
+        progs = rdv_programs(S, dev, queues)
     total = sum(_dur(k, s, split, Fs, Bs, Ws) for q in queues for (k, s, m) in q)
     max_ticks = total + sum(max(r) for r in link) * 2 * S * M + 2
     ptr = [0] * P
@@ -161,6 +193,8 @@ def rdv_tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues):
                         running[d] = ("c", x)
                         busy_until[d] = t + _dur(x[0], x[1], split, Fs, Bs, Ws)
                         changed = True
+                elif what == "s" and not (x in fin and fin[x] <= t):
+                    pass                       # a send waits for its producer
                 elif what not in arrived.setdefault(x, set()):
                     arrived[x].add(what)
                     if arrived[x] == {"s", "r"}:

@@ -118,3 +118,97 @@ def test_invariants():
     p1 = R.problem(20, 1, 3, 8, one.shape[1], 0)
     l1 = np.zeros((1, 1), np.int64)
     assert (R.sim_batch(p1, costs, l1, one)[0] == R.sim_batch_rdv(p1, costs, l1, one)[0]).all()
+
+
+# ---------------------------------------------------------------------------------------------
+# The reordered coordination (deadlock-free, overlap-aware reordering of the communication,
+# §8 "Unified Pipeline Executor"): each transfer at its ideal start in the asynchronous schedule.
+# ---------------------------------------------------------------------------------------------
+
+def test_ordered_worked_example():
+    kv, _ = read_golden("rdv_worked_example.txt")
+    T = int(kv["T_ns"])
+    recs = I.pack_records(2, 1, 0, [I.POLICY["AFAB"], I.POLICY["1F1B"]], [1, 1], [[1], [1]],
+                          [[0, 1], [0, 1]])
+    prob = R.problem(2, 2, 1, 2, recs.shape[1], 0)
+    costs = np.array([[2, 2, 2], [4, 4, 4]], np.int64) * T
+    link = I.link_matrix(2, int(kv["transfer_T"]) * T)
+    ms, bub = R.sim_batch_ordered(prob, costs, link, recs)
+    assert ms[0] == int(kv["ordered_gpipe_makespan_T"]) * T
+    assert ms[1] == int(kv["ordered_1f1b_makespan_T"]) * T
+    assert bub[1].tolist() == [int(kv["ordered_1f1b_bubble0_T"]) * T,
+                               int(kv["ordered_1f1b_bubble1_T"]) * T]
+
+
+@pytest.mark.parametrize("P,M", [(2, 2), (2, 5), (3, 2), (4, 8), (8, 8), (8, 64)])
+@pytest.mark.parametrize("pol", ["1F1B", "ZB", "I1F1B"])
+def test_ordered_removes_the_deadlock(P, M, pol):
+    """Where the naive coordination deadlocks (1F1B's crossing sends), the reordered one runs,
+    and no faster than the asynchronous schedule."""
+    plain, (naive, _) = chain(P, M, I.POLICY[pol], 1000, 2000, 300, 500)
+    recs = I.pack_records(P, 1, 0, [I.POLICY[pol]], [1], [np.arange(1, P)], [np.arange(P)])
+    prob = R.problem(P, P, 1, M, recs.shape[1], 0)
+    costs = np.tile(np.array([[1000, 2000, 500]], np.int64), (P, 1))
+    ms, _ = R.sim_batch_ordered(prob, costs, I.link_matrix(P, 300), recs)
+    assert naive[0] == -1 and ms[0] >= plain > 0
+
+
+def test_ordered_tick_execution_tiny():
+    """Random tiny candidates: reordered programs built independently (from a tick-by-tick
+    asynchronous run) and executed tick by tick with blocking transfers, against the oracle
+    (links may cost nothing)."""
+    rng = np.random.default_rng(41)
+    checked = alive = 0
+    for trial in range(70):
+        P = int(rng.integers(1, 4))
+        v_max = int(rng.integers(1, 3))
+        M = int(rng.integers(1, 4))
+        L = P * v_max + int(rng.integers(0, 3))
+        recs = I.random_candidates(rng, L, P, v_max, M, 8, max_pert=2, pert_rate=0.5)
+        prob = R.problem(L, P, v_max, M, recs.shape[1], 2)
+        # ops of at least one tick: the asynchronous tick run is exact only for those
+        costs = rng.integers(1, 5, size=(L, 3)).astype(np.int64)
+        link = rng.integers(0, 6, size=(P, P)).astype(np.int64)
+        ms, bub = R.sim_batch_ordered(prob, costs, link, recs)
+        for i in range(len(recs)):
+            q = R.dump_queues(prob, recs[i])
+            if q is None:
+                assert ms[i] == -2
+                continue
+            c = I.unpack_record(recs[i], P, v_max, 2)
+            b = c["b"] + [L]
+            S = len(c["dev"])
+            Fs = [int(costs[b[s]:b[s + 1], 0].sum()) for s in range(S)]
+            Bs = [int(costs[b[s]:b[s + 1], 1].sum()) for s in range(S)]
+            Ws = [int(costs[b[s]:b[s + 1], 2].sum()) for s in range(S)]
+            split = c["policy"] == I.POLICY["ZB"]
+            starts = {}
+            ams, _ = BF.tick_simulate(P, S, M, split, c["dev"], Fs, Bs, Ws, link.tolist(), q,
+                                      starts=starts)
+            if ams == -1:
+                assert ms[i] == -1
+                continue
+            progs = BF.ordered_programs(S, M, split, c["dev"], Fs, Bs, Ws, q, starts)
+            tms, tbub = BF.rdv_tick_simulate(P, S, M, split, c["dev"], Fs, Bs, Ws,
+                                             link.tolist(), q, progs)
+            assert ms[i] == tms and list(bub[i]) == tbub, (trial, i)
+            checked += 1
+            alive += tms > 0
+    assert checked > 250 and alive > 200
+
+
+def test_ordered_never_deadlocks_with_positive_costs():
+    """With every op and transfer taking time, every dependency strictly increases the global
+    key, so the reordered programs never deadlock unless the compute orders themselves do; and
+    blocking transfers never beat asynchronous ones."""
+    rng = np.random.default_rng(43)
+    for (L, P, v, M) in [(20, 4, 2, 8), (24, 8, 1, 16), (30, 3, 3, 6)]:
+        recs = I.random_candidates(rng, L, P, v, M, 300, max_pert=3, pert_rate=0.4)
+        prob = R.problem(L, P, v, M, recs.shape[1], 3)
+        costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+        link = rng.integers(1, 2_000_000, size=(P, P)).astype(np.int64)
+        ms, _ = R.sim_batch(prob, costs, link, recs, NTHREADS)
+        os_, ob = R.sim_batch_ordered(prob, costs, link, recs, NTHREADS)
+        assert ((ms < 0) == (os_ < 0)).all() and (os_[ms < 0] == ms[ms < 0]).all()
+        ok = ms > 0
+        assert (os_[ok] >= ms[ok]).all() and (ob[ok] >= 0).all() and ok.sum() > 100
