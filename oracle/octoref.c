@@ -438,7 +438,7 @@ static void ordered_programs(const ref_dag_in* g, const ref_sop* queue, const in
     for (int i = 0; i < qlen[d]; ++i) {
       const ref_sop o = queue[qoff[d] + i];
       const int y = node_id(S, M, o.kind, o.s, o.m);
-      keys[n++] = (prog_key){start[y], 1, y, (PI_COMP << 28) | y};
+      keys[n++] = (prog_key){start[y], 1, i, (PI_COMP << 28) | y}; /* ties: queue order */
       const int x = cross_producer(g, o.kind, o.s, o.m);
       if (x >= 0) {
         const int xk = x / (S * M), xs = (x / M) % S;

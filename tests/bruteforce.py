@@ -136,16 +136,16 @@ def rdv_programs(S, dev, queues):
 def ordered_programs(S, M, split, dev, Fs, Bs, Ws, queues, starts):
     """The reordered coordination: a device keeps its compute order and places each transfer at
     the end of its producer in the asynchronous schedule (starts: op -> start); its items are
-    sorted by (time, communication first, node id), node id = (kind S + stage) M + m, a
-    transfer named by its producer."""
+    sorted by (time, communication first, then the producer's node id (kind S + stage) M + m
+    for a transfer or the queue position for a computation)."""
     node = lambda op: (op[0] * S + op[1]) * M + op[2]
     end = lambda op: starts[op] + _dur(op[0], op[1], split, Fs, Bs, Ws)
     progs = []
     for d, q in enumerate(queues):
         items = []
-        for op in q:
+        for i, op in enumerate(q):
             kind, s, m = op
-            items.append(((starts[op], 1, node(op)), ("c", op)))
+            items.append(((starts[op], 1, i), ("c", op)))
             src = None
             if kind == F and s > 0 and dev[s - 1] != d:
                 src = (F, s - 1, m)
