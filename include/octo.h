@@ -190,6 +190,25 @@ int octo_sim_batch_rdv(const octo_problem* prob, const int64_t* layer_costs, con
                        int64_t* out_bubble, void* stream);
 
 /*
+ * octo_sim_batch_ordered — blocking rendezvous transfers (as octo_sim_batch_rdv) in the
+ * deadlock-free, overlap-aware reordered coordination of §8 ("Unified Pipeline Executor":
+ * reorder the communication operations to break cyclic waits while keeping transfers beside
+ * the computation around them). Each device keeps its compute order; every transfer is placed at
+ * its ideal start, the end of its producer in the asynchronous schedule of octo_sim_batch, where
+ * its data becomes ready, so its send and receive are posted together. A device's program is
+ * its items sorted by (time, communication before computation, then the producer's (kind,
+ * stage, m) for a transfer or the queue position for a computation), a computation's time
+ * being its asynchronous start; a send also waits for its producer. Both ends of a transfer get
+ * one key, so all programs follow one global order: with positive op durations no cycle of
+ * waits can form, and the candidate deadlocks (OCTO_MS_DEADLOCK) only if its compute orders do
+ * (or zero-length ops tie the order). Busy time counts computation only. Arguments, results and
+ * status as octo_sim_batch.
+ */
+int octo_sim_batch_ordered(const octo_problem* prob, const int64_t* layer_costs,
+                           const int64_t* link, const void* candidates, int64_t n,
+                           int64_t* out_makespan, int64_t* out_bubble, void* stream);
+
+/*
  * octo_advance_w — selective W advancing (§6 "Scheduling Tuning", third policy) under the
  * per-device capacity of §6 Eq. 2, on a batch of candidate records. For each record, after its
  * queues are generated and its moves applied: while some device's peak (as octo_sim_batch_mem)

@@ -49,6 +49,7 @@ def lib():
         L.octo_sim_batch_comm.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_serial.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
         L.octo_sim_batch_rdv.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
+        L.octo_sim_batch_ordered.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
         L.octo_sim_batch_bounds.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_mem.restype = ctypes.c_int
         L.octo_tune_step.argtypes = [pp, vp, vp, vp, vp, i64, ctypes.c_uint64, i32, vp]
@@ -176,6 +177,25 @@ def sim_batch_rdv(prob, layer_costs, link, candidates, out_makespan=None, out_bu
         _dev_ptr(out_makespan, torch.int64, "out_makespan"),
         _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_rdv")
+    return out_makespan, out_bubble
+
+
+def sim_batch_ordered(prob, layer_costs, link, candidates, out_makespan=None, out_bubble=None,
+                      stream=None):
+    """octo_sim_batch_ordered: blocking rendezvous transfers in the reordered coordination
+    (every transfer at its ideal start in the asynchronous schedule)."""
+    n = candidates.shape[0]
+    dev = candidates.device
+    if out_makespan is None:
+        out_makespan = torch.empty(n, dtype=torch.int64, device=dev)
+    if out_bubble is None:
+        out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    rc = lib().octo_sim_batch_ordered(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+    _check(rc, "octo_sim_batch_ordered")
     return out_makespan, out_bubble
 
 

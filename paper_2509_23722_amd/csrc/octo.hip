@@ -1069,6 +1069,290 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// Deadlock-free reordered coordination (§8 "Unified Pipeline Executor"): every device keeps its
+// compute order and places each transfer at its ideal start — its producer's end in the
+// asynchronous schedule — with blocking rendezvous transfers. A device's program is its items
+// sorted by (time, communication before computation, then the producer's id (kind, stage, m) for
+// a transfer or the queue position for a computation); a compute item's time is its start.
+// One group per candidate (lane = device), queues materialised, 64-bit finish table:
+//   A. the plain rounds, recording each op's finish (by node) in the slot's time buffer;
+//   B. each lane builds its program: computations and sends come in queue order already, its
+//      receives (keyed by their producers' ends) are insertion-sorted, then the three merge;
+//   C. rounds over the programs: a send first announces itself in the sender's outbox (once its
+//      producer has finished), the receiver matches it, takes the transfer from max(sender's
+//      announce time, its own clock) for the link time and posts the end to the sender's
+//      mailbox; the sender resumes from there.
+// ---------------------------------------------------------------------------------------------
+constexpr uint32_t PI_COMP = 0, PI_SEND = 1, PI_RECV = 2;
+// program item: type << 30 | op kind << 28 | stage << 16 | m; a transfer is named by its producer
+__device__ __forceinline__ uint32_t pitem(uint32_t type, int kind, int s, int m) {
+  return type << 30 | (uint32_t)kind << 28 | (uint32_t)s << 16 | (uint32_t)m;
+}
+constexpr int32_t OB_NONE = -1;
+
+// Per-slot scratch of k_ordered.
+struct OrdBufs {
+  int64_t* tb;      // [slot][3 S_max M] finish time of each op
+  int64_t* rkey;    // [slot][P][rcap] receive keys (producer end)
+  uint32_t* rid;    // [slot][P][rcap] receive producers (pitem with type 0)
+  uint32_t* prog;   // [slot][P][pcap] programs
+  int rcap, pcap;
+};
+
+// (t, cls, tie) < (t', cls', tie')
+__device__ __forceinline__ bool key_less(int64_t t, uint32_t cls, uint32_t tie, int64_t t2,
+                                         uint32_t cls2, uint32_t tie2) {
+  return t != t2 ? t < t2 : cls != cls2 ? cls < cls2 : tie < tie2;
+}
+
+// The local chunk of stage s (hosted by this device; unused chunk slots hold stage 0, so only
+// the device's v chunks are searched).
+template <int VMAX>
+__device__ __forceinline__ int chunk_of(const Chunks<VMAX>& c, int s, int v) {
+  int k = 0;
+#pragma unroll
+  for (int i = 0; i < VMAX; ++i) k = (i < v && c.st[i] == s) ? i : k;
+  return k;
+}
+
+// Phase B for lane d: returns the program length.
+template <int VMAX>
+__device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16_t* row, int nq,
+                                             const int64_t* tb, int S, int M, int64_t* rkey,
+                                             uint32_t* rid, uint32_t* prog) {
+  auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
+  auto dur_of = [&](int kind, int k) {
+    return kind == KF ? pick<VMAX>(c.dF, k) : kind == KB ? pick<VMAX>(c.dB, k) : pick<VMAX>(c.dW, k);
+  };
+  // receives in queue order, insertion-sorted by (producer end, producer)
+  int nr = 0;
+  for (int i = 0; i < nq; ++i) {
+    const uint32_t e = row[i];
+    const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+    const int s = pick<VMAX>(c.st, k);
+    const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
+    if (!(cx & CX_IN)) continue;
+    const int ps = kind == KF ? s - 1 : s + 1;
+    const int64_t key = tb[node(kind, ps, m)];
+    const uint32_t id = pitem(0, kind, ps, m);
+    int j = nr++;
+    while (j > 0 && key_less(key, 0, id, rkey[j - 1], 0, rid[j - 1])) {
+      rkey[j] = rkey[j - 1];
+      rid[j] = rid[j - 1];
+      --j;
+    }
+    rkey[j] = key;
+    rid[j] = id;
+  }
+  // merge: computations (queue order), sends (queue order), receives (sorted)
+  int ci = 0, si = 0, ri = 0, n = 0;
+  int64_t sk = 0;
+  uint32_t sid = 0;
+  auto next_send = [&]() {
+    while (si < nq) {
+      const uint32_t e = row[si];
+      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
+      if (cx & CX_OUT) {
+        const int s = pick<VMAX>(c.st, k);
+        sk = tb[node(kind, s, m)];
+        sid = pitem(0, kind, s, m);
+        return;
+      }
+      ++si;
+    }
+  };
+  next_send();
+  while (ci < nq || si < nq || ri < nr) {
+    int64_t ck = 0;
+    uint32_t citem = 0;
+    if (ci < nq) {
+      const uint32_t e = row[ci];
+      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      const int s = pick<VMAX>(c.st, k);
+      ck = tb[node(kind, s, m)] - dur_of(kind, k);
+      citem = pitem(PI_COMP, kind, s, m);
+    }
+    // the smallest of the three heads
+    int pick_src = ci < nq ? 0 : -1;
+    int64_t bt = ck;
+    uint32_t bc = 1, bt2 = (uint32_t)ci;
+    if (si < nq && (pick_src < 0 || key_less(sk, 0, sid, bt, bc, bt2)))
+      pick_src = 1, bt = sk, bc = 0, bt2 = sid;
+    if (ri < nr && (pick_src < 0 || key_less(rkey[ri], 0, rid[ri], bt, bc, bt2)))
+      pick_src = 2, bt = rkey[ri], bc = 0, bt2 = rid[ri];
+    if (pick_src == 0) {
+      prog[n++] = citem;
+      ++ci;
+    } else if (pick_src == 1) {
+      prog[n++] = (PI_SEND << 30) | sid;
+      ++si;
+      next_send();
+    } else {
+      prog[n++] = (PI_RECV << 30) | rid[ri];
+      ++ri;
+    }
+  }
+  return n;
+}
+
+template <int VMAX>
+__global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int64_t mbox[WAVE];    // transfer end posted by the receiver, per sender lane
+  __shared__ int64_t obt[WAVE];     // outbox: the sender's announce time ...
+  __shared__ int32_t obn[WAVE];     // ... and its producer (OB_NONE: nothing announced)
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  const int me = lane_id(), g0 = me - d;
+  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
+  const Table64 T{reinterpret_cast<int64_t*>(lds_group)};
+  uint8_t* rec = lds_group + a.table_bytes;
+  const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
+  const int dl = d < P ? d : 0;
+  uint16_t* row = a.qscratch + ((size_t)slot * P + dl) * a.qcap;
+  int64_t* tb = ob.tb + (size_t)slot * 3 * a.pr.s_max * M;
+  int64_t* rkey = ob.rkey + ((size_t)slot * P + dl) * ob.rcap;
+  uint32_t* rid = ob.rid + ((size_t)slot * P + dl) * ob.rcap;
+  uint32_t* prog = ob.prog + ((size_t)slot * P + dl) * ob.pcap;
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < a.n; base += n_groups) {
+    const int64_t cand = base + g;
+    const bool has = g < a.CPW && cand < a.n;
+    const uint8_t* grec = a.cands + (has ? cand : 0) * a.pr.stride;
+    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
+    __syncthreads();
+    Resolved r;
+    r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
+    if (has) r = resolve_record(a.pr, grec);
+    const bool run = has && r.valid;
+    const bool mine = run && d < P;
+    const int v = run ? r.v : 1;
+    const int S = P * v;
+    const Ring ring = make_ring(M, M);
+    Chunks<VMAX> c;
+    int64_t busy = 0;
+    Lane L;
+    L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
+    L.cm.reset();
+    L.fs = -1;
+    L.tb = tb, L.tS = S, L.tM = M;
+    if (mine) {
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, nullptr,
+                                nullptr, XR);
+      L.nops = materialise<VMAX>(a, c, v, r.gen, r.split, row);
+      const uint8_t* pp = grec + pert_off(a.pr.s_max);
+      for (int i = 0; i < r.n_pert; ++i) {
+        const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
+        if (pd != d) continue;
+        move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
+      }
+    } else {
+      zero_chunks<VMAX>(c);
+    }
+    if (run) T.clear(S * M, d, G);
+    __syncthreads();
+    // A: the asynchronous schedule, finish times recorded
+    bool dead = false;
+    {
+      GenMat q;
+      q.init(row, L.nops);
+      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+      relax<VMAX, true, XT>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    }
+    __syncthreads();  // every lane's finish times visible to the group
+    // B: programs
+    int plen = 0;
+    if (mine && !dead) plen = build_program<VMAX>(c, row, L.nops, tb, S, M, rkey, rid, prog);
+    if (run) T.clear(S * M, d, G);
+    mbox[me] = RDV_EMPTY;
+    obn[me] = OB_NONE;
+    obt[me] = 0;
+    __syncthreads();
+    // C: rounds over the programs
+    int64_t clock = 0;
+    bool cdead = false;
+    if (!dead) {
+      const uint8_t* devs = rec + 3 + a.pr.s_max;
+      int pos = 0;
+      bool live = pos < plen, arrived = false;
+      // the current item, decoded
+      uint32_t type = 0, tag = 0;
+      int rd = 0, wr = 0, store = 0, src = 0;
+      uint32_t mask = 0, want = 0, state = 0;
+      int64_t w = 0, dur = 0;
+      auto decode = [&]() {
+        const uint32_t it = live ? prog[pos] : 0u;
+        type = it >> 30;
+        const int kind = (int)((it >> 28) & 3u), s = (int)((it >> 16) & 63u), m = (int)(it & 0x7FFu);
+        tag = it & 0x3FFFFFFFu;
+        if (type == PI_COMP) {
+          Desc D;
+          describe<VMAX>(D, c, ring, kind, chunk_of<VMAX>(c, s, v), m);
+          rd = D.rd, wr = D.wr, store = D.store, mask = (uint32_t)D.mask, want = (uint32_t)D.want;
+          state = D.state, w = D.w, dur = D.dur;
+        } else if (type == PI_SEND) {  // its producer (an own op) must have finished
+          rd = s * M + m;
+          mask = want = kind == KF ? ST_F : ST_B;
+        } else {  // receive: the producer's device and the consumer's link weight
+          src = devs[s];
+          const int cs = kind == KF ? s + 1 : s - 1;
+          const int ck = chunk_of<VMAX>(c, cs, v);
+          w = kind == KF ? pick<VMAX>(c.wF, ck) : pick<VMAX>(c.wB, ck);
+        }
+      };
+      decode();
+      for (;;) {
+        uint32_t plo, phi;
+        T.issue(live && type != PI_RECV ? rd : 0, plo, phi);
+        const int64_t box = mbox[me];
+        const int32_t on = obn[g0 + (type == PI_RECV ? src : 0)];
+        const int64_t ot = obt[g0 + (type == PI_RECV ? src : 0)];
+        const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
+        const bool rdy = (plo & mask) == want;
+        const bool okC = live && type == PI_COMP && rdy;
+        const int64_t tin = (int64_t)(p >> 3) + w;
+        const int64_t st = tin > clock ? tin : clock;
+        const int64_t fin = st + dur;
+        const bool okSA = live && type == PI_SEND && !arrived && rdy;
+        const bool okSD = live && type == PI_SEND && arrived && box != RDV_EMPTY;
+        const bool okR = live && type == PI_RECV && on == (int32_t)tag;
+        const int64_t xend = (ot > clock ? ot : clock) + w;
+        if (okC && store) T.store(wr, ((uint64_t)fin << 3) | state);
+        if (okSA) obn[me] = (int32_t)tag, obt[me] = clock;
+        if (okSD) mbox[me] = RDV_EMPTY, obn[me] = OB_NONE;
+        if (okR) mbox[g0 + src] = xend;
+        clock = okC ? fin : okSD ? box : okR ? xend : clock;
+        arrived = okSA ? true : okSD ? false : arrived;
+        const bool done = okC || okSD || okR;
+        pos += done ? 1 : 0;
+        live = pos < plen;
+        if (done) decode();
+        __asm__ volatile("" ::: "memory");
+        if (__ballot(okC || okSA || okSD || okR) == 0) {
+          const uint64_t actm = __ballot(live);
+          if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) cdead = true;
+          break;
+        }
+      }
+    }
+    const int64_t ms = group_max(clock, G);
+    if (mine) {
+      const int64_t sv = dead || cdead ? (int64_t)OCTO_MS_DEADLOCK : 0;
+      if (d == 0) a.out_ms[cand] = sv ? sv : ms;
+      a.out_bub[cand * P + d] = sv ? sv : ms - busy;
+    } else if (has && !run && d < P) {
+      if (d == 0) a.out_ms[cand] = OCTO_MS_INVALID;
+      a.out_bub[cand * P + d] = OCTO_MS_INVALID;
+    }
+    __syncthreads();  // before the next candidate reuses the staged record and the tables
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Selective W advancing (§6 "Scheduling Tuning", third policy) under per-device capacities
 // (§6 Eq. 2). While a device's peak exceeds its capacity, take the lowest such device d and
 // the queue position p at which its running activation total first reaches the peak (an F).
@@ -1818,6 +2102,9 @@ struct Workspace {
   // Algorithm 1: search state and each iteration's neighbour batch
   void* a1 = nullptr;
   size_t a1_bytes = 0;
+  // reordered coordination: per-slot finish times, receive lists and programs
+  void* ord = nullptr;
+  size_t ord_bytes = 0;
 };
 
 std::mutex g_mu;
@@ -2542,6 +2829,59 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   return OCTO_OK;
 }
 
+
+// The reordered coordination behind octo_sim_batch_ordered: k_ordered over all records, one
+// group per candidate, its scratch sized for the materialised-queue grid's group slots.
+template <int VC>
+int launch_ordered(const octo_problem* prob, const Setup& su, const int64_t* link,
+                   const void* cands, int64_t n, int64_t* ms, int64_t* bub, hipStream_t stream) {
+  SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
+  int grid = 0;
+  int rc = occupancy_grid(k_ordered<VC>, su.big.lds_bytes, su.di.cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (n + su.big.CPW - 1) / su.big.CPW;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min(grid, su.mat_grid), need));
+  const size_t slots = (size_t)su.mat_grid * su.big.CPW;
+  OrdBufs ob;
+  ob.rcap = 2 * prob->v_max * prob->M;
+  ob.pcap = 7 * prob->v_max * prob->M;
+  size_t o = 0;
+  const size_t o_tb = o;
+  o = align_up(o + slots * 3 * prob->P * prob->v_max * prob->M * 8, 256);
+  const size_t o_rk = o;
+  o = align_up(o + slots * prob->P * ob.rcap * 8, 256);
+  const size_t o_ri = o;
+  o = align_up(o + slots * prob->P * ob.rcap * 4, 256);
+  const size_t o_pg = o;
+  o = align_up(o + slots * prob->P * ob.pcap * 4, 256);
+  if ((rc = ensure_buf(su.ws->ord, su.ws->ord_bytes, o, stream))) return rc;
+  char* base = static_cast<char*>(su.ws->ord);
+  ob.tb = reinterpret_cast<int64_t*>(base + o_tb);
+  ob.rkey = reinterpret_cast<int64_t*>(base + o_rk);
+  ob.rid = reinterpret_cast<uint32_t*>(base + o_ri);
+  ob.prog = reinterpret_cast<uint32_t*>(base + o_pg);
+  hipLaunchKernelGGL(k_ordered<VC>, dim3(grid), dim3(WAVE), su.big.lds_bytes, stream, a, ob);
+  return launch_ok();
+}
+
+int ordered_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                 const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
+                 hipStream_t stream) {
+  int rc = check_problem(prob);
+  if (rc) return rc;
+  if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
+  if (n == 0) return OCTO_OK;
+  if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
+  std::lock_guard<std::mutex> lock(g_mu);
+  Setup su;
+  rc = prepare(prob, layer_costs, nullptr, stream, 0, &su);
+  if (rc) return rc;
+  return prob->v_max <= 2
+             ? launch_ordered<2>(prob, su, link, candidates, n, out_makespan, out_bubble, stream)
+             : launch_ordered<8>(prob, su, link, candidates, n, out_makespan, out_bubble, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -2598,6 +2938,13 @@ int octo_sim_batch_rdv(const octo_problem* prob, const int64_t* layer_costs, con
                        int64_t* out_bubble, void* stream) {
   return sim_batch_impl<XR>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
                             out_bubble, Extra{}, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_ordered(const octo_problem* prob, const int64_t* layer_costs,
+                           const int64_t* link, const void* candidates, int64_t n,
+                           int64_t* out_makespan, int64_t* out_bubble, void* stream) {
+  return ordered_impl(prob, layer_costs, link, candidates, n, out_makespan, out_bubble,
+                      static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_bounds(const octo_problem* prob, const int64_t* layer_costs,

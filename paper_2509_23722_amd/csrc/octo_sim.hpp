@@ -43,7 +43,8 @@ constexpr uint32_t ST_B = 1, ST_F = 2, ST_PAR = 4;
 // device's first start and last finish (its leading and trailing idle).
 // XR: blocking rendezvous transfers (a device receives an op's cross-device input right before
 // the op and sends its cross-device output right after it; a transfer holds both devices).
-constexpr int XP = 0, XM = 1, XC = 2, XS = 3, XB = 4, XR = 5;
+// XT: the plain times, each op's finish recorded by node id (L.tb) for building programs.
+constexpr int XP = 0, XM = 1, XC = 2, XS = 3, XB = 4, XR = 5, XT = 6;
 // Weight of a weight-gradient op's read under serialised links: its B is on its own device and
 // earlier in its queue, so only the readiness bit matters, not the (possibly delayed) slot time.
 constexpr int64_t W_NO_TIME = -((int64_t)1 << 50);
@@ -194,6 +195,8 @@ struct Lane : Desc {
   int64_t lf[16];     // serialised links: when the link to device dst is free, per stream
                       // (forward outputs of chunk k at k, backward outputs at VMAX + k)
   int64_t fs;         // start of the device's first op (-1 before it), bounds variants
+  int64_t* tb;        // XT: finish time of every op, at (kind * tS + stage) * tM + m
+  int tS, tM;
 };
 
 template <int VMAX, typename T>
@@ -292,6 +295,9 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
       rec[L.pos] = ((uint32_t)st << 16) | ((uint32_t)gen.kind << 12) | (uint32_t)gen.m;
     if constexpr (X == XC) L.cm.op(ok, L.cx, tin, L.w, L.clock, st, fin, L.cout);
     if constexpr (X == XB) L.fs = (ok && L.fs < 0) ? st : L.fs;
+    if constexpr (X == XT) {
+      if (ok) L.tb[(gen.kind * L.tS + pick<VMAX>(c.st, gen.k)) * L.tM + gen.m] = fin;
+    }
     L.clock = ok ? fin : L.clock;
     if constexpr (X == XM) {
       L.mem = ok ? L.mem + L.dm : L.mem;
