@@ -77,13 +77,20 @@ def copy_calibration(torch):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}), flush=True)
 
 
-def time_variant(torch, _lib, call, n, steps, warmup):
+def time_variant(torch, _lib, call, n, steps, warmup, kernels=True):
     """Time `call` (one batch evaluation) like the headline: wall clock over `steps` calls after
-    `warmup`, and each simulation kernel by the library's HIP events. Returns (candidates/s,
-    ms per call, {kernel: ms})."""
+    `warmup`, and (kernels) each simulation kernel by the library's HIP events, which only the
+    batch-evaluation entry points record. Returns (candidates/s, ms per call, {kernel: ms})."""
     for _ in range(warmup):
         call()
     torch.cuda.synchronize()
+    if not kernels:
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            call()
+        torch.cuda.synchronize()
+        secs = time.perf_counter() - t0
+        return round(n * steps / secs, 1), round(secs / steps * 1e3, 4), {}
     nb = len(SIM_KERNELS) + 1
     hip, evs = hip_events(nb * steps)
     torch.cuda.synchronize()
@@ -343,6 +350,19 @@ def main():
     rendezvous = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "sim_kernels_ms": k_,
                   "deadlocked": int((r_np == -1).sum()), "completed": int((r_np > 0).sum())}
 
+    # the reordered coordination (deadlock-free): every 16th candidate of the batch
+    sub = recs[::16].contiguous()
+    ns = sub.shape[0]
+    oms = torch.empty(ns, dtype=torch.int64, device=dev)
+    obub = torch.empty((ns, w.P), dtype=torch.int64, device=dev)
+    v_, t_, _ = time_variant(
+        torch, _lib, lambda: _lib.sim_batch_ordered(prob, costs, link, sub, oms, obub), ns,
+        args.steps, args.warmup, kernels=False)
+    o_np = oms.cpu().numpy()
+    ordered = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "candidates": ns,
+               "sample": "every 16th candidate of the batch", "deadlocked": int((o_np == -1).sum()),
+               "mean_slowdown_vs_async": round(float((o_np / ms[::16].cpu().numpy()).mean()), 4)}
+
     gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
                                args.warmup, min(args.steps, 3), not args.no_cpu)
@@ -380,6 +400,7 @@ def main():
         "comm_model": comm_model,
         "serial_links": serial_links,
         "rendezvous": rendezvous,
+        "ordered": ordered,
         "w_advance": w_advance,
         "alg1": alg1,
     }
