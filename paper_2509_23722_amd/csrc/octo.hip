@@ -34,7 +34,7 @@ constexpr int WAVE = 64;
 // Workspace control block (int32 words).
 constexpr int CTL_COUNTS = 0;     // [NBINS] candidates per bin
 constexpr int CTL_START = 192;    // [NBINS] first index position of each bin
-constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (5)
+constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (7)
 constexpr int CTL_WORK_MAT = 136; // chunk counter of k_sim_mat, perturbed list
 constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
 constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
@@ -52,7 +52,6 @@ struct SimArgs {
   const uint8_t* cands;
   int64_t n;
   const int32_t* n_live;  // nullable: only the first *n_live of the n records are evaluated
-  int afab_mat;           // GPipe queues take the materialised path (rendezvous calls)
   int64_t* out_ms;
   int64_t* out_bub;
   int32_t* ctl;
@@ -582,8 +581,7 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
       if (a.out_bound)
         for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
     } else {
-      bin = (r.n_pert > 0 || (a.afab_mat && r.gen == GEN_AFAB)) ? BIN_MAT
-                                                                 : bin_of(r.v, r.gen, r.split);
+      bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
     }
     bins[i] = (uint8_t)bin;
   }
@@ -647,6 +645,12 @@ template <int VMAX, int X>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
                                              int split, uint8_t* lds_wave, int64_t* mbox) {
   const bool p2 = (a.pr.P & (a.pr.P - 1)) == 0 && (v & (v - 1)) == 0;
+  if constexpr (X == XR) {  // rendezvous: GPipe queues run here too, with full rows
+    if (gen == GEN_AFAB) {
+      run_generated<VMAX, GEN_AFAB, false, X>(a, cand, v, split, lds_wave, mbox);
+      return;
+    }
+  }
   if (gen == GEN_MERGE)
     run_generated<VMAX, GEN_MERGE, false, X>(a, cand, v, split, lds_wave, mbox);
   else if (p2)
@@ -676,7 +680,7 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
     const int cnt = a.ctl[CTL_COUNTS + bin];
     const int e = entry0 + g;
     const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
-    if (gen == GEN_AFAB || ((a.redo_bins >> bin) & 1)) {
+    if ((gen == GEN_AFAB && X != XR) || ((a.redo_bins >> bin) & 1)) {
       // queues that may hold more than a.ring micro-batches of a stage in flight
       if (cand >= 0 && d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
       continue;
@@ -2456,7 +2460,6 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
   a.n_live = nullptr;
-  a.afab_mat = 0;
   a.out_ms = ms;
   a.out_bub = bub;
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
@@ -2634,7 +2637,6 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   a.out_comm = cm;
   a.out_bound = bd;
   a.n_live = ex.n_live;
-  a.afab_mat = X == XR;
   const int tb = CLS_THREADS;
   const int nb = (int)((n + tb - 1) / tb);
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
@@ -2670,9 +2672,23 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
                              P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if constexpr (X != XR) {  // rendezvous: GPipe queues were sent to the materialised path
+  if constexpr (X != XR) {
     if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
                              stream)))
+      return rc;
+  } else {
+    // rendezvous: GPipe queues in the generated kernels, with full rows (a stage holds all M
+    // micro-batches before its first backward), per v class
+    if (prob->v_max >= 2 &&
+        (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                               bd, 2 * P, M, bins_of(2, 2, true), CTL_WORK + 4, stream)))
+      return rc;
+    if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                               bd, P, M, bins_of(1, 1, true), CTL_WORK + 5, stream)))
+      return rc;
+    if (prob->v_max >= 3 &&
+        (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                               bd, P * prob->v_max, M, bins_of(3, 8, true), CTL_WORK + 6, stream)))
       return rc;
   }
   if ((rc = record_mark(4, stream))) return rc;
