@@ -52,6 +52,7 @@ struct SimArgs {
   const uint8_t* cands;
   int64_t n;
   const int32_t* n_live;  // nullable: only the first *n_live of the n records are evaluated
+  int mat_lists;          // lists k_sim_mat takes: 1 the perturbed candidates, 2 the 64-bit redo
   int64_t* out_ms;
   int64_t* out_bub;
   int32_t* ctl;
@@ -1009,7 +1010,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
     const int32_t* list = phase == 0 ? a.idx + base : a.redo;
     const int cnt = phase == 0 ? a.ctl[CTL_COUNTS + BIN_MAT] : a.ctl[CTL_REDO];
     const int counter = phase == 0 ? CTL_WORK_MAT : CTL_WORK_REDO;
-    if (cnt == 0) continue;  // no work: leave the shared counter alone
+    if (cnt == 0 || !((a.mat_lists >> phase) & 1)) continue;  // no work here
     for (;;) {
       int ch = 0;
       if (lane_id() == 0) ch = atomicAdd(&a.ctl[counter], 1);
@@ -1068,6 +1069,91 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       CommTally tot = L.cm;
       if constexpr (X == XC) tot = group_tally(L.cm, G);
       if (mine) put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot, L.fs, L.clock);
+    }
+  }
+}
+
+
+// Candidates with perturbations, 40-bit slots in full rows (R = M) shared by the wave's groups
+// like the generated kernels (5 bytes a slot instead of 8, so more waves fit a CU): queues
+// materialised in global memory, moves applied. A candidate whose times pass the 40-bit slots
+// joins the redo list of the 64-bit kernel, which runs after this one.
+template <int VMAX, int X>
+__global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int64_t mbox[X == XR ? WAVE : 1];  // rendezvous mailboxes
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  const int gg = g < a.CPW ? g : 0;
+  const Table40 T{reinterpret_cast<uint32_t*>(smem), smem + (size_t)a.slots * a.CPW * 4,
+                  __ffs(a.CPW) - 1, gg};
+  uint8_t* rec = smem + (size_t)gg * a.rec_stride;  // until the table is cleared
+  const int slot = (int)blockIdx.x * a.CPW + gg;
+  uint16_t* row = a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap;
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  const int base = a.ctl[CTL_START + BIN_MAT];
+  const int cnt = a.ctl[CTL_COUNTS + BIN_MAT];
+  if (cnt == 0) return;
+  const Ring ring = make_ring(M, M);
+  for (;;) {
+    int ch = 0;
+    if (lane_id() == 0) ch = atomicAdd(&a.ctl[CTL_WORK_MAT], 1);
+    ch = bcast(ch);
+    if (ch * a.CPW >= cnt) break;
+    const int e = ch * a.CPW + g;
+    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[base + e] : -1;
+    const bool has = cand >= 0;
+    const bool mine = has && d < P;
+    const uint8_t* grec = has ? a.cands + cand * a.pr.stride : a.cands;
+    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
+    __asm__ volatile("" ::: "memory");
+    const int policy = has ? rec[0] : 0;
+    const int v = has ? rec[1] : 1;
+    const int split = policy == POL_ZB;
+    int gen = GEN_AFAB;
+    if (has) gen = resolve_record(a.pr, grec).gen;
+    Chunks<VMAX> c;
+    int64_t busy = 0, stat = 0;
+    Lane L;
+    L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
+    L.cm.reset();
+    L.fs = -1;
+    if constexpr (X == XS)
+      for (int i = 0; i < 16; ++i) L.lf[i] = 0;
+    if (mine) {
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, a.pre_mem,
+                                &stat, X);
+      L.nops = materialise<VMAX>(a, c, v, gen, split, row);
+      const uint8_t* pp = grec + pert_off(a.pr.s_max);
+      const int np = grec[2];
+      for (int i = 0; i < np; ++i) {
+        const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
+        if (pd != d) continue;
+        move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
+      }
+    } else {
+      zero_chunks<VMAX>(c);
+    }
+    __asm__ volatile("" ::: "memory");
+    T.clear_all(a.slots, lane_id(), WAVE);  // every candidate's rows fit a.slots
+    __asm__ volatile("" ::: "memory");
+    GenMat q;
+    q.init(row, L.nops);
+    describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+    if constexpr (X == XR) mbox[lane_id()] = RDV_EMPTY;
+    bool dead = false;
+    rounds<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, mbox);
+    const int64_t ms = group_max(L.clock, G);
+    CommTally tot = L.cm;
+    if constexpr (X == XC) tot = group_tally(L.cm, G);
+    if (mine) {
+      if (ms >= Table40::LIMIT) {
+        if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      } else {
+        put_results<X>(a, cand, d, dead, ms, busy, stat, L.peak, tot, L.fs, L.clock);
+      }
     }
   }
 }
@@ -2273,6 +2359,8 @@ struct Setup {
   Workspace* ws;
   DevInfo di;
   int mat_grid;
+  Plan m40;      // 40-bit full-row plan of k_sim_mat40 (CPW 0: does not fit)
+  int m40_grid;  // its blocks (queue rows of the workspace are sized for them too)
 };
 
 template <int VC>
@@ -2410,7 +2498,18 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
   rc = prob->v_max <= 2 ? mat_grid_for<2>(su->big, su->di.cus, &su->mat_grid)
                         : mat_grid_for<8>(su->big, su->di.cus, &su->mat_grid);
   if (rc) return rc;
-  su->l = layout(prob, su->big, n, (int64_t)su->mat_grid * su->big.CPW);
+  su->m40 = fast_plan(prob, su->di.lds_max, prob->P * prob->v_max, prob->M, 0);
+  su->m40_grid = 0;
+  if (su->m40.CPW >= 1) {
+    // the memory variant's grid bounds every variant's (as for k_sim_mat)
+    rc = prob->v_max <= 2
+             ? occupancy_grid(k_sim_mat40<2, XM>, su->m40.lds_bytes, su->di.cus, &su->m40_grid)
+             : occupancy_grid(k_sim_mat40<8, XM>, su->m40.lds_bytes, su->di.cus, &su->m40_grid);
+    if (rc) return rc;
+  }
+  su->l = layout(prob, su->big, n,
+                 std::max<int64_t>((int64_t)su->mat_grid * su->big.CPW,
+                                   (int64_t)su->m40_grid * std::max(su->m40.CPW, 0)));
   Workspace& ws = g_ws[std::make_pair(dev, stream)];
   rc = ensure_buf(ws.base, ws.bytes, su->l.total, stream);
   if (rc) return rc;
@@ -2460,6 +2559,7 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.cands = static_cast<const uint8_t*>(cands);
   a.n = n;
   a.n_live = nullptr;
+  a.mat_lists = 3;
   a.out_ms = ms;
   a.out_bub = bub;
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
@@ -2692,6 +2792,25 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
       return rc;
   }
   if ((rc = record_mark(4, stream))) return rc;
+  // candidates with moves: 40-bit full rows where they fit, then the 64-bit redo list
+  if (su.m40.CPW >= 1) {
+    SimArgs a40 = make_args(prob, su.m40, su, link, candidates, n, out_makespan, out_bubble, pk);
+    a40.out_comm = cm;
+    a40.out_bound = bd;
+    int g40 = 0;
+    rc = prob->v_max <= 2 ? occupancy_grid(k_sim_mat40<2, X>, su.m40.lds_bytes, su.di.cus, &g40)
+                          : occupancy_grid(k_sim_mat40<8, X>, su.m40.lds_bytes, su.di.cus, &g40);
+    if (rc) return rc;
+    g40 = std::min(g40, su.m40_grid);
+    if (prob->v_max <= 2)
+      hipLaunchKernelGGL((k_sim_mat40<2, X>), dim3(g40), dim3(WAVE), su.m40.lds_bytes, stream,
+                         a40);
+    else
+      hipLaunchKernelGGL((k_sim_mat40<8, X>), dim3(g40), dim3(WAVE), su.m40.lds_bytes, stream,
+                         a40);
+    if ((rc = launch_ok())) return rc;
+    a.mat_lists = 2;
+  }
   if (prob->v_max <= 2)
     hipLaunchKernelGGL((k_sim_mat<2, X>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
                        stream, a);
