@@ -1234,11 +1234,21 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
     rkey[j] = key;
     rid[j] = id;
   }
-  // merge: computations (queue order), sends (queue order), receives (sorted)
+  // merge: computations (queue order), sends (queue order), receives (sorted); each stream's
+  // head stays in registers and only the stream that was taken fetches its next one
   int ci = 0, si = 0, ri = 0, n = 0;
-  int64_t sk = 0;
-  uint32_t sid = 0;
-  auto next_send = [&]() {
+  int64_t ck = 0, sk = 0, rk = 0;
+  uint32_t citem = 0, sid = 0, rdd = 0;
+  auto fetch_comp = [&]() {
+    if (ci < nq) {
+      const uint32_t e = row[ci];
+      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      const int s = pick<VMAX>(c.st, k);
+      ck = tb[node(kind, s, m)] - dur_of(kind, k);
+      citem = pitem(PI_COMP, kind, s, m);
+    }
+  };
+  auto fetch_send = [&]() {
     while (si < nq) {
       const uint32_t e = row[si];
       const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
@@ -1252,35 +1262,31 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
       ++si;
     }
   };
-  next_send();
+  auto fetch_recv = [&]() {
+    if (ri < nr) rk = rkey[ri], rdd = rid[ri];
+  };
+  fetch_comp();
+  fetch_send();
+  fetch_recv();
   while (ci < nq || si < nq || ri < nr) {
-    int64_t ck = 0;
-    uint32_t citem = 0;
-    if (ci < nq) {
-      const uint32_t e = row[ci];
-      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
-      const int s = pick<VMAX>(c.st, k);
-      ck = tb[node(kind, s, m)] - dur_of(kind, k);
-      citem = pitem(PI_COMP, kind, s, m);
-    }
     // the smallest of the three heads
-    int pick_src = ci < nq ? 0 : -1;
+    int src = ci < nq ? 0 : -1;
     int64_t bt = ck;
     uint32_t bc = 1, bt2 = (uint32_t)ci;
-    if (si < nq && (pick_src < 0 || key_less(sk, 0, sid, bt, bc, bt2)))
-      pick_src = 1, bt = sk, bc = 0, bt2 = sid;
-    if (ri < nr && (pick_src < 0 || key_less(rkey[ri], 0, rid[ri], bt, bc, bt2)))
-      pick_src = 2, bt = rkey[ri], bc = 0, bt2 = rid[ri];
-    if (pick_src == 0) {
+    if (si < nq && (src < 0 || key_less(sk, 0, sid, bt, bc, bt2))) src = 1, bt = sk, bc = 0, bt2 = sid;
+    if (ri < nr && (src < 0 || key_less(rk, 0, rdd, bt, bc, bt2))) src = 2;
+    if (src == 0) {
       prog[n++] = citem;
       ++ci;
-    } else if (pick_src == 1) {
+      fetch_comp();
+    } else if (src == 1) {
       prog[n++] = (PI_SEND << 30) | sid;
       ++si;
-      next_send();
+      fetch_send();
     } else {
-      prog[n++] = (PI_RECV << 30) | rid[ri];
+      prog[n++] = (PI_RECV << 30) | rdd;
       ++ri;
+      fetch_recv();
     }
   }
   return n;
@@ -1369,13 +1375,14 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
       const uint8_t* devs = rec + 3 + a.pr.s_max;
       int pos = 0;
       bool live = pos < plen, arrived = false;
+      // the next item is loaded one advance ahead, so decoding never waits for memory
+      uint32_t nitem = plen > 1 ? prog[1] : 0u;
       // the current item, decoded
       uint32_t type = 0, tag = 0;
       int rd = 0, wr = 0, store = 0, src = 0;
       uint32_t mask = 0, want = 0, state = 0;
       int64_t w = 0, dur = 0;
-      auto decode = [&]() {
-        const uint32_t it = live ? prog[pos] : 0u;
+      auto decode = [&](uint32_t it) {
         type = it >> 30;
         const int kind = (int)((it >> 28) & 3u), s = (int)((it >> 16) & 63u), m = (int)(it & 0x7FFu);
         tag = it & 0x3FFFFFFFu;
@@ -1394,7 +1401,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
           w = kind == KF ? pick<VMAX>(c.wF, ck) : pick<VMAX>(c.wB, ck);
         }
       };
-      decode();
+      decode(live ? prog[0] : 0u);
       for (;;) {
         uint32_t plo, phi;
         T.issue(live && type != PI_RECV ? rd : 0, plo, phi);
@@ -1418,9 +1425,14 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
         clock = okC ? fin : okSD ? box : okR ? xend : clock;
         arrived = okSA ? true : okSD ? false : arrived;
         const bool done = okC || okSD || okR;
-        pos += done ? 1 : 0;
-        live = pos < plen;
-        if (done) decode();
+        if (done) {
+          ++pos;
+          live = pos < plen;
+          const uint32_t it = live ? nitem : 0u;
+          __asm__ volatile("" : "+v"(nitem));
+          nitem = pos + 1 < plen ? prog[pos + 1] : 0u;
+          decode(it);
+        }
         __asm__ volatile("" ::: "memory");
         if (__ballot(okC || okSA || okSD || okR) == 0) {
           const uint64_t actm = __ballot(live);
