@@ -296,6 +296,14 @@ def main():
         if t.get("kernel_source_sha") == kernel_source_hash() and tk == SIM_KERNELS[dom]:
             traffic = t.get("hbm_bytes_per_launch")
     all_ms = float(per_kernel_ms.sum())
+    # per stratum: the candidates each simulation kernel handles, at that kernel's rate
+    names = ["v2_generated", "v1_generated", "v3plus_generated", "gpipe_all_v", "with_moves"]
+    strata = {}
+    for name, kname, sel, kms in zip(names, SIM_KERNELS, sets, per_kernel_ms):
+        cnt = int(sel.sum())
+        if cnt:
+            strata[name] = {"kernel": kname, "candidates": cnt, "ms": round(float(kms), 4),
+                            "candidates_per_s": round(cnt / (float(kms) * 1e-3), 1)}
     roofline = {
         "bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU_TOPS, 2),
         "unit": "Tops/s (32-bit VALU lane-ops)", "frac": round(achieved / PEAK_VALU_TOPS, 5),
@@ -307,6 +315,7 @@ def main():
         "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, per_kernel_ms)},
         "all_sim_kernels_frac": round(int(lane_c.sum()) / (all_ms * 1e-3) / 1e12 / PEAK_VALU_TOPS,
                                       5),
+        "strata": strata,
     }
 
     # the same batch with the memory model (peak bytes per device), timed the same way
