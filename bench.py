@@ -217,6 +217,80 @@ def time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, warmup, steps, 
     return out
 
 
+def time_tuner(torch, _lib, inputs, warmup, steps, with_cpu):
+    """The local-search tuner (octo_tune_step) on its own workload: 96 layers, P = 32, M = 256,
+    v = 2, 4,096 chains; one job = step 0 (generate and evaluate) plus 64 move steps, every
+    chain re-simulated at every step. The unit of work is one chain-step (one candidate
+    evaluated and accepted or rejected)."""
+    w = inputs.WORKLOADS[5]
+    dev = torch.device("cuda:0")
+    recs_np = inputs.tuner_chains(w)
+    n = recs_np.shape[0]
+    prob = _lib.problem(w.L, w.P, w.v_max, w.M, recs_np.shape[1], 0)
+    costs_np, link_np = inputs.layer_costs(w), inputs.link_matrix(w.P, w.link_ns)
+    costs = torch.from_numpy(costs_np).to(dev)
+    link = torch.from_numpy(link_np).to(dev)
+    c0_np = np.zeros((n, _lib.chain_stride(prob)), np.uint8)
+    c0_np[:, :recs_np.shape[1]] = recs_np
+    c0 = torch.from_numpy(c0_np).to(dev)
+    chains = torch.empty_like(c0)
+    queues = torch.empty((n, w.P, _lib.queue_capacity(prob)), dtype=torch.int16, device=dev)
+
+    def job():
+        chains.copy_(c0)
+        for t in range(w.steps + 1):
+            _lib.tune_step(prob, costs, link, chains, queues, w.seed, t)
+
+    for _ in range(max(warmup, 1)):
+        job()
+    torch.cuda.synchronize()
+    hip, evs = hip_events(2)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    t0 = time.perf_counter()
+    hip.hipEventRecord(evs[0], stream)
+    for _ in range(steps):
+        job()
+    hip.hipEventRecord(evs[1], stream)
+    torch.cuda.synchronize()
+    secs = (time.perf_counter() - t0) / steps
+    f = ctypes.c_float()
+    hip.hipEventElapsedTime(ctypes.byref(f), evs[0], evs[1])
+    ev_secs = f.value * 1e-3 / steps
+    for e in evs:
+        hip.hipEventDestroy(e)
+    g_ms, g_acc, _ = _lib.chain_state(chains, prob)
+    g_ms, g_acc = g_ms.numpy(), g_acc.numpy()
+    init_ms = _lib.sim_batch(prob, costs, link, torch.from_numpy(recs_np).to(dev))[0]
+    init_ms = init_ms.cpu().numpy()
+    ok = (init_ms > 0) & (g_ms > 0)
+    evals = n * (w.steps + 1)
+    out = {"value": round(evals / secs, 1), "unit": "chain-steps/s",
+           "ms_per_job": round(secs * 1e3, 3), "ms_per_job_events": round(ev_secs * 1e3, 3),
+           "chains": n, "steps": w.steps + 1, "workload": w.name,
+           "accepted_moves": int(g_acc.sum()),
+           "mean_makespan_gain": round(float(1 - (g_ms[ok] / init_ms[ok]).mean()), 4),
+           "cpu_baseline": None}
+    if with_cpu:
+        from oracle import octoref
+        sample = np.arange(0, n, 16)
+        threads = min(16, os.cpu_count() or 1)
+        rprob = octoref.problem(w.L, w.P, w.v_max, w.M, recs_np.shape[1], 0)
+        t1 = time.perf_counter()
+        rr = octoref.tune_chains(rprob, costs_np, link_np, recs_np, sample, w.seed, w.steps,
+                                 nthreads=threads)
+        t2 = time.perf_counter()
+        g_rec = chains.cpu().numpy()[:, :recs_np.shape[1]]
+        same = bool((rr[0] == g_rec[sample]).all() and (rr[1] == g_ms[sample]).all() and
+                    (rr[3] == g_acc[sample]).all())
+        out["cpu_baseline"] = {"value": round(len(sample) * (w.steps + 1) / (t2 - t1), 1),
+                               "unit": "chain-steps/s", "cores": threads, "kind": "oracle",
+                               "sample": f"every 16th chain of the same job ({len(sample)} "
+                                         f"chains x {w.steps + 1} steps)",
+                               "parity_on_sample": same}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -377,6 +451,7 @@ def main():
                                args.warmup, min(args.steps, 3), not args.no_cpu)
     alg1 = time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, args.warmup,
                      min(args.steps, 3), not args.no_cpu)
+    tuner = time_tuner(torch, _lib, inputs, args.warmup, min(args.steps, 3), not args.no_cpu)
     cpu = None
     if not args.no_cpu:
         from oracle import octoref
@@ -412,6 +487,7 @@ def main():
         "ordered": ordered,
         "w_advance": w_advance,
         "alg1": alg1,
+        "tuner": tuner,
     }
     print(json.dumps(out), flush=True)
 

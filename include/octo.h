@@ -242,6 +242,8 @@ int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const i
  *   +8  int64 accepted moves
  *   +16 int64 current bubble[P]
  *   +16+8P int64 current peak bytes[P] (written by octo_tune_step_mem only)
+ *   +16+16P int64 an upper bound of the queues' micro-batch window (octo_tune_step only): the
+ *          largest m_i - m_j over queue entries i < j of one stage on one device
  * Queue store: uint16 [n_chains][P][octo_queue_capacity(prob)]; entry = kind << 14 | chunk << 11
  * | m with kind 0 = F, 1 = B, 2 = W and chunk the index into the device's ascending stage list.
  *

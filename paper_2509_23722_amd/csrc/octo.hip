@@ -1683,7 +1683,8 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
 }
 
 // ---------------------------------------------------------------------------------------------
-// Local-search step (one chain per group, 64-bit finish tables).
+// Local-search step: one chain per group. k_tune uses 64-bit full-row finish tables; k_tune_ring
+// 40-bit ring tables for chains whose queue order allows it, the rest going to k_tune.
 // ---------------------------------------------------------------------------------------------
 struct TuneArgs {
   SimArgs s;
@@ -1695,12 +1696,112 @@ struct TuneArgs {
   int step;
   const int64_t* cap;  // memory-constrained search: capacity per device [P]
   int max_adv;         // W advances per evaluation
+  const int32_t* list;    // nullable: step only the chains list[0 .. *list_n - 1]
+  const int32_t* list_n;
 };
 
-// One step of every chain. MEM: the memory-constrained search — proposals are built in a
-// working copy of the chain's queues (group slot rows of qscratch), selective W advancing runs
-// on it, and a state is feasible only if every device fits; the copy replaces the chain's
-// queues when the proposal is kept.
+// int64 word of the chain state (after makespan, accepted count, bubble[P], peak[P]) holding an
+// upper bound of the window of the chain's queues (queue_window).
+__host__ __device__ __forceinline__ int window_word(int P) { return 2 + 2 * P; }
+
+// Window of a queue row: the largest m_i - m_j over entries i < j of one chunk (0 when every
+// chunk's micro-batches never go backwards by more than 0). When the window of every device is
+// below R, each op of micro-batch m precedes every op of m + R of the same stage.
+template <int VMAX>
+__device__ int queue_window(const uint16_t* row, int n) {
+  int hi[VMAX];
+#pragma unroll
+  for (int k = 0; k < VMAX; ++k) hi[k] = 0;
+  int w = 0;
+  for (int i = 0; i < n; ++i) {
+    const int e = row[i];
+    const int k = (e >> 11) & 7, m = e & 0x7FF;
+    const int h = pick<VMAX>(hi, k);
+    w = h - m > w ? h - m : w;
+#pragma unroll
+    for (int j = 0; j < VMAX; ++j) hi[j] = (k == j && m > h) ? m : hi[j];
+  }
+  return w;
+}
+
+// One move of a chain (step >= 1). (u0, u1, u2, u3) = Philox4x64-10(key = (seed, 0),
+// counter = (chain, step, 0, 0)); u0 mod 3 picks the family (§6's partitioning, placement and
+// scheduling tuning):
+//   0  stage boundary mi = 1 + u1 mod (S-1) moves by one layer, up if u2 is odd, to nb;
+//   1  devices d1 = u1 mod P and d2 = (d1 + 1 + u2 mod (P-1)) mod P exchange their stages, each
+//      keeping its queue;
+//   2  entries mi = u2 mod (qlen-1) and mi + 1 of device sd = u1 mod P swap.
+// The move is applied to the staged record (lane 0) and to device sd's queue row (lane sd).
+// Lane sd also returns in `pair` the window term the swap adds (the later entry now first) when
+// both entries belong to one chunk: an adjacent swap reorders only that pair.
+struct Move {
+  int kind, mi, sd, nb, d1, d2, pair;
+  bool valid;
+};
+
+__device__ __forceinline__ Move propose(uint64_t seed, int64_t chain, int step, uint8_t* rec,
+                                        const Problem& pr, int S, int qlen, uint16_t* qrow,
+                                        int d) {
+  Move mv;
+  mv.kind = -1, mv.mi = 0, mv.sd = 0, mv.nb = 0, mv.d1 = 0, mv.d2 = 0, mv.pair = 0;
+  mv.valid = true;
+  const int P = pr.P;
+  const U4 u = philox4x64_10((uint64_t)chain, (uint64_t)step, 0, 0, seed, 0);
+  mv.kind = (int)(u.x[0] % 3);
+  if (mv.kind == 0) {
+    if (S < 2) {
+      mv.valid = false;
+    } else {
+      mv.mi = 1 + (int)(u.x[1] % (uint64_t)(S - 1));
+      const int lo = mv.mi > 1 ? rec[4 + mv.mi - 2] : 0;
+      const int hi = mv.mi < S - 1 ? rec[4 + mv.mi] : pr.L;
+      mv.nb = rec[4 + mv.mi - 1] + ((u.x[2] & 1) ? 1 : -1);
+      mv.valid = mv.nb > lo && mv.nb < hi;
+      __asm__ volatile("" ::: "memory");
+      if (mv.valid && d == 0) rec[4 + mv.mi - 1] = (uint8_t)mv.nb;
+    }
+  } else if (mv.kind == 1) {
+    if (P < 2) {
+      mv.valid = false;
+    } else {
+      mv.d1 = (int)(u.x[1] % (uint64_t)P);
+      mv.d2 = (int)((mv.d1 + 1 + (int)(u.x[2] % (uint64_t)(P - 1))) % P);
+      uint8_t* dv = rec + 3 + pr.s_max;
+      __asm__ volatile("" ::: "memory");
+      if (d == 0)
+        for (int s = 0; s < S; ++s)
+          dv[s] = dv[s] == mv.d1 ? (uint8_t)mv.d2 : dv[s] == mv.d2 ? (uint8_t)mv.d1 : dv[s];
+    }
+  } else {
+    mv.sd = (int)(u.x[1] % (uint64_t)P);
+    if (qlen < 2) {
+      mv.valid = false;
+    } else {
+      mv.mi = (int)(u.x[2] % (uint64_t)(qlen - 1));
+      if (d == mv.sd) {
+        const uint16_t x = qrow[mv.mi], y = qrow[mv.mi + 1];
+        qrow[mv.mi] = y;
+        qrow[mv.mi + 1] = x;
+        if (((x >> 11) & 7) == ((y >> 11) & 7)) mv.pair = (int)(y & 0x7FF) - (int)(x & 0x7FF);
+      }
+    }
+  }
+  return mv;
+}
+
+// Undo a kind-2 move on device sd's queue row (lane sd).
+__device__ __forceinline__ void unswap(const Move& mv, uint16_t* row, int d) {
+  if (mv.kind == 2 && mv.valid && d == mv.sd) {
+    const uint16_t x = row[mv.mi];
+    row[mv.mi] = row[mv.mi + 1];
+    row[mv.mi + 1] = x;
+  }
+}
+
+// One step of every chain (of the list, when given). MEM: the memory-constrained search —
+// proposals are built in a working copy of the chain's queues (group slot rows of qscratch),
+// selective W advancing runs on it, and a state is feasible only if every device fits; the copy
+// replaces the chain's queues when the proposal is kept.
 template <int VMAX, bool MEM>
 __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   extern __shared__ __align__(16) uint8_t smem[];
@@ -1718,12 +1819,13 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   const int gl = lane_id() - d;
   const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
-  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < t.n_chains; base += n_groups) {
-    const int64_t chain = base + g;
-    const bool has = g < a.CPW && chain < t.n_chains;
-    uint8_t* crec = t.chains + (has ? chain : 0) * t.chain_stride;
+  const int64_t total = t.list ? (int64_t)*t.list_n : t.n_chains;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < total; base += n_groups) {
+    const bool has = g < a.CPW && base + g < total;
+    const int64_t chain = has ? (t.list ? (int64_t)t.list[base + g] : base + g) : 0;
+    uint8_t* crec = t.chains + chain * t.chain_stride;
     int64_t* cstate = reinterpret_cast<int64_t*>(crec + a.pr.stride);
-    uint16_t* row = t.queues + ((size_t)(has ? chain : 0) * P + (d < P ? d : 0)) * a.qcap;
+    uint16_t* row = t.queues + ((size_t)chain * P + (d < P ? d : 0)) * a.qcap;
     uint16_t* qrow = MEM ? wrow : row;  // the queues the proposal is evaluated on
     if (has) stage_record(rec, crec, a.rec_bytes, d, G);
     __asm__ volatile("" ::: "memory");
@@ -1758,61 +1860,28 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
       for (int i = 0; i < qlen; ++i) wrow[i] = row[i];
 
     // propose (step >= 1); the move is applied to the staged record / the queue row qrow
-    int kind = -1, mi = 0, sd = -1;
-    bool valid = true;
-    if (!skip && t.step > 0) {
-      U4 u = philox4x64_10((uint64_t)chain, (uint64_t)t.step, 0, 0, t.seed, 0);
-      kind = (int)(u.x[0] % 3);
-      if (kind == 0) {
-        if (S < 2) {
-          valid = false;
-        } else {
-          mi = 1 + (int)(u.x[1] % (uint64_t)(S - 1));
-          const int lo = mi > 1 ? rec[4 + mi - 2] : 0;
-          const int hi = mi < S - 1 ? rec[4 + mi] : a.pr.L;
-          const int nb = rec[4 + mi - 1] + ((u.x[2] & 1) ? 1 : -1);
-          valid = nb > lo && nb < hi;
-          __asm__ volatile("" ::: "memory");
-          if (valid && d == 0) rec[4 + mi - 1] = (uint8_t)nb;
-        }
-      } else if (kind == 1) {
-        if (P < 2) {
-          valid = false;
-        } else {
-          const int d1 = (int)(u.x[1] % (uint64_t)P);
-          const int d2 = (int)((d1 + 1 + (int)(u.x[2] % (uint64_t)(P - 1))) % P);
-          uint8_t* dv = rec + 3 + a.pr.s_max;
-          __asm__ volatile("" ::: "memory");
-          if (d == 0)
-            for (int s = 0; s < S; ++s)
-              dv[s] = dv[s] == d1 ? (uint8_t)d2 : dv[s] == d2 ? (uint8_t)d1 : dv[s];
-        }
-      } else {
-        sd = (int)(u.x[1] % (uint64_t)P);
-        if (qlen < 2) {
-          valid = false;
-        } else {
-          mi = (int)(u.x[2] % (uint64_t)(qlen - 1));
-          if (d == sd) {
-            const uint16_t x = qrow[mi];
-            qrow[mi] = qrow[mi + 1];
-            qrow[mi + 1] = x;
-          }
-        }
-      }
-    }
+    Move mv;
+    mv.kind = -1, mv.valid = true, mv.pair = 0, mv.sd = 0;
+    if (!skip && t.step > 0) mv = propose(t.seed, chain, t.step, rec, a.pr, S, qlen, qrow, d);
+    const int pair = __shfl(mv.pair, gl + (mv.sd < G ? mv.sd : 0));
     __asm__ volatile("" ::: "memory");
+    const bool valid = mv.valid;
     const bool run = !skip && valid;
 
     Chunks<VMAX> c;
     int64_t busy = 0, stat = 0;
+    int win = 0;
     if (run && d < P) {
       busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring,
                                 MEM ? a.pre_mem : nullptr, &stat);
-      if (t.step == 0) materialise<VMAX>(a, c, v, gen, split, qrow);
+      if (t.step == 0) {
+        materialise<VMAX>(a, c, v, gen, split, qrow);
+        if (!MEM) win = queue_window<VMAX>(qrow, qlen);
+      }
     } else {
       zero_chunks<VMAX>(c);
     }
+    if (!MEM && t.step == 0) win = (int)group_max((int64_t)win, G);
     __asm__ volatile("" ::: "memory");
     bool dead = false, fits = true;
     int64_t ms = 0, held = 0;
@@ -1850,6 +1919,10 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
         cstate[1] = t.step == 0 ? 0 : cstate[1] + 1;
         if (t.step > 0)
           for (int i = 0; i < a.rec_bytes; ++i) crec[i] = rec[i];
+        if (!MEM) {
+          const int64_t w0 = t.step == 0 ? 0 : cstate[window_word(P)];
+          cstate[window_word(P)] = t.step == 0 ? win : (pair > w0 ? pair : w0);
+        }
       }
       if (d < P) cstate[2 + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
       if constexpr (MEM) {
@@ -1858,10 +1931,130 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
           for (int i = 0; i < qlen; ++i) row[i] = wrow[i];
         }
       }
-    } else if (!MEM && kind == 2 && valid && d == sd) {
-      const uint16_t x = row[mi];
-      row[mi] = row[mi + 1];
-      row[mi + 1] = x;
+    } else if (!MEM) {
+      unswap(mv, row, d);
+    }
+  }
+}
+
+// One step of every chain on 40-bit ring tables: R rows per stage (R < M), the wave's groups
+// sharing the slot arrays as in the generated kernels, so several chains fit a CU. A ring is
+// exact for a chain whose queue window (queue_window; its bound is kept in the chain state) is
+// below R: then each op of micro-batch m precedes every op of m + R of its stage on its device,
+// so a slot is rewritten by m + R only after the readers of m have read it, and a reader of
+// (s, m) can meet only generation m or m - R there, which the slot's parity bit tells apart. A
+// chain whose window reaches R, or whose times pass the 40-bit slots, is left as it was and
+// joins the redo list, which k_tune then steps.
+template <int VMAX>
+__global__ void __launch_bounds__(WAVE) k_tune_ring(TuneArgs t) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const SimArgs& a = t.s;
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  const int gg = g < a.CPW ? g : 0;
+  const Table40 T{reinterpret_cast<uint32_t*>(smem), smem + (size_t)a.slots * a.CPW * 4,
+                  __ffs(a.CPW) - 1, gg};
+  uint8_t* rec = smem + (size_t)gg * a.rec_stride;  // until the table is cleared
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  const int gl = lane_id() - d;
+  const Ring ring = make_ring(M, a.ring);
+  const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < t.n_chains; base += n_groups) {
+    const bool has = g < a.CPW && base + g < t.n_chains;
+    const int64_t chain = has ? base + g : 0;
+    uint8_t* crec = t.chains + chain * t.chain_stride;
+    int64_t* cstate = reinterpret_cast<int64_t*>(crec + a.pr.stride);
+    uint16_t* row = t.queues + ((size_t)chain * P + (d < P ? d : 0)) * a.qcap;
+    if (has) stage_record(rec, crec, a.rec_bytes, d, G);
+    __asm__ volatile("" ::: "memory");
+
+    bool skip = !has;
+    int v = 1, gen = GEN_AFAB, split = 0;
+    int64_t cur = 0, w0 = 0;
+    if (has) {
+      if (t.step == 0) {
+        Resolved r = resolve_record(a.pr, crec);
+        if (!r.valid || r.n_pert != 0) {
+          if (d == 0) cstate[0] = OCTO_MS_INVALID, cstate[1] = 0;
+          if (d < P) cstate[2 + d] = OCTO_MS_INVALID;
+          skip = true;
+        }
+        v = r.v, gen = r.gen, split = r.split;
+      } else {
+        cur = cstate[0];
+        w0 = cstate[window_word(P)];
+        Resolved r = resolve_record(a.pr, rec);
+        if (cur == OCTO_MS_INVALID || !r.valid || r.n_pert != 0) skip = true;
+        v = r.valid ? r.v : 1;
+        split = r.split;
+      }
+    }
+    const int S = P * v;
+    const int qlen = (split ? 3 : 2) * v * M;
+
+    Move mv;
+    mv.kind = -1, mv.valid = true, mv.pair = 0, mv.sd = 0;
+    if (!skip && t.step > 0) mv = propose(t.seed, chain, t.step, rec, a.pr, S, qlen, row, d);
+    const int pair = __shfl(mv.pair, gl + (mv.sd < G ? mv.sd : 0));
+    __asm__ volatile("" ::: "memory");
+    const bool valid = mv.valid;
+    int64_t win = pair > w0 ? pair : w0;
+
+    Chunks<VMAX> c;
+    int64_t busy = 0, stat = 0;
+    int wl = 0;
+    const bool eval = !skip && valid;
+    if (eval && d < P) {
+      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, split, ring, nullptr, &stat);
+      if (t.step == 0) {
+        materialise<VMAX>(a, c, v, gen, split, row);
+        wl = queue_window<VMAX>(row, qlen);
+      }
+    } else {
+      zero_chunks<VMAX>(c);
+    }
+    if (t.step == 0) win = group_max((int64_t)wl, G);
+    const bool fits = win < ring.R;
+    const bool run = eval && fits;
+    __asm__ volatile("" ::: "memory");
+    T.clear_all(a.slots, lane_id(), WAVE);  // every chain's rows fit a.slots
+    __asm__ volatile("" ::: "memory");
+    Lane L;
+    L.clock = 0, L.pos = 0, L.nops = run && d < P ? qlen : 0, L.mem = L.peak = 0;
+    GenMat q;
+    q.init(row, L.nops);
+    describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+    bool dead = false;
+    relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    const int64_t ms = group_max(L.clock, G);
+
+    if (!has || skip) continue;
+    if (eval && (!fits || ms >= Table40::LIMIT)) {
+      // stepped again by k_tune, from the state this step started with
+      unswap(mv, row, d);
+      if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)chain;
+      continue;
+    }
+    const bool keep = t.step == 0 || (valid && !dead && (cur < 0 || ms <= cur));
+    if (keep) {
+      if (d == 0) {
+        cstate[0] = dead ? OCTO_MS_DEADLOCK : ms;
+        cstate[1] = t.step == 0 ? 0 : cstate[1] + 1;
+        cstate[window_word(P)] = win;
+        // the record in LDS is gone (the table took its place): apply the move to the chain's
+        if (mv.kind == 0) {
+          crec[4 + mv.mi - 1] = (uint8_t)mv.nb;
+        } else if (mv.kind == 1) {
+          uint8_t* dv = crec + 3 + a.pr.s_max;
+          for (int s = 0; s < S; ++s)
+            dv[s] = dv[s] == mv.d1 ? (uint8_t)mv.d2 : dv[s] == mv.d2 ? (uint8_t)mv.d1 : dv[s];
+        }
+      }
+      if (d < P) cstate[2 + d] = dead ? OCTO_MS_DEADLOCK : ms - busy;
+    } else {
+      unswap(mv, row, d);
     }
   }
 }
@@ -2702,6 +2895,19 @@ int launch_tune(const TuneArgs& t, const Plan& pl, int cus, int mat_grid, int64_
   return launch_ok();
 }
 
+// k_tune_ring over all chains, persistent blocks at the plan's occupancy.
+template <int VC>
+int launch_tune_ring(const TuneArgs& t, const Plan& pl, int cus, int64_t n_chains,
+                     hipStream_t stream) {
+  int grid = 0;
+  int rc = occupancy_grid(k_tune_ring<VC>, pl.lds_bytes, cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (n_chains + pl.CPW - 1) / pl.CPW;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+  hipLaunchKernelGGL((k_tune_ring<VC>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, t);
+  return launch_ok();
+}
+
 // k_advance over n records; its queue rows are group slots of the workspace (mat_grid blocks).
 template <int VC>
 int launch_advance(const SimArgs& a, const Plan& pl, int cus, int mat_grid, const int64_t* cap,
@@ -2867,8 +3073,11 @@ int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   if (MEM && (!layer_mem || !capacity)) return OCTO_EINVAL;
   if ((reinterpret_cast<uintptr_t>(chains) & 15) != 0) return OCTO_EINVAL;
   std::lock_guard<std::mutex> lock(g_mu);
+  // the ring pass's redo list holds int32 chain indices, one per chain
+  const bool ring_pass = !MEM && n_chains <= (int64_t)INT32_MAX;
   Setup su;
-  rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, 0, &su);
+  rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, ring_pass ? n_chains : 0,
+               &su);
   if (rc) return rc;
   TuneArgs t;
   t.s = make_args(prob, su.big, su, link, nullptr, 0, nullptr, nullptr);
@@ -2882,6 +3091,24 @@ int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   t.step = step;
   t.cap = capacity;
   t.max_adv = max_advance;
+  t.list = nullptr;
+  t.list_n = nullptr;
+  if (ring_pass) {
+    // rings of the smallest power of two >= P v_max rows, the window of the interleaved orders
+    // the chains start from; chains with wider windows (or larger times) go to k_tune
+    const Ring rr = make_ring(prob->M, prob->P * prob->v_max);
+    const Plan rp = fast_plan(prob, su.di.lds_max, prob->P * prob->v_max, rr.R, 0);
+    if (rr.R < prob->M && rp.CPW >= 1) {
+      TuneArgs tr = t;
+      tr.s = make_args(prob, rp, su, link, nullptr, 0, nullptr, nullptr);
+      tr.s.ring = rr.R;
+      rc = prob->v_max <= 2 ? launch_tune_ring<2>(tr, rp, su.di.cus, n_chains, stream)
+                            : launch_tune_ring<8>(tr, rp, su.di.cus, n_chains, stream);
+      if (rc) return rc;
+      t.list = tr.s.redo;
+      t.list_n = tr.s.ctl + CTL_REDO;
+    }
+  }
   return prob->v_max <= 2
              ? launch_tune<2, MEM>(t, su.big, su.di.cus, su.mat_grid, n_chains, stream)
              : launch_tune<8, MEM>(t, su.big, su.di.cus, su.mat_grid, n_chains, stream);
@@ -3048,7 +3275,7 @@ int32_t octo_record_stride(int32_t P, int32_t v_max, int32_t max_pert) {
 
 int32_t octo_chain_stride(const octo_problem* prob) {
   if (check_problem(prob)) return OCTO_EINVAL;
-  return (int32_t)align_up((size_t)prob->cand_stride + 16 + 16 * prob->P, 16);
+  return (int32_t)align_up((size_t)prob->cand_stride + 8 * (window_word(prob->P) + 1), 16);
 }
 
 int32_t octo_queue_capacity(const octo_problem* prob) {

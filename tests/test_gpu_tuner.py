@@ -58,11 +58,11 @@ def run_gpu_tuner(dev, prob, costs, link, recs, seed, steps, split_at=None):
     torch.cuda.synchronize()
     ms, acc, bub = _lib.chain_state(chains, prob)
     return (chains.cpu().numpy()[:, :recs.shape[1]], ms.numpy(), bub.numpy(), acc.numpy(),
-            queues.cpu().numpy().view(np.uint16))
+            queues.cpu().numpy().view(np.uint16), chains.cpu().numpy())
 
 
 def compare(g, r, prob, label, rec_bytes):
-    grec, gms, gbub, gacc, gq = g
+    grec, gms, gbub, gacc, gq = g[:5]
     rrec, rms, rbub, racc, rq = r
     bad = np.nonzero((gms != rms) | (gbub != rbub).any(axis=1) | (gacc != racc))[0]
     if len(bad):
@@ -91,6 +91,56 @@ def test_tuner_small_all_chains(gpu, P, v, M, L):
     r = R.tune(rprob, costs, link, recs, seed, steps, nthreads=NTHREADS, want_queues=True)
     compare(g, r, prob, f"P={P} v={v} M={M}", 3 + 2 * P * v)
     assert (g[3] > 0).any()  # some moves were accepted
+
+
+def queue_window(q, n):
+    """Largest m_i - m_j over entries i < j of one chunk in the first n entries of a row."""
+    ch, m = (q[:n] >> 11) & 7, (q[:n] & 0x7FF).astype(np.int64)
+    w = 0
+    for k in np.unique(ch):
+        mk = m[ch == k]
+        if len(mk) > 1:
+            w = max(w, int((np.maximum.accumulate(mk)[:-1] - mk[1:]).max()))
+    return w
+
+
+@pytest.mark.parametrize("P,v,M,L", [(4, 1, 32, 12), (2, 2, 16, 10), (4, 2, 32, 16),
+                                     (3, 1, 16, 12), (4, 3, 24, 18)])
+def test_tuner_ring_rows_and_redo(gpu, P, v, M, L):
+    """Shapes with P v_max < M, where chains step on ring tables of the smallest power of two
+    >= P v_max rows while their queue window stays below it, and on full rows once a kept swap
+    widens it (or from the start, for all-forward-all-backward chains, whose window is M - 1).
+    Many steps so that chains cross over; the result must not depend on the path taken. The
+    window bound kept in the chain state must cover the final queues' window."""
+    from paper_2509_23722_amd import _lib
+    rng = np.random.default_rng(P * 1000 + v * 100 + M)
+    n, steps, seed = 128, 150, 31 + P
+    log(f"tuner ring P={P} v={v} M={M} L={L} chains={n} steps={steps}")
+    costs = rng.integers(100_000, 3_000_000, size=(L, 3)).astype(np.int64)
+    link = rng.integers(0, 500_000, size=(P, P)).astype(np.int64)
+    recs = I.random_candidates(rng, L, P, v, M, n, policies=(0, 1, 2, 3))
+    prob = _lib.problem(L, P, v, M, recs.shape[1], 0)
+    g = run_gpu_tuner(gpu, prob, costs, link, recs, seed, steps)
+    rprob = R.problem(L, P, v, M, recs.shape[1], 0)
+    r = R.tune(rprob, costs, link, recs, seed, steps, nthreads=NTHREADS, want_queues=True)
+    compare(g, r, prob, f"ring P={P} v={v} M={M}", 3 + 2 * P * v)
+    # the window bound: over the final queues of every valid chain
+    R_rows = 1 << int(np.ceil(np.log2(P * v)))
+    chains = g[5]
+    off = prob.cand_stride + 8 * (2 + 2 * P)
+    bound = chains[:, off:off + 8].copy().view(np.int64)[:, 0]
+    wins = []
+    for c in range(n):
+        if g[1][c] == -2:
+            continue
+        vv, split = int(g[0][c, 1]), int(g[0][c, 0]) == 3
+        qlen = (3 if split else 2) * vv * M
+        w = max(queue_window(g[4][c, d], qlen) for d in range(P))
+        assert w <= bound[c], f"chain {c}: window {w} above its bound {bound[c]}"
+        wins.append(w)
+    wins = np.array(wins)
+    log(f"  windows below {R_rows}: {(wins < R_rows).sum()} of {len(wins)}")
+    assert (wins < R_rows).any() and (wins >= R_rows).any()
 
 
 def test_tuner_invalid_chains_stay_invalid(gpu):

@@ -36,7 +36,7 @@ def test_record_layout_matches_inputs():
 def test_argument_checks_without_gpu():
     L = _lib.lib()
     good = _lib.problem(16, 4, 1, 8, inputs.record_stride(4, 1, 0), 0)
-    assert _lib.chain_stride(good) == (good.cand_stride + 16 + 16 * 4 + 15) // 16 * 16
+    assert _lib.chain_stride(good) == (good.cand_stride + 24 + 16 * 4 + 15) // 16 * 16
     assert _lib.queue_capacity(good) == 3 * 1 * 8
     bad = [
         _lib.problem(16, 65, 1, 8, 256, 0),       # P > 64
