@@ -978,6 +978,26 @@ __device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>&
   return n;
 }
 
+// Window of a queue row: the largest m_i - m_j over entries i < j of one chunk (0 when every
+// chunk's micro-batches never go backwards by more than 0). When the window of every device is
+// below R, each op of micro-batch m precedes every op of m + R of the same stage.
+template <int VMAX>
+__device__ int queue_window(const uint16_t* row, int n) {
+  int hi[VMAX];
+#pragma unroll
+  for (int k = 0; k < VMAX; ++k) hi[k] = 0;
+  int w = 0;
+  for (int i = 0; i < n; ++i) {
+    const int e = row[i];
+    const int k = (e >> 11) & 7, m = e & 0x7FF;
+    const int h = pick<VMAX>(hi, k);
+    w = h - m > w ? h - m : w;
+#pragma unroll
+    for (int j = 0; j < VMAX; ++j) hi[j] = (k == j && m > h) ? m : hi[j];
+  }
+  return w;
+}
+
 // Move row[from] so that it ends at index to.
 __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
   const uint16_t x = row[from];
@@ -1473,6 +1493,7 @@ struct AdvOut {
   int adv;      // advances made
   int64_t ms;   // makespan of the final queues
   int64_t hi;   // largest activation total this lane's device holds
+  int64_t top;  // largest makespan of any simulation run (40-bit tables: overflow test)
 };
 
 // Running activation total along one device queue: its maximum and the first position that
@@ -1515,8 +1536,8 @@ __device__ __forceinline__ int next_eligible(const uint16_t* row, int n, int p, 
 // take no part). row: this lane's queue (n entries, changed in place); cap: this device's
 // capacity; stat: its static bytes. pert (nullable): where advance k of the group is written as
 // (device, from, to), uint16 each, by the lane of that device.
-template <int VMAX>
-__device__ AdvOut advance_w(const Table64& T, uint16_t* row, int n, const Chunks<VMAX>& c,
+template <int VMAX, class Tab>
+__device__ AdvOut advance_w(const Tab& T, uint16_t* row, int n, const Chunks<VMAX>& c,
                             const Ring& ring, int S, int M, int P, bool run, int64_t cap,
                             int64_t stat, int max_adv, int G, uint64_t gbit, uint64_t lsb,
                             uint16_t* pert) {
@@ -1524,7 +1545,7 @@ __device__ AdvOut advance_w(const Table64& T, uint16_t* row, int n, const Chunks
   const int gl = lane_id() - d;
   const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
   AdvOut o;
-  o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0;
+  o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0, o.top = 0;
   int phase = run ? AW_SIM : AW_DONE;
   int dstar = 0, p = -1, cursor = -1, first = -1, j = -1, at = -1;
   int64_t ms_first = 0;
@@ -1535,13 +1556,14 @@ __device__ AdvOut advance_w(const Table64& T, uint16_t* row, int n, const Chunks
     if (__ballot(need) != 0) {
       Lane L;
       L.clock = 0, L.pos = 0, L.nops = need && d < P ? n : 0, L.mem = L.peak = 0;
-      if (need) T.clear(S * M, d, G);
+      if (need) T.clear(S * ring.R, d, G);
       __asm__ volatile("" ::: "memory");
       GenMat q;
       q.init(row, L.nops);
       describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
       relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       ms = group_max(L.clock, G);
+      o.top = ms > o.top ? ms : o.top;
     }
     if (phase == AW_SIM) {
       o.dead = dead;
@@ -1611,17 +1633,35 @@ __device__ AdvOut advance_w(const Table64& T, uint16_t* row, int n, const Chunks
   return o;
 }
 
+// The finish table of one group: 40-bit slots (RING) or 64-bit, at the start of its LDS area.
+template <bool RING>
+__device__ __forceinline__ auto group_table(uint8_t* p, int slots) {
+  if constexpr (RING)
+    return Table40{reinterpret_cast<uint32_t*>(p), p + (size_t)slots * 4, 0, 0};
+  else
+    return Table64{reinterpret_cast<int64_t*>(p)};
+}
+
 // Selective W advancing on candidate records: queues materialised (policy, then the record's
-// moves), at most max_pert - n_pert advances appended to the output record as moves.
-template <int VMAX>
+// moves), at most max_pert - n_pert advances appended to the output record as moves. list
+// (nullable): the candidates list[0 .. *list_n - 1] only.
+// RING: a 40-bit ring table of a.ring rows per stage per group (several times more candidates
+// fit a CU than with 64-bit full rows). Advancing a W never widens the queue window: the W moves
+// ahead only of entries that follow its own B, so a same-stage entry it passes has a micro-batch
+// at most the window below its own. A candidate whose starting window is below the ring's rows
+// therefore stays exact on the ring for every simulation of the search; the others, and those
+// whose times pass the 40-bit slots, join the redo list, which the 64-bit kernel then processes.
+template <int VMAX, bool RING>
 __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __restrict__ cap,
-                                                  uint8_t* __restrict__ out_cands) {
+                                                  uint8_t* __restrict__ out_cands,
+                                                  const int32_t* __restrict__ list,
+                                                  const int32_t* __restrict__ list_n) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int G = a.G, P = a.pr.P, M = a.pr.M;
   const int g = lane_id() / G;
   const int d = lane_id() % G;
   uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
-  const Table64 T{reinterpret_cast<int64_t*>(lds_group)};
+  const auto T = group_table<RING>(lds_group, a.slots);
   uint8_t* rec = lds_group + a.table_bytes;
   const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
   uint16_t* row = a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap;
@@ -1629,24 +1669,25 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
   group_bits(G, &gbit, &lsb);
   const int po = pert_off(a.pr.s_max);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
-  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < a.n; base += n_groups) {
-    const int64_t cand = base + g;
-    const bool has = g < a.CPW && cand < a.n;
-    const uint8_t* grec = a.cands + (has ? cand : 0) * a.pr.stride;
-    uint8_t* orec = out_cands + (has ? cand : 0) * a.pr.stride;
+  const int64_t total = list ? (int64_t)*list_n : a.n;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < total; base += n_groups) {
+    const bool has = g < a.CPW && base + g < total;
+    const int64_t cand = has ? (list ? (int64_t)list[base + g] : base + g) : 0;
+    const uint8_t* grec = a.cands + cand * a.pr.stride;
+    uint8_t* orec = out_cands + cand * a.pr.stride;
     if (has) stage_record(rec, grec, a.rec_bytes, d, G);
     __asm__ volatile("" ::: "memory");
     Resolved r;
     r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
     if (has) r = resolve_record(a.pr, grec);
-    const bool run = has && r.valid;
-    const int v = run ? r.v : 1;
+    const bool valid = has && r.valid;
+    const int v = valid ? r.v : 1;
     const int S = P * v;
-    const Ring ring = make_ring(M, M);
+    const Ring ring = make_ring(M, RING ? a.ring : M);
     Chunks<VMAX> c;
     int64_t busy = 0, stat = 0;
-    int n = 0;
-    if (run && d < P) {
+    int n = 0, wl = 0;
+    if (valid && d < P) {
       busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, a.pre_mem,
                                 &stat);
       n = materialise<VMAX>(a, c, v, r.gen, r.split, row);
@@ -1656,15 +1697,23 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
         if (pd != d) continue;
         move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
       }
+      if (RING) wl = queue_window<VMAX>(row, n);
     } else {
       zero_chunks<VMAX>(c);
     }
+    const bool on_ring = !RING || group_max((int64_t)wl, G) < ring.R;
+    const bool run = valid && on_ring;
     __asm__ volatile("" ::: "memory");
     const int n0 = run ? r.n_pert : 0;
     uint16_t* pert = reinterpret_cast<uint16_t*>(orec + po) + 3 * n0;
-    const AdvOut o = advance_w<VMAX>(T, row, n, c, ring, S, M, P, run, d < P ? cap[d] : 0, stat,
-                                     a.pr.max_pert - n0, G, gbit, lsb, has ? pert : nullptr);
+    const AdvOut o = advance_w<VMAX>(T, row, run ? n : 0, c, ring, S, M, P, run,
+                                     d < P ? cap[d] : 0, stat, a.pr.max_pert - n0, G, gbit, lsb,
+                                     has ? pert : nullptr);
     if (!has) continue;
+    if (RING && valid && (!on_ring || o.top >= Table40::LIMIT)) {
+      if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      continue;
+    }
     // the output record: the input's bytes (the new moves aside), then the move count
     const int halves = a.pr.stride >> 1;
     const int a0 = (po >> 1) + 3 * n0, a1 = a0 + 3 * o.adv;
@@ -1703,26 +1752,6 @@ struct TuneArgs {
 // int64 word of the chain state (after makespan, accepted count, bubble[P], peak[P]) holding an
 // upper bound of the window of the chain's queues (queue_window).
 __host__ __device__ __forceinline__ int window_word(int P) { return 2 + 2 * P; }
-
-// Window of a queue row: the largest m_i - m_j over entries i < j of one chunk (0 when every
-// chunk's micro-batches never go backwards by more than 0). When the window of every device is
-// below R, each op of micro-batch m precedes every op of m + R of the same stage.
-template <int VMAX>
-__device__ int queue_window(const uint16_t* row, int n) {
-  int hi[VMAX];
-#pragma unroll
-  for (int k = 0; k < VMAX; ++k) hi[k] = 0;
-  int w = 0;
-  for (int i = 0; i < n; ++i) {
-    const int e = row[i];
-    const int k = (e >> 11) & 7, m = e & 0x7FF;
-    const int h = pick<VMAX>(hi, k);
-    w = h - m > w ? h - m : w;
-#pragma unroll
-    for (int j = 0; j < VMAX; ++j) hi[j] = (k == j && m > h) ? m : hi[j];
-  }
-  return w;
-}
 
 // One move of a chain (step >= 1). (u0, u1, u2, u3) = Philox4x64-10(key = (seed, 0),
 // counter = (chain, step, 0, 0)); u0 mod 3 picks the family (§6's partitioning, placement and
@@ -2476,6 +2505,23 @@ Plan fast_plan(const octo_problem* p, int lds_max, int s_cap, int R, int streams
   return pl;
 }
 
+// 40-bit ring plan with one table per group (groups that run their own phases gain nothing from
+// interleaving): s_cap stages of R slots, then the staged record.
+Plan ring_plan(const octo_problem* p, int lds_max, int s_cap, int R) {
+  Plan pl;
+  pl.G = lanes_per_candidate(p->P);
+  pl.slots = (int)align_up((size_t)s_cap * R, 16);
+  pl.rec_bytes = pert_off(p->P * p->v_max);
+  pl.rec_stride = (int)align_up(pl.rec_bytes, 16);
+  pl.table_bytes = pl.slots * 5;
+  pl.group_bytes = pl.table_bytes + pl.rec_stride;
+  pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
+  pl.lds_bytes = pl.CPW * pl.group_bytes;
+  pl.strm_off = 0;
+  pl.qcap = 3 * p->v_max * p->M;
+  return pl;
+}
+
 // 64-bit-slot plan for materialised queues and tuner chains (record staged separately).
 Plan big_plan(const octo_problem* p, int lds_max) {
   Plan pl;
@@ -2693,7 +2739,7 @@ int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool wide, hip
 // sums, MERGE tables.
 // mem (nullable): layer memory [L][2], prefix-summed next to the costs.
 int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
-            hipStream_t stream, int64_t n, Setup* su) {
+            hipStream_t stream, int64_t n, Setup* su, int64_t extra_slots = 0) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
   int rc = dev_info(dev, &su->di);
@@ -2713,8 +2759,9 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
     if (rc) return rc;
   }
   su->l = layout(prob, su->big, n,
-                 std::max<int64_t>((int64_t)su->mat_grid * su->big.CPW,
-                                   (int64_t)su->m40_grid * std::max(su->m40.CPW, 0)));
+                 std::max<int64_t>({(int64_t)su->mat_grid * su->big.CPW,
+                                    (int64_t)su->m40_grid * std::max(su->m40.CPW, 0),
+                                    extra_slots}));
   Workspace& ws = g_ws[std::make_pair(dev, stream)];
   rc = ensure_buf(ws.base, ws.bytes, su->l.total, stream);
   if (rc) return rc;
@@ -2908,17 +2955,33 @@ int launch_tune_ring(const TuneArgs& t, const Plan& pl, int cus, int64_t n_chain
   return launch_ok();
 }
 
-// k_advance over n records; its queue rows are group slots of the workspace (mat_grid blocks).
-template <int VC>
-int launch_advance(const SimArgs& a, const Plan& pl, int cus, int mat_grid, const int64_t* cap,
-                   uint8_t* out, hipStream_t stream) {
+// k_advance over n records (or the list); its queue rows are group slots of the workspace, of
+// which there are at least max_grid blocks.
+template <int VC, bool RING>
+int launch_advance(const SimArgs& a, const Plan& pl, int cus, int max_grid, const int64_t* cap,
+                   uint8_t* out, const int32_t* list, const int32_t* list_n, hipStream_t stream) {
   int grid = 0;
-  int rc = occupancy_grid(k_advance<VC>, pl.lds_bytes, cus, &grid);
+  int rc = occupancy_grid(k_advance<VC, RING>, pl.lds_bytes, cus, &grid);
   if (rc) return rc;
   const int64_t need = (a.n + pl.CPW - 1) / pl.CPW;
-  grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min(grid, mat_grid), need));
-  hipLaunchKernelGGL(k_advance<VC>, dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a, cap, out);
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min(grid, max_grid), need));
+  hipLaunchKernelGGL((k_advance<VC, RING>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a, cap,
+                     out, list, list_n);
   return launch_ok();
+}
+
+// The ring pass of octo_advance_w: its plan and its grid (0: no ring pass for this problem).
+template <int VC>
+int advance_ring_grid(const octo_problem* prob, const DevInfo& di, int64_t n, Plan* rp,
+                      int* grid) {
+  *grid = 0;
+  const Ring rr = make_ring(prob->M, prob->P * prob->v_max);
+  *rp = ring_plan(prob, di.lds_max, prob->P * prob->v_max, rr.R);
+  if (rr.R >= prob->M || rp->CPW < 1) return OCTO_OK;
+  int rc = occupancy_grid(k_advance<VC, true>, rp->lds_bytes, di.cus, grid);
+  if (rc) return rc;
+  *grid = (int)std::max<int64_t>(1, std::min<int64_t>(*grid, (n + rp->CPW - 1) / rp->CPW));
+  return OCTO_OK;
 }
 
 int record_mark(int i, hipStream_t stream) {
@@ -3357,14 +3420,40 @@ int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const i
     return OCTO_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   std::lock_guard<std::mutex> lock(g_mu);
+  // ring pass first (its queue rows need grid * CPW group slots of the workspace), then the
+  // 64-bit pass over the candidates it left
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
+  DevInfo di;
+  if ((rc = dev_info(dev, &di))) return rc;
+  Plan rp;
+  int rgrid = 0;
+  rc = prob->v_max <= 2 ? advance_ring_grid<2>(prob, di, n, &rp, &rgrid)
+                        : advance_ring_grid<8>(prob, di, n, &rp, &rgrid);
+  if (rc) return rc;
   Setup su;
-  rc = prepare(prob, layer_costs, layer_mem, stream, 0, &su);
+  rc = prepare(prob, layer_costs, layer_mem, stream, n, &su, (int64_t)rgrid * rp.CPW);
   if (rc) return rc;
   SimArgs a = make_args(prob, su.big, su, link, candidates, n, out_makespan, out_bubble, out_peak);
   uint8_t* out = static_cast<uint8_t*>(out_candidates);
-  return prob->v_max <= 2
-             ? launch_advance<2>(a, su.big, su.di.cus, su.mat_grid, capacity, out, stream)
-             : launch_advance<8>(a, su.big, su.di.cus, su.mat_grid, capacity, out, stream);
+  const int32_t* list = nullptr;
+  const int32_t* list_n = nullptr;
+  if (rgrid > 0) {
+    SimArgs ar = make_args(prob, rp, su, link, candidates, n, out_makespan, out_bubble, out_peak);
+    ar.ring = make_ring(prob->M, prob->P * prob->v_max).R;
+    rc = prob->v_max <= 2
+             ? launch_advance<2, true>(ar, rp, di.cus, rgrid, capacity, out, nullptr, nullptr,
+                                       stream)
+             : launch_advance<8, true>(ar, rp, di.cus, rgrid, capacity, out, nullptr, nullptr,
+                                       stream);
+    if (rc) return rc;
+    list = a.redo;
+    list_n = a.ctl + CTL_REDO;
+  }
+  return prob->v_max <= 2 ? launch_advance<2, false>(a, su.big, su.di.cus, su.mat_grid, capacity,
+                                                     out, list, list_n, stream)
+                          : launch_advance<8, false>(a, su.big, su.di.cus, su.mat_grid, capacity,
+                                                     out, list, list_n, stream);
 }
 
 int octo_tune_step(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,

@@ -107,6 +107,14 @@ struct Table40 {
     lo[j] = (uint32_t)v;
     hi[j] = (uint8_t)(v >> 32);
   }
+  // Clear n slots of this group (its G lanes together).
+  __device__ __forceinline__ void clear(int n, int d, int G) const {
+    for (int i = d; i < n; i += G) {
+      const int j = (i << lg) | g;
+      lo[j] = 0;
+      hi[j] = 0;
+    }
+  }
   // Clear n slots of every group (all lanes of the wave together), 16 bytes per store; the
   // arrays start 16-byte aligned and a plan rounds both up to 16 bytes.
   __device__ __forceinline__ void clear_all(int n, int lane, int nlanes) const {

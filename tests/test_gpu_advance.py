@@ -83,7 +83,8 @@ def test_capacity_of_1f1b(gpu, P, M):
 @pytest.mark.parametrize("P,v_max,M,L,mp,pct", [
     (1, 1, 4, 3, 8, 30), (2, 2, 4, 6, 16, 30), (3, 2, 6, 14, 24, 30), (4, 2, 8, 16, 40, 20),
     (4, 3, 4, 14, 24, 30), (5, 1, 7, 9, 20, 40), (8, 2, 16, 24, 60, 30), (16, 1, 8, 20, 40, 30),
-    (8, 1, 32, 20, 80, 10), (4, 2, 64, 16, 120, 20),
+    (8, 1, 32, 20, 80, 10), (4, 2, 64, 16, 120, 20), (4, 2, 32, 16, 80, 20),
+    (3, 1, 16, 10, 40, 30), (6, 2, 24, 20, 60, 25),
 ])
 def test_random_structures(gpu, P, v_max, M, L, mp, pct):
     """Every policy and placement kind, records with moves already (some deadlocked), invalid
@@ -123,6 +124,33 @@ def test_in_place_and_huge_costs(gpu):
     g = run_advance(gpu, L, P, v_max, M, mp, costs, mem, cap, link, recs, in_place=True)
     r = R.advance_w(prob, costs, mem, cap, link, recs, NTHREADS)
     check_advance(g, r, "in place")
+
+
+@pytest.mark.parametrize("M", [8, 32])
+def test_huge_costs_ring_and_full_rows(gpu, M):
+    """Times beyond 2^37 ns, in place, on a shape whose search runs on 40-bit ring tables (M = 32:
+    such candidates are searched again on 64-bit rows, from the input record the ring pass left
+    as it was) and on one that uses 64-bit rows only (M = 8); the same records under ordinary
+    costs stay on the rings."""
+    rng = np.random.default_rng(47 + M)
+    P, v_max, L, mp = 4, 2, 12, 60
+    log(f"advance: huge costs M={M}")
+    costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+    huge = costs.copy()
+    huge[3] = [40_000_000_000, 30_000_000_000, 20_000_000_000]
+    mem = np.stack([rng.integers(1, 1 << 20, L), rng.integers(0, 1 << 24, L)], axis=1)
+    link = I.link_matrix(P, 5000)
+    recs = widen(I.random_candidates(rng, L, P, v_max, M, 200, policies=(3,)), P, v_max, mp)
+    prob = R.problem(L, P, v_max, M, recs.shape[1], mp)
+    _, _, pk0 = R.sim_batch_mem(prob, costs, mem, link, recs, NTHREADS)
+    cap = np.percentile(pk0, 25, axis=0).astype(np.int64)
+    for cs, label in ((costs, "ordinary"), (huge, "huge")):
+        g = run_advance(gpu, L, P, v_max, M, mp, cs, mem, cap, link, recs, in_place=True)
+        r = R.advance_w(prob, cs, mem, cap, link, recs, NTHREADS)
+        check_advance(g, r, f"{label} M={M}")
+        assert (g[0][:, 2] > recs[:, 2]).sum() > 20
+        if label == "huge":
+            assert (g[1] > (1 << 37)).sum() > 50
 
 
 def test_workload3_sample(gpu):
