@@ -40,6 +40,8 @@ constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
 constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
 constexpr int CTL_POS = 64;       // [NBINS] next index position of each bin (scatter cursor)
 constexpr int CTL_WORDS = 256;
+// rounds a materialised queue is read ahead of its use (GenMatK; rows of at least 8 entries)
+constexpr int QK = 6;
 
 struct SimArgs {
   Problem pr;
@@ -998,6 +1000,29 @@ __device__ int queue_window(const uint16_t* row, int n) {
   return w;
 }
 
+// The rounds of one evaluation over a materialised queue row of capacity qcap entries: read QK
+// rounds ahead (GenMatK) when the row holds at least eight entries, else one entry ahead;
+// rendezvous transfers take their own rounds (mbox: their mailboxes).
+template <int VMAX, int X, class Tab>
+__device__ __forceinline__ void rounds_mat(const uint16_t* row, int qcap, const Chunks<VMAX>& c,
+                                           const Ring& ring, Lane& L, const Tab& T, int G,
+                                           uint64_t gbit, uint64_t lsb, bool& dead,
+                                           int64_t* mbox) {
+  if constexpr (X != XR) {
+    if (qcap >= 8) {
+      GenMatK<QK> q;
+      q.init(row, qcap);
+      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+      relax_k<VMAX, X>(q, c, ring, L, T, G, gbit, lsb, dead);
+      return;
+    }
+  }
+  GenMat q;
+  q.init(row, L.nops);
+  describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
+  rounds<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, mbox);
+}
+
 // Move row[from] so that it ends at index to.
 __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
   const uint16_t x = row[from];
@@ -1079,12 +1104,9 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
       }
       if (has) T.clear(S * M, d, G);
       __asm__ volatile("" ::: "memory");
-      GenMat q;
-      q.init(row, L.nops);
-      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
       if constexpr (X == XR) mbox[lane_id()] = RDV_EMPTY;
       bool dead = false;
-      rounds<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, mbox);
+      rounds_mat<VMAX, X>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, mbox);
       const int64_t ms = group_max(L.clock, G);
       CommTally tot = L.cm;
       if constexpr (X == XC) tot = group_tally(L.cm, G);
@@ -1159,12 +1181,9 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
     __asm__ volatile("" ::: "memory");
     T.clear_all(a.slots, lane_id(), WAVE);  // every candidate's rows fit a.slots
     __asm__ volatile("" ::: "memory");
-    GenMat q;
-    q.init(row, L.nops);
-    describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
     if constexpr (X == XR) mbox[lane_id()] = RDV_EMPTY;
     bool dead = false;
-    rounds<VMAX, true, X>(q, c, ring, L, T, G, gbit, lsb, dead, mbox);
+    rounds_mat<VMAX, X>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, mbox);
     const int64_t ms = group_max(L.clock, G);
     CommTally tot = L.cm;
     if constexpr (X == XC) tot = group_tally(L.cm, G);
@@ -1374,10 +1393,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
     // A: the asynchronous schedule, finish times recorded
     bool dead = false;
     {
-      GenMat q;
-      q.init(row, L.nops);
-      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
-      relax<VMAX, true, XT>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      rounds_mat<VMAX, XT>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     }
     __syncthreads();  // every lane's finish times visible to the group
     // B: programs
@@ -1537,7 +1553,7 @@ __device__ __forceinline__ int next_eligible(const uint16_t* row, int n, int p, 
 // capacity; stat: its static bytes. pert (nullable): where advance k of the group is written as
 // (device, from, to), uint16 each, by the lane of that device.
 template <int VMAX, class Tab>
-__device__ AdvOut advance_w(const Tab& T, uint16_t* row, int n, const Chunks<VMAX>& c,
+__device__ AdvOut advance_w(const Tab& T, uint16_t* row, int n, int qcap, const Chunks<VMAX>& c,
                             const Ring& ring, int S, int M, int P, bool run, int64_t cap,
                             int64_t stat, int max_adv, int G, uint64_t gbit, uint64_t lsb,
                             uint16_t* pert) {
@@ -1558,10 +1574,7 @@ __device__ AdvOut advance_w(const Tab& T, uint16_t* row, int n, const Chunks<VMA
       L.clock = 0, L.pos = 0, L.nops = need && d < P ? n : 0, L.mem = L.peak = 0;
       if (need) T.clear(S * ring.R, d, G);
       __asm__ volatile("" ::: "memory");
-      GenMat q;
-      q.init(row, L.nops);
-      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
-      relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      rounds_mat<VMAX, XP>(row, qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       ms = group_max(L.clock, G);
       o.top = ms > o.top ? ms : o.top;
     }
@@ -1644,22 +1657,29 @@ __device__ __forceinline__ auto group_table(uint8_t* p, int slots) {
 
 // Selective W advancing on candidate records: queues materialised (policy, then the record's
 // moves), at most max_pert - n_pert advances appended to the output record as moves. list
-// (nullable): the candidates list[0 .. *list_n - 1] only.
+// (nullable): the candidates list[0 .. *list_n - 1] only; ctl[work]: the shared cursor.
+// Groups are persistent: the policy's steps run as in advance_w (simulations wave-wide, walks and
+// searches per group), and a group whose candidate is done writes it out and takes the next one
+// while the others go on, so that a wave is not held by its longest search (advance counts
+// range from none to hundreds).
 // RING: a 40-bit ring table of a.ring rows per stage per group (several times more candidates
 // fit a CU than with 64-bit full rows). Advancing a W never widens the queue window: the W moves
 // ahead only of entries that follow its own B, so a same-stage entry it passes has a micro-batch
 // at most the window below its own. A candidate whose starting window is below the ring's rows
 // therefore stays exact on the ring for every simulation of the search; the others, and those
 // whose times pass the 40-bit slots, join the redo list, which the 64-bit kernel then processes.
+constexpr int AW_LOAD = 5, AW_EXIT = 6;
 template <int VMAX, bool RING>
 __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __restrict__ cap,
                                                   uint8_t* __restrict__ out_cands,
                                                   const int32_t* __restrict__ list,
-                                                  const int32_t* __restrict__ list_n) {
+                                                  const int32_t* __restrict__ list_n, int work) {
   extern __shared__ __align__(16) uint8_t smem[];
   const int G = a.G, P = a.pr.P, M = a.pr.M;
   const int g = lane_id() / G;
   const int d = lane_id() % G;
+  const int gl = lane_id() - d;
+  const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
   uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
   const auto T = group_table<RING>(lds_group, a.slots);
   uint8_t* rec = lds_group + a.table_bytes;
@@ -1668,52 +1688,156 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
   const int po = pert_off(a.pr.s_max);
-  const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
   const int64_t total = list ? (int64_t)*list_n : a.n;
-  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < total; base += n_groups) {
-    const bool has = g < a.CPW && base + g < total;
-    const int64_t cand = has ? (list ? (int64_t)list[base + g] : base + g) : 0;
-    const uint8_t* grec = a.cands + cand * a.pr.stride;
-    uint8_t* orec = out_cands + cand * a.pr.stride;
-    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
-    __asm__ volatile("" ::: "memory");
-    Resolved r;
-    r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
-    if (has) r = resolve_record(a.pr, grec);
-    const bool valid = has && r.valid;
-    const int v = valid ? r.v : 1;
-    const int S = P * v;
-    const Ring ring = make_ring(M, RING ? a.ring : M);
-    Chunks<VMAX> c;
-    int64_t busy = 0, stat = 0;
-    int n = 0, wl = 0;
-    if (valid && d < P) {
-      busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, a.pre_mem,
-                                &stat);
-      n = materialise<VMAX>(a, c, v, r.gen, r.split, row);
-      const uint8_t* pp = grec + po;
-      for (int i = 0; i < r.n_pert; ++i) {
-        const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
-        if (pd != d) continue;
-        move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
+  const Ring ring = make_ring(M, RING ? a.ring : M);
+  const int64_t capd = d < P ? cap[d] : 0;
+
+  // the group's candidate and the state of its search
+  int phase = g < a.CPW ? AW_LOAD : AW_EXIT;
+  int64_t cand = 0;
+  Resolved r;
+  r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
+  Chunks<VMAX> c;
+  zero_chunks<VMAX>(c);
+  int64_t busy = 0, stat = 0, ms_first = 0;
+  int S = P, n = 0, n0 = 0, max_adv = 0;
+  int dstar = 0, p = -1, cursor = -1, first = -1, j = -1, at = -1;
+  AdvOut o;
+  o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0, o.top = 0;
+  for (;;) {
+    // groups without a candidate take the next one (invalid records and, on rings, candidates
+    // sent to the redo list are settled here)
+    while (phase == AW_LOAD) {
+      int e = 0;
+      if (d == 0) e = atomicAdd(&a.ctl[work], 1);
+      e = __shfl(e, gl);
+      if (e >= total) {
+        phase = AW_EXIT;
+        break;
       }
-      if (RING) wl = queue_window<VMAX>(row, n);
-    } else {
-      zero_chunks<VMAX>(c);
+      cand = list ? (int64_t)list[e] : (int64_t)e;
+      const uint8_t* grec = a.cands + cand * a.pr.stride;
+      stage_record(rec, grec, a.rec_bytes, d, G);
+      __asm__ volatile("" ::: "memory");
+      r = resolve_record(a.pr, grec);
+      const int v = r.valid ? r.v : 1;
+      S = P * v;
+      n = 0;
+      int wl = 0;
+      if (r.valid && d < P) {
+        busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, a.pre_mem,
+                                  &stat);
+        n = materialise<VMAX>(a, c, v, r.gen, r.split, row);
+        const uint8_t* pp = grec + po;
+        for (int i = 0; i < r.n_pert; ++i) {
+          const int pd = pp[6 * i] | (pp[6 * i + 1] << 8);
+          if (pd != d) continue;
+          move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8),
+                     pp[6 * i + 4] | (pp[6 * i + 5] << 8));
+        }
+        if (RING) wl = queue_window<VMAX>(row, n);
+      } else {
+        zero_chunks<VMAX>(c);
+        busy = stat = 0;
+      }
+      if (RING && r.valid && group_max((int64_t)wl, G) >= ring.R) {
+        if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+        continue;
+      }
+      __asm__ volatile("" ::: "memory");
+      n0 = r.valid ? r.n_pert : 0;
+      max_adv = a.pr.max_pert - n0;
+      o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0, o.top = 0;
+      dstar = 0, p = -1, cursor = -1, first = -1, j = -1, at = -1, ms_first = 0;
+      phase = r.valid ? AW_SIM : AW_DONE;
     }
-    const bool on_ring = !RING || group_max((int64_t)wl, G) < ring.R;
-    const bool run = valid && on_ring;
-    __asm__ volatile("" ::: "memory");
-    const int n0 = run ? r.n_pert : 0;
-    uint16_t* pert = reinterpret_cast<uint16_t*>(orec + po) + 3 * n0;
-    const AdvOut o = advance_w<VMAX>(T, row, run ? n : 0, c, ring, S, M, P, run,
-                                     d < P ? cap[d] : 0, stat, a.pr.max_pert - n0, G, gbit, lsb,
-                                     has ? pert : nullptr);
-    if (!has) continue;
-    if (RING && valid && (!on_ring || o.top >= Table40::LIMIT)) {
+    if (__ballot(phase != AW_EXIT) == 0) break;
+    uint16_t* pert =
+        reinterpret_cast<uint16_t*>(out_cands + cand * a.pr.stride + po) + 3 * n0;
+
+    // one simulation for every group that needs one
+    const bool need = phase == AW_SIM || phase == AW_TRIAL;
+    int64_t ms = 0;
+    bool dead = false;
+    if (__ballot(need) != 0) {
+      Lane L;
+      L.clock = 0, L.pos = 0, L.nops = need && d < P ? n : 0, L.mem = L.peak = 0;
+      if (need) T.clear(S * ring.R, d, G);
+      __asm__ volatile("" ::: "memory");
+      rounds_mat<VMAX, XP>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      ms = group_max(L.clock, G);
+      o.top = need && ms > o.top ? ms : o.top;
+    }
+    if (phase == AW_SIM) {
+      o.dead = dead;
+      o.ms = ms;
+      phase = dead ? AW_DONE : AW_WALK;
+    } else if (phase == AW_TRIAL) {
+      if (j == first) ms_first = ms;
+      if (ms <= o.ms) {
+        o.ms = ms;
+        if (d == dstar) {
+          pert[3 * o.adv] = (uint16_t)dstar, pert[3 * o.adv + 1] = (uint16_t)j;
+          pert[3 * o.adv + 2] = (uint16_t)p;
+        }
+        ++o.adv;
+        phase = AW_WALK;
+      } else {
+        if (d == dstar) move_entry(row, p, j);
+        cursor = j;
+        phase = AW_NEXT;
+      }
+    }
+    // walks and searches need no simulation: settle them before the next round
+    while (phase == AW_WALK || phase == AW_NEXT) {
+      if (phase == AW_WALK) {
+        if (d < P) act_walk<VMAX>(row, n, c, o.hi, at);
+        const bool over = d < P && stat + o.hi > capd;
+        const uint64_t om = (__ballot(over) >> gl) & gmask;
+        if (om == 0) {
+          o.fits = true;
+          phase = AW_DONE;
+        } else if (o.adv >= max_adv) {
+          phase = AW_DONE;
+        } else {
+          dstar = __ffsll((unsigned long long)om) - 1;
+          p = __shfl(at, gl + dstar);
+          cursor = p, first = -1;
+          phase = p < 0 ? AW_DONE : AW_NEXT;
+        }
+      } else {
+        int jj = d == dstar ? next_eligible<VMAX>(row, n, p, cursor, c) : -1;
+        jj = __shfl(jj, gl + dstar);
+        if (jj >= 0) {
+          first = first < 0 ? jj : first;
+          j = jj;
+          if (d == dstar) move_entry(row, jj, p);
+          phase = AW_TRIAL;
+        } else if (first >= 0) {
+          // every eligible W lengthens the makespan: take the earliest
+          j = first;
+          if (d == dstar) {
+            move_entry(row, first, p);
+            pert[3 * o.adv] = (uint16_t)dstar, pert[3 * o.adv + 1] = (uint16_t)first;
+            pert[3 * o.adv + 2] = (uint16_t)p;
+          }
+          o.ms = ms_first;
+          ++o.adv;
+          phase = AW_WALK;
+        } else {
+          phase = AW_DONE;
+        }
+      }
+    }
+    if (phase != AW_DONE) continue;
+    // the group's candidate is settled: write it out (or hand it to the 64-bit pass)
+    phase = AW_LOAD;
+    if (RING && r.valid && o.top >= Table40::LIMIT) {
       if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
       continue;
     }
+    const uint8_t* grec = a.cands + cand * a.pr.stride;
+    uint8_t* orec = out_cands + cand * a.pr.stride;
     // the output record: the input's bytes (the new moves aside), then the move count
     const int halves = a.pr.stride >> 1;
     const int a0 = (po >> 1) + 3 * n0, a1 = a0 + 3 * o.adv;
@@ -1723,7 +1847,8 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
       if (h != 1 && (h < a0 || h >= a1)) out16[h] = in16[h];
     if (d == 0) out16[1] = (uint16_t)((rec[2] + o.adv) | (rec[3] << 8));
     if (d < P) {
-      const int64_t sv = run ? (o.dead ? (int64_t)OCTO_MS_DEADLOCK : 0) : (int64_t)OCTO_MS_INVALID;
+      const int64_t sv =
+          r.valid ? (o.dead ? (int64_t)OCTO_MS_DEADLOCK : 0) : (int64_t)OCTO_MS_INVALID;
       if (d == 0) a.out_ms[cand] = sv ? sv : o.ms;
       a.out_bub[cand * P + d] = sv ? sv : o.ms - busy;
       a.out_peak[cand * P + d] = sv ? sv : stat + o.hi;
@@ -1915,8 +2040,8 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
     bool dead = false, fits = true;
     int64_t ms = 0, held = 0;
     if constexpr (MEM) {
-      const AdvOut o = advance_w<VMAX>(T, qrow, run && d < P ? qlen : 0, c, ring, S, M, P, run,
-                                       d < P ? t.cap[d] : 0, stat, t.max_adv, G, gbit, lsb,
+      const AdvOut o = advance_w<VMAX>(T, qrow, run && d < P ? qlen : 0, a.qcap, c, ring, S, M, P,
+                                       run, d < P ? t.cap[d] : 0, stat, t.max_adv, G, gbit, lsb,
                                        nullptr);
       dead = o.dead, fits = o.fits, ms = o.ms, held = o.hi;
     } else {
@@ -1924,10 +2049,7 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
       L.clock = 0, L.pos = 0, L.nops = run && d < P ? qlen : 0, L.mem = L.peak = 0;
       if (run) T.clear(S * M, d, G);
       __asm__ volatile("" ::: "memory");
-      GenMat q;
-      q.init(qrow, L.nops);
-      describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
-      relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+      rounds_mat<VMAX, XP>(qrow, a.qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
       ms = group_max(L.clock, G);
     }
 
@@ -2052,11 +2174,8 @@ __global__ void __launch_bounds__(WAVE) k_tune_ring(TuneArgs t) {
     __asm__ volatile("" ::: "memory");
     Lane L;
     L.clock = 0, L.pos = 0, L.nops = run && d < P ? qlen : 0, L.mem = L.peak = 0;
-    GenMat q;
-    q.init(row, L.nops);
-    describe<VMAX>(L, c, ring, q.kind, q.k, q.m);
     bool dead = false;
-    relax<VMAX, true, XP>(q, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    rounds_mat<VMAX, XP>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     const int64_t ms = group_max(L.clock, G);
 
     if (!has || skip) continue;
@@ -2966,7 +3085,7 @@ int launch_advance(const SimArgs& a, const Plan& pl, int cus, int max_grid, cons
   const int64_t need = (a.n + pl.CPW - 1) / pl.CPW;
   grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min(grid, max_grid), need));
   hipLaunchKernelGGL((k_advance<VC, RING>), dim3(grid), dim3(WAVE), pl.lds_bytes, stream, a, cap,
-                     out, list, list_n);
+                     out, list, list_n, RING ? CTL_WORK : CTL_WORK + 1);
   return launch_ok();
 }
 

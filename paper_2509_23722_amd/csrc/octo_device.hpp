@@ -358,6 +358,71 @@ struct GenMat {
   }
 };
 
+// Materialised queue row read K rounds ahead, for the unrolled speculative relaxation
+// (relax_k): in round t every lane loads a 16-byte span of eight entries starting at its
+// position (rounded down to a dword) into buffer t mod K, which round t + K consumes. A lane
+// advances at most one entry a round, so the entry after its position K rounds later is still
+// in that span (K <= 6); the loads are unconditional, so each buffer keeps its registers and a
+// round waits only for the load issued K rounds before. Spans are clamped to the row's capacity
+// (cap entries, rounded up to a dword), so every dword read holds a byte of the row: no read
+// leaves the pages the row lies in. Needs cap >= 8.
+template <int K>
+struct GenMatK {
+  static_assert(K >= 1 && K <= 6, "the span of eight entries covers K + 1 advances");
+  const uint32_t* base;  // the row's first entry, rounded down to a dword
+  int off, e0max;        // the row's first entry within that dword; the last span's start
+  int pos;               // position in the row
+  int kind, k, m;
+  uint4 buf[K];
+  int e0[K];             // first entry (from base, even) of each buffer's span
+  struct __attribute__((aligned(4))) Span {
+    uint32_t x, y, z, w;
+  };
+  __device__ __forceinline__ uint4 load(int e) const {
+    const Span v = *reinterpret_cast<const Span*>(base + (e >> 1));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
+  __device__ __forceinline__ int span_of(int p) const {
+    const int e = (p + off) & ~1;
+    return e < e0max ? e : e0max;
+  }
+  // entry j of a span: a select of one 64-bit half and a shift (a select chain over the four
+  // words would be turned into an indexed copy in private memory)
+  __device__ __forceinline__ void set(const uint4& b, int j) {
+    const uint64_t lo = (uint64_t)b.x | ((uint64_t)b.y << 32);
+    const uint64_t hi = (uint64_t)b.z | ((uint64_t)b.w << 32);
+    const uint64_t q = (j & 4) ? hi : lo;
+    const uint32_t e = (uint32_t)(q >> ((j & 3) * 16)) & 0xFFFFu;
+    kind = (int)((e >> 14) & 3);
+    k = (int)((e >> 11) & 7);
+    m = (int)(e & 0x7FF);
+  }
+  __device__ __forceinline__ void init(const uint16_t* r, int cap) {
+    off = (int)((reinterpret_cast<uintptr_t>(r) & 3) >> 1);
+    base = reinterpret_cast<const uint32_t*>(r - off);
+    e0max = ((off + cap + 1) & ~1) - 8;
+    pos = 0;
+    const uint4 b = load(0);
+#pragma unroll
+    for (int u = 0; u < K; ++u) buf[u] = b, e0[u] = 0;
+    set(b, off);
+  }
+  // speculative: the entry after the current one, from buffer U
+  template <int U>
+  __device__ __forceinline__ void advance(bool ok) {
+    pos += ok ? 1 : 0;
+    set(buf[U], pos + off - e0[U]);
+  }
+  // once per round, after the outcome: keep o's position if t, then refill buffer U
+  template <int U>
+  __device__ __forceinline__ void take_if(bool t, const GenMatK& o) {
+    pos = t ? o.pos : pos;
+    kind = t ? o.kind : kind, k = t ? o.k : k, m = t ? o.m : m;
+    e0[U] = span_of(pos);
+    buf[U] = load(e0[U]);
+  }
+};
+
 // ------------------------------------------------------------------------------------------
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): published multipliers and Weyl constants.
 // ------------------------------------------------------------------------------------------

@@ -258,19 +258,33 @@ __device__ __forceinline__ uint64_t fold_groups(uint64_t x, int G, uint64_t lsb)
 // latency hidden by other waves).
 // X: XM also tracks the activation bytes each device holds (L.mem) and their maximum
 // (L.peak); XC tallies communication nodes and their overlap (L.cm).
-template <int VMAX, bool SPEC, int X, class Tab, class Gen>
-__device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
-                                      const Tab& T, int G, uint64_t gbit, uint64_t lsb,
-                                      bool& dead, uint32_t* rec) {
-  bool live = L.pos < L.nops;
-  for (;;) {
+// Queue-generator steps of one round. Generators ignore the round's slot U; GenMatK reads and
+// refills its buffer U.
+template <int U, class Gen>
+__device__ __forceinline__ void gen_advance(Gen& g, bool ok) { g.advance(ok); }
+template <int U, class Gen>
+__device__ __forceinline__ void gen_take(Gen& g, bool t, const Gen& o) { g.take_if(t, o); }
+template <int U, int K>
+__device__ __forceinline__ void gen_advance(GenMatK<K>& g, bool ok) { g.template advance<U>(ok); }
+template <int U, int K>
+__device__ __forceinline__ void gen_take(GenMatK<K>& g, bool t, const GenMatK<K>& o) {
+  g.template take_if<U>(t, o);
+}
+
+// One round of relax (U: the round's slot for generators that keep per-round buffers). Returns
+// false once the wave has settled.
+template <int VMAX, bool SPEC, int X, int U, class Tab, class Gen>
+__device__ __forceinline__ bool relax_round(Gen& gen, const Chunks<VMAX>& c, const Ring& ring,
+                                            Lane& L, const Tab& T, int G, uint64_t gbit,
+                                            uint64_t lsb, bool& dead, uint32_t* rec, bool& live) {
+  {
     uint32_t plo, phi;
     T.issue(live ? L.rd : 0, plo, phi);
     Gen g2 = gen;
     Desc d2;
     if constexpr (SPEC) {
       // the next op, computed while the read is in flight; kept only if this op completes
-      g2.advance(true);
+      gen_advance<U>(g2, true);
       describe<VMAX>(d2, c, ring, g2.kind, g2.k, g2.m);
       // the slot is consumed only after the next op's descriptor exists
       __asm__ volatile("" : "+v"(plo), "+v"(phi), "+v"(d2.rd), "+v"(d2.want), "+v"(d2.dur));
@@ -314,18 +328,56 @@ __device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Rin
     L.pos += ok ? 1 : 0;
     live = L.pos < L.nops;
     if constexpr (SPEC) {
-      gen.take_if(ok, g2);
+      gen_take<U>(gen, ok, g2);
       L.take_if(ok, d2);
     } else {
-      gen.advance(ok);
+      gen_advance<U>(gen, ok);
       describe<VMAX>(L, c, ring, gen.kind, gen.k, gen.m);
     }
     __asm__ volatile("" ::: "memory");
     if (__ballot(ok) == 0) {
       const uint64_t actm = __ballot(live);
       if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
-      break;
+      return false;
     }
+  }
+  return true;
+}
+
+template <int VMAX, bool SPEC, int X, class Tab, class Gen>
+__device__ __forceinline__ void relax(Gen& gen, const Chunks<VMAX>& c, const Ring& ring, Lane& L,
+                                      const Tab& T, int G, uint64_t gbit, uint64_t lsb,
+                                      bool& dead, uint32_t* rec) {
+  bool live = L.pos < L.nops;
+  while (relax_round<VMAX, SPEC, X, 0>(gen, c, ring, L, T, G, gbit, lsb, dead, rec, live)) {
+  }
+}
+
+// relax over a queue read K rounds ahead (GenMatK): the loop is unrolled K times so that each
+// round's buffer is fixed registers, and it leaves only after a whole group of K rounds (a round
+// after the wave has settled changes nothing: no lane is ready, and the deadlock test gives the
+// same answer), so the loop has one exit and the load of each buffer is awaited only K rounds
+// after it was issued.
+template <int VMAX, int X, int K, int U, class Tab>
+__device__ __forceinline__ bool rounds_k(GenMatK<K>& gen, const Chunks<VMAX>& c, const Ring& ring,
+                                         Lane& L, const Tab& T, int G, uint64_t gbit,
+                                         uint64_t lsb, bool& dead, bool& live) {
+  const bool go =
+      relax_round<VMAX, true, X, U>(gen, c, ring, L, T, G, gbit, lsb, dead, nullptr, live);
+  if constexpr (U + 1 < K) {
+    const bool more = rounds_k<VMAX, X, K, U + 1>(gen, c, ring, L, T, G, gbit, lsb, dead, live);
+    return go && more;
+  } else {
+    return go;
+  }
+}
+
+template <int VMAX, int X, int K, class Tab>
+__device__ __forceinline__ void relax_k(GenMatK<K>& gen, const Chunks<VMAX>& c, const Ring& ring,
+                                        Lane& L, const Tab& T, int G, uint64_t gbit, uint64_t lsb,
+                                        bool& dead) {
+  bool live = L.pos < L.nops;
+  while (rounds_k<VMAX, X, K, 0>(gen, c, ring, L, T, G, gbit, lsb, dead, live)) {
   }
 }
 
