@@ -244,8 +244,10 @@ int octo_advance_w(const octo_problem* prob, const int64_t* layer_costs, const i
  *   +16+8P int64 current peak bytes[P] (written by octo_tune_step_mem only)
  *   +16+16P int64 an upper bound of the queues' micro-batch window (octo_tune_step only): the
  *          largest m_i - m_j over queue entries i < j of one stage on one device
- * Queue store: uint16 [n_chains][P][octo_queue_capacity(prob)]; entry = kind << 14 | chunk << 11
- * | m with kind 0 = F, 1 = B, 2 = W and chunk the index into the device's ascending stage list.
+ * Queue store: uint16 [n_chains][P][octo_queue_capacity(prob)], 16-byte aligned (else
+ * OCTO_EINVAL); the capacity is 3 v_max M rounded up to a multiple of 8 so that every row is
+ * 16-byte aligned too. Entry = kind << 14 | chunk << 11 | m with kind 0 = F, 1 = B, 2 = W and
+ * chunk the index into the device's ascending stage list.
  *
  * octo_tune_step(step = 0) validates each chain, generates its queues from the policy and
  * evaluates it. step t >= 1 draws (u0, u1, u2, u3) = Philox4x64-10(key = {seed, 0},

@@ -980,22 +980,42 @@ __device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>&
   return n;
 }
 
-// Window of a queue row: the largest m_i - m_j over entries i < j of one chunk (0 when every
-// chunk's micro-batches never go backwards by more than 0). When the window of every device is
-// below R, each op of micro-batch m precedes every op of m + R of the same stage.
+// Queue rows (the workspace's and the tuner's store) start 16-byte aligned and hold a multiple
+// of eight entries (queue_capacity), so a row reads in whole 16-byte spans, several in flight.
+// Entry u of a span (u a constant after unrolling).
+__device__ __forceinline__ uint32_t span_entry(const uint4& b, int u) {
+  const uint32_t w = u < 2 ? b.x : u < 4 ? b.y : u < 6 ? b.z : b.w;
+  return (u & 1) ? w >> 16 : w & 0xFFFFu;
+}
+
+// Span q (of 16-byte spans) of a row of n entries, clamped to the row's last span.
+__device__ __forceinline__ uint4 row_span(const uint16_t* row, int q, int n) {
+  return reinterpret_cast<const uint4*>(row)[min(q, max(n - 1, 0) >> 3)];
+}
+
+// Window of a queue row: the largest m_i - m_j over entries i < j of one chunk (0 when no
+// chunk's micro-batches ever go backwards). When the window of every device is below R, each op
+// of micro-batch m precedes every op of m + R of the same stage.
 template <int VMAX>
 __device__ int queue_window(const uint16_t* row, int n) {
   int hi[VMAX];
 #pragma unroll
   for (int k = 0; k < VMAX; ++k) hi[k] = 0;
   int w = 0;
-  for (int i = 0; i < n; ++i) {
-    const int e = row[i];
-    const int k = (e >> 11) & 7, m = e & 0x7FF;
-    const int h = pick<VMAX>(hi, k);
-    w = h - m > w ? h - m : w;
+  for (int i0 = 0; i0 < n; i0 += 32) {
+    uint4 b[4];
 #pragma unroll
-    for (int j = 0; j < VMAX; ++j) hi[j] = (k == j && m > h) ? m : hi[j];
+    for (int q = 0; q < 4; ++q) b[q] = row_span(row, (i0 >> 3) + q, n);
+#pragma unroll
+    for (int u = 0; u < 32; ++u) {
+      const uint32_t e = span_entry(b[u >> 3], u & 7);
+      const bool in = i0 + u < n;
+      const int k = (int)(e >> 11) & 7, m = (int)(e & 0x7FF);
+      const int h = pick<VMAX>(hi, k);
+      w = (in && h - m > w) ? h - m : w;
+#pragma unroll
+      for (int c = 0; c < VMAX; ++c) hi[c] = (in && k == c && m > h) ? m : hi[c];
+    }
   }
   return w;
 }
@@ -1024,12 +1044,28 @@ __device__ __forceinline__ void rounds_mat(const uint16_t* row, int qcap, const 
 }
 
 // Move row[from] so that it ends at index to.
+// Eight entries are read before any is written, so that their loads are in flight together.
 __device__ __forceinline__ void move_entry(uint16_t* row, int from, int to) {
   const uint16_t x = row[from];
-  if (from < to)
-    for (int i = from; i < to; ++i) row[i] = row[i + 1];
-  else
-    for (int i = from; i > to; --i) row[i] = row[i - 1];
+  uint16_t t[8];
+  int i = from;
+  if (from < to) {
+    for (; i + 8 <= to; i += 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = row[i + 1 + u];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) row[i + u] = t[u];
+    }
+    for (; i < to; ++i) row[i] = row[i + 1];
+  } else {
+    for (; i - 8 >= to; i -= 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = row[i - 1 - u];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) row[i - u] = t[u];
+    }
+    for (; i > to; --i) row[i] = row[i - 1];
+  }
   row[to] = x;
 }
 
@@ -1519,24 +1555,64 @@ __device__ __forceinline__ void act_walk(const uint16_t* row, int n, const Chunk
                                          int64_t& hi, int& at) {
   int64_t cur = 0;
   hi = 0, at = -1;
-  for (int i = 0; i < n; ++i) {
-    const uint32_t e = row[i];
-    const int kind = (int)(e >> 14) & 3;
-    const int64_t a = pick<VMAX>(c.mA, (int)(e >> 11) & 7);
-    if (kind == KF) {
-      cur += a;
-      if (cur > hi) hi = cur, at = i;
-    } else if (kind == KW || !c.split) {
-      cur -= a;
+  for (int i0 = 0; i0 < n; i0 += 32) {
+    uint4 b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) b[q] = row_span(row, (i0 >> 3) + q, n);
+#pragma unroll
+    for (int u = 0; u < 32; ++u) {
+      const uint32_t e = span_entry(b[u >> 3], u & 7);
+      const bool in = i0 + u < n;
+      const int kind = (int)(e >> 14) & 3;
+      const int64_t a = pick<VMAX>(c.mA, (int)(e >> 11) & 7);
+      const bool isF = kind == KF;
+      const bool rel = kind == KW || !c.split;
+      cur += !in ? 0 : isF ? a : rel ? -a : 0;
+      const bool up = in && isF && cur > hi;
+      hi = up ? cur : hi;
+      at = up ? i0 + u : at;
     }
   }
 }
 
 // First eligible W after position `from` (>= p): its B is not between p and it (a live queue
 // has B before W, so B precedes p), and its stage holds activations. -1 if none.
+// One pass from p + 1, spans two at a time, keeping the B's passed as a bit set over
+// (chunk, micro-batch) in registers when VMAX M <= 512; otherwise each W rescans (p, j).
 template <int VMAX>
 __device__ __forceinline__ int next_eligible(const uint16_t* row, int n, int p, int from,
-                                             const Chunks<VMAX>& c) {
+                                             const Chunks<VMAX>& c, int M) {
+  if (VMAX * M <= 512) {
+    uint64_t bs[8];
+#pragma unroll
+    for (int w = 0; w < 8; ++w) bs[w] = 0;
+    for (int j0 = (p + 1) & ~7; j0 < n; j0 += 16) {
+      uint4 b[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) b[q] = row_span(row, (j0 >> 3) + q, n);
+      int found = -1;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const uint32_t e = span_entry(b[u >> 3], u & 7);
+        const int j = j0 + u;
+        const bool in = j > p && j < n && found < 0;
+        const int kind = (int)(e >> 14) & 3, k = (int)(e >> 11) & 7;
+        const int bi = k * M + (int)(e & 0x7FF);
+        const int wd = (bi >> 6) & 7;
+        const uint64_t bit = 1ull << (bi & 63);
+        bool seen = false;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) seen = seen || (wd == w && (bs[w] & bit) != 0);
+        const bool elig =
+            in && kind == KW && j > from && !seen && pick<VMAX>(c.mA, k) > 0;
+        found = elig ? j : found;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) bs[w] |= (in && kind == KB && wd == w) ? bit : 0;
+      }
+      if (found >= 0) return found;
+    }
+    return -1;
+  }
   for (int j = from + 1; j < n; ++j) {
     const uint32_t e = row[j];
     if (((e >> 14) & 3) != (uint32_t)KW || pick<VMAX>(c.mA, (int)(e >> 11) & 7) <= 0) continue;
@@ -1616,7 +1692,7 @@ __device__ AdvOut advance_w(const Tab& T, uint16_t* row, int n, int qcap, const 
           phase = p < 0 ? AW_DONE : AW_NEXT;
         }
       } else {
-        int jj = d == dstar ? next_eligible<VMAX>(row, n, p, cursor, c) : -1;
+        int jj = d == dstar ? next_eligible<VMAX>(row, n, p, cursor, c, M) : -1;
         jj = __shfl(jj, gl + dstar);
         if (jj >= 0) {
           first = first < 0 ? jj : first;
@@ -1806,7 +1882,7 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
           phase = p < 0 ? AW_DONE : AW_NEXT;
         }
       } else {
-        int jj = d == dstar ? next_eligible<VMAX>(row, n, p, cursor, c) : -1;
+        int jj = d == dstar ? next_eligible<VMAX>(row, n, p, cursor, c, M) : -1;
         jj = __shfl(jj, gl + dstar);
         if (jj >= 0) {
           first = first < 0 ? jj : first;
@@ -2597,6 +2673,10 @@ struct Plan {
   int strm_off;  // table-driven plans: per-lane stream table after the finish tables
 };
 
+// Entries per materialised queue row: 3 v_max M rounded up to a multiple of eight, so that rows
+// start 16-byte aligned and read in whole 16-byte spans.
+int queue_cap(const octo_problem* p) { return (int)align_up((size_t)3 * p->v_max * p->M, 8); }
+
 int lanes_per_candidate(int P) {
   int G = 1;
   while (G < P) G <<= 1;
@@ -2620,7 +2700,7 @@ Plan fast_plan(const octo_problem* p, int lds_max, int s_cap, int R, int streams
   while (pl.CPW & (pl.CPW - 1)) pl.CPW &= pl.CPW - 1;  // interleaving uses shifts
   pl.strm_off = (int)align_up((size_t)pl.CPW * pl.group_bytes, 16);
   pl.lds_bytes = streams > 0 ? pl.strm_off + strm : pl.CPW * pl.group_bytes;
-  pl.qcap = 3 * p->v_max * p->M;
+  pl.qcap = queue_cap(p);
   return pl;
 }
 
@@ -2637,7 +2717,7 @@ Plan ring_plan(const octo_problem* p, int lds_max, int s_cap, int R) {
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
   pl.lds_bytes = pl.CPW * pl.group_bytes;
   pl.strm_off = 0;
-  pl.qcap = 3 * p->v_max * p->M;
+  pl.qcap = queue_cap(p);
   return pl;
 }
 
@@ -2653,7 +2733,7 @@ Plan big_plan(const octo_problem* p, int lds_max) {
   pl.CPW = std::min(WAVE / pl.G, lds_max / pl.group_bytes);
   pl.lds_bytes = pl.CPW * pl.group_bytes;
   pl.strm_off = 0;
-  pl.qcap = 3 * p->v_max * p->M;
+  pl.qcap = queue_cap(p);
   return pl;
 }
 
@@ -3253,7 +3333,9 @@ int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   if (n_chains == 0) return OCTO_OK;
   if (!layer_costs || !link || !chains || !queues) return OCTO_EINVAL;
   if (MEM && (!layer_mem || !capacity)) return OCTO_EINVAL;
-  if ((reinterpret_cast<uintptr_t>(chains) & 15) != 0) return OCTO_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(chains) & 15) != 0 ||
+      (reinterpret_cast<uintptr_t>(queues) & 15) != 0)
+    return OCTO_EINVAL;
   std::lock_guard<std::mutex> lock(g_mu);
   // the ring pass's redo list holds int32 chain indices, one per chain
   const bool ring_pass = !MEM && n_chains <= (int64_t)INT32_MAX;
@@ -3462,7 +3544,7 @@ int32_t octo_chain_stride(const octo_problem* prob) {
 
 int32_t octo_queue_capacity(const octo_problem* prob) {
   if (check_problem(prob)) return OCTO_EINVAL;
-  return 3 * prob->v_max * prob->M;
+  return queue_cap(prob);
 }
 
 int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,

@@ -38,6 +38,8 @@ def test_argument_checks_without_gpu():
     good = _lib.problem(16, 4, 1, 8, inputs.record_stride(4, 1, 0), 0)
     assert _lib.chain_stride(good) == (good.cand_stride + 24 + 16 * 4 + 15) // 16 * 16
     assert _lib.queue_capacity(good) == 3 * 1 * 8
+    # rows hold a multiple of eight entries (16-byte spans)
+    assert _lib.queue_capacity(_lib.problem(9, 4, 1, 5, inputs.record_stride(4, 1, 0), 0)) == 16
     bad = [
         _lib.problem(16, 65, 1, 8, 256, 0),       # P > 64
         _lib.problem(0, 4, 1, 8, 32, 0),          # L < 1
