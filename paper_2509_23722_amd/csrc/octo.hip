@@ -1020,6 +1020,15 @@ __device__ int queue_window(const uint16_t* row, int n) {
   return w;
 }
 
+// The finish table of one group: 40-bit slots (RING) or 64-bit, at the start of its LDS area.
+template <bool RING>
+__device__ __forceinline__ auto group_table(uint8_t* p, int slots) {
+  if constexpr (RING)
+    return Table40{reinterpret_cast<uint32_t*>(p), p + (size_t)slots * 4, 0, 0};
+  else
+    return Table64{reinterpret_cast<int64_t*>(p)};
+}
+
 // The rounds of one evaluation over a materialised queue row of capacity qcap entries: read QK
 // rounds ahead (GenMatK) when the row holds at least eight entries, else one entry ahead;
 // rendezvous transfers take their own rounds (mbox: their mailboxes).
@@ -1367,8 +1376,15 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
   return n;
 }
 
-template <int VMAX>
-__global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
+// RING: 40-bit ring tables of a.ring rows per stage per group. Phase C keeps each device's
+// computations in queue order and adds only the sends, each of which reads its producer's slot
+// after the producer and before any later computation of the stage, so the ring argument of
+// k_tune_ring holds for both rounds; a candidate whose queue window reaches the ring, or whose
+// times pass 40 bits, joins the redo list that the 64-bit kernel (list, list_n) then takes.
+template <int VMAX, bool RING>
+__global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
+                                                  const int32_t* __restrict__ list,
+                                                  const int32_t* __restrict__ list_n) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int64_t mbox[WAVE];    // transfer end posted by the receiver, per sender lane
   __shared__ int64_t obt[WAVE];     // outbox: the sender's announce time ...
@@ -1378,7 +1394,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
   const int d = lane_id() % G;
   const int me = lane_id(), g0 = me - d;
   uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
-  const Table64 T{reinterpret_cast<int64_t*>(lds_group)};
+  const auto T = group_table<RING>(lds_group, a.slots);
   uint8_t* rec = lds_group + a.table_bytes;
   const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
   const int dl = d < P ? d : 0;
@@ -1390,20 +1406,20 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
-  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < a.n; base += n_groups) {
-    const int64_t cand = base + g;
-    const bool has = g < a.CPW && cand < a.n;
-    const uint8_t* grec = a.cands + (has ? cand : 0) * a.pr.stride;
+  const int64_t total = list ? (int64_t)*list_n : a.n;
+  const Ring ring = make_ring(M, RING ? a.ring : M);
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < total; base += n_groups) {
+    const bool has = g < a.CPW && base + g < total;
+    const int64_t cand = has ? (list ? (int64_t)list[base + g] : base + g) : 0;
+    const uint8_t* grec = a.cands + cand * a.pr.stride;
     if (has) stage_record(rec, grec, a.rec_bytes, d, G);
     __syncthreads();
     Resolved r;
     r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
     if (has) r = resolve_record(a.pr, grec);
-    const bool run = has && r.valid;
-    const bool mine = run && d < P;
-    const int v = run ? r.v : 1;
+    const bool valid = has && r.valid;
+    const int v = valid ? r.v : 1;
     const int S = P * v;
-    const Ring ring = make_ring(M, M);
     Chunks<VMAX> c;
     int64_t busy = 0;
     Lane L;
@@ -1411,7 +1427,8 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
     L.cm.reset();
     L.fs = -1;
     L.tb = tb, L.tS = S, L.tM = M;
-    if (mine) {
+    int wl = 0;
+    if (valid && d < P) {
       busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, nullptr,
                                 nullptr, XR);
       L.nops = materialise<VMAX>(a, c, v, r.gen, r.split, row);
@@ -1421,10 +1438,15 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
         if (pd != d) continue;
         move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
       }
+      if (RING) wl = queue_window<VMAX>(row, L.nops);
     } else {
       zero_chunks<VMAX>(c);
     }
-    if (run) T.clear(S * M, d, G);
+    const bool on_ring = !RING || group_max((int64_t)wl, G) < ring.R;
+    const bool run = valid && on_ring;
+    const bool mine = run && d < P;
+    if (!mine) L.nops = 0;
+    if (run) T.clear(S * ring.R, d, G);
     __syncthreads();
     // A: the asynchronous schedule, finish times recorded
     bool dead = false;
@@ -1435,7 +1457,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
     // B: programs
     int plen = 0;
     if (mine && !dead) plen = build_program<VMAX>(c, row, L.nops, tb, S, M, rkey, rid, prog);
-    if (run) T.clear(S * M, d, G);
+    if (run) T.clear(S * ring.R, d, G);
     mbox[me] = RDV_EMPTY;
     obn[me] = OB_NONE;
     obt[me] = 0;
@@ -1464,8 +1486,10 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
           rd = D.rd, wr = D.wr, store = D.store, mask = (uint32_t)D.mask, want = (uint32_t)D.want;
           state = D.state, w = D.w, dur = D.dur;
         } else if (type == PI_SEND) {  // its producer (an own op) must have finished
-          rd = s * M + m;
-          mask = want = kind == KF ? ST_F : ST_B;
+          rd = s * ring.R + (m & ring.mask);
+          const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
+          mask = (kind == KF ? ST_F : ST_B) | ST_PAR;
+          want = (kind == KF ? ST_F : ST_B) | (par ? ST_PAR : 0u);
         } else {  // receive: the producer's device and the consumer's link weight
           src = devs[s];
           const int cs = kind == KF ? s + 1 : s - 1;
@@ -1514,11 +1538,15 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob) {
       }
     }
     const int64_t ms = group_max(clock, G);
-    if (mine) {
+    // overflow test over both rounds' clocks (phase A's alone when it deadlocked)
+    const int64_t top = RING ? group_max(clock > L.clock ? clock : L.clock, G) : 0;
+    if (has && valid && (!on_ring || top >= Table40::LIMIT)) {
+      if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+    } else if (mine) {
       const int64_t sv = dead || cdead ? (int64_t)OCTO_MS_DEADLOCK : 0;
       if (d == 0) a.out_ms[cand] = sv ? sv : ms;
       a.out_bub[cand * P + d] = sv ? sv : ms - busy;
-    } else if (has && !run && d < P) {
+    } else if (has && !valid && d < P) {
       if (d == 0) a.out_ms[cand] = OCTO_MS_INVALID;
       a.out_bub[cand * P + d] = OCTO_MS_INVALID;
     }
@@ -1720,15 +1748,6 @@ __device__ AdvOut advance_w(const Tab& T, uint16_t* row, int n, int qcap, const 
     if (__ballot(phase != AW_DONE) == 0) break;
   }
   return o;
-}
-
-// The finish table of one group: 40-bit slots (RING) or 64-bit, at the start of its LDS area.
-template <bool RING>
-__device__ __forceinline__ auto group_table(uint8_t* p, int slots) {
-  if constexpr (RING)
-    return Table40{reinterpret_cast<uint32_t*>(p), p + (size_t)slots * 4, 0, 0};
-  else
-    return Table64{reinterpret_cast<int64_t*>(p)};
 }
 
 // Selective W advancing on candidate records: queues materialised (policy, then the record's
@@ -3469,17 +3488,42 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
 
 
 // The reordered coordination behind octo_sim_batch_ordered: k_ordered over all records, one
-// group per candidate, its scratch sized for the materialised-queue grid's group slots.
+// group per candidate — first on 40-bit ring tables (when the ring is shorter than M), then on
+// 64-bit full rows over the candidates the ring pass left (or over all of them). The scratch
+// (finish-time buffers, receive keys, programs) is sized for the larger pass's group slots.
 template <int VC>
-int launch_ordered(const octo_problem* prob, const Setup& su, const int64_t* link,
+int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    const void* cands, int64_t n, int64_t* ms, int64_t* bub, hipStream_t stream) {
-  SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
-  int grid = 0;
-  int rc = occupancy_grid(k_ordered<VC>, su.big.lds_bytes, su.di.cus, &grid);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
+  DevInfo di;
+  int rc = dev_info(dev, &di);
   if (rc) return rc;
-  const int64_t need = (n + su.big.CPW - 1) / su.big.CPW;
-  grid = (int)std::max<int64_t>(1, std::min<int64_t>(std::min(grid, su.mat_grid), need));
-  const size_t slots = (size_t)su.mat_grid * su.big.CPW;
+  const Ring rr = make_ring(prob->M, prob->P * prob->v_max);
+  const Plan rp = ring_plan(prob, di.lds_max, prob->P * prob->v_max, rr.R);
+  int rgrid = 0;
+  if (rr.R < prob->M && rp.CPW >= 1) {
+    if ((rc = occupancy_grid(k_ordered<VC, true>, rp.lds_bytes, di.cus, &rgrid))) return rc;
+    rgrid = (int)std::max<int64_t>(1, std::min<int64_t>(rgrid, (n + rp.CPW - 1) / rp.CPW));
+    // at most 4 GiB of per-slot scratch (finish times, receive keys, programs, queue rows)
+    const size_t per_slot = (size_t)prob->P * prob->v_max * prob->M * (3 * 8 + 2 * 12 + 7 * 4) +
+                            (size_t)prob->P * queue_cap(prob) * 2;
+    const int64_t max_blocks = std::max<int64_t>(1, ((int64_t)4 << 30) / per_slot / rp.CPW);
+    rgrid = (int)std::min<int64_t>(rgrid, max_blocks);
+  }
+  Setup su;
+  if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su))) return rc;
+  int grid = 0;
+  if ((rc = occupancy_grid(k_ordered<VC, false>, su.big.lds_bytes, su.di.cus, &grid))) return rc;
+  grid = (int)std::max<int64_t>(
+      1, std::min<int64_t>(std::min(grid, su.mat_grid), (n + su.big.CPW - 1) / su.big.CPW));
+  // group slots: the ring pass's and the full-row pass's share the same buffers (one at a time)
+  const size_t slots = std::max((size_t)grid * su.big.CPW, (size_t)rgrid * std::max(rp.CPW, 0));
+  const size_t qslots = (size_t)su.mat_grid * su.big.CPW;
+  if (slots > qslots) {
+    // the queue rows of the workspace cover mat_grid * CPW slots; take a larger workspace
+    if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su, (int64_t)slots))) return rc;
+  }
   OrdBufs ob;
   ob.rcap = 2 * prob->v_max * prob->M;
   ob.pcap = 7 * prob->v_max * prob->M;
@@ -3498,7 +3542,20 @@ int launch_ordered(const octo_problem* prob, const Setup& su, const int64_t* lin
   ob.rkey = reinterpret_cast<int64_t*>(base + o_rk);
   ob.rid = reinterpret_cast<uint32_t*>(base + o_ri);
   ob.prog = reinterpret_cast<uint32_t*>(base + o_pg);
-  hipLaunchKernelGGL(k_ordered<VC>, dim3(grid), dim3(WAVE), su.big.lds_bytes, stream, a, ob);
+  SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
+  const int32_t* list = nullptr;
+  const int32_t* list_n = nullptr;
+  if (rgrid > 0) {
+    SimArgs ar = make_args(prob, rp, su, link, cands, n, ms, bub);
+    ar.ring = rr.R;
+    hipLaunchKernelGGL((k_ordered<VC, true>), dim3(rgrid), dim3(WAVE), rp.lds_bytes, stream, ar,
+                       ob, nullptr, nullptr);
+    if ((rc = launch_ok())) return rc;
+    list = a.redo;
+    list_n = a.ctl + CTL_REDO;
+  }
+  hipLaunchKernelGGL((k_ordered<VC, false>), dim3(grid), dim3(WAVE), su.big.lds_bytes, stream, a,
+                     ob, list, list_n);
   return launch_ok();
 }
 
@@ -3512,12 +3569,10 @@ int ordered_impl(const octo_problem* prob, const int64_t* layer_costs, const int
   if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
   if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
   std::lock_guard<std::mutex> lock(g_mu);
-  Setup su;
-  rc = prepare(prob, layer_costs, nullptr, stream, 0, &su);
-  if (rc) return rc;
-  return prob->v_max <= 2
-             ? launch_ordered<2>(prob, su, link, candidates, n, out_makespan, out_bubble, stream)
-             : launch_ordered<8>(prob, su, link, candidates, n, out_makespan, out_bubble, stream);
+  return prob->v_max <= 2 ? launch_ordered<2>(prob, layer_costs, link, candidates, n,
+                                              out_makespan, out_bubble, stream)
+                          : launch_ordered<8>(prob, layer_costs, link, candidates, n,
+                                              out_makespan, out_bubble, stream);
 }
 
 }  // namespace

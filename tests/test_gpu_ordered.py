@@ -113,13 +113,15 @@ def test_workload4_and_huge(gpu):
     sample = np.arange(0, len(recs), 10)
     r = run_oracle(w.L, w.P, w.v_max, w.M, w.max_pert, costs, link, recs[sample])
     assert_same(tuple(x[sample] for x in g), r, "workload 4 sample")
-    rng = np.random.default_rng(126)
-    P, v_max, M, L = 4, 2, 8, 12
-    costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
-    costs[5] = [40_000_000_000, 30_000_000_000, 20_000_000_000]
-    link = I.link_matrix(P, 20_000_000_000)
-    recs = I.random_candidates(rng, L, P, v_max, M, 300, max_pert=1, pert_rate=0.1)
-    args = (L, P, v_max, M, 1, costs, link, recs)
-    g = run_gpu(gpu, *args)
-    assert_same(g, run_oracle(*args), "huge")
-    assert (g[0] > (1 << 37)).sum() > 10
+    # M = 8: 64-bit rows only; M = 32: 40-bit rings first, such candidates redone on 64 bits
+    for M in (8, 32):
+        rng = np.random.default_rng(126 + M)
+        P, v_max, L = 4, 2, 12
+        costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+        costs[5] = [40_000_000_000, 30_000_000_000, 20_000_000_000]
+        link = I.link_matrix(P, 20_000_000_000)
+        recs = I.random_candidates(rng, L, P, v_max, M, 300, max_pert=1, pert_rate=0.1)
+        args = (L, P, v_max, M, 1, costs, link, recs)
+        g = run_gpu(gpu, *args)
+        assert_same(g, run_oracle(*args), f"huge M={M}")
+        assert (g[0] > (1 << 37)).sum() > 10
