@@ -38,6 +38,8 @@ constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (7)
 constexpr int CTL_WORK_MAT = 136; // chunk counter of k_sim_mat, perturbed list
 constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
 constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
+constexpr int CTL_WIDE = 139;     // perturbed candidates whose queue window passes the ring
+constexpr int CTL_WORK_WIDE = 140;// chunk counter of k_sim_mat40 over the wide list
 constexpr int CTL_POS = 64;       // [NBINS] next index position of each bin (scatter cursor)
 constexpr int CTL_WORDS = 256;
 // rounds a materialised queue is read ahead of its use (GenMatK; rows of at least 8 entries)
@@ -60,7 +62,10 @@ struct SimArgs {
   int32_t* ctl;
   const int32_t* idx;    // candidate indices sorted by bin
   int32_t* redo;         // candidates to recompute with 64-bit slots
+  int32_t* wide;         // perturbed candidates too wide for the ring (k_sim_mat40 full rows)
   const uint32_t* mtab;  // MERGE tables, merge_offset() entries apart
+  const uint16_t* mrows; // v = 2 MERGE queues by (split, s0, s1) (merge_rows); null: none
+  int mrow_stride;       // entries per row of mrows
   uint16_t* qscratch;    // materialised queues, [group slot][P][qcap]
   int G, CPW;            // lanes per candidate, candidates per wave
   int slots;             // slots of one finish table (S_cap * M)
@@ -956,6 +961,41 @@ __device__ __forceinline__ void emit_queue(Gen& g, uint16_t* row, int n) {
   }
 }
 
+// Copy the first n entries of a queue row (both rows 16-byte aligned; whole 16-byte spans, the
+// last one padded within the rows' capacities), eight spans in flight.
+__device__ __forceinline__ void copy_row(const uint16_t* src, uint16_t* dst, int n) {
+  const uint4* s4 = reinterpret_cast<const uint4*>(src);
+  uint4* d4 = reinterpret_cast<uint4*>(dst);
+  const int spans = (n + 7) >> 3;
+  for (int q0 = 0; q0 < spans; q0 += 8) {
+    uint4 t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (q0 + u < spans) t[u] = s4[q0 + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (q0 + u < spans) d4[q0 + u] = t[u];
+  }
+}
+
+// The v = 2 MERGE queue of a device hosting stages s0 < s1 (both splits), as materialise would
+// generate it, for every stage pair: row (split * S + s0) * S + s1 of `rows`, S = 2P, `stride`
+// entries apart. Built once per (P, v_max, M) beside the MERGE tables, so that materialising
+// such a queue is a copy in 16-byte spans instead of a merge with one dependent table load per
+// entry. One thread per row.
+__global__ void k_merge_rows(int P, int M, const uint32_t* __restrict__ mtab,
+                             uint16_t* __restrict__ rows, int stride) {
+  const int S = 2 * P;
+  const int t = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (t >= 2 * S * S) return;
+  const int split = t / (S * S), s0 = (t / S) % S, s1 = t % S;
+  if (s0 >= s1) return;
+  GenMerge<2> g;
+  g.init(mtab + merge_offset(P, M, 2, split), (split ? 3 : 2) * M, 2,
+         [&](int k) { return k == 0 ? s0 : s1; });
+  emit_queue(g, rows + (size_t)t * stride, (split ? 3 : 2) * 2 * M);
+}
+
 // Materialise the queue of lane d for a staged record; returns the queue length.
 template <int VMAX>
 __device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>& c, int v,
@@ -971,6 +1011,9 @@ __device__ __forceinline__ int materialise(const SimArgs& a, const Chunks<VMAX>&
     const int r = c.st[0];
     g.init(P, v, M, r, split, split ? r : 0);
     emit_queue(g, row, n);
+  } else if (v == 2 && a.mrows) {
+    const int S2 = 2 * P;
+    copy_row(a.mrows + ((size_t)(split * S2 + c.st[0]) * S2 + c.st[1]) * a.mrow_stride, row, n);
   } else {
     GenMerge<VMAX> g;
     g.init(a.mtab + (v >= 2 ? merge_offset(P, M, v, split) : 0), (split ? 3 : 2) * M, v,
@@ -1161,12 +1204,16 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
 }
 
 
-// Candidates with perturbations, 40-bit slots in full rows (R = M) shared by the wave's groups
-// like the generated kernels (5 bytes a slot instead of 8, so more waves fit a CU): queues
-// materialised in global memory, moves applied. A candidate whose times pass the 40-bit slots
-// joins the redo list of the 64-bit kernel, which runs after this one.
+// Candidates with perturbations, 40-bit slots shared by the wave's groups like the generated
+// kernels (5 bytes a slot instead of 8, so more waves fit a CU), in rings of a.ring rows per
+// stage (twice the window of the interleaved orders, so that orders a few moves away from a
+// generated one fit; see k_tune_ring for why a ring is exact when the queue window is below
+// it): queues materialised in global memory, moves applied. A candidate whose window reaches
+// the ring joins the wide list, which a second launch (wide_pass, full rows: a.ring = M) takes;
+// one whose times pass the 40-bit slots joins the redo list of the 64-bit kernel, which runs
+// after both.
 template <int VMAX, int X>
-__global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
+__global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a, int mode) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int64_t mbox[X == XR ? WAVE : 1];  // rendezvous mailboxes
   const int G = a.G, P = a.pr.P, M = a.pr.M;
@@ -1180,17 +1227,21 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
   uint16_t* row = a.qscratch + ((size_t)slot * P + (d < P ? d : 0)) * a.qcap;
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
-  const int base = a.ctl[CTL_START + BIN_MAT];
-  const int cnt = a.ctl[CTL_COUNTS + BIN_MAT];
+  // mode bit 0: take the wide list of the ring pass, not the perturbed candidates of the bin
+  // index; bit 1: send candidates wider than the ring to the redo list (no full-row pass)
+  const bool wide_pass = (mode & 1) != 0;
+  const int32_t* list = wide_pass ? a.wide : a.idx + a.ctl[CTL_START + BIN_MAT];
+  const int cnt = wide_pass ? a.ctl[CTL_WIDE] : a.ctl[CTL_COUNTS + BIN_MAT];
+  const int work = wide_pass ? CTL_WORK_WIDE : CTL_WORK_MAT;
   if (cnt == 0) return;
-  const Ring ring = make_ring(M, M);
+  const Ring ring = make_ring(M, a.ring);
   for (;;) {
     int ch = 0;
-    if (lane_id() == 0) ch = atomicAdd(&a.ctl[CTL_WORK_MAT], 1);
+    if (lane_id() == 0) ch = atomicAdd(&a.ctl[work], 1);
     ch = bcast(ch);
     if (ch * a.CPW >= cnt) break;
     const int e = ch * a.CPW + g;
-    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[base + e] : -1;
+    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)list[e] : -1;
     const bool has = cand >= 0;
     const bool mine = has && d < P;
     const uint8_t* grec = has ? a.cands + cand * a.pr.stride : a.cands;
@@ -1203,6 +1254,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
     if (has) gen = resolve_record(a.pr, grec).gen;
     Chunks<VMAX> c;
     int64_t busy = 0, stat = 0;
+    int wl = 0;
     Lane L;
     L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
     L.cm.reset();
@@ -1220,8 +1272,20 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
         if (pd != d) continue;
         move_entry(row, pp[6 * i + 2] | (pp[6 * i + 3] << 8), pp[6 * i + 4] | (pp[6 * i + 5] << 8));
       }
+      if (ring.R < M) wl = queue_window<VMAX>(row, L.nops);
     } else {
       zero_chunks<VMAX>(c);
+    }
+    // a candidate whose order does not fit the ring goes to the wide list (full rows)
+    const bool on_ring = group_max((int64_t)wl, G) < ring.R;
+    if (!on_ring) {
+      L.nops = 0;
+      if (mine && d == 0) {
+        if (mode & 2)
+          a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+        else
+          a.wide[atomicAdd(&a.ctl[CTL_WIDE], 1)] = (int32_t)cand;
+      }
     }
     __asm__ volatile("" ::: "memory");
     T.clear_all(a.slots, lane_id(), WAVE);  // every candidate's rows fit a.slots
@@ -1232,7 +1296,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a) {
     const int64_t ms = group_max(L.clock, G);
     CommTally tot = L.cm;
     if constexpr (X == XC) tot = group_tally(L.cm, G);
-    if (mine) {
+    if (mine && on_ring) {
       if (ms >= Table40::LIMIT) {
         if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
       } else {
@@ -2627,6 +2691,9 @@ struct Workspace {
   size_t mt_bytes = 0;
   bool mt_valid = false;
   int mt_P = 0, mt_vmax = 0, mt_M = 0;
+  // v = 2 MERGE queues by stage pair (k_merge_rows), rebuilt with the MERGE tables
+  void* mr = nullptr;
+  size_t mr_bytes = 0;
   // largest number of micro-batches in flight per stage, per generated bin of v = 1, 2
   int inflight[NBIN_GEN] = {};
   int if_P = 0, if_M = 0;
@@ -2760,9 +2827,15 @@ size_t mtab_entries(const octo_problem* p) {
   return p->v_max >= 2 ? (size_t)merge_offset(p->P, p->M, p->v_max + 1, 0) : 0;
 }
 
+// v = 2 MERGE queue rows (k_merge_rows): entries per row, and the bytes of all rows.
+int merge_row_stride(const octo_problem* p) { return (int)align_up((size_t)6 * p->M, 8); }
+size_t merge_rows_bytes(const octo_problem* p) {
+  return (size_t)2 * (2 * p->P) * (2 * p->P) * merge_row_stride(p) * 2;
+}
+
 // Workspace layout (byte offsets).
 struct Layout {
-  size_t ctl, pre, pre_mem, bin_of, idx, redo, qscr, total;
+  size_t ctl, pre, pre_mem, bin_of, idx, redo, wide, qscr, total;
 };
 
 Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slots) {
@@ -2779,6 +2852,8 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   l.idx = o;
   o = align_up(o + (size_t)n * 4, 256);
   l.redo = o;
+  o = align_up(o + (size_t)n * 4, 256);
+  l.wide = o;
   o = align_up(o + (size_t)n * 4, 256);
   l.qscr = o;
   o = align_up(o + (size_t)mat_slots * p->P * big.qcap * 2, 256);
@@ -2828,8 +2903,11 @@ struct Setup {
   Workspace* ws;
   DevInfo di;
   int mat_grid;
-  Plan m40;      // 40-bit full-row plan of k_sim_mat40 (CPW 0: does not fit)
+  Plan m40;      // 40-bit ring plan of k_sim_mat40 (CPW 0: does not fit)
   int m40_grid;  // its blocks (queue rows of the workspace are sized for them too)
+  int m40_ring;  // its rows per stage
+  Plan m40f;     // 40-bit full-row plan of its wide pass (CPW 0: does not fit)
+  int m40f_grid;
 };
 
 template <int VC>
@@ -2967,18 +3045,27 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
   rc = prob->v_max <= 2 ? mat_grid_for<2>(su->big, su->di.cus, &su->mat_grid)
                         : mat_grid_for<8>(su->big, su->di.cus, &su->mat_grid);
   if (rc) return rc;
-  su->m40 = fast_plan(prob, su->di.lds_max, prob->P * prob->v_max, prob->M, 0);
-  su->m40_grid = 0;
+  su->m40_ring = make_ring(prob->M, 2 * prob->P * prob->v_max).R;
+  su->m40 = fast_plan(prob, su->di.lds_max, prob->P * prob->v_max, su->m40_ring, 0);
+  su->m40f = fast_plan(prob, su->di.lds_max, prob->P * prob->v_max, prob->M, 0);
+  su->m40_grid = su->m40f_grid = 0;
+  // the memory variant's grid bounds every variant's (as for k_sim_mat)
   if (su->m40.CPW >= 1) {
-    // the memory variant's grid bounds every variant's (as for k_sim_mat)
     rc = prob->v_max <= 2
              ? occupancy_grid(k_sim_mat40<2, XM>, su->m40.lds_bytes, su->di.cus, &su->m40_grid)
              : occupancy_grid(k_sim_mat40<8, XM>, su->m40.lds_bytes, su->di.cus, &su->m40_grid);
     if (rc) return rc;
   }
+  if (su->m40f.CPW >= 1) {
+    rc = prob->v_max <= 2
+             ? occupancy_grid(k_sim_mat40<2, XM>, su->m40f.lds_bytes, su->di.cus, &su->m40f_grid)
+             : occupancy_grid(k_sim_mat40<8, XM>, su->m40f.lds_bytes, su->di.cus, &su->m40f_grid);
+    if (rc) return rc;
+  }
   su->l = layout(prob, su->big, n,
                  std::max<int64_t>({(int64_t)su->mat_grid * su->big.CPW,
                                     (int64_t)su->m40_grid * std::max(su->m40.CPW, 0),
+                                    (int64_t)su->m40f_grid * std::max(su->m40f.CPW, 0),
                                     extra_slots}));
   Workspace& ws = g_ws[std::make_pair(dev, stream)];
   rc = ensure_buf(ws.base, ws.bytes, su->l.total, stream);
@@ -2995,6 +3082,10 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
     rc = ensure_buf(ws.mt, ws.mt_bytes, std::max<size_t>(mtab_entries(prob) * 4, 256), stream);
     if (rc) return rc;
     if (ws.mt != old) ws.mt_valid = false;
+    void* old_mr = ws.mr;
+    rc = ensure_buf(ws.mr, ws.mr_bytes, merge_rows_bytes(prob), stream);
+    if (rc) return rc;
+    if (ws.mr != old_mr) ws.mt_valid = false;
   }
   if (prob->v_max >= 2 && !(ws.mt_valid && ws.mt_P == prob->P && ws.mt_vmax == prob->v_max &&
                             ws.mt_M == prob->M)) {
@@ -3004,6 +3095,11 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     hipLaunchKernelGGL(k_merge_tab, dim3(2 * (prob->v_max - 1)), dim3(WAVE), lds, stream, prob->P,
                        prob->M, 2, prob->v_max, static_cast<uint32_t*>(ws.mt));
+    if ((rc = launch_ok())) return rc;
+    const int rows = 2 * (2 * prob->P) * (2 * prob->P);
+    hipLaunchKernelGGL(k_merge_rows, dim3((rows + WAVE - 1) / WAVE), dim3(WAVE), 0, stream,
+                       prob->P, prob->M, static_cast<const uint32_t*>(ws.mt),
+                       static_cast<uint16_t*>(ws.mr), merge_row_stride(prob));
     if ((rc = launch_ok())) return rc;
     ws.mt_valid = true;
     ws.mt_P = prob->P, ws.mt_vmax = prob->v_max, ws.mt_M = prob->M;
@@ -3035,7 +3131,10 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
   a.ctl = reinterpret_cast<int32_t*>(base + l.ctl);
   a.idx = reinterpret_cast<const int32_t*>(base + l.idx);
   a.redo = reinterpret_cast<int32_t*>(base + l.redo);
+  a.wide = reinterpret_cast<int32_t*>(base + l.wide);
   a.mtab = static_cast<const uint32_t*>(su.ws->mt);
+  a.mrows = prob->v_max >= 2 ? static_cast<const uint16_t*>(su.ws->mr) : nullptr;
+  a.mrow_stride = merge_row_stride(prob);
   a.qscratch = reinterpret_cast<uint16_t*>(base + l.qscr);
   a.G = pl.G;
   a.CPW = pl.CPW;
@@ -3291,25 +3390,37 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
       return rc;
   }
   if ((rc = record_mark(4, stream))) return rc;
-  // candidates with moves: 40-bit full rows where they fit, then the 64-bit redo list
-  if (su.m40.CPW >= 1) {
-    SimArgs a40 = make_args(prob, su.m40, su, link, candidates, n, out_makespan, out_bubble, pk);
+  // candidates with moves: 40-bit rings, 40-bit full rows for those wider than the ring, then
+  // the 64-bit redo list
+  bool m40_any = false;
+  for (int pass = 0; pass < 2; ++pass) {
+    const Plan& pl = pass == 0 ? su.m40 : su.m40f;
+    // a ring as long as M needs no second pass; nor does a ring pass that did not fit (then
+    // the full rows do not fit either and the 64-bit kernel takes every perturbed candidate)
+    if (pass == 1 && (su.m40_ring >= M || su.m40.CPW < 1)) break;
+    if (pl.CPW < 1) continue;
+    SimArgs a40 = make_args(prob, pl, su, link, candidates, n, out_makespan, out_bubble, pk);
+    a40.ring = pass == 0 ? su.m40_ring : M;
     a40.out_comm = cm;
     a40.out_bound = bd;
     int g40 = 0;
-    rc = prob->v_max <= 2 ? occupancy_grid(k_sim_mat40<2, X>, su.m40.lds_bytes, su.di.cus, &g40)
-                          : occupancy_grid(k_sim_mat40<8, X>, su.m40.lds_bytes, su.di.cus, &g40);
+    rc = prob->v_max <= 2 ? occupancy_grid(k_sim_mat40<2, X>, pl.lds_bytes, su.di.cus, &g40)
+                          : occupancy_grid(k_sim_mat40<8, X>, pl.lds_bytes, su.di.cus, &g40);
     if (rc) return rc;
-    g40 = std::min(g40, su.m40_grid);
+    g40 = std::min(g40, pass == 0 ? su.m40_grid : su.m40f_grid);
+    // pass 1 reads the wide list of pass 0; pass 0 sends wide candidates to the redo list when
+    // no full-row pass follows
+    const int wide = pass == 1 ? 1 : (su.m40_ring < M && su.m40f.CPW < 1 ? 2 : 0);
     if (prob->v_max <= 2)
-      hipLaunchKernelGGL((k_sim_mat40<2, X>), dim3(g40), dim3(WAVE), su.m40.lds_bytes, stream,
-                         a40);
+      hipLaunchKernelGGL((k_sim_mat40<2, X>), dim3(g40), dim3(WAVE), pl.lds_bytes, stream, a40,
+                         wide);
     else
-      hipLaunchKernelGGL((k_sim_mat40<8, X>), dim3(g40), dim3(WAVE), su.m40.lds_bytes, stream,
-                         a40);
+      hipLaunchKernelGGL((k_sim_mat40<8, X>), dim3(g40), dim3(WAVE), pl.lds_bytes, stream, a40,
+                         wide);
     if ((rc = launch_ok())) return rc;
-    a.mat_lists = 2;
+    m40_any = true;
   }
+  if (m40_any) a.mat_lists = 2;
   if (prob->v_max <= 2)
     hipLaunchKernelGGL((k_sim_mat<2, X>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
                        stream, a);
