@@ -1353,6 +1353,25 @@ __device__ __forceinline__ int chunk_of(const Chunks<VMAX>& c, int s, int v) {
   return k;
 }
 
+// Entry j (0..7, a run-time value) of a 16-byte span: one select of a 64-bit half and a shift.
+__device__ __forceinline__ uint32_t span_entry_at(const uint4& b, int j) {
+  const uint64_t lo = (uint64_t)b.x | ((uint64_t)b.y << 32);
+  const uint64_t hi = (uint64_t)b.z | ((uint64_t)b.w << 32);
+  return (uint32_t)(((j & 4) ? hi : lo) >> ((j & 3) * 16)) & 0xFFFFu;
+}
+
+// A forward walk over a queue row that loads each 16-byte span once.
+struct RowCursor {
+  const uint16_t* row;
+  int n, blk;
+  uint4 b;
+  __device__ __forceinline__ void init(const uint16_t* r, int n_) { row = r, n = n_, blk = -1; }
+  __device__ __forceinline__ uint32_t at(int i) {
+    if ((i >> 3) != blk) blk = i >> 3, b = row_span(row, blk, n);
+    return span_entry_at(b, i & 7);
+  }
+};
+
 // Phase B for lane d: returns the program length.
 template <int VMAX>
 __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16_t* row, int nq,
@@ -1362,60 +1381,94 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
   auto dur_of = [&](int kind, int k) {
     return kind == KF ? pick<VMAX>(c.dF, k) : kind == KB ? pick<VMAX>(c.dB, k) : pick<VMAX>(c.dW, k);
   };
-  // receives in queue order, insertion-sorted by (producer end, producer)
+  // receives in queue order, insertion-sorted by (producer end, producer): eight entries per
+  // span, their producers' ends loaded together; a receive at or after the last one (the usual
+  // case) is appended without reading the list back
   int nr = 0;
-  for (int i = 0; i < nq; ++i) {
-    const uint32_t e = row[i];
-    const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
-    const int s = pick<VMAX>(c.st, k);
-    const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
-    if (!(cx & CX_IN)) continue;
-    const int ps = kind == KF ? s - 1 : s + 1;
-    const int64_t key = tb[node(kind, ps, m)];
-    const uint32_t id = pitem(0, kind, ps, m);
-    int j = nr++;
-    while (j > 0 && key_less(key, 0, id, rkey[j - 1], 0, rid[j - 1])) {
-      rkey[j] = rkey[j - 1];
-      rid[j] = rid[j - 1];
-      --j;
-    }
-    rkey[j] = key;
-    rid[j] = id;
-  }
-  // merge: computations (queue order), sends (queue order), receives (sorted); each stream's
-  // head stays in registers and only the stream that was taken fetches its next one
-  int ci = 0, si = 0, ri = 0, n = 0;
-  int64_t ck = 0, sk = 0, rk = 0;
-  uint32_t citem = 0, sid = 0, rdd = 0;
-  auto fetch_comp = [&]() {
-    if (ci < nq) {
-      const uint32_t e = row[ci];
+  int64_t lastk = 0;
+  uint32_t lastid = 0;
+  for (int i0 = 0; i0 < nq; i0 += 8) {
+    const uint4 b = row_span(row, i0 >> 3, nq);
+    int64_t key[8];
+    uint32_t id[8];
+    bool isr[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t e = span_entry(b, u);
       const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
       const int s = pick<VMAX>(c.st, k);
-      ck = tb[node(kind, s, m)] - dur_of(kind, k);
-      citem = pitem(PI_COMP, kind, s, m);
-    }
-  };
-  auto fetch_send = [&]() {
-    while (si < nq) {
-      const uint32_t e = row[si];
-      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
       const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
-      if (cx & CX_OUT) {
-        const int s = pick<VMAX>(c.st, k);
-        sk = tb[node(kind, s, m)];
-        sid = pitem(0, kind, s, m);
-        return;
-      }
-      ++si;
+      isr[u] = i0 + u < nq && (cx & CX_IN) != 0;
+      const int ps = kind == KF ? s - 1 : s + 1;
+      id[u] = pitem(0, kind, ps, m);
+      key[u] = isr[u] ? tb[node(kind, ps, m)] : 0;
     }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (!isr[u]) continue;
+      if (nr == 0 || !key_less(key[u], 0, id[u], lastk, 0, lastid)) {
+        rkey[nr] = key[u], rid[nr] = id[u];
+        lastk = key[u], lastid = id[u];
+        ++nr;
+        continue;
+      }
+      int j = nr++;
+      while (j > 0 && key_less(key[u], 0, id[u], rkey[j - 1], 0, rid[j - 1])) {
+        rkey[j] = rkey[j - 1];
+        rid[j] = rid[j - 1];
+        --j;
+      }
+      rkey[j] = key[u];
+      rid[j] = id[u];
+    }
+  }
+  // merge: computations (queue order), sends (queue order), receives (sorted). Each stream
+  // keeps its head and its next item in registers; the stream taken moves its next item to the
+  // head and loads the one after, so that a load is awaited an iteration after it was issued,
+  // and the three streams' steps are selects rather than branches (lanes take different
+  // streams).
+  RowCursor rc_c, rc_s;
+  rc_c.init(row, nq);
+  rc_s.init(row, nq);
+  // computations: item ci (head) and ci + 1 (next); the next one's finish is kept as loaded
+  // and its duration beside it, so that the load is first used when it becomes the head
+  auto comp_at = [&](int i, int64_t& fin, int64_t& dur, uint32_t& item) {
+    const uint32_t e = rc_c.at(i < nq ? i : 0);
+    const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+    const int s = pick<VMAX>(c.st, k);
+    fin = i < nq ? tb[node(kind, s, m)] : 0;
+    dur = dur_of(kind, k);
+    item = pitem(PI_COMP, kind, s, m);
   };
-  auto fetch_recv = [&]() {
-    if (ri < nr) rk = rkey[ri], rdd = rid[ri];
+  // sends: the first send entry at or after position i (nq: none)
+  auto send_from = [&](int i, int64_t& key, uint32_t& id) {
+    int j = i;
+    int kind = 0, k = 0, m = 0;
+    for (; j < nq; ++j) {
+      const uint32_t e = rc_s.at(j);
+      kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
+      if (cx & CX_OUT) break;
+    }
+    const int s = pick<VMAX>(c.st, k);
+    key = j < nq ? tb[node(kind, s, m)] : 0;
+    id = pitem(0, kind, s, m);
+    return j;
   };
-  fetch_comp();
-  fetch_send();
-  fetch_recv();
+  int ci = 0, ri = 0, n = 0;
+  int64_t ck, cf2, cd2, sk, sk2, rk, rk2;
+  uint32_t citem, citem2, sid, sid2, rdd, rdd2;
+  {
+    int64_t f0, d0;
+    comp_at(0, f0, d0, citem);
+    ck = f0 - d0;
+  }
+  comp_at(1, cf2, cd2, citem2);
+  int si = send_from(0, sk, sid);
+  int si2 = send_from(si + 1 < nq ? si + 1 : nq, sk2, sid2);
+  rk = ri < nr ? rkey[0] : 0, rdd = ri < nr ? rid[0] : 0;
+  rk2 = 1 < nr ? rkey[1] : 0, rdd2 = 1 < nr ? rid[1] : 0;
+  uint4 pk4 = make_uint4(0, 0, 0, 0);
   while (ci < nq || si < nq || ri < nr) {
     // the smallest of the three heads
     int src = ci < nq ? 0 : -1;
@@ -1423,20 +1476,30 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
     uint32_t bc = 1, bt2 = (uint32_t)ci;
     if (si < nq && (src < 0 || key_less(sk, 0, sid, bt, bc, bt2))) src = 1, bt = sk, bc = 0, bt2 = sid;
     if (ri < nr && (src < 0 || key_less(rk, 0, rdd, bt, bc, bt2))) src = 2;
-    if (src == 0) {
-      prog[n++] = citem;
-      ++ci;
-      fetch_comp();
-    } else if (src == 1) {
-      prog[n++] = (PI_SEND << 30) | sid;
-      ++si;
-      fetch_send();
-    } else {
-      prog[n++] = (PI_RECV << 30) | rdd;
-      ++ri;
-      fetch_recv();
-    }
+    // items are gathered four at a time and written as one 16-byte store: a store is counted
+    // with the loads, so one per item would make every later load wait for its write
+    const uint32_t item = src == 0 ? citem : src == 1 ? ((PI_SEND << 30) | sid) : ((PI_RECV << 30) | rdd);
+    const int q = n & 3;
+    pk4.x = q == 0 ? item : pk4.x;
+    pk4.y = q == 1 ? item : pk4.y;
+    pk4.z = q == 2 ? item : pk4.z;
+    pk4.w = q == 3 ? item : pk4.w;
+    if (q == 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
+    ++n;
+    // the stream taken: next to head, and the item after next requested
+    const bool tc = src == 0, ts = src == 1, tr = src == 2;
+    ci += tc ? 1 : 0;
+    ck = tc ? cf2 - cd2 : ck, citem = tc ? citem2 : citem;
+    si = ts ? si2 : si;
+    sk = ts ? sk2 : sk, sid = ts ? sid2 : sid;
+    ri += tr ? 1 : 0;
+    rk = tr ? rk2 : rk, rdd = tr ? rdd2 : rdd;
+    if (tc) comp_at(ci + 1, cf2, cd2, citem2);
+    if (ts) si2 = send_from(si + 1 < nq ? si + 1 : nq, sk2, sid2);
+    if (tr && ri + 1 < nr) rk2 = rkey[ri + 1], rdd2 = rid[ri + 1];
   }
+  // the last, partial group of four
+  if (n & 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
   return n;
 }
 
@@ -3637,7 +3700,7 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   }
   OrdBufs ob;
   ob.rcap = 2 * prob->v_max * prob->M;
-  ob.pcap = 7 * prob->v_max * prob->M;
+  ob.pcap = (int)align_up((size_t)7 * prob->v_max * prob->M, 4);  // 16-byte aligned rows
   size_t o = 0;
   const size_t o_tb = o;
   o = align_up(o + slots * 3 * prob->P * prob->v_max * prob->M * 8, 256);
