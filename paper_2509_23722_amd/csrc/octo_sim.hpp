@@ -385,11 +385,11 @@ __device__ __forceinline__ void relax_k(GenMatK<K>& gen, const Chunks<VMAX>& c, 
 // op's input comes from another device — ready once the producer's slot shows it finished; the
 // transfer runs from max(producer's finish, this device's clock) for the link time, this
 // device's clock moves to its end, and the end goes to the producer's mailbox; compute, as in
-// relax; send, when the op's output goes to another device — the lane waits until its mailbox
-// holds the transfer's end (posted by the receiver), takes it as its clock and clears the box.
-// A producer reaches its send in the round it finishes the op, so the receiver (which reads the
-// slot in a later round) always posts to a waiting sender, and each box has one writer at a
-// time. mbox: one int64 per lane of the wave (RDV_EMPTY = nothing posted), set to RDV_EMPTY by
+// relax (in the same round as the receive); send, when the op's output goes to another device —
+// the lane waits until its mailbox holds the transfer's end (posted by the receiver), takes it as
+// its clock and clears the box. A producer reaches its send in the round it finishes the op, so
+// the receiver (which reads the slot in a later round) always posts to a waiting sender, and
+// each box has one writer at a time. mbox: one int64 per lane of the wave (RDV_EMPTY = nothing posted), set to RDV_EMPTY by
 // the caller. A round in which no lane of the wave takes a step changes nothing, so every group
 // with work left is deadlocked.
 constexpr int64_t RDV_EMPTY = -1;
@@ -404,24 +404,32 @@ __device__ __forceinline__ void relax_rdv(Gen& gen, const Chunks<VMAX>& c, const
   for (;;) {
     uint32_t plo, phi;
     T.issue(live ? L.rd : 0, plo, phi);
-    const int64_t box = mbox[me];
     const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
     const bool rdy = live && (plo & (uint32_t)L.mask) == (uint32_t)L.want;
     const int64_t tx = (int64_t)(p >> 3);
     const bool okR = step == 0 && rdy;
     const int64_t xend = (tx > L.clock ? tx : L.clock) + L.w;
-    const bool okC = step == 1 && rdy;
+    // a receive takes its op's compute in the same round: the input slot stays ready (it is
+    // rewritten only after this consumer's own backward), and the op starts at the transfer's
+    // end, which is at least tin
+    const bool okC = (step == 1 && rdy) || okR;
+    const int64_t c0 = okR ? xend : L.clock;
     const int64_t tin = tx + L.w;
-    const int64_t st = tin > L.clock ? tin : L.clock;
+    const int64_t st = tin > c0 ? tin : c0;
     const int64_t fin = st + L.dur;
-    const bool okS = step == 2 && box != RDV_EMPTY;
     if (okR) mbox[g0 + L.dst] = xend;
+    __asm__ volatile("" ::: "memory");
+    // the mailbox is read after this round's posts, so a send completes in the round its
+    // receiver posts (a lane that computes this round cannot be posted to before the next one:
+    // its receiver sees the slot only then)
+    const int64_t box = mbox[me];
+    const bool okS = step == 2 && box != RDV_EMPTY;
     if (okC && L.store) T.store(L.wr, ((uint64_t)fin << 3) | L.state);
     if (okS) mbox[me] = RDV_EMPTY;
-    L.clock = okR ? xend : okC ? fin : okS ? box : L.clock;
+    L.clock = okC ? fin : okS ? box : L.clock;
     const bool sends = (L.cx & CX_OUT) != 0;
     const bool done = (okC && !sends) || okS;
-    step = okR ? 1 : (okC && sends) ? 2 : step;
+    step = (okC && sends) ? 2 : step;
     L.pos += done ? 1 : 0;
     live = L.pos < L.nops;
     gen.advance(done);
