@@ -1506,12 +1506,14 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
 // RING: 40-bit ring tables of a.ring rows per stage per group. Phase C keeps each device's
 // computations in queue order and adds only the sends, each of which reads its producer's slot
 // after the producer and before any later computation of the stage, so the ring argument of
-// k_tune_ring holds for both rounds; a candidate whose queue window reaches the ring, or whose
-// times pass 40 bits, joins the redo list that the 64-bit kernel (list, list_n) then takes.
+// k_tune_ring holds for both rounds; a candidate whose queue window reaches the ring joins the
+// wide list (wide_list: taken by a 40-bit full-row pass, a.ring = M) or else the redo list, and
+// one whose times pass 40 bits the redo list, which the 64-bit kernel (list, list_n) takes.
 template <int VMAX, bool RING>
 __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
                                                   const int32_t* __restrict__ list,
-                                                  const int32_t* __restrict__ list_n) {
+                                                  const int32_t* __restrict__ list_n,
+                                                  int wide_list) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int64_t mbox[WAVE];    // transfer end posted by the receiver, per sender lane
   __shared__ int64_t obt[WAVE];     // outbox: the sender's announce time ...
@@ -1668,7 +1670,13 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
     // overflow test over both rounds' clocks (phase A's alone when it deadlocked)
     const int64_t top = RING ? group_max(clock > L.clock ? clock : L.clock, G) : 0;
     if (has && valid && (!on_ring || top >= Table40::LIMIT)) {
-      if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      // too wide for the ring: the full-row 40-bit pass (when one follows); overflow: 64 bits
+      if (d == 0) {
+        if (!on_ring && wide_list)
+          a.wide[atomicAdd(&a.ctl[CTL_WIDE], 1)] = (int32_t)cand;
+        else
+          a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      }
     } else if (mine) {
       const int64_t sv = dead || cdead ? (int64_t)OCTO_MS_DEADLOCK : 0;
       if (d == 0) a.out_ms[cand] = sv ? sv : ms;
@@ -3673,17 +3681,24 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   DevInfo di;
   int rc = dev_info(dev, &di);
   if (rc) return rc;
+  // at most 4 GiB of per-slot scratch (finish times, receive keys, programs, queue rows)
+  const size_t per_slot = (size_t)prob->P * prob->v_max * prob->M * (3 * 8 + 2 * 12 + 7 * 4) +
+                          (size_t)prob->P * queue_cap(prob) * 2;
+  auto grid_of = [&](auto kern, const Plan& pl, int* g) {
+    int rc2 = occupancy_grid(kern, pl.lds_bytes, di.cus, g);
+    if (rc2) return rc2;
+    *g = (int)std::max<int64_t>(1, std::min<int64_t>(*g, (n + pl.CPW - 1) / pl.CPW));
+    *g = (int)std::min<int64_t>(*g, std::max<int64_t>(1, ((int64_t)4 << 30) / per_slot / pl.CPW));
+    return 0;
+  };
+  // pass 1: rings; pass 2: 40-bit full rows for the orders too wide for the ring
   const Ring rr = make_ring(prob->M, prob->P * prob->v_max);
   const Plan rp = ring_plan(prob, di.lds_max, prob->P * prob->v_max, rr.R);
-  int rgrid = 0;
+  const Plan fp = ring_plan(prob, di.lds_max, prob->P * prob->v_max, prob->M);
+  int rgrid = 0, fgrid = 0;
   if (rr.R < prob->M && rp.CPW >= 1) {
-    if ((rc = occupancy_grid(k_ordered<VC, true>, rp.lds_bytes, di.cus, &rgrid))) return rc;
-    rgrid = (int)std::max<int64_t>(1, std::min<int64_t>(rgrid, (n + rp.CPW - 1) / rp.CPW));
-    // at most 4 GiB of per-slot scratch (finish times, receive keys, programs, queue rows)
-    const size_t per_slot = (size_t)prob->P * prob->v_max * prob->M * (3 * 8 + 2 * 12 + 7 * 4) +
-                            (size_t)prob->P * queue_cap(prob) * 2;
-    const int64_t max_blocks = std::max<int64_t>(1, ((int64_t)4 << 30) / per_slot / rp.CPW);
-    rgrid = (int)std::min<int64_t>(rgrid, max_blocks);
+    if ((rc = grid_of(k_ordered<VC, true>, rp, &rgrid))) return rc;
+    if (fp.CPW >= 1 && (rc = grid_of(k_ordered<VC, true>, fp, &fgrid))) return rc;
   }
   Setup su;
   if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su))) return rc;
@@ -3692,7 +3707,8 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   grid = (int)std::max<int64_t>(
       1, std::min<int64_t>(std::min(grid, su.mat_grid), (n + su.big.CPW - 1) / su.big.CPW));
   // group slots: the ring pass's and the full-row pass's share the same buffers (one at a time)
-  const size_t slots = std::max((size_t)grid * su.big.CPW, (size_t)rgrid * std::max(rp.CPW, 0));
+  const size_t slots = std::max({(size_t)grid * su.big.CPW, (size_t)rgrid * std::max(rp.CPW, 0),
+                                 (size_t)fgrid * std::max(fp.CPW, 0)});
   const size_t qslots = (size_t)su.mat_grid * su.big.CPW;
   if (slots > qslots) {
     // the queue rows of the workspace cover mat_grid * CPW slots; take a larger workspace
@@ -3723,13 +3739,20 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
     SimArgs ar = make_args(prob, rp, su, link, cands, n, ms, bub);
     ar.ring = rr.R;
     hipLaunchKernelGGL((k_ordered<VC, true>), dim3(rgrid), dim3(WAVE), rp.lds_bytes, stream, ar,
-                       ob, nullptr, nullptr);
+                       ob, nullptr, nullptr, fgrid > 0 ? 1 : 0);
     if ((rc = launch_ok())) return rc;
+    if (fgrid > 0) {
+      SimArgs af = make_args(prob, fp, su, link, cands, n, ms, bub);
+      af.ring = prob->M;
+      hipLaunchKernelGGL((k_ordered<VC, true>), dim3(fgrid), dim3(WAVE), fp.lds_bytes, stream, af,
+                         ob, a.wide, a.ctl + CTL_WIDE, 0);
+      if ((rc = launch_ok())) return rc;
+    }
     list = a.redo;
     list_n = a.ctl + CTL_REDO;
   }
   hipLaunchKernelGGL((k_ordered<VC, false>), dim3(grid), dim3(WAVE), su.big.lds_bytes, stream, a,
-                     ob, list, list_n);
+                     ob, list, list_n, 0);
   return launch_ok();
 }
 
