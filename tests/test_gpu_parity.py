@@ -168,12 +168,14 @@ def test_edge_cases(gpu):
         assert_same(*g, *r, f"edge {c}")
 
 
-def test_times_beyond_40bit_slots(gpu):
+@pytest.mark.parametrize("M", [8, 32])
+def test_times_beyond_40bit_slots(gpu, M):
     """Layer costs so large that finish times pass 2^37 ns: those candidates are recomputed with
-    64-bit finish tables and must still match the oracle exactly; small ones stay fast."""
-    rng = np.random.default_rng(21)
-    P, v_max, M, L = 4, 2, 8, 12
-    log("huge costs P=4 v_max=2 M=8")
+    64-bit finish tables and must still match the oracle exactly; small ones stay fast. At M = 32
+    the candidates with moves start on 40-bit rings."""
+    rng = np.random.default_rng(21 + M)
+    P, v_max, L = 4, 2, 12
+    log(f"huge costs P=4 v_max=2 M={M}")
     costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
     costs[5] = [40_000_000_000, 30_000_000_000, 20_000_000_000]  # ~ 2^35 per op of that layer
     link = I.link_matrix(P, 1000)
