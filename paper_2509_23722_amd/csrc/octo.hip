@@ -40,6 +40,7 @@ constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
 constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
 constexpr int CTL_WIDE = 139;     // perturbed candidates whose queue window passes the ring
 constexpr int CTL_WORK_WIDE = 140;// chunk counter of k_sim_mat40 over the wide list
+constexpr int CTL_TOTAL = 141;    // valid records (all bins; set by k_plan)
 constexpr int CTL_POS = 64;       // [NBINS] next index position of each bin (scatter cursor)
 constexpr int CTL_WORDS = 256;
 // rounds a materialised queue is read ahead of its use (GenMatK; rows of at least 8 entries)
@@ -608,6 +609,7 @@ __global__ void k_plan(int32_t* __restrict__ ctl) {
       ctl[CTL_START + b] = ctl[CTL_POS + b] = acc;
       acc += ctl[CTL_COUNTS + b];
     }
+    ctl[CTL_TOTAL] = acc;
   }
 }
 
@@ -3386,6 +3388,28 @@ struct Extra {
   const int32_t* n_live = nullptr;  // device count of the records to evaluate (<= n)
 };
 
+// Validity and bin of every record (k_classify writes the sentinels of invalid ones), bin
+// offsets (k_plan; ctl[CTL_TOTAL] = the valid records), and the record indices sorted by bin
+// (k_scatter, into the workspace's idx).
+int classify_sort(const octo_problem* prob, const Setup& su, const SimArgs& a, int64_t n,
+                  hipStream_t stream) {
+  char* base = static_cast<char*>(su.ws->base);
+  const int tb = CLS_THREADS;
+  const int nb = (int)((n + tb - 1) / tb);
+  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
+  const int hb = (int)align_up((size_t)pert_off(prob->P * prob->v_max), 16);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, tb * hb);
+  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), tb * hb, stream, a, bins, hb);
+  int rc = launch_ok();
+  if (rc) return rc;
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, a.ctl);
+  if ((rc = launch_ok())) return rc;
+  hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
+                     reinterpret_cast<int32_t*>(base + su.l.idx));
+  return launch_ok();
+}
+
 // The batch evaluation behind octo_sim_batch (X = XP), octo_sim_batch_mem (XM),
 // octo_sim_batch_comm (XC), octo_sim_batch_serial (XS: generated queues, not tables) and
 // octo_sim_batch_bounds (XB). The caller has checked the arguments and holds g_mu.
@@ -3406,19 +3430,7 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   a.out_comm = cm;
   a.out_bound = bd;
   a.n_live = ex.n_live;
-  const int tb = CLS_THREADS;
-  const int nb = (int)((n + tb - 1) / tb);
-  uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
-  const int hb = (int)align_up((size_t)pert_off(prob->P * prob->v_max), 16);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, tb * hb);
-  hipLaunchKernelGGL(k_classify, dim3(nb), dim3(tb), tb * hb, stream, a, bins, hb);
-  if ((rc = launch_ok())) return rc;
-  hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, a.ctl);
-  if ((rc = launch_ok())) return rc;
-  hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(tb), 0, stream, a, bins,
-                     reinterpret_cast<int32_t*>(base + su.l.idx));
-  if ((rc = launch_ok())) return rc;
+  if ((rc = classify_sort(prob, su, a, n, stream))) return rc;
   // generated INTER / MERGE queues, one launch per v class with finish tables sized for it:
   // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
   // materialised queues (perturbations, 64-bit redo).
@@ -3733,13 +3745,16 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   ob.rid = reinterpret_cast<uint32_t*>(base + o_ri);
   ob.prog = reinterpret_cast<uint32_t*>(base + o_pg);
   SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
-  const int32_t* list = nullptr;
-  const int32_t* list_n = nullptr;
+  // the valid records sorted by (v, generator, split), so that the groups of a wave have queues
+  // and programs of one length (invalid ones get their sentinels here)
+  if ((rc = classify_sort(prob, su, a, n, stream))) return rc;
+  const int32_t* list = a.idx;
+  const int32_t* list_n = a.ctl + CTL_TOTAL;
   if (rgrid > 0) {
     SimArgs ar = make_args(prob, rp, su, link, cands, n, ms, bub);
     ar.ring = rr.R;
     hipLaunchKernelGGL((k_ordered<VC, true>), dim3(rgrid), dim3(WAVE), rp.lds_bytes, stream, ar,
-                       ob, nullptr, nullptr, fgrid > 0 ? 1 : 0);
+                       ob, list, list_n, fgrid > 0 ? 1 : 0);
     if ((rc = launch_ok())) return rc;
     if (fgrid > 0) {
       SimArgs af = make_args(prob, fp, su, link, cands, n, ms, bub);
