@@ -2320,6 +2320,26 @@ __global__ void __launch_bounds__(WAVE) k_tune(TuneArgs t) {
   }
 }
 
+// Chains by queue length, for the ring pass: class (v - 1) * 2 + split from each chain's record
+// header (records whose header is out of range take class 2 * v_max, last); counts into the bin
+// counters, offsets by k_plan, then the chain indices scattered by class.
+__device__ __forceinline__ int chain_class(const TuneArgs& t, int64_t i) {
+  const uint8_t* r = t.chains + i * t.chain_stride;
+  const int pol = r[0], v = r[1];
+  return (v >= 1 && v <= t.s.pr.v_max && pol <= POL_ZB) ? (v - 1) * 2 + (pol == POL_ZB)
+                                                          : 2 * t.s.pr.v_max;
+}
+
+__global__ void k_chain_count(TuneArgs t) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < t.n_chains) atomicAdd(&t.s.ctl[CTL_COUNTS + chain_class(t, i)], 1);
+}
+
+__global__ void k_chain_scatter(TuneArgs t, int32_t* __restrict__ list) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < t.n_chains) list[atomicAdd(&t.s.ctl[CTL_POS + chain_class(t, i)], 1)] = (int32_t)i;
+}
+
 // One step of every chain on 40-bit ring tables: R rows per stage (R < M), the wave's groups
 // sharing the slot arrays as in the generated kernels, so several chains fit a CU. A ring is
 // exact for a chain whose queue window (queue_window; its bound is kept in the chain state) is
@@ -2344,9 +2364,10 @@ __global__ void __launch_bounds__(WAVE) k_tune_ring(TuneArgs t) {
   const int gl = lane_id() - d;
   const Ring ring = make_ring(M, a.ring);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
-  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < t.n_chains; base += n_groups) {
-    const bool has = g < a.CPW && base + g < t.n_chains;
-    const int64_t chain = has ? base + g : 0;
+  const int64_t total = t.list ? (int64_t)*t.list_n : t.n_chains;
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < total; base += n_groups) {
+    const bool has = g < a.CPW && base + g < total;
+    const int64_t chain = has ? (t.list ? (int64_t)t.list[base + g] : base + g) : 0;
     uint8_t* crec = t.chains + chain * t.chain_stride;
     int64_t* cstate = reinterpret_cast<int64_t*>(crec + a.pr.stride);
     uint16_t* row = t.queues + ((size_t)chain * P + (d < P ? d : 0)) * a.qcap;
@@ -3579,6 +3600,17 @@ int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const i
       TuneArgs tr = t;
       tr.s = make_args(prob, rp, su, link, nullptr, 0, nullptr, nullptr);
       tr.s.ring = rr.R;
+      // chains in queue-length order (the groups of a wave run in lockstep)
+      const int nb = (int)((n_chains + 255) / 256);
+      int32_t* order = const_cast<int32_t*>(tr.s.idx);
+      hipLaunchKernelGGL(k_chain_count, dim3(nb), dim3(256), 0, stream, tr);
+      if ((rc = launch_ok())) return rc;
+      hipLaunchKernelGGL(k_plan, dim3(1), dim3(WAVE), 0, stream, tr.s.ctl);
+      if ((rc = launch_ok())) return rc;
+      hipLaunchKernelGGL(k_chain_scatter, dim3(nb), dim3(256), 0, stream, tr, order);
+      if ((rc = launch_ok())) return rc;
+      tr.list = order;
+      tr.list_n = tr.s.ctl + CTL_TOTAL;
       rc = prob->v_max <= 2 ? launch_tune_ring<2>(tr, rp, su.di.cus, n_chains, stream)
                             : launch_tune_ring<8>(tr, rp, su.di.cus, n_chains, stream);
       if (rc) return rc;
