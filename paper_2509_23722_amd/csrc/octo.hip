@@ -590,7 +590,7 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
       if (a.out_bound)
         for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
     } else {
-      bin = r.n_pert > 0 ? BIN_MAT : bin_of(r.v, r.gen, r.split);
+      bin = r.n_pert > 0 ? BIN_MAT + mat_sub(r.v, r.split) : bin_of(r.v, r.gen, r.split);
     }
     bins[i] = (uint8_t)bin;
   }
@@ -1140,10 +1140,10 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat(SimArgs a) {
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
   int base = 0;
-  base = a.ctl[CTL_START + BIN_MAT];
+  base = a.ctl[CTL_START + BIN_MAT];  // the perturbed bins are the last ones
   for (int phase = 0; phase < 2; ++phase) {
     const int32_t* list = phase == 0 ? a.idx + base : a.redo;
-    const int cnt = phase == 0 ? a.ctl[CTL_COUNTS + BIN_MAT] : a.ctl[CTL_REDO];
+    const int cnt = phase == 0 ? a.ctl[CTL_TOTAL] - base : a.ctl[CTL_REDO];
     const int counter = phase == 0 ? CTL_WORK_MAT : CTL_WORK_REDO;
     if (cnt == 0 || !((a.mat_lists >> phase) & 1)) continue;  // no work here
     for (;;) {
@@ -1233,7 +1233,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a, int mode) {
   // index; bit 1: send candidates wider than the ring to the redo list (no full-row pass)
   const bool wide_pass = (mode & 1) != 0;
   const int32_t* list = wide_pass ? a.wide : a.idx + a.ctl[CTL_START + BIN_MAT];
-  const int cnt = wide_pass ? a.ctl[CTL_WIDE] : a.ctl[CTL_COUNTS + BIN_MAT];
+  const int cnt = wide_pass ? a.ctl[CTL_WIDE] : a.ctl[CTL_TOTAL] - a.ctl[CTL_START + BIN_MAT];
   const int work = wide_pass ? CTL_WORK_WIDE : CTL_WORK_MAT;
   if (cnt == 0) return;
   const Ring ring = make_ring(M, a.ring);

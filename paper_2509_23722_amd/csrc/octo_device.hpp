@@ -22,8 +22,11 @@ constexpr int GEN_AFAB = 0, GEN_INTER = 1, GEN_MERGE = 2, GEN_MAT = 3;
 // code path; bins are numbered heaviest first (large v first; within one v: AFAB, then split
 // backward, then fused).
 constexpr int NBIN_GEN = 40;          // (8 - v) * 5 + rank, v = 1..8
-constexpr int BIN_MAT = 40;           // candidates with perturbations: queues materialised
-constexpr int NBINS = 41;
+// candidates with perturbations (queues materialised): bins BIN_MAT + mat_sub(v, split), the
+// last ones, by queue length like the generated bins (large v first, split first)
+constexpr int BIN_MAT = 40;
+constexpr int NBINS = BIN_MAT + 16;
+__host__ __device__ __forceinline__ int mat_sub(int v, int split) { return (8 - v) * 2 + (split ? 0 : 1); }
 constexpr int BIN_NONE = 0xFF;        // invalid: sentinel already written
 // rank of a generator within one v: 0 AFAB, 1 MERGE split, 2 INTER split, 3 MERGE fused,
 // 4 INTER fused
