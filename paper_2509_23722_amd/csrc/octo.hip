@@ -964,19 +964,26 @@ __device__ __forceinline__ void emit_queue(Gen& g, uint16_t* row, int n) {
 }
 
 // Copy the first n entries of a queue row (both rows 16-byte aligned; whole 16-byte spans, the
-// last one padded within the rows' capacities), eight spans in flight.
+// last one padded within the rows' capacities), eight spans in flight. The loads are
+// unconditional (a block past the end re-reads the last span) so that the eight spans stay in
+// registers and are waited for together.
 __device__ __forceinline__ void copy_row(const uint16_t* src, uint16_t* dst, int n) {
   const uint4* s4 = reinterpret_cast<const uint4*>(src);
   uint4* d4 = reinterpret_cast<uint4*>(dst);
   const int spans = (n + 7) >> 3;
   for (int q0 = 0; q0 < spans; q0 += 8) {
-    uint4 t[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (q0 + u < spans) t[u] = s4[q0 + u];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (q0 + u < spans) d4[q0 + u] = t[u];
+    uint4 t0 = s4[min(q0 + 0, spans - 1)], t1 = s4[min(q0 + 1, spans - 1)];
+    uint4 t2 = s4[min(q0 + 2, spans - 1)], t3 = s4[min(q0 + 3, spans - 1)];
+    uint4 t4 = s4[min(q0 + 4, spans - 1)], t5 = s4[min(q0 + 5, spans - 1)];
+    uint4 t6 = s4[min(q0 + 6, spans - 1)], t7 = s4[min(q0 + 7, spans - 1)];
+    d4[q0] = t0;
+    if (q0 + 1 < spans) d4[q0 + 1] = t1;
+    if (q0 + 2 < spans) d4[q0 + 2] = t2;
+    if (q0 + 3 < spans) d4[q0 + 3] = t3;
+    if (q0 + 4 < spans) d4[q0 + 4] = t4;
+    if (q0 + 5 < spans) d4[q0 + 5] = t5;
+    if (q0 + 6 < spans) d4[q0 + 6] = t6;
+    if (q0 + 7 < spans) d4[q0 + 7] = t7;
   }
 }
 
