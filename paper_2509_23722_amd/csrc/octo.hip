@@ -3270,12 +3270,13 @@ uint64_t bins_of(int v_lo, int v_hi, bool afab) {
 
 // Launch k_sim<VC> over the generated bins in `mask` with its own 40-bit plan: s_cap stages of
 // ring_want (rounded up to a power of two, or M) slots; bins whose in-flight bound exceeds the
-// ring go to the 64-bit path.
+// ring go to the 64-bit path, unless any_ring (rendezvous GPipe queues, exact with one slot per
+// stage).
 template <int VC, int X>
 int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
                int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm,
                int64_t* bound, int s_cap, int ring_want, uint64_t mask, int work,
-               hipStream_t stream) {
+               hipStream_t stream, bool any_ring = false) {
   const Ring ring = make_ring(prob->M, ring_want);
   // table-driven launches (v <= 2) keep 3 v {w, dur} streams per lane in LDS and need tables
   // encoded for exactly this geometry
@@ -3297,7 +3298,7 @@ int launch_sim(const octo_problem* prob, const Setup& su, const int64_t* link, c
   a.bin_mask = mask, a.work = work;
   a.ring = ring.R;
   a.redo_bins = 0;
-  for (int b = 0; b < NBIN_GEN; ++b)
+  for (int b = 0; b < NBIN_GEN && !any_ring; ++b)
     if (((mask >> b) & 1) && ring.R < prob->M && su.ws->inflight[b] > ring.R)
       a.redo_bins |= 1ull << b;
   int grid = 0;
@@ -3450,7 +3451,6 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   Setup su;
   int rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, n, &su);
   if (rc) return rc;
-  char* base = static_cast<char*>(su.ws->base);
   int64_t* pk = MEM ? ex.peak : nullptr;
   int64_t* cm = X == XC ? ex.comm : nullptr;
   int64_t* bd = X == XB ? ex.bound : nullptr;
@@ -3486,18 +3486,19 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
                              stream)))
       return rc;
   } else {
-    // rendezvous: GPipe queues in the generated kernels, with full rows (a stage holds all M
-    // micro-batches before its first backward), per v class
+    // rendezvous: GPipe queues in the generated kernels, per v class, with one slot per stage
+    // (the blocking sends keep at most one value of a stage row untaken; relax_rdv)
     if (prob->v_max >= 2 &&
         (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                               bd, 2 * P, M, bins_of(2, 2, true), CTL_WORK + 4, stream)))
+                               bd, 2 * P, 1, bins_of(2, 2, true), CTL_WORK + 4, stream, true)))
       return rc;
     if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                               bd, P, M, bins_of(1, 1, true), CTL_WORK + 5, stream)))
+                               bd, P, 1, bins_of(1, 1, true), CTL_WORK + 5, stream, true)))
       return rc;
     if (prob->v_max >= 3 &&
         (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                               bd, P * prob->v_max, M, bins_of(3, 8, true), CTL_WORK + 6, stream)))
+                               bd, P * prob->v_max, 1, bins_of(3, 8, true), CTL_WORK + 6, stream,
+                               true)))
       return rc;
   }
   if ((rc = record_mark(4, stream))) return rc;

@@ -31,6 +31,8 @@
 // The round body is straight-line code: generators and descriptors advance under a predicate.
 #pragma once
 
+#include <type_traits>
+
 #include "octo_device.hpp"
 
 namespace octo {
@@ -392,11 +394,19 @@ __device__ __forceinline__ void relax_k(GenMatK<K>& gen, const Chunks<VMAX>& c, 
 // each box has one writer at a time. mbox: one int64 per lane of the wave (RDV_EMPTY = nothing posted), set to RDV_EMPTY by
 // the caller. A round in which no lane of the wave takes a step changes nothing, so every group
 // with work left is deadlocked.
+// GPipe queues (GenAfab) skip the readiness test of an input from the own device: such a
+// producer always comes earlier in the queue (forwards by ascending stage, backwards by
+// descending stage, all forwards first), so it has finished and the device clock covers it.
+// Every other input crosses devices and is received while its producer waits at the send, so
+// the producer writes its stage row again only after the value was taken, and a consumer wants
+// micro-batch m only after taking m - 1 from the same row: one slot per stage, with the parity
+// of m, is exact for any M.
 constexpr int64_t RDV_EMPTY = -1;
 template <int VMAX, class Tab, class Gen>
 __device__ __forceinline__ void relax_rdv(Gen& gen, const Chunks<VMAX>& c, const Ring& ring,
                                           Lane& L, const Tab& T, int G, uint64_t gbit,
                                           uint64_t lsb, bool& dead, int64_t* mbox) {
+  constexpr bool LOCAL = std::is_same<Gen, GenAfab>::value;
   const int me = (int)(threadIdx.x & 63);
   const int g0 = me - me % G;  // the group's first lane
   bool live = L.pos < L.nops;
@@ -412,7 +422,7 @@ __device__ __forceinline__ void relax_rdv(Gen& gen, const Chunks<VMAX>& c, const
     // a receive takes its op's compute in the same round: the input slot stays ready (it is
     // rewritten only after this consumer's own backward), and the op starts at the transfer's
     // end, which is at least tin
-    const bool okC = (step == 1 && rdy) || okR;
+    const bool okC = (step == 1 && (LOCAL ? live : rdy)) || okR;
     const int64_t c0 = okR ? xend : L.clock;
     const int64_t tin = tx + L.w;
     const int64_t st = tin > c0 ? tin : c0;

@@ -82,6 +82,25 @@ def test_random_structures(gpu, P, v_max, M, L, pert):
     assert_same(g, run_oracle(*args), f"P={P} v_max={v_max} M={M}")
 
 
+@pytest.mark.parametrize("P,v_max,M,L", [
+    (4, 2, 64, 16), (8, 2, 33, 20), (8, 1, 64, 12), (3, 4, 20, 24), (6, 3, 17, 30), (2, 2, 9, 6),
+])
+def test_gpipe_one_slot_per_stage(gpu, P, v_max, M, L):
+    """GPipe orders alone, every placement kind (V-shape turns and random placements put
+    neighbouring stages on one device): the rendezvous GPipe path keeps one finish slot per
+    stage, far fewer than M."""
+    rng = np.random.default_rng(7700 + 100 * P + 10 * v_max + M)
+    log(f"rdv: GPipe P={P} v_max={v_max} M={M} L={L}")
+    costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+    link = rng.integers(0, 2_000_000, size=(P, P)).astype(np.int64)
+    link[rng.random((P, P)) < 0.2] = 0
+    recs = I.random_candidates(rng, L, P, v_max, M, 400, policies=(I.POLICY["AFAB"],))
+    args = (L, P, v_max, M, 0, costs, link, recs)
+    g = run_gpu(gpu, *args)
+    assert_same(g, run_oracle(*args), f"GPipe P={P} v_max={v_max} M={M}")
+    assert (g[0] > 0).sum() > len(recs) // 2
+
+
 def test_workload3_sample_and_bounds(gpu):
     """The 1,048,576-candidate P = 8, M = 64 batch: a stratified sample against the oracle;
     for every candidate, blocking never shortens a schedule and keeps every deadlock."""
