@@ -513,7 +513,7 @@ constexpr uint32_t QT_END = 1u << 20;
 // nothing: the slot is empty or holds the backward of micro-batch m - R, which this device has
 // already run, so its time never exceeds the device clock. Each round decodes its op first, so
 // the stream read and the slot read are in flight together, and loads the entry after next at
-// its start, to be committed at its end. Rl = R << lg. XM: streams are 16-byte records
+// its start, to be taken at the end of the next round. Rl = R << lg. XM: streams are 16-byte records
 // {w, dur, activation delta}; mem / peak track the activation bytes held. XC: 16-byte records
 // {w, dur, output transfer time, CX flags}; cm tallies the communication nodes.
 template <int X>
@@ -524,9 +524,12 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
                                           int64_t& fs) {
   uint32_t cur = qt[row], nxt = qt[row + 1u];
   uint32_t qa = row + 2u;  // entry after next
-  for (;;) {
-    // the entry after next, needed only if this op completes; its load overlaps the round
-    const uint32_t ahead = qt[qa];
+  bool okp = false;        // whether the previous round completed its op
+  // One round: `prev` is the previous round's load of the entry after next, which becomes the
+  // next entry if that round completed its op; `ahead` receives this round's load. Returns
+  // whether any lane of the wave completed an op.
+  auto round = [&](uint32_t prev, uint32_t& ahead) -> bool {
+    ahead = qt[qa];
     const int rdj = (int)(cur & 0x7FFFu) | T.g;
     const int wrj = rdj + __mul24((int)((cur >> 15) & 3u), Rl) - Rl;
     const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
@@ -553,15 +556,24 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
       mem = ok ? mem + dm : mem;
       peak = mem > peak ? mem : peak;
     }
+    __asm__ volatile("" : "+v"(prev));  // the previous load is used here, after this one issued
+    const uint32_t n1 = okp ? prev : nxt;
     qa += ok ? 1u : 0u;
-    cur = ok ? nxt : cur;
-    nxt = ok ? ahead : nxt;
-    if (__ballot(ok) == 0) {
-      const uint64_t actm = __ballot(cur != QT_END);
-      if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
-      break;
-    }
+    cur = ok ? n1 : cur;
+    nxt = n1;
+    okp = ok;
+    return __ballot(ok) != 0;
+  };
+  // two rounds per iteration, the loads alternating between a0 and a1, and one exit: a round
+  // after one in which no lane moved changes nothing either, so the wave has settled
+  uint32_t a0 = 0, a1 = 0;
+  for (;;) {
+    const bool g0 = round(a1, a0);
+    const bool g1 = round(a0, a1);
+    if (!(g0 && g1)) break;
   }
+  const uint64_t actm = __ballot(cur != QT_END);
+  if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
 }
 
 __device__ __forceinline__ int64_t group_max(int64_t x, int G) {
