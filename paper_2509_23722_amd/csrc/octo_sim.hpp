@@ -523,13 +523,16 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
                                           int64_t& mem, int64_t& peak, CommTally& cm,
                                           int64_t& fs) {
   uint32_t cur = qt[row], nxt = qt[row + 1u];
-  uint32_t qa = row + 2u;  // entry after next
-  bool okp = false;        // whether the previous round completed its op
+  // byte offset of the entry after next (32 bits: the load takes the table's address as its
+  // scalar base and this offset as its only per-lane address)
+  uint32_t qb = (row + 2u) * 4u;
+  const char* qtb = reinterpret_cast<const char*>(qt);
+  bool okp = false;  // whether the previous round completed its op
   // One round: `prev` is the previous round's load of the entry after next, which becomes the
   // next entry if that round completed its op; `ahead` receives this round's load. Returns
   // whether any lane of the wave completed an op.
   auto round = [&](uint32_t prev, uint32_t& ahead) -> bool {
-    ahead = qt[qa];
+    ahead = *reinterpret_cast<const uint32_t*>(qtb + qb);
     const int rdj = (int)(cur & 0x7FFFu) | T.g;
     const int wrj = rdj + __mul24((int)((cur >> 15) & 3u), Rl) - Rl;
     const uint32_t mask = (cur >> 17) & 7u, want = (cur >> 20) & 7u, state = (cur >> 23) & 7u;
@@ -558,7 +561,7 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
     }
     __asm__ volatile("" : "+v"(prev));  // the previous load is used here, after this one issued
     const uint32_t n1 = okp ? prev : nxt;
-    qa += ok ? 1u : 0u;
+    qb += ok ? 4u : 0u;
     cur = ok ? n1 : cur;
     nxt = n1;
     okp = ok;
