@@ -2337,14 +2337,35 @@ __device__ __forceinline__ int chain_class(const TuneArgs& t, int64_t i) {
                                                           : 2 * t.s.pr.v_max;
 }
 
+// Both count per block in LDS first (one LDS atomic per class per wave, one global atomic per
+// class per block): a global atomic per chain on a handful of counters serialises.
+constexpr int NCLASS = 2 * 8 + 1;
 __global__ void k_chain_count(TuneArgs t) {
+  __shared__ int hist[NCLASS];
+  for (int b = threadIdx.x; b < NCLASS; b += blockDim.x) hist[b] = 0;
+  __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < t.n_chains) atomicAdd(&t.s.ctl[CTL_COUNTS + chain_class(t, i)], 1);
+  const bool in = i < t.n_chains;
+  wave_hist_add(hist, in ? chain_class(t, i) : 0, in);
+  __syncthreads();
+  for (int b = threadIdx.x; b < NCLASS; b += blockDim.x)
+    if (hist[b]) atomicAdd(&t.s.ctl[CTL_COUNTS + b], hist[b]);
 }
 
 __global__ void k_chain_scatter(TuneArgs t, int32_t* __restrict__ list) {
+  __shared__ int hist[NCLASS];
+  __shared__ int res[NCLASS];
+  for (int b = threadIdx.x; b < NCLASS; b += blockDim.x) hist[b] = 0;
+  __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < t.n_chains) list[atomicAdd(&t.s.ctl[CTL_POS + chain_class(t, i)], 1)] = (int32_t)i;
+  const bool in = i < t.n_chains;
+  const int cls = in ? chain_class(t, i) : 0;
+  const int local = wave_hist_add(hist, cls, in);
+  __syncthreads();
+  for (int b = threadIdx.x; b < NCLASS; b += blockDim.x)
+    res[b] = hist[b] ? atomicAdd(&t.s.ctl[CTL_POS + b], hist[b]) : 0;
+  __syncthreads();
+  if (in) list[res[cls] + local] = (int32_t)i;
 }
 
 // One step of every chain on 40-bit ring tables: R rows per stage (R < M), the wave's groups
