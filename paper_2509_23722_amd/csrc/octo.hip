@@ -556,45 +556,51 @@ __device__ __forceinline__ int64_t live_count(const SimArgs& a) {
   return l < a.n ? l : a.n;
 }
 
-// One thread per candidate, blocks of CLS_THREADS. The records' heads (first hb bytes: header,
-// boundaries, placement) are staged through LDS with 16-byte coalesced loads.
-constexpr int CLS_THREADS = 256;
+// One thread per candidate, blocks of CLS_THREADS taking CLS_ITEMS runs of CLS_THREADS
+// candidates each, so that each block adds its bin counts to the global counters once for all
+// its runs (one global atomic per bin and block: with one block per run, thousands of blocks
+// queue on the same few counters). The records' heads (first hb bytes: header, boundaries,
+// placement) are staged through LDS with 16-byte coalesced loads.
+constexpr int CLS_THREADS = 256, CLS_ITEMS = 4;
 __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __restrict__ bins,
                                                           int hb) {
   extern __shared__ __align__(16) uint8_t heads[];
   __shared__ int hist[NBINS];
   for (int i = threadIdx.x; i < NBINS; i += blockDim.x) hist[i] = 0;
-  const int64_t first = (int64_t)blockIdx.x * CLS_THREADS;
   const int64_t n = live_count(a);
-  const int cnt = first >= n ? 0 : (int)(n - first < CLS_THREADS ? n - first : CLS_THREADS);
   const int q = hb / 16, stride16 = a.pr.stride / 16;
-  const uint4* src = reinterpret_cast<const uint4*>(a.cands + first * a.pr.stride);
-  uint4* dst = reinterpret_cast<uint4*>(heads);
-  for (int j = threadIdx.x; j < cnt * q; j += CLS_THREADS) {
-    const int r = j / q, c = j - r * q;
-    dst[j] = src[(int64_t)r * stride16 + c];
-  }
-  __syncthreads();
-  const int64_t i = first + threadIdx.x;
-  int bin = BIN_NONE;
-  if (threadIdx.x < cnt) {
-    const Resolved r = resolve_record(a.pr, heads + threadIdx.x * hb,
-                                      a.cands + i * a.pr.stride + pert_off(a.pr.s_max));
-    if (!r.valid) {
-      a.out_ms[i] = OCTO_MS_INVALID;
-      for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
-      if (a.out_peak)
-        for (int d = 0; d < a.pr.P; ++d) a.out_peak[i * a.pr.P + d] = OCTO_MS_INVALID;
-      if (a.out_comm)
-        for (int k = 0; k < 4; ++k) a.out_comm[i * 4 + k] = OCTO_MS_INVALID;
-      if (a.out_bound)
-        for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
-    } else {
-      bin = r.n_pert > 0 ? BIN_MAT + mat_sub(r.v, r.split) : bin_of(r.v, r.gen, r.split);
+  for (int run = 0; run < CLS_ITEMS; ++run) {
+    const int64_t first = ((int64_t)blockIdx.x * CLS_ITEMS + run) * CLS_THREADS;
+    const int cnt = first >= n ? 0 : (int)(n - first < CLS_THREADS ? n - first : CLS_THREADS);
+    const uint4* src = reinterpret_cast<const uint4*>(a.cands + first * a.pr.stride);
+    uint4* dst = reinterpret_cast<uint4*>(heads);
+    __syncthreads();  // the previous run's heads are read
+    for (int j = threadIdx.x; j < cnt * q; j += CLS_THREADS) {
+      const int r = j / q, c = j - r * q;
+      dst[j] = src[(int64_t)r * stride16 + c];
     }
-    bins[i] = (uint8_t)bin;
+    __syncthreads();
+    const int64_t i = first + threadIdx.x;
+    int bin = BIN_NONE;
+    if (threadIdx.x < cnt) {
+      const Resolved r = resolve_record(a.pr, heads + threadIdx.x * hb,
+                                        a.cands + i * a.pr.stride + pert_off(a.pr.s_max));
+      if (!r.valid) {
+        a.out_ms[i] = OCTO_MS_INVALID;
+        for (int d = 0; d < a.pr.P; ++d) a.out_bub[i * a.pr.P + d] = OCTO_MS_INVALID;
+        if (a.out_peak)
+          for (int d = 0; d < a.pr.P; ++d) a.out_peak[i * a.pr.P + d] = OCTO_MS_INVALID;
+        if (a.out_comm)
+          for (int k = 0; k < 4; ++k) a.out_comm[i * 4 + k] = OCTO_MS_INVALID;
+        if (a.out_bound)
+          for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
+      } else {
+        bin = r.n_pert > 0 ? BIN_MAT + mat_sub(r.v, r.split) : bin_of(r.v, r.gen, r.split);
+      }
+      bins[i] = (uint8_t)bin;
+    }
+    wave_hist_add(hist, bin, bin != BIN_NONE);
   }
-  wave_hist_add(hist, bin, bin != BIN_NONE);
   __syncthreads();
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
     if (hist[b]) atomicAdd(&a.ctl[CTL_COUNTS + b], hist[b]);
@@ -613,20 +619,35 @@ __global__ void k_plan(int32_t* __restrict__ ctl) {
   }
 }
 
-__global__ void k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
-                          int32_t* __restrict__ idx) {
+// Index of every valid record at its bin's cursor; blocks cover the same CLS_ITEMS runs as
+// k_classify: the runs' bins are counted first, one global atomic per bin reserves the block's
+// positions, then each run takes its part in order.
+__global__ void __launch_bounds__(CLS_THREADS) k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
+                                                         int32_t* __restrict__ idx) {
   __shared__ int hist[NBINS];
   __shared__ int res[NBINS];
   for (int b = threadIdx.x; b < NBINS; b += blockDim.x) hist[b] = 0;
   __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int bin = i < live_count(a) ? bins[i] : BIN_NONE;
-  const int local = wave_hist_add(hist, bin, bin != BIN_NONE);
+  const int64_t n = live_count(a);
+  const int64_t first = (int64_t)blockIdx.x * CLS_ITEMS * CLS_THREADS + threadIdx.x;
+  int bin[CLS_ITEMS];
+#pragma unroll
+  for (int run = 0; run < CLS_ITEMS; ++run) {
+    const int64_t i = first + run * CLS_THREADS;
+    bin[run] = i < n ? bins[i] : BIN_NONE;
+    wave_hist_add(hist, bin[run], bin[run] != BIN_NONE);
+  }
   __syncthreads();
-  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x) {
     res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_POS + b], hist[b]) : 0;
+    hist[b] = 0;
+  }
   __syncthreads();
-  if (bin != BIN_NONE) idx[res[bin] + local] = (int32_t)i;
+#pragma unroll
+  for (int run = 0; run < CLS_ITEMS; ++run) {
+    const int local = wave_hist_add(hist, bin[run], bin[run] != BIN_NONE);
+    if (bin[run] != BIN_NONE) idx[res[bin[run]] + local] = (int32_t)(first + run * CLS_THREADS);
+  }
 }
 
 // Locate chunk `ch` (of CPW candidates) among the generated bins in `mask`, in bin order;
@@ -3445,7 +3466,7 @@ int classify_sort(const octo_problem* prob, const Setup& su, const SimArgs& a, i
                   hipStream_t stream) {
   char* base = static_cast<char*>(su.ws->base);
   const int tb = CLS_THREADS;
-  const int nb = (int)((n + tb - 1) / tb);
+  const int nb = (int)((n + (int64_t)tb * CLS_ITEMS - 1) / ((int64_t)tb * CLS_ITEMS));
   uint8_t* bins = reinterpret_cast<uint8_t*>(base + su.l.bin_of);
   const int hb = (int)align_up((size_t)pert_off(prob->P * prob->v_max), 16);
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_classify),
