@@ -421,17 +421,24 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
 // Kernels
 // ---------------------------------------------------------------------------------------------
 
-// mem (nullable): layer memory [L][2], its prefix sums go to pre_mem.
+// mem (nullable): layer memory [L][2], its prefix sums go to pre_mem. The block loads the
+// tables into LDS first (L <= 255), so the serial sums wait on LDS, not on a global load and
+// store per layer.
 __global__ void k_prep(const int64_t* __restrict__ costs, const int64_t* __restrict__ mem, int L,
                        int64_t* __restrict__ pre, int64_t* __restrict__ pre_mem,
                        int32_t* __restrict__ ctl) {
+  __shared__ int64_t sc[3 * 255], sm[2 * 255];
   const int t = threadIdx.x;
   for (int i = t; i < CTL_WORDS; i += blockDim.x) ctl[i] = 0;
+  for (int i = t; i < 3 * L; i += blockDim.x) sc[i] = costs[i];
+  if (mem)
+    for (int i = t; i < 2 * L; i += blockDim.x) sm[i] = mem[i];
+  __syncthreads();
   if (t < 3) {
     int64_t acc = 0;
     pre[t] = 0;
     for (int l = 0; l < L; ++l) {
-      acc += costs[3 * l + t];
+      acc += sc[3 * l + t];
       pre[3 * (l + 1) + t] = acc;
     }
   } else if (t < 5 && mem) {
@@ -439,7 +446,7 @@ __global__ void k_prep(const int64_t* __restrict__ costs, const int64_t* __restr
     int64_t acc = 0;
     pre_mem[c] = 0;
     for (int l = 0; l < L; ++l) {
-      acc += mem[2 * l + c];
+      acc += sm[2 * l + c];
       pre_mem[2 * (l + 1) + c] = acc;
     }
   }
