@@ -144,7 +144,7 @@ int octo_sim_batch_bounds(const octo_problem* prob, const int64_t* layer_costs,
 /*
  * octo_sim_batch_comm — octo_sim_batch plus communication accounting (§5: send and receive
  * nodes of the cross-device dependencies; the simulator marks a node overlappable when it can
- * run beside a computation and records the overlap time; §7's communication statistics). Every
+ * run beside a computation and records the overlap time; §8's communication statistics). Every
  * data edge between stages on different devices, F(s,m) -> F(s+1,m) or B(s+1,m) -> B(s,m), is
  * one send node on the producer's device and one receive node on the consumer's, each lasting
  * c = link[producer device][consumer device], the transfer running from the producer's end for
@@ -191,7 +191,7 @@ int octo_sim_batch_rdv(const octo_problem* prob, const int64_t* layer_costs, con
 
 /*
  * octo_sim_batch_ordered — blocking rendezvous transfers (as octo_sim_batch_rdv) in the
- * deadlock-free, overlap-aware reordered coordination of §8 ("Unified Pipeline Executor":
+ * deadlock-free, overlap-aware reordered coordination of §7 ("Unified Pipeline Executor":
  * reorder the communication operations to break cyclic waits while keeping transfers beside
  * the computation around them). Each device keeps its compute order; every transfer is placed at
  * its ideal start, the end of its producer in the asynchronous schedule of octo_sim_batch, where

@@ -20,7 +20,7 @@
  * of earliest start times. A cycle (ops left unvisited) is a deadlock.
  *
  * Parity pins (tests/test_oracle_*.py): closed forms for AFAB/1F1B/interleaved/ZB, the §3.2
- * Fig. 3 worked example, the §3.3 order count, the §7 comm-count table, invariants, a pure-Python
+ * Fig. 3 worked example, the §3.3 order count, the §8 comm-count table, invariants, a pure-Python
  * tick simulator and DFS cycle check on tiny instances, and numpy's Philox.
  */
 #include <pthread.h>
@@ -405,7 +405,7 @@ static void naive_programs(const ref_dag_in* g, const ref_sop* queue, const int*
 }
 
 /*
- * Deadlock-free, overlap-aware reordering of the communication (§8, "Unified Pipeline Executor"):
+ * Deadlock-free, overlap-aware reordering of the communication (§7, "Unified Pipeline Executor"):
  * each device keeps its compute order, and every transfer is placed at its ideal start — the end
  * of its producer in the asynchronous schedule (start[] of the plain model), the moment its data
  * is ready. A device's items are sorted by one global key: (time, communication before
@@ -778,7 +778,7 @@ static void peak_memory(const ref_dag_in* g, const ref_sop* sq, const int* qoff,
 }
 
 /* Communication nodes and their overlap (§5 "Estimating Pipeline Performance"; the comm counts
- * of §7's communication table). Every cross-device data edge X -> Y is a send node on X's device
+ * of §8's communication table). Every cross-device data edge X -> Y is a send node on X's device
  * and a receive node on Y's, each lasting c = link[dev X][dev Y]; the transfer runs from X's
  * end for c. A node overlaps with the computation adjacent to it in its device's order — a send
  * with the op that follows X, a receive with the op that precedes Y — by the time both run:

@@ -1344,7 +1344,7 @@ __global__ void __launch_bounds__(WAVE) k_sim_mat40(SimArgs a, int mode) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Deadlock-free reordered coordination (§8 "Unified Pipeline Executor"): every device keeps its
+// Deadlock-free reordered coordination (§7 "Unified Pipeline Executor"): every device keeps its
 // compute order and places each transfer at its ideal start — its producer's end in the
 // asynchronous schedule — with blocking rendezvous transfers. A device's program is its items
 // sorted by (time, communication before computation, then the producer's id (kind, stage, m) for

@@ -5,7 +5,7 @@ only draws random numbers and packs the candidate-record byte format that the C 
 that the CPU oracle and the HIP path can be fed identical inputs.
 
 The workloads stand in for the paper's profiled layer costs of LLaMA / Jamba / Nemotron-H
-(§7, model table), which are not available: per-layer forward costs are drawn per layer type
+(§8, model table), which are not available: per-layer forward costs are drawn per layer type
 (uniform or lognormal around a type mean) and the backward halves cost one forward each
 (``{F, B, W} = {f, f, f}``; a fused backward therefore costs 2f).
 """

@@ -150,7 +150,7 @@ def test_deadlock_backward_before_own_forward():
 
 def test_deadlock_cross_device_two_cycle():
     """Device 0 runs B(0,m) before F(0,m'), while device 1 runs F(1,m') before B(1,m): each waits
-    on the other (the cyclic wait of §3.3 / §8)."""
+    on the other (the cyclic wait of §3.3 / §7)."""
     P = S = 2
     M = 2
     ones = np.ones(2, dtype=np.int64)

@@ -1,6 +1,6 @@
 """Pins of the oracle's communication accounting (§5: send and receive nodes of every
 cross-device dependency, overlappable when they can run beside a computation, overlap time the
-length both run; the #Comm column of §7's communication table).
+length both run; the #Comm column of §8's communication table).
 
 Reading: a send node overlaps with the op that follows its producer on the producer's device, a
 receive node with the op that precedes its consumer on the consumer's device, by the length of
@@ -48,7 +48,7 @@ def test_afab_closed_form(P, M, f, b, c):
 
 
 def test_comm_count_table():
-    """§7 communication table: #Comm = 4 (S-1) M when every stage boundary crosses devices."""
+    """§8 communication table: #Comm = 4 (S-1) M when every stage boundary crosses devices."""
     kv, rows = read_golden("comm_table.txt")
     P, M = int(kv["devices"]), int(kv["micro_batches"])
     for S_str, comm_str in rows:

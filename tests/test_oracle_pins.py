@@ -79,7 +79,7 @@ def test_zero_bubble_closed_form(P, v, M):
 
 
 def test_comm_count_table():
-    """§7 comm table: #Comm = send + recv nodes = 2 x cross-device edges = 4 (S-1) M."""
+    """§8 comm table: #Comm = send + recv nodes = 2 x cross-device edges = 4 (S-1) M."""
     kv, rows = read_golden("comm_table.txt")
     P, M = int(kv["devices"]), int(kv["micro_batches"])
     for S_str, comm_str in rows:

@@ -122,7 +122,7 @@ def test_invariants():
 
 # ---------------------------------------------------------------------------------------------
 # The reordered coordination (deadlock-free, overlap-aware reordering of the communication,
-# §8 "Unified Pipeline Executor"): each transfer at its ideal start in the asynchronous schedule.
+# §7 "Unified Pipeline Executor"): each transfer at its ideal start in the asynchronous schedule.
 # ---------------------------------------------------------------------------------------------
 
 def test_ordered_worked_example():
