@@ -143,14 +143,16 @@ int octo_sim_batch_bounds(const octo_problem* prob, const int64_t* layer_costs,
 
 /*
  * octo_sim_batch_comm — octo_sim_batch plus communication accounting (§5: send and receive
- * nodes of the cross-device dependencies; the simulator marks a node overlappable when it can
- * run beside a computation and records the overlap time; §8's communication statistics). Every
- * data edge between stages on different devices, F(s,m) -> F(s+1,m) or B(s+1,m) -> B(s,m), is
- * one send node on the producer's device and one receive node on the consumer's, each lasting
+ * nodes of the cross-device dependencies; a node that can overlap with subsequent computation
+ * is overlappable and records the minimum of the computation's and the communication's
+ * durations as its overlap time; §8's communication statistics). Every data edge between
+ * stages on different devices, F(s,m) -> F(s+1,m) or B(s+1,m) -> B(s,m), is one send node on
+ * the producer's device and one receive node on the consumer's, each lasting
  * c = link[producer device][consumer device], the transfer running from the producer's end for
- * c (as in the time model). A send overlaps with the op that follows the producer on its device,
- * a receive with the op that precedes the consumer on its device, by the length of time that op
- * and the transfer both run; a node is overlappable iff that length is > 0.
+ * c (as in the time model). A send can run beside the op that follows the producer on its
+ * device, a receive beside the op that precedes the consumer on its device (the consumer waits
+ * for the data); the node is overlappable iff that op runs during the transfer (a positive
+ * shared length), and its overlap time is min(duration of that op, c).
  *   out_comm  int64 [n][4]: {comm nodes, overlappable nodes, total node time (each edge counted
  *             twice, once per node), total overlap time}; OCTO_MS_DEADLOCK / OCTO_MS_INVALID in
  *             all four like the makespan.

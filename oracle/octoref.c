@@ -780,9 +780,12 @@ static void peak_memory(const ref_dag_in* g, const ref_sop* sq, const int* qoff,
 /* Communication nodes and their overlap (§5 "Estimating Pipeline Performance"; the comm counts
  * of §8's communication table). Every cross-device data edge X -> Y is a send node on X's device
  * and a receive node on Y's, each lasting c = link[dev X][dev Y]; the transfer runs from X's
- * end for c. A node overlaps with the computation adjacent to it in its device's order — a send
- * with the op that follows X, a receive with the op that precedes Y — by the time both run:
- * overlap = |[start, end] of that op ∩ [end of X, end of X + c]|; overlappable iff > 0.
+ * end for c. §5 marks a node overlappable when it can run beside subsequent computation and
+ * then records the smaller of the computation's and the communication's durations. The
+ * computation a node can run beside is the one adjacent to it in its device's order that does
+ * not wait for it: for a send, the op that follows X; for a receive, the op that precedes Y
+ * (Y itself needs the data). The node is overlappable when that op runs during the transfer
+ * (their intervals share a positive length); overlap = min(duration of that op, c).
  * comm[4] += {nodes, overlappable nodes, node time (2c per edge), overlap time}. */
 static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff, const int* qlen,
                          const int64_t* start, int64_t* comm) {
@@ -806,7 +809,7 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
           const int64_t zs = start[node_id(S, M, z.kind, z.s, z.m)];
           const int64_t zf = zs + op_dur(g, z.kind, z.s);
           const int64_t lo = zs > xf ? zs : xf, hi = zf < xf + c ? zf : xf + c;
-          if (hi > lo) comm[1] += 1, comm[3] += hi - lo;
+          if (hi > lo) comm[1] += 1, comm[3] += zf - zs < c ? zf - zs : c;
         }
       }
       /* the op's output to another device, and the op it is sent during */
@@ -821,7 +824,7 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
           const int64_t ns = start[node_id(S, M, nx.kind, nx.s, nx.m)];
           const int64_t nf = ns + op_dur(g, nx.kind, nx.s);
           const int64_t lo = ns > fin ? ns : fin, hi = nf < fin + c ? nf : fin + c;
-          if (hi > lo) comm[1] += 1, comm[3] += hi - lo;
+          if (hi > lo) comm[1] += 1, comm[3] += nf - ns < c ? nf - ns : c;
         }
       }
     }

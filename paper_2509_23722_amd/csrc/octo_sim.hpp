@@ -173,13 +173,18 @@ struct Desc {
 
 // Communication tally of one device (XC): nodes and overlappable nodes, their time and the
 // overlap time; the last op's start and the end of its outgoing transfer (-1: none).
+// §5: a send or receive node is overlappable when the computation that can run beside it —
+// for a send the op after its producer, for a receive the op before its consumer (the
+// consumer itself waits for the data) — runs during the transfer; its overlap time is then the
+// smaller of that computation's and the transfer's durations.
 struct CommTally {
   int n, nov;
   int64_t t, tov, pst, pend;
   __device__ __forceinline__ void reset() { n = nov = 0, t = tov = 0, pst = 0, pend = -1; }
-  // An op ran over [st, fin] after a device clock `clock` (the previous op's end); its input
-  // arrived at tin after a transfer of w (cx & CX_IN); its output leaves for cout
-  // (cx & CX_OUT). A receive overlaps the previous op, a send the next one (§5).
+  // An op ran over [st, fin] after a device clock `clock` (the previous op's end, which ran
+  // from pst); its input arrived at tin after a transfer of w (cx & CX_IN); its output leaves
+  // for cout (cx & CX_OUT); the previous op's output transfer ends at pend, having left at
+  // `clock`.
   __device__ __forceinline__ void op(bool ok, int cx, int64_t tin, int64_t w, int64_t clock,
                                      int64_t st, int64_t fin, int64_t cout) {
     const bool rin = ok && (cx & CX_IN);
@@ -188,10 +193,11 @@ struct CommTally {
     const int64_t shi = fin < pend ? fin : pend;
     const bool sov = ok && shi > st;
     const bool sout = ok && (cx & CX_OUT);
+    const int64_t rcomp = clock - pst, scomp = fin - st, scomm = pend - clock;
     n += (rin ? 1 : 0) + (sout ? 1 : 0);
     t += (rin ? w : 0) + (sout ? cout : 0);
     nov += (rov ? 1 : 0) + (sov ? 1 : 0);
-    tov += (rov ? rhi - rlo : 0) + (sov ? shi - st : 0);
+    tov += (rov ? (rcomp < w ? rcomp : w) : 0) + (sov ? (scomp < scomm ? scomp : scomm) : 0);
     pend = ok ? (sout ? fin + cout : -1) : pend;
     pst = ok ? st : pst;
   }

@@ -1,10 +1,12 @@
 """Pins of the oracle's communication accounting (§5: send and receive nodes of every
-cross-device dependency, overlappable when they can run beside a computation, overlap time the
-length both run; the #Comm column of §8's communication table).
+cross-device dependency; a node that can run beside subsequent computation is overlappable and
+records the smaller of the computation's and the communication's durations; the #Comm column of
+§8's communication table).
 
-Reading: a send node overlaps with the op that follows its producer on the producer's device, a
-receive node with the op that precedes its consumer on the consumer's device, by the length of
-the intersection of that op's run with the transfer [end of producer, + c]."""
+Reading: a send node can run beside the op that follows its producer on the producer's device,
+a receive node beside the op that precedes its consumer on the consumer's device (the consumer
+itself waits for the data); the node is overlappable when that op runs during the transfer
+[end of producer, + c], and its overlap time is min(duration of that op, c)."""
 import numpy as np
 import pytest
 
@@ -35,13 +37,41 @@ def test_worked_example():
                                 int(kv["comm_time_T"]) * T, int(kv["overlap_time_T"]) * T]
 
 
+def test_min_rule_example():
+    """A GPipe case worked by hand where a receive's transfer only partly meets the op it runs
+    beside: §5's min(computation, communication) gives 6T, the intersection would give 5T."""
+    kv, _ = read_golden("comm_min_rule_example.txt")
+    T = int(kv["T_ns"])
+    recs = I.pack_records(2, 1, 0, [I.POLICY["AFAB"]], [1], [[1]], [[0, 1]])
+    prob = R.problem(2, 2, 1, 2, recs.shape[1], 0)
+    f0, b0 = int(kv["stage0_F_T"]) * T, int(kv["stage0_bwd_T"]) * T
+    f1, b1 = int(kv["stage1_F_T"]) * T, int(kv["stage1_bwd_T"]) * T
+    costs = np.array([[f0, b0 // 2, b0 - b0 // 2], [f1, b1 // 2, b1 - b1 // 2]], np.int64)
+    ms, _, comm = R.sim_batch_comm(prob, costs, I.link_matrix(2, int(kv["transfer_T"]) * T), recs)
+    assert ms[0] == int(kv["makespan_T"]) * T
+    assert comm[0].tolist() == [int(kv["comm_nodes"]), int(kv["overlapped_nodes"]),
+                                int(kv["comm_time_T"]) * T, int(kv["overlap_time_T"]) * T]
+
+
+def test_overlap_time_is_min_of_durations():
+    """Overlap time per overlappable node is at most min(c, longest op) and, on uniform stages
+    with every op at least as long as c, exactly c: the sum is then c x overlappable nodes."""
+    for pol in ("1F1B", "AFAB"):
+        ms, _, comm = chain(6, 12, I.POLICY[pol], 1000, 2000, 700)
+        assert comm[0, 1] > 0 and comm[0, 3] == 700 * comm[0, 1]
+    ms, _, comm = chain(6, 12, I.POLICY["1F1B"], 1000, 2000, 1500)
+    assert 0 < comm[0, 3] <= 1500 * comm[0, 1]
+    assert comm[0, 3] >= 1000 * comm[0, 1]
+
+
 @pytest.mark.parametrize("P,M,f,b,c", [(2, 2, 1000, 2000, 300), (4, 8, 1000, 1000, 1000),
                                        (8, 16, 700, 1500, 50), (3, 5, 900, 1900, 899)])
 def test_afab_closed_form(P, M, f, b, c):
     """GPipe on uniform stages with 0 < c <= min(f, b): F(d, m) runs [(m+d) f + d c, +f], so
     each forward's transfer runs beside the next forward of its device and arrives during the
     previous forward of the receiver — except the last forward's send and the first forward's
-    receive; the backward sweep mirrors it. Overlapped nodes 4 (P-1)(M-1), each for c."""
+    receive; the backward sweep mirrors it. Overlapped nodes 4 (P-1)(M-1), each for
+    min(op, c) = c."""
     ms, _, comm = chain(P, M, I.POLICY["AFAB"], f, b, c)
     n = 4 * (P - 1)
     assert comm[0].tolist() == [n * M, n * (M - 1), n * M * c, n * (M - 1) * c]
@@ -96,3 +126,23 @@ def test_counts_and_bounds_on_random_candidates():
     ok = ~bad
     assert (comm[ok, 1] <= comm[ok, 0]).all() and (comm[ok, 3] <= comm[ok, 2]).all()
     assert ((comm[ok, 1] > 0) == (comm[ok, 3] > 0)).all() and (comm[ok, 1] > 0).sum() > 100
+
+
+def test_table_schedules_under_the_adopted_rule():
+    """§8's communication table prints #Overlap 112 of 224 for 1F1B at 8 stages and 1,330 of
+    1,760 for Interleaved at 56 stages (PP 8, M 8). Under the adopted reading of §5 the
+    textbook schedules on uniform costs (a 1F1B stage of 7 chunk costs, transfers a tenth of a
+    1F1B stage's forward) give 98 and 1,074 overlappable nodes, each overlapping for c (every op
+    is longer): the table's overlap counts are not reproduced (its #Comm is). This records the
+    figures the reading gives; it pins nothing of the paper."""
+    P, M, f, c = 8, 8, 1000, 700
+    ms, _, comm = chain(P, M, I.POLICY["1F1B"], 7 * f, 14 * f, c)
+    assert comm[0].tolist() == [224, 98, 224 * c, 98 * c]
+    v = 7
+    S = P * v
+    recs = I.pack_records(P, v, 0, [I.POLICY["I1F1B"]], [v], [np.arange(1, S)],
+                          [I.placement("looped", P, v)])
+    prob = R.problem(S, P, v, M, recs.shape[1], 0)
+    costs = np.tile(np.array([[f, f, f]], np.int64), (S, 1))
+    ms, _, comm = R.sim_batch_comm(prob, costs, I.link_matrix(P, c), recs)
+    assert comm[0].tolist() == [1760, 1074, 1760 * c, 1074 * c]
