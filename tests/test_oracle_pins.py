@@ -55,6 +55,34 @@ def test_gpipe_and_1f1b_closed_form(P, M):
         assert all(b == (P - 1) * 3 * f for b in bub)
 
 
+@pytest.mark.parametrize("P,v,M", [(2, 2, 2), (2, 2, 4), (4, 2, 4), (4, 2, 8), (8, 2, 8),
+                                   (8, 2, 64), (3, 3, 5), (4, 3, 4), (4, 2, 3), (5, 3, 2),
+                                   (16, 2, 8)])
+def test_gpipe_looped_closed_form(P, v, M):
+    """GPipe (AFAB) with v chunks per device on the looped placement, homogeneous stages, no
+    transfer cost. Every forward wave of chunk k + 1 follows chunk k's: with M >= P a device
+    is the bottleneck, F(kP + d, m) starts at (kM + d + m) f, so the forwards end at
+    (vM + P - 1) f and the backwards mirror them; with M <= P the data are, F(s, m) starts at
+    (s + m) f and the forwards end at (vP + M - 1) f. Makespan
+    (v max(M, P) + min(M, P) - 1)(f + b). A micro-batch-major forward order (every chunk of
+    micro-batch 0 before micro-batch 1), also deadlock-free, gives more, so this pins the
+    order, not only the absence of cycles."""
+    f = 5
+    want = (v * max(M, P) + min(M, P) - 1) * 3 * f
+    ms, bub = homogeneous(P, v, M, I.POLICY["AFAB"], f)
+    assert ms == want
+    S = P * v
+    dev = I.placement("looped", P, v)
+    qs = []
+    for d in range(P):
+        A = [s for s in range(S) if dev[s] == d]
+        qs.append([(F, s, m) for m in range(M) for s in A] +
+                  [(B, s, m) for m in range(M) for s in reversed(A)])
+    rc, ms_mb, *_ = R.sim_queues(P, S, M, False, dev, [f] * S, [2 * f] * S, [0] * S,
+                                 I.link_matrix(P, 0), qs)
+    assert rc == 0 and ms_mb > want
+
+
 @pytest.mark.parametrize("P,v,M", [(2, 2, 2), (2, 2, 6), (4, 2, 8), (8, 2, 64), (8, 2, 16),
                                    (4, 3, 8), (2, 4, 4), (16, 2, 32)])
 def test_interleaved_closed_form(P, v, M):

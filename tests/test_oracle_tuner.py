@@ -59,3 +59,92 @@ def test_tuner_moves_follow_philox_draws():
             assert sorted(f["dev"]) == [0, 1, 2, 3]
         else:
             assert acc[chain] in (0, 1)
+
+
+# ---------------------------------------------------------------------------------------------
+# Hand-worked pins of move kinds 1 and 2 on the two-stage example of §3.2 (Fig. 3)
+# ---------------------------------------------------------------------------------------------
+
+def _numpy_draw(seed, chain, step):
+    """(u0, u1, u2, u3) for counter (chain, step, 0, 0), key (seed, 0) from numpy's own
+    Philox4x64-10, which produces the block after the counter it holds."""
+    if chain:
+        ctr = [chain - 1, step, 0, 0]
+    else:
+        ctr = [2**64 - 1, step - 1, 0, 0]
+    bg = np.random.Philox(key=np.array([seed, 0], dtype=np.uint64),
+                          counter=np.array(ctr, dtype=np.uint64))
+    return [int(x) for x in bg.random_raw(4)]
+
+
+def _seed_for(want):
+    """The smallest seed whose step-1 draw of chain 0 satisfies want(u)."""
+    for seed in range(1, 100_000):
+        if want(_numpy_draw(seed, 0, 1)):
+            return seed
+    raise AssertionError("no seed found")
+
+
+def _fig3_chain():
+    from conftest import read_golden
+    kv, _ = read_golden("tuner_moves_fig3.txt")
+    T = int(kv["T_ns"])
+    rec = I.pack_records(2, 1, 0, [I.POLICY["1F1B"]], [1], [[1]], [[0, 1]])
+    prob = R.problem(2, 2, 1, 2, rec.shape[1], 0)
+    costs = np.array([[2, 2, 2], [4, 4, 4]], np.int64) * T
+    return kv, T, rec, prob, costs, I.link_matrix(2, 0)
+
+
+def _qrow(queues, d, n=4):
+    return [((int(e) >> 14), (int(e) >> 11) & 7, int(e) & 0x7FF) for e in queues[0, d, :n]]
+
+
+def test_start_state_of_fig3():
+    kv, T, rec, prob, costs, link = _fig3_chain()
+    out, ms, bub, acc, q = R.tune(prob, costs, link, rec, 1, 0, want_queues=True)
+    assert ms[0] == int(kv["start_makespan_T"]) * T and acc[0] == 0
+    assert _qrow(q, 0) == [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1)]
+    assert _qrow(q, 1) == [(0, 0, 0), (1, 0, 0), (0, 0, 1), (1, 0, 1)]
+
+
+def test_placement_swap_keeps_each_devices_slot_pattern():
+    """Move 1 exchanges the two devices' stage sets; each keeps its queue slot pattern, so the
+    proposal deadlocks and is rejected. Swapping the queues too would be a relabelling that is
+    accepted with the devices exchanged — the result this pin rules out."""
+    kv, T, rec, prob, costs, link = _fig3_chain()
+    seed = _seed_for(lambda u: u[0] % 3 == 1)
+    out, ms, bub, acc, q = R.tune(prob, costs, link, rec, seed, 1, want_queues=True)
+    f = I.unpack_record(out[0], 2, 1, 0)
+    assert ms[0] == int(kv["swap_makespan_T"]) * T
+    assert acc[0] == int(kv["swap_accepted"])
+    assert f["dev"] == [int(x) for x in kv["swap_dev"].split()]
+    assert f["dev"] != [int(x) for x in kv["relabel_dev"].split()]
+    # the proposal itself, evaluated directly: stage 1 on device 0 with device 0's pattern
+    qs = [[(0, 1, 0), (0, 1, 1), (1, 1, 0), (1, 1, 1)], [(0, 0, 0), (1, 0, 0), (0, 0, 1), (1, 0, 1)]]
+    rc, *_ = R.sim_queues(2, 2, 2, False, [1, 0], [2 * T, 4 * T], [4 * T, 8 * T], [0, 0], link, qs)
+    assert rc == 1  # deadlock
+
+
+def test_adjacent_swap_accepted_on_equal_makespan():
+    """Move 2 on device 1 at index 1: F0 B0 F1 B1 -> F0 F1 B0 B1, makespan 30T again, kept."""
+    kv, T, rec, prob, costs, link = _fig3_chain()
+    seed = _seed_for(lambda u: u[0] % 3 == 2 and u[1] % 2 == 1 and u[2] % 3 == 1)
+    out, ms, bub, acc, q = R.tune(prob, costs, link, rec, seed, 1, want_queues=True)
+    assert ms[0] == int(kv["adj_d1_i1_makespan_T"]) * T
+    assert acc[0] == int(kv["adj_d1_i1_accepted"])
+    assert bub[0].tolist() == [int(x) * T for x in kv["adj_d1_i1_bubble_T"].split()]
+    assert _qrow(q, 1) == [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1)]
+    assert _qrow(q, 0) == [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1)]
+
+
+def test_adjacent_swap_rejected_when_longer():
+    """Move 2 on device 0 at index 0: F1 F0 B0 B1 runs 32T > 30T, so it is not kept."""
+    kv, T, rec, prob, costs, link = _fig3_chain()
+    seed = _seed_for(lambda u: u[0] % 3 == 2 and u[1] % 2 == 0 and u[2] % 3 == 0)
+    out, ms, bub, acc, q = R.tune(prob, costs, link, rec, seed, 1, want_queues=True)
+    assert ms[0] == int(kv["start_makespan_T"]) * T and acc[0] == int(kv["adj_d0_i0_accepted"])
+    assert _qrow(q, 0) == [(0, 0, 0), (0, 0, 1), (1, 0, 0), (1, 0, 1)]
+    qs = [[(0, 0, 1), (0, 0, 0), (1, 0, 0), (1, 0, 1)], [(0, 1, 0), (1, 1, 0), (0, 1, 1), (1, 1, 1)]]
+    rc, m2, *_ = R.sim_queues(2, 2, 2, False, [0, 1], [2 * T, 4 * T], [4 * T, 8 * T], [0, 0],
+                              link, qs)
+    assert rc == 0 and m2 == int(kv["adj_d0_i0_proposal_T"]) * T
