@@ -153,12 +153,12 @@ def test_huge_costs_ring_and_full_rows(gpu, M):
             assert (g[1] > (1 << 37)).sum() > 50
 
 
-def test_workload3_sample(gpu):
+def test_workload3_candidates(gpu):
     """The 52-layer, P = 8, M = 64 batch with its memory recipe: 4,096 of its candidates
     (every stratum), 255 move slots, one capacity for all devices at the 40th percentile of the
-    candidates' largest peaks."""
+    candidates' largest peaks; every one of them against the oracle."""
     w = I.WORKLOADS[3]
-    log("advance: workload 3 sample")
+    log("advance: workload 3, 4096 candidates")
     costs, mem, link = I.layer_costs(w), I.layer_mem(w), I.link_matrix(w.P, w.link_ns)
     rng = np.random.default_rng(303)
     recs = I.candidates(w)
@@ -167,9 +167,8 @@ def test_workload3_sample(gpu):
     ms0, _, pk0 = R.sim_batch_mem(prob, costs, mem, link, recs, NTHREADS)
     cap = np.full(w.P, int(np.percentile(pk0.max(axis=1)[ms0 > 0], 40)), np.int64)
     g = run_advance(gpu, w.L, w.P, w.v_max, w.M, 255, costs, mem, cap, link, recs)
-    sample = np.sort(rng.choice(len(recs), 400, replace=False))
-    r = R.advance_w(prob, costs, mem, cap, link, recs[sample], NTHREADS)
-    check_advance(tuple(x[sample] for x in g), r, "workload 3 sample")
+    r = R.advance_w(prob, costs, mem, cap, link, recs, NTHREADS)
+    check_advance(g, r, "workload 3")
     fit0 = (pk0 <= cap).all(axis=1) & (ms0 > 0)
     fit1 = (g[3] <= cap).all(axis=1) & (g[1] > 0)
     assert (g[0][:, 2] > 0).sum() > 400 and fit1.sum() > fit0.sum() and (fit1 >= fit0).all()
@@ -259,13 +258,13 @@ def test_tune_mem_with_room_is_the_plain_search(gpu):
     check_tune(a, b, "ample capacity", 3 + 2 * P * v, peaks=False)
 
 
-def test_tune_mem_workload5_sample(gpu):
+def test_tune_mem_workload5_chains(gpu):
     """The 96-layer, P = 32, M = 256 chains with layer memory, one capacity for all devices at
-    the median of the chains' largest initial peaks: 64 chains x 6 steps on the GPU, 16 of them
+    the median of the chains' largest initial peaks: 64 chains x 6 steps on the GPU, every one
     replayed by the oracle."""
     from paper_2509_23722_amd import _lib
     w = I.WORKLOADS[5]
-    log("tune_mem: workload 5 sample")
+    log("tune_mem: workload 5, 64 chains")
     costs, link = I.layer_costs(w), I.link_matrix(w.P, w.link_ns)
     mem = I.layer_mem(w)
     recs = I.tuner_chains(w, 64)
@@ -274,9 +273,6 @@ def test_tune_mem_workload5_sample(gpu):
     cap = np.full(w.P, int(np.percentile(pk0.max(axis=1), 50)), np.int64)
     prob = _lib.problem(w.L, w.P, w.v_max, w.M, recs.shape[1], 0)
     g = run_tune_mem(gpu, prob, costs, mem, cap, 64, link, recs, w.seed, 6)
-    sample = np.arange(0, 64, 4)
-    r = R.tune_mem(rprob, costs, mem, cap, 64, link, recs[sample], w.seed, 6, NTHREADS,
-                   chain_ids=sample)
-    check_tune(tuple(x[sample] for x in g[:5]) + (None,), r[:5] + (None,), "workload 5 sample",
-               3 + 2 * w.s_max)
+    r = R.tune_mem(rprob, costs, mem, cap, 64, link, recs, w.seed, 6, NTHREADS)
+    check_tune(tuple(g[:5]) + (None,), r[:5] + (None,), "workload 5", 3 + 2 * w.s_max)
     assert (g[4] > 0).sum() > 20

@@ -128,14 +128,14 @@ def test_zero_iterations_and_sentinels(gpu):
 
 def test_benchmark_shape(gpu):
     """Records of the 1,048,576-candidate P = 8, M = 64 workload (52 layers, v <= 2), widened to
-    four move slots: the search on the GPU equals the oracle's for a sample of strata."""
+    four move slots: the search on the GPU equals the oracle's on 16 records of every stratum."""
     w = I.WORKLOADS[3]
-    log("alg1: workload 3 sample")
+    log("alg1: workload 3, 256 records")
     costs, link = I.layer_costs(w), I.link_matrix(w.P, w.link_ns)
     recs = I.candidates(w)
     rng = np.random.default_rng(9203)
     strata = recs[:, 1].astype(np.int64) * 4 + recs[:, 0]
-    pick = np.concatenate([rng.choice(np.nonzero(strata == s)[0], size=2, replace=False)
+    pick = np.concatenate([rng.choice(np.nonzero(strata == s)[0], size=16, replace=False)
                            for s in np.unique(strata)])
     sub = restride(recs[pick], w.P, w.v_max, 4)
     g = check(gpu, w.L, w.P, w.v_max, w.M, 4, costs, link, sub, 30, "workload 3")

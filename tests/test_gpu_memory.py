@@ -94,13 +94,12 @@ def test_same_times_as_plain_call(gpu):
     t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(gpu)
     ms, bub = _lib.sim_batch(prob, t(costs), t(link), t(recs))
     assert (ms.cpu().numpy() == g[0]).all() and (bub.cpu().numpy() == g[1]).all()
-    sample = np.arange(0, len(recs), 10)
-    r = run_oracle(w.L, w.P, w.v_max, w.M, 0, costs, mem, link, recs[sample])
-    assert_same(tuple(x[sample] for x in g), r, "workload 2 sample")
+    r = run_oracle(w.L, w.P, w.v_max, w.M, 0, costs, mem, link, recs)
+    assert_same(g, r, "workload 2, every candidate")
 
 
 def test_workload3_full_size(gpu):
-    """The 1,048,576-candidate batch with its memory recipe: a stratified sample against the
+    """The 1,048,576-candidate batch with its memory recipe: every candidate against the
     oracle; every peak at least the static bytes plus one micro-batch of the largest stage."""
     w = I.WORKLOADS[3]
     log("memory: workload 3")
@@ -109,15 +108,11 @@ def test_workload3_full_size(gpu):
     g = run_gpu(gpu, w.L, w.P, w.v_max, w.M, w.max_pert, costs, mem, link, recs)
     assert (g[2] > 0).all()
     assert (g[2].min(axis=1) >= mem[:, 1].min()).all()
-    rng = np.random.default_rng(33)
-    strata = recs[:, 1].astype(np.int64) * 4 + recs[:, 0]
-    sample = np.concatenate([rng.choice(np.nonzero(strata == s)[0], size=300, replace=False)
-                             for s in np.unique(strata)])
-    r = run_oracle(w.L, w.P, w.v_max, w.M, w.max_pert, costs, mem, link, recs[sample])
-    assert_same(tuple(x[sample] for x in g), r, "workload 3 sample")
+    r = run_oracle(w.L, w.P, w.v_max, w.M, w.max_pert, costs, mem, link, recs)
+    assert_same(g, r, "workload 3, every candidate")
 
 
-def test_workload4_cyclic_and_sample(gpu):
+def test_workload4_every_candidate(gpu):
     w = I.WORKLOADS[4]
     log("memory: workload 4")
     costs, mem, link = I.layer_costs(w), I.layer_mem(w), I.link_matrix(w.P, w.link_ns)
@@ -125,11 +120,8 @@ def test_workload4_cyclic_and_sample(gpu):
     g = run_gpu(gpu, w.L, w.P, w.v_max, w.M, w.max_pert, costs, mem, link, recs)
     cyc = recs[:, 2] > 0
     assert (g[2][cyc] == -1).all() and (g[2][~cyc] > 0).all()
-    rng = np.random.default_rng(44)
-    sample = np.concatenate([rng.choice(np.nonzero(~cyc)[0], size=800, replace=False),
-                             rng.choice(np.nonzero(cyc)[0], size=100, replace=False)])
-    r = run_oracle(w.L, w.P, w.v_max, w.M, w.max_pert, costs, mem, link, recs[sample])
-    assert_same(tuple(x[sample] for x in g), r, "workload 4 sample")
+    r = run_oracle(w.L, w.P, w.v_max, w.M, w.max_pert, costs, mem, link, recs)
+    assert_same(g, r, "workload 4, every candidate")
 
 
 def test_times_beyond_40bit_slots(gpu):
