@@ -5,7 +5,11 @@ with M = 64 micro-batches, v in {1, 2} stages per device, four placements and fo
 policies in equal strata (paper_2509_23722_amd/inputs.py, workload 3). One step = one
 octo_sim_batch call over the whole batch, inputs resident in GPU memory. Prints one JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--copy-calibration]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--headline-only]
+                    [--copy-calibration]
+
+The CPU oracle's results are compared with the GPU's for every candidate of the batch; on any
+difference the line carries "value": null and the script exits with status 1.
 """
 import argparse
 import ctypes
@@ -48,6 +52,35 @@ def algorithmic_work(recs, P, M):
     N = np.where(split, 3, 2) * S * M
     E = (N - P) + 2 * (S - 1) * M + S * M + np.where(split, S * M, 0)
     return 2 * E + N, 5 * E + 2 * N
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def host_threads():
+    """Threads for the oracle: the CPUs this process may run on, at most 16 (the host share of
+    one GPU on the benchmark machines)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def gpipe_sweep_lane_ops(recs, P, M):
+    """Work a GPipe row sweep needs per candidate: every op takes one input (its row's producer,
+    or its own device clock), so one add for the input's arrival, one max against the clock and
+    one add for the duration: 7 32-bit lane-ops per op (N = 2 S M ops, all fused)."""
+    v = recs[:, 1].astype(np.int64)
+    return 7 * 2 * P * v * M
 
 
 def hip_events(n):
@@ -291,6 +324,58 @@ def time_tuner(torch, _lib, inputs, warmup, steps, with_cpu):
     return out
 
 
+def time_strata(torch, _lib, prob, costs, link, recs_np, dev, steps, warmup):
+    """octo_sim_batch on each (v, policy) stratum of the batch on its own (131,072 candidates
+    each), timed like the headline: wall clock over `steps` calls."""
+    names = {0: "AFAB", 1: "1F1B", 2: "I1F1B", 3: "ZB"}
+    out = {}
+    for v in (1, 2):
+        for p in range(4):
+            sel = (recs_np[:, 1] == v) & (recs_np[:, 0] == p)
+            if not sel.any():
+                continue
+            r = torch.from_numpy(np.ascontiguousarray(recs_np[sel])).to(dev)
+            m = torch.empty(r.shape[0], dtype=torch.int64, device=dev)
+            b = torch.empty((r.shape[0], prob.P), dtype=torch.int64, device=dev)
+            rate, ms_, _ = time_variant(torch, _lib,
+                                        lambda: _lib.sim_batch(prob, costs, link, r, m, b),
+                                        r.shape[0], steps, warmup, kernels=False)
+            out[f"v{v}_{names[p]}"] = {"candidates": int(sel.sum()), "ms_per_call": ms_,
+                                       "candidates_per_s": rate}
+    return out
+
+
+def time_transfers(torch, recs_np, P, step_ms):
+    """Host <-> device copies a caller starting from host memory would add per batch: the
+    records in, makespans and bubbles out (pinned host buffers), and the rate they imply."""
+    n = recs_np.shape[0]
+    h_in = torch.from_numpy(recs_np).pin_memory()
+    d_in = torch.empty(h_in.shape, dtype=torch.uint8, device="cuda:0")
+    d_out = torch.empty((n, 1 + P), dtype=torch.int64, device="cuda:0")
+    h_out = torch.empty((n, 1 + P), dtype=torch.int64, pin_memory=True)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    reps = 10
+    for _ in range(2):
+        d_in.copy_(h_in, non_blocking=True)
+        h_out.copy_(d_out, non_blocking=True)
+    torch.cuda.synchronize()
+    e[0].record()
+    for _ in range(reps):
+        d_in.copy_(h_in, non_blocking=True)
+    e[1].record()
+    for _ in range(reps):
+        h_out.copy_(d_out, non_blocking=True)
+    e[2].record()
+    torch.cuda.synchronize()
+    h2d = e[0].elapsed_time(e[1]) / reps
+    d2h = e[1].elapsed_time(e[2]) / reps
+    return {"h2d_bytes": int(recs_np.nbytes), "h2d_ms": round(h2d, 4),
+            "h2d_gbs": round(recs_np.nbytes / (h2d * 1e-3) / 1e9, 2),
+            "d2h_bytes": int(n * (1 + P) * 8), "d2h_ms": round(d2h, 4),
+            "d2h_gbs": round(n * (1 + P) * 8 / (d2h * 1e-3) / 1e9, 2),
+            "pcie_inclusive_candidates_per_s": round(n / ((h2d + step_ms + d2h) * 1e-3), 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -298,6 +383,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline leg")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the headline call (for kernel traces: every simulation "
+                         "kernel dispatch is then a headline one); no other legs, no oracle")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the batch is split across GPUs by candidate "
@@ -349,6 +437,7 @@ def main():
 
     secs = t1 - t0
     value = n * args.steps / secs
+    gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()  # the headline call's results
     ms_per_step = secs / args.steps * 1e3
     per_kernel_ms = kern_ms.mean(axis=0)
     int64_c, lane_c = algorithmic_work(recs_np, w.P, w.M)
@@ -370,14 +459,21 @@ def main():
         if t.get("kernel_source_sha") == kernel_source_hash() and tk == SIM_KERNELS[dom]:
             traffic = t.get("hbm_bytes_per_launch")
     all_ms = float(per_kernel_ms.sum())
+    # every kernel priced by its own work: the generated-queue kernels by the DAG relaxation
+    # count, k_afab by what a GPipe row sweep needs
+    lane_all = lane_c.copy()
+    lane_all[pol == 0] = gpipe_sweep_lane_ops(recs_np[pol == 0], w.P, w.M)
     # per stratum: the candidates each simulation kernel handles, at that kernel's rate
     names = ["v2_generated", "v1_generated", "v3plus_generated", "gpipe_all_v", "with_moves"]
     strata = {}
     for name, kname, sel, kms in zip(names, SIM_KERNELS, sets, per_kernel_ms):
         cnt = int(sel.sum())
         if cnt:
+            work = int(lane_all[sel].sum())
             strata[name] = {"kernel": kname, "candidates": cnt, "ms": round(float(kms), 4),
-                            "candidates_per_s": round(cnt / (float(kms) * 1e-3), 1)}
+                            "candidates_per_s": round(cnt / (float(kms) * 1e-3), 1),
+                            "alg_lane_ops": work,
+                            "frac": round(work / (float(kms) * 1e-3) / 1e12 / PEAK_VALU_TOPS, 5)}
     roofline = {
         "bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU_TOPS, 2),
         "unit": "Tops/s (32-bit VALU lane-ops)", "frac": round(achieved / PEAK_VALU_TOPS, 5),
@@ -387,10 +483,27 @@ def main():
         "hbm_alg_gbs": round(n_dom * (recs_np.shape[1] + 8 + 8 * w.P) / (dom_ms * 1e-3) / 1e9, 2),
         "hbm_peak_gbs": HBM_PEAK_GBS,
         "sim_kernels_ms": {k: round(float(x), 4) for k, x in zip(SIM_KERNELS, per_kernel_ms)},
-        "all_sim_kernels_frac": round(int(lane_c.sum()) / (all_ms * 1e-3) / 1e12 / PEAK_VALU_TOPS,
-                                      5),
+        "all_sim_kernels_frac": round(int(lane_all.sum()) / (all_ms * 1e-3) / 1e12 /
+                                      PEAK_VALU_TOPS, 5),
         "strata": strata,
     }
+    out = {
+        "metric": "candidate schedules simulated/sec at P=8,M=64",
+        "value": round(value, 1), "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": w.name, "candidates": n, "P": w.P, "M": w.M, "L": w.L,
+                   "v": [1, 2], "policies": ["AFAB", "1F1B", "I1F1B", "ZB"],
+                   "placements": list(inputs.PLACEMENTS), "seed": w.seed},
+        "roofline": roofline,
+    }
+    if args.headline_only:
+        print(json.dumps(out), flush=True)
+        return
+
+    out["strata_v_policy"] = time_strata(torch, _lib, prob, costs, link, recs_np, dev,
+                                         args.steps, args.warmup)
+    out["transfers"] = time_transfers(torch, recs_np, w.P, ms_per_step)
 
     # the same batch with the memory model (peak bytes per device), timed the same way
     mem = torch.from_numpy(inputs.layer_mem(w)).to(dev)
@@ -446,39 +559,46 @@ def main():
                "sample": "every 16th candidate of the batch", "deadlocked": int((o_np == -1).sum()),
                "mean_slowdown_vs_async": round(float((o_np / ms[::16].cpu().numpy()).mean()), 4)}
 
-    gms, gbub = ms.cpu().numpy(), bub.cpu().numpy()
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
                                args.warmup, min(args.steps, 3), not args.no_cpu)
     alg1 = time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, args.warmup,
                      min(args.steps, 3), not args.no_cpu)
     tuner = time_tuner(torch, _lib, inputs, args.warmup, min(args.steps, 3), not args.no_cpu)
-    cpu = None
+    cpu, parity_ok = None, True
     if not args.no_cpu:
         from oracle import octoref
-        sample = np.arange(0, n, 4)
-        threads = min(16, os.cpu_count() or 1)
+        threads = host_threads()
         rprob = octoref.problem(w.L, w.P, w.v_max, w.M, recs_np.shape[1], w.max_pert)
+        # the whole batch on every thread the process may use: the baseline rate and the
+        # parity check of every candidate
         c0 = time.perf_counter()
-        rms, rbub = octoref.sim_batch(rprob, costs_np, link_np, recs_np[sample], nthreads=threads)
+        rms, rbub = octoref.sim_batch(rprob, costs_np, link_np, recs_np, nthreads=threads)
         c1 = time.perf_counter()
-        same = bool((rms == gms[sample]).all() and (rbub == gbub[sample]).all())
-        cpu = {"value": round(len(sample) / (c1 - c0), 1), "unit": "candidates/s",
-               "cores": threads, "kind": "oracle",
-               "sample": f"every 4th candidate of the same batch ({len(sample)} candidates, "
-                         f"{c1 - c0:.2f} s wall on {threads} threads)",
-               "parity_on_sample": same}
-        if not same:
-            print("bench: GPU results differ from the oracle on the sample", file=sys.stderr)
+        bad = (rms != gms) | (rbub != gbub).any(axis=1)
+        parity_ok = not bad.any()
+        # one thread on every 16th candidate (all strata; about as long as the full run)
+        sample = np.arange(0, n, 16)
+        c2 = time.perf_counter()
+        octoref.sim_batch(rprob, costs_np, link_np, recs_np[sample], nthreads=1)
+        c3 = time.perf_counter()
+        cpu = {"value": round(n / (c1 - c0), 1), "unit": "candidates/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"the whole batch ({n} candidates, {c1 - c0:.2f} s wall on {threads} "
+                         f"threads)",
+               "single_thread": {"value": round(len(sample) / (c3 - c2), 1),
+                                 "unit": "candidates/s",
+                                 "sample": f"every 16th candidate ({len(sample)}, "
+                                           f"{c3 - c2:.2f} s on one thread)"},
+               "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count(),
+               "parity_every_candidate": parity_ok, "mismatches": int(bad.sum())}
+        if not parity_ok:
+            i = int(np.nonzero(bad)[0][0])
+            print(f"bench: {int(bad.sum())} of {n} GPU results differ from the oracle; first "
+                  f"{i}: gpu {gms[i]} oracle {rms[i]}", file=sys.stderr)
 
-    out = {
-        "metric": "candidate schedules simulated/sec at P=8,M=64",
-        "value": round(value, 1), "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
-        "config": {"workload": w.name, "candidates": n, "P": w.P, "M": w.M, "L": w.L,
-                   "v": [1, 2], "policies": ["AFAB", "1F1B", "I1F1B", "ZB"],
-                   "placements": list(inputs.PLACEMENTS), "seed": w.seed},
-        "roofline": roofline,
+    if not parity_ok:
+        out["value"] = None
+    out.update({
         "cpu_baseline": cpu,
         "memory_model": memory_model,
         "comm_model": comm_model,
@@ -488,8 +608,10 @@ def main():
         "w_advance": w_advance,
         "alg1": alg1,
         "tuner": tuner,
-    }
+    })
     print(json.dumps(out), flush=True)
+    if not parity_ok:
+        sys.exit(1)
 
 
 if __name__ == "__main__":
