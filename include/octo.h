@@ -38,6 +38,7 @@ extern "C" {
 #define OCTO_EUNSUPPORTED (-2) /* valid problem that exceeds this GPU's limits (LDS) */
 #define OCTO_EHIP (-3)         /* a HIP runtime call or kernel launch failed */
 #define OCTO_ENOMEM (-4)       /* workspace allocation failed */
+#define OCTO_ESCRATCH (-5)     /* octo_sim_batch_noalloc: the batch does not fit its scratch */
 
 /* Per-candidate sentinel values written to makespan and every bubble entry. */
 #define OCTO_MS_DEADLOCK (-1) /* the op orders and data dependencies form a cycle */
@@ -108,6 +109,27 @@ int32_t octo_record_stride(int32_t P, int32_t v_max, int32_t max_pert);
 int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
                    void* stream);
+
+/*
+ * octo_sim_batch_noalloc — octo_sim_batch for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same evaluation, same arguments, results and per-candidate sentinels, but every buffer the
+ * call needs besides its inputs and outputs comes from a static device array of
+ * OCTO_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on until the process
+ * ends; the call makes no hipMalloc, hipFree or other allocation. The caller still passes the
+ * inputs and outputs.
+ *   A batch whose candidate lists and cached tables do not fit the array returns OCTO_ESCRATCH
+ * before any launch (at P = 8, M = 64, v_max = 2 they fit up to about 2.5 million candidates);
+ * materialised queues (candidates with moves) use as many persistent workgroups as the
+ * remaining space holds.
+ *   Every call on one GPU shares that GPU's array, which keeps the last call's contents (the
+ * call clears what must start at zero itself): calls that overlap on one GPU — on different
+ * streams, or from different threads without ordering — race and give undefined results.
+ */
+#define OCTO_NOALLOC_SCRATCH_BYTES (32u << 20)
+int octo_sim_batch_noalloc(const octo_problem* prob, const int64_t* layer_costs,
+                           const int64_t* link, const void* candidates, int64_t n,
+                           int64_t* out_makespan, int64_t* out_bubble, void* stream);
 
 /*
  * octo_sim_batch_mem — octo_sim_batch plus the memory model (§5: every compute node has a memory

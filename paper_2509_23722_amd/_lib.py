@@ -45,6 +45,8 @@ def lib():
         L.octo_queue_capacity.restype = i32
         L.octo_sim_batch.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
         L.octo_sim_batch.restype = ctypes.c_int
+        L.octo_sim_batch_noalloc.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
+        L.octo_sim_batch_noalloc.restype = ctypes.c_int
         L.octo_sim_batch_mem.argtypes = [pp, vp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_comm.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_serial.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
@@ -116,6 +118,20 @@ def sim_batch(prob, layer_costs, link, candidates, out_makespan=None, out_bubble
         _dev_ptr(out_makespan, torch.int64, "out_makespan"),
         _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
     _check(rc, "octo_sim_batch")
+    return out_makespan, out_bubble
+
+
+def sim_batch_noalloc(prob, layer_costs, link, candidates, out_makespan, out_bubble,
+                      stream=None):
+    """octo_sim_batch_noalloc: as sim_batch, with caller-allocated outputs and every other
+    buffer in the library's static device scratch (nothing is allocated by the call)."""
+    n = candidates.shape[0]
+    rc = lib().octo_sim_batch_noalloc(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+    _check(rc, "octo_sim_batch_noalloc")
     return out_makespan, out_bubble
 
 

@@ -2874,6 +2874,19 @@ struct DevInfo {
 };
 std::map<int, DevInfo> g_dev;
 
+// The static scratch of octo_sim_batch_noalloc: every device buffer that call needs besides its
+// inputs and outputs — control words, prefix sums, bins, candidate lists, materialised-queue
+// rows and the MERGE and queue tables — is carved from this array, one copy per GPU, held until
+// the process ends. Host code never passes the symbol itself (on the host it is only a stand-in
+// name): it looks up each device's address of the array once (hipGetSymbolAddress, with that
+// device current) and uses that address everywhere.
+static __device__ __align__(256) uint8_t scratch[OCTO_NOALLOC_SCRATCH_BYTES];
+struct ScratchDev {
+  char* ptr = nullptr;  // this device's address of `scratch` (null until looked up)
+  Workspace ws;         // the regions carved from it; tables cached there between calls
+};
+std::map<int, ScratchDev> g_scratch;
+
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 int check_problem(const octo_problem* p) {
@@ -3132,6 +3145,30 @@ TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool wide) {
 // Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), encoded for
 // each v's launch geometry; rebuilt when (P, v_max, M), the geometry or the MERGE tables
 // change. Entry offsets are kept in the workspace.
+// Entry offsets of the queue tables: INTER rows by (v, split), MERGE rows by split, and the
+// final terminators; returns the number of entries, terminators included.
+int64_t qtab_offsets(const octo_problem* p, int64_t inter[2][2], int64_t merge[2],
+                     int64_t* end) {
+  const int P = p->P, M = p->M, vmax2 = std::min(p->v_max, 2);
+  int64_t off = 0;
+  // rows of n entries + 2 terminators
+  for (int v = 1; v <= 2; ++v)
+    for (int split = 0; split <= 1; ++split) {
+      inter[v - 1][split] = off;
+      if (v <= vmax2) off += (int64_t)P * ((split ? 3 : 2) * v * M + 2);
+    }
+  const int S2 = 2 * P;
+  const int64_t pairs = (int64_t)S2 * (S2 - 1) / 2;
+  for (int split = 0; split <= 1; ++split) {
+    merge[split] = off;
+    if (vmax2 >= 2) off += pairs * ((split ? 3 : 2) * 2 * M + 2);
+  }
+  *end = off;
+  // the final terminators: idle lanes start there, and a lane past its last op reads up to
+  // two entries beyond its row
+  return off + 3;
+}
+
 int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool wide, hipStream_t stream) {
   const int P = p->P, M = p->M, vmax2 = std::min(p->v_max, 2);
   TabGeom geo[2] = {tab_geom(p, lds_max, 1, wide), tab_geom(p, lds_max, 2, wide)};
@@ -3141,25 +3178,13 @@ int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool wide, hip
   if (same) return OCTO_OK;
   for (int v = 1; v <= vmax2; ++v)
     if (geo[v - 1].plan.CPW < 1) return OCTO_OK;  // no table-driven launch fits: generate
-  int64_t off = 0;
-  // rows of n entries + 2 terminators
-  for (int v = 1; v <= vmax2; ++v)
-    for (int split = 0; split <= 1; ++split) {
-      ws.qt_inter[v - 1][split] = off;
-      off += (int64_t)P * ((split ? 3 : 2) * v * M + 2);
-    }
+  const int64_t entries = qtab_offsets(p, ws.qt_inter, ws.qt_merge, &ws.qt_end);
+  if (entries > INT32_MAX) return OCTO_OK;  // entry indices are 32-bit: generate instead
+  const int64_t off = ws.qt_end;
   const int S2 = 2 * P;
   const int64_t pairs = (int64_t)S2 * (S2 - 1) / 2;
-  for (int split = 0; split <= 1; ++split) {
-    ws.qt_merge[split] = off;
-    if (vmax2 >= 2) off += pairs * ((split ? 3 : 2) * 2 * M + 2);
-  }
-  ws.qt_end = off;
-  if (off + 3 > INT32_MAX) return OCTO_OK;  // entry indices are 32-bit: generate instead
   ws.qt_valid = false;
-  // the final terminators: idle lanes start there, and a lane past its last op reads up to
-  // two entries beyond its row
-  const size_t bytes = (size_t)(off + 3) * 4;
+  const size_t bytes = (size_t)entries * 4;
   const int rc = ensure_buf(ws.qt, ws.qt_bytes, bytes, stream);
   if (rc) return rc;
   uint32_t* q = static_cast<uint32_t*>(ws.qt);
@@ -3181,11 +3206,64 @@ int build_qtab(const octo_problem* p, Workspace& ws, int lds_max, bool wide, hip
   return OCTO_OK;
 }
 
+// Carve the device's static scratch for one octo_sim_batch_noalloc call: the MERGE tables,
+// the v = 2 MERGE rows and the queue tables first (their sizes depend only on the problem, so
+// they stay where they are, and stay cached, while the problem does not change), then the
+// per-call part. Narrows the materialised-queue grids to the queue rows that fit after the
+// per-call lists. On the first call on a device, looks up its address of the array.
+int scratch_regions(const octo_problem* prob, int dev, int64_t n, Setup* su) {
+  ScratchDev& sd = g_scratch[dev];
+  if (!sd.ptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, scratch) != hipSuccess || !p) return OCTO_EHIP;
+    sd.ptr = static_cast<char*>(p);
+  }
+  Workspace& ws = sd.ws;
+  const size_t cap = OCTO_NOALLOC_SCRATCH_BYTES;
+  const size_t mt = prob->v_max >= 2 ? align_up(std::max<size_t>(mtab_entries(prob) * 4, 256), 256)
+                                     : 0;
+  const size_t mr = prob->v_max >= 2 ? align_up(merge_rows_bytes(prob), 256) : 0;
+  int64_t qi[2][2], qm[2], qe;
+  const size_t qt = align_up((size_t)qtab_offsets(prob, qi, qm, &qe) * 4, 256);
+  const size_t tables = mt + mr + qt;
+  // the per-call part without materialised-queue rows, then the rows that fit after it
+  const size_t lists = layout(prob, su->big, n, 0).total;
+  if (tables + lists > cap) return OCTO_ESCRATCH;
+  const size_t row_bytes = (size_t)prob->P * su->big.qcap * 2;
+  const int64_t slots = (int64_t)((cap - tables - lists) / row_bytes);
+  auto narrow = [&](int& grid, int cpw) -> bool {
+    if (cpw < 1 || grid < 1) return true;
+    grid = (int)std::min<int64_t>(grid, slots / cpw);
+    return grid >= 1;
+  };
+  if (!narrow(su->mat_grid, su->big.CPW) || !narrow(su->m40_grid, su->m40.CPW) ||
+      !narrow(su->m40f_grid, su->m40f.CPW))
+    return OCTO_ESCRATCH;
+  char* base = sd.ptr;
+  char* mt_p = mt ? base : nullptr;
+  char* mr_p = mr ? base + mt : nullptr;
+  char* qt_p = base + mt + mr;
+  // tables moved (another problem shape): rebuild them
+  if (ws.mt != mt_p || ws.mt_bytes != mt || ws.mr != mr_p || ws.mr_bytes != mr ||
+      ws.qt != qt_p || ws.qt_bytes != qt)
+    ws.mt_valid = ws.qt_valid = false;
+  ws.mt = mt_p, ws.mt_bytes = mt;
+  ws.mr = mr_p, ws.mr_bytes = mr;
+  ws.qt = qt_p, ws.qt_bytes = qt;
+  ws.base = base + tables;
+  ws.bytes = cap - tables;
+  return OCTO_OK;
+}
+
 // Shared front half of octo_sim_batch and octo_tune_step: device, plans, workspace, prefix
 // sums, MERGE tables.
 // mem (nullable): layer memory [L][2], prefix-summed next to the costs.
+// noalloc: take every buffer from the device's static scratch (octo_sim_batch_noalloc) instead
+// of the grow-only workspace; the persistent materialised-queue launches are then narrowed to
+// the queue rows that fit, and a batch whose other buffers do not fit is OCTO_ESCRATCH.
 int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
-            hipStream_t stream, int64_t n, Setup* su, int64_t extra_slots = 0) {
+            hipStream_t stream, int64_t n, Setup* su, int64_t extra_slots = 0,
+            bool noalloc = false) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
   int rc = dev_info(dev, &su->di);
@@ -3212,12 +3290,14 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
              : occupancy_grid(k_sim_mat40<8, XM>, su->m40f.lds_bytes, su->di.cus, &su->m40f_grid);
     if (rc) return rc;
   }
+  if (noalloc && (rc = scratch_regions(prob, dev, n, su))) return rc;
   su->l = layout(prob, su->big, n,
                  std::max<int64_t>({(int64_t)su->mat_grid * su->big.CPW,
                                     (int64_t)su->m40_grid * std::max(su->m40.CPW, 0),
                                     (int64_t)su->m40f_grid * std::max(su->m40f.CPW, 0),
                                     extra_slots}));
-  Workspace& ws = g_ws[std::make_pair(dev, stream)];
+  Workspace& ws = noalloc ? g_scratch[dev].ws : g_ws[std::make_pair(dev, stream)];
+  if (noalloc && su->l.total > ws.bytes) return OCTO_ESCRATCH;
   rc = ensure_buf(ws.base, ws.bytes, su->l.total, stream);
   if (rc) return rc;
   su->ws = &ws;
@@ -3494,11 +3574,12 @@ int classify_sort(const octo_problem* prob, const Setup& su, const SimArgs& a, i
 template <int X>
 int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
                   const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
-                  int64_t* out_bubble, const Extra& ex, hipStream_t stream) {
+                  int64_t* out_bubble, const Extra& ex, hipStream_t stream,
+                  bool noalloc = false) {
   constexpr bool MEM = X == XM;
   if (n == 0) return OCTO_OK;
   Setup su;
-  int rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, n, &su);
+  int rc = prepare(prob, layer_costs, MEM ? layer_mem : nullptr, stream, n, &su, 0, noalloc);
   if (rc) return rc;
   int64_t* pk = MEM ? ex.peak : nullptr;
   int64_t* cm = X == XC ? ex.comm : nullptr;
@@ -3596,7 +3677,8 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
 template <int X>
 int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* layer_mem,
                    const int64_t* link, const void* candidates, int64_t n, int64_t* out_makespan,
-                   int64_t* out_bubble, const Extra& ex, hipStream_t stream) {
+                   int64_t* out_bubble, const Extra& ex, hipStream_t stream,
+                   bool noalloc = false) {
   int rc = check_problem(prob);
   if (rc) return rc;
   if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
@@ -3608,7 +3690,7 @@ int sim_batch_impl(const octo_problem* prob, const int64_t* layer_costs, const i
   if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
   std::lock_guard<std::mutex> lock(g_mu);
   return sim_batch_run<X>(prob, layer_costs, layer_mem, link, candidates, n, out_makespan,
-                          out_bubble, ex, stream);
+                          out_bubble, ex, stream, noalloc);
 }
 
 // The local-search step behind octo_tune_step (MEM = false) and octo_tune_step_mem.
@@ -3910,6 +3992,13 @@ int octo_sim_batch(const octo_problem* prob, const int64_t* layer_costs, const i
                             out_bubble, Extra{}, static_cast<hipStream_t>(stream));
 }
 
+int octo_sim_batch_noalloc(const octo_problem* prob, const int64_t* layer_costs,
+                           const int64_t* link, const void* candidates, int64_t n,
+                           int64_t* out_makespan, int64_t* out_bubble, void* stream) {
+  return sim_batch_impl<XP>(prob, layer_costs, nullptr, link, candidates, n, out_makespan,
+                            out_bubble, Extra{}, static_cast<hipStream_t>(stream), true);
+}
+
 int octo_sim_batch_mem(const octo_problem* prob, const int64_t* layer_costs,
                        const int64_t* layer_mem, const int64_t* link, const void* candidates,
                        int64_t n, int64_t* out_makespan, int64_t* out_bubble, int64_t* out_peak,
@@ -4050,6 +4139,9 @@ const char* octo_strerror(int status) {
     case OCTO_EUNSUPPORTED: return "problem exceeds this GPU's limits (LDS per workgroup)";
     case OCTO_EHIP: return "HIP runtime error";
     case OCTO_ENOMEM: return "workspace allocation failed";
+    case OCTO_ESCRATCH:
+      return "the batch needs more device memory than the static scratch array of "
+             "octo_sim_batch_noalloc holds (OCTO_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }
