@@ -9,7 +9,8 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboctoref.so")
+# OCTOREF_LIB may name another build of the same source (the sanitizer build)
+LIB_PATH = os.environ.get("OCTOREF_LIB") or os.path.join(HERE, "liboctoref.so")
 
 
 class RefProblem(ctypes.Structure):
