@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 PEAK_VALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 HBM_PEAK_GBS = 8000.0
 # simulation kernels, in launch order, between the library's measurement boundaries
-SIM_KERNELS = ["k_sim<2>", "k_sim<1>", "k_sim<8>", "k_afab", "k_sim_mat<2>"]
+SIM_KERNELS = ["k_static", "k_sim<2>", "k_sim<1>", "k_sim<8>", "k_afab", "k_sim_mat<2>"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_nemotron-h-like-52L-P8-M64.json")
 
 
@@ -52,6 +52,23 @@ def algorithmic_work(recs, P, M):
     N = np.where(split, 3, 2) * S * M
     E = (N - P) + 2 * (S - 1) * M + S * M + np.where(split, S * M, 0)
     return 2 * E + N, 5 * E + 2 * N
+
+
+def static_class_mask(recs, P, v_max):
+    """Candidates that the library evaluates with a static round schedule: no moves, not AFAB,
+    v = 1, or v = 2 with looped, blocked or V-shape stage pairs (the structure classes)."""
+    pol, v, npert = recs[:, 0], recs[:, 1], recs[:, 2]
+    s_max = P * v_max
+    dev = recs[:, 3 + s_max:3 + 2 * s_max].astype(np.int64)
+    ok = (pol != 0) & (npert == 0)
+    st = ok & (v == 1)
+    if v_max >= 2:
+        i = np.arange(P)
+        lp = (dev[:, i] == dev[:, i + P]).all(axis=1)
+        bl = (dev[:, 2 * i] == dev[:, 2 * i + 1]).all(axis=1)
+        vs = (dev[:, i] == dev[:, 2 * P - 1 - i]).all(axis=1)
+        st |= ok & (v == 2) & (lp | bl | vs)
+    return st
 
 
 def cpu_model():
@@ -443,8 +460,9 @@ def main():
     int64_c, lane_c = algorithmic_work(recs_np, w.P, w.M)
     v, pol = recs_np[:, 1], recs_np[:, 0]
     # candidates each simulation kernel handles (no moves in this workload)
-    sets = [(v == 2) & (pol != 0), (v == 1) & (pol != 0), (v >= 3) & (pol != 0), pol == 0,
-            np.zeros(n, dtype=bool)]
+    stat = static_class_mask(recs_np, w.P, w.v_max)
+    sets = [stat, (v == 2) & (pol != 0) & ~stat, (v == 1) & (pol != 0) & ~stat,
+            (v >= 3) & (pol != 0), pol == 0, np.zeros(n, dtype=bool)]
     # the dominant kernel: the one that takes longest
     dom = int(np.argmax(per_kernel_ms))
     dom_ms = float(per_kernel_ms[dom])
@@ -464,7 +482,8 @@ def main():
     lane_all = lane_c.copy()
     lane_all[pol == 0] = gpipe_sweep_lane_ops(recs_np[pol == 0], w.P, w.M)
     # per stratum: the candidates each simulation kernel handles, at that kernel's rate
-    names = ["v2_generated", "v1_generated", "v3plus_generated", "gpipe_all_v", "with_moves"]
+    names = ["static_schedules", "v2_generated", "v1_generated", "v3plus_generated", "gpipe_all_v",
+             "with_moves"]
     strata = {}
     for name, kname, sel, kms in zip(names, SIM_KERNELS, sets, per_kernel_ms):
         cnt = int(sel.sum())

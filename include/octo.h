@@ -350,10 +350,12 @@ int octo_alg1_tune(const octo_problem* prob, const int64_t* layer_costs, const i
 /*
  * Measurement hook. events[0..n_events-1] are hipEvent_t handles (n_events <= 8; entries may be
  * NULL). Each later octo_sim_batch call records them on its stream at fixed boundaries around
- * its simulation kernels: events[0] before the v = 2 kernel (1F1B, I1F1B, ZB queues), [1]
- * after it, [2] after the v = 1 kernel, [3] after the v = 3..8 kernel, [4] after the AFAB
- * kernel (every v), [5] after the materialised-queue kernel (a kernel that a problem does not
- * need is skipped, so its interval is empty). A caller can time each kernel alone on the stream
+ * its simulation kernels: events[0] before the static-schedule kernel (candidates of the
+ * structure classes: v = 1, and v = 2 with looped, blocked or V-shape stage pairs), [1] after
+ * it, [2] after the v = 2 generated-queue kernel (other 1F1B, I1F1B, ZB queues), [3] after the
+ * v = 1 kernel, [4] after the v = 3..8 kernel, [5] after the AFAB kernel (every v), [6] after
+ * the materialised-queue kernel (a kernel that a problem does not need is skipped, so its
+ * interval is empty). A caller can time each kernel alone on the stream
  * it runs on. octo_profile_events(NULL, 0) turns it off. Process-wide.
  */
 int octo_profile_events(void* const* events, int32_t n_events);

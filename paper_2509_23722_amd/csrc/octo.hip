@@ -33,16 +33,17 @@ constexpr int WAVE = 64;
 
 // Workspace control block (int32 words).
 constexpr int CTL_COUNTS = 0;     // [NBINS] candidates per bin
-constexpr int CTL_START = 192;    // [NBINS] first index position of each bin
-constexpr int CTL_WORK = 128;     // chunk counters of the k_sim launches (7)
-constexpr int CTL_WORK_MAT = 136; // chunk counter of k_sim_mat, perturbed list
-constexpr int CTL_WORK_REDO = 137;// chunk counter of k_sim_mat, redo list
-constexpr int CTL_REDO = 138;     // candidates for the 64-bit path (40-bit overflow, ring bound)
-constexpr int CTL_WIDE = 139;     // perturbed candidates whose queue window passes the ring
-constexpr int CTL_WORK_WIDE = 140;// chunk counter of k_sim_mat40 over the wide list
-constexpr int CTL_TOTAL = 141;    // valid records (all bins; set by k_plan)
-constexpr int CTL_POS = 64;       // [NBINS] next index position of each bin (scatter cursor)
+constexpr int CTL_POS = 80;       // [NBINS] next index position of each bin (scatter cursor)
+constexpr int CTL_WORK = 160;     // chunk counters of the k_sim launches (7)
+constexpr int CTL_WORK_MAT = 168; // chunk counter of k_sim_mat, perturbed list
+constexpr int CTL_WORK_REDO = 169;// chunk counter of k_sim_mat, redo list
+constexpr int CTL_REDO = 170;     // candidates for the 64-bit path (40-bit overflow, ring bound)
+constexpr int CTL_WIDE = 171;     // perturbed candidates whose queue window passes the ring
+constexpr int CTL_WORK_WIDE = 172;// chunk counter of k_sim_mat40 over the wide list
+constexpr int CTL_TOTAL = 173;    // valid records (all bins; set by k_plan)
+constexpr int CTL_START = 176;    // [NBINS] first index position of each bin
 constexpr int CTL_WORDS = 256;
+static_assert(NBINS <= 80, "bin arrays of the control block hold 80 bins");
 // rounds a materialised queue is read ahead of its use (GenMatK; rows of at least 8 entries)
 constexpr int QK = 6;
 
@@ -86,6 +87,13 @@ struct SimArgs {
   int64_t qt_merge[2];     // [split], v = 2, one row per stage pair s0 < s1
   int64_t qt_end;          // the table's final terminators
   int strm_off;            // LDS byte offset of the per-lane stream table
+  // static round schedules (null: every candidate takes the generated-queue kernels): rows of
+  // st_rowlen entries, P + 1 rows per class (one per role, then a row of SC_NOP), st_cls
+  // entries apart; smeta [NSC][4] = {valid, rounds, slots, 0}
+  const uint32_t* stab;
+  const int32_t* smeta;
+  int64_t st_cls;
+  int st_rowlen;
 };
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (WAVE - 1)); }
@@ -603,6 +611,10 @@ __global__ void __launch_bounds__(CLS_THREADS) k_classify(SimArgs a, uint8_t* __
           for (int k = 0; k < 2 * a.pr.P; ++k) a.out_bound[i * 2 * a.pr.P + k] = OCTO_MS_INVALID;
       } else {
         bin = r.n_pert > 0 ? BIN_MAT + mat_sub(r.v, r.split) : bin_of(r.v, r.gen, r.split);
+        if (a.smeta) {
+          const int sc = static_class(a.pr, heads + threadIdx.x * hb + 3 + a.pr.s_max, r);
+          if (sc >= 0 && a.smeta[4 * sc] != 0) bin = BIN_STATIC + sc;
+        }
       }
       bins[i] = (uint8_t)bin;
     }
@@ -657,27 +669,35 @@ __global__ void __launch_bounds__(CLS_THREADS) k_scatter(SimArgs a, const uint8_
   }
 }
 
-// Locate chunk `ch` (of CPW candidates) among the generated bins in `mask`, in bin order;
-// returns the bin or -1. entry0: first entry of the chunk in its bin; pos0: the bin's first
-// position in the index array.
-__device__ __forceinline__ int locate_chunk(const int32_t* ctl, int CPW, uint64_t mask, int ch,
-                                            int* entry0, int* pos0) {
-  int acc = 0, base = 0;
-  for (int b = 0; b < NBIN_GEN; ++b) {
-    const int cnt = ctl[CTL_COUNTS + b];
-    if ((mask >> b) & 1) {
-      const int nch = (cnt + CPW - 1) / CPW;
-      if (ch < acc + nch) {
-        *entry0 = (ch - acc) * CPW;
-        *pos0 = base;
-        return b;
-      }
-      acc += nch;
+// The chunks of the bins in `mask` (bins < nbins <= 64), one bin per lane: its candidate count,
+// first position in the index array and the end of its chunk range (an inclusive prefix over the
+// bins in order; bins outside the mask have none). Built once per wave from the control block.
+struct ChunkMap {
+  int cnt, start, nch, end;
+  __device__ __forceinline__ void init(const int32_t* ctl, int CPW, uint64_t mask, int nbins) {
+    const int b = lane_id();
+    const bool in = b < nbins && ((mask >> b) & 1);
+    cnt = in ? ctl[CTL_COUNTS + b] : 0;
+    start = b < nbins ? ctl[CTL_START + b] : 0;
+    nch = (cnt + CPW - 1) / CPW;
+    end = nch;
+    for (int off = 1; off < WAVE; off <<= 1) {
+      const int y = __shfl_up(end, off, WAVE);
+      end += b >= off ? y : 0;
     }
-    base += cnt;
   }
-  return -1;
-}
+  // Bin of chunk ch (wave-uniform), or -1 past the last chunk; entry0: its first entry in the
+  // bin, pos0: the bin's first index position, count: the bin's candidates.
+  __device__ __forceinline__ int locate(int ch, int nbins, int CPW, int* entry0, int* pos0,
+                                        int* count) const {
+    const int b = __popcll(__ballot(lane_id() < nbins && end <= ch));
+    if (b >= nbins) return -1;
+    *count = __shfl(cnt, b, WAVE);
+    *pos0 = __shfl(start, b, WAVE);
+    *entry0 = (ch - (__shfl(end, b, WAVE) - __shfl(nch, b, WAVE))) * CPW;
+    return b;
+  }
+};
 
 template <int VMAX, int X>
 __device__ __forceinline__ void dispatch_gen(const SimArgs& a, int gen, int64_t cand, int v,
@@ -706,16 +726,23 @@ __global__ void __launch_bounds__(WAVE) k_sim(SimArgs a) {
   __shared__ int64_t mbox[X == XR ? WAVE : 1];  // rendezvous mailboxes
   const int g = lane_id() / a.G;
   const int d = lane_id() % a.G;
-  for (;;) {
-    int ch = 0;
-    if (lane_id() == 0) ch = atomicAdd(&a.ctl[a.work], 1);
-    ch = bcast(ch);
-    int entry0 = 0, pos0 = 0;
-    const int bin = locate_chunk(a.ctl, a.CPW, a.bin_mask, ch, &entry0, &pos0);
+  ChunkMap cm;
+  cm.init(a.ctl, a.CPW, a.bin_mask, NBIN_GEN);
+  // chunks from a work counter: their rounds vary with each candidate's structure, and the
+  // queue keeps the waves evenly loaded (these launches take few enough chunks that the
+  // counter's atomics do not serialise them). The first chunk of every wave is its block index,
+  // so a launch with little or no work takes no atomic at all.
+  for (int first = 1;; first = 0) {
+    int ch = (int)blockIdx.x;
+    if (!first) {
+      if (lane_id() == 0) ch = (int)gridDim.x + atomicAdd(&a.ctl[a.work], 1);
+      ch = bcast(ch);
+    }
+    int entry0 = 0, pos0 = 0, cnt = 0;
+    const int bin = cm.locate(ch, NBIN_GEN, a.CPW, &entry0, &pos0, &cnt);
     if (bin < 0) break;
     int v, gen, split;
     bin_decode(bin, &v, &gen, &split);
-    const int cnt = a.ctl[CTL_COUNTS + bin];
     const int e = entry0 + g;
     const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
     if ((gen == GEN_AFAB && X != XR) || ((a.redo_bins >> bin) & 1)) {
@@ -881,17 +908,18 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
   int64_t* lfr = bsy + (size_t)P * lanes;  // XS: link free time after row t, lfr[t * lanes]
   int64_t* bfs = bsy + (size_t)P * lanes;  // XB: first start bfs[d * lanes] (-1 before)
-  for (;;) {
-    int ch = 0;
-    if (lane == 0) ch = atomicAdd(&a.ctl[a.work], 1);
-    ch = bcast(ch);
-    int entry0 = 0, pos0 = 0;
-    const int bin = locate_chunk(a.ctl, lanes, a.bin_mask, ch, &entry0, &pos0);
+  ChunkMap cmap;
+  cmap.init(a.ctl, lanes, a.bin_mask, NBIN_GEN);
+  // chunks by grid stride: AFAB candidates of one bin cost alike, and an atomic work counter
+  // would serialise the waves
+  for (int ch = (int)blockIdx.x;; ch += (int)gridDim.x) {
+    int entry0 = 0, pos0 = 0, cnt = 0;
+    const int bin = cmap.locate(ch, NBIN_GEN, lanes, &entry0, &pos0, &cnt);
     if (bin < 0) break;
     int v, gen, split;
     bin_decode(bin, &v, &gen, &split);
     const int e = entry0 + lane;
-    if (lane >= lanes || e >= a.ctl[CTL_COUNTS + bin]) continue;
+    if (lane >= lanes || e >= cnt) continue;
     const int64_t cand = a.idx[pos0 + e];
     const uint8_t* rec = a.cands + cand * a.pr.stride;
     const uint8_t* bnd = rec + 4;
@@ -979,6 +1007,299 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
         a.out_bound[(cand * P + d) * 2] = bfs[d * lanes] < 0 ? 0 : bfs[d * lanes];
         a.out_bound[(cand * P + d) * 2 + 1] = clk[d * lanes];
       }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Static round schedules (structure classes, octo_device.hpp)
+// ---------------------------------------------------------------------------------------------
+
+__device__ __forceinline__ uint64_t wave_or(uint64_t x) {
+  for (int off = WAVE / 2; off > 0; off >>= 1) x |= __shfl_xor(x, off, WAVE);
+  return x;
+}
+
+// Node id of op (kind, s, m) among the 3 S M ops of a structure.
+__device__ __forceinline__ int sc_node(int S, int M, int kind, int s, int m) {
+  return (kind * S + s) * M + m;
+}
+
+// LDS bytes of k_static_build for (P, M): node rounds (int16) and slots (uint8) of the largest
+// structure (v = 2, split), then every device's op list (uint32 per op).
+__host__ __device__ inline size_t sc_build_lds(int P, int M) {
+  const size_t nn = (size_t)3 * 2 * P * M;
+  const size_t a = (nn * 2 + 15) / 16 * 16, b = (nn + 15) / 16 * 16;
+  return a + b + (size_t)P * 6 * M * 4;
+}
+
+// One workgroup (one wave, lane = canonical device) per structure class: run the lockstep rounds
+// of the class's structure once, costs aside — each round every device takes its next op if the
+// op's producer ran in an earlier round — recording the round of each op; give every finish
+// time that another device reads a slot for the rounds it is live (from its producer's round to
+// its reader's: every such value has exactly one reader), lowest free slot first, a slot freed
+// in a round being free for that round's writers (reads precede writes); then write every
+// device's row of round entries. smeta[class] = {valid, rounds, slots used}; a class is invalid
+// (its candidates take the generated-queue kernels) when its rounds pass nr_cap or it needs more
+// than SC_NEG slots. v = 2 classes need P v_max >= 2 P.
+__global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
+                                                       const uint32_t* __restrict__ mtab,
+                                                       uint32_t* __restrict__ stab,
+                                                       int32_t* __restrict__ smeta,
+                                                       int64_t cls_stride, int rowlen,
+                                                       int nr_cap) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int cls = blockIdx.x;
+  int v, gen, split, pat;
+  sc_decode(cls, &v, &gen, &split, &pat);
+  uint32_t* rows = stab + cls * cls_stride;
+  const int c = lane_id();
+  if (v > v_max) {
+    for (int i = c; i < (P + 1) * rowlen; i += WAVE) rows[i] = SC_NOP;
+    if (c == 0) smeta[4 * cls] = 0, smeta[4 * cls + 1] = 0, smeta[4 * cls + 2] = 0;
+    return;
+  }
+  const int S = P * v, q = (split ? 3 : 2) * v * M;
+  const int nn = 3 * 2 * P * M;
+  int16_t* rnd = reinterpret_cast<int16_t*>(smem);
+  uint8_t* slot = smem + ((size_t)nn * 2 + 15) / 16 * 16;
+  uint32_t* ops = reinterpret_cast<uint32_t*>(slot + ((size_t)nn + 15) / 16 * 16);
+  for (int i = c; i < nn; i += WAVE) rnd[i] = -1, slot[i] = SC_DUMMY;
+  __syncthreads();
+  const bool lane = c < P;
+  int st0 = 0, st1 = 0;
+  if (lane) sc_stages(pat, P, c, &st0, &st1);
+  GenInter gi;
+  GenMerge<2> gm;
+  if (gen == GEN_INTER) {
+    gi.init(P, v, M, lane ? st0 : 0, split, split ? (lane ? st0 : 0) : 0);
+  } else {
+    gm.init(mtab + merge_offset(P, M, 2, split), (split ? 3 : 2) * M, lane ? 2 : 0,
+            [&](int k) { return k == 0 ? st0 : st1; });
+  }
+  // pass 1: the lockstep rounds
+  int pos = 0, round = 0;
+  for (;;) {
+    const int kind = gen == GEN_INTER ? gi.kind : gm.kind;
+    const int k = gen == GEN_INTER ? gi.k : gm.k;
+    const int m = gen == GEN_INTER ? gi.m : gm.m;
+    const int s = k == 0 ? st0 : st1;
+    const bool has = lane && pos < q;
+    int prod = -1;
+    if (kind == KF) prod = s > 0 ? sc_node(S, M, KF, s - 1, m) : -1;
+    else if (kind == KB) prod = s < S - 1 ? sc_node(S, M, KB, s + 1, m) : sc_node(S, M, KF, s, m);
+    else prod = sc_node(S, M, KB, s, m);
+    const bool ready = has && (prod < 0 || rnd[prod] >= 0);
+    if (__ballot(ready) == 0 || round >= nr_cap) break;
+    __asm__ volatile("" ::: "memory");
+    if (ready) {
+      rnd[sc_node(S, M, kind, s, m)] = (int16_t)round;
+      ops[c * q + pos] = (uint32_t)round << 16 | (uint32_t)kind << 14 | (uint32_t)k << 11 |
+                         (uint32_t)m;
+      ++pos;
+    }
+    if (gen == GEN_INTER) gi.advance(ready);
+    else gm.advance(ready);
+    __asm__ volatile("" ::: "memory");
+    ++round;
+  }
+  const int nrounds = round;
+  bool valid = __ballot(lane && pos != q) == 0 && nrounds <= nr_cap;
+  // pass 2: slots of the cross-device finish times, in round order
+  uint64_t freem = (1ull << SC_NEG) - 1;  // slots 0 .. SC_NEG - 1
+  uint64_t used = 0;
+  int p2 = 0;
+  for (int r = 0; valid && r < nrounds; ++r) {
+    const uint32_t o = lane && p2 < q ? ops[c * q + p2] : 0xFFFFFFFFu;
+    const bool act = lane && p2 < q && (int)(o >> 16) == r;
+    const int kind = (o >> 14) & 3, k = (o >> 11) & 7, m = o & 0x7FF;
+    const int s = k == 0 ? st0 : st1;
+    // the op's input from another device: its one reader is this op, so the slot frees now
+    int pin = -1;
+    if (act && kind == KF && s > 0 && sc_device(pat, P, s - 1) != c) pin = sc_node(S, M, KF, s - 1, m);
+    if (act && kind == KB && s < S - 1 && sc_device(pat, P, s + 1) != c)
+      pin = sc_node(S, M, KB, s + 1, m);
+    freem |= wave_or(pin >= 0 ? 1ull << slot[pin] : 0);
+    // its output to another device needs a slot
+    const bool out = act && ((kind == KF && s < S - 1 && sc_device(pat, P, s + 1) != c) ||
+                             (kind == KB && s > 0 && sc_device(pat, P, s - 1) != c));
+    const uint64_t wm = __ballot(out);
+    if (__popcll(wm) > __popcll(freem)) {
+      valid = false;
+      break;
+    }
+    int sl = SC_DUMMY;
+    if (out) {
+      uint64_t x = freem;
+      const int rank = __popcll(wm & ((1ull << c) - 1));
+      for (int i = 0; i < rank; ++i) x &= x - 1;
+      sl = __ffsll((unsigned long long)x) - 1;
+      slot[sc_node(S, M, kind, s, m)] = (uint8_t)sl;
+    }
+    const uint64_t took = wave_or(out ? 1ull << sl : 0);
+    freem &= ~took;
+    used |= took;
+    p2 += act ? 1 : 0;
+  }
+  __syncthreads();
+  // pass 3: the rows (role c; row P is all SC_NOP)
+  for (int i = c; i < rowlen; i += WAVE) rows[(int64_t)P * rowlen + i] = SC_NOP;
+  if (lane) {
+    uint32_t* row = rows + (int64_t)c * rowlen;
+    int p3 = 0;
+    for (int r = 0; r < rowlen; ++r) {
+      uint32_t e = SC_NOP;
+      const uint32_t o = valid && p3 < q ? ops[c * q + p3] : 0xFFFFFFFFu;
+      if (valid && p3 < q && (int)(o >> 16) == r) {
+        const int kind = (o >> 14) & 3, k = (o >> 11) & 7, m = o & 0x7FF;
+        const int s = k == 0 ? st0 : st1;
+        int rd = SC_NEG;
+        if (kind == KF && s > 0 && sc_device(pat, P, s - 1) != c)
+          rd = slot[sc_node(S, M, KF, s - 1, m)];
+        if (kind == KB && s < S - 1 && sc_device(pat, P, s + 1) != c)
+          rd = slot[sc_node(S, M, KB, s + 1, m)];
+        const int wr = kind == KW ? SC_DUMMY : slot[sc_node(S, M, kind, s, m)];
+        e = sc_entry(rd, kind * v + k, wr);
+        ++p3;
+      }
+      row[r] = e;
+    }
+  }
+  if (c == 0) {
+    smeta[4 * cls] = valid ? 1 : 0;
+    smeta[4 * cls + 1] = valid ? nrounds : 0;
+    smeta[4 * cls + 2] = __popcll(used);
+    smeta[4 * cls + 3] = 0;
+  }
+}
+
+// Static-schedule evaluation: persistent waves take chunks of CPW candidates of one class bin;
+// each lane runs its role's row of the class's schedule with its candidate's costs. Per round:
+// read the slot its op reads and its stream's {input weight, duration}, start = max(device
+// clock, slot + weight), finish = start + duration, write the finish to the slot its op writes.
+// LDS: each group's 64 slots (64-bit, 512 B per group), then one 512-byte row per stream
+// ({weight, duration} as two uint32 per lane; stream SC_NOP_STREAM is zero), then the staged
+// records. The groups of a wave run one class, so in a round they read and write the same slot
+// numbers: slot k of group g lives at k ^ 4g, which spreads the groups' accesses over the LDS
+// banks (without it every group hits the same banks). A candidate whose weights or durations
+// pass 32 bits goes to the 64-bit redo list.
+typedef __attribute__((address_space(3))) int64_t lds_i64;
+typedef __attribute__((address_space(3))) uint64_t lds_u64;
+__global__ void __launch_bounds__(WAVE) k_static(SimArgs a, int sbase, int rbase) {
+  extern __shared__ __align__(512) uint8_t st_smem[];
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  const int gg = g < a.CPW ? g : 0;
+  const uint32_t lb = (uint32_t)(uintptr_t)st_smem;  // LDS address of the array (512-aligned)
+  // group base | salt: slot addresses are (slot * 8) ^ sg
+  const uint32_t sg = (lb + (uint32_t)gg * 512u) | (((uint32_t)gg * 32u) & 0x1F8u);
+  const uint32_t sb = lb + (uint32_t)sbase + (uint32_t)lane_id() * 8u;
+  uint8_t* rec = st_smem + rbase + gg * a.rec_stride;
+  // the class bins' counts, first positions and chunk ranges, one class per lane
+  const int ci = lane_id();
+  const int cnt_i = ci < NSC ? a.ctl[CTL_COUNTS + BIN_STATIC + ci] : 0;
+  const int start_i = ci < NSC ? a.ctl[CTL_START + BIN_STATIC + ci] : 0;
+  const int nch_i = (cnt_i + a.CPW - 1) / a.CPW;
+  int end_i = nch_i;  // inclusive prefix: chunks of classes 0..ci
+  for (int off = 1; off < 16; off <<= 1) {
+    const int y = __shfl_up(end_i, off, WAVE);
+    end_i += ci >= off ? y : 0;
+  }
+  // chunks by grid stride, not by an atomic work counter: thousands of waves taking chunks of
+  // a few hundred rounds would serialise on one counter's atomics. Chunks are in class order,
+  // so each sweep of the grid hands every wave chunks of about one cost.
+  for (int ch = (int)blockIdx.x;; ch += (int)gridDim.x) {
+    // the class whose chunk range holds ch: the number of classes that end at or before it
+    const int cls = __popcll(__ballot(ci < NSC && end_i <= ch));
+    if (cls >= NSC) break;
+    const int cnt = __shfl(cnt_i, cls, WAVE);
+    const int pos0 = __shfl(start_i, cls, WAVE);
+    const int entry0 = (ch - (__shfl(end_i, cls, WAVE) - __shfl(nch_i, cls, WAVE))) * a.CPW;
+    int v, gen, split, pat;
+    sc_decode(cls, &v, &gen, &split, &pat);
+    const int e = entry0 + g;
+    const int64_t cand = (g < a.CPW && e < cnt) ? (int64_t)a.idx[pos0 + e] : -1;
+    const bool mine = cand >= 0 && d < P;
+    if (cand >= 0) stage_record(rec, a.cands + cand * a.pr.stride, a.rec_bytes, d, G);
+    __asm__ volatile("" ::: "memory");
+    Chunks<2> c;
+    int64_t busy = 0;
+    bool fits = true;
+    int role = P;
+    if (mine) {
+      busy = setup_chunks<2>(c, a.pr, rec, a.pre, a.link, d, v, split, make_ring(M, M));
+      role = sc_role(pat, c.st[0]);
+    } else {
+      zero_chunks<2>(c);
+    }
+#pragma unroll
+    for (int kind = 0; kind < 3; ++kind)
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int64_t w = kind == KF ? c.wF[k] : kind == KB ? c.wB[k] : 0;
+        const int64_t du = kind == KF ? c.dF[k] : kind == KB ? c.dB[k] : c.dW[k];
+        fits = fits && (uint64_t)w <= 0xFFFFFFFFull && (uint64_t)du <= 0xFFFFFFFFull;
+        if (k < v)
+          *reinterpret_cast<lds_u64*>((uintptr_t)(sb + (uint32_t)(kind * v + k) * 512u)) =
+              ((uint64_t)du << 32) | (uint32_t)w;
+      }
+    *reinterpret_cast<lds_u64*>((uintptr_t)(sb + SC_NOP_STREAM * 512u)) = 0;
+    if (d == 0)
+      *reinterpret_cast<lds_i64*>((uintptr_t)(((uint32_t)SC_NEG * 8u) ^ sg)) =
+          -((int64_t)1 << 62);
+    uint64_t gbit, lsb;
+    group_bits(G, &gbit, &lsb);
+    const bool wide = (fold_groups(__ballot(!fits), G, lsb) & gbit) != 0;
+    if (wide) role = P;
+    const int nrounds = a.smeta[4 * cls + 1];
+    const uint4* rowp = reinterpret_cast<const uint4*>(a.stab + cls * a.st_cls +
+                                                       (int64_t)role * a.st_rowlen);
+    __asm__ volatile("" ::: "memory");
+    int64_t clock = 0;
+    auto step = [&](uint32_t en) {
+      const uint32_t ra = (en & 0x1F8u) ^ sg;
+      const uint32_t sa = (en & 0xE00u) | sb;
+      const uint32_t wa = ((en >> 9) & 0x1F8u) ^ sg;
+      const int64_t x = *reinterpret_cast<const lds_i64*>((uintptr_t)ra);
+      const uint64_t sr = *reinterpret_cast<const lds_u64*>((uintptr_t)sa);
+      const int64_t tin = x + (int64_t)(uint32_t)sr;
+      const int64_t st = tin > clock ? tin : clock;
+      clock = st + (int64_t)(sr >> 32);
+      *reinterpret_cast<lds_i64*>((uintptr_t)wa) = clock;
+    };
+    // blocks of four rounds, their entries loaded four blocks ahead (a row is L2-resident, so a
+    // load takes far longer than one block of rounds); a row ends with four blocks of SC_NOP,
+    // so every look-ahead stays in it, and the rounds run in whole groups of four blocks (the
+    // rounds past the class's last are SC_NOP)
+    uint4 q0 = rowp[0], q1 = rowp[1], q2 = rowp[2], q3 = rowp[3];
+    auto block = [&](const uint4& q) {
+      step(q.x);
+      step(q.y);
+      step(q.z);
+      step(q.w);
+    };
+    for (int b = 0; b < nrounds; b += 16) {
+      const int i = b >> 2;
+      block(q0);
+      q0 = rowp[i + 4];
+      block(q1);
+      q1 = rowp[i + 5];
+      block(q2);
+      q2 = rowp[i + 6];
+      block(q3);
+      q3 = rowp[i + 7];
+    }
+    const int64_t ms = group_max(clock, G);
+    if (mine) {
+      if (wide) {
+        if (d == 0) a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      } else {
+        CommTally none;
+        none.reset();
+        put_results<XP>(a, cand, d, false, ms, busy, 0, 0, none);
+      }
+    }
+    __asm__ volatile("" ::: "memory");
   }
 }
 
@@ -2860,6 +3181,12 @@ struct Workspace {
   // reordered coordination: per-slot finish times, receive lists and programs
   void* ord = nullptr;
   size_t ord_bytes = 0;
+  // static round schedules of the structure classes and their metadata, same cache key as mt;
+  // st_ok: the tables exist (false: k_static_build does not fit this problem)
+  void* st = nullptr;
+  size_t st_bytes = 0;
+  bool st_valid = false, st_ok = false;
+  int st_P = 0, st_vmax = 0, st_M = 0;
 };
 
 std::mutex g_mu;
@@ -3142,6 +3469,52 @@ TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool wide) {
   return t;
 }
 
+// Geometry of the static round schedules for a problem: rounds a class may take (a lockstep
+// pass takes about a device's op count plus the pipeline depth; twice the largest op count plus
+// four times the stages is a safe cap, a class past it is marked invalid), entries per row (the
+// cap rounded up to whole groups of sixteen rounds, plus sixteen SC_NOP entries for the
+// look-ahead of k_static), and the entries per class (P + 1 rows).
+struct StGeom {
+  int nr_cap, rowlen;
+  int64_t cls;
+  size_t bytes;  // tables, then NSC x 4 int32 of metadata
+};
+StGeom st_geom(const octo_problem* p) {
+  StGeom g;
+  g.nr_cap = 2 * 6 * p->M + 4 * 2 * p->P;
+  g.rowlen = (g.nr_cap + 15) / 16 * 16 + 16;
+  g.cls = (int64_t)(p->P + 1) * g.rowlen;
+  g.bytes = align_up((size_t)NSC * g.cls * 4, 256) + NSC * 16;
+  return g;
+}
+
+// Build the static round schedules (k_static_build) into the workspace when the problem shape
+// changed or the MERGE tables were rebuilt; needs the MERGE tables (v_max >= 2) in place.
+int build_static(const octo_problem* p, Workspace& ws, int lds_max, hipStream_t stream) {
+  if (ws.st_valid && ws.st_P == p->P && ws.st_vmax == p->v_max && ws.st_M == p->M) return OCTO_OK;
+  ws.st_valid = false;
+  ws.st_ok = false;
+  const size_t lds = sc_build_lds(p->P, p->M);
+  if (p->M > 2047 || (int)lds > lds_max || p->P > WAVE) {
+    ws.st_valid = true;  // no static schedules for this shape
+    ws.st_P = p->P, ws.st_vmax = p->v_max, ws.st_M = p->M;
+    return OCTO_OK;
+  }
+  const StGeom g = st_geom(p);
+  const int rc = ensure_buf(ws.st, ws.st_bytes, g.bytes, stream);
+  if (rc) return rc;
+  uint32_t* tab = static_cast<uint32_t*>(ws.st);
+  int32_t* meta = reinterpret_cast<int32_t*>(static_cast<char*>(ws.st) + g.bytes - NSC * 16);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k_static_build),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL(k_static_build, dim3(NSC), dim3(WAVE), lds, stream, p->P, p->M, p->v_max,
+                     static_cast<const uint32_t*>(ws.mt), tab, meta, g.cls, g.rowlen, g.nr_cap);
+  if (hipGetLastError() != hipSuccess) return OCTO_EHIP;
+  ws.st_valid = ws.st_ok = true;
+  ws.st_P = p->P, ws.st_vmax = p->v_max, ws.st_M = p->M;
+  return OCTO_OK;
+}
+
 // Queue tables for v = 1 and 2 (INTER rows per rank, MERGE rows per stage pair), encoded for
 // each v's launch geometry; rebuilt when (P, v_max, M), the geometry or the MERGE tables
 // change. Entry offsets are kept in the workspace.
@@ -3225,7 +3598,8 @@ int scratch_regions(const octo_problem* prob, int dev, int64_t n, Setup* su) {
   const size_t mr = prob->v_max >= 2 ? align_up(merge_rows_bytes(prob), 256) : 0;
   int64_t qi[2][2], qm[2], qe;
   const size_t qt = align_up((size_t)qtab_offsets(prob, qi, qm, &qe) * 4, 256);
-  const size_t tables = mt + mr + qt;
+  const size_t stb = align_up(st_geom(prob).bytes, 256);
+  const size_t tables = mt + mr + qt + stb;
   // the per-call part without materialised-queue rows, then the rows that fit after it
   const size_t lists = layout(prob, su->big, n, 0).total;
   if (tables + lists > cap) return OCTO_ESCRATCH;
@@ -3243,13 +3617,15 @@ int scratch_regions(const octo_problem* prob, int dev, int64_t n, Setup* su) {
   char* mt_p = mt ? base : nullptr;
   char* mr_p = mr ? base + mt : nullptr;
   char* qt_p = base + mt + mr;
+  char* st_p = base + mt + mr + qt;
   // tables moved (another problem shape): rebuild them
   if (ws.mt != mt_p || ws.mt_bytes != mt || ws.mr != mr_p || ws.mr_bytes != mr ||
-      ws.qt != qt_p || ws.qt_bytes != qt)
-    ws.mt_valid = ws.qt_valid = false;
+      ws.qt != qt_p || ws.qt_bytes != qt || ws.st != st_p || ws.st_bytes != stb)
+    ws.mt_valid = ws.qt_valid = ws.st_valid = false;
   ws.mt = mt_p, ws.mt_bytes = mt;
   ws.mr = mr_p, ws.mr_bytes = mr;
   ws.qt = qt_p, ws.qt_bytes = qt;
+  ws.st = st_p, ws.st_bytes = stb;
   ws.base = base + tables;
   ws.bytes = cap - tables;
   return OCTO_OK;
@@ -3334,6 +3710,7 @@ int prepare(const octo_problem* prob, const int64_t* costs, const int64_t* mem,
     ws.mt_valid = true;
     ws.mt_P = prob->P, ws.mt_vmax = prob->v_max, ws.mt_M = prob->M;
     ws.qt_valid = false;
+    ws.st_valid = false;
   }
   return OCTO_OK;
 }
@@ -3385,6 +3762,10 @@ SimArgs make_args(const octo_problem* prob, const Plan& pl, const Setup& su, con
     for (int j = 0; j < 2; ++j) a.qt_inter[i][j] = su.ws->qt_inter[i][j];
   }
   a.strm_off = pl.strm_off;
+  a.stab = nullptr;
+  a.smeta = nullptr;
+  a.st_cls = 0;
+  a.st_rowlen = 0;
   return a;
 }
 
@@ -3395,6 +3776,25 @@ uint64_t bins_of(int v_lo, int v_hi, bool afab) {
     for (int b = first_bin(v); b < first_bin(v) + 5; ++b)
       if ((b == bin_of(v, GEN_AFAB, 0)) == afab) m |= 1ull << b;
   return m;
+}
+
+// Launch k_static over the class bins: CPW = 64 / G candidates per wave, each group's 64 slots
+// (512 B), the stream rows from the next multiple of 4 KiB (4 KiB), then the staged records.
+int launch_static(const SimArgs& base, const Setup& su, int64_t n, hipStream_t stream) {
+  SimArgs a = base;
+  a.G = lanes_per_candidate(a.pr.P);
+  a.CPW = WAVE / a.G;
+  const int sbase = (int)align_up((size_t)a.CPW * 512, 4096);
+  const int rbase = sbase + 8 * 512;
+  const int lds = rbase + a.CPW * a.rec_stride;
+  if (lds > su.di.lds_max) return OCTO_OK;  // cannot happen for P <= 64; leave to k_sim
+  int grid = 0;
+  int rc = occupancy_grid(k_static, lds, su.di.cus, &grid);
+  if (rc) return rc;
+  const int64_t need = (n + a.CPW - 1) / a.CPW;
+  grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+  hipLaunchKernelGGL(k_static, dim3(grid), dim3(WAVE), lds, stream, a, sbase, rbase);
+  return launch_ok();
 }
 
 // Launch k_sim<VC> over the generated bins in `mask` with its own 40-bit plan: s_cap stages of
@@ -3588,6 +3988,18 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
   a.out_comm = cm;
   a.out_bound = bd;
   a.n_live = ex.n_live;
+  // plain evaluations take the static round schedules for the structure classes
+  if (X == XP) {
+    if ((rc = build_static(prob, *su.ws, su.di.lds_max, stream))) return rc;
+    if (su.ws->st_ok) {
+      const StGeom sg = st_geom(prob);
+      a.stab = static_cast<const uint32_t*>(su.ws->st);
+      a.smeta = reinterpret_cast<const int32_t*>(static_cast<const char*>(su.ws->st) +
+                                                 sg.bytes - NSC * 16);
+      a.st_cls = sg.cls;
+      a.st_rowlen = sg.rowlen;
+    }
+  }
   if ((rc = classify_sort(prob, su, a, n, stream))) return rc;
   // generated INTER / MERGE queues, one launch per v class with finish tables sized for it:
   // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
@@ -3597,20 +4009,22 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
     return rc;
   const int P = prob->P, M = prob->M;
   if ((rc = record_mark(0, stream))) return rc;
+  if (a.smeta && (rc = launch_static(a, su, n, stream))) return rc;
+  if ((rc = record_mark(1, stream))) return rc;
   if (prob->v_max >= 2 &&
       (rc = launch_sim<2, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
                              2 * P, 2 * P, bins_of(2, 2, false), CTL_WORK + 1, stream)))
     return rc;
-  if ((rc = record_mark(1, stream))) return rc;
+  if ((rc = record_mark(2, stream))) return rc;
   if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
                              P, P, bins_of(1, 1, false), CTL_WORK + 0, stream)))
     return rc;
-  if ((rc = record_mark(2, stream))) return rc;
+  if ((rc = record_mark(3, stream))) return rc;
   if (prob->v_max >= 3 &&
       (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
                              P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
     return rc;
-  if ((rc = record_mark(3, stream))) return rc;
+  if ((rc = record_mark(4, stream))) return rc;
   if constexpr (X != XR) {
     if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
                              stream)))
@@ -3631,7 +4045,7 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
                                true)))
       return rc;
   }
-  if ((rc = record_mark(4, stream))) return rc;
+  if ((rc = record_mark(5, stream))) return rc;
   // candidates with moves: 40-bit rings, 40-bit full rows for those wider than the ring, then
   // the 64-bit redo list
   bool m40_any = false;
@@ -3670,7 +4084,7 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
     hipLaunchKernelGGL((k_sim_mat<8, X>), dim3(su.mat_grid), dim3(WAVE), su.big.lds_bytes,
                        stream, a);
   if ((rc = launch_ok())) return rc;
-  return record_mark(5, stream);
+  return record_mark(6, stream);
 }
 
 // Argument checks and locking around sim_batch_run.

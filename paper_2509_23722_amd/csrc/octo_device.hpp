@@ -22,9 +22,12 @@ constexpr int GEN_AFAB = 0, GEN_INTER = 1, GEN_MERGE = 2, GEN_MAT = 3;
 // code path; bins are numbered heaviest first (large v first; within one v: AFAB, then split
 // backward, then fused).
 constexpr int NBIN_GEN = 40;          // (8 - v) * 5 + rank, v = 1..8
+// candidates of a structure class with a static round schedule: bins BIN_STATIC + class
+constexpr int NSC = 9;
+constexpr int BIN_STATIC = 40;
 // candidates with perturbations (queues materialised): bins BIN_MAT + mat_sub(v, split), the
 // last ones, by queue length like the generated bins (large v first, split first)
-constexpr int BIN_MAT = 40;
+constexpr int BIN_MAT = BIN_STATIC + NSC;
 constexpr int NBINS = BIN_MAT + 16;
 __host__ __device__ __forceinline__ int mat_sub(int v, int split) { return (8 - v) * 2 + (split ? 0 : 1); }
 constexpr int BIN_NONE = 0xFF;        // invalid: sentinel already written
@@ -133,6 +136,70 @@ __device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint
   r.valid = 1;
   return r;
 }
+
+// ------------------------------------------------------------------------------------------
+// Structure classes with static round schedules. In the lockstep rounds an op is ready when its
+// producers finished in earlier rounds, which depends on the structure — which stages share a
+// device, the generator, a split backward — and never on the costs. These classes recur among
+// candidates, so each has one precomputed schedule: v = 1 (any placement: relabelling devices
+// does not change the structure), and v = 2 with the looped {c, c+P}, blocked {2c, 2c+1} or
+// V-shape {c, 2P-1-c} stage pairs. A device's row is picked by its role, the canonical device
+// that hosts the same stages.
+//   class: 0 v1 INTER fused, 1 v1 INTER split, 2 looped INTER fused, 3 looped INTER split,
+//          4 looped MERGE fused, 5 blocked MERGE fused, 6 blocked MERGE split,
+//          7 V-shape MERGE fused, 8 V-shape MERGE split
+// pattern: 0 one stage per device, 1 looped, 2 blocked, 3 V-shape.
+// ------------------------------------------------------------------------------------------
+__host__ __device__ __forceinline__ void sc_decode(int c, int* v, int* gen, int* split, int* pat) {
+  *v = c < 2 ? 1 : 2;
+  *gen = (c < 4) ? GEN_INTER : GEN_MERGE;
+  *split = (c == 1 || c == 3 || c == 6 || c == 8) ? 1 : 0;
+  *pat = c < 2 ? 0 : c < 5 ? 1 : c < 7 ? 2 : 3;
+}
+
+// Class of a valid record (resolved as r), or -1: its queues are generated per candidate.
+__device__ __forceinline__ int static_class(const Problem& pr, const uint8_t* dev,
+                                            const Resolved& r) {
+  if (r.n_pert > 0 || r.gen == GEN_AFAB || r.v > 2) return -1;
+  if (r.v == 1) return r.split ? 1 : 0;
+  const int P = pr.P;
+  bool lp = true, bl = true, vs = true;
+  for (int i = 0; i < P; ++i) {
+    lp = lp && dev[i] == dev[i + P];
+    bl = bl && dev[2 * i] == dev[2 * i + 1];
+    vs = vs && dev[i] == dev[2 * P - 1 - i];
+  }
+  if (lp) return r.gen == GEN_INTER ? (r.split ? 3 : 2) : (r.split ? -1 : 4);
+  if (r.gen != GEN_MERGE) return -1;
+  if (bl) return r.split ? 6 : 5;
+  if (vs) return r.split ? 8 : 7;
+  return -1;
+}
+
+// Canonical device of stage s under a pattern, and the role of a device whose lowest stage
+// is s0.
+__host__ __device__ __forceinline__ int sc_device(int pat, int P, int s) {
+  return pat == 0 ? s : pat == 1 ? s % P : pat == 2 ? s / 2 : (s < P ? s : 2 * P - 1 - s);
+}
+__host__ __device__ __forceinline__ int sc_role(int pat, int s0) { return pat == 2 ? s0 / 2 : s0; }
+// Stages of canonical device c (the second is unused at v = 1).
+__host__ __device__ __forceinline__ void sc_stages(int pat, int P, int c, int* s0, int* s1) {
+  *s0 = pat == 2 ? 2 * c : c;
+  *s1 = pat == 1 ? c + P : pat == 2 ? 2 * c + 1 : pat == 3 ? 2 * P - 1 - c : c;
+}
+
+// Schedule entry of one device in one round: the slot its op reads (a cross-device producer's
+// finish time, else SC_NEG, which holds a time far below zero), the stream of its duration and
+// input weight (kind * v + chunk; SC_NOP_STREAM: zero duration), and the slot it writes (its
+// finish time if another device reads it, else SC_DUMMY). Bits: read slot << 3, stream << 9,
+// write slot << 12, so that address = (entry & mask) | base needs one instruction. A round in
+// which the device runs nothing is SC_NOP.
+constexpr int SC_SLOTS = 64, SC_NEG = 62, SC_DUMMY = 63, SC_NOP_STREAM = 7;
+__host__ __device__ __forceinline__ uint32_t sc_entry(int rd, int stream, int wr) {
+  return (uint32_t)rd << 3 | (uint32_t)stream << 9 | (uint32_t)wr << 12;
+}
+constexpr uint32_t SC_NOP = ((uint32_t)SC_NEG << 3) | ((uint32_t)SC_NOP_STREAM << 9) |
+                            ((uint32_t)SC_DUMMY << 12);
 
 // ------------------------------------------------------------------------------------------
 // Queue generators. Each lane owns one device queue and walks it front to back. A generator
