@@ -1,9 +1,9 @@
 """Condense rocprofv3 CSV output of ``bench.py`` runs into the short text summaries kept under
 ``profiles/``, and the per-launch HBM traffic record ``bench.py`` reports.
 
-    python -m paper_2509_23722_amd.rocprof_summary --trace DIR --fetch DIR --write DIR \\
-        --copy-fetch DIR --copy-write DIR [--sq DIR ...] --kernel NAME --workload NAME \\
-        --commands FILE --out-dir profiles
+    python -m paper_2509_23722_amd.rocprof_summary --trace DIR [--fetch DIR --write DIR \\
+        --copy-fetch DIR --copy-write DIR --kernel NAME] [--sq DIR ...] --workload NAME \\
+        [--tag TAG] [--what TEXT] --commands FILE --out-dir profiles
 
 Each DIR is a rocprofv3 ``-d`` output directory holding ``*_kernel_stats.csv`` (kernel trace) or
 ``*_counter_collection.csv`` (``--pmc``). HBM bytes: FETCH_SIZE and WRITE_SIZE (KiB per
@@ -67,21 +67,26 @@ def copy_factor(d, counter):
 
 def main():
     ap = argparse.ArgumentParser()
-    for k in ("trace", "fetch", "write", "copy-fetch", "copy-write"):
-        ap.add_argument("--" + k, required=True)
+    ap.add_argument("--trace", required=True)
+    for k in ("fetch", "write", "copy-fetch", "copy-write"):
+        ap.add_argument("--" + k)
     ap.add_argument("--sq", action="append", default=[])
-    ap.add_argument("--kernel", required=True, help="short name of the dominant kernel")
+    ap.add_argument("--kernel", help="short name of the dominant kernel")
     ap.add_argument("--workload", required=True)
+    ap.add_argument("--tag", help="file name tag (default: the workload)")
+    ap.add_argument("--what", default="one `bench.py --headline-only` run: every simulation "
+                    "kernel dispatch is a headline-call one (the first call of a run also builds "
+                    "the cached MERGE and static-schedule tables)")
     ap.add_argument("--commands", required=True, help="text file with the commands that ran")
     ap.add_argument("--out-dir", default="profiles")
     args = ap.parse_args()
     cmds = open(args.commands).read().strip()
-    tag = f"{args.workload}"
+    tag = args.tag or args.workload
 
     stats = kernel_stats(args.trace)
     lines = [f"# Kernel trace: simulation kernels, {args.workload}", "",
-             "rocprofv3 kernel-trace statistics of one `bench.py` run (the first call of a run",
-             "also builds the cached MERGE tables).", "", "Commands:", "", "```", cmds, "```", "",
+             f"rocprofv3 kernel-trace statistics of {args.what}.", "", "Commands:", "", "```",
+             cmds, "```", "",
              "| kernel | calls | average us | min us | max us | % of GPU time |",
              "|---|---:|---:|---:|---:|---:|"]
     for name, calls, avg, mn, mx, pct in stats:
@@ -90,6 +95,27 @@ def main():
     with open(os.path.join(args.out_dir, f"kernel_trace_{tag}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
+    if args.sq:
+        lines = [f"# SQ counters per dispatch, {args.workload}", "", "Commands:", "", "```",
+                 cmds, "```", ""]
+        for d in args.sq:
+            c = counters(d)
+            names = sorted({n for cs in c.values() for n in cs})
+            lines += ["| kernel | " + " | ".join(names) + " |",
+                      "|---|" + "---:|" * len(names)]
+            for k, cs in c.items():
+                if "copyBuffer" in k:
+                    continue
+                lines.append(f"| {k} | " + " | ".join(
+                    f"{cs[n][0]:.4g}" if n in cs else "" for n in names) + " |")
+            lines.append("")
+        with open(os.path.join(args.out_dir, f"sq_counters_{tag}.md"), "w") as f:
+            f.write("\n".join(lines) + "\n")
+    if args.fetch and args.write and args.copy_fetch and args.copy_write and args.kernel:
+        traffic_summary(args, cmds, tag)
+
+
+def traffic_summary(args, cmds, tag):
     ff, fkib_copy = copy_factor(args.copy_fetch, "FETCH_SIZE")
     wf, wkib_copy = copy_factor(args.copy_write, "WRITE_SIZE")
     fetch, write = counters(args.fetch), counters(args.write)
@@ -121,24 +147,6 @@ def main():
     with open(os.path.join(args.out_dir, f"traffic_{tag}.json"), "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
-
-    if args.sq:
-        lines = [f"# SQ counters per dispatch, {args.workload}", "", "Commands:", "", "```",
-                 cmds, "```", ""]
-        for d in args.sq:
-            c = counters(d)
-            names = sorted({n for cs in c.values() for n in cs})
-            lines += ["| kernel | " + " | ".join(names) + " |",
-                      "|---|" + "---:|" * len(names)]
-            for k, cs in c.items():
-                if "copyBuffer" in k:
-                    continue
-                lines.append(f"| {k} | " + " | ".join(
-                    f"{cs[n][0]:.4g}" if n in cs else "" for n in names) + " |")
-            lines.append("")
-        with open(os.path.join(args.out_dir, f"sq_counters_{tag}.md"), "w") as f:
-            f.write("\n".join(lines) + "\n")
-
 
 if __name__ == "__main__":
     main()
