@@ -555,6 +555,309 @@ static int simulate_programs(const ref_dag_in* g, const ref_sop* queue, const in
   return rc;
 }
 
+/*
+ * The executor's deadlock-free, overlap-aware reordering (§7, "Unified Pipeline Executor": its
+ * three steps), evaluated with handshake transfers.
+ *
+ * Transfers: a device that reaches a send or a receive in its program waits there until the
+ * other end has been reached too (a blocking point-to-point handshake); then both go on at
+ * once, and the data arrives c = link[p][q] after the handshake, while both devices compute
+ * (the transfer runs beside computation). The consumer may start once the data has arrived.
+ *
+ * Every transfer t (producer X on device p -> consumer Y on device q) has a key: the end of X in
+ * the asynchronous schedule (§1.3), then X's level (the number of ops on the longest dependency
+ * chain before X, queue order included), then X's node id. The key order is a total order in
+ * which every dependency strictly increases (positive durations not needed: the level breaks
+ * ties). The program starts as the naive coordination of §3.3: the receive of t in the gap
+ * before Y, the send after X; a gap g of a device is the point before its computation g (gap
+ * n: after the last of its n computations).
+ *  1. Mismatched pairs: walk each device's communication items in program order; an item whose
+ *     key is below the largest key before it is out of the order the other devices follow for
+ *     their ends of the same transfers (a pair that can close a cycle of waits). Only receives
+ *     can be out of order: whatever precedes a send ends before its producer does.
+ *  2. Feasible window of a mismatched receive: its dependent computations are X (on p) and Y
+ *     (on q). The receive must stay before Y and, to restore the order, after every in-order
+ *     item of a smaller key and before the first one of a larger key; within that range, only
+ *     gaps whose post time (the end of q's previous computation in the asynchronous schedule,
+ *     0 for gap 0) is not before X starts (earlier, q would only wait): the window
+ *     [max(lo, gX), hi] (just hi if that is empty).
+ *  3. Cost of a gap: the communication span, |X's end - the gap's post time| (the time one end
+ *     waits for the other), minus the overlap with neighbouring computation, min(c, the
+ *     durations of q's computations from that gap up to Y) (what q computes while the data is
+ *     in flight). Mismatched receives are placed greedily in key order, each at its cheapest
+ *     gap (ties: the latest), and the next one's range starts at that gap.
+ * Within a gap, communication items run in key order. Every device then meets its transfers in
+ * key order, so no cycle of waits can form.
+ */
+typedef struct {
+  int64_t t, lvl;
+  int node, gap, code;
+} comm_item;
+
+static int cmp_comm_item(const void* a, const void* b) {
+  const comm_item *x = (const comm_item*)a, *y = (const comm_item*)b;
+  if (x->t != y->t) return x->t < y->t ? -1 : 1;
+  if (x->lvl != y->lvl) return x->lvl < y->lvl ? -1 : 1;
+  return x->node < y->node ? -1 : x->node > y->node;
+}
+
+/* Returns 0, or -1 if the programs' communication is not in key order (cannot happen). stats
+ * (nullable): [0] += transfers (receives), [1] += mismatched receives. */
+static int reorder_programs(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                            const int* qlen, const int64_t* start, const int64_t* lvl, int* prog,
+                            int* plen, int64_t* stats) {
+  const int S = g->S, M = g->M;
+  int rc = 0;
+  for (int d = 0; d < g->P && rc == 0; ++d) {
+    const int n = qlen[d];
+    const ref_sop* q = queue + qoff[d];
+    comm_item* it = (comm_item*)malloc(sizeof(comm_item) * (size_t)(2 * n + 1));
+    int* flagged = (int*)malloc(sizeof(int) * (size_t)(2 * n + 1));
+    int64_t* post = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n + 1)); /* post time of gap */
+    post[0] = 0;
+    for (int i = 0; i < n; ++i)
+      post[i + 1] = start[node_id(S, M, q[i].kind, q[i].s, q[i].m)] + op_dur(g, q[i].kind, q[i].s);
+    int ni = 0;
+    for (int i = 0; i < n; ++i) {
+      const int y = node_id(S, M, q[i].kind, q[i].s, q[i].m);
+      const int x = cross_producer(g, q[i].kind, q[i].s, q[i].m);
+      if (x >= 0) {
+        const int xk = x / (S * M), xs = (x / M) % S;
+        it[ni++] = (comm_item){start[x] + op_dur(g, xk, xs), lvl[x], x, i, (PI_RECV << 28) | x};
+      }
+      if (cross_consumer(g, q[i].kind, q[i].s, q[i].m) >= 0)
+        it[ni++] = (comm_item){post[i + 1], lvl[y], y, i + 1, (PI_SEND << 28) | y};
+    }
+    /* step 1 */
+    int nf = 0, top = -1, nrecv = 0;
+    int* rec_ok = (int*)calloc((size_t)(ni + 1), sizeof(int)); /* 1: in order (a record) */
+    for (int j = 0; j < ni; ++j) {
+      nrecv += (it[j].code >> 28) == PI_RECV;
+      if (top < 0 || cmp_comm_item(&it[j], &it[top]) > 0) {
+        top = j;
+        rec_ok[j] = 1;
+      } else {
+        flagged[nf++] = j;
+      }
+    }
+    if (stats) stats[0] += nrecv, stats[1] += nf;
+    /* steps 2 and 3, in key order */
+    for (int a = 1; a < nf; ++a) { /* insertion sort of the flagged items by key */
+      const int v = flagged[a];
+      int b = a;
+      while (b > 0 && cmp_comm_item(&it[v], &it[flagged[b - 1]]) < 0) {
+        flagged[b] = flagged[b - 1];
+        --b;
+      }
+      flagged[b] = v;
+    }
+    int lastg = 0;
+    for (int a = 0; a < nf; ++a) {
+      comm_item* f = &it[flagged[a]];
+      int lo = lastg, hi = -1;
+      for (int j = 0; j < ni; ++j) {
+        if (!rec_ok[j]) continue;
+        if (cmp_comm_item(&it[j], f) < 0) {
+          if (it[j].gap > lo) lo = it[j].gap;
+        } else {
+          hi = it[j].gap;
+          break;
+        }
+      }
+      if ((f->code >> 28) != PI_RECV || hi < 0) { /* cannot happen (see above) */
+        rc = -1;
+        break;
+      }
+      const int X = f->node, iY = f->gap;
+      const int xk = X / (S * M), xs = (X / M) % S;
+      const int64_t c = g->link[g->dev[xs] * g->P + d];
+      const int64_t xend = start[X] + op_dur(g, xk, xs);
+      int gx = 0;
+      while (gx <= n && post[gx] < start[X]) ++gx;
+      int first = lo > gx ? lo : gx;
+      if (first > hi) first = hi;
+      int64_t D = 0; /* durations of the computations in gaps [gap, iY) */
+      for (int i = hi; i < iY; ++i) D += op_dur(g, q[i].kind, q[i].s);
+      int best = -1;
+      int64_t bestc = 0;
+      for (int gp = hi; gp >= first; --gp) {
+        if (gp < hi) D += op_dur(g, q[gp].kind, q[gp].s);
+        const int64_t span = xend > post[gp] ? xend - post[gp] : post[gp] - xend;
+        const int64_t cost = span - (D < c ? D : c);
+        if (best < 0 || cost < bestc) best = gp, bestc = cost;
+      }
+      f->gap = best;
+      lastg = best;
+    }
+    if (rc == 0) {
+      qsort(it, (size_t)ni, sizeof(comm_item), cmp_comm_item);
+      for (int j = 1; j < ni; ++j)
+        if (it[j].gap < it[j - 1].gap) rc = -1;
+      int np = 0, j = 0;
+      int* out = prog + 3 * qoff[d];
+      for (int i = 0; i < n; ++i) {
+        while (j < ni && it[j].gap <= i) out[np++] = it[j++].code;
+        out[np++] = (PI_COMP << 28) | node_id(S, M, q[i].kind, q[i].s, q[i].m);
+      }
+      while (j < ni) out[np++] = it[j++].code;
+      plen[d] = np;
+    }
+    free(it);
+    free(flagged);
+    free(post);
+    free(rec_ok);
+  }
+  return rc;
+}
+
+/*
+ * Evaluate device programs with handshake transfers. Nodes: the computations; per transfer a
+ * handshake node (duration 0) in both its devices' programs and an arrival node (duration c)
+ * between the handshake and the consumer. Edges: program order; the producer before its
+ * handshake; same-device data edges; F(s,m) -> B(s,m); B(s,m) -> W(s,m). Longest path by Kahn's
+ * algorithm; a cycle is a deadlock. Busy time counts computation only.
+ */
+static int simulate_handshake(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                              const int* qlen, const int* prog, const int* plen,
+                              int64_t* makespan, int64_t* bubble) {
+  const int S = g->S, M = g->M, nk = g->split ? 3 : 2;
+  const int nc = nk * S * M, nt = 2 * S * M, nn = nc + 2 * nt;
+  int* succ = (int*)malloc(sizeof(int) * (size_t)nn * 6);
+  int* nsucc = (int*)calloc(nn, sizeof(int));
+  int* indeg = (int*)calloc(nn, sizeof(int));
+  int64_t* dur = (int64_t*)calloc(nn, sizeof(int64_t));
+  int64_t* est = (int64_t*)calloc(nn, sizeof(int64_t));
+  int64_t* fin = (int64_t*)malloc(sizeof(int64_t) * nn);
+  int* ready = (int*)malloc(sizeof(int) * nn);
+  char* used = (char*)calloc(nn, 1);
+#define HS_EDGE(a, b) (succ[(size_t)(a) * 6 + nsucc[a]++] = (b), indeg[b]++)
+  /* transfer index of producer (kind, s, m): (dir * S + s) * M + m, dir 0 forward, 1 backward */
+  for (int s = 0; s < S; ++s)
+    for (int m = 0; m < M; ++m) {
+      for (int k = 0; k < nk; ++k) dur[node_id(S, M, k, s, m)] = op_dur(g, k, s), used[node_id(S, M, k, s, m)] = 1;
+      if (s + 1 < S && g->dev[s] != g->dev[s + 1])
+        dur[nc + nt + (0 * S + s) * M + m] = g->link[g->dev[s] * g->P + g->dev[s + 1]];
+      if (s > 0 && g->dev[s] != g->dev[s - 1])
+        dur[nc + nt + (1 * S + s) * M + m] = g->link[g->dev[s] * g->P + g->dev[s - 1]];
+    }
+  for (int d = 0; d < g->P; ++d) {
+    int prev = -1;
+    for (int i = 0; i < plen[d]; ++i) {
+      const int code = prog[3 * qoff[d] + i], node = code & 0x0FFFFFFF;
+      int item = node;
+      if ((code >> 28) != PI_COMP) {
+        const int xk = node / (S * M), xs = (node / M) % S, xm = node % M;
+        item = nc + ((xk == KF ? 0 : 1) * S + xs) * M + xm;
+      }
+      used[item] = 1;
+      if (prev >= 0) HS_EDGE(prev, item);
+      prev = item;
+    }
+  }
+  for (int s = 0; s < S; ++s)
+    for (int m = 0; m < M; ++m) {
+      if (s + 1 < S) {
+        const int x = node_id(S, M, KF, s, m), y = node_id(S, M, KF, s + 1, m);
+        if (g->dev[s] == g->dev[s + 1]) {
+          HS_EDGE(x, y);
+        } else {
+          const int h = nc + (0 * S + s) * M + m;
+          HS_EDGE(x, h);
+          HS_EDGE(h, h + nt);
+          HS_EDGE(h + nt, y);
+          used[h] = used[h + nt] = 1;
+        }
+      }
+      if (s > 0) {
+        const int x = node_id(S, M, KB, s, m), y = node_id(S, M, KB, s - 1, m);
+        if (g->dev[s] == g->dev[s - 1]) {
+          HS_EDGE(x, y);
+        } else {
+          const int h = nc + (1 * S + s) * M + m;
+          HS_EDGE(x, h);
+          HS_EDGE(h, h + nt);
+          HS_EDGE(h + nt, y);
+          used[h] = used[h + nt] = 1;
+        }
+      }
+      HS_EDGE(node_id(S, M, KF, s, m), node_id(S, M, KB, s, m));
+      if (g->split) HS_EDGE(node_id(S, M, KB, s, m), node_id(S, M, KW, s, m));
+    }
+#undef HS_EDGE
+  int nr = 0, head = 0, nused = 0, rc = SIM_OK;
+  for (int i = 0; i < nn; ++i) {
+    nused += used[i];
+    if (used[i] && indeg[i] == 0) ready[nr++] = i;
+  }
+  while (head < nr) {
+    const int u = ready[head++];
+    fin[u] = est[u] + dur[u];
+    for (int e = 0; e < nsucc[u]; ++e) {
+      const int x = succ[(size_t)u * 6 + e];
+      if (fin[u] > est[x]) est[x] = fin[u];
+      if (--indeg[x] == 0) ready[nr++] = x;
+    }
+  }
+  if (nr < nused) {
+    rc = SIM_CYCLE;
+  } else {
+    int64_t ms = 0;
+    for (int i = 0; i < nr; ++i)
+      if (fin[ready[i]] > ms) ms = fin[ready[i]];
+    *makespan = ms;
+    for (int d = 0; d < g->P; ++d) {
+      int64_t busy = 0;
+      for (int i = 0; i < qlen[d]; ++i)
+        busy += op_dur(g, queue[qoff[d] + i].kind, queue[qoff[d] + i].s);
+      bubble[d] = ms - busy;
+    }
+  }
+  free(succ);
+  free(nsucc);
+  free(indeg);
+  free(dur);
+  free(est);
+  free(fin);
+  free(ready);
+  free(used);
+  return rc;
+}
+
+/* The reordering above on the asynchronous schedule of the queues, then its evaluation. */
+static int simulate_reordered(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
+                              const int* qlen, int64_t* makespan, int64_t* bubble,
+                              int64_t* stats) {
+  const int S = g->S, M = g->M, P = g->P, nk = g->split ? 3 : 2;
+  int total = 0;
+  for (int d = 0; d < P; ++d) total += qlen[d];
+  int* prog = (int*)malloc(sizeof(int) * (size_t)(3 * total + 1));
+  int plen[64];
+  int64_t* start = (int64_t*)malloc(sizeof(int64_t) * (size_t)nk * S * M);
+  int64_t* lvl = (int64_t*)malloc(sizeof(int64_t) * (size_t)nk * S * M);
+  int64_t ms0, bub0[64];
+  ref_dag_in plain = *g;
+  plain.serial = 0;
+  int rc = simulate(&plain, queue, qoff, qlen, &ms0, bub0, start, NULL);
+  if (rc == SIM_OK) {
+    /* levels: the same queues with every op taking 1 and every transfer nothing */
+    int64_t one[64], zero_w[64];
+    int64_t* nolink = (int64_t*)calloc((size_t)P * P, sizeof(int64_t));
+    for (int s = 0; s < S; ++s) one[s] = 1, zero_w[s] = g->split ? 1 : 0;
+    ref_dag_in unit = {S, M, g->split, P, g->dev, one, one, zero_w, nolink, 0};
+    rc = simulate(&unit, queue, qoff, qlen, &ms0, bub0, lvl, NULL);
+    free(nolink);
+  }
+  if (stats) stats[0] = stats[1] = 0;
+  if (rc == SIM_OK &&
+      reorder_programs(g, queue, qoff, qlen, start, lvl, prog, plen, stats) != 0)
+    rc = SIM_BADQ;
+  if (rc == SIM_OK) rc = simulate_handshake(g, queue, qoff, qlen, prog, plen, makespan, bubble);
+  free(start);
+  free(lvl);
+  free(prog);
+  return rc;
+}
+
 /* xfer 2: the naive coordination; xfer 3: the reordered one (needs the asynchronous schedule). */
 static int simulate_coordinated(const ref_dag_in* g, const ref_sop* queue, const int* qoff,
                                 const int* qlen, int ordered, int64_t* makespan,
@@ -836,7 +1139,9 @@ static void comm_overlap(const ref_dag_in* g, const ref_sop* sq, const int* qoff
  * ppos[P] (nullable) with the queue position at which each device first reaches its peak (-1
  * when it holds no activations). */
 /* xfer: 0 asynchronous transfers (the plain model), 1 serialised links, 2 blocking rendezvous in
- * the naive coordination, 3 blocking rendezvous in the reordered coordination. */
+ * the naive coordination, 3 blocking rendezvous in the reordered coordination (transfers at
+ * their ideal start), 4 the executor's three-step reordering with handshake transfers (comm then
+ * receives its two statistics). */
 static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t* costs,
                         const int64_t* link, const ref_op* q, int qcap, const int* qlen,
                         const int64_t* mem, int64_t* ms, int64_t* bub, int64_t* peak, int* ppos,
@@ -862,8 +1167,9 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
   int64_t* start = (mem || comm || bounds)
                        ? (int64_t*)malloc(sizeof(int64_t) * (size_t)3 * S * pr->M)
                        : NULL;
-  int rc = xfer >= 2 ? simulate_coordinated(&g, sq, qoff, qlen, xfer == 3, ms, bub)
-                     : simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
+  int rc = xfer == 4   ? simulate_reordered(&g, sq, qoff, qlen, ms, bub, comm)
+           : xfer >= 2 ? simulate_coordinated(&g, sq, qoff, qlen, xfer == 3, ms, bub)
+                       : simulate(&g, sq, qoff, qlen, ms, bub, start, NULL);
   if (bounds && rc == SIM_OK) {
     /* per device: start of its first op, end of its last op (0, 0 for an empty queue) */
     for (int d = 0; d < P; ++d) {
@@ -875,7 +1181,7 @@ static int eval_local_c(const ref_problem* pr, const ref_cand* c, const int64_t*
       }
     }
   }
-  if (comm && rc == SIM_OK) {
+  if (comm && rc == SIM_OK && xfer != 4) {
     for (int k = 0; k < 4; ++k) comm[k] = 0;
     comm_overlap(&g, sq, qoff, qlen, start, comm);
   }
@@ -930,7 +1236,7 @@ static void eval_record(const ref_problem* pr, const int64_t* costs, const int64
     if (peak)
       for (int d = 0; d < P; ++d) peak[d] = sentinel;
     if (comm)
-      for (int k = 0; k < 4; ++k) comm[k] = sentinel;
+      for (int k = 0; k < (xfer == 4 ? 2 : 4); ++k) comm[k] = sentinel;
     if (bounds)
       for (int k = 0; k < 2 * P; ++k) bounds[k] = sentinel;
   }
@@ -1060,7 +1366,7 @@ static void* batch_worker(void* arg) {
     eval_record(j->pr, j->costs, j->mem, j->link, j->cands + (size_t)i * j->pr->cand_stride,
                 j->out_ms + i, j->out_bub + (size_t)i * j->pr->P,
                 j->out_peak ? j->out_peak + (size_t)i * j->pr->P : NULL,
-                j->out_comm ? j->out_comm + (size_t)i * 4 : NULL, j->xfer,
+                j->out_comm ? j->out_comm + (size_t)i * (j->xfer == 4 ? 2 : 4) : NULL, j->xfer,
                 j->out_bounds ? j->out_bounds + (size_t)i * 2 * j->pr->P : NULL);
   return NULL;
 }
@@ -1128,6 +1434,17 @@ int oracle_sim_batch_ordered(const ref_problem* pr, const int64_t* costs, const 
                              const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
                              int nthreads) {
   return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, NULL, 3, NULL,
+                   nthreads);
+}
+
+/* The executor's reordering of the communication (§7's three steps, reorder_programs) evaluated
+ * with handshake transfers (simulate_handshake). out_stats (nullable) [n][2] = {transfers,
+ * mismatched receives the reordering moved} (sentinels for deadlocked / invalid candidates).
+ * Deadlocks (-1) only where the asynchronous schedule itself deadlocks. */
+int oracle_sim_batch_reorder(const ref_problem* pr, const int64_t* costs, const int64_t* link,
+                             const uint8_t* cands, int64_t n, int64_t* out_ms, int64_t* out_bub,
+                             int64_t* out_stats, int nthreads) {
+  return run_batch(pr, costs, NULL, link, cands, n, out_ms, out_bub, NULL, out_stats, 4, NULL,
                    nthreads);
 }
 

@@ -45,6 +45,9 @@ def lib():
         L.oracle_sim_batch_ordered.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                                ctypes.c_int64, p, p, ctypes.c_int]
         L.oracle_sim_batch_ordered.restype = ctypes.c_int
+        L.oracle_sim_batch_reorder.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
+                                               ctypes.c_int64, p, p, p, ctypes.c_int]
+        L.oracle_sim_batch_reorder.restype = ctypes.c_int
         L.oracle_sim_batch_bounds.argtypes = [ctypes.POINTER(RefProblem), p, p, p,
                                               ctypes.c_int64, p, p, p, ctypes.c_int]
         L.oracle_sim_batch_bounds.restype = ctypes.c_int
@@ -146,6 +149,25 @@ def sim_batch_ordered(prob, costs, link, cands, nthreads=1):
     if rc != 0:
         raise ValueError(f"oracle_sim_batch_ordered rejected the arguments (rc={rc})")
     return ms, bub
+
+
+def sim_batch_reorder(prob, costs, link, cands, nthreads=1):
+    """Evaluate candidate records under the executor's three-step reordering of the
+    communication (mismatched pairs, feasible windows, greedy minimum of span - overlap) with
+    handshake transfers. Returns (makespan[n], bubble[n, P], stats[n, 2] = {transfers,
+    mismatched receives})."""
+    costs = np.ascontiguousarray(costs, dtype=np.int64)
+    link = np.ascontiguousarray(link, dtype=np.int64)
+    cands = np.ascontiguousarray(cands, dtype=np.uint8)
+    n = cands.shape[0]
+    ms = np.zeros(n, dtype=np.int64)
+    bub = np.zeros((n, prob.P), dtype=np.int64)
+    st = np.zeros((n, 2), dtype=np.int64)
+    rc = lib().oracle_sim_batch_reorder(ctypes.byref(prob), _ptr(costs), _ptr(link), _ptr(cands),
+                                        n, _ptr(ms), _ptr(bub), _ptr(st), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_sim_batch_reorder rejected the arguments (rc={rc})")
+    return ms, bub, st
 
 
 def sim_batch_serial(prob, costs, link, cands, nthreads=1):

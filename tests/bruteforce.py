@@ -14,6 +14,11 @@ is pinned to something other than itself:
   sends its cross-device output right after it; a device that reaches a send or receive waits
   there, and once both ends have arrived the transfer runs for the link time, holding both.
   Tick by tick, with no graph: a program that can never move again is a deadlock.
+* ``reorder_programs`` builds the executor's reordered programs (§7's three steps: mismatched
+  receives, their feasible windows, the greedy cheapest gap by span minus overlap) from a
+  tick-by-tick asynchronous run and levels found by fixpoint iteration; ``handshake_tick_simulate``
+  executes programs tick by tick with handshake transfers (a device waits at a send or receive
+  until the other end is reached; the data arrives the link time later while both compute).
 * ``has_cycle`` builds the dependency graph from its definition (§5, §6 "Scheduling Tuning") and
   runs an iterative three-colour DFS.
 
@@ -210,6 +215,143 @@ def rdv_tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, progs=None)
     if not all(ptr[d] == len(progs[d]) for d in range(P)):
         return -1, [-1] * P
     ms = max(max(fin.values(), default=0), max(busy_until, default=0))
+    bub = [ms - sum(_dur(k, s, split, Fs, Bs, Ws) for (k, s, m) in queues[d]) for d in range(P)]
+    return ms, bub
+
+
+def levels(S, split, dev, queues):
+    """Number of ops on the longest dependency chain before each op (queue order and data
+    dependencies), by iterating lvl(op) = max(lvl(pred) + 1) to a fixpoint."""
+    lvl = {op: 0 for q in queues for op in q}
+    preds = {}
+    for q in queues:
+        for i, op in enumerate(q):
+            ps = [p for p, _ in _producers(op, S, split, dev, [[0] * len(queues)] * len(queues))]
+            if i > 0:
+                ps.append(q[i - 1])
+            preds[op] = ps
+    changed = True
+    while changed:
+        changed = False
+        for op, ps in preds.items():
+            v = max([lvl[p] + 1 for p in ps], default=0)
+            if v != lvl[op]:
+                lvl[op], changed = v, True
+    return lvl
+
+
+def reorder_programs(S, M, split, dev, Fs, Bs, Ws, link, queues, starts, lvl):
+    """The executor's reordering (see the module docstring). Returns (programs, transfers,
+    mismatched receives)."""
+    node = lambda op: (op[0] * S + op[1]) * M + op[2]
+    dur = lambda op: _dur(op[0], op[1], split, Fs, Bs, Ws)
+    end = lambda op: starts[op] + dur(op)
+    progs, ntr, nmis = [], 0, 0
+    for d, q in enumerate(queues):
+        post = [0] + [end(op) for op in q]
+        items = []                                   # [key, gap, item]
+        for i, op in enumerate(q):
+            kind, s, m = op
+            src = None
+            if kind == F and s > 0 and dev[s - 1] != d:
+                src = (F, s - 1, m)
+            if kind == B and s < S - 1 and dev[s + 1] != d:
+                src = (B, s + 1, m)
+            if src is not None:
+                items.append([(end(src), lvl[src], node(src)), i, ("r", src)])
+                ntr += 1
+            if _consumers(op, S, dev):
+                items.append([(end(op), lvl[op], node(op)), i + 1, ("s", op)])
+        rec, flagged = [], []
+        for it in items:
+            if not rec or it[0] > rec[-1][0]:
+                rec.append(it)
+            else:
+                flagged.append(it)
+        nmis += len(flagged)
+        lastg = 0
+        for f in sorted(flagged, key=lambda it: it[0]):
+            assert f[2][0] == "r"
+            lo = max([lastg] + [r[1] for r in rec if r[0] < f[0]])
+            hi = min(r[1] for r in rec if r[0] > f[0])
+            X, iY = f[2][1], f[1]
+            c = link[dev[X[1]]][d]
+            gx = next((g for g in range(len(q) + 1) if post[g] >= starts[X]), len(q) + 1)
+            first = min(max(lo, gx), hi)
+            best = None
+            for g in range(hi, first - 1, -1):
+                cost = abs(end(X) - post[g]) - min(c, sum(dur(q[j]) for j in range(g, iY)))
+                if best is None or cost < best[0]:
+                    best = (cost, g)
+            f[1] = lastg = best[1]
+        allc = sorted(items, key=lambda it: it[0])
+        assert all(allc[j][1] <= allc[j + 1][1] for j in range(len(allc) - 1))
+        prog, j = [], 0
+        for i, op in enumerate(q):
+            while j < len(allc) and allc[j][1] <= i:
+                prog.append(allc[j][2])
+                j += 1
+            prog.append(("c", op))
+        prog += [it[2] for it in allc[j:]]
+        progs.append(prog)
+    return progs, ntr, nmis
+
+
+def handshake_tick_simulate(P, S, M, split, dev, Fs, Bs, Ws, link, queues, progs):
+    """Returns (makespan, bubbles) or (-1, [-1]*P) on deadlock."""
+    total = sum(_dur(k, s, split, Fs, Bs, Ws) for q in queues for (k, s, m) in q)
+    max_ticks = total + sum(max(r) for r in link) * 2 * S * M + 2
+    ptr = [0] * P
+    running = [None] * P
+    busy_until = [0] * P
+    waiting = {}                       # transfer -> the device waiting at its other end
+    arrival = {}                       # transfer -> tick its data arrives
+    fin = {}
+    t = 0
+    while t <= max_ticks:
+        changed = True
+        while changed:
+            changed = False
+            for d in range(P):
+                if running[d] is not None and busy_until[d] <= t:
+                    fin[running[d]] = busy_until[d]
+                    running[d] = None
+                    ptr[d] += 1
+                    changed = True
+            for d in range(P):
+                if running[d] is not None or ptr[d] >= len(progs[d]):
+                    continue
+                what, x = progs[d][ptr[d]]
+                if what == "c":
+                    ok = True
+                    for p, _ in _producers(x, S, split, dev, link):
+                        if dev[p[1]] == d:
+                            ok = ok and p in fin and fin[p] <= t
+                        else:
+                            ok = ok and p in arrival and arrival[p] <= t
+                    if ok:
+                        running[d] = x
+                        busy_until[d] = t + _dur(x[0], x[1], split, Fs, Bs, Ws)
+                        changed = True
+                elif what == "s" and not (x in fin and fin[x] <= t):
+                    pass                               # a send waits for its producer
+                elif x in waiting and waiting[x] != d:
+                    other = waiting.pop(x)
+                    p = dev[x[1]]
+                    q = dev[_consumers(x, S, dev)[0][1]]
+                    arrival[x] = t + link[p][q]
+                    ptr[other] += 1
+                    ptr[d] += 1
+                    changed = True
+                elif x not in waiting:
+                    waiting[x] = d
+                    changed = True
+        if all(ptr[d] == len(progs[d]) and running[d] is None for d in range(P)):
+            break
+        t += 1
+    if not all(ptr[d] == len(progs[d]) for d in range(P)):
+        return -1, [-1] * P
+    ms = max(fin.values(), default=0)
     bub = [ms - sum(_dur(k, s, split, Fs, Bs, Ws) for (k, s, m) in queues[d]) for d in range(P)]
     return ms, bub
 
