@@ -651,29 +651,32 @@ static int reorder_programs(const ref_dag_in* g, const ref_sop* queue, const int
       }
       flagged[b] = v;
     }
-    int lastg = 0;
+    /* the in-order items are sorted by key and by gap; as the mismatched ones come in key
+     * order, the in-order items below each one only grow: one cursor (j) serves them all */
+    int lastg = 0, lo_rec = 0, j = 0;
     for (int a = 0; a < nf; ++a) {
       comm_item* f = &it[flagged[a]];
-      int lo = lastg, hi = -1;
-      for (int j = 0; j < ni; ++j) {
+      for (; j < ni; ++j) {
         if (!rec_ok[j]) continue;
-        if (cmp_comm_item(&it[j], f) < 0) {
-          if (it[j].gap > lo) lo = it[j].gap;
-        } else {
-          hi = it[j].gap;
-          break;
-        }
+        if (cmp_comm_item(&it[j], f) > 0) break;
+        lo_rec = it[j].gap; /* an in-order item of a smaller key */
       }
-      if ((f->code >> 28) != PI_RECV || hi < 0) { /* cannot happen (see above) */
+      if ((f->code >> 28) != PI_RECV || j == ni) { /* cannot happen (see above) */
         rc = -1;
         break;
       }
+      const int lo = lastg > lo_rec ? lastg : lo_rec, hi = it[j].gap;
       const int X = f->node, iY = f->gap;
       const int xk = X / (S * M), xs = (X / M) % S;
       const int64_t c = g->link[g->dev[xs] * g->P + d];
       const int64_t xend = start[X] + op_dur(g, xk, xs);
-      int gx = 0;
-      while (gx <= n && post[gx] < start[X]) ++gx;
+      /* gx: the first gap whose post time is not before X starts (post[] never decreases) */
+      int gx = 0, gend = n + 1;
+      while (gx < gend) {
+        const int mid = (gx + gend) / 2;
+        if (post[mid] < start[X]) gx = mid + 1;
+        else gend = mid;
+      }
       int first = lo > gx ? lo : gx;
       if (first > hi) first = hi;
       int64_t D = 0; /* durations of the computations in gaps [gap, iY) */
