@@ -233,6 +233,35 @@ int octo_sim_batch_ordered(const octo_problem* prob, const int64_t* layer_costs,
                            int64_t* out_makespan, int64_t* out_bubble, void* stream);
 
 /*
+ * octo_sim_batch_reorder — the unified executor's deadlock-free, overlap-aware reordering of the
+ * communication (§7, its three steps) with handshake transfers: a device that reaches a send or
+ * a receive waits until the other device has reached the other end; then both go on at once,
+ * and the data arrives c = link[p][q] later while both compute; the consumer starts once it has
+ * arrived. Every transfer has a key: its producer's end in the asynchronous schedule of
+ * octo_sim_batch, then the producer's level (the number of ops on the longest dependency chain
+ * before it, queue order included), then its node id (kind S + stage) M + m. Starting from the
+ * naive programs of octo_sim_batch_rdv (a receive before its consumer, a send after its
+ * producer): (1) on every device, a communication item whose key is below the largest key
+ * before it in program order is a mismatched pair (only receives can be); (2) its feasible
+ * window is the gaps between computations that lie between the in-order items just below and
+ * just above its key, at most its consumer's, whose post time (the end of the previous
+ * computation in the asynchronous schedule) is not before its producer starts; (3) each
+ * mismatched receive, in key order, takes the gap of least cost = |producer end - post time|
+ * (the communication span) - min(c, the durations of the computations between that gap and the
+ * consumer) (the overlap with neighbouring computation), the highest gap on ties, and the next
+ * one's window starts there. Communication items of one gap run in key order, so every device
+ * meets its transfers in key order and no cycle of waits can form: OCTO_MS_DEADLOCK only where
+ * the compute orders themselves deadlock. Busy time counts computation only.
+ * out_stats (device int64 [n][2], nullable): transfers (send/receive pairs) and mismatched
+ * receives of each candidate (the sentinels for deadlocked and invalid records). Other
+ * arguments, results and status as octo_sim_batch.
+ */
+int octo_sim_batch_reorder(const octo_problem* prob, const int64_t* layer_costs,
+                           const int64_t* link, const void* candidates, int64_t n,
+                           int64_t* out_makespan, int64_t* out_bubble, int64_t* out_stats,
+                           void* stream);
+
+/*
  * octo_advance_w — selective W advancing (§6 "Scheduling Tuning", third policy) under the
  * per-device capacity of §6 Eq. 2, on a batch of candidate records. For each record, after its
  * queues are generated and its moves applied: while some device's peak (as octo_sim_batch_mem)

@@ -52,6 +52,7 @@ def lib():
         L.octo_sim_batch_serial.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
         L.octo_sim_batch_rdv.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
         L.octo_sim_batch_ordered.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp]
+        L.octo_sim_batch_reorder.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_bounds.argtypes = [pp, vp, vp, vp, i64, vp, vp, vp, vp]
         L.octo_sim_batch_mem.restype = ctypes.c_int
         L.octo_tune_step.argtypes = [pp, vp, vp, vp, vp, i64, ctypes.c_uint64, i32, vp]
@@ -213,6 +214,29 @@ def sim_batch_ordered(prob, layer_costs, link, candidates, out_makespan=None, ou
         _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_ordered")
     return out_makespan, out_bubble
+
+
+def sim_batch_reorder(prob, layer_costs, link, candidates, out_makespan=None, out_bubble=None,
+                      out_stats=None, stream=None):
+    """octo_sim_batch_reorder: the executor's three-step reordering of the communication with
+    handshake transfers. Returns (makespan, bubble, stats int64 [n, 2] = {transfers,
+    mismatched receives})."""
+    n = candidates.shape[0]
+    dev = candidates.device
+    if out_makespan is None:
+        out_makespan = torch.empty(n, dtype=torch.int64, device=dev)
+    if out_bubble is None:
+        out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    if out_stats is None:
+        out_stats = torch.empty((n, 2), dtype=torch.int64, device=dev)
+    rc = lib().octo_sim_batch_reorder(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
+        _dev_ptr(out_stats, torch.int64, "out_stats"), _stream(candidates, stream))
+    _check(rc, "octo_sim_batch_reorder")
+    return out_makespan, out_bubble, out_stats
 
 
 def sim_batch_bounds(prob, layer_costs, link, candidates, out_makespan=None, out_bubble=None,

@@ -504,6 +504,12 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t x) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = x;
 }
 
+__global__ void k_fill_i64(int64_t* __restrict__ p, int64_t n, int64_t x) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = x;
+}
+
 // Queue-table rows of the interleaved order (v <= 2) for one launch geometry: thread r writes
 // rank r's queue; chunk k of rank r is stage r + k P.
 __global__ void k_qtab_inter(uint32_t* __restrict__ out, int P, int v, int M, int split, int R,
@@ -1688,11 +1694,20 @@ constexpr int32_t OB_NONE = -1;
 
 // Per-slot scratch of k_ordered.
 struct OrdBufs {
-  int64_t* tb;      // [slot][3 S_max M] finish time of each op
+  int64_t* tb;      // [slot][3 S_max M] finish time of each op (REORDER, phase C: arrivals)
   int64_t* rkey;    // [slot][P][rcap] receive keys (producer end)
   uint32_t* rid;    // [slot][P][rcap] receive producers (pitem with type 0)
   uint32_t* prog;   // [slot][P][pcap] programs
   int rcap, pcap;
+  // REORDER only
+  int64_t* ts;      // [slot][3 S_max M] start time of each op
+  int32_t* tl;      // [slot][3 S_max M] level of each op
+  int64_t* ikey;    // [slot][P][icap] communication items: producer end ...
+  uint64_t* iln;    // ... level << 32 | producer node ...
+  int32_t* igap;    // ... and gap
+  int32_t* iord;    // [slot][P][2 icap] in-order items, then the mismatched ones
+  int64_t* stats;   // [n][2] (nullable): transfers, mismatched receives
+  int icap;
 };
 
 // (t, cls, tie) < (t', cls', tie')
@@ -1861,13 +1876,176 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
   return n;
 }
 
+// Phase B of the executor's reordering for lane d (REORDER): the communication items of the
+// naive programs (a receive in the gap before its consumer, a send after its producer) with
+// their keys (producer end, level, node); step 1, the items below the running maximum key are
+// the mismatched receives; steps 2 and 3, each of those in key order takes the gap of least
+// cost (|producer end - the gap's post time| - min(transfer, the computations from the gap to
+// the consumer)) among the gaps between the in-order items around its key, at most its
+// consumer's, whose post time is not before the producer starts (the highest gap always
+// qualifies; ties: the highest); then the items, in key order, are merged with the computations
+// by gap. Returns the program length; *nrecv and *nmis get the two counts.
+template <int VMAX>
+__device__ __forceinline__ int build_program3(const Chunks<VMAX>& c, const uint16_t* row, int nq,
+                                              const int64_t* tb, const int64_t* ts,
+                                              const int32_t* tl, int S, int M, int64_t* ikey,
+                                              uint64_t* iln, int32_t* igap, int32_t* iord,
+                                              int icap, uint32_t* prog, int* nrecv, int* nmis) {
+  auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
+  auto dur_of = [&](int kind, int k) {
+    return kind == KF ? pick<VMAX>(c.dF, k) : kind == KB ? pick<VMAX>(c.dB, k) : pick<VMAX>(c.dW, k);
+  };
+  auto less = [&](int64_t t, uint64_t ln, int64_t t2, uint64_t ln2) {
+    return t != t2 ? t < t2 : ln < ln2;
+  };
+  int* recs = iord;
+  int* flg = iord + icap;
+  // the items in program order; step 1 on the fly
+  int ni = 0, nr = 0, nf = 0, nrv = 0;
+  int64_t topk = 0;
+  uint64_t topl = 0;
+  auto add = [&](int64_t t, uint64_t ln, int gap, bool recv) {
+    ikey[ni] = t, iln[ni] = ln, igap[ni] = gap;
+    if (nr == 0 || less(topk, topl, t, ln)) {
+      recs[nr++] = ni;
+      topk = t, topl = ln;
+    } else {
+      flg[nf++] = ni;
+    }
+    nrv += recv ? 1 : 0;
+    ++ni;
+  };
+  for (int i0 = 0; i0 < nq; i0 += 8) {
+    const uint4 b = row_span(row, i0 >> 3, nq);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (i0 + u >= nq) break;
+      const uint32_t e = span_entry(b, u);
+      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      const int s = pick<VMAX>(c.st, k);
+      const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
+      if (cx & CX_IN) {
+        const int x = node(kind, kind == KF ? s - 1 : s + 1, m);
+        add(tb[x], (uint64_t)(uint32_t)tl[x] << 32 | (uint32_t)x, i0 + u, true);
+      }
+      if (cx & CX_OUT) {
+        const int y = node(kind, s, m);
+        add(tb[y], (uint64_t)(uint32_t)tl[y] << 32 | (uint32_t)y, i0 + u + 1, false);
+      }
+    }
+  }
+  *nrecv = nrv, *nmis = nf;
+  // the mismatched items in key order (few, and nearly sorted)
+  for (int a2 = 1; a2 < nf; ++a2) {
+    const int v = flg[a2];
+    const int64_t vk = ikey[v];
+    const uint64_t vl = iln[v];
+    int j = a2;
+    while (j > 0 && less(vk, vl, ikey[flg[j - 1]], iln[flg[j - 1]])) {
+      flg[j] = flg[j - 1];
+      --j;
+    }
+    flg[j] = v;
+  }
+  // steps 2 and 3: the in-order items are sorted by key and by gap, so one cursor serves all
+  RowCursor rc;
+  rc.init(row, nq);
+  auto post = [&](int g) -> int64_t {  // end of computation g - 1 (0 before the first)
+    if (g == 0) return 0;
+    const uint32_t e = rc.at(g - 1);
+    const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+    return tb[node(kind, pick<VMAX>(c.st, k), m)];
+  };
+  int rp = 0, lastg = 0, logap = 0;
+  for (int a2 = 0; a2 < nf; ++a2) {
+    const int f = flg[a2];
+    const int64_t fk = ikey[f];
+    const uint64_t fl = iln[f];
+    while (rp < nr && less(ikey[recs[rp]], iln[recs[rp]], fk, fl)) logap = igap[recs[rp++]];
+    const int hi = rp < nr ? igap[recs[rp]] : igap[f];  // rp < nr always: f is below a record
+    const int lo = lastg > logap ? lastg : logap;
+    const int iY = igap[f];
+    const int x = (int)(uint32_t)fl;
+    const int64_t xst = ts[x];
+    // the transfer's time: the consumer's input weight
+    const uint32_t ey = rc.at(iY);
+    const int ky = (ey >> 11) & 7;
+    const int64_t cw = ((ey >> 14) & 3) == KF ? pick<VMAX>(c.wF, ky) : pick<VMAX>(c.wB, ky);
+    int64_t D = 0;
+    for (int i = hi; i < iY; ++i) {
+      const uint32_t e = rc.at(i);
+      D += dur_of((e >> 14) & 3, (e >> 11) & 7);
+    }
+    int best = hi;
+    int64_t bestc = 0;
+    for (int gp = hi; gp >= lo; --gp) {
+      if (gp < hi) {
+        const uint32_t e = rc.at(gp);
+        D += dur_of((e >> 14) & 3, (e >> 11) & 7);
+      }
+      const int64_t pt = post(gp);
+      if (gp < hi && pt < xst) break;
+      const int64_t span = fk > pt ? fk - pt : pt - fk;
+      const int64_t cost = span - (D < cw ? D : cw);
+      if (gp == hi || cost < bestc) best = gp, bestc = cost;
+    }
+    igap[f] = best;
+    lastg = best;
+  }
+  // the program: items in key order (in-order ones and mismatched ones merged), each before
+  // the computation its gap names, written four per 16-byte store
+  int n = 0, ri = 0, fi = 0;
+  uint4 pk4 = make_uint4(0, 0, 0, 0);
+  auto emit = [&](uint32_t item) {
+    const int q = n & 3;
+    pk4.x = q == 0 ? item : pk4.x;
+    pk4.y = q == 1 ? item : pk4.y;
+    pk4.z = q == 2 ? item : pk4.z;
+    pk4.w = q == 3 ? item : pk4.w;
+    if (q == 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
+    ++n;
+  };
+  RowCursor cc;
+  cc.init(row, nq);
+  for (int i = 0; i <= nq; ++i) {
+    for (;;) {
+      int src = -1;
+      if (ri < nr) src = recs[ri];
+      if (fi < nf && (src < 0 || less(ikey[flg[fi]], iln[flg[fi]], ikey[src], iln[src])))
+        src = flg[fi];
+      if (src < 0 || (i < nq && igap[src] > i)) break;
+      if (ri < nr && src == recs[ri]) ++ri;
+      else ++fi;
+      const int x = (int)(uint32_t)iln[src];
+      const int xk = x / (S * M), xs = (x / M) % S, xm = x % M;
+      // a send's producer is an own op at the gap before; a receive's is on another device
+      const uint32_t pe = igap[src] > 0 ? cc.at(igap[src] - 1) : 0xFFFFFFFFu;
+      const bool own = igap[src] > 0 && (int)((pe >> 14) & 3) == xk &&
+                       pick<VMAX>(c.st, (pe >> 11) & 7) == xs && (int)(pe & 0x7FF) == xm;
+      emit(((own ? PI_SEND : PI_RECV) << 30) | pitem(0, xk, xs, xm));
+    }
+    if (i < nq) {
+      const uint32_t e = cc.at(i);
+      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      emit(pitem(PI_COMP, kind, pick<VMAX>(c.st, k), m));
+    }
+  }
+  if (n & 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
+  return n;
+}
+
 // RING: 40-bit ring tables of a.ring rows per stage per group. Phase C keeps each device's
 // computations in queue order and adds only the sends, each of which reads its producer's slot
 // after the producer and before any later computation of the stage, so the ring argument of
 // k_tune_ring holds for both rounds; a candidate whose queue window reaches the ring joins the
 // wide list (wide_list: taken by a 40-bit full-row pass, a.ring = M) or else the redo list, and
 // one whose times pass 40 bits the redo list, which the 64-bit kernel (list, list_n) takes.
-template <int VMAX, bool RING>
+// REORDER: the executor's three-step reordering (build_program3) with handshake transfers in
+// phase C: a receive completes when the sender has announced itself, at h = max(the sender's
+// announce time, the receiver's clock); both clocks go to h, and the data's arrival h + w is kept
+// in the finish-time buffer at the producer's node (phase B is done with it), where the consumer,
+// a later computation of the same lane, takes it as its input time.
+template <int VMAX, bool RING, bool REORDER>
 __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
                                                   const int32_t* __restrict__ list,
                                                   const int32_t* __restrict__ list_n,
@@ -1887,8 +2065,11 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
   const int dl = d < P ? d : 0;
   uint16_t* row = a.qscratch + ((size_t)slot * P + dl) * a.qcap;
   int64_t* tb = ob.tb + (size_t)slot * 3 * a.pr.s_max * M;
-  int64_t* rkey = ob.rkey + ((size_t)slot * P + dl) * ob.rcap;
-  uint32_t* rid = ob.rid + ((size_t)slot * P + dl) * ob.rcap;
+  int64_t* rkey = REORDER ? nullptr : ob.rkey + ((size_t)slot * P + dl) * ob.rcap;
+  uint32_t* rid = REORDER ? nullptr : ob.rid + ((size_t)slot * P + dl) * ob.rcap;
+  int64_t* ts = REORDER ? ob.ts + (size_t)slot * 3 * a.pr.s_max * M : nullptr;
+  int32_t* tl = REORDER ? ob.tl + (size_t)slot * 3 * a.pr.s_max * M : nullptr;
+  const size_t io = ((size_t)slot * P + dl) * ob.icap;
   uint32_t* prog = ob.prog + ((size_t)slot * P + dl) * ob.pcap;
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
@@ -1914,6 +2095,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
     L.cm.reset();
     L.fs = -1;
     L.tb = tb, L.tS = S, L.tM = M;
+    L.ts = ts, L.tl = tl, L.rnd = 0;
     int wl = 0;
     if (valid && d < P) {
       busy = setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, nullptr,
@@ -1942,8 +2124,14 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
     }
     __syncthreads();  // every lane's finish times visible to the group
     // B: programs
-    int plen = 0;
-    if (mine && !dead) plen = build_program<VMAX>(c, row, L.nops, tb, S, M, rkey, rid, prog);
+    int plen = 0, nrecv = 0, nmis = 0;
+    if constexpr (REORDER) {
+      if (mine && !dead)
+        plen = build_program3<VMAX>(c, row, L.nops, tb, ts, tl, S, M, ob.ikey + io, ob.iln + io,
+                                    ob.igap + io, ob.iord + 2 * io, ob.icap, prog, &nrecv, &nmis);
+    } else {
+      if (mine && !dead) plen = build_program<VMAX>(c, row, L.nops, tb, S, M, rkey, rid, prog);
+    }
     if (run) T.clear(S * ring.R, d, G);
     mbox[me] = RDV_EMPTY;
     obn[me] = OB_NONE;
@@ -1963,15 +2151,27 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
       int rd = 0, wr = 0, store = 0, src = 0;
       uint32_t mask = 0, want = 0, state = 0;
       int64_t w = 0, dur = 0;
-      auto decode = [&](uint32_t it) {
+      // REORDER: a computation with a cross-device input takes the arrival its receive left at
+      // the producer's node (xat); a receive names that node (xnode). Only a real item (real:
+      // the lane has one; otherwise the code 0 stands in, whose op need not be the lane's)
+      // loads an arrival.
+      bool xarr = false;
+      int64_t xat = 0;
+      int xnode = 0;
+      auto decode = [&](uint32_t it, bool real) {
         type = it >> 30;
         const int kind = (int)((it >> 28) & 3u), s = (int)((it >> 16) & 63u), m = (int)(it & 0x7FFu);
         tag = it & 0x3FFFFFFFu;
+        xarr = false;
         if (type == PI_COMP) {
           Desc D;
           describe<VMAX>(D, c, ring, kind, chunk_of<VMAX>(c, s, v), m);
           rd = D.rd, wr = D.wr, store = D.store, mask = (uint32_t)D.mask, want = (uint32_t)D.want;
           state = D.state, w = D.w, dur = D.dur;
+          if constexpr (REORDER) {
+            xarr = real && (D.cx & CX_IN) != 0;
+            if (xarr) xat = tb[(kind * S + (kind == KF ? s - 1 : s + 1)) * M + m];
+          }
         } else if (type == PI_SEND) {  // its producer (an own op) must have finished
           rd = s * ring.R + (m & ring.mask);
           const uint32_t par = ((uint32_t)m >> ring.lg) & 1u;
@@ -1982,9 +2182,10 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
           const int cs = kind == KF ? s + 1 : s - 1;
           const int ck = chunk_of<VMAX>(c, cs, v);
           w = kind == KF ? pick<VMAX>(c.wF, ck) : pick<VMAX>(c.wB, ck);
+          xnode = (kind * S + s) * M + m;
         }
       };
-      decode(live ? prog[0] : 0u);
+      decode(live ? prog[0] : 0u, live);
       for (;;) {
         uint32_t plo, phi;
         T.issue(live && type != PI_RECV ? rd : 0, plo, phi);
@@ -1994,17 +2195,20 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
         const uint64_t p = (uint64_t)plo | ((uint64_t)phi << 32);
         const bool rdy = (plo & mask) == want;
         const bool okC = live && type == PI_COMP && rdy;
-        const int64_t tin = (int64_t)(p >> 3) + w;
+        const int64_t tin = xarr ? xat : (int64_t)(p >> 3) + w;
         const int64_t st = tin > clock ? tin : clock;
         const int64_t fin = st + dur;
         const bool okSA = live && type == PI_SEND && !arrived && rdy;
         const bool okSD = live && type == PI_SEND && arrived && box != RDV_EMPTY;
         const bool okR = live && type == PI_RECV && on == (int32_t)tag;
-        const int64_t xend = (ot > clock ? ot : clock) + w;
+        // the handshake, and where both clocks go: its end (blocking) or its start (REORDER)
+        const int64_t hs = ot > clock ? ot : clock;
+        const int64_t xend = REORDER ? hs : hs + w;
         if (okC && store) T.store(wr, ((uint64_t)fin << 3) | state);
         if (okSA) obn[me] = (int32_t)tag, obt[me] = clock;
         if (okSD) mbox[me] = RDV_EMPTY, obn[me] = OB_NONE;
         if (okR) mbox[g0 + src] = xend;
+        if (REORDER && okR) tb[xnode] = hs + w;
         clock = okC ? fin : okSD ? box : okR ? xend : clock;
         arrived = okSA ? true : okSD ? false : arrived;
         const bool done = okC || okSD || okR;
@@ -2014,7 +2218,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
           const uint32_t it = live ? nitem : 0u;
           __asm__ volatile("" : "+v"(nitem));
           nitem = pos + 1 < plen ? prog[pos + 1] : 0u;
-          decode(it);
+          decode(it, live);
         }
         __asm__ volatile("" ::: "memory");
         if (__ballot(okC || okSA || okSD || okR) == 0) {
@@ -2025,6 +2229,8 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
       }
     }
     const int64_t ms = group_max(clock, G);
+    int64_t srecv = 0, smis = 0;
+    if constexpr (REORDER) srecv = group_sum(nrecv, G), smis = group_sum(nmis, G);
     // overflow test over both rounds' clocks (phase A's alone when it deadlocked)
     const int64_t top = RING ? group_max(clock > L.clock ? clock : L.clock, G) : 0;
     if (has && valid && (!on_ring || top >= Table40::LIMIT)) {
@@ -2039,6 +2245,8 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
       const int64_t sv = dead || cdead ? (int64_t)OCTO_MS_DEADLOCK : 0;
       if (d == 0) a.out_ms[cand] = sv ? sv : ms;
       a.out_bub[cand * P + d] = sv ? sv : ms - busy;
+      if (REORDER && ob.stats && d == 0)
+        ob.stats[2 * cand] = sv ? sv : srecv, ob.stats[2 * cand + 1] = sv ? sv : smis;
     } else if (has && !valid && d < P) {
       if (d == 0) a.out_ms[cand] = OCTO_MS_INVALID;
       a.out_bub[cand * P + d] = OCTO_MS_INVALID;
@@ -4266,21 +4474,26 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
 }
 
 
-// The reordered coordination behind octo_sim_batch_ordered: k_ordered over all records, one
-// group per candidate — first on 40-bit ring tables (when the ring is shorter than M), then on
-// 64-bit full rows over the candidates the ring pass left (or over all of them). The scratch
-// (finish-time buffers, receive keys, programs) is sized for the larger pass's group slots.
-template <int VC>
+// The reordered coordinations behind octo_sim_batch_ordered (REORDER false) and
+// octo_sim_batch_reorder (REORDER true): k_ordered over all records, one group per candidate —
+// first on 40-bit ring tables (when the ring is shorter than M), then on 64-bit full rows over
+// the candidates the ring pass left (or over all of them). The scratch (finish-time buffers,
+// receive keys or communication items, programs) is sized for the larger pass's group slots.
+template <int VC, bool REORDER>
 int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
-                   const void* cands, int64_t n, int64_t* ms, int64_t* bub, hipStream_t stream) {
+                   const void* cands, int64_t n, int64_t* ms, int64_t* bub, int64_t* stats,
+                   hipStream_t stream) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
   DevInfo di;
   int rc = dev_info(dev, &di);
   if (rc) return rc;
-  // at most 4 GiB of per-slot scratch (finish times, receive keys, programs, queue rows)
-  const size_t per_slot = (size_t)prob->P * prob->v_max * prob->M * (3 * 8 + 2 * 12 + 7 * 4) +
-                          (size_t)prob->P * queue_cap(prob) * 2;
+  // at most 4 GiB of per-slot scratch (finish times, receive keys or communication items,
+  // programs, queue rows)
+  const size_t per_slot =
+      (size_t)prob->P * prob->v_max * prob->M *
+          (REORDER ? 3 * (8 + 8 + 4) + 4 * (8 + 8 + 4 + 8) + 7 * 4 : 3 * 8 + 2 * 12 + 7 * 4) +
+      (size_t)prob->P * queue_cap(prob) * 2;
   auto grid_of = [&](auto kern, const Plan& pl, int* g) {
     int rc2 = occupancy_grid(kern, pl.lds_bytes, di.cus, g);
     if (rc2) return rc2;
@@ -4294,13 +4507,14 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   const Plan fp = ring_plan(prob, di.lds_max, prob->P * prob->v_max, prob->M);
   int rgrid = 0, fgrid = 0;
   if (rr.R < prob->M && rp.CPW >= 1) {
-    if ((rc = grid_of(k_ordered<VC, true>, rp, &rgrid))) return rc;
-    if (fp.CPW >= 1 && (rc = grid_of(k_ordered<VC, true>, fp, &fgrid))) return rc;
+    if ((rc = grid_of(k_ordered<VC, true, REORDER>, rp, &rgrid))) return rc;
+    if (fp.CPW >= 1 && (rc = grid_of(k_ordered<VC, true, REORDER>, fp, &fgrid))) return rc;
   }
   Setup su;
   if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su))) return rc;
   int grid = 0;
-  if ((rc = occupancy_grid(k_ordered<VC, false>, su.big.lds_bytes, su.di.cus, &grid))) return rc;
+  if ((rc = occupancy_grid(k_ordered<VC, false, REORDER>, su.big.lds_bytes, su.di.cus, &grid)))
+    return rc;
   grid = (int)std::max<int64_t>(
       1, std::min<int64_t>(std::min(grid, su.mat_grid), (n + su.big.CPW - 1) / su.big.CPW));
   // group slots: the ring pass's and the full-row pass's share the same buffers (one at a time)
@@ -4312,23 +4526,45 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
     if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su, (int64_t)slots))) return rc;
   }
   OrdBufs ob;
-  ob.rcap = 2 * prob->v_max * prob->M;
+  ob.rcap = REORDER ? 0 : 2 * prob->v_max * prob->M;
   ob.pcap = (int)align_up((size_t)7 * prob->v_max * prob->M, 4);  // 16-byte aligned rows
+  // communication items: at most a receive and a send per F or B
+  ob.icap = REORDER ? 4 * prob->v_max * prob->M : 0;
+  const size_t nodes = (size_t)3 * prob->P * prob->v_max * prob->M;
   size_t o = 0;
-  const size_t o_tb = o;
-  o = align_up(o + slots * 3 * prob->P * prob->v_max * prob->M * 8, 256);
-  const size_t o_rk = o;
-  o = align_up(o + slots * prob->P * ob.rcap * 8, 256);
-  const size_t o_ri = o;
-  o = align_up(o + slots * prob->P * ob.rcap * 4, 256);
-  const size_t o_pg = o;
-  o = align_up(o + slots * prob->P * ob.pcap * 4, 256);
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  const size_t o_tb = take(slots * nodes * 8);
+  const size_t o_rk = take(slots * prob->P * ob.rcap * 8);
+  const size_t o_ri = take(slots * prob->P * ob.rcap * 4);
+  const size_t o_pg = take(slots * prob->P * ob.pcap * 4);
+  const size_t o_ts = take(REORDER ? slots * nodes * 8 : 0);
+  const size_t o_tl = take(REORDER ? slots * nodes * 4 : 0);
+  const size_t o_ik = take(slots * prob->P * ob.icap * 8);
+  const size_t o_il = take(slots * prob->P * ob.icap * 8);
+  const size_t o_ig = take(slots * prob->P * ob.icap * 4);
+  const size_t o_io = take(slots * prob->P * ob.icap * 8);
   if ((rc = ensure_buf(su.ws->ord, su.ws->ord_bytes, o, stream))) return rc;
   char* base = static_cast<char*>(su.ws->ord);
   ob.tb = reinterpret_cast<int64_t*>(base + o_tb);
   ob.rkey = reinterpret_cast<int64_t*>(base + o_rk);
   ob.rid = reinterpret_cast<uint32_t*>(base + o_ri);
   ob.prog = reinterpret_cast<uint32_t*>(base + o_pg);
+  ob.ts = reinterpret_cast<int64_t*>(base + o_ts);
+  ob.tl = reinterpret_cast<int32_t*>(base + o_tl);
+  ob.ikey = reinterpret_cast<int64_t*>(base + o_ik);
+  ob.iln = reinterpret_cast<uint64_t*>(base + o_il);
+  ob.igap = reinterpret_cast<int32_t*>(base + o_ig);
+  ob.iord = reinterpret_cast<int32_t*>(base + o_io);
+  ob.stats = stats;
+  if (stats) {  // sentinels for the invalid records, which no group takes
+    hipLaunchKernelGGL(k_fill_i64, dim3((unsigned)std::min<int64_t>(1024, (2 * n + 255) / 256)),
+                       dim3(256), 0, stream, stats, 2 * n, (int64_t)OCTO_MS_INVALID);
+    if ((rc = launch_ok())) return rc;
+  }
   SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub);
   // the valid records sorted by (v, generator, split), so that the groups of a wave have queues
   // and programs of one length (invalid ones get their sentinels here)
@@ -4338,27 +4574,27 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   if (rgrid > 0) {
     SimArgs ar = make_args(prob, rp, su, link, cands, n, ms, bub);
     ar.ring = rr.R;
-    hipLaunchKernelGGL((k_ordered<VC, true>), dim3(rgrid), dim3(WAVE), rp.lds_bytes, stream, ar,
-                       ob, list, list_n, fgrid > 0 ? 1 : 0);
+    hipLaunchKernelGGL((k_ordered<VC, true, REORDER>), dim3(rgrid), dim3(WAVE), rp.lds_bytes,
+                       stream, ar, ob, list, list_n, fgrid > 0 ? 1 : 0);
     if ((rc = launch_ok())) return rc;
     if (fgrid > 0) {
       SimArgs af = make_args(prob, fp, su, link, cands, n, ms, bub);
       af.ring = prob->M;
-      hipLaunchKernelGGL((k_ordered<VC, true>), dim3(fgrid), dim3(WAVE), fp.lds_bytes, stream, af,
-                         ob, a.wide, a.ctl + CTL_WIDE, 0);
+      hipLaunchKernelGGL((k_ordered<VC, true, REORDER>), dim3(fgrid), dim3(WAVE), fp.lds_bytes,
+                         stream, af, ob, a.wide, a.ctl + CTL_WIDE, 0);
       if ((rc = launch_ok())) return rc;
     }
     list = a.redo;
     list_n = a.ctl + CTL_REDO;
   }
-  hipLaunchKernelGGL((k_ordered<VC, false>), dim3(grid), dim3(WAVE), su.big.lds_bytes, stream, a,
-                     ob, list, list_n, 0);
+  hipLaunchKernelGGL((k_ordered<VC, false, REORDER>), dim3(grid), dim3(WAVE), su.big.lds_bytes,
+                     stream, a, ob, list, list_n, 0);
   return launch_ok();
 }
 
 int ordered_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                  const void* candidates, int64_t n, int64_t* out_makespan, int64_t* out_bubble,
-                 hipStream_t stream) {
+                 bool reorder, int64_t* out_stats, hipStream_t stream) {
   int rc = check_problem(prob);
   if (rc) return rc;
   if (n < 0 || n > (int64_t)INT32_MAX) return OCTO_EINVAL;
@@ -4366,10 +4602,15 @@ int ordered_impl(const octo_problem* prob, const int64_t* layer_costs, const int
   if (!layer_costs || !link || !candidates || !out_makespan || !out_bubble) return OCTO_EINVAL;
   if ((reinterpret_cast<uintptr_t>(candidates) & 15) != 0) return OCTO_EINVAL;
   std::lock_guard<std::mutex> lock(g_mu);
-  return prob->v_max <= 2 ? launch_ordered<2>(prob, layer_costs, link, candidates, n,
-                                              out_makespan, out_bubble, stream)
-                          : launch_ordered<8>(prob, layer_costs, link, candidates, n,
-                                              out_makespan, out_bubble, stream);
+  if (reorder)
+    return prob->v_max <= 2 ? launch_ordered<2, true>(prob, layer_costs, link, candidates, n,
+                                                      out_makespan, out_bubble, out_stats, stream)
+                            : launch_ordered<8, true>(prob, layer_costs, link, candidates, n,
+                                                      out_makespan, out_bubble, out_stats, stream);
+  return prob->v_max <= 2 ? launch_ordered<2, false>(prob, layer_costs, link, candidates, n,
+                                                     out_makespan, out_bubble, nullptr, stream)
+                          : launch_ordered<8, false>(prob, layer_costs, link, candidates, n,
+                                                     out_makespan, out_bubble, nullptr, stream);
 }
 
 }  // namespace
@@ -4440,8 +4681,16 @@ int octo_sim_batch_rdv(const octo_problem* prob, const int64_t* layer_costs, con
 int octo_sim_batch_ordered(const octo_problem* prob, const int64_t* layer_costs,
                            const int64_t* link, const void* candidates, int64_t n,
                            int64_t* out_makespan, int64_t* out_bubble, void* stream) {
-  return ordered_impl(prob, layer_costs, link, candidates, n, out_makespan, out_bubble,
-                      static_cast<hipStream_t>(stream));
+  return ordered_impl(prob, layer_costs, link, candidates, n, out_makespan, out_bubble, false,
+                      nullptr, static_cast<hipStream_t>(stream));
+}
+
+int octo_sim_batch_reorder(const octo_problem* prob, const int64_t* layer_costs,
+                           const int64_t* link, const void* candidates, int64_t n,
+                           int64_t* out_makespan, int64_t* out_bubble, int64_t* out_stats,
+                           void* stream) {
+  return ordered_impl(prob, layer_costs, link, candidates, n, out_makespan, out_bubble, true,
+                      out_stats, static_cast<hipStream_t>(stream));
 }
 
 int octo_sim_batch_bounds(const octo_problem* prob, const int64_t* layer_costs,

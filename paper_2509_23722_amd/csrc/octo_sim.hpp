@@ -212,7 +212,10 @@ struct Lane : Desc {
                       // (forward outputs of chunk k at k, backward outputs at VMAX + k)
   int64_t fs;         // start of the device's first op (-1 before it), bounds variants
   int64_t* tb;        // XT: finish time of every op, at (kind * tS + stage) * tM + m
-  int tS, tM;
+  int64_t* ts;        // XT (nullable, with tl): start time of every op, same index
+  int32_t* tl;        // XT: the round each op ran in — its level, the number of ops on the
+                      // longest dependency chain before it (queue order included)
+  int tS, tM, rnd;
 };
 
 template <int VMAX, typename T>
@@ -326,7 +329,12 @@ __device__ __forceinline__ bool relax_round(Gen& gen, const Chunks<VMAX>& c, con
     if constexpr (X == XC) L.cm.op(ok, L.cx, tin, L.w, L.clock, st, fin, L.cout);
     if constexpr (X == XB) L.fs = (ok && L.fs < 0) ? st : L.fs;
     if constexpr (X == XT) {
-      if (ok) L.tb[(gen.kind * L.tS + pick<VMAX>(c.st, gen.k)) * L.tM + gen.m] = fin;
+      const int nd = (gen.kind * L.tS + pick<VMAX>(c.st, gen.k)) * L.tM + gen.m;
+      if (ok) {
+        L.tb[nd] = fin;
+        if (L.tl) L.ts[nd] = st, L.tl[nd] = L.rnd;
+      }
+      L.rnd += 1;
     }
     L.clock = ok ? fin : L.clock;
     if constexpr (X == XM) {
@@ -583,6 +591,11 @@ __device__ __forceinline__ void relax_tab(const uint32_t* __restrict__ qt, uint3
   }
   const uint64_t actm = __ballot(cur != QT_END);
   if (actm != 0 && (fold_groups(actm, G, lsb) & gbit)) dead = true;
+}
+
+__device__ __forceinline__ int64_t group_sum(int64_t x, int G) {
+  for (int off = G >> 1; off > 0; off >>= 1) x += __shfl_xor(x, off, G);
+  return x;
 }
 
 __device__ __forceinline__ int64_t group_max(int64_t x, int G) {
