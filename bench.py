@@ -578,6 +578,18 @@ def main():
                "sample": "every 16th candidate of the batch", "deadlocked": int((o_np == -1).sum()),
                "mean_slowdown_vs_async": round(float((o_np / ms[::16].cpu().numpy()).mean()), 4)}
 
+    # the executor's three-step reordering with handshake transfers, on the same sample
+    rst = torch.empty((ns, 2), dtype=torch.int64, device=dev)
+    v_, t_, _ = time_variant(
+        torch, _lib, lambda: _lib.sim_batch_reorder(prob, costs, link, sub, oms, obub, rst), ns,
+        args.steps, args.warmup, kernels=False)
+    o_np, st_np = oms.cpu().numpy(), rst.cpu().numpy()
+    reorder = {"value": v_, "unit": "candidates/s", "ms_per_step": t_, "candidates": ns,
+               "sample": "every 16th candidate of the batch", "deadlocked": int((o_np == -1).sum()),
+               "mean_slowdown_vs_async": round(float((o_np / ms[::16].cpu().numpy()).mean()), 4),
+               "mean_transfers": round(float(st_np[:, 0].mean()), 1),
+               "mean_mismatched_receives": round(float(st_np[:, 1].mean()), 1)}
+
     w_advance = time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev,
                                args.warmup, min(args.steps, 3), not args.no_cpu)
     alg1 = time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, args.warmup,
@@ -624,6 +636,7 @@ def main():
         "serial_links": serial_links,
         "rendezvous": rendezvous,
         "ordered": ordered,
+        "reorder": reorder,
         "w_advance": w_advance,
         "alg1": alg1,
         "tuner": tuner,
