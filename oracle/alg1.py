@@ -15,7 +15,10 @@ One search per record, all independent. Each iteration (Algorithm 1's loop body)
    scheduling (the priority order of §6). A phase whose last search found nothing better is
    exhausted until some phase improves; an exhausted pick falls to the first non-exhausted
    phase in the order partitioning, placement, scheduling; with all three exhausted the search
-   has converged.
+   has converged. The random-search variant of §8 ("Pipeline Search Cost": the same iterative
+   framework, phases picked at random without regard to the bubbles) takes instead the
+   ``u mod n``-th of the n open phases (in that order), u the first word of
+   Philox4x64-10(counter = (record, iteration, 1, 0), key = (seed, 0)).
 3. ``argmin`` over the phase's neighbourhood (below): the first record, in neighbourhood order,
    of the smallest makespan among those that neither deadlock nor are invalid. It replaces the
    current record iff its makespan is strictly smaller; otherwise the phase is exhausted.
@@ -34,7 +37,19 @@ Neighbourhoods (§6 Partitioning / Placement / Scheduling Tuning):
   (stage k on the device of old stage k mod S), moves cleared.
 * scheduling — each other policy (moves cleared), then, if the record has a free move slot, every
   adjacent swap ``(d, i, i+1)`` appended as a move on the device with the largest residual bubble
-  (bubble minus its leading and trailing idle).
+  (bubble minus its leading and trailing idle), then that device's overlap-aware insertions
+  (§6 "Scheduling Tuning", the second policy), appended as moves ``(d, j, k)``.
+
+Overlap-aware insertion. On the current schedule (§5's times: every op's start and finish), for
+each position k >= 1 of device d's queue, with A = Q[k-1] and B = Q[k]: if the device idles
+between them (B starts after A finishes) and a communication there is not overlappable in §5's
+sense — A's output goes to another device and B does not run during that transfer
+[end A, end A + c], or B's input comes from another device and A does not run during that
+transfer — then the first later op Z = Q[j] (j > k) that is ready when A finishes (each of its
+producers finished, plus the transfer time for one on another device, by the end of A) moves to
+index k, between A and B, where it computes while the communication is in flight. Z cannot
+depend on the pending communication, nor on any op it moves ahead of (those start after A
+ends), so the move adds no cycle. One insertion per such position, in position order.
 """
 import numpy as np
 
@@ -86,8 +101,83 @@ def first_arg(x, largest):
     return best
 
 
-def neighbours(lay, rec, phase, L, M, busy, bub, resid):
-    """Records of the phase's neighbourhood, in order."""
+def stage_costs(c, costs, L):
+    """Per-stage forward, input-gradient and weight-gradient durations of record c."""
+    b = c["b"] + [L]
+    S = len(c["dev"])
+    return ([int(costs[b[s]:b[s + 1], k].sum()) for s in range(S)] for k in range(3))
+
+
+def producers(op, S):
+    """The ops whose outputs op takes (kind 0 F, 1 B, 2 W)."""
+    kind, s, m = op
+    if kind == 0:
+        return [(0, s - 1, m)] if s > 0 else []
+    if kind == 1:
+        return [(0, s, m)] + ([(1, s + 1, m)] if s < S - 1 else [])
+    return [(1, s, m)]
+
+
+def insertions(prob, costs, link, rec, lay, d):
+    """Overlap-aware insertions on device d of record rec: moves (d, j, k), in k order."""
+    c = lay.read(rec)
+    q = R.dump_queues(prob, rec)
+    if q is None:
+        return []
+    S, M = prob.P * c["v"], prob.M
+    split = c["policy"] == POL_ZB
+    F, B, W = stage_costs(c, costs, prob.L)
+    rc, _, _, start, _ = R.sim_queues(prob.P, S, M, split, c["dev"], F, B, W, link, q,
+                                      want_start=True)
+    if rc != 0:
+        return []
+    dev = c["dev"]
+    node = lambda op: (op[0] * S + op[1]) * M + op[2]
+    dur = lambda op: F[op[1]] if op[0] == 0 else (B[op[1]] + (0 if split else W[op[1]])
+                                                    if op[0] == 1 else W[op[1]])
+    st = lambda op: int(start[node(op)])
+    fin = lambda op: st(op) + dur(op)
+    w = lambda p, op: 0 if dev[p[1]] == dev[op[1]] else int(link[dev[p[1]]][dev[op[1]]])
+    ready = lambda op: max([fin(p) + w(p, op) for p in producers(op, S)], default=0)
+
+    def out_of(op):  # the consumer on another device and the transfer time, or None
+        kind, s, m = op
+        t = s + 1 if kind == 0 else s - 1 if kind == 1 else None
+        if t is None or t < 0 or t >= S or dev[t] == dev[s]:
+            return None
+        return int(link[dev[s]][dev[t]])
+
+    def into(op):  # the producer on another device and the transfer time, or None
+        for p in producers(op, S):
+            if dev[p[1]] != dev[op[1]]:
+                return p, int(link[dev[p[1]]][dev[op[1]]])
+        return None
+
+    def meets(op, lo, hi):  # op runs during [lo, hi] for a positive length
+        return min(fin(op), hi) - max(st(op), lo) > 0
+
+    Q = q[d]
+    out = []
+    for k in range(1, len(Q)):
+        A, Bo = Q[k - 1], Q[k]
+        if st(Bo) <= fin(A):
+            continue
+        co = out_of(A)
+        send_alone = co is not None and not meets(Bo, fin(A), fin(A) + co)
+        xi = into(Bo)
+        recv_alone = xi is not None and not meets(A, fin(xi[0]), fin(xi[0]) + xi[1])
+        if not (send_alone or recv_alone):
+            continue
+        for j in range(k + 1, len(Q)):
+            if ready(Q[j]) <= fin(A):
+                out.append((d, j, k))
+                break
+    return out
+
+
+def neighbours(lay, rec, phase, L, M, busy, bub, resid, ins=()):
+    """Records of the phase's neighbourhood, in order (ins: the scheduling phase's insertion
+    moves)."""
     c = lay.read(rec)
     P, S = lay.P, lay.P * c["v"]
     stages = [[s for s in range(S) if c["dev"][s] == d] for d in range(P)]
@@ -135,6 +225,8 @@ def neighbours(lay, rec, phase, L, M, busy, bub, resid):
             qlen = (3 if c["policy"] == POL_ZB else 2) * c["v"] * M
             for i in range(qlen - 1):
                 out.append(lay.write(dict(c, pert=c["pert"] + [(d, i, i + 1)]), rec))
+            for mv in ins:
+                out.append(lay.write(dict(c, pert=c["pert"] + [mv]), rec))
     return out
 
 
@@ -147,6 +239,16 @@ def choose_phase(delta_b, t_layer, b_bd, b_res, exhausted):
     return next((p for p in range(3) if p not in exhausted), None)
 
 
+def random_phase(record, iteration, seed, exhausted):
+    """The random-search variant's pick: the (u mod n)-th of the n open phases; None: all
+    exhausted."""
+    open_ = [p for p in range(3) if p not in exhausted]
+    if not open_:
+        return None
+    u = R.philox4x64_10([record, iteration, 1, 0], [seed, 0])[0]
+    return open_[u % len(open_)]
+
+
 def bubble_split(ms, bub, bounds):
     """(Δb, b_bd, b_res, busy per device, residual bubble per device) of one evaluation."""
     P = len(bub)
@@ -157,11 +259,15 @@ def bubble_split(ms, bub, bounds):
     return max(bub) - min(bub), b_bd, sum(bub) - b_bd, busy, resid
 
 
-def tune(prob, costs, link, recs, iters, nthreads=1, trace=None):
+def tune(prob, costs, link, recs, iters, nthreads=1, trace=None, random_search=False, seed=0,
+         insert=True, phase_iters=None):
     """Run `iters` iterations of Algorithm 1 on every record. Returns (final records, makespan,
     bubbles, accepted moves per phase [n, 3], iterations that searched a phase [n] — the rest
     idle after convergence). trace (a list, optional) receives per record a list of
-    (phase, kept, makespan after) per searching iteration."""
+    (phase, kept, makespan after) per searching iteration. random_search: the phase is drawn at
+    random (seed) instead of by the bubbles; insert: the scheduling phase includes the
+    overlap-aware insertions; phase_iters (an [n, 3] array, optional) receives the iterations
+    that searched each phase."""
     lay = Layout(prob.P, prob.v_max, prob.max_pert, prob.cand_stride)
     costs = np.asarray(costs, dtype=np.int64)
     t_layer = prob.M * int(costs.sum(axis=1).min())
@@ -172,17 +278,25 @@ def tune(prob, costs, link, recs, iters, nthreads=1, trace=None):
     for i in range(n):
         exhausted = set()
         steps = []
-        for _ in range(iters):
+        for it in range(iters):
             ms, bub, bounds = R.sim_batch_bounds(prob, costs, link, recs[i:i + 1])
             ms, bub, bounds = int(ms[0]), [int(x) for x in bub[0]], bounds[0]
             if ms < 0:
                 break
             delta_b, b_bd, b_res, busy, resid = bubble_split(ms, bub, bounds)
-            phase = choose_phase(delta_b, t_layer, b_bd, b_res, exhausted)
+            if random_search:
+                phase = random_phase(i, it, seed, exhausted)
+            else:
+                phase = choose_phase(delta_b, t_layer, b_bd, b_res, exhausted)
             if phase is None:
                 break
             used[i] += 1
-            nb = neighbours(lay, recs[i], phase, prob.L, prob.M, busy, bub, resid)
+            if phase_iters is not None:
+                phase_iters[i, phase] += 1
+            ins = ()
+            if phase == 2 and insert and lay.read(recs[i])["n_pert"] < lay.max_pert:
+                ins = insertions(prob, costs, link, recs[i], lay, first_arg(resid, True))
+            nb = neighbours(lay, recs[i], phase, prob.L, prob.M, busy, bub, resid, ins)
             best = None
             if nb:
                 nms, _ = R.sim_batch(prob, costs, link, np.array(nb), nthreads=nthreads)

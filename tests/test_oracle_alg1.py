@@ -117,3 +117,125 @@ def test_search_properties():
                     nms, _ = R.sim_batch(prob, costs, link, np.array(nb))
                     assert not ((nms >= 0) & (nms < m1[0])).any()
     assert (used < iters).sum() >= 3
+
+
+def _insertion_example():
+    from conftest import read_golden
+    kv, _ = read_golden("overlap_insertion_example.txt")
+    T = int(kv["T_ns"])
+    recs = I.pack_records(2, 1, 2, [I.POLICY["ZB"]], [1], [[1]], [[0, 1]])
+    prob = R.problem(2, 2, 1, 3, recs.shape[1], 2)
+    costs = np.array([[1, 4, 1], [2, 4, 2]], np.int64) * T
+    link = I.link_matrix(2, int(kv["transfer_T"]) * T)
+    return kv, T, recs, prob, costs, link
+
+
+def test_overlap_insertion_worked_example():
+    """§6's overlap-aware insertion on a hand-worked timeline: the one insertion of device 0
+    (the device with the larger residual bubble), and the makespan after it."""
+    kv, T, recs, prob, costs, link = _insertion_example()
+    lay = A.Layout(prob.P, prob.v_max, prob.max_pert, prob.cand_stride)
+    ms, bub, bounds = R.sim_batch_bounds(prob, costs, link, recs)
+    assert ms[0] == int(kv["before_makespan_T"]) * T
+    resid = A.bubble_split(int(ms[0]), bub[0].tolist(), bounds[0])[4]
+    assert A.first_arg(resid, True) == int(kv["device"])
+    ins = A.insertions(prob, costs, link, recs[0], lay, 0)
+    assert ins == [tuple(int(x) for x in kv["insertion"].split())]
+    assert A.insertions(prob, costs, link, recs[0], lay, 1) == \
+        [tuple(int(x) for x in kv["device1_insertion"].split())]
+    nb = lay.write(dict(lay.read(recs[0]), pert=list(ins)), recs[0])
+    assert R.sim_batch(prob, costs, link, nb[None])[0][0] == int(kv["after_makespan_T"]) * T
+
+
+def test_scheduling_phase_takes_the_insertion():
+    """On that record Algorithm 1 searches the scheduling phase; no other policy nor adjacent
+    swap reaches 30T, so the kept move is the insertion; without insertions the phase keeps the
+    adjacent swap at 31T."""
+    kv, T, recs, prob, costs, link = _insertion_example()
+    lay = A.Layout(prob.P, prob.v_max, prob.max_pert, prob.cand_stride)
+    trace = []
+    out, ms, _, acc, _ = A.tune(prob, costs, link, recs, 1, trace=trace)
+    assert trace[0] == [(2, True, int(kv["after_makespan_T"]) * T)]
+    assert lay.read(out[0])["pert"] == [tuple(int(x) for x in kv["insertion"].split())]
+    trace = []
+    out0, ms0, _, _, _ = A.tune(prob, costs, link, recs, 1, insert=False, trace=trace)
+    assert trace[0] == [(2, True, int(kv["without_insertion_T"]) * T)]
+    assert lay.read(out0[0])["pert"] == [tuple(int(x) for x in
+                                               kv["without_insertion_move"].split())]
+
+
+def test_insertions_follow_their_rule_on_random_records():
+    """Every insertion the oracle proposes, re-derived from the timeline by the rule's
+    definition (idle before B, a communication not overlappable, the first later op ready when
+    A ends), and no neighbour built from one deadlocks."""
+    rng = np.random.default_rng(61)
+    found = 0
+    for trial in range(40):
+        P, v_max, M = int(rng.integers(2, 5)), int(rng.integers(1, 3)), int(rng.integers(2, 6))
+        L = P * v_max + 2
+        recs = I.random_candidates(rng, L, P, v_max, M, 6, max_pert=2, pert_rate=0.3)
+        prob = R.problem(L, P, v_max, M, recs.shape[1], 2)
+        lay = A.Layout(P, v_max, 2, prob.cand_stride)
+        costs = rng.integers(1, 6, size=(L, 3)).astype(np.int64)
+        link = rng.integers(0, 8, size=(P, P)).astype(np.int64)
+        for r in recs:
+            c = lay.read(r)
+            q = R.dump_queues(prob, r)
+            if q is None or c["n_pert"] >= 2:
+                continue
+            S = P * c["v"]
+            split = c["policy"] == A.POL_ZB
+            F, B, W = A.stage_costs(c, costs, L)
+            rc, _, _, start, _ = R.sim_queues(P, S, M, split, c["dev"], F, B, W, link, q, True)
+            if rc != 0:
+                continue
+            node = lambda op: (op[0] * S + op[1]) * M + op[2]
+            dur = lambda op: [F, [B[s] + (0 if split else W[s]) for s in range(S)], W][op[0]][op[1]]
+            st = lambda op: int(start[node(op)])
+            fin = lambda op: st(op) + dur(op)
+            for d in range(P):
+                ins = A.insertions(prob, costs, link, r, lay, d)
+                Q = q[d]
+                for (dd, j, k) in ins:
+                    assert dd == d and j > k >= 1 and st(Q[k]) > fin(Q[k - 1])
+                    for jj in range(k + 1, j):   # no earlier op was ready
+                        rdy = max([fin(p) + (0 if c["dev"][p[1]] == d else
+                                             int(link[c["dev"][p[1]]][d]))
+                                   for p in A.producers(Q[jj], S)], default=0)
+                        assert rdy > fin(Q[k - 1])
+                if ins:
+                    nbs = np.array([lay.write(dict(c, pert=c["pert"] + [mv]), r) for mv in ins])
+                    assert (R.sim_batch(prob, costs, link, nbs)[0] > 0).all()
+                    found += len(ins)
+    assert found > 20
+
+
+def test_random_phase_follows_philox():
+    """The random-search variant: each searched iteration's phase is the (u mod n)-th open phase,
+    u from Philox4x64-10 at counter (record, iteration, 1, 0) and key (seed, 0), computed here
+    with numpy's own Philox; the per-phase iteration counts add up."""
+    rng = np.random.default_rng(62)
+    P, v_max, M, L = 4, 2, 4, 12
+    recs = I.random_candidates(rng, L, P, v_max, M, 6, max_pert=2, pert_rate=0.0,
+                               policies=(I.POLICY["1F1B"], I.POLICY["ZB"]))
+    prob = R.problem(L, P, v_max, M, recs.shape[1], 2)
+    costs = rng.integers(1, 6, size=(L, 3)).astype(np.int64) * 1000
+    link = I.link_matrix(P, 700)
+    seed = 777
+    trace = []
+    pit = np.zeros((len(recs), 3), np.int64)
+    _, _, _, acc, used = A.tune(prob, costs, link, recs, 12, trace=trace, random_search=True,
+                                seed=seed, phase_iters=pit)
+    for i, steps in enumerate(trace):
+        exhausted = set()
+        for it, (phase, kept, _) in enumerate(steps):
+            open_ = [p for p in range(3) if p not in exhausted]
+            ctr = [i, it, 1, 0]
+            bg = np.random.Philox(key=np.array([seed, 0], dtype=np.uint64),
+                                  counter=np.array([ctr[0] - 1 if i else 2**64 - 1,
+                                                    it if i else it - 1 if it else 2**64 - 1,
+                                                    1 if (i or it) else 0, 0], dtype=np.uint64))
+            u = int(bg.random_raw(1)[0])
+            assert phase == open_[u % len(open_)], (i, it)
+            exhausted = set() if kept else exhausted | {phase}
+        assert pit[i].sum() == used[i] == len(steps)
