@@ -216,10 +216,12 @@ def time_w_advance(torch, _lib, inputs, w, costs, link, mem, recs_np, dev, warmu
 
 
 def time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, warmup, steps, with_cpu):
-    """Algorithm 1 (octo_alg1_tune) on 4,096 records of the batch (every 256th), widened to four
-    move slots, 32 iterations per call; the unit of work is one iteration of one record's search
-    (phase choice, its whole neighbourhood evaluated, best kept)."""
-    from oracle import alg1 as A
+    """Algorithm 1 (octo_alg1_tune: bubble-aware phases, overlap-aware insertions in the
+    scheduling phase) on 4,096 records of the batch (every 256th), widened to four move slots,
+    32 iterations per call; the unit of work is one iteration of one record's search (phase
+    choice, its whole neighbourhood evaluated, best kept). Beside it, the random-search variant
+    (octo_alg1_tune_ex with random phases, the same insertions) on the same records: rate,
+    gain, and the iterations each variant gave each phase."""
     n, iters, mp = 4096, 32, 4
     base = recs_np[::len(recs_np) // n][:n]
     stride = inputs.record_stride(w.P, w.v_max, mp)
@@ -249,7 +251,29 @@ def time_alg1(torch, _lib, inputs, w, costs, link, recs_np, dev, warmup, steps, 
                           "schedule": int(stats[:, 2].sum())},
            "mean_makespan_gain": round(float(1 - (o_ms[ok] / ms0[ok]).mean()), 4),
            "cpu_baseline": None}
+    # the phase iterations of the bubble-aware search, then the random-search variant
+    flags = _lib.A1_INSERT
+    r.copy_(r0)
+    pit = _lib.alg1_tune_ex(prob, costs, link, r, iters, flags)[3].cpu().numpy()
+    out["phase_iterations"] = {k: int(x) for k, x in zip(("partition", "placement", "schedule"), pit.sum(axis=0))}
+    for _ in range(max(warmup, 1)):
+        r.copy_(r0)
+        rres = _lib.alg1_tune_ex(prob, costs, link, r, iters, flags | _lib.A1_RANDOM, 20250929)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r.copy_(r0)
+        rres = _lib.alg1_tune_ex(prob, costs, link, r, iters, flags | _lib.A1_RANDOM, 20250929)
+    torch.cuda.synchronize()
+    rsecs = (time.perf_counter() - t0) / steps
+    r_ms, r_pit = rres[0].cpu().numpy(), rres[3].cpu().numpy()
+    out["random_phases"] = {
+        "value": round(n * iters / rsecs, 1), "unit": "record-iterations/s",
+        "ms_per_call": round(rsecs * 1e3, 3), "seed": 20250929,
+        "mean_makespan_gain": round(float(1 - (r_ms[ok] / ms0[ok]).mean()), 4),
+        "phase_iterations": {k: int(x) for k, x in zip(("partition", "placement", "schedule"), r_pit.sum(axis=0))}}
     if with_cpu:
+        from oracle import alg1 as A
         from oracle import octoref
         sample = np.arange(0, n, 256)
         threads = min(16, os.cpu_count() or 1)

@@ -358,7 +358,8 @@ int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
  *        of old stage k mod S, v doubled, moves cleared;
  *      scheduling — each other policy, moves cleared; then, if n_pert < max_pert, every
  *        adjacent swap {d, i, i+1} of the device d with the largest residual bubble (bubble
- *        minus leading and trailing idle), appended as a move.
+ *        minus leading and trailing idle), appended as a move, then d's overlap-aware
+ *        insertions (octo_alg1_tune_ex, OCTO_A1_INSERT).
  *      Reserved boundary and placement bytes read as 0 in every neighbour; other bytes copy.
  *   4. The neighbour with the smallest makespan among those that neither deadlock nor are
  *      invalid (the first on ties) replaces the record iff its makespan is strictly smaller;
@@ -369,12 +370,39 @@ int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
  *   out_stats     int64 [n][4]: moves kept in the partitioning, placement and scheduling
  *                 phases, and the iterations in which a phase was searched.
  * The library evaluates each iteration's neighbours as one batch in its workspace, at most
- * n * max(v_max^2, (P-1) v_max^2 + 1, 3 v_max M + 2) records (OCTO_EINVAL above 2^31 - 1;
+ * n * max(v_max^2, (P-1) v_max^2 + 1, 6 v_max M + 1) records (OCTO_EINVAL above 2^31 - 1;
  * OCTO_ENOMEM if it cannot be allocated). Returns OCTO_OK or a negative status.
  */
 int octo_alg1_tune(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    void* records, int64_t n, int32_t iters, int64_t* out_makespan,
                    int64_t* out_bubble, int64_t* out_stats, void* stream);
+
+/*
+ * octo_alg1_tune_ex — octo_alg1_tune with its options. flags:
+ *   OCTO_A1_INSERT  the scheduling phase also tries the overlap-aware insertions (§6 "Scheduling
+ *                   Tuning", the second policy), after the adjacent swaps, as moves {d, j, k} of
+ *                   the same device d: on d's current schedule, at each position k >= 1 where d
+ *                   idles between A = Q[k-1] and B = Q[k] and a communication there is not
+ *                   overlappable in §5's sense (A's output goes to another device and B does not
+ *                   run during that transfer, or B's input comes from another device and A does
+ *                   not run during it), the first later op Q[j] ready when A ends (its
+ *                   producers' ends plus the transfer time across devices) moves to index k.
+ *                   octo_alg1_tune sets this flag.
+ *   OCTO_A1_RANDOM  the random-search variant of §8 ("Pipeline Search Cost"): each iteration's
+ *                   phase is the (u mod n)-th of the n open phases (partitioning, placement,
+ *                   scheduling), u the first word of Philox4x64-10(counter (record index,
+ *                   iteration, 1, 0), key (seed, 0)), instead of the bubble-aware branch.
+ *   other bits: OCTO_EINVAL.
+ * out_phase_iters (device int64 [n][3], nullable): the iterations that searched each phase.
+ * The neighbour batch holds at most n * max(v_max^2, (P-1) v_max^2 + 1, 6 v_max M + 1) records.
+ * Other arguments, results and status as octo_alg1_tune.
+ */
+#define OCTO_A1_INSERT 1
+#define OCTO_A1_RANDOM 2
+int octo_alg1_tune_ex(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                      void* records, int64_t n, int32_t iters, int32_t flags, uint64_t seed,
+                      int64_t* out_makespan, int64_t* out_bubble, int64_t* out_stats,
+                      int64_t* out_phase_iters, void* stream);
 
 /*
  * Measurement hook. events[0..n_events-1] are hipEvent_t handles (n_events <= 8; entries may be

@@ -61,6 +61,8 @@ def lib():
         L.octo_advance_w.argtypes = [pp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
         L.octo_tune_step.restype = ctypes.c_int
         L.octo_alg1_tune.argtypes = [pp, vp, vp, vp, i64, i32, vp, vp, vp, vp]
+        L.octo_alg1_tune_ex.argtypes = [pp, vp, vp, vp, i64, i32, i32, ctypes.c_uint64, vp, vp,
+                                        vp, vp, vp]
         L.octo_alg1_tune.restype = ctypes.c_int
         L.octo_profile_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), i32]
         L.octo_profile_events.restype = ctypes.c_int
@@ -363,6 +365,35 @@ def alg1_tune(prob, layer_costs, link, records, iters, out_makespan=None, out_bu
         _dev_ptr(out_stats, torch.int64, "out_stats"), _stream(records, stream))
     _check(rc, "octo_alg1_tune")
     return out_makespan, out_bubble, out_stats
+
+
+A1_INSERT, A1_RANDOM = 1, 2
+
+
+def alg1_tune_ex(prob, layer_costs, link, records, iters, flags, seed=0, out_makespan=None,
+                 out_bubble=None, out_stats=None, out_phase_iters=None, stream=None):
+    """octo_alg1_tune_ex: alg1_tune with flags (A1_INSERT: overlap-aware insertions in the
+    scheduling phase; A1_RANDOM: phases drawn at random with `seed`). Returns (makespan,
+    bubble, stats [n, 4], phase iterations [n, 3])."""
+    n = records.shape[0]
+    dev = records.device
+    if out_makespan is None:
+        out_makespan = torch.empty(n, dtype=torch.int64, device=dev)
+    if out_bubble is None:
+        out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
+    if out_stats is None:
+        out_stats = torch.empty((n, 4), dtype=torch.int64, device=dev)
+    if out_phase_iters is None:
+        out_phase_iters = torch.empty((n, 3), dtype=torch.int64, device=dev)
+    rc = lib().octo_alg1_tune_ex(
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
+        _dev_ptr(link, torch.int64, "link"), _dev_ptr(records, torch.uint8, "records"), n,
+        int(iters), int(flags), int(seed), _dev_ptr(out_makespan, torch.int64, "out_makespan"),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
+        _dev_ptr(out_stats, torch.int64, "out_stats"),
+        _dev_ptr(out_phase_iters, torch.int64, "out_phase_iters"), _stream(records, stream))
+    _check(rc, "octo_alg1_tune_ex")
+    return out_makespan, out_bubble, out_stats, out_phase_iters
 
 
 def profile_events(events):

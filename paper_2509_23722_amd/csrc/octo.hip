@@ -3056,9 +3056,13 @@ __global__ void __launch_bounds__(WAVE) k_tune_ring(TuneArgs t) {
 
 // Search state per record (int32 words): the phase searched this iteration, flags (bits 0..2:
 // phases whose last search found nothing better; A1_OVER: the search has ended), the first
-// neighbour's position in the batch and the neighbour count.
-constexpr int A1_PHASE = 0, A1_FLAGS = 1, A1_BASE = 2, A1_CNT = 3, A1_WORDS = 4;
+// neighbour's position in the batch and the neighbour count; for the insertions: the first
+// placeholder's position, their number and the device searched.
+constexpr int A1_PHASE = 0, A1_FLAGS = 1, A1_BASE = 2, A1_CNT = 3, A1_INSB = 4, A1_NINS = 5,
+              A1_DR = 6, A1_WORDS = 8;
 constexpr int A1_OVER = 8;
+// Search options (octo_alg1_tune_ex flags)
+constexpr int A1F_INSERT = 1, A1F_RANDOM = 2;
 constexpr int A1_REC_MAX = 1664;  // largest record stride (S_max = 64, 255 moves)
 
 struct A1Args {
@@ -3071,6 +3075,12 @@ struct A1Args {
   int64_t* bnd;            // [n][P][2] current first start, last finish
   int32_t* st;             // [n][A1_WORDS]
   int64_t* stats;          // [n][4] kept moves per phase, iterations that searched
+  int64_t* pit;            // [n][3] (nullable): iterations that searched each phase
+  int flags;               // A1F_*
+  uint64_t seed;           // random phases: Philox key (seed, 0)
+  int iter;                // this iteration (random phases: Philox counter word 1)
+  int32_t* ins_list;       // records whose insertions k_alg1_insert finds this iteration ...
+  int32_t* ins_n;          // ... and their count
   uint8_t* nb_rec;         // neighbour records of this iteration, compacted
   const int64_t* nb_ms;    // [batch] their makespan
   const int64_t* nb_bub;   // [batch][P]
@@ -3107,17 +3117,22 @@ __device__ __forceinline__ int wave_argmax64(int64_t x) {
   return i;
 }
 
-__global__ void k_alg1_init(int32_t* __restrict__ st, int64_t* __restrict__ stats, int64_t n) {
+__global__ void k_alg1_init(int32_t* __restrict__ st, int64_t* __restrict__ stats,
+                            int64_t* __restrict__ pit, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     for (int k = 0; k < A1_WORDS; ++k) st[i * A1_WORDS + k] = 0;
     for (int k = 0; k < 4; ++k) stats[i * 4 + k] = 0;
+    if (pit)
+      for (int k = 0; k < 3; ++k) pit[i * 3 + k] = 0;
   }
 }
 
 // One neighbour as byte edits of the current record: edited spans [lo, hi) and what goes there.
 struct A1Edit {
-  int kind;  // 0 layer migration, 1 stage exchange, 2 stage dispersion, 3 policy, 4 op swap
+  int kind;  // 0 layer migration, 1 stage exchange, 2 stage dispersion, 3 policy, 4 op swap,
+             // 5 insertion placeholder (the record with its flags byte set: invalid until
+             //   k_alg1_insert writes a move into it)
   int x, y;  // 0: boundaries x+1..y shift by -1 (x < y) or x+1..y by +1 (swapped: y < x holds
              //    the lower stage); 1: stages x, y; 3: new policy; 4: device x, position y
   int lo1, hi1, lo2, hi2;
@@ -3150,6 +3165,8 @@ __device__ __forceinline__ uint32_t a1_byte(const A1Edit& e, const uint8_t* rec,
     }
     case 3:
       return p == 0 ? (uint32_t)e.x : p == 2 ? 0u : rec[p];
+    case 5:
+      return 1u;  // the flags byte
     default: {
       if (p == 2) return (uint32_t)(rec[2] + 1);
       const int q = p - (po + 6 * rec[2]);  // the appended move {device, from, to}, u16 LE
@@ -3169,7 +3186,11 @@ __device__ __forceinline__ uint32_t a1_byte(const A1Edit& e, const uint8_t* rec,
 //    and every stage has two layers, every stage splits at its middle layer and the 2S stages
 //    go round the old devices (new stage k on the device of old stage k mod S), moves cleared;
 //  2 scheduling: each other policy (moves cleared); then, with a move slot free, each adjacent
-//    swap of the device with the largest bubble between its first and last op, as a move.
+//    swap of the device with the largest bubble between its first and last op, as a move; then
+//    (A1F_INSERT) as many placeholders as that device can have overlap-aware insertions, which
+//    k_alg1_insert fills.
+// The phase: Algorithm 1's branch, or (A1F_RANDOM) the (u mod n)-th of the n open phases, u the
+// first word of Philox4x64-10(counter (record, iteration, 1, 0), key (seed, 0)).
 __global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
   __shared__ __align__(16) uint8_t rec[A1_REC_MAX];
   __shared__ uint8_t sd[64];     // stages of device d at sd[d v ..], ascending
@@ -3203,7 +3224,20 @@ __global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
     const int64_t b_res = wave_sum64(dv ? bub : 0) - b_bd;
     const int pref = delta > tl ? 0 : b_bd > b_res ? 1 : 2;
     const int ex = flags & 7;
-    const int phase = !((ex >> pref) & 1) ? pref : !(ex & 1) ? 0 : !(ex & 2) ? 1 : !(ex & 4) ? 2 : -1;
+    int phase = !((ex >> pref) & 1) ? pref : !(ex & 1) ? 0 : !(ex & 2) ? 1 : !(ex & 4) ? 2 : -1;
+    if (a.flags & A1F_RANDOM) {
+      const int open = ~ex & 7, nopen = __popc(open);
+      phase = -1;
+      if (nopen > 0) {
+        const U4 u = philox4x64_10((uint64_t)i, (uint64_t)a.iter, 1, 0, a.seed, 0);
+        int r = (int)(u.x[0] % (uint64_t)nopen);
+        for (int p = 0; p < 3; ++p) {
+          const bool o = (open >> p) & 1;
+          if (o && r == 0 && phase < 0) phase = p;
+          r -= o && phase < 0 ? 1 : 0;
+        }
+      }
+    }
     if (phase < 0) {  // every phase exhausted: converged
       if (lane == 0) st[A1_FLAGS] = flags | A1_OVER, st[A1_CNT] = 0;
       continue;
@@ -3243,15 +3277,19 @@ __global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
       const bool thin = lane < S && bnd(lane + 1) - bnd(lane) < 2;
       const bool disp = 2 * v <= a.pr.v_max && __ballot(thin) == 0;
       cnt = (P - 1) * v * v + (disp ? 1 : 0);
-    } else {
-      const int qlen = (policy == POL_ZB ? 3 : 2) * v * M;
-      cnt = 3 + (np < a.pr.max_pert ? qlen - 1 : 0);
     }
+    const int qlen = (policy == POL_ZB ? 3 : 2) * v * M;
+    const int nswap = phase == 2 && np < a.pr.max_pert ? qlen - 1 : 0;
+    const int nins = phase == 2 && np < a.pr.max_pert && (a.flags & A1F_INSERT) ? qlen - 1 : 0;
+    if (phase == 2) cnt = 3 + nswap + nins;
     int base = 0;
     if (lane == 0) {
       base = atomicAdd(a.total, cnt);
       st[A1_PHASE] = phase, st[A1_BASE] = base, st[A1_CNT] = cnt;
+      st[A1_INSB] = base + 3 + nswap, st[A1_NINS] = nins, st[A1_DR] = dr;
       a.stats[i * 4 + 3] += 1;
+      if (a.pit) a.pit[i * 3 + phase] += 1;
+      if (nins > 0) a.ins_list[atomicAdd(a.ins_n, 1)] = (int32_t)i;
     }
     base = __shfl(base, 0);
     __syncthreads();
@@ -3281,11 +3319,14 @@ __global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
         e.kind = 3;
         e.x = j < policy ? j : j + 1;
         e.lo1 = 0, e.hi1 = 3;
-      } else {
+      } else if (j < 3 + nswap) {
         e.kind = 4;
         e.x = dr, e.y = j - 3;
         e.lo1 = 2, e.hi1 = 3;
         e.lo2 = po + 6 * np, e.hi2 = e.lo2 + 6;
+      } else {
+        e.kind = 5;
+        e.lo1 = 3, e.hi1 = 4;
       }
       uint4* dst = reinterpret_cast<uint4*>(a.nb_rec + (int64_t)(base + j) * stride);
       for (int q = 0; q < stride / 16; ++q) {
@@ -3307,6 +3348,140 @@ __global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
       }
     }
     __syncthreads();
+  }
+}
+
+// Overlap-aware insertions (§6 "Scheduling Tuning", the second policy) of the records on
+// b.ins_list, written into the placeholders k_alg1_expand reserved. One group per record
+// (64-bit finish tables), lane = device: the record's queues with its moves, the asynchronous
+// rounds recording every op's start and finish, then the lane of the searched device walks its
+// queue: at each position k >= 1 with A = Q[k-1], B = Q[k], if the device idles between them and
+// A's output goes to another device while B does not run during that transfer [end A,
+// end A + c], or B's input comes from another device while A does not run during that transfer
+// (§5: a node overlaps when a computation runs beside it for a positive time), the first later
+// op Z = Q[j] that is ready when A ends (each producer's end, plus the transfer time across
+// devices) becomes the move (device, j, k) of the next placeholder (flags byte cleared, one
+// more move). Placeholders left over stay invalid.
+template <int VMAX>
+__global__ void __launch_bounds__(WAVE) k_alg1_insert(SimArgs a, A1Args b,
+                                                      int64_t* __restrict__ tbuf) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int G = a.G, P = a.pr.P, M = a.pr.M;
+  const int g = lane_id() / G;
+  const int d = lane_id() % G;
+  uint8_t* lds_group = smem + (size_t)(g < a.CPW ? g : 0) * a.group_bytes;
+  const auto T = group_table<false>(lds_group, a.slots);
+  uint8_t* rec = lds_group + a.table_bytes;
+  const int slot = (int)blockIdx.x * a.CPW + (g < a.CPW ? g : 0);
+  const int dl = d < P ? d : 0;
+  uint16_t* row = a.qscratch + ((size_t)slot * P + dl) * a.qcap;
+  const size_t nodes = (size_t)3 * a.pr.s_max * M;
+  int64_t* tb = tbuf + (size_t)slot * 2 * nodes;  // finish times, then start times
+  int64_t* ts = tb + nodes;
+  uint64_t gbit, lsb;
+  group_bits(G, &gbit, &lsb);
+  const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
+  const int64_t total = *b.ins_n;
+  const Ring ring = make_ring(M, M);
+  const int po = pert_off(a.pr.s_max);
+  for (int64_t base = (int64_t)blockIdx.x * a.CPW; base < total; base += n_groups) {
+    const bool has = g < a.CPW && base + g < total;
+    const int64_t i = has ? (int64_t)b.ins_list[base + g] : 0;
+    const uint8_t* grec = b.recs + i * a.pr.stride;
+    if (has) stage_record(rec, grec, a.rec_bytes, d, G);
+    __syncthreads();
+    Resolved r;
+    r.valid = 0, r.v = 1, r.split = 0, r.gen = GEN_AFAB, r.n_pert = 0;
+    if (has) r = resolve_record(a.pr, grec);
+    const bool valid = has && r.valid;
+    const int v = valid ? r.v : 1;
+    const int S = P * v;
+    Chunks<VMAX> c;
+    Lane L;
+    L.clock = 0, L.pos = 0, L.nops = 0, L.mem = L.peak = 0;
+    L.cm.reset();
+    L.fs = -1;
+    L.tb = tb, L.ts = ts, L.tl = nullptr, L.tS = S, L.tM = M, L.rnd = 0;
+    if (valid && d < P) {
+      (void)setup_chunks<VMAX>(c, a.pr, rec, a.pre, a.link, d, v, r.split, ring, nullptr,
+                               nullptr, XR);
+      L.nops = materialise<VMAX>(a, c, v, r.gen, r.split, row);
+      const uint8_t* pp = grec + po;
+      for (int q = 0; q < r.n_pert; ++q) {
+        const int pd = pp[6 * q] | (pp[6 * q + 1] << 8);
+        if (pd != d) continue;
+        move_entry(row, pp[6 * q + 2] | (pp[6 * q + 3] << 8), pp[6 * q + 4] | (pp[6 * q + 5] << 8));
+      }
+    } else {
+      zero_chunks<VMAX>(c);
+    }
+    const bool mine = valid && d < P;
+    if (!mine) L.nops = 0;
+    if (valid) T.clear(S * M, d, G);
+    __syncthreads();
+    bool dead = false;
+    rounds_mat<VMAX, XT>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
+    __syncthreads();  // every lane's times visible to the group
+    const int32_t* st = b.st + i * A1_WORDS;
+    if (mine && !dead && d == st[A1_DR]) {
+      const int nq = L.nops, insb = st[A1_INSB], nins = st[A1_NINS], np = rec[2];
+      auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
+      RowCursor ca, cz;
+      ca.init(row, nq);
+      cz.init(row, nq);
+      int found = 0;
+      for (int k = 1; k < nq && found < nins; ++k) {
+        const uint32_t ea = ca.at(k - 1), eb = ca.at(k);
+        const int kindA = (ea >> 14) & 3, kA = (ea >> 11) & 7, mA = ea & 0x7FF;
+        const int kindB = (eb >> 14) & 3, kB = (eb >> 11) & 7, mB = eb & 0x7FF;
+        const int sA = pick<VMAX>(c.st, kA), sB = pick<VMAX>(c.st, kB);
+        const int64_t finA = tb[node(kindA, sA, mA)], stA = ts[node(kindA, sA, mA)];
+        const int64_t finB = tb[node(kindB, sB, mB)], stB = ts[node(kindB, sB, mB)];
+        if (stB <= finA) continue;
+        const int cxA = kindA == KF ? pick<VMAX>(c.xF, kA) : kindA == KB ? pick<VMAX>(c.xB, kA) : 0;
+        const int cxB = kindB == KF ? pick<VMAX>(c.xF, kB) : kindB == KB ? pick<VMAX>(c.xB, kB) : 0;
+        bool alone = false;
+        if (cxA & CX_OUT) {  // A's output in flight over [finA, finA + c]; does B run then?
+          const int64_t hi = finA + (kindA == KF ? pick<VMAX>(c.cF, kA) : pick<VMAX>(c.cB, kA));
+          alone = alone || (finB < hi ? finB : hi) - (stB > finA ? stB : finA) <= 0;
+        }
+        if (cxB & CX_IN) {  // B's input in flight from its producer's end; does A run then?
+          const int64_t fx = tb[node(kindB, kindB == KF ? sB - 1 : sB + 1, mB)];
+          const int64_t hi = fx + (kindB == KF ? pick<VMAX>(c.wF, kB) : pick<VMAX>(c.wB, kB));
+          alone = alone || (finA < hi ? finA : hi) - (stA > fx ? stA : fx) <= 0;
+        }
+        if (!alone) continue;
+        for (int j = k + 1; j < nq; ++j) {
+          const uint32_t ez = cz.at(j);
+          const int kindZ = (ez >> 14) & 3, kZ = (ez >> 11) & 7, mZ = ez & 0x7FF;
+          const int sZ = pick<VMAX>(c.st, kZ);
+          int64_t rdy = 0;
+          if (kindZ == KF) {
+            if (sZ > 0) rdy = tb[node(KF, sZ - 1, mZ)] + pick<VMAX>(c.wF, kZ);
+          } else if (kindZ == KB) {
+            rdy = tb[node(KF, sZ, mZ)];
+            if (sZ < S - 1) {
+              const int64_t y = tb[node(KB, sZ + 1, mZ)] + pick<VMAX>(c.wB, kZ);
+              rdy = y > rdy ? y : rdy;
+            }
+          } else {
+            rdy = tb[node(KB, sZ, mZ)];
+          }
+          if (rdy <= finA) {
+            uint8_t* nb = b.nb_rec + (int64_t)(insb + found) * a.pr.stride;
+            nb[3] = 0;
+            nb[2] = (uint8_t)(np + 1);
+            uint8_t* mv = nb + po + 6 * np;
+            mv[0] = (uint8_t)d, mv[1] = 0;
+            mv[2] = (uint8_t)(j & 0xFF), mv[3] = (uint8_t)(j >> 8);
+            mv[4] = (uint8_t)(k & 0xFF), mv[5] = (uint8_t)(k >> 8);
+            ++found;
+            break;
+          }
+        }
+      }
+    }
+    __syncthreads();  // before the next record reuses the staged record and the tables
   }
 }
 
@@ -4389,14 +4564,16 @@ int tune_step_impl(const octo_problem* prob, const int64_t* layer_costs, const i
 // neighbourhoods over v <= v_max).
 int64_t alg1_slots(const octo_problem* p) {
   const int64_t v = p->v_max;
-  return std::max({v * v, (int64_t)(p->P - 1) * v * v + 1, 3 * v * p->M + 2});
+  // scheduling: 3 policies, qlen - 1 swaps and qlen - 1 insertion placeholders
+  return std::max({v * v, (int64_t)(p->P - 1) * v * v + 1, 6 * v * p->M + 1});
 }
 
 // Algorithm 1 behind octo_alg1_tune: state and batch in the workspace's a1 buffer, iterations
 // enqueued back to back on the stream (no host synchronisation).
 int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
-              void* records, int64_t n, int32_t iters, int64_t* out_makespan, int64_t* out_bubble,
-              int64_t* out_stats, hipStream_t stream) {
+              void* records, int64_t n, int32_t iters, int32_t flags, uint64_t seed,
+              int64_t* out_makespan, int64_t* out_bubble, int64_t* out_stats,
+              int64_t* out_phase_iters, hipStream_t stream) {
   int rc = check_problem(prob);
   if (rc) return rc;
   if (n < 0 || iters < 0) return OCTO_EINVAL;
@@ -4405,11 +4582,26 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   if (n > (int64_t)INT32_MAX / slots || prob->cand_stride > A1_REC_MAX) return OCTO_EINVAL;
   if (!layer_costs || !link || !records || !out_makespan || !out_bubble || !out_stats)
     return OCTO_EINVAL;
+  if ((flags & ~(A1F_INSERT | A1F_RANDOM)) != 0) return OCTO_EINVAL;
   if ((reinterpret_cast<uintptr_t>(records) & 15) != 0) return OCTO_EINVAL;
   const int64_t nb = n * slots;
   std::lock_guard<std::mutex> lock(g_mu);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return OCTO_EHIP;
+  // the insertion pass: 64-bit finish tables, one group per record; its grid bounds the group
+  // slots whose finish and start times it keeps
+  int ins_grid = 0;
+  Setup su;
+  if (flags & A1F_INSERT) {
+    if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su))) return rc;
+    if ((rc = prob->v_max <= 2
+                  ? occupancy_grid(k_alg1_insert<2>, su.big.lds_bytes, su.di.cus, &ins_grid)
+                  : occupancy_grid(k_alg1_insert<8>, su.big.lds_bytes, su.di.cus, &ins_grid)))
+      return rc;
+    ins_grid = (int)std::max<int64_t>(
+        1, std::min<int64_t>(std::min(ins_grid, su.mat_grid), (n + su.big.CPW - 1) / su.big.CPW));
+  }
+  const size_t nodes = (size_t)3 * prob->P * prob->v_max * prob->M;
   Workspace& ws = g_ws[std::make_pair(dev, stream)];
   const int P = prob->P;
   size_t o = 0;
@@ -4427,6 +4619,10 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   o = align_up(o + (size_t)nb * P * 8, 256);
   const size_t o_nbnd = o;
   o = align_up(o + (size_t)nb * P * 16, 256);
+  const size_t o_ins = o;
+  o = align_up(o + (size_t)n * 4, 256);
+  const size_t o_tbuf = o;
+  o = align_up(o + (size_t)ins_grid * std::max(su.big.CPW, 0) * 2 * nodes * 8, 256);
   if ((rc = ensure_buf(ws.a1, ws.a1_bytes, o, stream))) return rc;
   char* base = static_cast<char*>(ws.a1);
   A1Args a;
@@ -4440,6 +4636,12 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   a.bnd = reinterpret_cast<int64_t*>(base + o_bnd);
   a.st = reinterpret_cast<int32_t*>(base + o_st);
   a.stats = out_stats;
+  a.pit = out_phase_iters;
+  a.flags = flags;
+  a.seed = seed;
+  a.iter = 0;
+  a.ins_list = reinterpret_cast<int32_t*>(base + o_ins);
+  a.ins_n = reinterpret_cast<int32_t*>(base + o_total) + 1;
   a.nb_rec = reinterpret_cast<uint8_t*>(base + o_rec);
   a.nb_ms = reinterpret_cast<int64_t*>(base + o_ms);
   a.nb_bub = reinterpret_cast<int64_t*>(base + o_bub);
@@ -4447,7 +4649,7 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   a.total = reinterpret_cast<int32_t*>(base + o_total);
   const int grid = (int)std::min<int64_t>(n, 1 << 16);
   hipLaunchKernelGGL(k_alg1_init, dim3((int)std::min<int64_t>((n + 255) / 256, 1024)), dim3(256),
-                     0, stream, a.st, a.stats, n);
+                     0, stream, a.st, a.stats, a.pit, n);
   if ((rc = launch_ok())) return rc;
   Extra cur;
   cur.bound = a.bnd;
@@ -4458,11 +4660,24 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   nbx.bound = reinterpret_cast<int64_t*>(base + o_nbnd);
   nbx.n_live = a.total;
   for (int it = 0; it < iters; ++it) {
+    a.iter = it;
     hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, stream,
-                       reinterpret_cast<uint32_t*>(a.total), 1, 0u);
+                       reinterpret_cast<uint32_t*>(a.total), 2, 0u);  // cursor, insertion count
     if ((rc = launch_ok())) return rc;
     hipLaunchKernelGGL(k_alg1_expand, dim3(grid), dim3(WAVE), 0, stream, a);
     if ((rc = launch_ok())) return rc;
+    if (flags & A1F_INSERT) {
+      if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su))) return rc;
+      SimArgs sa = make_args(prob, su.big, su, link, records, n, nullptr, nullptr);
+      int64_t* tbuf = reinterpret_cast<int64_t*>(static_cast<char*>(ws.a1) + o_tbuf);
+      if (prob->v_max <= 2)
+        hipLaunchKernelGGL(k_alg1_insert<2>, dim3(ins_grid), dim3(WAVE), su.big.lds_bytes, stream,
+                           sa, a, tbuf);
+      else
+        hipLaunchKernelGGL(k_alg1_insert<8>, dim3(ins_grid), dim3(WAVE), su.big.lds_bytes, stream,
+                           sa, a, tbuf);
+      if ((rc = launch_ok())) return rc;
+    }
     if ((rc = sim_batch_run<XB>(prob, layer_costs, nullptr, link, a.nb_rec, nb,
                                 reinterpret_cast<int64_t*>(base + o_ms),
                                 reinterpret_cast<int64_t*>(base + o_bub), nbx, stream)))
@@ -4783,8 +4998,16 @@ int octo_tune_step_mem(const octo_problem* prob, const int64_t* layer_costs,
 int octo_alg1_tune(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
                    void* records, int64_t n, int32_t iters, int64_t* out_makespan,
                    int64_t* out_bubble, int64_t* out_stats, void* stream) {
-  return alg1_impl(prob, layer_costs, link, records, n, iters, out_makespan, out_bubble,
-                   out_stats, static_cast<hipStream_t>(stream));
+  return alg1_impl(prob, layer_costs, link, records, n, iters, A1F_INSERT, 0, out_makespan,
+                   out_bubble, out_stats, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int octo_alg1_tune_ex(const octo_problem* prob, const int64_t* layer_costs, const int64_t* link,
+                      void* records, int64_t n, int32_t iters, int32_t flags, uint64_t seed,
+                      int64_t* out_makespan, int64_t* out_bubble, int64_t* out_stats,
+                      int64_t* out_phase_iters, void* stream) {
+  return alg1_impl(prob, layer_costs, link, records, n, iters, flags, seed, out_makespan,
+                   out_bubble, out_stats, out_phase_iters, static_cast<hipStream_t>(stream));
 }
 
 int octo_profile_events(void* const* events, int32_t n_events) {

@@ -212,8 +212,8 @@ struct Lane : Desc {
                       // (forward outputs of chunk k at k, backward outputs at VMAX + k)
   int64_t fs;         // start of the device's first op (-1 before it), bounds variants
   int64_t* tb;        // XT: finish time of every op, at (kind * tS + stage) * tM + m
-  int64_t* ts;        // XT (nullable, with tl): start time of every op, same index
-  int32_t* tl;        // XT: the round each op ran in — its level, the number of ops on the
+  int64_t* ts;        // XT (nullable): start time of every op, same index
+  int32_t* tl;        // XT (nullable): the round each op ran in — its level, the number of ops on the
                       // longest dependency chain before it (queue order included)
   int tS, tM, rnd;
 };
@@ -332,7 +332,8 @@ __device__ __forceinline__ bool relax_round(Gen& gen, const Chunks<VMAX>& c, con
       const int nd = (gen.kind * L.tS + pick<VMAX>(c.st, gen.k)) * L.tM + gen.m;
       if (ok) {
         L.tb[nd] = fin;
-        if (L.tl) L.ts[nd] = st, L.tl[nd] = L.rnd;
+        if (L.ts) L.ts[nd] = st;
+        if (L.tl) L.tl[nd] = L.rnd;
       }
       L.rnd += 1;
     }

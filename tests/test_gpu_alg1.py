@@ -151,3 +151,56 @@ def test_empty_batch(gpu):
     ms, bub, st = _lib.alg1_tune(prob, c, torch.zeros((2, 2), dtype=torch.int64, device=gpu), z, 5)
     torch.cuda.synchronize()
     assert ms.numel() == 0 and st.numel() == 0
+
+
+@pytest.mark.parametrize("flags", [0, 2, 3])
+def test_options_random_phase_and_no_insertion(gpu, flags):
+    """octo_alg1_tune_ex: insertions off (0), random phases without (2) and with (3)
+    insertions: the same search step for step as the oracle with those options, per-phase
+    iteration counts included."""
+    import torch
+    from paper_2509_23722_amd import _lib
+    rng = np.random.default_rng(9300 + flags)
+    P, v_max, M, L, mp, iters, seed = 4, 2, 8, 24, 4, 30, 4242 + flags
+    log(f"alg1: options flags={flags}")
+    costs = rng.integers(100_000, 3_000_000, size=(L, 3)).astype(np.int64)
+    link = rng.integers(0, 900_000, size=(P, P)).astype(np.int64)
+    recs = I.random_candidates(rng, L, P, v_max, M, 48, max_pert=mp, pert_rate=0.2,
+                               invalid_rate=0.05)
+    prob = _lib.problem(L, P, v_max, M, recs.shape[1], mp)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(gpu)
+    r = t(recs)
+    ms, bub, stats, pit = _lib.alg1_tune_ex(prob, t(costs), t(link), r, iters, flags, seed)
+    torch.cuda.synchronize()
+    g = (r.cpu().numpy(), ms.cpu().numpy(), bub.cpu().numpy(), stats.cpu().numpy())
+    rprob = R.problem(L, P, v_max, M, recs.shape[1], mp)
+    opit = np.zeros((len(recs), 3), np.int64)
+    out, oms, obub, acc, used = A.tune(rprob, costs, link, recs, iters, nthreads=NTHREADS,
+                                      random_search=bool(flags & 2), seed=seed,
+                                      insert=bool(flags & 1), phase_iters=opit)
+    assert_same(g, (out, oms, obub, np.concatenate([acc, used[:, None]], axis=1)),
+                f"flags={flags}")
+    assert (pit.cpu().numpy() == opit).all()
+
+
+def test_insertion_worked_example_on_gpu(gpu):
+    """The hand-worked insertion (tests/golden/overlap_insertion_example.txt): one iteration
+    keeps the move (0, 4, 2) at 30T."""
+    import torch
+    from paper_2509_23722_amd import _lib
+    from conftest import read_golden
+    kv, _ = read_golden("overlap_insertion_example.txt")
+    T = int(kv["T_ns"])
+    recs = I.pack_records(2, 1, 2, [I.POLICY["ZB"]], [1], [[1]], [[0, 1]])
+    prob = _lib.problem(2, 2, 1, 3, recs.shape[1], 2)
+    costs = np.array([[1, 4, 1], [2, 4, 2]], np.int64) * T
+    link = I.link_matrix(2, int(kv["transfer_T"]) * T)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(gpu)
+    r = t(recs)
+    ms, _, stats = _lib.alg1_tune(prob, t(costs), t(link), r, 1)
+    torch.cuda.synchronize()
+    rec = r.cpu().numpy()[0]
+    po = I.pert_offset(2, 1)
+    assert int(ms[0]) == int(kv["after_makespan_T"]) * T and int(rec[2]) == 1
+    assert np.frombuffer(bytes(rec[po:po + 6]), np.uint16).tolist() == \
+        [int(x) for x in kv["insertion"].split()]
