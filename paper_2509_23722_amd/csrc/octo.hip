@@ -3361,7 +3361,9 @@ __global__ void __launch_bounds__(WAVE) k_alg1_expand(A1Args a) {
 // (§5: a node overlaps when a computation runs beside it for a positive time), the first later
 // op Z = Q[j] that is ready when A ends (each producer's end, plus the transfer time across
 // devices) becomes the move (device, j, k) of the next placeholder (flags byte cleared, one
-// more move). Placeholders left over stay invalid.
+// more move). Placeholders left over stay invalid. The group's lanes share the walk: each takes
+// every G-th position, then every G-th insertion point, and the insertions found are numbered
+// in position order by a ballot.
 template <int VMAX>
 __global__ void __launch_bounds__(WAVE) k_alg1_insert(SimArgs a, A1Args b,
                                                       int64_t* __restrict__ tbuf) {
@@ -3376,7 +3378,8 @@ __global__ void __launch_bounds__(WAVE) k_alg1_insert(SimArgs a, A1Args b,
   const int dl = d < P ? d : 0;
   uint16_t* row = a.qscratch + ((size_t)slot * P + dl) * a.qcap;
   const size_t nodes = (size_t)3 * a.pr.s_max * M;
-  int64_t* tb = tbuf + (size_t)slot * 2 * nodes;  // finish times, then start times
+  // per slot: finish times, start times (node-indexed), then two rows of the searched queue
+  int64_t* tb = tbuf + (size_t)slot * (2 * nodes + 2 * (size_t)a.qcap);
   int64_t* ts = tb + nodes;
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
@@ -3422,64 +3425,100 @@ __global__ void __launch_bounds__(WAVE) k_alg1_insert(SimArgs a, A1Args b,
     bool dead = false;
     rounds_mat<VMAX, XT>(row, a.qcap, c, ring, L, T, G, gbit, lsb, dead, nullptr);
     __syncthreads();  // every lane's times visible to the group
+    // the searched device's queue, decoded by every lane of the group: (1) per position p, when
+    // the op could start (its inputs' arrivals) and, for an insertion before p, the end of
+    // op p - 1 when the device idles there and a communication there is alone (else -1);
+    // (2) per such p, the first later op ready by then; (3) the placeholders, in p order
     const int32_t* st = b.st + i * A1_WORDS;
-    if (mine && !dead && d == st[A1_DR]) {
-      const int nq = L.nops, insb = st[A1_INSB], nins = st[A1_NINS], np = rec[2];
-      auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
-      RowCursor ca, cz;
-      ca.init(row, nq);
-      cz.init(row, nq);
-      int found = 0;
-      for (int k = 1; k < nq && found < nins; ++k) {
-        const uint32_t ea = ca.at(k - 1), eb = ca.at(k);
+    const int dr = has ? st[A1_DR] : 0, insb = has ? st[A1_INSB] : 0;
+    const int nins = has ? st[A1_NINS] : 0, np = rec[2];
+    const bool go = valid && !dead && nins > 0;
+    Chunks<VMAX> cr;
+    if (go) {
+      (void)setup_chunks<VMAX>(cr, a.pr, rec, a.pre, a.link, dr, v, r.split, ring, nullptr,
+                               nullptr, XR);
+    } else {
+      zero_chunks<VMAX>(cr);
+    }
+    const uint16_t* rrow = a.qscratch + ((size_t)slot * P + dr) * a.qcap;
+    const int nq = go ? (r.split ? 3 : 2) * v * M : 0;
+    int64_t* rdy = tb + 2 * nodes;
+    int64_t* thr = rdy + a.qcap;
+    auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
+    for (int q = d; q < nq && d < G; q += G) {
+      const uint32_t eb = rrow[q];
+      const int kindB = (eb >> 14) & 3, kB = (eb >> 11) & 7, mB = eb & 0x7FF;
+      const int sB = pick<VMAX>(cr.st, kB);
+      int64_t ry = 0;
+      if (kindB == KF) {
+        if (sB > 0) ry = tb[node(KF, sB - 1, mB)] + pick<VMAX>(cr.wF, kB);
+      } else if (kindB == KB) {
+        ry = tb[node(KF, sB, mB)];
+        if (sB < S - 1) {
+          const int64_t y = tb[node(KB, sB + 1, mB)] + pick<VMAX>(cr.wB, kB);
+          ry = y > ry ? y : ry;
+        }
+      } else {
+        ry = tb[node(KB, sB, mB)];
+      }
+      rdy[q] = ry;
+      int64_t t = -1;
+      if (q >= 1) {
+        const uint32_t ea = rrow[q - 1];
         const int kindA = (ea >> 14) & 3, kA = (ea >> 11) & 7, mA = ea & 0x7FF;
-        const int kindB = (eb >> 14) & 3, kB = (eb >> 11) & 7, mB = eb & 0x7FF;
-        const int sA = pick<VMAX>(c.st, kA), sB = pick<VMAX>(c.st, kB);
+        const int sA = pick<VMAX>(cr.st, kA);
         const int64_t finA = tb[node(kindA, sA, mA)], stA = ts[node(kindA, sA, mA)];
         const int64_t finB = tb[node(kindB, sB, mB)], stB = ts[node(kindB, sB, mB)];
-        if (stB <= finA) continue;
-        const int cxA = kindA == KF ? pick<VMAX>(c.xF, kA) : kindA == KB ? pick<VMAX>(c.xB, kA) : 0;
-        const int cxB = kindB == KF ? pick<VMAX>(c.xF, kB) : kindB == KB ? pick<VMAX>(c.xB, kB) : 0;
-        bool alone = false;
-        if (cxA & CX_OUT) {  // A's output in flight over [finA, finA + c]; does B run then?
-          const int64_t hi = finA + (kindA == KF ? pick<VMAX>(c.cF, kA) : pick<VMAX>(c.cB, kA));
-          alone = alone || (finB < hi ? finB : hi) - (stB > finA ? stB : finA) <= 0;
-        }
-        if (cxB & CX_IN) {  // B's input in flight from its producer's end; does A run then?
-          const int64_t fx = tb[node(kindB, kindB == KF ? sB - 1 : sB + 1, mB)];
-          const int64_t hi = fx + (kindB == KF ? pick<VMAX>(c.wF, kB) : pick<VMAX>(c.wB, kB));
-          alone = alone || (finA < hi ? finA : hi) - (stA > fx ? stA : fx) <= 0;
-        }
-        if (!alone) continue;
-        for (int j = k + 1; j < nq; ++j) {
-          const uint32_t ez = cz.at(j);
-          const int kindZ = (ez >> 14) & 3, kZ = (ez >> 11) & 7, mZ = ez & 0x7FF;
-          const int sZ = pick<VMAX>(c.st, kZ);
-          int64_t rdy = 0;
-          if (kindZ == KF) {
-            if (sZ > 0) rdy = tb[node(KF, sZ - 1, mZ)] + pick<VMAX>(c.wF, kZ);
-          } else if (kindZ == KB) {
-            rdy = tb[node(KF, sZ, mZ)];
-            if (sZ < S - 1) {
-              const int64_t y = tb[node(KB, sZ + 1, mZ)] + pick<VMAX>(c.wB, kZ);
-              rdy = y > rdy ? y : rdy;
-            }
-          } else {
-            rdy = tb[node(KB, sZ, mZ)];
+        if (stB > finA) {
+          const int cxA =
+              kindA == KF ? pick<VMAX>(cr.xF, kA) : kindA == KB ? pick<VMAX>(cr.xB, kA) : 0;
+          const int cxB =
+              kindB == KF ? pick<VMAX>(cr.xF, kB) : kindB == KB ? pick<VMAX>(cr.xB, kB) : 0;
+          bool alone = false;
+          if (cxA & CX_OUT) {  // A's output in flight over [finA, finA + c]; does B run then?
+            const int64_t hi =
+                finA + (kindA == KF ? pick<VMAX>(cr.cF, kA) : pick<VMAX>(cr.cB, kA));
+            alone = alone || (finB < hi ? finB : hi) - (stB > finA ? stB : finA) <= 0;
           }
-          if (rdy <= finA) {
-            uint8_t* nb = b.nb_rec + (int64_t)(insb + found) * a.pr.stride;
-            nb[3] = 0;
-            nb[2] = (uint8_t)(np + 1);
-            uint8_t* mv = nb + po + 6 * np;
-            mv[0] = (uint8_t)d, mv[1] = 0;
-            mv[2] = (uint8_t)(j & 0xFF), mv[3] = (uint8_t)(j >> 8);
-            mv[4] = (uint8_t)(k & 0xFF), mv[5] = (uint8_t)(k >> 8);
-            ++found;
-            break;
+          if (cxB & CX_IN) {  // B's input in flight from its producer's end; does A run then?
+            const int64_t fx = tb[node(kindB, kindB == KF ? sB - 1 : sB + 1, mB)];
+            const int64_t hi =
+                fx + (kindB == KF ? pick<VMAX>(cr.wF, kB) : pick<VMAX>(cr.wB, kB));
+            alone = alone || (finA < hi ? finA : hi) - (stA > fx ? stA : fx) <= 0;
           }
+          t = alone ? finA : -1;
         }
       }
+      thr[q] = t;
+    }
+    __syncthreads();  // the group's rdy and thr visible to all its lanes
+    const uint64_t gmask = G >= WAVE ? ~0ull : ((1ull << G) - 1);
+    const int g0 = lane_id() - d;
+    int found = 0;
+    for (int k0 = 0; k0 < nq; k0 += G) {
+      const int k = k0 + d;
+      int jk = -1;
+      if (d < G && k >= 1 && k < nq) {
+        const int64_t t = thr[k];
+        if (t >= 0)
+          for (int j = k + 1; j < nq; ++j)
+            if (rdy[j] <= t) {
+              jk = j;
+              break;
+            }
+      }
+      const uint64_t gm = (__ballot(jk >= 0) >> g0) & gmask;
+      const int at = found + __popcll(gm & ((1ull << d) - 1));
+      if (jk >= 0 && at < nins) {
+        uint8_t* nb = b.nb_rec + (int64_t)(insb + at) * a.pr.stride;
+        nb[3] = 0;
+        nb[2] = (uint8_t)(np + 1);
+        uint8_t* mv = nb + po + 6 * np;
+        mv[0] = (uint8_t)dr, mv[1] = 0;
+        mv[2] = (uint8_t)(jk & 0xFF), mv[3] = (uint8_t)(jk >> 8);
+        mv[4] = (uint8_t)(k & 0xFF), mv[5] = (uint8_t)(k >> 8);
+      }
+      found += __popcll(gm);
     }
     __syncthreads();  // before the next record reuses the staged record and the tables
   }
@@ -4622,7 +4661,9 @@ int alg1_impl(const octo_problem* prob, const int64_t* layer_costs, const int64_
   const size_t o_ins = o;
   o = align_up(o + (size_t)n * 4, 256);
   const size_t o_tbuf = o;
-  o = align_up(o + (size_t)ins_grid * std::max(su.big.CPW, 0) * 2 * nodes * 8, 256);
+  o = align_up(o + (size_t)ins_grid * std::max(su.big.CPW, 0) *
+                       (2 * nodes + 2 * (size_t)std::max(su.big.qcap, 0)) * 8,
+                256);
   if ((rc = ensure_buf(ws.a1, ws.a1_bytes, o, stream))) return rc;
   char* base = static_cast<char*>(ws.a1);
   A1Args a;
