@@ -402,7 +402,7 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   const uint32_t row = (mine && !wide) ? (uint32_t)qt_row<VMAX>(a, gen, v, split, c)
                                        : (uint32_t)a.qt_end;
   __asm__ volatile("" ::: "memory");
-  T.clear_all(S * ring.R, lane_id(), WAVE);
+  T.clear_all(S * qt_row_stride(ring), lane_id(), WAVE);
   __asm__ volatile("" ::: "memory");
 
   bool dead = false;
@@ -410,8 +410,8 @@ __device__ __forceinline__ void run_tab(const SimArgs& a, int64_t cand, int v, i
   CommTally cm;
   cm.reset();
   int64_t fs = -1;
-  relax_tab<X>(a.qtab, row, ring.R << T.lg, strm, clock, T, G, gbit, lsb, dead, mem, peak, cm,
-               fs);
+  relax_tab<X>(a.qtab, row, qt_row_stride(ring) << T.lg, strm, clock, T, G, gbit, lsb, dead, mem,
+               peak, cm, fs);
 
   const int64_t ms = group_max(clock, G);
   CommTally tot = cm;
@@ -3886,7 +3886,7 @@ struct TabGeom {
 TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool wide) {
   TabGeom t;
   t.ring = make_ring(p->M, v * p->P);
-  t.plan = fast_plan(p, lds_max, v * p->P, t.ring.R, 3 * v * (wide ? 2 : 1));
+  t.plan = fast_plan(p, lds_max, v * p->P, qt_row_stride(t.ring), 3 * v * (wide ? 2 : 1));
   t.lg = t.plan.CPW > 0 ? __builtin_ctz(t.plan.CPW) : 0;
   return t;
 }

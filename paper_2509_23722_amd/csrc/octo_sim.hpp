@@ -486,13 +486,19 @@ __device__ __forceinline__ void rounds(Gen& gen, const Chunks<VMAX>& c, const Ri
 // ascending order), each op pre-encoded in 32 bits, for one launch geometry (ring R,
 // CPW = 2^lg candidates per wave), with everything that does not depend on the candidate:
 //   bits 0-14 read slot << lg | 15-16 write row relative to the read row, + 1 (the write slot
-//   is read slot + (code - 1) R << lg) | 17-19 state bits needed (B, F, parity) | 20-22 their
+//   is read slot + (code - 1) RS << lg) | 17-19 state bits needed (B, F, parity) | 20-22 their
 //   wanted values | 23-25 state bits written, parity included (0 = writes nothing) |
 //   26-28 stream e = kind * v + chunk.
 // The candidate's per-stream input weight and duration (32-bit) sit in LDS, 64 lanes
 // interleaved: the pair of lane l for stream e at byte e * 512 + l * 8 (memory-model variants:
 // 16-byte records {w, dur, activation delta} at e * 1024 + l * 16).
 // ------------------------------------------------------------------------------------------
+// Rows are RS = R + 5 slots apart: with rows of R slots (R and the interleave are powers of
+// two) the same micro-batch of every stage falls in one LDS bank, and the lanes of a group
+// often touch one micro-batch in several stages in the same round. Measured on the P = 8,
+// M = 64 batch's generated v = 2 queues (ms per call of that kernel): R 0.452, R + 1 0.407,
+// R + 3 0.394, R + 5 0.390, R + 7 0.390, R + 9 0.400.
+__host__ __device__ __forceinline__ int qt_row_stride(const Ring& ring) { return ring.R + 5; }
 __host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, int v, int s,
                                                       int S, const Ring& ring, int lg) {
   int rdrow, need, wst;
@@ -511,7 +517,7 @@ __host__ __device__ __forceinline__ uint32_t qt_entry(int kind, int k, int m, in
   }
   const int mr = m & ring.mask;
   const int par = (m >> ring.lg) & 1;
-  const uint32_t rd = (uint32_t)(rdrow * ring.R + mr) << lg;
+  const uint32_t rd = (uint32_t)(rdrow * qt_row_stride(ring) + mr) << lg;
   const uint32_t code = (uint32_t)(s - rdrow + 1);
   const int want = need & (par ? (int)(ST_B | ST_F | ST_PAR) : (int)(ST_B | ST_F));
   const int state = wst ? (wst | (par << 2)) : 0;
@@ -528,7 +534,7 @@ constexpr uint32_t QT_END = 1u << 20;
 // nothing: the slot is empty or holds the backward of micro-batch m - R, which this device has
 // already run, so its time never exceeds the device clock. Each round decodes its op first, so
 // the stream read and the slot read are in flight together, and loads the entry after next at
-// its start, to be taken at the end of the next round. Rl = R << lg. XM: streams are 16-byte records
+// its start, to be taken at the end of the next round. Rl = RS << lg. XM: streams are 16-byte records
 // {w, dur, activation delta}; mem / peak track the activation bytes held. XC: 16-byte records
 // {w, dur, output transfer time, CX flags}; cm tallies the communication nodes.
 template <int X>
