@@ -2499,6 +2499,9 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
   int64_t busy = 0, stat = 0, ms_first = 0;
   int S = P, n = 0, n0 = 0, max_adv = 0;
   int dstar = 0, p = -1, cursor = -1, first = -1, j = -1, at = -1;
+  // whether this lane's queue changed since its last activation walk: only the device whose W
+  // moved needs a new walk, the others keep theirs
+  bool stale = true;
   AdvOut o;
   o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0, o.top = 0;
   for (;;) {
@@ -2546,6 +2549,7 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
       max_adv = a.pr.max_pert - n0;
       o.dead = false, o.fits = false, o.adv = 0, o.ms = 0, o.hi = 0, o.top = 0;
       dstar = 0, p = -1, cursor = -1, first = -1, j = -1, at = -1, ms_first = 0;
+      stale = true;
       phase = r.valid ? AW_SIM : AW_DONE;
     }
     if (__ballot(phase != AW_EXIT) == 0) break;
@@ -2573,6 +2577,7 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
       if (j == first) ms_first = ms;
       if (ms <= o.ms) {
         o.ms = ms;
+        stale = stale || d == dstar;
         if (d == dstar) {
           pert[3 * o.adv] = (uint16_t)dstar, pert[3 * o.adv + 1] = (uint16_t)j;
           pert[3 * o.adv + 2] = (uint16_t)p;
@@ -2588,7 +2593,8 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
     // walks and searches need no simulation: settle them before the next round
     while (phase == AW_WALK || phase == AW_NEXT) {
       if (phase == AW_WALK) {
-        if (d < P) act_walk<VMAX>(row, n, c, o.hi, at);
+        if (d < P && stale) act_walk<VMAX>(row, n, c, o.hi, at);
+        stale = false;
         const bool over = d < P && stat + o.hi > capd;
         const uint64_t om = (__ballot(over) >> gl) & gmask;
         if (om == 0) {
@@ -2619,6 +2625,7 @@ __global__ void __launch_bounds__(WAVE) k_advance(SimArgs a, const int64_t* __re
             pert[3 * o.adv + 2] = (uint16_t)p;
           }
           o.ms = ms_first;
+          stale = stale || d == dstar;
           ++o.adv;
           phase = AW_WALK;
         } else {
