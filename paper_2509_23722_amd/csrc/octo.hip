@@ -1694,22 +1694,72 @@ __device__ __forceinline__ uint32_t pitem(uint32_t type, int kind, int s, int m)
 constexpr int32_t OB_NONE = -1;
 
 // Per-slot scratch of k_ordered.
+// A communication item of the reordering: its key is (producer end, level, producer node);
+// pk = level << 37 | node << 17 | receive << 16 | gap, so that comparing pk compares (level,
+// node), which no two items of a lane share. Levels (lockstep rounds of a live group) and
+// nodes are below 3 S M <= 3 * 64 * 2047 < 2^19; gaps are at most 3 v M < 2^16.
+struct __align__(16) CItem {
+  int64_t key;
+  uint64_t pk;
+};
+__device__ __forceinline__ bool item_less(const CItem& a, const CItem& b) {
+  return a.key != b.key ? a.key < b.key : a.pk < b.pk;
+}
+
+// Per-lane scratch of a wave, lane-interleaved: element i of lane l is at [i][l] of the wave's
+// block, so that the lanes' accesses at one index share cache lines.
+template <class T>
+struct LaneArr {
+  T* p;  // the lane's element 0
+  __device__ __forceinline__ T& operator[](int i) const { return p[(size_t)i * WAVE]; }
+};
+template <class T>
+__device__ __forceinline__ LaneArr<T> lane_arr(T* base, int cap) {
+  return LaneArr<T>{base + (size_t)blockIdx.x * cap * WAVE + lane_id()};
+}
+
 struct OrdBufs {
   int64_t* tb;      // [slot][3 S_max M] finish time of each op (REORDER, phase C: arrivals)
-  int64_t* rkey;    // [slot][P][rcap] receive keys (producer end)
-  uint32_t* rid;    // [slot][P][rcap] receive producers (pitem with type 0)
-  uint32_t* prog;   // [slot][P][pcap] programs
+  // the rest: [wave][cap][WAVE], lane-interleaved
+  int64_t* rkey;    // rcap: receive keys (producer end)
+  uint32_t* rid;    // rcap: receive producers (pitem with type 0)
+  uint4* prog;      // pcap / 4: programs, four items per entry
   int rcap, pcap;
   // REORDER only
   int64_t* ts;      // [slot][3 S_max M] start time of each op
   int32_t* tl;      // [slot][3 S_max M] level of each op
-  int64_t* ikey;    // [slot][P][icap] communication items: producer end ...
-  uint64_t* iln;    // ... level << 32 | producer node ...
-  int32_t* igap;    // ... and gap
-  int32_t* iord;    // [slot][P][2 icap] in-order items, then the mismatched ones
+  CItem* items;     // icap: in-order items from the front, mismatched ones from the back
+  int64_t* pst;     // pcap2: post time of each gap (end of the computation before)
+  int64_t* pdur;    // pcap2: durations of the computations before each gap
+  int pcap2;
   int64_t* stats;   // [n][2] (nullable): transfers, mismatched receives
   int icap;
 };
+
+// Program writer: items gathered four at a time into one 16-byte store (a store is counted
+// with the loads, so one per item would make every later load wait for its write).
+struct ProgOut {
+  LaneArr<uint4> prog;
+  uint4 pk4;
+  int n;
+  __device__ __forceinline__ void init(LaneArr<uint4> p) { prog = p, pk4 = make_uint4(0, 0, 0, 0), n = 0; }
+  __device__ __forceinline__ void emit(uint32_t item) {
+    const int q = n & 3;
+    pk4.x = q == 0 ? item : pk4.x;
+    pk4.y = q == 1 ? item : pk4.y;
+    pk4.z = q == 2 ? item : pk4.z;
+    pk4.w = q == 3 ? item : pk4.w;
+    if (q == 3) prog[n >> 2] = pk4;
+    ++n;
+  }
+  __device__ __forceinline__ int finish() {  // the last, partial group of four
+    if (n & 3) prog[n >> 2] = pk4;
+    return n;
+  }
+};
+__device__ __forceinline__ uint32_t prog_at(LaneArr<uint4> prog, int i) {
+  return reinterpret_cast<const uint32_t*>(&prog[i >> 2])[i & 3];
+}
 
 // (t, cls, tie) < (t', cls', tie')
 __device__ __forceinline__ bool key_less(int64_t t, uint32_t cls, uint32_t tie, int64_t t2,
@@ -1749,8 +1799,8 @@ struct RowCursor {
 // Phase B for lane d: returns the program length.
 template <int VMAX>
 __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16_t* row, int nq,
-                                             const int64_t* tb, int S, int M, int64_t* rkey,
-                                             uint32_t* rid, uint32_t* prog) {
+                                             const int64_t* tb, int S, int M, LaneArr<int64_t> rkey,
+                                             LaneArr<uint32_t> rid, LaneArr<uint4> prog) {
   auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
   auto dur_of = [&](int kind, int k) {
     return kind == KF ? pick<VMAX>(c.dF, k) : kind == KB ? pick<VMAX>(c.dB, k) : pick<VMAX>(c.dW, k);
@@ -1858,7 +1908,7 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
     pk4.y = q == 1 ? item : pk4.y;
     pk4.z = q == 2 ? item : pk4.z;
     pk4.w = q == 3 ? item : pk4.w;
-    if (q == 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
+    if (q == 3) prog[n >> 2] = pk4;
     ++n;
     // the stream taken: next to head, and the item after next requested
     const bool tc = src == 0, ts = src == 1, tr = src == 2;
@@ -1873,7 +1923,7 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
     if (tr && ri + 1 < nr) rk2 = rkey[ri + 1], rdd2 = rid[ri + 1];
   }
   // the last, partial group of four
-  if (n & 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
+  if (n & 3) prog[n >> 2] = pk4;
   return n;
 }
 
@@ -1885,154 +1935,168 @@ __device__ __forceinline__ int build_program(const Chunks<VMAX>& c, const uint16
 // the consumer)) among the gaps between the in-order items around its key, at most its
 // consumer's, whose post time is not before the producer starts (the highest gap always
 // qualifies; ties: the highest); then the items, in key order, are merged with the computations
-// by gap. Returns the program length; *nrecv and *nmis get the two counts.
+// by gap. Returns the program length; *nrecv and *nmis get the two counts. pst and pdur
+// (nq + 1 entries) hold each gap's post time and the prefix sums of the computations'
+// durations, so that a window's costs read two arrays instead of walking the queue.
+// A send is never mismatched: its key is its own op's end, which is later than the end of every
+// earlier op and of every producer an earlier op received from.
 template <int VMAX>
 __device__ __forceinline__ int build_program3(const Chunks<VMAX>& c, const uint16_t* row, int nq,
                                               const int64_t* tb, const int64_t* ts,
-                                              const int32_t* tl, int S, int M, int64_t* ikey,
-                                              uint64_t* iln, int32_t* igap, int32_t* iord,
-                                              int icap, uint32_t* prog, int* nrecv, int* nmis) {
+                                              const int32_t* tl, int S, int M,
+                                              LaneArr<CItem> items, int icap,
+                                              LaneArr<int64_t> pst, LaneArr<int64_t> pdur,
+                                              LaneArr<uint4> prog, int* nrecv, int* nmis) {
   auto node = [&](int kind, int s, int m) { return (kind * S + s) * M + m; };
   auto dur_of = [&](int kind, int k) {
     return kind == KF ? pick<VMAX>(c.dF, k) : kind == KB ? pick<VMAX>(c.dB, k) : pick<VMAX>(c.dW, k);
   };
-  auto less = [&](int64_t t, uint64_t ln, int64_t t2, uint64_t ln2) {
-    return t != t2 ? t < t2 : ln < ln2;
+  // the node field is kind << 17 | stage << 11 | m, ordered as the node index is
+  auto pack = [](int level, int kind, int s, int m, uint32_t recv, int gap) {
+    return (uint64_t)(uint32_t)level << 37 |
+           (uint64_t)((uint32_t)kind << 17 | (uint32_t)s << 11 | (uint32_t)m) << 17 |
+           (uint64_t)recv << 16 | (uint64_t)(uint32_t)gap;
   };
-  int* recs = iord;
-  int* flg = iord + icap;
-  // the items in program order; step 1 on the fly
-  int ni = 0, nr = 0, nf = 0, nrv = 0;
-  int64_t topk = 0;
-  uint64_t topl = 0;
-  auto add = [&](int64_t t, uint64_t ln, int gap, bool recv) {
-    ikey[ni] = t, iln[ni] = ln, igap[ni] = gap;
-    if (nr == 0 || less(topk, topl, t, ln)) {
-      recs[nr++] = ni;
-      topk = t, topl = ln;
+  auto gap_of = [](const CItem& x) { return (int)(x.pk & 0xFFFFu); };
+  // mismatched item j sits at icap - 1 - j
+  auto mis = [&](int j) -> CItem& { return items[icap - 1 - j]; };
+  // the items in program order, step 1 on the fly: eight queue entries per span, whose loads
+  // are all issued before the items are stored
+  int nr = 0, nf = 0, nrv = 0;
+  CItem top;
+  top.key = 0, top.pk = 0;
+  auto add = [&](int64_t t, uint64_t pk) {
+    CItem x;
+    x.key = t, x.pk = pk;
+    if (nr == 0 || item_less(top, x)) {
+      items[nr++] = x;
+      top = x;
     } else {
-      flg[nf++] = ni;
+      mis(nf++) = x;
     }
-    nrv += recv ? 1 : 0;
-    ++ni;
   };
+  pst[0] = 0, pdur[0] = 0;
+  int64_t dsum = 0;
   for (int i0 = 0; i0 < nq; i0 += 8) {
     const uint4 b = row_span(row, i0 >> 3, nq);
+    int64_t fy[8], fx[8], ds[8];
+    int32_t ly[8], lx[8];
+    int cxs[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t e = span_entry(b, u);
+      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
+      const int s = pick<VMAX>(c.st, k);
+      const bool in = i0 + u < nq;
+      const int cx =
+          !in ? 0 : kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
+      const int y = node(kind, s, m), x = node(kind, kind == KF ? s - 1 : s + 1, m);
+      cxs[u] = cx;
+      fy[u] = in ? tb[y] : 0;
+      fx[u] = (cx & CX_IN) ? tb[x] : 0;
+      lx[u] = (cx & CX_IN) ? tl[x] : 0;
+      ly[u] = (cx & CX_OUT) ? tl[y] : 0;
+      dsum += in ? dur_of(kind, k) : 0;
+      ds[u] = dsum;
+    }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (i0 + u >= nq) break;
       const uint32_t e = span_entry(b, u);
       const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
       const int s = pick<VMAX>(c.st, k);
-      const int cx = kind == KF ? pick<VMAX>(c.xF, k) : kind == KB ? pick<VMAX>(c.xB, k) : 0;
-      if (cx & CX_IN) {
-        const int x = node(kind, kind == KF ? s - 1 : s + 1, m);
-        add(tb[x], (uint64_t)(uint32_t)tl[x] << 32 | (uint32_t)x, i0 + u, true);
+      pst[i0 + u + 1] = fy[u], pdur[i0 + u + 1] = ds[u];
+      if (cxs[u] & CX_IN) {
+        add(fx[u], pack(lx[u], kind, kind == KF ? s - 1 : s + 1, m, 1u, i0 + u));
+        ++nrv;
       }
-      if (cx & CX_OUT) {
-        const int y = node(kind, s, m);
-        add(tb[y], (uint64_t)(uint32_t)tl[y] << 32 | (uint32_t)y, i0 + u + 1, false);
-      }
+      if (cxs[u] & CX_OUT) add(fy[u], pack(ly[u], kind, s, m, 0u, i0 + u + 1));
     }
   }
   *nrecv = nrv, *nmis = nf;
-  // the mismatched items in key order (few, and nearly sorted)
+  // the mismatched items in key order
   for (int a2 = 1; a2 < nf; ++a2) {
-    const int v = flg[a2];
-    const int64_t vk = ikey[v];
-    const uint64_t vl = iln[v];
+    const CItem v = mis(a2);
     int j = a2;
-    while (j > 0 && less(vk, vl, ikey[flg[j - 1]], iln[flg[j - 1]])) {
-      flg[j] = flg[j - 1];
-      --j;
+    CItem pv = mis(j - 1);
+    while (item_less(v, pv)) {
+      mis(j) = pv;
+      if (--j == 0) break;
+      pv = mis(j - 1);
     }
-    flg[j] = v;
+    mis(j) = v;
   }
-  // steps 2 and 3: the in-order items are sorted by key and by gap, so one cursor serves all
-  RowCursor rc;
-  rc.init(row, nq);
-  auto post = [&](int g) -> int64_t {  // end of computation g - 1 (0 before the first)
-    if (g == 0) return 0;
-    const uint32_t e = rc.at(g - 1);
-    const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
-    return tb[node(kind, pick<VMAX>(c.st, k), m)];
-  };
+  // steps 2 and 3: the in-order items are sorted by key and by gap, so one walk serves all; a
+  // mismatched item lies below the record that was the maximum when it came, so the walk
+  // stops inside the records
   int rp = 0, lastg = 0, logap = 0;
+  CItem rh = items[0];
   for (int a2 = 0; a2 < nf; ++a2) {
-    const int f = flg[a2];
-    const int64_t fk = ikey[f];
-    const uint64_t fl = iln[f];
-    while (rp < nr && less(ikey[recs[rp]], iln[recs[rp]], fk, fl)) logap = igap[recs[rp++]];
-    const int hi = rp < nr ? igap[recs[rp]] : igap[f];  // rp < nr always: f is below a record
+    CItem f = mis(a2);
+    while (item_less(rh, f)) {
+      logap = gap_of(rh);
+      rh = items[++rp];
+    }
+    const int hi = gap_of(rh);
     const int lo = lastg > logap ? lastg : logap;
-    const int iY = igap[f];
-    const int x = (int)(uint32_t)fl;
-    const int64_t xst = ts[x];
+    const int iY = gap_of(f);
+    const uint32_t code = (uint32_t)(f.pk >> 17) & 0x7FFFFu;
+    const int64_t xst = ts[node(code >> 17, (code >> 11) & 63, code & 0x7FF)];
     // the transfer's time: the consumer's input weight
-    const uint32_t ey = rc.at(iY);
+    const uint32_t ey = row[iY];
     const int ky = (ey >> 11) & 7;
     const int64_t cw = ((ey >> 14) & 3) == KF ? pick<VMAX>(c.wF, ky) : pick<VMAX>(c.wB, ky);
-    int64_t D = 0;
-    for (int i = hi; i < iY; ++i) {
-      const uint32_t e = rc.at(i);
-      D += dur_of((e >> 14) & 3, (e >> 11) & 7);
+    // the window's lowest gap: the first at or above lo posted at or after X's start (post
+    // times never decrease), or just hi
+    int gx = lo, ge = hi + 1;
+    while (gx < ge) {
+      const int mid = (gx + ge) >> 1;
+      if (pst[mid] < xst) gx = mid + 1;
+      else ge = mid;
     }
+    const int first = gx < hi ? gx : hi;
+    const int64_t pY = pdur[iY], fk = f.key;
     int best = hi;
     int64_t bestc = 0;
-    for (int gp = hi; gp >= lo; --gp) {
-      if (gp < hi) {
-        const uint32_t e = rc.at(gp);
-        D += dur_of((e >> 14) & 3, (e >> 11) & 7);
-      }
-      const int64_t pt = post(gp);
-      if (gp < hi && pt < xst) break;
+    for (int gp = hi; gp >= first; --gp) {
+      const int64_t pt = pst[gp], D = pY - pdur[gp];
       const int64_t span = fk > pt ? fk - pt : pt - fk;
       const int64_t cost = span - (D < cw ? D : cw);
       if (gp == hi || cost < bestc) best = gp, bestc = cost;
     }
-    igap[f] = best;
+    f.pk = (f.pk & ~(uint64_t)0xFFFFu) | (uint64_t)best;
+    mis(a2) = f;
     lastg = best;
   }
-  // the program: items in key order (in-order ones and mismatched ones merged), each before
-  // the computation its gap names, written four per 16-byte store
-  int n = 0, ri = 0, fi = 0;
-  uint4 pk4 = make_uint4(0, 0, 0, 0);
-  auto emit = [&](uint32_t item) {
-    const int q = n & 3;
-    pk4.x = q == 0 ? item : pk4.x;
-    pk4.y = q == 1 ? item : pk4.y;
-    pk4.z = q == 2 ? item : pk4.z;
-    pk4.w = q == 3 ? item : pk4.w;
-    if (q == 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
-    ++n;
-  };
+  // the program: items in key order (in-order ones and mismatched ones merged; their gaps never
+  // decrease), each after the computations before its gap
+  ProgOut po;
+  po.init(prog);
   RowCursor cc;
   cc.init(row, nq);
-  for (int i = 0; i <= nq; ++i) {
-    for (;;) {
-      int src = -1;
-      if (ri < nr) src = recs[ri];
-      if (fi < nf && (src < 0 || less(ikey[flg[fi]], iln[flg[fi]], ikey[src], iln[src])))
-        src = flg[fi];
-      if (src < 0 || (i < nq && igap[src] > i)) break;
-      if (ri < nr && src == recs[ri]) ++ri;
-      else ++fi;
-      const int x = (int)(uint32_t)iln[src];
-      const int xk = x / (S * M), xs = (x / M) % S, xm = x % M;
-      // a send's producer is an own op at the gap before; a receive's is on another device
-      const uint32_t pe = igap[src] > 0 ? cc.at(igap[src] - 1) : 0xFFFFFFFFu;
-      const bool own = igap[src] > 0 && (int)((pe >> 14) & 3) == xk &&
-                       pick<VMAX>(c.st, (pe >> 11) & 7) == xs && (int)(pe & 0x7FF) == xm;
-      emit(((own ? PI_SEND : PI_RECV) << 30) | pitem(0, xk, xs, xm));
+  int ci = 0, ri = 0, fi = 0;
+  CItem rh2 = items[0], fh = mis(0);
+  while (ri < nr || fi < nf) {
+    const bool tr = ri < nr && (fi >= nf || item_less(rh2, fh));
+    const CItem h = tr ? rh2 : fh;
+    for (const int gp = gap_of(h); ci < gp; ++ci) {
+      const uint32_t e = cc.at(ci);
+      po.emit(pitem(PI_COMP, (e >> 14) & 3, pick<VMAX>(c.st, (e >> 11) & 7), e & 0x7FF));
     }
-    if (i < nq) {
-      const uint32_t e = cc.at(i);
-      const int kind = (e >> 14) & 3, k = (e >> 11) & 7, m = e & 0x7FF;
-      emit(pitem(PI_COMP, kind, pick<VMAX>(c.st, k), m));
+    const uint32_t code = (uint32_t)(h.pk >> 17) & 0x7FFFFu;
+    po.emit(((h.pk >> 16) & 1u ? PI_RECV : PI_SEND) << 30 |
+            pitem(0, code >> 17, (code >> 11) & 63, code & 0x7FF));
+    if (tr) {
+      if (++ri < nr) rh2 = items[ri];
+    } else {
+      if (++fi < nf) fh = mis(fi);
     }
   }
-  if (n & 3) reinterpret_cast<uint4*>(prog)[n >> 2] = pk4;
-  return n;
+  for (; ci < nq; ++ci) {
+    const uint32_t e = cc.at(ci);
+    po.emit(pitem(PI_COMP, (e >> 14) & 3, pick<VMAX>(c.st, (e >> 11) & 7), e & 0x7FF));
+  }
+  return po.finish();
 }
 
 // RING: 40-bit ring tables of a.ring rows per stage per group. Phase C keeps each device's
@@ -2066,12 +2130,9 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
   const int dl = d < P ? d : 0;
   uint16_t* row = a.qscratch + ((size_t)slot * P + dl) * a.qcap;
   int64_t* tb = ob.tb + (size_t)slot * 3 * a.pr.s_max * M;
-  int64_t* rkey = REORDER ? nullptr : ob.rkey + ((size_t)slot * P + dl) * ob.rcap;
-  uint32_t* rid = REORDER ? nullptr : ob.rid + ((size_t)slot * P + dl) * ob.rcap;
   int64_t* ts = REORDER ? ob.ts + (size_t)slot * 3 * a.pr.s_max * M : nullptr;
   int32_t* tl = REORDER ? ob.tl + (size_t)slot * 3 * a.pr.s_max * M : nullptr;
-  const size_t io = ((size_t)slot * P + dl) * ob.icap;
-  uint32_t* prog = ob.prog + ((size_t)slot * P + dl) * ob.pcap;
+  const LaneArr<uint4> prog = lane_arr(ob.prog, ob.pcap / 4);
   uint64_t gbit, lsb;
   group_bits(G, &gbit, &lsb);
   const int64_t n_groups = (int64_t)gridDim.x * a.CPW;
@@ -2128,10 +2189,13 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
     int plen = 0, nrecv = 0, nmis = 0;
     if constexpr (REORDER) {
       if (mine && !dead)
-        plen = build_program3<VMAX>(c, row, L.nops, tb, ts, tl, S, M, ob.ikey + io, ob.iln + io,
-                                    ob.igap + io, ob.iord + 2 * io, ob.icap, prog, &nrecv, &nmis);
+        plen = build_program3<VMAX>(c, row, L.nops, tb, ts, tl, S, M, lane_arr(ob.items, ob.icap),
+                                    ob.icap, lane_arr(ob.pst, ob.pcap2),
+                                    lane_arr(ob.pdur, ob.pcap2), prog, &nrecv, &nmis);
     } else {
-      if (mine && !dead) plen = build_program<VMAX>(c, row, L.nops, tb, S, M, rkey, rid, prog);
+      if (mine && !dead)
+        plen = build_program<VMAX>(c, row, L.nops, tb, S, M, lane_arr(ob.rkey, ob.rcap),
+                                   lane_arr(ob.rid, ob.rcap), prog);
     }
     if (run) T.clear(S * ring.R, d, G);
     mbox[me] = RDV_EMPTY;
@@ -2146,7 +2210,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
       int pos = 0;
       bool live = pos < plen, arrived = false;
       // the next item is loaded one advance ahead, so decoding never waits for memory
-      uint32_t nitem = plen > 1 ? prog[1] : 0u;
+      uint32_t nitem = plen > 1 ? prog_at(prog, 1) : 0u;
       // the current item, decoded
       uint32_t type = 0, tag = 0;
       int rd = 0, wr = 0, store = 0, src = 0;
@@ -2186,7 +2250,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
           xnode = (kind * S + s) * M + m;
         }
       };
-      decode(live ? prog[0] : 0u, live);
+      decode(live ? prog_at(prog, 0) : 0u, live);
       for (;;) {
         uint32_t plo, phi;
         T.issue(live && type != PI_RECV ? rd : 0, plo, phi);
@@ -2218,7 +2282,7 @@ __global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
           live = pos < plen;
           const uint32_t it = live ? nitem : 0u;
           __asm__ volatile("" : "+v"(nitem));
-          nitem = pos + 1 < plen ? prog[pos + 1] : 0u;
+          nitem = pos + 1 < plen ? prog_at(prog, pos + 1) : 0u;
           decode(it, live);
         }
         __asm__ volatile("" ::: "memory");
@@ -4752,17 +4816,25 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   DevInfo di;
   int rc = dev_info(dev, &di);
   if (rc) return rc;
-  // at most 4 GiB of per-slot scratch (finish times, receive keys or communication items,
-  // programs, queue rows)
-  const size_t per_slot =
-      (size_t)prob->P * prob->v_max * prob->M *
-          (REORDER ? 3 * (8 + 8 + 4) + 4 * (8 + 8 + 4 + 8) + 7 * 4 : 3 * 8 + 2 * 12 + 7 * 4) +
-      (size_t)prob->P * queue_cap(prob) * 2;
+  OrdBufs ob;
+  ob.rcap = REORDER ? 0 : 2 * prob->v_max * prob->M;
+  ob.pcap = (int)align_up((size_t)7 * prob->v_max * prob->M, 4);  // whole 16-byte entries
+  // communication items: at most a receive and a send per F or B
+  ob.icap = REORDER ? 4 * prob->v_max * prob->M : 0;
+  ob.pcap2 = REORDER ? queue_cap(prob) + 1 : 0;
+  const size_t nodes = (size_t)3 * prob->P * prob->v_max * prob->M;
+  // at most 4 GiB of scratch per launch: per group slot the finish times (REORDER: start times
+  // and levels too) and queue rows, per lane the receive keys or the communication items and gap
+  // tables, and the program
+  const size_t per_slot = nodes * (REORDER ? 8 + 8 + 4 : 8) + (size_t)prob->P * queue_cap(prob) * 2;
+  const size_t per_lane = (size_t)ob.rcap * 12 + (size_t)ob.pcap * 4 + (size_t)ob.icap * 16 +
+                          (size_t)ob.pcap2 * 16;
   auto grid_of = [&](auto kern, const Plan& pl, int* g) {
     int rc2 = occupancy_grid(kern, pl.lds_bytes, di.cus, g);
     if (rc2) return rc2;
     *g = (int)std::max<int64_t>(1, std::min<int64_t>(*g, (n + pl.CPW - 1) / pl.CPW));
-    *g = (int)std::min<int64_t>(*g, std::max<int64_t>(1, ((int64_t)4 << 30) / per_slot / pl.CPW));
+    const size_t per_wave = per_slot * pl.CPW + per_lane * WAVE;
+    *g = (int)std::min<int64_t>(*g, std::max<int64_t>(1, (int64_t)(((size_t)4 << 30) / per_wave)));
     return 0;
   };
   // pass 1: rings; pass 2: 40-bit full rows for the orders too wide for the ring
@@ -4784,45 +4856,39 @@ int launch_ordered(const octo_problem* prob, const int64_t* layer_costs, const i
   // group slots: the ring pass's and the full-row pass's share the same buffers (one at a time)
   const size_t slots = std::max({(size_t)grid * su.big.CPW, (size_t)rgrid * std::max(rp.CPW, 0),
                                  (size_t)fgrid * std::max(fp.CPW, 0)});
+  const size_t waves = std::max({(size_t)grid, (size_t)rgrid, (size_t)fgrid});
   const size_t qslots = (size_t)su.mat_grid * su.big.CPW;
   if (slots > qslots) {
     // the queue rows of the workspace cover mat_grid * CPW slots; take a larger workspace
     if ((rc = prepare(prob, layer_costs, nullptr, stream, n, &su, (int64_t)slots))) return rc;
   }
-  OrdBufs ob;
-  ob.rcap = REORDER ? 0 : 2 * prob->v_max * prob->M;
-  ob.pcap = (int)align_up((size_t)7 * prob->v_max * prob->M, 4);  // 16-byte aligned rows
-  // communication items: at most a receive and a send per F or B
-  ob.icap = REORDER ? 4 * prob->v_max * prob->M : 0;
-  const size_t nodes = (size_t)3 * prob->P * prob->v_max * prob->M;
   size_t o = 0;
   auto take = [&](size_t bytes) {
     const size_t at = o;
     o = align_up(o + bytes, 256);
     return at;
   };
+  const size_t lanes = waves * WAVE;
   const size_t o_tb = take(slots * nodes * 8);
-  const size_t o_rk = take(slots * prob->P * ob.rcap * 8);
-  const size_t o_ri = take(slots * prob->P * ob.rcap * 4);
-  const size_t o_pg = take(slots * prob->P * ob.pcap * 4);
+  const size_t o_rk = take(lanes * ob.rcap * 8);
+  const size_t o_ri = take(lanes * ob.rcap * 4);
+  const size_t o_pg = take(lanes * ob.pcap * 4);
   const size_t o_ts = take(REORDER ? slots * nodes * 8 : 0);
   const size_t o_tl = take(REORDER ? slots * nodes * 4 : 0);
-  const size_t o_ik = take(slots * prob->P * ob.icap * 8);
-  const size_t o_il = take(slots * prob->P * ob.icap * 8);
-  const size_t o_ig = take(slots * prob->P * ob.icap * 4);
-  const size_t o_io = take(slots * prob->P * ob.icap * 8);
+  const size_t o_it = take(lanes * ob.icap * 16);
+  const size_t o_ps = take(lanes * ob.pcap2 * 8);
+  const size_t o_pd = take(lanes * ob.pcap2 * 8);
   if ((rc = ensure_buf(su.ws->ord, su.ws->ord_bytes, o, stream))) return rc;
   char* base = static_cast<char*>(su.ws->ord);
   ob.tb = reinterpret_cast<int64_t*>(base + o_tb);
   ob.rkey = reinterpret_cast<int64_t*>(base + o_rk);
   ob.rid = reinterpret_cast<uint32_t*>(base + o_ri);
-  ob.prog = reinterpret_cast<uint32_t*>(base + o_pg);
+  ob.prog = reinterpret_cast<uint4*>(base + o_pg);
   ob.ts = reinterpret_cast<int64_t*>(base + o_ts);
   ob.tl = reinterpret_cast<int32_t*>(base + o_tl);
-  ob.ikey = reinterpret_cast<int64_t*>(base + o_ik);
-  ob.iln = reinterpret_cast<uint64_t*>(base + o_il);
-  ob.igap = reinterpret_cast<int32_t*>(base + o_ig);
-  ob.iord = reinterpret_cast<int32_t*>(base + o_io);
+  ob.items = reinterpret_cast<CItem*>(base + o_it);
+  ob.pst = reinterpret_cast<int64_t*>(base + o_ps);
+  ob.pdur = reinterpret_cast<int64_t*>(base + o_pd);
   ob.stats = stats;
   if (stats) {  // sentinels for the invalid records, which no group takes
     hipLaunchKernelGGL(k_fill_i64, dim3((unsigned)std::min<int64_t>(1024, (2 * n + 255) / 256)),
