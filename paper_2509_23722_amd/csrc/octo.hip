@@ -2110,8 +2110,12 @@ __device__ __forceinline__ int build_program3(const Chunks<VMAX>& c, const uint1
 // announce time, the receiver's clock); both clocks go to h, and the data's arrival h + w is kept
 // in the finish-time buffer at the producer's node (phase B is done with it), where the consumer,
 // a later computation of the same lane, takes it as its input time.
+// Three waves per SIMD for the ideal-start variant (its phases wait on global loads: 27.5 ->
+// 25.1 ms on 65,536 candidates of the P = 8, M = 64 batch, a few registers spilled); the
+// reordering variant keeps its registers (at three waves it spills and slows by a third).
 template <int VMAX, bool RING, bool REORDER>
-__global__ void __launch_bounds__(WAVE) k_ordered(SimArgs a, OrdBufs ob,
+__global__ void __launch_bounds__(WAVE) __attribute__((amdgpu_waves_per_eu(REORDER ? 1 : 3, 8)))
+k_ordered(SimArgs a, OrdBufs ob,
                                                   const int32_t* __restrict__ list,
                                                   const int32_t* __restrict__ list_n,
                                                   int wide_list) {
