@@ -88,7 +88,7 @@ struct SimArgs {
   int64_t qt_end;          // the table's final terminators
   int strm_off;            // LDS byte offset of the per-lane stream table
   // static round schedules (null: every candidate takes the generated-queue kernels): rows of
-  // st_rowlen entries, P + 1 rows per class (one per role, then a row of SC_NOP), st_cls
+  // st_rowlen entries, P + 1 rows per class (one per role, then a row of sc_nop), st_cls
   // entries apart; smeta [NSC][4] = {valid, rounds, slots, 0}
   const uint32_t* stab;
   const int32_t* smeta;
@@ -1046,7 +1046,7 @@ __host__ __device__ inline size_t sc_build_lds(int P, int M) {
 // in a round being free for that round's writers (reads precede writes); then write every
 // device's row of round entries. smeta[class] = {valid, rounds, slots used}; a class is invalid
 // (its candidates take the generated-queue kernels) when its rounds pass nr_cap or it needs more
-// than SC_NEG slots. v = 2 classes need P v_max >= 2 P.
+// than sc_neg(sc_slots(P)) slots. v = 2 classes need P v_max >= 2 P.
 __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
                                                        const uint32_t* __restrict__ mtab,
                                                        uint32_t* __restrict__ stab,
@@ -1059,8 +1059,10 @@ __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
   sc_decode(cls, &v, &gen, &split, &pat);
   uint32_t* rows = stab + cls * cls_stride;
   const int c = lane_id();
+  const int ns = sc_slots(P), neg = sc_neg(ns), dummy = sc_dummy(ns);
+  const uint32_t nop = sc_nop(ns);
   if (v > v_max) {
-    for (int i = c; i < (P + 1) * rowlen; i += WAVE) rows[i] = SC_NOP;
+    for (int i = c; i < (P + 1) * rowlen; i += WAVE) rows[i] = nop;
     if (c == 0) smeta[4 * cls] = 0, smeta[4 * cls + 1] = 0, smeta[4 * cls + 2] = 0;
     return;
   }
@@ -1069,7 +1071,7 @@ __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
   int16_t* rnd = reinterpret_cast<int16_t*>(smem);
   uint8_t* slot = smem + ((size_t)nn * 2 + 15) / 16 * 16;
   uint32_t* ops = reinterpret_cast<uint32_t*>(slot + ((size_t)nn + 15) / 16 * 16);
-  for (int i = c; i < nn; i += WAVE) rnd[i] = -1, slot[i] = SC_DUMMY;
+  for (int i = c; i < nn; i += WAVE) rnd[i] = -1, slot[i] = (uint8_t)dummy;
   __syncthreads();
   const bool lane = c < P;
   int st0 = 0, st1 = 0;
@@ -1111,7 +1113,7 @@ __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
   const int nrounds = round;
   bool valid = __ballot(lane && pos != q) == 0 && nrounds <= nr_cap;
   // pass 2: slots of the cross-device finish times, in round order
-  uint64_t freem = (1ull << SC_NEG) - 1;  // slots 0 .. SC_NEG - 1
+  uint64_t freem = (1ull << neg) - 1;  // slots 0 .. neg - 1
   uint64_t used = 0;
   int p2 = 0;
   for (int r = 0; valid && r < nrounds; ++r) {
@@ -1133,7 +1135,7 @@ __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
       valid = false;
       break;
     }
-    int sl = SC_DUMMY;
+    int sl = dummy;
     if (out) {
       uint64_t x = freem;
       const int rank = __popcll(wm & ((1ull << c) - 1));
@@ -1147,23 +1149,23 @@ __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
     p2 += act ? 1 : 0;
   }
   __syncthreads();
-  // pass 3: the rows (role c; row P is all SC_NOP)
-  for (int i = c; i < rowlen; i += WAVE) rows[(int64_t)P * rowlen + i] = SC_NOP;
+  // pass 3: the rows (role c; row P is all nop)
+  for (int i = c; i < rowlen; i += WAVE) rows[(int64_t)P * rowlen + i] = nop;
   if (lane) {
     uint32_t* row = rows + (int64_t)c * rowlen;
     int p3 = 0;
     for (int r = 0; r < rowlen; ++r) {
-      uint32_t e = SC_NOP;
+      uint32_t e = nop;
       const uint32_t o = valid && p3 < q ? ops[c * q + p3] : 0xFFFFFFFFu;
       if (valid && p3 < q && (int)(o >> 16) == r) {
         const int kind = (o >> 14) & 3, k = (o >> 11) & 7, m = o & 0x7FF;
         const int s = k == 0 ? st0 : st1;
-        int rd = SC_NEG;
+        int rd = neg;
         if (kind == KF && s > 0 && sc_device(pat, P, s - 1) != c)
           rd = slot[sc_node(S, M, KF, s - 1, m)];
         if (kind == KB && s < S - 1 && sc_device(pat, P, s + 1) != c)
           rd = slot[sc_node(S, M, KB, s + 1, m)];
-        const int wr = kind == KW ? SC_DUMMY : slot[sc_node(S, M, kind, s, m)];
+        const int wr = kind == KW ? dummy : slot[sc_node(S, M, kind, s, m)];
         e = sc_entry(rd, kind * v + k, wr);
         ++p3;
       }
@@ -1182,25 +1184,28 @@ __global__ void __launch_bounds__(WAVE) k_static_build(int P, int M, int v_max,
 // each lane runs its role's row of the class's schedule with its candidate's costs. Per round:
 // read the slot its op reads and its stream's {input weight, duration}, start = max(device
 // clock, slot + weight), finish = start + duration, write the finish to the slot its op writes.
-// LDS: each group's 64 slots (64-bit, 512 B per group), then one 512-byte row per stream
-// ({weight, duration} as two uint32 per lane; stream SC_NOP_STREAM is zero), then the staged
-// records. The groups of a wave run one class, so in a round they read and write the same slot
-// numbers: slot k of group g lives at k ^ (9g mod 64), which spreads the groups' accesses over
-// the LDS banks (without it every group hits the same banks; of the XOR steps 4g, 5g, 7g, 9g
-// and 13g, 9g measured fastest on the P = 8, M = 64 batch, 3 % ahead of 4g). A candidate whose
-// weights or durations pass 32 bits goes to the 64-bit redo list.
+// LDS: one 512-byte row per stream ({weight, duration} as two uint32 per lane; stream
+// SC_NOP_STREAM is zero) from offset 0, so that a stream address is (entry & mask) | lane
+// offset; then each group's ns = sc_slots(P) slots (64-bit, 8 ns bytes per group), then the
+// staged records. The groups of a wave run one class, so in a round they read and write the same
+// slot numbers: slot k of group g lives at k ^ (9g mod ns), which spreads the groups' accesses
+// over the LDS banks (without it every group hits the same banks; of the XOR steps 4g, 5g, 7g,
+// 9g and 13g, 9g measured fastest on the P = 8, M = 64 batch, 3 % ahead of 4g). A candidate
+// whose weights or durations pass 32 bits goes to the 64-bit redo list.
 typedef __attribute__((address_space(3))) int64_t lds_i64;
 typedef __attribute__((address_space(3))) uint64_t lds_u64;
 __global__ void __launch_bounds__(WAVE) k_static(SimArgs a, int sbase, int rbase) {
-  extern __shared__ __align__(512) uint8_t st_smem[];
+  extern __shared__ __align__(4096) uint8_t st_smem[];
   const int G = a.G, P = a.pr.P, M = a.pr.M;
   const int g = lane_id() / G;
   const int d = lane_id() % G;
   const int gg = g < a.CPW ? g : 0;
-  const uint32_t lb = (uint32_t)(uintptr_t)st_smem;  // LDS address of the array (512-aligned)
+  const uint32_t lb = (uint32_t)(uintptr_t)st_smem;  // LDS address of the array (4096-aligned)
   // group base | salt: slot addresses are (slot * 8) ^ sg
-  const uint32_t sg = (lb + (uint32_t)gg * 512u) | (((uint32_t)gg * 72u) & 0x1F8u);
-  const uint32_t sb = lb + (uint32_t)sbase + (uint32_t)lane_id() * 8u;
+  const int ns = sc_slots(P);
+  const uint32_t sg = (lb + (uint32_t)sbase + (uint32_t)(gg * ns) * 8u) |
+                      (((uint32_t)gg * 72u) & (uint32_t)(8 * ns - 8));
+  const uint32_t sb = lb + (uint32_t)lane_id() * 8u;
   uint8_t* rec = st_smem + rbase + gg * a.rec_stride;
   // the class bins' counts, first positions and chunk ranges, one class per lane
   const int ci = lane_id();
@@ -1252,7 +1257,7 @@ __global__ void __launch_bounds__(WAVE) k_static(SimArgs a, int sbase, int rbase
       }
     *reinterpret_cast<lds_u64*>((uintptr_t)(sb + SC_NOP_STREAM * 512u)) = 0;
     if (d == 0)
-      *reinterpret_cast<lds_i64*>((uintptr_t)(((uint32_t)SC_NEG * 8u) ^ sg)) =
+      *reinterpret_cast<lds_i64*>((uintptr_t)(((uint32_t)sc_neg(ns) * 8u) ^ sg)) =
           -((int64_t)1 << 62);
     uint64_t gbit, lsb;
     group_bits(G, &gbit, &lsb);
@@ -1275,9 +1280,9 @@ __global__ void __launch_bounds__(WAVE) k_static(SimArgs a, int sbase, int rbase
       *reinterpret_cast<lds_i64*>((uintptr_t)wa) = clock;
     };
     // blocks of four rounds, their entries loaded four blocks ahead (a row is L2-resident, so a
-    // load takes far longer than one block of rounds); a row ends with four blocks of SC_NOP,
+    // load takes far longer than one block of rounds); a row ends with four blocks of sc_nop,
     // so every look-ahead stays in it, and the rounds run in whole groups of four blocks (the
-    // rounds past the class's last are SC_NOP)
+    // rounds past the class's last are sc_nop)
     uint4 q0 = rowp[0], q1 = rowp[1], q2 = rowp[2], q3 = rowp[3];
     auto block = [&](const uint4& q) {
       step(q.x);
@@ -3970,7 +3975,7 @@ TabGeom tab_geom(const octo_problem* p, int lds_max, int v, bool wide) {
 // Geometry of the static round schedules for a problem: rounds a class may take (a lockstep
 // pass takes about a device's op count plus the pipeline depth; twice the largest op count plus
 // four times the stages is a safe cap, a class past it is marked invalid), entries per row (the
-// cap rounded up to whole groups of sixteen rounds, plus sixteen SC_NOP entries for the
+// cap rounded up to whole groups of sixteen rounds, plus sixteen sc_nop entries for the
 // look-ahead of k_static), and the entries per class (P + 1 rows).
 struct StGeom {
   int nr_cap, rowlen;
@@ -4276,14 +4281,15 @@ uint64_t bins_of(int v_lo, int v_hi, bool afab) {
   return m;
 }
 
-// Launch k_static over the class bins: CPW = 64 / G candidates per wave, each group's 64 slots
-// (512 B), the stream rows from the next multiple of 4 KiB (4 KiB), then the staged records.
+// Launch k_static over the class bins: CPW = 64 / G candidates per wave; the eight stream rows
+// (4 KiB), each group's sc_slots(P) slots (256 or 512 B), then the staged records: 6.4 KB per
+// wave at P = 8 (with 64-slot blocks, 8.4 KB and 1.28 instead of 1.13 ms per headline call).
 int launch_static(const SimArgs& base, const Setup& su, int64_t n, hipStream_t stream) {
   SimArgs a = base;
   a.G = lanes_per_candidate(a.pr.P);
   a.CPW = WAVE / a.G;
-  const int sbase = (int)align_up((size_t)a.CPW * 512, 4096);
-  const int rbase = sbase + 8 * 512;
+  const int sbase = 8 * 512;
+  const int rbase = sbase + a.CPW * sc_slots(a.pr.P) * 8;
   const int lds = rbase + a.CPW * a.rec_stride;
   if (lds > su.di.lds_max) return OCTO_OK;  // cannot happen for P <= 64; leave to k_sim
   int grid = 0;

@@ -189,17 +189,24 @@ __host__ __device__ __forceinline__ void sc_stages(int pat, int P, int c, int* s
 }
 
 // Schedule entry of one device in one round: the slot its op reads (a cross-device producer's
-// finish time, else SC_NEG, which holds a time far below zero), the stream of its duration and
-// input weight (kind * v + chunk; SC_NOP_STREAM: zero duration), and the slot it writes (its
-// finish time if another device reads it, else SC_DUMMY). Bits: read slot << 3, stream << 9,
-// write slot << 12, so that address = (entry & mask) | base needs one instruction. A round in
-// which the device runs nothing is SC_NOP.
-constexpr int SC_SLOTS = 64, SC_NEG = 62, SC_DUMMY = 63, SC_NOP_STREAM = 7;
+// finish time, else the sentinel slot sc_neg, which holds a time far below zero), the stream of
+// its duration and input weight (kind * v + chunk; SC_NOP_STREAM: zero duration), and the slot
+// it writes (its finish time if another device reads it, else the sink slot sc_dummy). Bits:
+// read slot << 3, stream << 9, write slot << 12, so that address = (entry & mask) | base needs
+// one instruction. A round in which the device runs nothing is sc_nop.
+// Slots per candidate: 32 up to P = 8 (the classes there keep at most 16 values live at M = 64,
+// and the smaller LDS block lets more waves run), else 64; the last two are the sentinel and the
+// sink. A class that needs more is left to the generated-queue kernels.
+constexpr int SC_NOP_STREAM = 7;
+__host__ __device__ __forceinline__ int sc_slots(int P) { return P <= 8 ? 32 : 64; }
+__host__ __device__ __forceinline__ int sc_neg(int ns) { return ns - 2; }
+__host__ __device__ __forceinline__ int sc_dummy(int ns) { return ns - 1; }
 __host__ __device__ __forceinline__ uint32_t sc_entry(int rd, int stream, int wr) {
   return (uint32_t)rd << 3 | (uint32_t)stream << 9 | (uint32_t)wr << 12;
 }
-constexpr uint32_t SC_NOP = ((uint32_t)SC_NEG << 3) | ((uint32_t)SC_NOP_STREAM << 9) |
-                            ((uint32_t)SC_DUMMY << 12);
+__host__ __device__ __forceinline__ uint32_t sc_nop(int ns) {
+  return sc_entry(sc_neg(ns), SC_NOP_STREAM, sc_dummy(ns));
+}
 
 // ------------------------------------------------------------------------------------------
 // Queue generators. Each lane owns one device queue and walks it front to back. A generator
