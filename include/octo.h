@@ -17,7 +17,8 @@
  * Units: all times are int64 nanoseconds; results are exact integers.
  * Memory: every array pointer passed to octo_sim_batch / octo_tune_step is a DEVICE pointer owned
  * by the caller; problem structs are host memory. The library keeps a private per-(device,
- * stream) workspace that it allocates on first use and grows when needed.
+ * stream) workspace that it allocates on first use and grows when needed, stream-ordered
+ * (hipMallocAsync / hipFreeAsync on the call's stream): no call synchronises the host.
  * Streams: `stream` is a hipStream_t (NULL = the null stream). Calls are asynchronous; results
  * are ready when the stream is synchronised. Concurrent calls on different streams are allowed.
  * Errors: argument problems return a negative status before anything is launched; per-candidate

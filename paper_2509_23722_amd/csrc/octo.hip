@@ -3854,20 +3854,23 @@ Layout layout(const octo_problem* p, const Plan& big, int64_t n, int64_t mat_slo
   return l;
 }
 
-// Grow-only device buffer; the old one is freed after the stream's pending work.
+// Grow-only device buffer, stream-ordered: the old one is released after the work already
+// queued on the stream and the new one serves the work queued after it, so the host never
+// waits (the buffer belongs to this stream's workspace and no other stream uses it).
 int ensure_buf(void*& ptr, size_t& have, size_t bytes, hipStream_t stream) {
   if (have >= bytes) return OCTO_OK;
+  size_t want = std::max(bytes, have * 3 / 2);
   if (ptr) {
-    if (hipStreamSynchronize(stream) != hipSuccess) return OCTO_EHIP;
-    (void)hipFree(ptr);
+    if (hipFreeAsync(ptr, stream) != hipSuccess) return OCTO_EHIP;
     ptr = nullptr;
     have = 0;
   }
-  size_t want = std::max(bytes, have * 3 / 2);
-  if (hipMalloc(&ptr, want) != hipSuccess) {
+  if (hipMallocAsync(&ptr, want, stream) != hipSuccess) {
     ptr = nullptr;
-    if (hipMalloc(&ptr, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    if (hipMallocAsync(&ptr, bytes, stream) != hipSuccess) {
       ptr = nullptr;
+      (void)hipGetLastError();
       return OCTO_ENOMEM;
     }
     want = bytes;
