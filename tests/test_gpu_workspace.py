@@ -1,0 +1,54 @@
+"""Workspace growth on a fresh stream: calls queued back to back, with batches that grow (and
+an entry point with buffers of its own between them), give the oracle's results with no host
+wait between the calls; the workspace of a stream grows in stream order."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import octoref as R
+from paper_2509_23722_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+NTHREADS = min(16, os.cpu_count() or 1)
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    from paper_2509_23722_amd import _lib
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    _lib.lib()
+    return torch.device("cuda:0")
+
+
+def test_growing_batches_on_a_fresh_stream(gpu):
+    import torch
+    from paper_2509_23722_amd import _lib
+    w = I.WORKLOADS[3]
+    costs, link = I.layer_costs(w), I.link_matrix(w.P, w.link_ns)
+    recs = I.candidates(w)[:131072]
+    prob = _lib.problem(w.L, w.P, w.v_max, w.M, recs.shape[1], w.max_pert)
+    c = torch.from_numpy(costs).to(gpu)
+    lk = torch.from_numpy(link).to(gpu)
+    r = torch.from_numpy(recs).to(gpu)
+    torch.cuda.synchronize()
+    plan = [("sim", 64), ("sim", 8192), ("ordered", 1024), ("sim", 131072), ("ordered", 4096),
+            ("sim", 1000)]
+    s = torch.cuda.Stream()
+    outs = []
+    print("workspace: queueing", plan, flush=True)
+    with torch.cuda.stream(s):
+        for kind, n in plan:
+            fn = _lib.sim_batch if kind == "sim" else _lib.sim_batch_ordered
+            outs.append(fn(prob, c, lk, r[:n])[:2])
+    s.synchronize()
+    rp = R.problem(w.L, w.P, w.v_max, w.M, recs.shape[1], w.max_pert)
+    ref = {"sim": R.sim_batch(rp, costs, link, recs, nthreads=NTHREADS),
+           "ordered": R.sim_batch_ordered(rp, costs, link, recs[:4096], nthreads=NTHREADS)}
+    for (kind, n), (ms, bub) in zip(plan, outs):
+        ms, bub = ms.cpu().numpy(), bub.cpu().numpy()
+        rms, rbub = ref[kind][0][:n], ref[kind][1][:n]
+        bad = np.nonzero((ms != rms) | (bub != rbub).any(axis=1))[0]
+        assert len(bad) == 0, f"{kind} n={n}: {len(bad)} differ, first {int(bad[0])}"
