@@ -42,7 +42,10 @@ constexpr int CTL_WIDE = 171;     // perturbed candidates whose queue window pas
 constexpr int CTL_WORK_WIDE = 172;// chunk counter of k_sim_mat40 over the wide list
 constexpr int CTL_TOTAL = 173;    // valid records (all bins; set by k_plan)
 constexpr int CTL_START = 176;    // [NBINS] first index position of each bin
+constexpr int CTL_WORK_V = 241;   // chunk counters of the v = 3..8 k_sim launches (6), then of
+                                  // their rendezvous GPipe launches (6)
 constexpr int CTL_WORDS = 256;
+static_assert(CTL_START + NBINS <= CTL_WORK_V && CTL_WORK_V + 12 <= CTL_WORDS, "control words");
 static_assert(NBINS <= 80, "bin arrays of the control block hold 80 bins");
 // rounds a materialised queue is read ahead of its use (GenMatK; rows of at least 8 entries)
 constexpr int QK = 6;
@@ -3670,7 +3673,7 @@ struct Workspace {
   size_t mr_bytes = 0;
   // largest number of micro-batches in flight per stage, per generated bin of v = 1, 2
   int inflight[NBIN_GEN] = {};
-  int if_P = 0, if_M = 0;
+  int if_P = 0, if_M = 0, if_vmax = 0;
   // queue tables for v <= 2 (INTER by rank, MERGE by stage pair), same cache key as mt
   void* qt = nullptr;
   size_t qt_bytes = 0;
@@ -3936,15 +3939,15 @@ int inflight_inter(int P, int v, int M, int r, int split, int lag) {
   return worst;
 }
 
-// Per generated bin of v = 1, 2: the in-flight bound of its queues. INTER queues depend on the
+// Per generated bin of v <= v_max: the in-flight bound of its queues. INTER queues depend on the
 // device's first stage r; a MERGE queue keeps, for each of its stages s, the order of stage s in
 // the ideal stage-level schedule (interleaved order on S devices, v = 1, device s), so its bound
 // is the largest over those orders. AFAB keeps all M micro-batches in flight.
 void compute_inflight(const octo_problem* p, Workspace& ws) {
-  if (ws.if_P == p->P && ws.if_M == p->M) return;
+  if (ws.if_P == p->P && ws.if_M == p->M && ws.if_vmax == p->v_max) return;
   const int P = p->P, M = p->M;
   for (int b = 0; b < NBIN_GEN; ++b) ws.inflight[b] = M;
-  for (int v = 1; v <= 2; ++v) {
+  for (int v = 1; v <= p->v_max; ++v) {
     for (int split = 0; split <= 1; ++split) {
       int wi = 0, wm = 0;
       for (int r = 0; r < P; ++r)
@@ -3956,7 +3959,7 @@ void compute_inflight(const octo_problem* p, Workspace& ws) {
       ws.inflight[bin_of(v, GEN_MERGE, split)] = wm;
     }
   }
-  ws.if_P = P, ws.if_M = M;
+  ws.if_P = P, ws.if_M = M, ws.if_vmax = p->v_max;
 }
 
 // Launch geometry of the table-driven k_sim launch for v (1 or 2): ring rows and plan.
@@ -4508,9 +4511,9 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
     }
   }
   if ((rc = classify_sort(prob, su, a, n, stream))) return rc;
-  // generated INTER / MERGE queues, one launch per v class with finish tables sized for it:
-  // v = 2, v = 1, v = 3..8 (ring rows where the in-flight bound allows); then AFAB queues; then
-  // materialised queues (perturbations, 64-bit redo).
+  // generated INTER / MERGE queues, one launch per v with finish tables sized for it (ring
+  // rows of the next power of two >= P v where the in-flight bound allows): v = 2, v = 1, then
+  // v = 3..8; then AFAB queues; then materialised queues (perturbations, 64-bit redo).
   compute_inflight(prob, *su.ws);
   if (X != XS && X != XR && (rc = build_qtab(prob, *su.ws, su.di.lds_max, X != XP, stream)))
     return rc;
@@ -4527,10 +4530,11 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
                              P, P, bins_of(1, 1, false), CTL_WORK + 0, stream)))
     return rc;
   if ((rc = record_mark(3, stream))) return rc;
-  if (prob->v_max >= 3 &&
-      (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
-                             P * prob->v_max, M, bins_of(3, 8, false), CTL_WORK + 2, stream)))
-    return rc;
+  for (int v = 3; v <= prob->v_max; ++v)
+    if ((rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                               bd, P * v, P * v, bins_of(v, v, false), CTL_WORK_V + v - 3,
+                               stream)))
+      return rc;
   if ((rc = record_mark(4, stream))) return rc;
   if constexpr (X != XR) {
     if ((rc = launch_afab<X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm, bd,
@@ -4546,11 +4550,11 @@ int sim_batch_run(const octo_problem* prob, const int64_t* layer_costs, const in
     if ((rc = launch_sim<1, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
                                bd, P, 1, bins_of(1, 1, true), CTL_WORK + 5, stream, true)))
       return rc;
-    if (prob->v_max >= 3 &&
-        (rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
-                               bd, P * prob->v_max, 1, bins_of(3, 8, true), CTL_WORK + 6, stream,
-                               true)))
-      return rc;
+    for (int v = 3; v <= prob->v_max; ++v)
+      if ((rc = launch_sim<8, X>(prob, su, link, candidates, n, out_makespan, out_bubble, pk, cm,
+                                 bd, P * v, 1, bins_of(v, v, true), CTL_WORK_V + 6 + v - 3,
+                                 stream, true)))
+        return rc;
   }
   if ((rc = record_mark(5, stream))) return rc;
   // candidates with moves: 40-bit rings, 40-bit full rows for those wider than the ring, then

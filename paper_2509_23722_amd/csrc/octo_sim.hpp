@@ -218,12 +218,18 @@ struct Lane : Desc {
   int tS, tM, rnd;
 };
 
+// Entry k of a per-chunk array: a select chain while the arrays stay in registers (v <= 2);
+// the eight-chunk arrays live in private memory, where one indexed load beats reading all eight.
 template <int VMAX, typename T>
 __device__ __forceinline__ T pick(const T (&a)[VMAX], int k) {
-  T x = a[0];
+  if constexpr (VMAX > 2) {
+    return a[k];
+  } else {
+    T x = a[0];
 #pragma unroll
-  for (int i = 1; i < VMAX; ++i) x = k == i ? a[i] : x;
-  return x;
+    for (int i = 1; i < VMAX; ++i) x = k == i ? a[i] : x;
+    return x;
+  }
 }
 
 // Describe op (kind, chunk k, micro-batch m).
