@@ -78,7 +78,8 @@ struct Resolved {
 
 // Validity, looped-placement and balanced-placement tests of one record.
 // head: the record's first pert_off(s_max) bytes (may be a staged copy); pert: its perturbation
-// list (in the record itself).
+// list (in the record itself). The stage loops run to the end and fold their tests into one
+// flag (no early exit per lane: the lanes of a wave would otherwise leave at different stages).
 __device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint8_t* head,
                                                   const uint8_t* pert) {
   const uint8_t* rec = head;
@@ -94,25 +95,51 @@ __device__ __forceinline__ Resolved resolve_record(const Problem& pr, const uint
   const int S = r.S;
   const uint8_t* bnd = rec + 4;
   const uint8_t* dev = rec + 3 + pr.s_max;
+  bool ok = true;
   int prev = 0;
+#pragma unroll 8
   for (int s = 1; s < S; ++s) {
-    int b = bnd[s - 1];
-    if (b <= prev) return r;
+    const int b = bnd[s - 1];
+    ok &= b > prev;
     prev = b;
   }
-  if (pr.L <= prev) return r;
-  // balanced placement: every device exactly v stages (counts kept as 4-bit fields)
-  uint64_t cnt[4] = {0, 0, 0, 0};
+  ok &= prev < pr.L;
+  // balanced placement: every device at most (so exactly) v stages, counted in 4-bit fields
+  // (one 64-bit word up to P = 16, four beyond); looped: stage s on the device of s mod P
   bool looped = true;
-  for (int s = 0; s < S; ++s) {
-    int d = dev[s];
-    if (d >= pr.P) return r;
-    int w = d >> 4, sh = (d & 15) * 4;
-    uint64_t c = (cnt[w] >> sh) & 15;
-    if ((int)c >= v) return r;
-    cnt[w] += (uint64_t)1 << sh;
-    if (s >= pr.P && dev[s] != dev[s % pr.P]) looped = false;
+  int j = 0;
+  if (pr.P <= 16) {
+    uint64_t c = 0;
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) {
+      const int d = dev[s];
+      ok &= d < pr.P;
+      const int sh = (d & 15) * 4;
+      const bool room = (int)((c >> sh) & 15) < v;
+      ok &= room;
+      c += room ? (uint64_t)1 << sh : 0;
+      looped &= s < pr.P || d == dev[j];
+      j = j + 1 == pr.P ? 0 : j + 1;
+    }
+  } else {
+    uint64_t c0 = 0, c1 = 0, c2 = 0, c3 = 0;
+    for (int s = 0; s < S; ++s) {
+      const int d = dev[s];
+      ok &= d < pr.P;
+      const int w = (d >> 4) & 3, sh = (d & 15) * 4;
+      const uint64_t cw = w == 0 ? c0 : w == 1 ? c1 : w == 2 ? c2 : c3;
+      const bool room = (int)((cw >> sh) & 15) < v;
+      ok &= room;
+      const uint64_t inc = room ? (uint64_t)1 << sh : 0;
+      c0 += w == 0 ? inc : 0;
+      c1 += w == 1 ? inc : 0;
+      c2 += w == 2 ? inc : 0;
+      c3 += w == 3 ? inc : 0;
+      looped &= s < pr.P || d == dev[j];
+      j = j + 1 == pr.P ? 0 : j + 1;
+    }
   }
+  if (!ok) return r;
   // every device got v stages: total S = P v stages and no device exceeds v
   if (policy == POL_AFAB) {
     r.gen = GEN_AFAB;
@@ -164,6 +191,7 @@ __device__ __forceinline__ int static_class(const Problem& pr, const uint8_t* de
   if (r.v == 1) return r.split ? 1 : 0;
   const int P = pr.P;
   bool lp = true, bl = true, vs = true;
+#pragma unroll 4
   for (int i = 0; i < P; ++i) {
     lp = lp && dev[i] == dev[i + P];
     bl = bl && dev[2 * i] == dev[2 * i + 1];
