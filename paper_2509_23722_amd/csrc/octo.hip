@@ -648,8 +648,10 @@ __global__ void k_plan(int32_t* __restrict__ ctl) {
 }
 
 // Index of every valid record at its bin's cursor; blocks cover the same CLS_ITEMS runs as
-// k_classify: the runs' bins are counted first, one global atomic per bin reserves the block's
-// positions, then each run takes its part in order.
+// k_classify: counting the runs' bins gives each record its place among the block's records of
+// its bin, one global atomic per bin reserves the block's positions, then every record is
+// written at the block's position plus its place (the order inside a block's range follows the
+// order in which its waves counted; every consumer handles its bin's records independently).
 __global__ void __launch_bounds__(CLS_THREADS) k_scatter(SimArgs a, const uint8_t* __restrict__ bins,
                                                          int32_t* __restrict__ idx) {
   __shared__ int hist[NBINS];
@@ -658,24 +660,22 @@ __global__ void __launch_bounds__(CLS_THREADS) k_scatter(SimArgs a, const uint8_
   __syncthreads();
   const int64_t n = live_count(a);
   const int64_t first = (int64_t)blockIdx.x * CLS_ITEMS * CLS_THREADS + threadIdx.x;
-  int bin[CLS_ITEMS];
+  int bin[CLS_ITEMS], local[CLS_ITEMS];
 #pragma unroll
   for (int run = 0; run < CLS_ITEMS; ++run) {
     const int64_t i = first + run * CLS_THREADS;
     bin[run] = i < n ? bins[i] : BIN_NONE;
-    wave_hist_add(hist, bin[run], bin[run] != BIN_NONE);
   }
+#pragma unroll
+  for (int run = 0; run < CLS_ITEMS; ++run)
+    local[run] = wave_hist_add(hist, bin[run], bin[run] != BIN_NONE);
   __syncthreads();
-  for (int b = threadIdx.x; b < NBINS; b += blockDim.x) {
+  for (int b = threadIdx.x; b < NBINS; b += blockDim.x)
     res[b] = hist[b] ? atomicAdd(&a.ctl[CTL_POS + b], hist[b]) : 0;
-    hist[b] = 0;
-  }
   __syncthreads();
 #pragma unroll
-  for (int run = 0; run < CLS_ITEMS; ++run) {
-    const int local = wave_hist_add(hist, bin[run], bin[run] != BIN_NONE);
-    if (bin[run] != BIN_NONE) idx[res[bin[run]] + local] = (int32_t)(first + run * CLS_THREADS);
-  }
+  for (int run = 0; run < CLS_ITEMS; ++run)
+    if (bin[run] != BIN_NONE) idx[res[bin[run]] + local[run]] = (int32_t)(first + run * CLS_THREADS);
 }
 
 // The chunks of the bins in `mask` (bins < nbins <= 64), one bin per lane: its candidate count,
