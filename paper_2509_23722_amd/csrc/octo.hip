@@ -811,6 +811,7 @@ __device__ __forceinline__ int64_t sweep_row(int64_t* row, int stride, int M, in
 template <int MMAX>
 struct AfabRow {
   int64_t r[MMAX];
+  __device__ __forceinline__ bool overflow() const { return false; }
   __device__ __forceinline__ void init(uint8_t*, int, int) {}
   __device__ __forceinline__ void clear(int) {
 #pragma unroll
@@ -857,6 +858,7 @@ template <>
 struct AfabRow<0> {
   int64_t* row;
   int stride;
+  __device__ __forceinline__ bool overflow() const { return false; }
   __device__ __forceinline__ void init(uint8_t* base, int li, int lanes) {
     row = reinterpret_cast<int64_t*>(base) + li;
     stride = lanes;
@@ -895,20 +897,85 @@ struct AfabRow<0> {
 // zero leaves fin(0, m) = dur + fin(0, m - 1).
 constexpr int64_t AFAB_NO_INPUT = -((int64_t)1 << 62);
 
+// A row of a k_afab lane as the upper envelope of at most K lines over 0 <= m < M (the plain,
+// memory and bounds variants). A row's finishes f(m) = max(f(m - 1), r(m) + w) + dur unroll to
+// the largest of c + (m + 1) dur (c: the device clock before the row) and, over k <= m, of
+// r(k) + w + (m - k + 1) dur. With the previous row r(k) = max_i (a_i + k b_i), the largest
+// a_i + k b_i + (m - k) dur over k <= m is a_i + m max(b_i, dur) (at k = m or k = 0), so f is
+// again a maximum of lines: every line with b_i <= dur joins the clock in one line of slope dur,
+// (max(c, a_i + w) + dur) + m dur, and each steeper one keeps its slope, shifted by w + dur. A
+// steeper line no higher than the joined one at m = M - 1 stays under it on the whole row and is
+// dropped. Each line is kept as its values at m = 0 and m = M - 1 and its slope, so a row costs
+// one multiplication. Exact; a candidate whose envelope needs more than K lines (slopes that no
+// later row's duration reaches) is flagged and goes to the 64-bit redo list. The first row (r = 0
+// everywhere) is the line (0, 0); an empty slot is the line AFAB_EMPTY of slope 0.
+constexpr int64_t AFAB_EMPTY = -((int64_t)1 << 62);
+template <int K>
+struct AfabLines {
+  int64_t v0[K], v1[K], b[K];
+  bool over;
+  __device__ __forceinline__ void init(uint8_t*, int, int) {}
+  __device__ __forceinline__ void clear(int) {
+#pragma unroll
+    for (int i = 0; i < K; ++i) v0[i] = v1[i] = i == 0 ? 0 : AFAB_EMPTY, b[i] = 0;
+    over = false;
+  }
+  __device__ __forceinline__ bool overflow() const { return over; }
+  __device__ __forceinline__ int64_t first() const {
+    int64_t x = v0[0];
+#pragma unroll
+    for (int i = 1; i < K; ++i) x = v0[i] > x ? v0[i] : x;
+    return x;
+  }
+  __device__ __forceinline__ int64_t sweep(int M, int64_t c, int64_t w, int64_t dur) {
+    int64_t low = c;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+      const int64_t y = v0[i] + w;
+      low = b[i] <= dur && y > low ? y : low;
+    }
+    const int64_t n0 = low + dur, n1 = n0 + (int64_t)(M - 1) * dur;
+    int64_t fend = n1;
+    bool placed = false;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+      const int64_t s0 = v0[i] + w + dur, s1 = v1[i] + w + dur;
+      const bool keep = b[i] > dur && s1 > n1;
+      const bool put = !keep && !placed;
+      v0[i] = keep ? s0 : put ? n0 : AFAB_EMPTY;
+      v1[i] = keep ? s1 : put ? n1 : AFAB_EMPTY;
+      b[i] = keep ? b[i] : put ? dur : 0;
+      fend = keep && s1 > fend ? s1 : fend;
+      placed = placed || put;
+    }
+    over = over || !placed;
+    return fend;
+  }
+};
+
 // XM: a GPipe device holds every micro-batch of all its stages after its forwards, so its peak
 // is its static bytes + M x its stages' activation bytes. XC: rows tally communication nodes,
 // each device's last op start and pending transfer end kept after its clock and busy time. XS:
 // a row whose outputs cross devices queues them on its link, whose free time it takes from the
 // latest earlier row on the same directed link (rows are visited in every device's op order,
 // so that is the link's issue order); the row then holds arrival times, read with weight 0.
+// MMAX: -1 rows as line envelopes (AfabLines), else AfabRow<MMAX>.
+template <int MMAX>
+struct AfabRowOf {
+  using type = AfabRow<MMAX>;
+};
+template <>
+struct AfabRowOf<-1> {
+  using type = AfabLines<8>;
+};
 template <int MMAX, int X>
-__global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
+__global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off, int rec_off) {
   constexpr bool MEM = X == XM;
   extern __shared__ __align__(16) uint8_t smem[];
   const int lane = lane_id();
   const int P = a.pr.P, M = a.pr.M, L = a.pr.L;
   const int li = lane < lanes ? lane : 0;
-  AfabRow<MMAX> row;
+  typename AfabRowOf<MMAX>::type row;
   row.init(smem, li, lanes);
   int64_t* clk = reinterpret_cast<int64_t*>(smem) + (MMAX == 0 ? (size_t)M * lanes : 0) + li;
   int64_t* bsy = clk + (size_t)P * lanes;  // clk[d * lanes], bsy[d * lanes]
@@ -917,6 +984,16 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
   int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
   int64_t* lfr = bsy + (size_t)P * lanes;  // XS: link free time after row t, lfr[t * lanes]
   int64_t* bfs = bsy + (size_t)P * lanes;  // XB: first start bfs[d * lanes] (-1 before)
+  // the prefix sums of the layer costs (and of the memory model), and the link matrix, staged
+  // in LDS after the lanes' arrays: every row reads them
+  int64_t* pre = reinterpret_cast<int64_t*>(smem + tab_off);
+  int64_t* pmem = pre + 3 * (L + 1);
+  int64_t* link = pmem + (MEM ? 2 * (L + 1) : 0);
+  for (int i = lane; i < 3 * (L + 1); i += WAVE) pre[i] = a.pre[i];
+  if constexpr (MEM)
+    for (int i = lane; i < 2 * (L + 1); i += WAVE) pmem[i] = a.pre_mem[i];
+  for (int i = lane; i < P * P; i += WAVE) link[i] = a.link[i];
+  __syncthreads();
   ChunkMap cmap;
   cmap.init(a.ctl, lanes, a.bin_mask, NBIN_GEN);
   // chunks by grid stride: AFAB candidates of one bin cost alike, and an atomic work counter
@@ -930,7 +1007,13 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
     const int e = entry0 + lane;
     if (lane >= lanes || e >= cnt) continue;
     const int64_t cand = a.idx[pos0 + e];
-    const uint8_t* rec = a.cands + cand * a.pr.stride;
+    // the record's head (header, boundaries, placement), staged in LDS: every row reads it
+    const int hq = (pert_off(a.pr.s_max) + 15) / 16;
+    uint8_t* rec = smem + rec_off + (size_t)lane * hq * 16;
+    {
+      const uint4* src = reinterpret_cast<const uint4*>(a.cands + cand * a.pr.stride);
+      for (int j = 0; j < hq; ++j) reinterpret_cast<uint4*>(rec)[j] = src[j];
+    }
     const uint8_t* bnd = rec + 4;
     const uint8_t* dev = rec + 3 + a.pr.s_max;
     const int S = P * v;
@@ -949,19 +1032,19 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
       const int st = fwd ? t : 2 * S - 1 - t;
       const int d = dev[st];
       const int b0 = st > 0 ? bnd[st - 1] : 0, b1 = st < S - 1 ? bnd[st] : L;
-      const int64_t df = a.pre[3 * b1] - a.pre[3 * b0];
-      const int64_t db = a.pre[3 * b1 + 1] - a.pre[3 * b0 + 1] + a.pre[3 * b1 + 2] -
-                         a.pre[3 * b0 + 2];
+      const int64_t df = pre[3 * b1] - pre[3 * b0];
+      const int64_t db = pre[3 * b1 + 1] - pre[3 * b0 + 1] + pre[3 * b1 + 2] -
+                         pre[3 * b0 + 2];
       if (fwd) bsy[d * lanes] += (df + db) * M;
       if constexpr (MEM) {
         if (fwd)
-          pk[d * lanes] += (a.pre_mem[2 * b1] - a.pre_mem[2 * b0]) * M +
-                           a.pre_mem[2 * b1 + 1] - a.pre_mem[2 * b0 + 1];
+          pk[d * lanes] += (pmem[2 * b1] - pmem[2 * b0]) * M +
+                           pmem[2 * b1 + 1] - pmem[2 * b0 + 1];
       }
       // the stage whose finish times this row consumes: st - 1 (forward), st + 1 (backward)
       const int q = fwd ? st - 1 : st + 1;
       const int dq = q >= 0 && q < S && t != S ? dev[q] : d;
-      const int64_t w = (fwd && st == 0) ? AFAB_NO_INPUT : dq != d ? a.link[dq * P + d] : 0;
+      const int64_t w = (fwd && st == 0) ? AFAB_NO_INPUT : dq != d ? link[dq * P + d] : 0;
       if constexpr (X == XB) {
         // the device's first op is micro-batch 0 of its first row
         if (bfs[d * lanes] < 0) {
@@ -982,7 +1065,7 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
               lf = lfr[u * lanes] > lf ? lfr[u * lanes] : lf;
           }
           clk[d * lanes] = row.sweep_s(M, clk[d * lanes], wr, fwd ? df : db,
-                                       a.link[d * P + dout], lf);
+                                       link[d * P + dout], lf);
           lfr[t * lanes] = lf;
         } else {
           clk[d * lanes] = row.sweep(M, clk[d * lanes], wr, fwd ? df : db);
@@ -995,11 +1078,15 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes) {
         const int cx = (dq != d ? CX_IN : 0) | (dout != d ? CX_OUT : 0);
         acc.pst = cps[d * lanes], acc.pend = cpe[d * lanes];
         clk[d * lanes] = row.sweep_c(M, clk[d * lanes], w, fwd ? df : db, cx,
-                                     dout != d ? a.link[d * P + dout] : 0, acc);
+                                     dout != d ? link[d * P + dout] : 0, acc);
         cps[d * lanes] = acc.pst, cpe[d * lanes] = acc.pend;
       } else {
         clk[d * lanes] = row.sweep(M, clk[d * lanes], w, fwd ? df : db);
       }
+    }
+    if (row.overflow()) {  // more lines than the envelope holds: the 64-bit path
+      a.redo[atomicAdd(&a.ctl[CTL_REDO], 1)] = (int32_t)cand;
+      continue;
     }
     int64_t ms = 0;
     for (int d = 0; d < P; ++d) ms = clk[d * lanes] > ms ? clk[d * lanes] : ms;
@@ -4355,15 +4442,26 @@ template <int X>
 int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, const void* cands,
                 int64_t n, int64_t* ms, int64_t* bub, int64_t* peak, int64_t* comm,
                 int64_t* bound, hipStream_t stream) {
-  // rows of exactly 32 or 64 micro-batches live in registers; other lengths, and the rows of
-  // the communication variant (whose unrolled sweep would not fit the register file), in LDS
-  const int mmax = X == XC ? 0 : prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
+  // rows as line envelopes (plain, memory and bounds variants); the communication and
+  // serialised-link variants, which need every op, keep rows of exactly 32 or 64 micro-batches
+  // in registers and other lengths (and the communication variant's, whose unrolled sweep would
+  // not fit the register file) in LDS
+  constexpr bool LINES = X == XP || X == XM || X == XB;
+  const int mmax = LINES ? -1 : X == XC ? 0 : prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
   const int words = (X == XM || X == XB) ? 3 : X == XC ? 4 : 2;  // per device
   const size_t per_lane =
-      (size_t)((mmax ? 0 : prob->M) + words * prob->P + (X == XS ? 2 * prob->P * prob->v_max : 0)) *
+      (size_t)((mmax == 0 ? prob->M : 0) + words * prob->P +
+               (X == XS ? 2 * prob->P * prob->v_max : 0)) *
       8;
   const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
-  const int lds = (int)(lanes * per_lane);
+  // then the staged tables: prefix sums (and memory prefix sums) and the link matrix
+  const int tab_off = (int)align_up(lanes * per_lane, 16);
+  const int rec_off = tab_off + (int)(((size_t)3 * (prob->L + 1) +
+                                       (X == XM ? (size_t)2 * (prob->L + 1) : 0) +
+                                       (size_t)prob->P * prob->P) *
+                                      8);
+  // then each lane's staged record head
+  const int lds = rec_off + lanes * (int)align_up(pert_off(prob->P * prob->v_max), 16);
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub, peak);
   a.out_comm = comm;
@@ -4371,18 +4469,25 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
   a.bin_mask = bins_of(1, prob->v_max, true);
   a.work = CTL_WORK + 3;
   int grid = 0;
-  int rc = mmax == 32   ? occupancy_grid(k_afab<32, X>, lds, su.di.cus, &grid)
-           : mmax == 64 ? occupancy_grid(k_afab<64, X>, lds, su.di.cus, &grid)
-                        : occupancy_grid(k_afab<0, X>, lds, su.di.cus, &grid);
-  if (rc) return rc;
   const int64_t need = (n + lanes - 1) / lanes;
-  grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
-  if (mmax == 32)
-    hipLaunchKernelGGL((k_afab<32, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
-  else if (mmax == 64)
-    hipLaunchKernelGGL((k_afab<64, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
-  else
-    hipLaunchKernelGGL((k_afab<0, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes);
+  if constexpr (LINES) {
+    const int rc = occupancy_grid(k_afab<-1, X>, lds, su.di.cus, &grid);
+    if (rc) return rc;
+    grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+    hipLaunchKernelGGL((k_afab<-1, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes, tab_off, rec_off);
+  } else {
+    const int rc = mmax == 32   ? occupancy_grid(k_afab<32, X>, lds, su.di.cus, &grid)
+                   : mmax == 64 ? occupancy_grid(k_afab<64, X>, lds, su.di.cus, &grid)
+                                : occupancy_grid(k_afab<0, X>, lds, su.di.cus, &grid);
+    if (rc) return rc;
+    grid = (int)std::max<int64_t>(1, std::min<int64_t>(grid, need));
+    if (mmax == 32)
+      hipLaunchKernelGGL((k_afab<32, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes, tab_off, rec_off);
+    else if (mmax == 64)
+      hipLaunchKernelGGL((k_afab<64, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes, tab_off, rec_off);
+    else
+      hipLaunchKernelGGL((k_afab<0, X>), dim3(grid), dim3(WAVE), lds, stream, a, lanes, tab_off, rec_off);
+  }
   return launch_ok();
 }
 
