@@ -517,6 +517,11 @@ def main():
                             "candidates_per_s": round(cnt / (float(kms) * 1e-3), 1),
                             "alg_lane_ops": work,
                             "frac": round(work / (float(kms) * 1e-3) / 1e12 / PEAK_VALU_TOPS, 5)}
+            if kname == "k_afab":
+                strata[name]["work_priced_as"] = (
+                    "the GPipe row sweep (an add, a max and an add per op); the kernel evaluates "
+                    "each row as an envelope of at most eight lines, fewer operations for the "
+                    "same times")
     roofline = {
         "bound": "alu", "achieved": round(achieved, 3), "peak": round(PEAK_VALU_TOPS, 2),
         "unit": "Tops/s (32-bit VALU lane-ops)", "frac": round(achieved / PEAK_VALU_TOPS, 5),
