@@ -3671,12 +3671,15 @@ __global__ void __launch_bounds__(WAVE) k_alg1_insert(SimArgs a, A1Args b,
       int jk = -1;
       if (d < G && k >= 1 && k < nq) {
         const int64_t t = thr[k];
+        // the first later op ready by t: eight readiness times loaded together per step
         if (t >= 0)
-          for (int j = k + 1; j < nq; ++j)
-            if (rdy[j] <= t) {
-              jk = j;
-              break;
-            }
+          for (int j0 = k + 1; j0 < nq && jk < 0; j0 += 8) {
+            int64_t r8[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) r8[u] = j0 + u < nq ? rdy[j0 + u] : INT64_MAX;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) jk = jk < 0 && r8[u] <= t ? j0 + u : jk;
+          }
       }
       const uint64_t gm = (__ballot(jk >= 0) >> g0) & gmask;
       const int at = found + __popcll(gm & ((1ull << d) - 1));
