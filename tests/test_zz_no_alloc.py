@@ -70,6 +70,21 @@ def test_two_calls_second_smaller(gpu):
     assert_same(*out, "P=8 M=32 batch")
 
 
+def test_deeper_interleaving(gpu):
+    """v up to 4 (one generated-queue launch per v, each with its own work counter in the
+    scratch's control block), with moves and invalid records."""
+    rng = np.random.default_rng(78)
+    L, P, v_max, M = 24, 4, 4, 24
+    log(f"noalloc: random P={P} v_max={v_max} M={M}, 2000 candidates")
+    costs = rng.integers(1, 3_000_000, size=(L, 3)).astype(np.int64)
+    link = rng.integers(0, 800_000, size=(P, P)).astype(np.int64)
+    recs = I.random_candidates(rng, L, P, v_max, M, 2000, max_pert=2, pert_rate=0.2,
+                               invalid_rate=0.05)
+    out = both(gpu, L, P, v_max, M, 2, costs, link, recs)
+    assert_same(*out, "v_max = 4 batch")
+    assert (recs[:, 1] >= 3).sum() > 500
+
+
 def test_too_large_for_the_scratch(gpu):
     import ctypes
     import torch
