@@ -81,11 +81,16 @@ def _check(rc, what):
         raise RuntimeError(f"{what} failed: {lib().octo_strerror(rc).decode()} (status {rc})")
 
 
-def _dev_ptr(t, dtype, name):
+def _dev_ptr(t, dtype, name, numel):
+    """The device address of a contiguous tensor of `dtype` holding exactly `numel` elements
+    (the library takes plain pointers and cannot check the extents itself)."""
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise TypeError(f"{name} must be a CUDA (HIP) tensor")
     if t.dtype != dtype or not t.is_contiguous():
         raise TypeError(f"{name} must be a contiguous {dtype} tensor")
+    if t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements, not {t.numel()} "
+                         f"(shape {tuple(t.shape)})")
     return ctypes.c_void_p(t.data_ptr())
 
 
@@ -116,10 +121,10 @@ def sim_batch(prob, layer_costs, link, candidates, out_makespan=None, out_bubble
     if out_bubble is None:
         out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch")
     return out_makespan, out_bubble
 
@@ -130,10 +135,10 @@ def sim_batch_noalloc(prob, layer_costs, link, candidates, out_makespan, out_bub
     buffer in the library's static device scratch (nothing is allocated by the call)."""
     n = candidates.shape[0]
     rc = lib().octo_sim_batch_noalloc(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_noalloc")
     return out_makespan, out_bubble
 
@@ -151,12 +156,12 @@ def sim_batch_mem(prob, layer_costs, layer_mem, link, candidates, out_makespan=N
     if out_peak is None:
         out_peak = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_mem(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(layer_mem, torch.int64, "layer_mem"), _dev_ptr(link, torch.int64, "link"),
-        _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_peak, torch.int64, "out_peak"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(layer_mem, torch.int64, "layer_mem", 2 * prob.L), _dev_ptr(link, torch.int64, "link", prob.P * prob.P),
+        _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_peak, torch.int64, "out_peak", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_mem")
     return out_makespan, out_bubble, out_peak
 
@@ -172,10 +177,10 @@ def sim_batch_serial(prob, layer_costs, link, candidates, out_makespan=None, out
     if out_bubble is None:
         out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_serial(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_serial")
     return out_makespan, out_bubble
 
@@ -191,10 +196,10 @@ def sim_batch_rdv(prob, layer_costs, link, candidates, out_makespan=None, out_bu
     if out_bubble is None:
         out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_rdv(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_rdv")
     return out_makespan, out_bubble
 
@@ -210,10 +215,10 @@ def sim_batch_ordered(prob, layer_costs, link, candidates, out_makespan=None, ou
     if out_bubble is None:
         out_bubble = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_ordered(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_ordered")
     return out_makespan, out_bubble
 
@@ -232,11 +237,11 @@ def sim_batch_reorder(prob, layer_costs, link, candidates, out_makespan=None, ou
     if out_stats is None:
         out_stats = torch.empty((n, 2), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_reorder(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_stats, torch.int64, "out_stats"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_stats, torch.int64, "out_stats", 2 * n), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_reorder")
     return out_makespan, out_bubble, out_stats
 
@@ -254,11 +259,11 @@ def sim_batch_bounds(prob, layer_costs, link, candidates, out_makespan=None, out
     if out_bounds is None:
         out_bounds = torch.empty((n, prob.P, 2), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_bounds(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_bounds, torch.int64, "out_bounds"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_bounds, torch.int64, "out_bounds", 2 * n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_bounds")
     return out_makespan, out_bubble, out_bounds
 
@@ -276,11 +281,11 @@ def sim_batch_comm(prob, layer_costs, link, candidates, out_makespan=None, out_b
     if out_comm is None:
         out_comm = torch.empty((n, 4), dtype=torch.int64, device=dev)
     rc = lib().octo_sim_batch_comm(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_comm, torch.int64, "out_comm"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_comm, torch.int64, "out_comm", 4 * n), _stream(candidates, stream))
     _check(rc, "octo_sim_batch_comm")
     return out_makespan, out_bubble, out_comm
 
@@ -292,9 +297,9 @@ def tune_step(prob, layer_costs, link, chains, queues, seed, step, stream=None):
     if q.dtype not in (torch.int16, torch.uint16):
         raise TypeError("queues must be a 16-bit tensor")
     rc = lib().octo_tune_step(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(chains, torch.uint8, "chains"),
-        _dev_ptr(q, q.dtype, "queues"), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(chains, torch.uint8, "chains", n * chain_stride(prob)),
+        _dev_ptr(q, q.dtype, "queues", n * prob.P * queue_capacity(prob)), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
         _stream(chains, stream))
     _check(rc, "octo_tune_step")
 
@@ -308,11 +313,11 @@ def tune_step_mem(prob, layer_costs, layer_mem, capacity, max_advance, link, cha
     if q.dtype not in (torch.int16, torch.uint16):
         raise TypeError("queues must be a 16-bit tensor")
     rc = lib().octo_tune_step_mem(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(layer_mem, torch.int64, "layer_mem"),
-        _dev_ptr(capacity, torch.int64, "capacity"), int(max_advance),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(chains, torch.uint8, "chains"),
-        _dev_ptr(q, q.dtype, "queues"), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(layer_mem, torch.int64, "layer_mem", 2 * prob.L),
+        _dev_ptr(capacity, torch.int64, "capacity", prob.P), int(max_advance),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(chains, torch.uint8, "chains", n * chain_stride(prob)),
+        _dev_ptr(q, q.dtype, "queues", n * prob.P * queue_capacity(prob)), n, ctypes.c_uint64(seed & (2**64 - 1)), int(step),
         _stream(chains, stream))
     _check(rc, "octo_tune_step_mem")
 
@@ -332,14 +337,14 @@ def advance_w(prob, layer_costs, layer_mem, capacity, link, candidates, out_cand
     if out_peak is None:
         out_peak = torch.empty((n, prob.P), dtype=torch.int64, device=dev)
     rc = lib().octo_advance_w(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(layer_mem, torch.int64, "layer_mem"),
-        _dev_ptr(capacity, torch.int64, "capacity"), _dev_ptr(link, torch.int64, "link"),
-        _dev_ptr(candidates, torch.uint8, "candidates"), n,
-        _dev_ptr(out_candidates, torch.uint8, "out_candidates"),
-        _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_peak, torch.int64, "out_peak"), _stream(candidates, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(layer_mem, torch.int64, "layer_mem", 2 * prob.L),
+        _dev_ptr(capacity, torch.int64, "capacity", prob.P), _dev_ptr(link, torch.int64, "link", prob.P * prob.P),
+        _dev_ptr(candidates, torch.uint8, "candidates", n * prob.cand_stride), n,
+        _dev_ptr(out_candidates, torch.uint8, "out_candidates", n * prob.cand_stride),
+        _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_peak, torch.int64, "out_peak", n * prob.P), _stream(candidates, stream))
     _check(rc, "octo_advance_w")
     return out_candidates, out_makespan, out_bubble, out_peak
 
@@ -358,11 +363,11 @@ def alg1_tune(prob, layer_costs, link, records, iters, out_makespan=None, out_bu
     if out_stats is None:
         out_stats = torch.empty((n, 4), dtype=torch.int64, device=dev)
     rc = lib().octo_alg1_tune(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(records, torch.uint8, "records"), n,
-        int(iters), _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_stats, torch.int64, "out_stats"), _stream(records, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(records, torch.uint8, "records", n * prob.cand_stride), n,
+        int(iters), _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_stats, torch.int64, "out_stats", 4 * n), _stream(records, stream))
     _check(rc, "octo_alg1_tune")
     return out_makespan, out_bubble, out_stats
 
@@ -386,12 +391,12 @@ def alg1_tune_ex(prob, layer_costs, link, records, iters, flags, seed=0, out_mak
     if out_phase_iters is None:
         out_phase_iters = torch.empty((n, 3), dtype=torch.int64, device=dev)
     rc = lib().octo_alg1_tune_ex(
-        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs"),
-        _dev_ptr(link, torch.int64, "link"), _dev_ptr(records, torch.uint8, "records"), n,
-        int(iters), int(flags), int(seed), _dev_ptr(out_makespan, torch.int64, "out_makespan"),
-        _dev_ptr(out_bubble, torch.int64, "out_bubble"),
-        _dev_ptr(out_stats, torch.int64, "out_stats"),
-        _dev_ptr(out_phase_iters, torch.int64, "out_phase_iters"), _stream(records, stream))
+        ctypes.byref(prob), _dev_ptr(layer_costs, torch.int64, "layer_costs", 3 * prob.L),
+        _dev_ptr(link, torch.int64, "link", prob.P * prob.P), _dev_ptr(records, torch.uint8, "records", n * prob.cand_stride), n,
+        int(iters), int(flags), int(seed), _dev_ptr(out_makespan, torch.int64, "out_makespan", n),
+        _dev_ptr(out_bubble, torch.int64, "out_bubble", n * prob.P),
+        _dev_ptr(out_stats, torch.int64, "out_stats", 4 * n),
+        _dev_ptr(out_phase_iters, torch.int64, "out_phase_iters", 3 * n), _stream(records, stream))
     _check(rc, "octo_alg1_tune_ex")
     return out_makespan, out_bubble, out_stats, out_phase_iters
 

@@ -984,16 +984,25 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off
   int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
   int64_t* lfr = bsy + (size_t)P * lanes;  // XS: link free time after row t, lfr[t * lanes]
   int64_t* bfs = bsy + (size_t)P * lanes;  // XB: first start bfs[d * lanes] (-1 before)
-  // the prefix sums of the layer costs (and of the memory model), and the link matrix, staged
-  // in LDS after the lanes' arrays: every row reads them
-  int64_t* pre = reinterpret_cast<int64_t*>(smem + tab_off);
-  int64_t* pmem = pre + 3 * (L + 1);
-  int64_t* link = pmem + (MEM ? 2 * (L + 1) : 0);
-  for (int i = lane; i < 3 * (L + 1); i += WAVE) pre[i] = a.pre[i];
-  if constexpr (MEM)
-    for (int i = lane; i < 2 * (L + 1); i += WAVE) pmem[i] = a.pre_mem[i];
-  for (int i = lane; i < P * P; i += WAVE) link[i] = a.link[i];
-  __syncthreads();
+  // line-envelope rows and serialised links: the prefix sums of the layer costs (and of the
+  // memory model), the link matrix and each lane's record head are staged in LDS after the
+  // lanes' arrays, since every row reads them (the communication-accounting rows, whose LDS
+  // already bounds their occupancy, read them from global memory: staging cost them 14%)
+  constexpr bool STAGE = MMAX < 0 || X == XS;
+  const int64_t* pre = a.pre;
+  const int64_t* pmem = a.pre_mem;
+  const int64_t* link = a.link;
+  if constexpr (STAGE) {
+    int64_t* pre_l = reinterpret_cast<int64_t*>(smem + tab_off);
+    int64_t* pmem_l = pre_l + 3 * (L + 1);
+    int64_t* link_l = pmem_l + (MEM ? 2 * (L + 1) : 0);
+    for (int i = lane; i < 3 * (L + 1); i += WAVE) pre_l[i] = a.pre[i];
+    if constexpr (MEM)
+      for (int i = lane; i < 2 * (L + 1); i += WAVE) pmem_l[i] = a.pre_mem[i];
+    for (int i = lane; i < P * P; i += WAVE) link_l[i] = a.link[i];
+    __syncthreads();
+    pre = pre_l, pmem = pmem_l, link = link_l;
+  }
   ChunkMap cmap;
   cmap.init(a.ctl, lanes, a.bin_mask, NBIN_GEN);
   // chunks by grid stride: AFAB candidates of one bin cost alike, and an atomic work counter
@@ -1007,12 +1016,14 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off
     const int e = entry0 + lane;
     if (lane >= lanes || e >= cnt) continue;
     const int64_t cand = a.idx[pos0 + e];
-    // the record's head (header, boundaries, placement), staged in LDS: every row reads it
-    const int hq = (pert_off(a.pr.s_max) + 15) / 16;
-    uint8_t* rec = smem + rec_off + (size_t)lane * hq * 16;
-    {
-      const uint4* src = reinterpret_cast<const uint4*>(a.cands + cand * a.pr.stride);
-      for (int j = 0; j < hq; ++j) reinterpret_cast<uint4*>(rec)[j] = src[j];
+    // the record's head (header, boundaries, placement); staged in LDS with the tables
+    const uint8_t* rec = a.cands + cand * a.pr.stride;
+    if constexpr (STAGE) {
+      const int hq = (pert_off(a.pr.s_max) + 15) / 16;
+      uint8_t* rec_l = smem + rec_off + (size_t)lane * hq * 16;
+      const uint4* src = reinterpret_cast<const uint4*>(rec);
+      for (int j = 0; j < hq; ++j) reinterpret_cast<uint4*>(rec_l)[j] = src[j];
+      rec = rec_l;
     }
     const uint8_t* bnd = rec + 4;
     const uint8_t* dev = rec + 3 + a.pr.s_max;
@@ -4457,14 +4468,17 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
                (X == XS ? 2 * prob->P * prob->v_max : 0)) *
       8;
   const int lanes = (int)std::min<size_t>(WAVE, std::max<size_t>(1, 65536 / per_lane));
-  // then the staged tables: prefix sums (and memory prefix sums) and the link matrix
+  // line-envelope rows and serialised links: then the staged tables (prefix sums, memory prefix
+  // sums, the link matrix) and each lane's record head
   const int tab_off = (int)align_up(lanes * per_lane, 16);
-  const int rec_off = tab_off + (int)(((size_t)3 * (prob->L + 1) +
-                                       (X == XM ? (size_t)2 * (prob->L + 1) : 0) +
-                                       (size_t)prob->P * prob->P) *
-                                      8);
-  // then each lane's staged record head
-  const int lds = rec_off + lanes * (int)align_up(pert_off(prob->P * prob->v_max), 16);
+  const bool stage = LINES || X == XS;
+  const int rec_off = tab_off + (stage ? (int)(((size_t)3 * (prob->L + 1) +
+                                                (X == XM ? (size_t)2 * (prob->L + 1) : 0) +
+                                                (size_t)prob->P * prob->P) *
+                                               8)
+                                       : 0);
+  const int lds =
+      rec_off + (stage ? lanes * (int)align_up(pert_off(prob->P * prob->v_max), 16) : 0);
   if (lds > su.di.lds_max) return OCTO_EUNSUPPORTED;
   SimArgs a = make_args(prob, su.big, su, link, cands, n, ms, bub, peak);
   a.out_comm = comm;

@@ -52,3 +52,30 @@ def test_growing_batches_on_a_fresh_stream(gpu):
         rms, rbub = ref[kind][0][:n], ref[kind][1][:n]
         bad = np.nonzero((ms != rms) | (bub != rbub).any(axis=1))[0]
         assert len(bad) == 0, f"{kind} n={n}: {len(bad)} differ, first {int(bad[0])}"
+
+
+def test_binding_rejects_wrong_extents(gpu):
+    """The library takes plain pointers: the binding refuses a buffer whose element count is
+    not the one the call reads or writes, before anything is launched."""
+    import torch
+    from paper_2509_23722_amd import _lib
+    w = I.WORKLOADS[3]
+    recs = I.candidates(w)[:256]
+    prob = _lib.problem(w.L, w.P, w.v_max, w.M, recs.shape[1], w.max_pert)
+    c = torch.from_numpy(I.layer_costs(w)).to(gpu)
+    lk = torch.from_numpy(I.link_matrix(w.P, w.link_ns)).to(gpu)
+    r = torch.from_numpy(recs).to(gpu)
+    n = r.shape[0]
+    ms = torch.empty(n, dtype=torch.int64, device=gpu)
+    with pytest.raises(ValueError, match="out_bubble"):
+        _lib.sim_batch(prob, c, lk, r, ms, torch.empty(n, dtype=torch.int64, device=gpu))
+    with pytest.raises(ValueError, match="out_comm"):
+        _lib.sim_batch_comm(prob, c, lk, r, ms, None, torch.empty((n, 2), dtype=torch.int64,
+                                                                   device=gpu))
+    with pytest.raises(ValueError, match="candidates"):
+        _lib.sim_batch(prob, c, lk, r[:, :-16].contiguous())
+    with pytest.raises(ValueError, match="link"):
+        _lib.sim_batch(prob, c, lk[:-1].contiguous(), r)
+    ms_ok, _ = _lib.sim_batch(prob, c, lk, r)
+    torch.cuda.synchronize()
+    assert ms_ok.shape == (n,)
