@@ -1416,12 +1416,24 @@ __global__ void __launch_bounds__(WAVE) k_static(SimArgs a, int sbase, int rbase
   }
 }
 
-// Generate one device queue into a global row (entry = kind << 14 | chunk << 11 | m).
+// Generate one device queue into a global row (entry = kind << 14 | chunk << 11 | m), eight
+// entries per 16-byte store. The row starts 16-byte aligned and holds n rounded up to a
+// multiple of eight entries; the entries past n in the last span are written as 0.
 template <class Gen>
 __device__ __forceinline__ void emit_queue(Gen& g, uint16_t* row, int n) {
-  for (int i = 0; i < n; ++i) {
-    row[i] = qpack(g.kind, g.k, g.m);
-    g.advance(true);
+  uint4* r4 = reinterpret_cast<uint4*>(row);
+  for (int i0 = 0; i0 < n; i0 += 8) {
+    uint32_t w[4];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      uint32_t e = 0;
+      if (i0 + u < n) {
+        e = qpack(g.kind, g.k, g.m);
+        g.advance(true);
+      }
+      w[u >> 1] = (u & 1) ? (w[u >> 1] | e << 16) : e;
+    }
+    r4[i0 >> 3] = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 
