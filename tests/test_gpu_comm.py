@@ -65,6 +65,7 @@ def test_workload1_all_candidates(gpu):
     (1, 1, 1, 1, 0), (2, 2, 2, 5, 2), (4, 2, 8, 12, 3), (4, 3, 4, 14, 2), (5, 1, 7, 9, 2),
     (8, 2, 16, 20, 2), (8, 4, 8, 40, 2), (16, 2, 16, 40, 2), (12, 1, 24, 20, 2),
     (4, 1, 5, 8, 1), (2, 2, 33, 8, 1), (8, 2, 17, 20, 1), (8, 1, 32, 20, 1), (4, 2, 64, 16, 1),
+    (64, 1, 64, 255, 1), (64, 1, 45, 255, 1), (32, 2, 37, 255, 1),
 ])
 def test_random_structures(gpu, P, v_max, M, L, pert):
     """Every policy, placement kind and v (table-driven, generated, GPipe and materialised

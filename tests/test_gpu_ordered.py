@@ -68,6 +68,7 @@ def test_workload1_all_candidates(gpu):
     (8, 2, 16, 20, 2), (8, 4, 8, 40, 2), (16, 2, 16, 40, 2), (12, 1, 24, 20, 2),
     (4, 1, 5, 8, 1), (2, 2, 33, 8, 1), (8, 2, 17, 20, 1), (8, 1, 32, 20, 1), (4, 2, 64, 16, 1),
     (3, 8, 4, 30, 1), (2, 1, 1, 4, 2), (3, 2, 1, 9, 2),
+    (64, 1, 64, 255, 1), (32, 2, 37, 255, 1),
 ])
 def test_random_structures(gpu, P, v_max, M, L, pert):
     """Every policy, placement kind and v, moves (some cyclic), invalid records, zero-cost
