@@ -75,6 +75,7 @@ def check(dev, L, P, v_max, M, max_pert, costs, link, recs, iters, label):
 @pytest.mark.parametrize("P,v_max,M,L,max_pert,iters", [
     (4, 2, 8, 24, 6, 40), (2, 2, 4, 9, 3, 30), (4, 1, 6, 11, 2, 25), (3, 2, 5, 13, 4, 30),
     (8, 2, 16, 40, 2, 12), (1, 2, 4, 6, 2, 10), (4, 4, 8, 40, 2, 15), (5, 1, 7, 9, 0, 20),
+    (16, 2, 16, 60, 2, 10), (32, 2, 8, 255, 2, 6), (64, 1, 8, 255, 2, 4),
 ])
 def test_random_searches(gpu, P, v_max, M, L, max_pert, iters):
     """Random candidates of every policy, placement kind and v, some with moves or invalid, on
