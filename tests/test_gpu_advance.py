@@ -84,7 +84,8 @@ def test_capacity_of_1f1b(gpu, P, M):
     (1, 1, 4, 3, 8, 30), (2, 2, 4, 6, 16, 30), (3, 2, 6, 14, 24, 30), (4, 2, 8, 16, 40, 20),
     (4, 3, 4, 14, 24, 30), (5, 1, 7, 9, 20, 40), (8, 2, 16, 24, 60, 30), (16, 1, 8, 20, 40, 30),
     (8, 1, 32, 20, 80, 10), (4, 2, 64, 16, 120, 20), (4, 2, 32, 16, 80, 20),
-    (3, 1, 16, 10, 40, 30), (6, 2, 24, 20, 60, 25),
+    (3, 1, 16, 10, 40, 30), (6, 2, 24, 20, 60, 25), (32, 2, 8, 255, 60, 30),
+    (64, 1, 24, 255, 80, 10),
 ])
 def test_random_structures(gpu, P, v_max, M, L, mp, pct):
     """Every policy and placement kind, records with moves already (some deadlocked), invalid
