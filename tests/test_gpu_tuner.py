@@ -77,7 +77,8 @@ def compare(g, r, prob, label, rec_bytes):
 
 
 @pytest.mark.parametrize("P,v,M,L", [(4, 2, 8, 16), (3, 2, 6, 12), (8, 1, 8, 20), (4, 1, 5, 9),
-                                     (2, 3, 4, 10)])
+                                     (2, 3, 4, 10), (16, 2, 16, 60), (32, 2, 8, 255),
+                                     (64, 1, 8, 255)])
 def test_tuner_small_all_chains(gpu, P, v, M, L):
     from paper_2509_23722_amd import _lib
     rng = np.random.default_rng(P * 100 + v * 10 + M)
