@@ -979,6 +979,10 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off
   row.init(smem, li, lanes);
   int64_t* clk = reinterpret_cast<int64_t*>(smem) + (MMAX == 0 ? (size_t)M * lanes : 0) + li;
   int64_t* bsy = clk + (size_t)P * lanes;  // clk[d * lanes], bsy[d * lanes]
+  // plain variant with up to eight devices: busy times in registers, not in LDS, so that more
+  // waves fit a CU
+  const bool breg = X == XP && P <= 8;
+  int64_t bus[8];
   int64_t* pk = bsy + (size_t)P * lanes;   // MEM: peak bytes pk[d * lanes]
   int64_t* cps = bsy + (size_t)P * lanes;  // XC: last op start cps[d * lanes], then
   int64_t* cpe = cps + (size_t)P * lanes;  //     pending transfer end cpe[d * lanes]
@@ -1028,8 +1032,11 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off
     const uint8_t* bnd = rec + 4;
     const uint8_t* dev = rec + 3 + a.pr.s_max;
     const int S = P * v;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) bus[k] = 0;
     for (int d = 0; d < P; ++d) {
-      clk[d * lanes] = 0, bsy[d * lanes] = 0;
+      clk[d * lanes] = 0;
+      if (!breg) bsy[d * lanes] = 0;
       if constexpr (MEM) pk[d * lanes] = 0;
       if constexpr (X == XC) cps[d * lanes] = 0, cpe[d * lanes] = -1;
       if constexpr (X == XB) bfs[d * lanes] = -1;
@@ -1046,7 +1053,15 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off
       const int64_t df = pre[3 * b1] - pre[3 * b0];
       const int64_t db = pre[3 * b1 + 1] - pre[3 * b0 + 1] + pre[3 * b1 + 2] -
                          pre[3 * b0 + 2];
-      if (fwd) bsy[d * lanes] += (df + db) * M;
+      if (fwd) {
+        const int64_t cst = (df + db) * M;
+        if (breg) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) bus[k] += d == k ? cst : 0;
+        } else {
+          bsy[d * lanes] += cst;
+        }
+      }
       if constexpr (MEM) {
         if (fwd)
           pk[d * lanes] += (pmem[2 * b1] - pmem[2 * b0]) * M +
@@ -1102,7 +1117,13 @@ __global__ void __launch_bounds__(WAVE) k_afab(SimArgs a, int lanes, int tab_off
     int64_t ms = 0;
     for (int d = 0; d < P; ++d) ms = clk[d * lanes] > ms ? clk[d * lanes] : ms;
     a.out_ms[cand] = ms;
-    for (int d = 0; d < P; ++d) a.out_bub[cand * P + d] = ms - bsy[d * lanes];
+    if (breg) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (k < P) a.out_bub[cand * P + k] = ms - bus[k];
+    } else {
+      for (int d = 0; d < P; ++d) a.out_bub[cand * P + d] = ms - bsy[d * lanes];
+    }
     if constexpr (MEM)
       for (int d = 0; d < P; ++d) a.out_peak[cand * P + d] = pk[d * lanes];
     if constexpr (X == XC) {
@@ -4474,7 +4495,9 @@ int launch_afab(const octo_problem* prob, const Setup& su, const int64_t* link, 
   // not fit the register file) in LDS
   constexpr bool LINES = X == XP || X == XM || X == XB;
   const int mmax = LINES ? -1 : X == XC ? 0 : prob->M == 32 ? 32 : prob->M == 64 ? 64 : 0;
-  const int words = (X == XM || X == XB) ? 3 : X == XC ? 4 : 2;  // per device
+  // per device: the clock, the busy time (in registers for the plain variant at P <= 8), then
+  // the variant's own words
+  const int words = (X == XM || X == XB) ? 3 : X == XC ? 4 : (X == XP && prob->P <= 8) ? 1 : 2;
   const size_t per_lane =
       (size_t)((mmax == 0 ? prob->M : 0) + words * prob->P +
                (X == XS ? 2 * prob->P * prob->v_max : 0)) *
